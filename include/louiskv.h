@@ -1,0 +1,309 @@
+/*
+ * libLouisKV: KV clustering and retrieval for long input/output decoding on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The calls follow the method of "LouisKV: Efficient KV Cache Retrieval for
+ * Long Input-Output Sequences" (arXiv 2510.11292):
+ *   louiskv_cluster_prefill     k-means of prompt keys per (layer, KV head),
+ *                               centroids as index vectors, cluster-packed
+ *                               KV pool             (Section 4.2 prefill stage;
+ *                                                    Algorithm 1 store_cache)
+ *   louiskv_segment_output      decode-stage store_cache: local window append,
+ *                               oldest-segment mean and offload
+ *                                                   (Section 4.2 decode stage;
+ *                                                    Algorithm 1 store_cache)
+ *   louiskv_boundary_check      head-averaged query cosine vs threshold
+ *                                                   (Section 4.1 equation for r_t;
+ *                                                    Algorithm 1 decode loop)
+ *   louiskv_retrieve            group-consistent unit scores, budgeted top
+ *                               units, gather of their KV rows
+ *                                                   (Appendix B equation for A_t;
+ *                                                    Section 3.1 budget;
+ *                                                    Algorithm 1 Retrieve)
+ *   louiskv_sparse_decode_attn  attention over [KV_critical : KV_local]
+ *                                                   (Section 3.1 attention;
+ *                                                    Algorithm 1 decode loop)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Ownership   The caller owns every buffer, including workspaces; the library
+ *             never allocates or frees memory and keeps no state except a
+ *             thread-local last-error string.
+ * Pointers    Device pointers, except KV pools that the caller declares host
+ *             resident (pool_on_host = 1): those must be pinned, device-mapped
+ *             host memory (hipHostMalloc), which kernels read and write
+ *             directly over the host link.
+ * Streams     `stream` is a hipStream_t (NULL = the legacy default stream).
+ *             Arguments are validated on the host; the work is then enqueued
+ *             and the call returns without synchronising.
+ * Errors      Every call returns a louiskv_status.  On a validation error
+ *             nothing is launched and no output is touched.  LOUISKV_ERR_HIP
+ *             reports a failed HIP runtime call or launch; the text is in
+ *             louiskv_last_error().  No C++ exception crosses the ABI.
+ * Types       dtype LOUISKV_F32 (float32) or LOUISKV_BF16 (bfloat16 stored as
+ *             uint16).  Centroids and segment means are always float32,
+ *             indices always int32.  Only head dimension d = 128 is supported
+ *             (LOUISKV_ERR_UNSUPPORTED otherwise).
+ * Indexing    A slice is one (sequence, layer, KV head): s = (seq*L + layer)*Hkv
+ *             + kv_head.  A group is one (sequence, layer): G = s / Hkv.  Query
+ *             heads of group G are [Hkv*g]; heads h*g .. h*g+g-1 share KV head h
+ *             (grouped-query attention, Appendix B).
+ * Units       Retrieval units of a slice are its C clusters (unit 0..C-1, in
+ *             cluster order) followed by its evicted output segments (unit C+e
+ *             for the e-th eviction).  unit_start/unit_size give each unit's
+ *             run of rows in the slice's pool; reps holds its index vector.
+ */
+#ifndef LOUISKV_H
+#define LOUISKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LOUISKV_ABI_VERSION 1
+
+typedef enum louiskv_status {
+  LOUISKV_OK = 0,
+  LOUISKV_ERR_NULL = 1,           /* a required pointer is NULL */
+  LOUISKV_ERR_SHAPE = 2,          /* sizes are inconsistent or out of range */
+  LOUISKV_ERR_DTYPE = 3,          /* unknown dtype code */
+  LOUISKV_ERR_UNSUPPORTED = 4,    /* valid request this build does not serve (d != 128 ...) */
+  LOUISKV_ERR_WORKSPACE = 5,      /* workspace NULL or smaller than *_workspace_size() */
+  LOUISKV_ERR_HIP = 6             /* HIP runtime or launch failure */
+} louiskv_status;
+
+typedef enum louiskv_dtype { LOUISKV_F32 = 0, LOUISKV_BF16 = 1 } louiskv_dtype;
+
+typedef enum louiskv_ref_mode {
+  LOUISKV_REF_PREV = 0,    /* reference = previous step's query (Section 4.1 equation) */
+  LOUISKV_REF_ANCHOR = 1   /* reference = query of the last boundary */
+} louiskv_ref_mode;
+
+/* Library ABI version (LOUISKV_ABI_VERSION of the build). */
+int louiskv_abi_version(void);
+/* Static text for a status code. */
+const char* louiskv_status_str(int status);
+/* Text of the last error recorded on the calling thread ("" if none). */
+const char* louiskv_last_error(void);
+
+/*
+ * Local-window bookkeeping of the decode stage (Section 4.2 decode stage;
+ * Algorithm 1 store_cache), a pure host function shared by callers and
+ * louiskv_segment_output so both apply the same rule.
+ *
+ * The window keeps the most recent generated tokens in a ring of `window`
+ * slots; generated token j lives in slot j % window.  When token `step`
+ * (0-based) is stored while the window already holds `window` tokens, the
+ * oldest `seg_len` tokens leave first and become one segment unit.
+ * Outputs (any may be NULL): *evicted_segment = index e of the segment that
+ * leaves while storing token `step` (its tokens are e*seg_len .. +seg_len-1),
+ * or -1; *n_evicted = segments evicted after storing it; *n_local and
+ * *local_start = live tokens in the window after storing it and the ring slot
+ * of the oldest one.  Requires window % seg_len == 0, seg_len >= 1, step >= 0.
+ */
+int louiskv_window_info(int32_t step, int32_t window, int32_t seg_len,
+                        int32_t* evicted_segment, int32_t* n_evicted,
+                        int32_t* n_local, int32_t* local_start);
+
+/* ------------------------------------------------------------------------ */
+/* Prefill: k-means of the prompt keys of every slice.                       */
+/* ------------------------------------------------------------------------ */
+
+size_t louiskv_cluster_prefill_workspace_size(int64_t n_slices, int32_t n_tokens,
+                                              int32_t d, int32_t n_clusters,
+                                              int32_t dtype);
+
+/*
+ * Section 4.2 prefill stage and Algorithm 1 store_cache(prefill): group the
+ * prompt keys of each slice with k-means, keep each cluster's centroid (the
+ * mean of its keys) as its index vector, and store the prompt K/V rows in a
+ * unified pool with each cluster as one contiguous run of rows.
+ *
+ * Lloyd iterations, `n_iters` times: assign every key to the nearest centroid
+ * operand in squared Euclidean distance (ties to the lower index), then replace
+ * every non-empty centroid by the mean of its keys (float64 sum, one rounding
+ * to float32); an empty cluster keeps its centroid.  For LOUISKV_BF16 keys the
+ * distance is taken to the bfloat16 rounding of each float32 centroid (the
+ * matrix-core operand); for LOUISKV_F32 keys to the float32 centroid.
+ *
+ * keys        [n_slices][n_tokens][d] dtype, prompt keys.
+ * init_idx    [n_slices][n_clusters] int32, token index of each initial centroid
+ *             (values in [0, n_tokens); out-of-range values are clamped).
+ * reps        out [n_slices][units_cap][d] float32: rows 0..C-1 = final centroids.
+ * unit_start, unit_size
+ *             out [n_slices][units_cap] int32: entries 0..C-1 = first pool row
+ *             and member count of each cluster (unit_start is the CSR offset).
+ * assign      out [n_slices][n_tokens] int32: cluster of each key after the
+ *             last assignment (the centroids above are the means of these).
+ * perm        out [n_slices][n_tokens] int32: token ids grouped by cluster,
+ *             ascending inside a cluster; pool row r holds token perm[r].
+ * values      [n_slices][n_tokens][d] dtype or NULL.
+ * k_pool, v_pool
+ *             out [n_slices][pool_rows][d] dtype or NULL: rows 0..n_tokens-1
+ *             are written in perm order (keys from `keys`, values from
+ *             `values`; v_pool requires values).  pool_on_host: see Pointers.
+ * iter_events NULL or an array of 2*n_iters hipEvent_t recorded on `stream`
+ *             just before and after each iteration's assignment kernel, for
+ *             callers that time it.
+ * Requires 1 <= n_clusters <= n_tokens, n_clusters <= units_cap, n_iters >= 1,
+ * pool_rows >= n_tokens when a pool is given.
+ */
+int louiskv_cluster_prefill(const void* keys, int32_t dtype, int64_t n_slices,
+                            int32_t n_tokens, int32_t d, int32_t n_clusters,
+                            int32_t n_iters, const int32_t* init_idx,
+                            float* reps, int32_t units_cap,
+                            int32_t* unit_start, int32_t* unit_size,
+                            int32_t* assign, int32_t* perm,
+                            const void* values, void* k_pool, void* v_pool,
+                            int64_t pool_rows, int32_t pool_on_host,
+                            void* const* iter_events,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * One assignment step alone (the first half of a Lloyd iteration above), for
+ * step-by-step checking: assign[s][i] = argmin_c ||keys[s][i] - op(c)||^2 over
+ * the n_clusters float32 centroids at centroids[s][0..C-1] (slice stride
+ * `centroid_stride` rows), op = bfloat16 rounding for LOUISKV_BF16 keys,
+ * identity for LOUISKV_F32.  Ties go to the lower index.  Same workspace as
+ * louiskv_cluster_prefill.
+ */
+int louiskv_kmeans_assign(const void* keys, int32_t dtype, int64_t n_slices,
+                          int32_t n_tokens, int32_t d, int32_t n_clusters,
+                          const float* centroids, int32_t centroid_stride,
+                          int32_t* assign, void* workspace, size_t workspace_bytes,
+                          void* stream);
+
+/*
+ * One update step alone (the second half of a Lloyd iteration): centroids_out
+ * [s][c] = float32(mean of keys with assign == c), float64 sum; clusters with
+ * no key copy centroids_in.  counts (out, nullable) [n_slices][n_clusters].
+ * centroids_in and centroids_out may alias.  Same workspace as
+ * louiskv_cluster_prefill.
+ */
+int louiskv_kmeans_update(const void* keys, int32_t dtype, int64_t n_slices,
+                          int32_t n_tokens, int32_t d, int32_t n_clusters,
+                          const int32_t* assign, const float* centroids_in,
+                          float* centroids_out, int32_t centroid_stride,
+                          int32_t* counts, void* workspace, size_t workspace_bytes,
+                          void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Decode stage                                                              */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Algorithm 1 store_cache(decode) and Section 4.2 decode stage: store this
+ * step's key and value of every slice in its local window.  If the window
+ * already holds `window` tokens (louiskv_window_info), its oldest `seg_len`
+ * tokens leave first: their mean key (float64 sum, one rounding to float32)
+ * becomes the index vector of unit n_clusters + e (reps, unit_start =
+ * prompt_len + e*seg_len, unit_size = seg_len) and their K/V rows are copied
+ * to pool rows prompt_len + e*seg_len .. +seg_len-1.
+ *
+ * k_new, v_new   [n_slices][d] dtype, this step's key and value.
+ * k_local, v_local  in/out [n_slices][window][d] dtype ring buffers.
+ * step           number of generated tokens stored before this one (0-based).
+ * reps, unit_start, unit_size  in/out unit tables (see louiskv_cluster_prefill),
+ *                capacity units_cap >= n_clusters + segments evicted.
+ * k_pool, v_pool [n_slices][pool_rows][d] dtype; pool_rows >= prompt_len +
+ *                step + 1 when a segment is evicted.
+ */
+int louiskv_segment_output(const void* k_new, const void* v_new, int32_t dtype,
+                           int64_t n_slices, int32_t d,
+                           void* k_local, void* v_local, int32_t window,
+                           int32_t step, int32_t seg_len,
+                           float* reps, int32_t* unit_start, int32_t* unit_size,
+                           int32_t units_cap, int32_t n_clusters,
+                           void* k_pool, void* v_pool, int64_t pool_rows,
+                           int32_t prompt_len, int32_t pool_on_host, void* stream);
+
+/*
+ * Section 4.1 and Algorithm 1 decode loop: per group, r = (1/H) sum_h
+ * cos(q_ref^h, q^h) over its H = n_q_heads query heads (float64, the cosine's
+ * denominator clamped at 1e-30); fire = first_step || r < tau.  The reference
+ * becomes q for every group in LOUISKV_REF_PREV mode, and for the groups that
+ * fire in LOUISKV_REF_ANCHOR mode.
+ *
+ * q        [n_groups][n_q_heads][d] dtype, this step's queries.
+ * q_ref    in/out [n_groups][n_q_heads][d] dtype (not read when first_step).
+ * r_out    out [n_groups] float64 or NULL (NaN when first_step).
+ * fire_out out [n_groups] uint8 (1 = boundary: retrieval runs this step).
+ */
+int louiskv_boundary_check(const void* q, void* q_ref, int32_t dtype,
+                           int64_t n_groups, int32_t n_q_heads, int32_t d,
+                           double tau, int32_t mode, int32_t first_step,
+                           double* r_out, uint8_t* fire_out, void* stream);
+
+size_t louiskv_retrieve_workspace_size(int64_t n_slices, int32_t units_cap,
+                                       int32_t budget);
+
+/*
+ * Algorithm 1 Retrieve with the group-consistent score of Appendix B, for the
+ * slices whose group fired (all slices when fire is NULL):
+ *   A_u = (1/g) sum_j softmax_u(q_j . reps_u * scale) over units 0..n_units-1
+ *   (float64), units ranked by A descending, equal scores by lower unit id;
+ *   the longest prefix of the ranking whose total unit_size is <= budget is
+ *   selected (Section 3.1 constraint |I_t| <= B); the rows of the selected
+ *   units, in rank order and ascending inside a unit, are copied from the
+ *   pools into the dense KV_critical buffers.
+ * Slices of groups that did not fire are left untouched (KV_critical is reused
+ * until the next boundary).
+ *
+ * q            [n_groups][n_kv_heads*group_size][d] dtype.
+ * scale        softmax temperature, normally 1/sqrt(d).
+ * reps         [n_slices][units_cap][d] float32; unit_start, unit_size
+ *              [n_slices][units_cap] int32; n_units <= units_cap.
+ * k_pool, v_pool  [n_slices][pool_rows][d] dtype (pool_on_host: see Pointers).
+ * fire         [n_groups] uint8 or NULL.
+ * sel_units    out [n_slices][units_cap] int32, selected unit ids in rank order.
+ * n_sel_units  out [n_slices] int32.
+ * n_sel        out [n_slices] int32, selected tokens (<= budget).
+ * k_buf, v_buf out [n_slices][budget][d] dtype, rows 0..n_sel-1 written.
+ * scores_out   out [n_slices][units_cap] float64 or NULL.
+ * Requires 1 <= n_units <= 16384, budget >= 0.
+ */
+int louiskv_retrieve(const void* q, int32_t dtype, int64_t n_slices,
+                     int32_t n_kv_heads, int32_t group_size, int32_t d, double scale,
+                     const float* reps, const int32_t* unit_start,
+                     const int32_t* unit_size, int32_t units_cap, int32_t n_units,
+                     const void* k_pool, const void* v_pool, int64_t pool_rows,
+                     int32_t pool_on_host, int32_t budget, const uint8_t* fire,
+                     int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel,
+                     void* k_buf, void* v_buf, double* scores_out,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+size_t louiskv_sparse_decode_attn_workspace_size(int64_t n_slices, int32_t group_size,
+                                                 int32_t d, int32_t buf_rows,
+                                                 int32_t window);
+
+/*
+ * Section 3.1 attention over Algorithm 1's KV_attn = [KV_critical : KV_local]:
+ * for each query head j of KV head h, o_j = softmax(q_j K^T * scale) V with K,V
+ * the rows 0..n_sel[s]-1 of k_buf/v_buf followed by the n_local live rows of
+ * the local ring (slots (local_start + i) % window).  float32 arithmetic.
+ *
+ * q          [n_groups][n_kv_heads*group_size][d] dtype.
+ * k_buf, v_buf [n_slices][buf_rows][d] dtype; n_sel [n_slices] int32 (<= buf_rows).
+ * k_local, v_local [n_slices][window][d] dtype; 0 <= n_local <= window.
+ * out        out [n_groups][n_kv_heads*group_size][d] in out_dtype.
+ * lse_out    out [n_groups][n_kv_heads*group_size] float32 or NULL: natural log of
+ *            each head's softmax denominator (max included); -inf and o = 0
+ *            when a slice has no row.
+ */
+int louiskv_sparse_decode_attn(const void* q, int32_t dtype, int64_t n_slices,
+                               int32_t n_kv_heads, int32_t group_size, int32_t d,
+                               float scale, const void* k_buf, const void* v_buf,
+                               const int32_t* n_sel, int32_t buf_rows,
+                               const void* k_local, const void* v_local,
+                               int32_t window, int32_t local_start, int32_t n_local,
+                               void* out, int32_t out_dtype, float* lse_out,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LOUISKV_H */

@@ -1,0 +1,59 @@
+// Status strings, the thread-local last-error text, and the local-window rule.
+#include <stdarg.h>
+
+#include "common.h"
+
+namespace louiskv {
+namespace {
+thread_local char g_err[1024] = "";
+}
+const char* g_err_text() { return g_err; }
+
+void set_error(const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+}
+
+int fail(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+}  // namespace louiskv
+
+extern "C" int louiskv_abi_version(void) { return LOUISKV_ABI_VERSION; }
+
+extern "C" const char* louiskv_status_str(int status) {
+  switch (status) {
+    case LOUISKV_OK: return "ok";
+    case LOUISKV_ERR_NULL: return "required pointer is NULL";
+    case LOUISKV_ERR_SHAPE: return "inconsistent or out-of-range sizes";
+    case LOUISKV_ERR_DTYPE: return "unknown dtype";
+    case LOUISKV_ERR_UNSUPPORTED: return "unsupported configuration";
+    case LOUISKV_ERR_WORKSPACE: return "workspace missing or too small";
+    case LOUISKV_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+extern "C" const char* louiskv_last_error(void) { return louiskv::g_err_text(); }
+
+extern "C" int louiskv_window_info(int32_t step, int32_t window, int32_t seg_len, int32_t* evicted_segment,
+                                   int32_t* n_evicted, int32_t* n_local, int32_t* local_start) {
+  if (step < 0 || seg_len < 1 || window < seg_len || window % seg_len != 0)
+    return louiskv::fail(LOUISKV_ERR_SHAPE, "window=%d must be a positive multiple of seg_len=%d, step=%d >= 0",
+                         window, seg_len, step);
+  const int32_t ev = step >= window && (step - window) % seg_len == 0 ? (step - window) / seg_len : -1;
+  const int32_t nev = step >= window ? (step - window) / seg_len + 1 : 0;
+  const int64_t first_live = (int64_t)nev * seg_len;
+  if (evicted_segment) *evicted_segment = ev;
+  if (n_evicted) *n_evicted = nev;
+  if (n_local) *n_local = (int32_t)(step + 1 - first_live);
+  if (local_start) *local_start = (int32_t)(first_live % window);
+  return LOUISKV_OK;
+}

@@ -1,0 +1,759 @@
+// Decode-stage kernels: boundary test (Section 4.1), decode store_cache with
+// segment eviction (Section 4.2 decode stage), group-consistent retrieval
+// (Appendix B; Algorithm 1 Retrieve) and sparse decode attention (Section 3.1).
+#include <algorithm>
+
+#include "common.h"
+
+namespace louiskv {
+namespace {
+
+constexpr int kMaxGroupSize = 8;
+constexpr int kMaxUnits = 8192;
+
+// ------------------------------------------------------------------ boundary
+
+// One block of 4 waves per group.  Each wave takes heads w, w+4, ...; a head's
+// 128 dims are 2 per lane.  Cosines in float64.
+template <class T>
+__global__ __launch_bounds__(256)
+void boundary_kernel(const T* __restrict__ q, T* __restrict__ q_ref, int n_heads, double tau, int mode,
+                     int first, double* __restrict__ r_out, uint8_t* __restrict__ fire_out) {
+  __shared__ double s_part[4];
+  __shared__ int s_fire;
+  const int g = blockIdx.x;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const size_t base = (size_t)g * n_heads * kHeadDim;
+  double acc = 0.0;
+  if (!first) {
+    for (int hh = w; hh < n_heads; hh += 4) {
+      const size_t o = base + (size_t)hh * kHeadDim + 2 * lane;
+      const double a0 = load_as_f32(q, o), a1 = load_as_f32(q, o + 1);
+      const double b0 = load_as_f32(q_ref, o), b1 = load_as_f32(q_ref, o + 1);
+      const double dot = wave_sum(a0 * b0 + a1 * b1);
+      const double na = wave_sum(a0 * a0 + a1 * a1);
+      const double nb = wave_sum(b0 * b0 + b1 * b1);
+      acc += dot / fmax(sqrt(na) * sqrt(nb), 1e-30);
+    }
+  }
+  if (lane == 0) s_part[w] = acc;
+  __syncthreads();
+  if (tid == 0) {
+    double r = __builtin_nan("");
+    int fire = 1;
+    if (!first) {
+      r = (s_part[0] + s_part[1] + s_part[2] + s_part[3]) / (double)n_heads;
+      fire = r < tau ? 1 : 0;
+    }
+    if (r_out) r_out[g] = r;
+    fire_out[g] = (uint8_t)fire;
+    s_fire = fire;
+  }
+  __syncthreads();
+  if (mode == LOUISKV_REF_PREV || s_fire) {
+    const int n = n_heads * kHeadDim;
+    for (int i = tid; i < n; i += 256) q_ref[base + i] = q[base + i];
+  }
+}
+
+// ------------------------------------------------------------------ decode store
+
+// One wave per slice: optional eviction of the oldest segment (mean key as a new
+// unit, rows copied to the pool), then the new token enters its ring slot.
+template <class T>
+__global__ __launch_bounds__(64)
+void store_decode_kernel(const T* __restrict__ k_new, const T* __restrict__ v_new, T* __restrict__ k_local,
+                         T* __restrict__ v_local, int window, int step, int seg_len, int evict_seg,
+                         float* __restrict__ reps, int32_t* __restrict__ unit_start, int32_t* __restrict__ unit_size,
+                         int units_cap, int n_clusters, T* __restrict__ k_pool, T* __restrict__ v_pool,
+                         int64_t pool_rows, int prompt_len) {
+  const int64_t s = blockIdx.x;
+  const int lane = threadIdx.x;
+  const size_t lbase = (size_t)s * window * kHeadDim;
+  if (evict_seg >= 0) {
+    const int slot0 = (int)(((int64_t)evict_seg * seg_len) % window);
+    const int unit = n_clusters + evict_seg;
+    const int64_t prow = (int64_t)prompt_len + (int64_t)evict_seg * seg_len;
+    double a0 = 0.0, a1 = 0.0;
+    for (int r = 0; r < seg_len; ++r) {
+      const size_t o = lbase + (size_t)(slot0 + r) * kHeadDim + 2 * lane;
+      const T k0 = k_local[o], k1 = k_local[o + 1];
+      a0 += (double)load_as_f32(&k0, 0);
+      a1 += (double)load_as_f32(&k1, 0);
+      if (k_pool) {
+        const size_t po = ((size_t)s * pool_rows + prow + r) * kHeadDim + 2 * lane;
+        k_pool[po] = k0;
+        k_pool[po + 1] = k1;
+        if (v_pool) {
+          v_pool[po] = v_local[o];
+          v_pool[po + 1] = v_local[o + 1];
+        }
+      }
+    }
+    float* rep = reps + ((size_t)s * units_cap + unit) * kHeadDim;
+    rep[2 * lane] = (float)(a0 / (double)seg_len);
+    rep[2 * lane + 1] = (float)(a1 / (double)seg_len);
+    if (lane == 0) {
+      unit_start[s * units_cap + unit] = (int32_t)prow;
+      unit_size[s * units_cap + unit] = seg_len;
+    }
+    __syncthreads();
+  }
+  const int slot = step % window;
+  const size_t o = lbase + (size_t)slot * kHeadDim + 2 * lane;
+  const size_t n = (size_t)s * kHeadDim + 2 * lane;
+  k_local[o] = k_new[n];
+  k_local[o + 1] = k_new[n + 1];
+  v_local[o] = v_new[n];
+  v_local[o + 1] = v_new[n + 1];
+}
+
+// ------------------------------------------------------------------ retrieve
+
+constexpr int kSelThreads = 512;
+
+__device__ __forceinline__ bool ranks_before(double sa, int ia, double sb, int ib) {
+  return sa > sb || (sa == sb && ia < ib);
+}
+
+// One block per fired slice: float64 group-consistent scores, LDS bitonic sort
+// by (score desc, id asc), prefix-stop under the budget, selected unit list and
+// the pool-row list that the gather kernel copies.
+template <class T>
+__global__ __launch_bounds__(kSelThreads)
+void score_select_kernel(const T* __restrict__ q, int n_kv_heads, int group_size, double scale,
+                         const float* __restrict__ reps, const int32_t* __restrict__ unit_start,
+                         const int32_t* __restrict__ unit_size, int units_cap, int n_units, int budget,
+                         const uint8_t* __restrict__ fire, int32_t* __restrict__ sel_units,
+                         int32_t* __restrict__ n_sel_units, int32_t* __restrict__ n_sel,
+                         double* __restrict__ scores_out, double* __restrict__ logit_ws,
+                         int32_t* __restrict__ row_ws, int n_pad) {
+  extern __shared__ __align__(16) char smem[];
+  double* s_sc = reinterpret_cast<double*>(smem);                // [n_pad]
+  int* s_id = reinterpret_cast<int*>(s_sc + n_pad);              // [n_pad]
+  __shared__ double s_q[kMaxGroupSize][kHeadDim];
+  __shared__ double s_red[kMaxGroupSize][kSelThreads / 64];
+  __shared__ double s_m[kMaxGroupSize], s_z[kMaxGroupSize];
+  __shared__ int s_ntake, s_nsel;
+  __shared__ int s_wsum[kSelThreads / 64];
+
+  const int64_t s = blockIdx.x;
+  const int64_t grp = s / n_kv_heads;
+  if (fire && !fire[grp]) return;
+  const int kvh = (int)(s - grp * n_kv_heads);
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int G = group_size;
+  const int n_q_heads = n_kv_heads * G;
+
+  for (int i = tid; i < G * kHeadDim; i += kSelThreads) {
+    const int j = i / kHeadDim, k = i % kHeadDim;
+    s_q[j][k] = load_as_f32(q, ((size_t)grp * n_q_heads + (size_t)kvh * G + j) * kHeadDim + k);
+  }
+  __syncthreads();
+
+  // pass 1: logits, 16 lanes per unit, each lane 8 dims
+  const int sub = lane & 15, quad = lane >> 4;
+  double mx[kMaxGroupSize];
+#pragma unroll
+  for (int j = 0; j < kMaxGroupSize; ++j) mx[j] = -__builtin_inf();
+  double* lg = logit_ws + (size_t)s * units_cap * G;
+  const float* rs = reps + (size_t)s * units_cap * kHeadDim;
+  for (int u0 = w * 4; u0 < n_units; u0 += (kSelThreads / 64) * 4) {
+    const int u = u0 + quad;
+    double part[kMaxGroupSize];
+#pragma unroll
+    for (int j = 0; j < kMaxGroupSize; ++j) part[j] = 0.0;
+    if (u < n_units) {
+      const float4* r4 = reinterpret_cast<const float4*>(rs + (size_t)u * kHeadDim + 8 * sub);
+      const float4 x0 = r4[0], x1 = r4[1];
+      const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+      for (int j = 0; j < kMaxGroupSize; ++j) {
+        if (j < G) {
+          double a = 0.0;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) a += s_q[j][8 * sub + e] * (double)x[e];
+          part[j] = a;
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kMaxGroupSize; ++j) {
+      if (j < G) {
+        double a = part[j];
+        a += __shfl_xor(a, 8, kWave);
+        a += __shfl_xor(a, 4, kWave);
+        a += __shfl_xor(a, 2, kWave);
+        a += __shfl_xor(a, 1, kWave);
+        a *= scale;
+        if (u < n_units) {
+          mx[j] = fmax(mx[j], a);
+          if (sub == j) lg[(size_t)u * G + j] = a;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kMaxGroupSize; ++j) {
+    if (j < G) {
+      const double m = wave_max(mx[j]);
+      if (lane == 0) s_red[j][w] = m;
+    }
+  }
+  __syncthreads();
+  if (tid < G) {
+    double m = s_red[tid][0];
+    for (int q2 = 1; q2 < kSelThreads / 64; ++q2) m = fmax(m, s_red[tid][q2]);
+    s_m[tid] = m;
+  }
+  __syncthreads();
+
+  // pass 2: exponentials and their sums per head
+  double zs[kMaxGroupSize];
+#pragma unroll
+  for (int j = 0; j < kMaxGroupSize; ++j) zs[j] = 0.0;
+  for (int u = tid; u < n_units; u += kSelThreads) {
+#pragma unroll
+    for (int j = 0; j < kMaxGroupSize; ++j) {
+      if (j < G) {
+        const double e = exp(lg[(size_t)u * G + j] - s_m[j]);
+        lg[(size_t)u * G + j] = e;
+        zs[j] += e;
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kMaxGroupSize; ++j) {
+    if (j < G) {
+      const double z = wave_sum(zs[j]);
+      if (lane == 0) s_red[j][w] = z;
+    }
+  }
+  __syncthreads();
+  if (tid < G) {
+    double z = 0.0;
+    for (int q2 = 0; q2 < kSelThreads / 64; ++q2) z += s_red[tid][q2];
+    s_z[tid] = z;
+  }
+  __syncthreads();
+
+  // pass 3: averaged probabilities as sort keys
+  for (int u = tid; u < n_pad; u += kSelThreads) {
+    if (u < n_units) {
+      double a = 0.0;
+      for (int j = 0; j < G; ++j) a += lg[(size_t)u * G + j] / s_z[j];
+      a /= (double)G;
+      s_sc[u] = a;
+      s_id[u] = u;
+      if (scores_out) scores_out[(size_t)s * units_cap + u] = a;
+    } else {
+      s_sc[u] = -1.0;
+      s_id[u] = 0x7fffffff;
+    }
+  }
+  __syncthreads();
+
+  // bitonic sort, first in rank order
+  for (int k = 2; k <= n_pad; k <<= 1) {
+    for (int jj = k >> 1; jj > 0; jj >>= 1) {
+      for (int i = tid; i < n_pad; i += kSelThreads) {
+        const int p = i ^ jj;
+        if (p > i) {
+          const bool up = (i & k) == 0;
+          const double si = s_sc[i], sp = s_sc[p];
+          const int ii = s_id[i], ip = s_id[p];
+          const bool swap = up ? ranks_before(sp, ip, si, ii) : ranks_before(si, ii, sp, ip);
+          if (swap) {
+            s_sc[i] = sp; s_sc[p] = si;
+            s_id[i] = ip; s_id[p] = ii;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+
+  // prefix stop: count ranks whose inclusive size sum stays within the budget
+  if (tid == 0) { s_ntake = 0; s_nsel = 0; }
+  __syncthreads();
+  const int32_t* us = unit_size + (size_t)s * units_cap;
+  int carry = 0;
+  double* incl_d = s_sc;   // reuse the score array as int storage for inclusive sums
+  int* incl = reinterpret_cast<int*>(incl_d);
+  for (int base = 0; base < n_units; base += kSelThreads) {
+    const int p = base + tid;
+    const int id = p < n_units ? s_id[p] : -1;
+    const int v = (id >= 0 && id < n_units) ? max(us[id], 0) : 0;
+    int x = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o, kWave);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) s_wsum[w] = x;
+    __syncthreads();
+    int wp = 0;
+    for (int q2 = 0; q2 < w; ++q2) wp += s_wsum[q2];
+    const long long inc = (long long)carry + wp + x;
+    if (p < n_units) {
+      incl[p] = inc > 0x3fffffff ? 0x3fffffff : (int)inc;
+      if (inc <= budget) atomicAdd(&s_ntake, 1);
+    }
+    int tot = 0;
+    for (int q2 = 0; q2 < kSelThreads / 64; ++q2) tot += s_wsum[q2];
+    carry = (int)std::min<long long>((long long)carry + tot, 0x3fffffff);
+    __syncthreads();
+  }
+  __syncthreads();
+  const int ntake = s_ntake;
+  const int nsel = ntake > 0 ? incl[ntake - 1] : 0;
+  const int32_t* ustart = unit_start + (size_t)s * units_cap;
+  int32_t* rows = row_ws + (size_t)s * budget;
+  for (int p = tid; p < ntake; p += kSelThreads) {
+    const int u = s_id[p];
+    const bool real = u >= 0 && u < n_units;
+    sel_units[(size_t)s * units_cap + p] = real ? u : -1;
+    const int sz = real ? max(us[u], 0) : 0;
+    const int ex = incl[p] - sz;
+    const int st0 = real ? ustart[u] : 0;
+    for (int i = 0; i < sz; ++i) rows[ex + i] = st0 + i;
+  }
+  if (tid == 0) {
+    n_sel_units[s] = ntake;
+    n_sel[s] = nsel;
+  }
+}
+
+// Copy selected pool rows into KV_critical: 16 lanes per row, 16 rows per pass.
+template <class T>
+__global__ __launch_bounds__(256)
+void gather_kernel(const T* __restrict__ k_pool, const T* __restrict__ v_pool, int64_t pool_rows,
+                   const int32_t* __restrict__ row_ws, const int32_t* __restrict__ n_sel,
+                   const uint8_t* __restrict__ fire, int n_kv_heads, int budget, int blocks_per_slice,
+                   int rows_per_block, T* __restrict__ k_buf, T* __restrict__ v_buf) {
+  const int64_t s = blockIdx.x / blocks_per_slice;
+  const int b = (int)(blockIdx.x - s * blocks_per_slice);
+  if (fire && !fire[s / n_kv_heads]) return;
+  const int n = n_sel[s];
+  const int r0 = b * rows_per_block;
+  if (r0 >= n) return;
+  const int r1 = min(n, r0 + rows_per_block);
+  constexpr int kU4 = kHeadDim * sizeof(T) / 16;     // 16 (bf16) or 32 (fp32)
+  const int sub = threadIdx.x & 15;
+  const int32_t* rows = row_ws + (size_t)s * budget;
+  for (int r = r0 + (threadIdx.x >> 4); r < r1; r += 16) {
+    const int64_t pr = rows[r];
+    if (pr < 0 || pr >= pool_rows) continue;   // unit table pointing outside the pool
+    const uint4* ks = reinterpret_cast<const uint4*>(k_pool + ((size_t)s * pool_rows + pr) * kHeadDim);
+    const uint4* vs = reinterpret_cast<const uint4*>(v_pool + ((size_t)s * pool_rows + pr) * kHeadDim);
+    uint4* kd = reinterpret_cast<uint4*>(k_buf + ((size_t)s * budget + r) * kHeadDim);
+    uint4* vd = reinterpret_cast<uint4*>(v_buf + ((size_t)s * budget + r) * kHeadDim);
+#pragma unroll
+    for (int q = sub; q < kU4; q += 16) {
+      const uint4 a = ks[q], c = vs[q];
+      kd[q] = a;
+      vd[q] = c;
+    }
+  }
+}
+
+// ------------------------------------------------------------------ attention
+
+constexpr int kAttnChunk = 256;   // rows per split-KV block
+
+__device__ __forceinline__ void load8(const uint16_t* p, float* x) {
+  const uint4 v = *reinterpret_cast<const uint4*>(p);
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[2 * i] = __uint_as_float(w[i] << 16);
+    x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ void load8(const float* p, float* x) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+
+// Block (chunk, slice): online softmax over up to kAttnChunk rows for the G
+// query heads of the slice; 16 lanes per row, lane sub owns dims 8*sub..+7.
+// Writes (m, l, acc[128]) per head to the partial buffer.
+template <class T, int G>
+__global__ __launch_bounds__(256)
+void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, const T* __restrict__ k_buf,
+                         const T* __restrict__ v_buf, const int32_t* __restrict__ n_sel, int buf_rows,
+                         const T* __restrict__ k_local, const T* __restrict__ v_local, int window, int local_start,
+                         int n_local, int n_chunks, float* __restrict__ part) {
+  __shared__ float s_m[4][G], s_l[4][G];
+  __shared__ float s_acc[4][G][kHeadDim];
+  const int64_t s = blockIdx.x / n_chunks;
+  const int chunk = (int)(blockIdx.x - s * n_chunks);
+  const int64_t grp = s / n_kv_heads;
+  const int kvh = (int)(s - grp * n_kv_heads);
+  const int tid = threadIdx.x, sub = tid & 15, rg = tid >> 4;   // 16 row groups of 16 lanes
+  const int nsel = max(0, min(n_sel[s], buf_rows));
+  const int total = nsel + n_local;
+  const int r0 = chunk * kAttnChunk;
+  const int r1 = min(total, r0 + kAttnChunk);
+
+  float qv[G][8];
+  const size_t qbase = ((size_t)grp * n_kv_heads * G + (size_t)kvh * G) * kHeadDim + 8 * sub;
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    load8(q + qbase + (size_t)j * kHeadDim, qv[j]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) qv[j][e] *= scale;
+  }
+  float m[G], l[G], acc[G][8];
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    m[j] = -__builtin_inff();
+    l[j] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[j][e] = 0.f;
+  }
+  for (int r = r0 + rg; r < r1; r += 16) {
+    const T* kr;
+    const T* vr;
+    if (r < nsel) {
+      kr = k_buf + ((size_t)s * buf_rows + r) * kHeadDim;
+      vr = v_buf + ((size_t)s * buf_rows + r) * kHeadDim;
+    } else {
+      const int slot = (local_start + (r - nsel)) % window;
+      kr = k_local + ((size_t)s * window + slot) * kHeadDim;
+      vr = v_local + ((size_t)s * window + slot) * kHeadDim;
+    }
+    float kx[8], vx[8];
+    load8(kr + 8 * sub, kx);
+    load8(vr + 8 * sub, vx);
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      float d = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) d = fmaf(qv[j][e], kx[e], d);
+      d += __shfl_xor(d, 8, kWave);
+      d += __shfl_xor(d, 4, kWave);
+      d += __shfl_xor(d, 2, kWave);
+      d += __shfl_xor(d, 1, kWave);
+      const float mn = fmaxf(m[j], d);
+      const float corr = expf(m[j] - mn);
+      const float p = expf(d - mn);
+      l[j] = l[j] * corr + p;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[j][e] = fmaf(acc[j][e], corr, p * vx[e]);
+      m[j] = mn;
+    }
+  }
+  // merge the 4 row groups of each wave (lanes l, l^16, l^32, l^48 share sub)
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+#pragma unroll
+    for (int o = 16; o <= 32; o <<= 1) {
+      const float mo = __shfl_xor(m[j], o, kWave);
+      const float lo = __shfl_xor(l[j], o, kWave);
+      const float mn = fmaxf(m[j], mo);
+      const float ca = mn == -__builtin_inff() ? 0.f : expf(m[j] - mn);
+      const float cb = mn == -__builtin_inff() ? 0.f : expf(mo - mn);
+      l[j] = l[j] * ca + lo * cb;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float ao = __shfl_xor(acc[j][e], o, kWave);
+        acc[j][e] = acc[j][e] * ca + ao * cb;
+      }
+      m[j] = mn;
+    }
+  }
+  const int w = tid >> 6;
+  if ((tid & 63) < 16) {
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      if (sub == 0) {
+        s_m[w][j] = m[j];
+        s_l[w][j] = l[j];
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s_acc[w][j][8 * sub + e] = acc[j][e];
+    }
+  }
+  __syncthreads();
+  // merge the 4 waves and write the block's partial
+  const size_t pstride = 2 + kHeadDim;
+  float* out = part + ((size_t)s * n_chunks + chunk) * G * pstride;
+  for (int i = tid; i < G * kHeadDim; i += 256) {
+    const int j = i / kHeadDim, k = i % kHeadDim;
+    float mm = -__builtin_inff();
+    for (int q2 = 0; q2 < 4; ++q2) mm = fmaxf(mm, s_m[q2][j]);
+    float ll = 0.f, aa = 0.f;
+    if (mm != -__builtin_inff()) {
+      for (int q2 = 0; q2 < 4; ++q2) {
+        const float c = expf(s_m[q2][j] - mm);
+        ll += s_l[q2][j] * c;
+        aa += s_acc[q2][j][k] * c;
+      }
+    }
+    out[j * pstride + 2 + k] = aa;
+    if (k == 0) {
+      out[j * pstride + 0] = mm;
+      out[j * pstride + 1] = ll;
+    }
+  }
+}
+
+// One wave per (slice, head): merge the chunk partials.
+template <class TO>
+__global__ __launch_bounds__(256)
+void attn_combine_kernel(const float* __restrict__ part, int n_chunks, int G, int64_t n_rows,
+                         TO* __restrict__ out, float* __restrict__ lse_out) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= n_rows) return;
+  const int lane = threadIdx.x & 63;
+  const int64_t s = row / G;
+  const int j = (int)(row - s * G);
+  const size_t pstride = 2 + kHeadDim;
+  const float* p = part + (size_t)s * n_chunks * G * pstride + (size_t)j * pstride;
+  float mm = -__builtin_inff();
+  for (int c = 0; c < n_chunks; ++c) mm = fmaxf(mm, p[(size_t)c * G * pstride]);
+  float ll = 0.f, a0 = 0.f, a1 = 0.f;
+  if (mm != -__builtin_inff()) {
+    for (int c = 0; c < n_chunks; ++c) {
+      const float* pc = p + (size_t)c * G * pstride;
+      const float w = expf(pc[0] - mm);
+      ll += pc[1] * w;
+      a0 += pc[2 + 2 * lane] * w;
+      a1 += pc[2 + 2 * lane + 1] * w;
+    }
+  }
+  const float inv = ll > 0.f ? 1.f / ll : 0.f;
+  TO* o = out + (size_t)row * kHeadDim;
+  store_from_f32(o, 2 * lane, a0 * inv);
+  store_from_f32(o, 2 * lane + 1, a1 * inv);
+  if (lse_out && lane == 0) lse_out[row] = ll > 0.f ? mm + logf(ll) : -__builtin_inff();
+}
+
+int check_dtype(int dtype) {
+  if (dtype != LOUISKV_F32 && dtype != LOUISKV_BF16) return fail(LOUISKV_ERR_DTYPE, "unknown dtype %d", dtype);
+  return LOUISKV_OK;
+}
+
+size_t retrieve_ws_bytes(int64_t S, int units_cap, int budget, int G) {
+  Carver cv(nullptr);
+  cv.take<double>((size_t)S * units_cap * G);
+  cv.take<int32_t>((size_t)S * std::max(budget, 1));
+  return align_up(cv.used, 256);
+}
+
+int attn_chunks(int buf_rows, int window) { return std::max(1, (buf_rows + window + kAttnChunk - 1) / kAttnChunk); }
+
+size_t attn_ws_bytes(int64_t S, int G, int buf_rows, int window) {
+  return align_up((size_t)S * attn_chunks(buf_rows, window) * G * (2 + kHeadDim) * sizeof(float), 256);
+}
+
+}  // namespace
+}  // namespace louiskv
+
+using namespace louiskv;
+
+extern "C" int louiskv_boundary_check(const void* q, void* q_ref, int32_t dtype, int64_t n_groups, int32_t n_q_heads,
+                                      int32_t d, double tau, int32_t mode, int32_t first_step, double* r_out,
+                                      uint8_t* fire_out, void* stream) {
+  if (!q || !q_ref || !fire_out) return fail(LOUISKV_ERR_NULL, "q, q_ref and fire_out are required");
+  int st = check_dtype(dtype);
+  if (st) return st;
+  if (d != kHeadDim) return fail(LOUISKV_ERR_UNSUPPORTED, "head dim %d not supported (only 128)", d);
+  if (n_groups < 1 || n_q_heads < 1 || n_groups > INT32_MAX)
+    return fail(LOUISKV_ERR_SHAPE, "n_groups=%lld n_q_heads=%d", (long long)n_groups, n_q_heads);
+  if (mode != LOUISKV_REF_PREV && mode != LOUISKV_REF_ANCHOR) return fail(LOUISKV_ERR_SHAPE, "unknown mode %d", mode);
+  hipStream_t s = as_stream(stream);
+  if (dtype == LOUISKV_BF16)
+    boundary_kernel<uint16_t><<<(unsigned)n_groups, 256, 0, s>>>(static_cast<const uint16_t*>(q),
+                                                                 static_cast<uint16_t*>(q_ref), n_q_heads, tau, mode,
+                                                                 first_step ? 1 : 0, r_out, fire_out);
+  else
+    boundary_kernel<float><<<(unsigned)n_groups, 256, 0, s>>>(static_cast<const float*>(q), static_cast<float*>(q_ref),
+                                                              n_q_heads, tau, mode, first_step ? 1 : 0, r_out,
+                                                              fire_out);
+  LKV_CHECK_LAUNCH();
+  return LOUISKV_OK;
+}
+
+extern "C" int louiskv_segment_output(const void* k_new, const void* v_new, int32_t dtype, int64_t n_slices, int32_t d,
+                                      void* k_local, void* v_local, int32_t window, int32_t step, int32_t seg_len,
+                                      float* reps, int32_t* unit_start, int32_t* unit_size, int32_t units_cap,
+                                      int32_t n_clusters, void* k_pool, void* v_pool, int64_t pool_rows,
+                                      int32_t prompt_len, int32_t pool_on_host, void* stream) {
+  (void)pool_on_host;
+  if (!k_new || !v_new || !k_local || !v_local) return fail(LOUISKV_ERR_NULL, "k_new, v_new, k_local, v_local required");
+  int st = check_dtype(dtype);
+  if (st) return st;
+  if (d != kHeadDim) return fail(LOUISKV_ERR_UNSUPPORTED, "head dim %d not supported (only 128)", d);
+  if (n_slices < 1 || n_slices > INT32_MAX) return fail(LOUISKV_ERR_SHAPE, "n_slices=%lld", (long long)n_slices);
+  int32_t ev = -1, n_ev = 0;
+  st = louiskv_window_info(step, window, seg_len, &ev, &n_ev, nullptr, nullptr);
+  if (st) return st;
+  if (ev >= 0) {
+    if (!reps || !unit_start || !unit_size) return fail(LOUISKV_ERR_NULL, "unit tables required for an eviction");
+    if (n_clusters < 0 || (int64_t)n_clusters + ev >= units_cap)
+      return fail(LOUISKV_ERR_SHAPE, "unit %d exceeds units_cap=%d", n_clusters + ev, units_cap);
+    if ((k_pool || v_pool) && (int64_t)prompt_len + (int64_t)(ev + 1) * seg_len > pool_rows)
+      return fail(LOUISKV_ERR_SHAPE, "segment rows exceed pool_rows=%lld", (long long)pool_rows);
+    if (v_pool && !k_pool) return fail(LOUISKV_ERR_NULL, "v_pool given without k_pool");
+  }
+  hipStream_t s = as_stream(stream);
+  if (dtype == LOUISKV_BF16)
+    store_decode_kernel<uint16_t><<<(unsigned)n_slices, 64, 0, s>>>(
+        static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new), static_cast<uint16_t*>(k_local),
+        static_cast<uint16_t*>(v_local), window, step, seg_len, ev, reps, unit_start, unit_size, units_cap, n_clusters,
+        static_cast<uint16_t*>(k_pool), static_cast<uint16_t*>(v_pool), pool_rows, prompt_len);
+  else
+    store_decode_kernel<float><<<(unsigned)n_slices, 64, 0, s>>>(
+        static_cast<const float*>(k_new), static_cast<const float*>(v_new), static_cast<float*>(k_local),
+        static_cast<float*>(v_local), window, step, seg_len, ev, reps, unit_start, unit_size, units_cap, n_clusters,
+        static_cast<float*>(k_pool), static_cast<float*>(v_pool), pool_rows, prompt_len);
+  LKV_CHECK_LAUNCH();
+  return LOUISKV_OK;
+}
+
+extern "C" size_t louiskv_retrieve_workspace_size(int64_t n_slices, int32_t units_cap, int32_t budget) {
+  if (n_slices < 1 || units_cap < 1 || budget < 0) return 0;
+  return retrieve_ws_bytes(n_slices, units_cap, budget, kMaxGroupSize);
+}
+
+extern "C" int louiskv_retrieve(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads, int32_t group_size,
+                                int32_t d, double scale, const float* reps, const int32_t* unit_start,
+                                const int32_t* unit_size, int32_t units_cap, int32_t n_units, const void* k_pool,
+                                const void* v_pool, int64_t pool_rows, int32_t pool_on_host, int32_t budget,
+                                const uint8_t* fire, int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel,
+                                void* k_buf, void* v_buf, double* scores_out, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  (void)pool_on_host;
+  if (!q || !reps || !unit_start || !unit_size || !k_pool || !v_pool || !sel_units || !n_sel_units || !n_sel || !k_buf ||
+      !v_buf)
+    return fail(LOUISKV_ERR_NULL, "a required pointer of louiskv_retrieve is NULL");
+  int st = check_dtype(dtype);
+  if (st) return st;
+  if (d != kHeadDim) return fail(LOUISKV_ERR_UNSUPPORTED, "head dim %d not supported (only 128)", d);
+  if (n_kv_heads < 1 || n_slices < 1 || n_slices % n_kv_heads != 0 || n_slices > INT32_MAX)
+    return fail(LOUISKV_ERR_SHAPE, "n_slices=%lld must be a positive multiple of n_kv_heads=%d", (long long)n_slices,
+                n_kv_heads);
+  if (group_size < 1 || group_size > kMaxGroupSize)
+    return fail(LOUISKV_ERR_UNSUPPORTED, "group_size=%d must be in [1, %d]", group_size, kMaxGroupSize);
+  if (n_units < 1 || n_units > units_cap || n_units > kMaxUnits)
+    return fail(LOUISKV_ERR_SHAPE, "n_units=%d must be in [1, min(units_cap=%d, %d)]", n_units, units_cap, kMaxUnits);
+  if (budget < 0) return fail(LOUISKV_ERR_SHAPE, "budget=%d < 0", budget);
+  const size_t need = retrieve_ws_bytes(n_slices, units_cap, budget, kMaxGroupSize);
+  if (!workspace || workspace_bytes < need)
+    return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  Carver cv(workspace);
+  double* logit_ws = cv.take<double>((size_t)n_slices * units_cap * kMaxGroupSize);
+  int32_t* row_ws = cv.take<int32_t>((size_t)n_slices * std::max(budget, 1));
+  int n_pad = 1;
+  while (n_pad < n_units) n_pad <<= 1;
+  const size_t lds = (size_t)n_pad * (sizeof(double) + sizeof(int));
+  hipStream_t s = as_stream(stream);
+  if (dtype == LOUISKV_BF16)
+    score_select_kernel<uint16_t><<<(unsigned)n_slices, kSelThreads, lds, s>>>(
+        static_cast<const uint16_t*>(q), n_kv_heads, group_size, scale, reps, unit_start, unit_size, units_cap, n_units,
+        budget, fire, sel_units, n_sel_units, n_sel, scores_out, logit_ws, row_ws, n_pad);
+  else
+    score_select_kernel<float><<<(unsigned)n_slices, kSelThreads, lds, s>>>(
+        static_cast<const float*>(q), n_kv_heads, group_size, scale, reps, unit_start, unit_size, units_cap, n_units,
+        budget, fire, sel_units, n_sel_units, n_sel, scores_out, logit_ws, row_ws, n_pad);
+  LKV_CHECK_LAUNCH();
+  if (budget > 0) {
+    const int rpb = 128;
+    const int bps = (budget + rpb - 1) / rpb;
+    const unsigned grid = (unsigned)(n_slices * bps);
+    if (dtype == LOUISKV_BF16)
+      gather_kernel<uint16_t><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(k_pool),
+                                                   static_cast<const uint16_t*>(v_pool), pool_rows, row_ws, n_sel, fire,
+                                                   n_kv_heads, budget, bps, rpb, static_cast<uint16_t*>(k_buf),
+                                                   static_cast<uint16_t*>(v_buf));
+    else
+      gather_kernel<float><<<grid, 256, 0, s>>>(static_cast<const float*>(k_pool), static_cast<const float*>(v_pool),
+                                                pool_rows, row_ws, n_sel, fire, n_kv_heads, budget, bps, rpb,
+                                                static_cast<float*>(k_buf), static_cast<float*>(v_buf));
+    LKV_CHECK_LAUNCH();
+  }
+  return LOUISKV_OK;
+}
+
+extern "C" size_t louiskv_sparse_decode_attn_workspace_size(int64_t n_slices, int32_t group_size, int32_t d,
+                                                            int32_t buf_rows, int32_t window) {
+  (void)d;
+  if (n_slices < 1 || group_size < 1 || buf_rows < 0 || window < 0) return 0;
+  return attn_ws_bytes(n_slices, group_size, buf_rows, window);
+}
+
+template <class T, int G>
+static void launch_attn_partial(const void* q, int n_kv_heads, float scale, const void* k_buf, const void* v_buf,
+                                const int32_t* n_sel, int buf_rows, const void* k_local, const void* v_local,
+                                int window, int local_start, int n_local, int n_chunks, float* part, unsigned grid,
+                                hipStream_t s) {
+  attn_partial_kernel<T, G><<<grid, 256, 0, s>>>(
+      static_cast<const T*>(q), n_kv_heads, scale, static_cast<const T*>(k_buf), static_cast<const T*>(v_buf), n_sel,
+      buf_rows, static_cast<const T*>(k_local), static_cast<const T*>(v_local), window, local_start, n_local, n_chunks,
+      part);
+}
+
+extern "C" int louiskv_sparse_decode_attn(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads,
+                                          int32_t group_size, int32_t d, float scale, const void* k_buf,
+                                          const void* v_buf, const int32_t* n_sel, int32_t buf_rows,
+                                          const void* k_local, const void* v_local, int32_t window,
+                                          int32_t local_start, int32_t n_local, void* out, int32_t out_dtype,
+                                          float* lse_out, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!q || !out || !n_sel) return fail(LOUISKV_ERR_NULL, "q, out and n_sel are required");
+  if (buf_rows > 0 && (!k_buf || !v_buf)) return fail(LOUISKV_ERR_NULL, "k_buf/v_buf required when buf_rows > 0");
+  if (n_local > 0 && (!k_local || !v_local)) return fail(LOUISKV_ERR_NULL, "k_local/v_local required when n_local > 0");
+  int st = check_dtype(dtype);
+  if (st) return st;
+  if ((st = check_dtype(out_dtype))) return st;
+  if (d != kHeadDim) return fail(LOUISKV_ERR_UNSUPPORTED, "head dim %d not supported (only 128)", d);
+  if (n_kv_heads < 1 || n_slices < 1 || n_slices % n_kv_heads != 0)
+    return fail(LOUISKV_ERR_SHAPE, "n_slices=%lld must be a positive multiple of n_kv_heads=%d", (long long)n_slices,
+                n_kv_heads);
+  if (group_size != 1 && group_size != 2 && group_size != 4 && group_size != 8)
+    return fail(LOUISKV_ERR_UNSUPPORTED, "group_size=%d must be 1, 2, 4 or 8", group_size);
+  if (buf_rows < 0 || window < 0 || n_local < 0 || n_local > window || (window > 0 && (local_start < 0 || local_start >= window)))
+    return fail(LOUISKV_ERR_SHAPE, "buf_rows=%d window=%d local_start=%d n_local=%d", buf_rows, window, local_start,
+                n_local);
+  const int n_chunks = attn_chunks(buf_rows, window);
+  if ((int64_t)n_slices * n_chunks > INT32_MAX) return fail(LOUISKV_ERR_SHAPE, "problem too large for one launch");
+  const size_t need = attn_ws_bytes(n_slices, group_size, buf_rows, window);
+  if (!workspace || workspace_bytes < need)
+    return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  float* part = static_cast<float*>(workspace);
+  hipStream_t s = as_stream(stream);
+  const unsigned grid = (unsigned)(n_slices * n_chunks);
+  const int win = window > 0 ? window : 1;
+  const int lstart = window > 0 ? local_start : 0;
+#define LKV_ATTN(T, G) \
+  launch_attn_partial<T, G>(q, n_kv_heads, scale, k_buf, v_buf, n_sel, buf_rows, k_local, v_local, win, lstart, n_local, \
+                            n_chunks, part, grid, s)
+  if (dtype == LOUISKV_BF16) {
+    switch (group_size) {
+      case 1: LKV_ATTN(uint16_t, 1); break;
+      case 2: LKV_ATTN(uint16_t, 2); break;
+      case 4: LKV_ATTN(uint16_t, 4); break;
+      default: LKV_ATTN(uint16_t, 8); break;
+    }
+  } else {
+    switch (group_size) {
+      case 1: LKV_ATTN(float, 1); break;
+      case 2: LKV_ATTN(float, 2); break;
+      case 4: LKV_ATTN(float, 4); break;
+      default: LKV_ATTN(float, 8); break;
+    }
+  }
+#undef LKV_ATTN
+  LKV_CHECK_LAUNCH();
+  const int64_t rows = n_slices * group_size;
+  const int cgrid = (int)((rows + 3) / 4);
+  if (out_dtype == LOUISKV_BF16)
+    attn_combine_kernel<uint16_t><<<cgrid, 256, 0, s>>>(part, n_chunks, group_size, rows, static_cast<uint16_t*>(out),
+                                                        lse_out);
+  else
+    attn_combine_kernel<float><<<cgrid, 256, 0, s>>>(part, n_chunks, group_size, rows, static_cast<float*>(out),
+                                                     lse_out);
+  LKV_CHECK_LAUNCH();
+  return LOUISKV_OK;
+}

@@ -1,0 +1,727 @@
+// Prefill-stage k-means of prompt keys (Section 4.2 prefill stage; Algorithm 1
+// store_cache prefill branch), one independent problem per (sequence, layer,
+// KV head) slice.
+//
+// Per Lloyd iteration:
+//   prep     centroid operand for the matrix cores: -2 * op(c) laid out as MFMA
+//            A-fragments (op = bf16 RNE rounding for bf16 keys, identity for fp32),
+//            plus ||op(c)||^2 (float64 sum, rounded to fp32); zero the counts.
+//   assign   D = ||op(c)||^2 - 2 op(c).k on MFMA (the norm enters as the
+//            accumulator input), running argmin per key kept in registers,
+//            block histogram of the chosen clusters into counts.
+//   scan     exclusive scan of counts -> CSR offsets and scatter cursors.
+//   scatter  key ids into their cluster's member range (order unspecified).
+//   sum      centroid = float64 sum of members / count, rounded once to fp32;
+//            empty clusters keep their centroid.  Sums of bf16 or fp32 inputs
+//            are exact in float64 at these sizes, so the order is irrelevant.
+// After the last iteration, finalize sorts each member range ascending (the
+// perm output), writes the unit table, and pack copies K/V rows into the pool.
+#include "common.h"
+
+namespace louiskv {
+namespace {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
+
+constexpr int kTileC = 32;                 // centroids per MFMA tile (rows of D)
+constexpr int kBf16Steps = 8;              // 32x32x16 MFMAs per 128-wide dot product
+constexpr int kBf16TileU4 = kBf16Steps * 64;       // uint4 per bf16 operand tile (8 KB)
+constexpr int kF32TileU4 = 16 * 64;                // uint4 per fp32 operand tile (16 KB)
+
+constexpr int kAssignThreads = 256;
+constexpr int kBf16KeyTiles = 4;                   // 32-key tiles held per wave
+constexpr int kBf16KeysPerBlock = 4 * 32 * kBf16KeyTiles;   // 512
+constexpr int kBf16StageTiles = 4;
+constexpr int kF32KeysPerBlock = 4 * 32;           // one 32-key tile per wave
+constexpr int kF32StageTiles = 2;
+
+__host__ __device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+template <class T>
+__global__ void init_centroids_kernel(const T* __restrict__ keys, const int32_t* __restrict__ init_idx,
+                                      float* __restrict__ reps, int n_tokens, int n_clusters,
+                                      int units_cap, int64_t n_rows) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= n_rows) return;
+  const int lane = threadIdx.x & 63;
+  const int64_t s = row / n_clusters;
+  const int c = (int)(row - s * n_clusters);
+  int t = init_idx[s * n_clusters + c];
+  t = t < 0 ? 0 : (t >= n_tokens ? n_tokens - 1 : t);
+  const T* src = keys + ((size_t)s * n_tokens + t) * kHeadDim;
+  float* dst = reps + ((size_t)s * units_cap + c) * kHeadDim;
+  dst[2 * lane] = load_as_f32(src, 2 * lane);
+  dst[2 * lane + 1] = load_as_f32(src, 2 * lane + 1);
+}
+
+// One wave per padded centroid row.  Writes the A-fragments of -2*op(c) and
+// ||op(c)||^2; padding rows get a zero operand and +inf norm so they never win.
+//
+// Dimension k of a centroid maps to MFMA operand position (lane half h, step,
+// element): bf16: k = 64h + 8*step + e; fp32: k = 64h + step.  The key operand
+// uses the same map, so each product pairs equal dimensions.
+template <bool kBf16>
+__global__ void prep_operand_kernel(const float* __restrict__ reps, int units_cap, int n_clusters,
+                                    int n_ctiles, uint4* __restrict__ frag, float* __restrict__ cnorm,
+                                    int32_t* __restrict__ counts, int64_t n_rows) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= n_rows) return;
+  const int lane = threadIdx.x & 63;
+  const int cpad = n_ctiles * kTileC;
+  const int64_t s = row / cpad;
+  const int c = (int)(row - s * cpad);
+  const bool real = c < n_clusters;
+  float v0 = 0.f, v1 = 0.f;
+  if (real) {
+    const float* src = reps + ((size_t)s * units_cap + c) * kHeadDim;
+    v0 = src[2 * lane];
+    v1 = src[2 * lane + 1];
+  }
+  if (kBf16) {
+    v0 = bf16_to_f32(f32_to_bf16(v0));
+    v1 = bf16_to_f32(f32_to_bf16(v1));
+  }
+  double nrm = wave_sum((double)v0 * v0 + (double)v1 * v1);
+  const int t = c / kTileC, ci = c % kTileC;
+  const int k0 = 2 * lane, h = k0 >> 6;
+  const int flane = h * 32 + ci;
+  if (kBf16) {
+    const int step = (k0 & 63) >> 3, e = k0 & 7;
+    uint16_t* f = reinterpret_cast<uint16_t*>(frag + ((size_t)s * n_ctiles + t) * kBf16TileU4);
+    const uint32_t lo = f32_to_bf16(-2.f * v0), hi = f32_to_bf16(-2.f * v1);
+    *reinterpret_cast<uint32_t*>(f + ((size_t)(step * 64 + flane) * 8 + e)) = lo | (hi << 16);
+  } else {
+    float* f = reinterpret_cast<float*>(frag + ((size_t)s * n_ctiles + t) * kF32TileU4);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int step = (k0 + q) & 63;
+      f[((size_t)(step >> 2) * 64 + flane) * 4 + (step & 3)] = -2.f * (q ? v1 : v0);
+    }
+  }
+  if (lane == 0) {
+    cnorm[(size_t)s * cpad + c] = real ? (float)nrm : __builtin_inff();
+    if (real && counts) counts[(size_t)s * n_clusters + c] = 0;
+  }
+}
+
+// Block histogram of chosen clusters, merged into counts[slice][*].
+__device__ __forceinline__ void block_histogram(int* hist, bool lds_ok, int n_clusters, int32_t* counts_slice,
+                                                const int* idx, const bool* valid, int n_local) {
+  const int tid = threadIdx.x;
+  if (lds_ok) {
+    for (int i = tid; i < n_clusters; i += blockDim.x) hist[i] = 0;
+    __syncthreads();
+    for (int q = 0; q < n_local; ++q)
+      if (valid[q]) atomicAdd(&hist[idx[q]], 1);
+    __syncthreads();
+    for (int i = tid; i < n_clusters; i += blockDim.x)
+      if (hist[i]) atomicAdd(&counts_slice[i], hist[i]);
+  } else {
+    for (int q = 0; q < n_local; ++q)
+      if (valid[q]) atomicAdd(&counts_slice[idx[q]], 1);
+  }
+}
+
+// bf16 keys: each wave holds kBf16KeyTiles tiles of 32 keys as MFMA B operands
+// for the whole sweep; centroid tiles stream through LDS.  Lane l owns key
+// column l % 32 and rows 8*(v/4) + 4*(l/32) + (v%4) of each 32x32 result, so
+// the argmin over a tile is in-lane; the two lane halves merge at the end.
+__global__ __launch_bounds__(kAssignThreads, 2)
+void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restrict__ frag,
+                        const float* __restrict__ cnorm, int32_t* __restrict__ assign,
+                        int32_t* __restrict__ counts, int n_tokens, int n_clusters, int n_ctiles,
+                        int blocks_per_slice, int hist_in_lds) {
+  extern __shared__ __align__(16) char smem[];
+  uint4* s_frag = reinterpret_cast<uint4*>(smem);
+  float* s_cn = reinterpret_cast<float*>(smem + kBf16StageTiles * kBf16TileU4 * 16);
+
+  const int slice = blockIdx.x / blocks_per_slice;
+  const int kb = blockIdx.x - slice * blocks_per_slice;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, j = lane & 31;
+  const int key_base = kb * kBf16KeysPerBlock + wave * (32 * kBf16KeyTiles);
+  const uint16_t* kslice = keys + (size_t)slice * n_tokens * kHeadDim;
+
+  bf16x8_t b[kBf16KeyTiles][kBf16Steps];
+#pragma unroll
+  for (int kt = 0; kt < kBf16KeyTiles; ++kt) {
+    const int key = key_base + kt * 32 + j;
+    const uint4* src = reinterpret_cast<const uint4*>(kslice + (size_t)key * kHeadDim + 64 * h);
+#pragma unroll
+    for (int s = 0; s < kBf16Steps; ++s) {
+      uint4 v = key < n_tokens ? src[s] : make_uint4(0, 0, 0, 0);
+      b[kt][s] = __builtin_bit_cast(bf16x8_t, v);
+    }
+  }
+  float best[kBf16KeyTiles];
+  int bidx[kBf16KeyTiles];
+#pragma unroll
+  for (int kt = 0; kt < kBf16KeyTiles; ++kt) {
+    best[kt] = __builtin_inff();
+    bidx[kt] = 0;
+  }
+
+  const uint4* fslice = frag + (size_t)slice * n_ctiles * kBf16TileU4;
+  const float* cslice = cnorm + (size_t)slice * n_ctiles * kTileC;
+  for (int t0 = 0; t0 < n_ctiles; t0 += kBf16StageTiles) {
+    const int nt = min(kBf16StageTiles, n_ctiles - t0);
+    __syncthreads();
+    for (int i = tid; i < nt * kBf16TileU4; i += kAssignThreads) s_frag[i] = fslice[(size_t)t0 * kBf16TileU4 + i];
+    for (int i = tid; i < nt * kTileC; i += kAssignThreads) s_cn[i] = cslice[t0 * kTileC + i];
+    __syncthreads();
+    for (int tt = 0; tt < nt; ++tt) {
+      bf16x8_t a[kBf16Steps];
+#pragma unroll
+      for (int s = 0; s < kBf16Steps; ++s)
+        a[s] = __builtin_bit_cast(bf16x8_t, s_frag[(tt * kBf16Steps + s) * 64 + lane]);
+      floatx16 cn;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const float4 x = *reinterpret_cast<const float4*>(&s_cn[tt * kTileC + 8 * g + 4 * h]);
+        cn[4 * g + 0] = x.x; cn[4 * g + 1] = x.y; cn[4 * g + 2] = x.z; cn[4 * g + 3] = x.w;
+      }
+      const int cbase = (t0 + tt) * kTileC + 4 * h;
+#pragma unroll
+      for (int kt = 0; kt < kBf16KeyTiles; ++kt) {
+        floatx16 acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], b[kt][0], cn, 0, 0, 0);
+#pragma unroll
+        for (int s = 1; s < kBf16Steps; ++s)
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s], b[kt][s], acc, 0, 0, 0);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float x = acc[v];
+          const int c = cbase + 8 * (v >> 2) + (v & 3);
+          if (x < best[kt]) { best[kt] = x; bidx[kt] = c; }
+        }
+      }
+    }
+  }
+
+  int zi[kBf16KeyTiles];
+  bool zv[kBf16KeyTiles];
+#pragma unroll
+  for (int kt = 0; kt < kBf16KeyTiles; ++kt) {
+    const float ob = __shfl_xor(best[kt], 32, kWave);
+    const int oi = __shfl_xor(bidx[kt], 32, kWave);
+    if (ob < best[kt] || (ob == best[kt] && oi < bidx[kt])) { best[kt] = ob; bidx[kt] = oi; }
+    const int key = key_base + kt * 32 + j;
+    zi[kt] = bidx[kt];
+    zv[kt] = (h == 0) && key < n_tokens;
+    if (zv[kt]) assign[(size_t)slice * n_tokens + key] = bidx[kt];
+  }
+  if (counts) {
+    __syncthreads();
+    block_histogram(reinterpret_cast<int*>(smem), hist_in_lds, n_clusters,
+                    counts + (size_t)slice * n_clusters, zi, zv, kBf16KeyTiles);
+  }
+}
+
+// fp32 keys: the same scheme with 32x32x2 fp32 MFMAs (64 steps per dot product)
+// and one 32-key tile per wave.
+__global__ __launch_bounds__(kAssignThreads, 2)
+void assign_f32_kernel(const float* __restrict__ keys, const uint4* __restrict__ frag,
+                       const float* __restrict__ cnorm, int32_t* __restrict__ assign,
+                       int32_t* __restrict__ counts, int n_tokens, int n_clusters, int n_ctiles,
+                       int blocks_per_slice, int hist_in_lds) {
+  extern __shared__ __align__(16) char smem[];
+  uint4* s_frag = reinterpret_cast<uint4*>(smem);
+  float* s_cn = reinterpret_cast<float*>(smem + kF32StageTiles * kF32TileU4 * 16);
+
+  const int slice = blockIdx.x / blocks_per_slice;
+  const int kb = blockIdx.x - slice * blocks_per_slice;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, j = lane & 31;
+  const int key = kb * kF32KeysPerBlock + wave * 32 + j;
+  const float* kslice = keys + (size_t)slice * n_tokens * kHeadDim;
+
+  float b[64];
+  {
+    const float4* src = reinterpret_cast<const float4*>(kslice + (size_t)key * kHeadDim + 64 * h);
+#pragma unroll
+    for (int s4 = 0; s4 < 16; ++s4) {
+      float4 v = key < n_tokens ? src[s4] : make_float4(0.f, 0.f, 0.f, 0.f);
+      b[4 * s4 + 0] = v.x; b[4 * s4 + 1] = v.y; b[4 * s4 + 2] = v.z; b[4 * s4 + 3] = v.w;
+    }
+  }
+  float best = __builtin_inff();
+  int bidx = 0;
+  const uint4* fslice = frag + (size_t)slice * n_ctiles * kF32TileU4;
+  const float* cslice = cnorm + (size_t)slice * n_ctiles * kTileC;
+  for (int t0 = 0; t0 < n_ctiles; t0 += kF32StageTiles) {
+    const int nt = min(kF32StageTiles, n_ctiles - t0);
+    __syncthreads();
+    for (int i = tid; i < nt * kF32TileU4; i += kAssignThreads) s_frag[i] = fslice[(size_t)t0 * kF32TileU4 + i];
+    for (int i = tid; i < nt * kTileC; i += kAssignThreads) s_cn[i] = cslice[t0 * kTileC + i];
+    __syncthreads();
+    for (int tt = 0; tt < nt; ++tt) {
+      floatx16 acc;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const float4 x = *reinterpret_cast<const float4*>(&s_cn[tt * kTileC + 8 * g + 4 * h]);
+        acc[4 * g + 0] = x.x; acc[4 * g + 1] = x.y; acc[4 * g + 2] = x.z; acc[4 * g + 3] = x.w;
+      }
+#pragma unroll
+      for (int s4 = 0; s4 < 16; ++s4) {
+        const float4 a4 = __builtin_bit_cast(float4, s_frag[(tt * 16 + s4) * 64 + lane]);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.x, b[4 * s4 + 0], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.y, b[4 * s4 + 1], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.z, b[4 * s4 + 2], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.w, b[4 * s4 + 3], acc, 0, 0, 0);
+      }
+      const int cbase = (t0 + tt) * kTileC + 4 * h;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float x = acc[v];
+        const int c = cbase + 8 * (v >> 2) + (v & 3);
+        if (x < best) { best = x; bidx = c; }
+      }
+    }
+  }
+  const float ob = __shfl_xor(best, 32, kWave);
+  const int oi = __shfl_xor(bidx, 32, kWave);
+  if (ob < best || (ob == best && oi < bidx)) { best = ob; bidx = oi; }
+  const bool valid = (h == 0) && key < n_tokens;
+  if (valid) assign[(size_t)slice * n_tokens + key] = bidx;
+  if (counts) {
+    __syncthreads();
+    int zi[1] = {bidx};
+    bool zv[1] = {valid};
+    block_histogram(reinterpret_cast<int*>(smem), hist_in_lds, n_clusters,
+                    counts + (size_t)slice * n_clusters, zi, zv, 1);
+  }
+}
+
+constexpr int kCountKeys = 1024;
+
+// counts[s][c] = number of keys with assign == c (used by the standalone update).
+__global__ void count_kernel(const int32_t* __restrict__ assign, int32_t* __restrict__ counts, int n_tokens,
+                             int n_clusters, int blocks_per_slice, int hist_in_lds) {
+  extern __shared__ __align__(16) char smem[];
+  const int slice = blockIdx.x / blocks_per_slice;
+  const int kb = blockIdx.x - slice * blocks_per_slice;
+  int zi[4];
+  bool zv[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int i = kb * kCountKeys + q * 256 + threadIdx.x;
+    zv[q] = i < n_tokens;
+    zi[q] = zv[q] ? assign[(size_t)slice * n_tokens + i] : 0;
+    zv[q] = zv[q] && zi[q] >= 0 && zi[q] < n_clusters;
+  }
+  block_histogram(reinterpret_cast<int*>(smem), hist_in_lds, n_clusters,
+                  counts + (size_t)slice * n_clusters, zi, zv, 4);
+}
+
+// Per slice: offsets[c] = sum of counts[<c], offsets[C] = total; cursor = offsets.
+__global__ __launch_bounds__(1024)
+void scan_kernel(const int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
+                 int32_t* __restrict__ cursor, int n_clusters) {
+  __shared__ int s_warp[16];
+  __shared__ int s_carry;
+  const int slice = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int32_t* cnt = counts + (size_t)slice * n_clusters;
+  int32_t* off = offsets + (size_t)slice * (n_clusters + 1);
+  int32_t* cur = cursor + (size_t)slice * n_clusters;
+  if (tid == 0) s_carry = 0;
+  __syncthreads();
+  for (int base = 0; base < n_clusters; base += 1024) {
+    const int c = base + tid;
+    const int v = c < n_clusters ? cnt[c] : 0;
+    int x = v;  // inclusive wave scan
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o, kWave);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) s_warp[w] = x;
+    __syncthreads();
+    int wprefix = 0;
+    for (int q = 0; q < w; ++q) wprefix += s_warp[q];
+    const int carry = s_carry;
+    const int excl = carry + wprefix + x - v;
+    if (c < n_clusters) {
+      off[c] = excl;
+      cur[c] = excl;
+    }
+    __syncthreads();
+    if (tid == 1023) s_carry = excl + v;
+    __syncthreads();
+  }
+  if (tid == 0) off[n_clusters] = s_carry;
+}
+
+constexpr int kScatterKeys = 1024;
+
+// members[s][offsets[z] + k] = i for the keys i of each cluster z, k unique per key.
+__global__ void scatter_kernel(const int32_t* __restrict__ assign, int32_t* __restrict__ cursor,
+                               int32_t* __restrict__ members, int n_tokens, int n_clusters,
+                               int blocks_per_slice, int lds_ok) {
+  extern __shared__ __align__(16) char smem[];
+  int* hist = reinterpret_cast<int*>(smem);
+  int* base = hist + n_clusters;
+  const int slice = blockIdx.x / blocks_per_slice;
+  const int kb = blockIdx.x - slice * blocks_per_slice;
+  const int tid = threadIdx.x;
+  int32_t* cur = cursor + (size_t)slice * n_clusters;
+  int32_t* mem = members + (size_t)slice * n_tokens;
+  int z[4], pos[4];
+  bool ok[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int i = kb * kScatterKeys + q * 256 + tid;
+    ok[q] = i < n_tokens;
+    z[q] = ok[q] ? assign[(size_t)slice * n_tokens + i] : 0;
+    ok[q] = ok[q] && z[q] >= 0 && z[q] < n_clusters;   // same keys as the count
+    if (!ok[q]) z[q] = 0;
+  }
+  if (!lds_ok) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (ok[q]) mem[atomicAdd(&cur[z[q]], 1)] = kb * kScatterKeys + q * 256 + tid;
+    return;
+  }
+  for (int i = tid; i < n_clusters; i += 256) hist[i] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < 4; ++q) pos[q] = ok[q] ? atomicAdd(&hist[z[q]], 1) : 0;
+  __syncthreads();
+  for (int i = tid; i < n_clusters; i += 256)
+    if (hist[i]) base[i] = atomicAdd(&cur[i], hist[i]);
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    if (ok[q]) mem[base[z[q]] + pos[q]] = kb * kScatterKeys + q * 256 + tid;
+}
+
+// One wave per (slice, cluster): mean of the member keys, float64 sum.
+template <class T>
+__global__ void centroid_sum_kernel(const T* __restrict__ keys, const int32_t* __restrict__ members,
+                                    const int32_t* __restrict__ offsets, const int32_t* __restrict__ counts,
+                                    const float* centroids_in, float* centroids_out, int stride,
+                                    int n_tokens, int n_clusters, int64_t n_rows) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= n_rows) return;
+  const int lane = threadIdx.x & 63;
+  const int64_t s = row / n_clusters;
+  const int c = (int)(row - s * n_clusters);
+  const int n = counts[s * n_clusters + c];
+  float* dst = centroids_out + ((size_t)s * stride + c) * kHeadDim;
+  if (n == 0) {
+    if (centroids_in != centroids_out) {
+      const float* src = centroids_in + ((size_t)s * stride + c) * kHeadDim;
+      dst[2 * lane] = src[2 * lane];
+      dst[2 * lane + 1] = src[2 * lane + 1];
+    }
+    return;
+  }
+  const int off = offsets[s * (n_clusters + 1) + c];
+  const int32_t* mem = members + (size_t)s * n_tokens + off;
+  const T* kslice = keys + (size_t)s * n_tokens * kHeadDim;
+  double a0 = 0.0, a1 = 0.0;
+  for (int m0 = 0; m0 < n; m0 += 64) {
+    const int mine = (m0 + lane < n) ? mem[m0 + lane] : 0;
+    const int cnt = min(64, n - m0);
+    int q = 0;
+    for (; q + 4 <= cnt; q += 4) {
+      float x[4][2];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int tok = __shfl(mine, q + u, kWave);
+        const T* r = kslice + (size_t)tok * kHeadDim;
+        x[u][0] = load_as_f32(r, 2 * lane);
+        x[u][1] = load_as_f32(r, 2 * lane + 1);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        a0 += (double)x[u][0];
+        a1 += (double)x[u][1];
+      }
+    }
+    for (; q < cnt; ++q) {
+      const int tok = __shfl(mine, q, kWave);
+      const T* r = kslice + (size_t)tok * kHeadDim;
+      a0 += (double)load_as_f32(r, 2 * lane);
+      a1 += (double)load_as_f32(r, 2 * lane + 1);
+    }
+  }
+  dst[2 * lane] = (float)(a0 / (double)n);
+  dst[2 * lane + 1] = (float)(a1 / (double)n);
+}
+
+// One wave per (slice, cluster): member ids sorted ascending into perm (rank =
+// number of smaller ids, ids are distinct), and the unit-table entry.
+__global__ void finalize_kernel(const int32_t* __restrict__ members, const int32_t* __restrict__ offsets,
+                                const int32_t* __restrict__ counts, int32_t* __restrict__ perm,
+                                int32_t* __restrict__ unit_start, int32_t* __restrict__ unit_size,
+                                int units_cap, int n_tokens, int n_clusters, int64_t n_rows) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= n_rows) return;
+  const int lane = threadIdx.x & 63;
+  const int64_t s = row / n_clusters;
+  const int c = (int)(row - s * n_clusters);
+  const int n = counts[s * n_clusters + c];
+  const int off = offsets[s * (n_clusters + 1) + c];
+  if (lane == 0) {
+    unit_start[s * units_cap + c] = off;
+    unit_size[s * units_cap + c] = n;
+  }
+  const int32_t* mem = members + (size_t)s * n_tokens + off;
+  int32_t* out = perm + (size_t)s * n_tokens + off;
+  if (n <= 64) {
+    const int mine = lane < n ? mem[lane] : 0x7fffffff;
+    int rank = 0;
+    for (int q = 0; q < n; ++q) rank += __shfl(mine, q, kWave) < mine;
+    if (lane < n) out[rank] = mine;
+    return;
+  }
+  for (int i = lane; i < n; i += 64) {
+    const int mine = mem[i];
+    int rank = 0;
+    for (int q = 0; q < n; ++q) rank += mem[q] < mine;
+    out[rank] = mine;
+  }
+}
+
+// pool[s][r] = src[s][perm[s][r]] for r < n_tokens; 16 lanes per row.
+template <class T>
+__global__ void pack_pool_kernel(const T* __restrict__ src, const int32_t* __restrict__ perm,
+                                 T* __restrict__ pool, int64_t pool_rows, int n_tokens, int64_t n_rows) {
+  const int64_t g = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);   // 16 rows per block of 256
+  if (g >= n_rows) return;
+  const int sub = threadIdx.x & 15;
+  const int64_t s = g / n_tokens;
+  const int r = (int)(g - s * n_tokens);
+  const int tok = perm[s * n_tokens + r];
+  constexpr int kU4 = kHeadDim * sizeof(T) / 16;
+  const uint4* a = reinterpret_cast<const uint4*>(src + ((size_t)s * n_tokens + tok) * kHeadDim);
+  uint4* b = reinterpret_cast<uint4*>(pool + ((size_t)s * pool_rows + r) * kHeadDim);
+#pragma unroll
+  for (int q = sub; q < kU4; q += 16) b[q] = a[q];
+}
+
+// ------------------------------------------------------------------ host side
+
+struct Ws {
+  uint4* frag;
+  float* cnorm;
+  int32_t* counts;
+  int32_t* offsets;
+  int32_t* cursor;
+  int32_t* members;
+  size_t bytes;
+};
+
+Ws carve(void* base, int64_t n_slices, int n_tokens, int n_clusters, int dtype) {
+  Carver cv(base);
+  const int n_ctiles = ceil_div(n_clusters, kTileC);
+  const int tile_u4 = dtype == LOUISKV_BF16 ? kBf16TileU4 : kF32TileU4;
+  Ws w;
+  w.frag = cv.take<uint4>((size_t)n_slices * n_ctiles * tile_u4);
+  w.cnorm = cv.take<float>((size_t)n_slices * n_ctiles * kTileC);
+  w.counts = cv.take<int32_t>((size_t)n_slices * n_clusters);
+  w.offsets = cv.take<int32_t>((size_t)n_slices * (n_clusters + 1));
+  w.cursor = cv.take<int32_t>((size_t)n_slices * n_clusters);
+  w.members = cv.take<int32_t>((size_t)n_slices * n_tokens);
+  w.bytes = align_up(cv.used, 256);
+  return w;
+}
+
+constexpr size_t kMaxHistLds = 64 * 1024;
+
+int launch_prep(const float* reps, int stride, int64_t S, int C, int dtype, const Ws& w, bool zero_counts,
+                hipStream_t st) {
+  const int n_ctiles = ceil_div(C, kTileC);
+  const int64_t rows = S * n_ctiles * kTileC;
+  const int grid = (int)((rows + 3) / 4);
+  if (dtype == LOUISKV_BF16)
+    prep_operand_kernel<true><<<grid, 256, 0, st>>>(reps, stride, C, n_ctiles, w.frag, w.cnorm,
+                                                     zero_counts ? w.counts : nullptr, rows);
+  else
+    prep_operand_kernel<false><<<grid, 256, 0, st>>>(reps, stride, C, n_ctiles, w.frag, w.cnorm,
+                                                      zero_counts ? w.counts : nullptr, rows);
+  LKV_CHECK_LAUNCH();
+  return LOUISKV_OK;
+}
+
+int launch_assign(const void* keys, int dtype, int64_t S, int N, int C, const Ws& w, int32_t* assign,
+                  bool with_counts, hipStream_t st) {
+  const int n_ctiles = ceil_div(C, kTileC);
+  if (dtype == LOUISKV_BF16) {
+    const int bps = ceil_div(N, kBf16KeysPerBlock);
+    size_t lds = (size_t)kBf16StageTiles * (kBf16TileU4 * 16 + kTileC * 4);
+    const bool hist_lds = (size_t)C * 4 <= std::max(lds, kMaxHistLds);
+    if (with_counts && hist_lds) lds = std::max(lds, (size_t)C * 4);
+    assign_bf16_kernel<<<(unsigned)(S * bps), kAssignThreads, lds, st>>>(
+        static_cast<const uint16_t*>(keys), w.frag, w.cnorm, assign, with_counts ? w.counts : nullptr, N, C,
+        n_ctiles, bps, hist_lds ? 1 : 0);
+  } else {
+    const int bps = ceil_div(N, kF32KeysPerBlock);
+    size_t lds = (size_t)kF32StageTiles * (kF32TileU4 * 16 + kTileC * 4);
+    const bool hist_lds = (size_t)C * 4 <= std::max(lds, kMaxHistLds);
+    if (with_counts && hist_lds) lds = std::max(lds, (size_t)C * 4);
+    assign_f32_kernel<<<(unsigned)(S * bps), kAssignThreads, lds, st>>>(
+        static_cast<const float*>(keys), w.frag, w.cnorm, assign, with_counts ? w.counts : nullptr, N, C,
+        n_ctiles, bps, hist_lds ? 1 : 0);
+  }
+  LKV_CHECK_LAUNCH();
+  return LOUISKV_OK;
+}
+
+int launch_scan_scatter(const int32_t* assign, int64_t S, int N, int C, const Ws& w, hipStream_t st) {
+  scan_kernel<<<(unsigned)S, 1024, 0, st>>>(w.counts, w.offsets, w.cursor, C);
+  LKV_CHECK_LAUNCH();
+  const int bps = ceil_div(N, kScatterKeys);
+  const bool lds_ok = (size_t)C * 8 <= kMaxHistLds;
+  scatter_kernel<<<(unsigned)(S * bps), 256, lds_ok ? (size_t)C * 8 : 0, st>>>(assign, w.cursor, w.members, N, C,
+                                                                              bps, lds_ok ? 1 : 0);
+  LKV_CHECK_LAUNCH();
+  return LOUISKV_OK;
+}
+
+int launch_sum(const void* keys, int dtype, int64_t S, int N, int C, const Ws& w, const float* cin, float* cout,
+               int stride, hipStream_t st) {
+  const int64_t rows = S * C;
+  const int grid = (int)((rows + 3) / 4);
+  if (dtype == LOUISKV_BF16)
+    centroid_sum_kernel<uint16_t><<<grid, 256, 0, st>>>(static_cast<const uint16_t*>(keys), w.members, w.offsets,
+                                                         w.counts, cin, cout, stride, N, C, rows);
+  else
+    centroid_sum_kernel<float><<<grid, 256, 0, st>>>(static_cast<const float*>(keys), w.members, w.offsets,
+                                                      w.counts, cin, cout, stride, N, C, rows);
+  LKV_CHECK_LAUNCH();
+  return LOUISKV_OK;
+}
+
+int check_common(const void* keys, int dtype, int64_t S, int N, int d, int C) {
+  if (!keys) return fail(LOUISKV_ERR_NULL, "keys is NULL");
+  if (dtype != LOUISKV_F32 && dtype != LOUISKV_BF16) return fail(LOUISKV_ERR_DTYPE, "unknown dtype %d", dtype);
+  if (d != kHeadDim) return fail(LOUISKV_ERR_UNSUPPORTED, "head dim %d not supported (only 128)", d);
+  if (S < 1 || N < 1) return fail(LOUISKV_ERR_SHAPE, "n_slices=%lld n_tokens=%d must be >= 1", (long long)S, N);
+  if (C < 1 || C > N) return fail(LOUISKV_ERR_SHAPE, "n_clusters=%d must be in [1, n_tokens=%d]", C, N);
+  if ((int64_t)S * ceil_div(N, kBf16KeysPerBlock) > (int64_t)INT32_MAX / 2 ||
+      (int64_t)S * ceil_div(N, kF32KeysPerBlock) > (int64_t)INT32_MAX / 2)
+    return fail(LOUISKV_ERR_SHAPE, "problem too large for one launch");
+  return LOUISKV_OK;
+}
+
+}  // namespace
+}  // namespace louiskv
+
+using namespace louiskv;
+
+extern "C" size_t louiskv_cluster_prefill_workspace_size(int64_t n_slices, int32_t n_tokens, int32_t d,
+                                                         int32_t n_clusters, int32_t dtype) {
+  (void)d;
+  if (n_slices < 1 || n_tokens < 1 || n_clusters < 1) return 0;
+  return carve(nullptr, n_slices, n_tokens, n_clusters, dtype == LOUISKV_BF16 ? LOUISKV_BF16 : LOUISKV_F32).bytes;
+}
+
+extern "C" int louiskv_cluster_prefill(const void* keys, int32_t dtype, int64_t n_slices, int32_t n_tokens,
+                                       int32_t d, int32_t n_clusters, int32_t n_iters, const int32_t* init_idx,
+                                       float* reps, int32_t units_cap, int32_t* unit_start, int32_t* unit_size,
+                                       int32_t* assign, int32_t* perm, const void* values, void* k_pool,
+                                       void* v_pool, int64_t pool_rows, int32_t pool_on_host,
+                                       void* const* iter_events, void* workspace, size_t workspace_bytes,
+                                       void* stream) {
+  int st = check_common(keys, dtype, n_slices, n_tokens, d, n_clusters);
+  if (st) return st;
+  if (!init_idx || !reps || !unit_start || !unit_size || !assign || !perm)
+    return fail(LOUISKV_ERR_NULL, "init_idx, reps, unit_start, unit_size, assign and perm are required");
+  if (n_iters < 1) return fail(LOUISKV_ERR_SHAPE, "n_iters=%d must be >= 1", n_iters);
+  if (units_cap < n_clusters) return fail(LOUISKV_ERR_SHAPE, "units_cap=%d < n_clusters=%d", units_cap, n_clusters);
+  if (v_pool && !values) return fail(LOUISKV_ERR_NULL, "v_pool given without values");
+  if ((k_pool || v_pool) && pool_rows < n_tokens)
+    return fail(LOUISKV_ERR_SHAPE, "pool_rows=%lld < n_tokens=%d", (long long)pool_rows, n_tokens);
+  (void)pool_on_host;
+  const Ws need = carve(nullptr, n_slices, n_tokens, n_clusters, dtype);
+  if (!workspace || workspace_bytes < need.bytes)
+    return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need.bytes, workspace_bytes);
+  const Ws w = carve(workspace, n_slices, n_tokens, n_clusters, dtype);
+  hipStream_t s = as_stream(stream);
+
+  {
+    const int64_t rows = n_slices * n_clusters;
+    const int grid = (int)((rows + 3) / 4);
+    if (dtype == LOUISKV_BF16)
+      init_centroids_kernel<uint16_t><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(keys), init_idx, reps,
+                                                            n_tokens, n_clusters, units_cap, rows);
+    else
+      init_centroids_kernel<float><<<grid, 256, 0, s>>>(static_cast<const float*>(keys), init_idx, reps, n_tokens,
+                                                         n_clusters, units_cap, rows);
+    LKV_CHECK_LAUNCH();
+  }
+  for (int it = 0; it < n_iters; ++it) {
+    if ((st = launch_prep(reps, units_cap, n_slices, n_clusters, dtype, w, true, s))) return st;
+    if (iter_events) LKV_CHECK_HIP(hipEventRecord(reinterpret_cast<hipEvent_t>(iter_events[2 * it]), s));
+    if ((st = launch_assign(keys, dtype, n_slices, n_tokens, n_clusters, w, assign, true, s))) return st;
+    if (iter_events) LKV_CHECK_HIP(hipEventRecord(reinterpret_cast<hipEvent_t>(iter_events[2 * it + 1]), s));
+    if ((st = launch_scan_scatter(assign, n_slices, n_tokens, n_clusters, w, s))) return st;
+    if ((st = launch_sum(keys, dtype, n_slices, n_tokens, n_clusters, w, reps, reps, units_cap, s))) return st;
+  }
+  {
+    const int64_t rows = n_slices * n_clusters;
+    finalize_kernel<<<(int)((rows + 3) / 4), 256, 0, s>>>(w.members, w.offsets, w.counts, perm, unit_start,
+                                                          unit_size, units_cap, n_tokens, n_clusters, rows);
+    LKV_CHECK_LAUNCH();
+  }
+  const int64_t prow = n_slices * n_tokens;
+  const int pgrid = (int)((prow + 15) / 16);
+  for (int which = 0; which < 2; ++which) {
+    void* pool = which == 0 ? k_pool : v_pool;
+    const void* src = which == 0 ? keys : values;
+    if (!pool) continue;
+    if (dtype == LOUISKV_BF16)
+      pack_pool_kernel<uint16_t><<<pgrid, 256, 0, s>>>(static_cast<const uint16_t*>(src), perm,
+                                                        static_cast<uint16_t*>(pool), pool_rows, n_tokens, prow);
+    else
+      pack_pool_kernel<float><<<pgrid, 256, 0, s>>>(static_cast<const float*>(src), perm, static_cast<float*>(pool),
+                                                     pool_rows, n_tokens, prow);
+    LKV_CHECK_LAUNCH();
+  }
+  return LOUISKV_OK;
+}
+
+extern "C" int louiskv_kmeans_assign(const void* keys, int32_t dtype, int64_t n_slices, int32_t n_tokens, int32_t d,
+                                     int32_t n_clusters, const float* centroids, int32_t centroid_stride,
+                                     int32_t* assign, void* workspace, size_t workspace_bytes, void* stream) {
+  int st = check_common(keys, dtype, n_slices, n_tokens, d, n_clusters);
+  if (st) return st;
+  if (!centroids || !assign) return fail(LOUISKV_ERR_NULL, "centroids and assign are required");
+  if (centroid_stride < n_clusters) return fail(LOUISKV_ERR_SHAPE, "centroid_stride < n_clusters");
+  const Ws need = carve(nullptr, n_slices, n_tokens, n_clusters, dtype);
+  if (!workspace || workspace_bytes < need.bytes)
+    return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need.bytes, workspace_bytes);
+  const Ws w = carve(workspace, n_slices, n_tokens, n_clusters, dtype);
+  hipStream_t s = as_stream(stream);
+  if ((st = launch_prep(centroids, centroid_stride, n_slices, n_clusters, dtype, w, false, s))) return st;
+  return launch_assign(keys, dtype, n_slices, n_tokens, n_clusters, w, assign, false, s);
+}
+
+extern "C" int louiskv_kmeans_update(const void* keys, int32_t dtype, int64_t n_slices, int32_t n_tokens, int32_t d,
+                                     int32_t n_clusters, const int32_t* assign, const float* centroids_in,
+                                     float* centroids_out, int32_t centroid_stride, int32_t* counts,
+                                     void* workspace, size_t workspace_bytes, void* stream) {
+  int st = check_common(keys, dtype, n_slices, n_tokens, d, n_clusters);
+  if (st) return st;
+  if (!assign || !centroids_in || !centroids_out) return fail(LOUISKV_ERR_NULL, "assign and centroids are required");
+  if (centroid_stride < n_clusters) return fail(LOUISKV_ERR_SHAPE, "centroid_stride < n_clusters");
+  const Ws need = carve(nullptr, n_slices, n_tokens, n_clusters, dtype);
+  if (!workspace || workspace_bytes < need.bytes)
+    return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need.bytes, workspace_bytes);
+  const Ws w = carve(workspace, n_slices, n_tokens, n_clusters, dtype);
+  hipStream_t s = as_stream(stream);
+  LKV_CHECK_HIP(hipMemsetAsync(w.counts, 0, sizeof(int32_t) * n_slices * n_clusters, s));
+  const int bps = ceil_div(n_tokens, kCountKeys);
+  const bool lds_ok = (size_t)n_clusters * 4 <= kMaxHistLds;
+  count_kernel<<<(unsigned)(n_slices * bps), 256, lds_ok ? (size_t)n_clusters * 4 : 0, s>>>(
+      assign, w.counts, n_tokens, n_clusters, bps, lds_ok ? 1 : 0);
+  LKV_CHECK_LAUNCH();
+  if ((st = launch_scan_scatter(assign, n_slices, n_tokens, n_clusters, w, s))) return st;
+  if ((st = launch_sum(keys, dtype, n_slices, n_tokens, n_clusters, w, centroids_in, centroids_out,
+                       centroid_stride, s)))
+    return st;
+  if (counts)
+    LKV_CHECK_HIP(hipMemcpyAsync(counts, w.counts, sizeof(int32_t) * n_slices * n_clusters,
+                                 hipMemcpyDeviceToDevice, s));
+  return LOUISKV_OK;
+}

@@ -1,0 +1,143 @@
+"""Buffers and call order of the LouisKV path for a batch of slices.
+
+LouisKVEngine owns the device (or pinned-host) tensors of one batch of
+(sequence, layer) groups and drives the library calls in the order of the
+paper's Algorithm 1:
+
+  prefill()  louiskv_cluster_prefill: k-means per slice, centroids as unit
+             index vectors, prompt K/V packed cluster by cluster into the pool.
+  step()     one decode step for every group: louiskv_boundary_check, then
+             louiskv_retrieve for the groups that fired (scores see the units
+             evicted before this step), louiskv_segment_output (window append,
+             oldest-segment eviction), louiskv_sparse_decode_attn over
+             [KV_critical : KV_local].
+
+Python only allocates tensors and passes pointers; every step of the path
+runs in the library's kernels.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+from . import louiskv as L
+
+
+@dataclass(frozen=True)
+class EngineConfig:
+    n_slices: int
+    n_kv_heads: int
+    n_q_heads: int
+    prompt_len: int
+    n_clusters: int
+    n_iters: int
+    gen_len: int
+    seg_len: int
+    budget: int
+    window: int
+    tau: float
+    mode: int = L.REF_ANCHOR
+    head_dim: int = 128
+
+    @property
+    def n_groups(self) -> int:
+        return self.n_slices // self.n_kv_heads
+
+    @property
+    def units_cap(self) -> int:
+        ev = 0 if self.gen_len <= self.window else (self.gen_len - self.window + self.seg_len - 1) // self.seg_len
+        return self.n_clusters + ev
+
+    @property
+    def pool_rows(self) -> int:
+        return self.prompt_len + self.gen_len
+
+
+def config_from_workload(wl, n_groups: Optional[int] = None, mode: int = L.REF_ANCHOR, **kw) -> EngineConfig:
+    g = wl.n_groups if n_groups is None else n_groups
+    base = dict(n_slices=g * wl.n_kv_heads, n_kv_heads=wl.n_kv_heads, n_q_heads=wl.n_q_heads,
+                prompt_len=wl.prompt_len, n_clusters=wl.n_clusters, n_iters=wl.n_iters, gen_len=wl.gen_len,
+                seg_len=wl.seg_len, budget=wl.budget, window=wl.window, tau=wl.tau, mode=mode,
+                head_dim=wl.head_dim)
+    base.update(kw)
+    return EngineConfig(**base)
+
+
+class LouisKVEngine:
+    def __init__(self, cfg: EngineConfig, dtype: torch.dtype, device="cuda", pool_on_host: bool = False,
+                 keep_scores: bool = False, out_dtype: Optional[torch.dtype] = None):
+        self.cfg = cfg
+        self.dtype = dtype
+        self.device = torch.device(device)
+        self.pool_on_host = pool_on_host
+        S, d, cap, G = cfg.n_slices, cfg.head_dim, cfg.units_cap, cfg.n_groups
+        dev = self.device
+        i32 = dict(dtype=torch.int32, device=dev)
+        self.reps = torch.zeros(S, cap, d, dtype=torch.float32, device=dev)
+        self.unit_start = torch.zeros(S, cap, **i32)
+        self.unit_size = torch.zeros(S, cap, **i32)
+        self.assign = torch.zeros(S, cfg.prompt_len, **i32)
+        self.perm = torch.zeros(S, cfg.prompt_len, **i32)
+        if pool_on_host:
+            self.k_pool = torch.empty(S, cfg.pool_rows, d, dtype=dtype, pin_memory=True)
+            self.v_pool = torch.empty(S, cfg.pool_rows, d, dtype=dtype, pin_memory=True)
+        else:
+            self.k_pool = torch.empty(S, cfg.pool_rows, d, dtype=dtype, device=dev)
+            self.v_pool = torch.empty(S, cfg.pool_rows, d, dtype=dtype, device=dev)
+        self.k_local = torch.zeros(S, cfg.window, d, dtype=dtype, device=dev)
+        self.v_local = torch.zeros(S, cfg.window, d, dtype=dtype, device=dev)
+        self.k_buf = torch.zeros(S, max(cfg.budget, 1), d, dtype=dtype, device=dev)
+        self.v_buf = torch.zeros(S, max(cfg.budget, 1), d, dtype=dtype, device=dev)
+        self.sel_units = torch.zeros(S, cap, **i32)
+        self.n_sel_units = torch.zeros(S, **i32)
+        self.n_sel = torch.zeros(S, **i32)
+        self.q_ref = torch.zeros(G, cfg.n_q_heads, d, dtype=dtype, device=dev)
+        self.fire = torch.zeros(G, dtype=torch.uint8, device=dev)
+        self.r = torch.zeros(G, dtype=torch.float64, device=dev)
+        self.out = torch.zeros(G, cfg.n_q_heads, d, dtype=out_dtype or dtype, device=dev)
+        self.lse = torch.zeros(G, cfg.n_q_heads, dtype=torch.float32, device=dev)
+        self.scores = torch.zeros(S, cap, dtype=torch.float64, device=dev) if keep_scores else None
+        dc = L.BF16 if dtype == torch.bfloat16 else L.F32
+        u8 = dict(dtype=torch.uint8, device=dev)
+        self.ws_prefill = torch.empty(L.cluster_prefill_workspace_size(S, cfg.prompt_len, cfg.n_clusters, dc), **u8)
+        self.ws_retrieve = torch.empty(L.retrieve_workspace_size(S, cap, cfg.budget), **u8)
+        self.ws_attn = torch.empty(
+            L.sparse_decode_attn_workspace_size(S, cfg.n_q_heads // cfg.n_kv_heads, self.k_buf.shape[1],
+                                                cfg.window), **u8)
+        self.t = 0
+
+    # ---------------------------------------------------------------- prefill
+    def prefill(self, prompt_keys: torch.Tensor, prompt_values: torch.Tensor, init_idx: torch.Tensor,
+                iter_events=None) -> None:
+        c = self.cfg
+        L.cluster_prefill(prompt_keys, c.n_clusters, c.n_iters, init_idx, self.reps, self.unit_start,
+                          self.unit_size, self.assign, self.perm, values=prompt_values, k_pool=self.k_pool,
+                          v_pool=self.v_pool, pool_on_host=self.pool_on_host, iter_events=iter_events,
+                          workspace=self.ws_prefill)
+        self.t = 0
+
+    # ---------------------------------------------------------------- decode
+    def n_units_before(self, t: int) -> int:
+        """Units scorable at decode step t (0-based): clusters plus segments evicted before it."""
+        if t == 0:
+            return self.cfg.n_clusters
+        return self.cfg.n_clusters + L.window_info(t - 1, self.cfg.window, self.cfg.seg_len)[1]
+
+    def step(self, q_t: torch.Tensor, k_t: torch.Tensor, v_t: torch.Tensor) -> None:
+        """One decode step: q_t [G][Hq][d], k_t and v_t [S][d]."""
+        c = self.cfg
+        t = self.t
+        L.boundary_check(q_t, self.q_ref, c.tau, c.mode, t == 0, self.fire, self.r)
+        L.retrieve(q_t, c.n_kv_heads, self.reps, self.unit_start, self.unit_size, self.n_units_before(t),
+                   self.k_pool, self.v_pool, c.budget, self.sel_units, self.n_sel_units, self.n_sel,
+                   self.k_buf, self.v_buf, fire=self.fire, pool_on_host=self.pool_on_host,
+                   scores_out=self.scores, workspace=self.ws_retrieve)
+        L.segment_output(k_t, v_t, self.k_local, self.v_local, t, c.seg_len, self.reps, self.unit_start,
+                         self.unit_size, c.n_clusters, self.k_pool, self.v_pool, c.prompt_len,
+                         pool_on_host=self.pool_on_host)
+        _, _, n_local, local_start = L.window_info(t, c.window, c.seg_len)
+        L.sparse_decode_attn(q_t, c.n_kv_heads, self.k_buf, self.v_buf, self.n_sel, self.k_local, self.v_local,
+                             local_start, n_local, self.out, self.lse, workspace=self.ws_attn)
+        self.t += 1

@@ -1,0 +1,116 @@
+"""The C-ABI library without a GPU: it loads, exports every function the public
+header declares, and its host-only logic (status strings, argument validation
+that returns before any launch, the local-window rule) behaves as documented."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "louiskv.h")
+LIB = os.path.join(ROOT, "paper_2510_11292_amd", "liblouiskv.so")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(louiskv_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        pytest.fail("liblouiskv.so is not built; run `python -m paper_2510_11292_amd.build`")
+    from paper_2510_11292_amd import louiskv
+    return louiskv.load_library()
+
+
+def test_exports_every_declared_function(lib):
+    names = declared_functions()
+    assert len(names) >= 13
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB], capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (louiskv_\w+)", out))
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+    from paper_2510_11292_amd import louiskv
+    assert sorted(louiskv.EXPORTED) == names
+
+
+def test_version_and_status_strings(lib):
+    assert lib.louiskv_abi_version() == 1
+    for st in range(7):
+        assert lib.louiskv_status_str(st)
+    assert lib.louiskv_status_str(99) == b"unknown status"
+
+
+def test_window_rule_matches_oracle_schedule(lib):
+    """The library's window rule gives the eviction steps, live counts and ring
+    positions that the oracle's decode loop produces."""
+    import oracle
+    from paper_2510_11292_amd import louiskv as L
+    window, seg = 32, 8
+    rng = np.random.default_rng(0)
+    p, d, c = 40, 4, 4
+    pk = rng.standard_normal((1, p, d))
+    res = [oracle.kmeans(pk[0], np.arange(c), 1, False)]
+    dec = oracle.GroupDecoder(oracle.prefill_state_from_kmeans(pk, pk, res), n_q_heads=1, budget=8,
+                              window=window, seg_len=seg, tau=0.0)
+    for t in range(150):
+        rec = dec.step(rng.standard_normal((1, d)), rng.standard_normal((1, d)), rng.standard_normal((1, d)))
+        ev, n_ev, n_local, start = L.window_info(t, window, seg)
+        assert (ev >= 0) == (rec.evicted_unit is not None)
+        if ev >= 0:
+            assert rec.evicted_unit == c + ev
+        assert n_ev == dec.n_evicted
+        assert n_local == len(dec.local[0])
+        assert start == dec.local[0][0][0] % window
+    with pytest.raises(L.LouisKVError):
+        L.window_info(0, 30, 8)
+
+
+def test_validation_errors_return_before_launch(lib):
+    """Bad arguments are rejected on the host with the documented status."""
+    P = ctypes.c_void_p
+    dummy = P(16)
+    # NULL keys
+    assert lib.louiskv_cluster_prefill(None, 1, 1, 64, 128, 8, 1, dummy, dummy, 8, dummy, dummy, dummy, dummy,
+                                       None, None, None, 0, 0, None, dummy, 1 << 30, None) == 1
+    # bad dtype
+    assert lib.louiskv_cluster_prefill(dummy, 7, 1, 64, 128, 8, 1, dummy, dummy, 8, dummy, dummy, dummy, dummy,
+                                       None, None, None, 0, 0, None, dummy, 1 << 30, None) == 3
+    # head dim other than 128
+    assert lib.louiskv_cluster_prefill(dummy, 1, 1, 64, 64, 8, 1, dummy, dummy, 8, dummy, dummy, dummy, dummy,
+                                       None, None, None, 0, 0, None, dummy, 1 << 30, None) == 4
+    # more clusters than tokens
+    assert lib.louiskv_cluster_prefill(dummy, 1, 1, 64, 128, 65, 1, dummy, dummy, 80, dummy, dummy, dummy, dummy,
+                                       None, None, None, 0, 0, None, dummy, 1 << 30, None) == 2
+    # workspace too small
+    assert lib.louiskv_cluster_prefill(dummy, 1, 1, 64, 128, 8, 1, dummy, dummy, 8, dummy, dummy, dummy, dummy,
+                                       None, None, None, 0, 0, None, dummy, 16, None) == 5
+    assert b"workspace" in lib.louiskv_last_error()
+    # boundary: unknown mode, NULL output
+    assert lib.louiskv_boundary_check(dummy, dummy, 1, 4, 32, 128, 0.9, 5, 0, None, dummy, None) == 2
+    assert lib.louiskv_boundary_check(dummy, dummy, 1, 4, 32, 128, 0.9, 0, 0, None, None, None) == 1
+    # retrieve: too many units, group size over the limit
+    args = [dummy, 1, 8, 8, 4, 128, 0.088, dummy, dummy, dummy, 100, 200, dummy, dummy, 1000, 0, 64, None,
+            dummy, dummy, dummy, dummy, dummy, None, dummy, 1 << 30, None]
+    assert lib.louiskv_retrieve(*args) == 2
+    args[10] = 50
+    args[4] = 16
+    assert lib.louiskv_retrieve(*args) == 4
+    # attention: local window overflow
+    assert lib.louiskv_sparse_decode_attn(dummy, 1, 8, 8, 4, 128, 0.088, dummy, dummy, dummy, 64, dummy, dummy,
+                                          32, 0, 33, dummy, 1, None, dummy, 1 << 30, None) == 2
+    # segment output: window not a multiple of the segment
+    assert lib.louiskv_segment_output(dummy, dummy, 1, 8, 128, dummy, dummy, 30, 0, 8, dummy, dummy, dummy, 100, 10,
+                                      None, None, 0, 0, 0, None) == 2
+
+
+def test_workspace_sizes_are_positive(lib):
+    assert lib.louiskv_cluster_prefill_workspace_size(256, 32768, 128, 1024, 1) > 256 * 32768 * 4
+    assert lib.louiskv_retrieve_workspace_size(256, 1024, 2048) > 0
+    assert lib.louiskv_sparse_decode_attn_workspace_size(256, 4, 128, 2048, 128) > 0
+    assert lib.louiskv_cluster_prefill_workspace_size(0, 1, 128, 1, 1) == 0

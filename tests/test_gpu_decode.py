@@ -1,0 +1,300 @@
+"""Decode-stage calls on the GPU (through the C ABI) against the CPU oracle."""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+sys.path.insert(0, os.path.dirname(__file__))
+import oracle  # noqa: E402
+import synth  # noqa: E402
+from parity_utils import REL, check_rows_rel, selection_matches, to64, to_np  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _L():
+    from paper_2510_11292_amd import louiskv
+    return louiskv
+
+
+def _gen(seed):
+    g = torch.Generator(device=DEV)
+    g.manual_seed(seed)
+    return g
+
+
+# ------------------------------------------------------------------ boundary
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("mode", [0, 1])
+def test_boundary_check(dtype, mode):
+    L = _L()
+    G, H = 64, 32
+    g = _gen(1)
+    base = torch.randn(G, H, 128, generator=g, device=DEV)
+    q_ref0 = base.to(dtype)
+    # a spread of similarities around tau: mix in noise of growing size
+    noise = torch.randn(G, H, 128, generator=g, device=DEV) * torch.linspace(0, 1.5, G, device=DEV)[:, None, None]
+    q = (base + noise).to(dtype)
+    q[3] = q_ref0[3]                 # identical: r = 1
+    q[4] = -q_ref0[4]                # opposite: r = -1
+    q[5] = 0                         # zero query: r = 0
+    for tau in (0.9, 0.5, 1.5, -1.5):
+        q_ref = q_ref0.clone()
+        fire = torch.empty(G, dtype=torch.uint8, device=DEV)
+        r = torch.empty(G, dtype=torch.float64, device=DEV)
+        L.boundary_check(q, q_ref, tau, mode, False, fire, r)
+        torch.cuda.synchronize()
+        q64, ref64 = to64(q), to64(q_ref0)
+        for i in range(G):
+            rr = oracle.query_similarity(q64[i], ref64[i])
+            assert abs(float(r[i]) - rr) <= 1e-12, (i, float(r[i]), rr)
+            want = oracle.boundary_fires(rr, tau, False)
+            if bool(fire[i]) != want:
+                assert abs(rr - tau) <= REL * max(abs(rr), abs(tau))
+            expect_ref = q[i] if (mode == 0 or bool(fire[i])) else q_ref0[i]
+            assert torch.equal(q_ref[i], expect_ref)
+    # first step: everything fires, r is NaN, the reference is taken
+    q_ref = torch.zeros_like(q)
+    fire = torch.zeros(G, dtype=torch.uint8, device=DEV)
+    r = torch.zeros(G, dtype=torch.float64, device=DEV)
+    L.boundary_check(q, q_ref, 0.9, mode, True, fire, r)
+    torch.cuda.synchronize()
+    assert torch.all(fire == 1) and torch.all(torch.isnan(r)) and torch.equal(q_ref, q)
+
+
+# ------------------------------------------------------------------ decode store
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_segment_output_window_and_eviction(dtype):
+    """Drive 300 steps of the store and compare the ring, the new units and the
+    pool with the oracle's bookkeeping."""
+    L = _L()
+    S, W, seg, C, P, T = 6, 64, 16, 10, 40, 300
+    g = _gen(2)
+    keys = torch.randn(T, S, 128, generator=g, device=DEV).mul(3).to(dtype)
+    vals = torch.randn(T, S, 128, generator=g, device=DEV).to(dtype)
+    n_ev_total = (T - W + seg - 1) // seg
+    cap = C + n_ev_total
+    reps = torch.zeros(S, cap, 128, device=DEV)
+    ustart = torch.zeros(S, cap, dtype=torch.int32, device=DEV)
+    usize = torch.zeros_like(ustart)
+    kl = torch.zeros(S, W, 128, dtype=dtype, device=DEV)
+    vl = torch.zeros_like(kl)
+    kp = torch.zeros(S, P + T, 128, dtype=dtype, device=DEV)
+    vp = torch.zeros_like(kp)
+    for t in range(T):
+        L.segment_output(keys[t], vals[t], kl, vl, t, seg, reps, ustart, usize, C, kp, vp, P)
+    torch.cuda.synchronize()
+    ev, n_ev, n_local, start = L.window_info(T - 1, W, seg)
+    assert n_ev == n_ev_total
+    k64 = to64(keys)
+    for e in range(n_ev):
+        u = C + e
+        assert torch.all(ustart[:, u] == P + e * seg) and torch.all(usize[:, u] == seg)
+        for s in range(S):
+            ref = oracle.segment_mean(k64[e * seg:(e + 1) * seg, s])
+            assert np.array_equal(to64(reps[s, u]), ref)
+        assert torch.equal(kp[:, P + e * seg:P + (e + 1) * seg], keys[e * seg:(e + 1) * seg].transpose(0, 1))
+        assert torch.equal(vp[:, P + e * seg:P + (e + 1) * seg], vals[e * seg:(e + 1) * seg].transpose(0, 1))
+    live = list(range(n_ev * seg, T))
+    assert len(live) == n_local
+    for i, tok in enumerate(live):
+        slot = (start + i) % W
+        assert slot == tok % W
+        assert torch.equal(kl[:, slot], keys[tok]) and torch.equal(vl[:, slot], vals[tok])
+
+
+# ------------------------------------------------------------------ retrieve
+
+RETRIEVE_CASES = [
+    # (dtype, n_groups, n_kv, g, n_units, budget, max unit size)
+    (torch.bfloat16, 4, 8, 4, 1024, 2048, 64),
+    (torch.float32, 2, 8, 4, 68, 512, 120),
+    (torch.bfloat16, 3, 2, 8, 3000, 4096, 20),
+    (torch.bfloat16, 2, 4, 1, 17, 100, 30),
+    (torch.float32, 1, 8, 4, 50, 0, 10),          # zero budget: nothing selected
+    (torch.bfloat16, 1, 8, 4, 64, 10 ** 6, 40),   # budget covers everything
+]
+
+
+@pytest.mark.parametrize("dtype,G,H,g,U,B,maxsz", RETRIEVE_CASES)
+def test_retrieve(dtype, G, H, g, U, B, maxsz):
+    L = _L()
+    S = G * H
+    gen = _gen(U + B)
+    q = torch.randn(G, H * g, 128, generator=gen, device=DEV).mul(2).to(dtype)
+    reps = torch.randn(S, U + 3, 128, generator=gen, device=DEV)
+    sizes = torch.randint(0, maxsz + 1, (S, U + 3), generator=gen, device=DEV, dtype=torch.int32)
+    sizes[:, 0] = maxsz                                   # a big unit at a fixed place
+    starts = torch.zeros_like(sizes)
+    starts[:, 1:] = torch.cumsum(sizes, 1)[:, :-1].to(torch.int32)
+    rows = int(sizes.sum(1).max()) + 5
+    kp = torch.randn(S, rows, 128, generator=gen, device=DEV).to(dtype)
+    vp = torch.randn(S, rows, 128, generator=gen, device=DEV).to(dtype)
+    fire = (torch.arange(G, device=DEV) % 3 != 1).to(torch.uint8)
+    bufrows = max(min(B, rows), 1)
+    kb = torch.full((S, bufrows, 128), 9, dtype=dtype, device=DEV)
+    vb = torch.full_like(kb, 9)
+    sel = torch.full((S, U + 3), -1, dtype=torch.int32, device=DEV)
+    nsu = torch.full((S,), -1, dtype=torch.int32, device=DEV)
+    nsel = torch.full((S,), -1, dtype=torch.int32, device=DEV)
+    scores = torch.zeros(S, U + 3, dtype=torch.float64, device=DEV)
+    Bcall = min(B, bufrows) if B > 0 else 0
+    L.retrieve(q, H, reps, starts, sizes, U, kp, vp, Bcall, sel, nsu, nsel, kb, vb, fire=fire, scores_out=scores)
+    torch.cuda.synchronize()
+    q64, r64, sz, st = to64(q), to64(reps), to_np(sizes), to_np(starts)
+    for s in range(S):
+        grp, h = divmod(s, H)
+        if not fire[grp]:
+            assert int(nsel[s]) == -1 and int(nsu[s]) == -1 and torch.all(kb[s] == 9)
+            continue
+        a = oracle.group_scores(q64[grp, h * g:(h + 1) * g], r64[s, :U], 1 / np.sqrt(128))
+        np.testing.assert_allclose(to_np(scores[s, :U]), a, rtol=1e-12, atol=1e-300)
+        got = to_np(sel[s, :int(nsu[s])]).tolist()
+        selection_matches(a, sz[s, :U], Bcall, got)
+        tot = int(sz[s, got].sum()) if got else 0
+        assert int(nsel[s]) == tot <= max(Bcall, 0)
+        ref_rows = oracle.gather_units(to64(kp[s]), st[s], sz[s], got)
+        assert np.array_equal(to64(kb[s, :tot]), ref_rows)
+        assert np.array_equal(to64(vb[s, :tot]), oracle.gather_units(to64(vp[s]), st[s], sz[s], got))
+
+
+# ------------------------------------------------------------------ attention
+
+ATTN_CASES = [
+    # (dtype, out dtype, n_groups, n_kv, g, buf_rows, window, n_local, local_start)
+    (torch.bfloat16, torch.float32, 4, 8, 4, 2048, 128, 128, 0),
+    (torch.float32, torch.float32, 1, 8, 4, 512, 128, 97, 32),
+    (torch.bfloat16, torch.bfloat16, 2, 8, 4, 300, 64, 10, 60),
+    (torch.bfloat16, torch.float32, 2, 4, 8, 100, 32, 0, 0),
+    (torch.float32, torch.float32, 3, 2, 1, 77, 16, 16, 5),
+    (torch.bfloat16, torch.float32, 1, 8, 2, 4096, 128, 1, 127),
+]
+
+
+@pytest.mark.parametrize("dtype,odt,G,H,g,BR,W,nl,ls", ATTN_CASES)
+def test_sparse_decode_attn(dtype, odt, G, H, g, BR, W, nl, ls):
+    L = _L()
+    S = G * H
+    gen = _gen(BR + W + nl)
+    q = torch.randn(G, H * g, 128, generator=gen, device=DEV).mul(1.5).to(dtype)
+    kb = torch.randn(S, BR, 128, generator=gen, device=DEV).mul(2).to(dtype)
+    vb = torch.randn(S, BR, 128, generator=gen, device=DEV).to(dtype)
+    kl = torch.randn(S, W, 128, generator=gen, device=DEV).mul(2).to(dtype)
+    vl = torch.randn(S, W, 128, generator=gen, device=DEV).to(dtype)
+    nsel = torch.randint(0, BR + 1, (S,), generator=gen, device=DEV, dtype=torch.int32)
+    nsel[0] = BR
+    nsel[-1] = 0
+    out = torch.empty(G, H * g, 128, dtype=odt, device=DEV)
+    lse = torch.empty(G, H * g, dtype=torch.float32, device=DEV)
+    L.sparse_decode_attn(q, H, kb, vb, nsel, kl, vl, ls, nl, out, lse)
+    torch.cuda.synchronize()
+    q64 = to64(q)
+    for s in range(S):
+        grp, h = divmod(s, H)
+        n = int(nsel[s])
+        slots = [(ls + i) % W for i in range(nl)]
+        kk = np.concatenate([to64(kb[s, :n]), to64(kl[s, slots])]) if slots else to64(kb[s, :n])
+        vv = np.concatenate([to64(vb[s, :n]), to64(vl[s, slots])]) if slots else to64(vb[s, :n])
+        o, l = oracle.attention(q64[grp, h * g:(h + 1) * g], kk, vv, 1 / np.sqrt(128))
+        got = to64(out[grp, h * g:(h + 1) * g])
+        if kk.shape[0] == 0:
+            assert np.all(got == 0) and np.all(np.isneginf(to_np(lse[grp, h * g:(h + 1) * g])))
+            continue
+        if odt == torch.bfloat16:
+            ref = oracle.round_to_bf16(o)
+            ulp = np.abs(ref) * 2.0 ** -7 + 1e-30
+            assert np.all(np.abs(got - ref) <= ulp + 1e-6)
+        elif dtype == torch.float32:
+            check_rows_rel(got, o, 1e-5, "fp32 attention")
+        else:
+            assert np.abs(got - o).max() <= 2e-3
+        np.testing.assert_allclose(to64(lse[grp, h * g:(h + 1) * g]), l, rtol=1e-5, atol=1e-5)
+
+
+# ------------------------------------------------------------------ whole decode loop
+
+def _run_loop(wl, n_groups, steps, mode):
+    """Prefill on the GPU, then `steps` decode steps on the GPU and in the
+    oracle (started from the GPU's prefill state), step-locked."""
+    from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
+    data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(n_groups)], gen_len=steps)
+    cfg = config_from_workload(wl, n_groups=n_groups, mode=mode, gen_len=steps)
+    odt = torch.float32
+    eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, keep_scores=True, out_dtype=odt)
+    eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    torch.cuda.synchronize()
+    H, g = wl.n_kv_heads, wl.group_size
+    decs = []
+    for gi in range(n_groups):
+        sl = slice(gi * H, (gi + 1) * H)
+        st = oracle.PrefillState(
+            reps=list(to64(eng.reps[sl, :wl.n_clusters])),
+            unit_start=list(to_np(eng.unit_start[sl, :wl.n_clusters]).astype(np.int64)),
+            unit_size=list(to_np(eng.unit_size[sl, :wl.n_clusters]).astype(np.int64)),
+            k_pool=list(to64(eng.k_pool[sl, :wl.prompt_len])),
+            v_pool=list(to64(eng.v_pool[sl, :wl.prompt_len])))
+        decs.append(oracle.GroupDecoder(st, wl.n_q_heads, wl.budget, wl.window, wl.seg_len, wl.tau,
+                                        "prev" if mode == 0 else "anchor"))
+    stats = dict(fires=0, excused=0)
+    for t in range(steps):
+        eng.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        torch.cuda.synchronize()
+        fire, r = to_np(eng.fire), to_np(eng.r)
+        for gi, dec in enumerate(decs):
+            q64 = to64(data.queries[t, gi])
+            want_fire = t == 0 or oracle.boundary_fires(oracle.query_similarity(q64, dec.q_ref), wl.tau, False)
+            if bool(fire[gi]) != want_fire:
+                rr = oracle.query_similarity(q64, dec.q_ref)
+                assert abs(rr - wl.tau) <= REL * max(abs(rr), wl.tau), (t, gi, rr)
+                stats["excused"] += 1
+            override = None
+            if fire[gi]:
+                stats["fires"] += 1
+                override = []
+                for h in range(H):
+                    s = gi * H + h
+                    got = to_np(eng.sel_units[s, :int(eng.n_sel_units[s])]).tolist()
+                    a = oracle.group_scores(q64[h * g:(h + 1) * g], np.asarray(dec.reps[h]), 1 / np.sqrt(128))
+                    np.testing.assert_allclose(to_np(eng.scores[s, :len(a)]), a, rtol=1e-12, atol=1e-300)
+                    stats["excused"] += selection_matches(a, dec.unit_size[h], wl.budget, got)
+                    override.append(got)
+            rec = dec.step(q64, to64(data.gen_keys[t, gi * H:(gi + 1) * H]),
+                           to64(data.gen_values[t, gi * H:(gi + 1) * H]), fire_override=bool(fire[gi]),
+                           select_override=override)
+            assert to_np(eng.n_sel[gi * H:(gi + 1) * H]).tolist() == rec.n_sel
+            got = to64(eng.out[gi])
+            if data.prompt_keys.dtype == torch.float32:
+                check_rows_rel(got, rec.out, 1e-5, f"step {t} attention")
+            else:
+                assert np.abs(got - rec.out).max() <= 2e-3, (t, np.abs(got - rec.out).max())
+            if rec.evicted_unit is not None:
+                u = rec.evicted_unit
+                for h in range(H):
+                    assert np.array_equal(to64(eng.reps[gi * H + h, u]), dec.reps[h][u])
+    return stats
+
+
+def test_decode_loop_tiny_workload_anchor():
+    """The tiny-4k workload end to end (fp32, 256 decode steps, anchor mode)."""
+    wl = synth.get_workload("tiny-4k")
+    st = _run_loop(wl, 1, wl.gen_len, mode=1)
+    assert st["fires"] > 20
+
+
+def test_decode_loop_tiny_workload_prev():
+    wl = synth.get_workload("tiny-4k")
+    st = _run_loop(wl, 1, wl.gen_len, mode=0)
+    assert st["fires"] >= 1
+
+
+def test_decode_loop_bf16_with_evictions():
+    """A bf16 reduction of the long-output shape: 2 groups, P=2048, C=64,
+    300 steps so several segments are evicted and later retrieved."""
+    wl = synth.get_workload("si-lo-16k").replace(prompt_len=2048, n_clusters=64, budget=512, name="si-lo-16k")
+    st = _run_loop(wl, 2, 300, mode=1)
+    assert st["fires"] > 40
