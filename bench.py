@@ -1,0 +1,229 @@
+#!/usr/bin/env python
+"""Throughput of the LouisKV clustering-and-retrieval path on one MI355X.
+
+One step is one full request pass of the long-input short-output workload
+(li-so-32k: 32 layers x 8 KV heads = 256 slices, 32768 prompt tokens, 1024
+clusters, 10 Lloyd iterations, bf16; then 128 decode steps with boundary test,
+retrieval at boundaries (budget 2048), window store and sparse attention for
+all layers):
+
+  prefill   louiskv_cluster_prefill (k-means + cluster-packed K/V pool)
+  decode    128 x [boundary_check, retrieve, segment_output, sparse_decode_attn]
+
+Inputs are seeded synthetic tensors already resident in HBM before timing.
+Prints one JSON line: value = prompt keys clustered per second; the decode
+rate is reported alongside; `roofline` covers the dominant kernel (the MFMA
+k-means assignment), timed with HIP events on the stream it runs on;
+`cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "prompt keys clustered/s; retrieval+sparse-attn decode steps/s at 32K ctx"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def make_inputs(wl, device):
+    import torch
+    import synth
+    t0 = time.time()
+    data = synth.make_slices(wl, device)
+    torch.cuda.synchronize()
+    log(f"generated inputs for {data.n_slices} slices in {time.time() - t0:.1f}s")
+    return data
+
+
+def cpu_baseline(wl, data, budget_s: float):
+    """The oracle on a bounded sample: k-means of one slice and the decode loop
+    of one (sequence, layer) group for a prefix of the decode steps, scaled to
+    the whole workload."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        blas_threads = 1
+
+    def f64(t):
+        return t.detach().float().cpu().numpy().astype(np.float64)
+
+    keys0 = f64(data.prompt_keys[0])
+    init0 = data.init_idx[0].cpu().numpy()
+    t0 = time.time()
+    res = oracle.kmeans(keys0, init0, wl.n_iters, bf16_operand=(wl.dtype == "bf16"))
+    t_km = time.time() - t0
+    keys_per_s = wl.prompt_len / t_km       # one slice; every slice costs the same
+
+    # decode: one group, steps until the time budget is used
+    H = wl.n_kv_heads
+    results = [res] + [oracle.kmeans(f64(data.prompt_keys[h]), data.init_idx[h].cpu().numpy(), 1,
+                                     wl.dtype == "bf16") for h in range(1, H)]
+    st = oracle.prefill_state_from_kmeans([f64(data.prompt_keys[h]) for h in range(H)],
+                                          [f64(data.prompt_values[h]) for h in range(H)], results)
+    dec = oracle.GroupDecoder(st, wl.n_q_heads, wl.budget, wl.window, wl.seg_len, wl.tau, "anchor")
+    t0 = time.time()
+    n = 0
+    while n < wl.gen_len and (time.time() - t0) < budget_s:
+        dec.step(f64(data.queries[n, 0]), f64(data.gen_keys[n, :H]), f64(data.gen_values[n, :H]))
+        n += 1
+    t_dec = (time.time() - t0) / n          # one group, one step
+    steps_per_s = 1.0 / (t_dec * wl.n_groups)
+    return {
+        "value": keys_per_s, "unit": "keys/s", "cores": int(blas_threads), "kind": "oracle",
+        "decode_steps_per_s": steps_per_s,
+        "sample": (f"k-means of 1 of {wl.n_slices} slices ({wl.prompt_len} keys, C={wl.n_clusters}, "
+                   f"{wl.n_iters} iterations) in {t_km:.1f}s, scaled linearly; decode: {n} of {wl.gen_len} steps "
+                   f"of 1 of {wl.n_groups} layer groups in {t_dec * n:.1f}s, scaled by the group count"),
+        "host_cpus": len(os.sched_getaffinity(0)), "cpu": platform.processor() or platform.machine(),
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="li-so-32k")
+    ap.add_argument("--mode", default="anchor", choices=["anchor", "prev"])
+    ap.add_argument("--cpu-budget-s", type=float, default=12.0,
+                    help="seconds of oracle decode steps in the CPU baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager", action="store_true", help="launch decode steps one by one (no HIP graph)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the LouisKV path is built and measured on a single MI355X "
+              "(slices shard across GPUs with no communication except one boundary all-reduce per "
+              "layer; see the design notes). Run with --gpus 1.", file=sys.stderr)
+        return 2
+
+    import torch
+    import synth
+    from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
+    from paper_2510_11292_amd import louiskv as L
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    dev = "cuda"
+    wl = synth.get_workload(args.workload)
+    mode = L.REF_ANCHOR if args.mode == "anchor" else L.REF_PREV
+    data = make_inputs(wl, dev)
+    cfg = config_from_workload(wl, mode=mode)
+    dtype = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    eng = LouisKVEngine(cfg, dtype, dev, pool_on_host=wl.pool_on_host)
+
+    total = args.warmup + args.steps
+    iters = wl.n_iters
+    assign_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * iters)] for _ in range(total)]
+    for evs in assign_ev:          # create the underlying events before handing them to the library
+        for e in evs:
+            e.record()
+    ph = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(total)]
+
+    def decode_all():
+        for t in range(wl.gen_len):
+            eng.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+
+    graph = None
+    if not args.eager:
+        # capture the whole decode loop once; replays follow a fresh prefill
+        eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            decode_all()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        eng.t = 0
+        with torch.cuda.graph(graph):
+            decode_all()
+        torch.cuda.synchronize()
+
+    fires = []
+    torch.cuda.synchronize()
+    wall0 = None
+    for i in range(total):
+        if i == args.warmup:
+            torch.cuda.synchronize()
+            wall0 = time.perf_counter()
+        ph[i][0].record()
+        eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx, iter_events=assign_ev[i])
+        ph[i][1].record()
+        if graph is not None:
+            graph.replay()
+        else:
+            decode_all()
+        ph[i][2].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+
+    timed = range(args.warmup, total)
+    t_pre = sum(ph[i][0].elapsed_time(ph[i][1]) for i in timed) / args.steps / 1e3
+    t_dec = sum(ph[i][1].elapsed_time(ph[i][2]) for i in timed) / args.steps / 1e3
+    t_assign = sum(assign_ev[i][2 * k].elapsed_time(assign_ev[i][2 * k + 1])
+                   for i in timed for k in range(iters)) / (args.steps * iters) / 1e3
+    flops_per_launch = 2.0 * wl.prompt_len * wl.n_clusters * wl.head_dim * wl.n_slices
+    keys = wl.n_slices * wl.prompt_len
+    ms_per_step = wall / args.steps * 1e3
+    fire_rate = float(eng.fire.float().mean())  # last step's groups (informational)
+    achieved = flops_per_launch / t_assign / 1e12
+    out = {
+        "metric": METRIC,
+        "value": keys / t_pre,
+        "unit": "keys/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name, "batch": wl.batch, "layers": wl.n_layers, "kv_heads": wl.n_kv_heads,
+            "q_heads": wl.n_q_heads, "head_dim": wl.head_dim, "prompt_tokens": wl.prompt_len,
+            "clusters": wl.n_clusters, "lloyd_iters": wl.n_iters, "decode_steps": wl.gen_len,
+            "budget": wl.budget, "window": wl.window, "segment": wl.seg_len, "tau": wl.tau,
+            "ref_mode": args.mode, "decode_launch": "eager" if graph is None else "hip_graph",
+        },
+        "decode_steps_per_s": wl.gen_len / t_dec,
+        "prefill_ms": t_pre * 1e3,
+        "decode_ms": t_dec * 1e3,
+        "roofline": {
+            "kernel": "kmeans_assign (bf16 MFMA, fused argmin)",
+            "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+            "avg_launch_ms": t_assign * 1e3, "flops_per_launch": flops_per_launch,
+        },
+    }
+    log(f"prefill {t_pre * 1e3:.2f} ms, decode {t_dec * 1e3:.2f} ms ({wl.gen_len / t_dec:.0f} steps/s), "
+        f"assign {t_assign * 1e3:.3f} ms/launch = {achieved:.1f} TFLOP/s, last-step fire rate {fire_rate:.2f}")
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(wl, data, args.cpu_budget_s)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -29,10 +29,21 @@ constexpr int kBf16Steps = 8;              // 32x32x16 MFMAs per 128-wide dot pr
 constexpr int kBf16TileU4 = kBf16Steps * 64;       // uint4 per bf16 operand tile (8 KB)
 constexpr int kF32TileU4 = 16 * 64;                // uint4 per fp32 operand tile (16 KB)
 
-constexpr int kAssignThreads = 256;
-constexpr int kBf16KeyTiles = 4;                   // 32-key tiles held per wave
-constexpr int kBf16KeysPerBlock = 4 * 32 * kBf16KeyTiles;   // 512
-constexpr int kBf16StageTiles = 4;
+#ifndef LKV_BF16_KEY_TILES
+#define LKV_BF16_KEY_TILES 4
+#endif
+#ifndef LKV_BF16_STAGE_TILES
+#define LKV_BF16_STAGE_TILES 4
+#endif
+#ifndef LKV_ASSIGN_WAVES
+#define LKV_ASSIGN_WAVES 4
+#endif
+constexpr int kAssignThreads = 256;                          // fp32 kernel block
+constexpr int kBf16Waves = LKV_ASSIGN_WAVES;                 // waves sharing one LDS stage
+constexpr int kBf16Threads = 64 * kBf16Waves;
+constexpr int kBf16KeyTiles = LKV_BF16_KEY_TILES;            // 32-key tiles held per wave
+constexpr int kBf16KeysPerBlock = kBf16Waves * 32 * kBf16KeyTiles;
+constexpr int kBf16StageTiles = LKV_BF16_STAGE_TILES;        // centroid tiles per LDS stage
 constexpr int kF32KeysPerBlock = 4 * 32;           // one 32-key tile per wave
 constexpr int kF32StageTiles = 2;
 
@@ -123,25 +134,145 @@ __device__ __forceinline__ void block_histogram(int* hist, bool lds_ok, int n_cl
   }
 }
 
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// Asynchronous copy of centroid tiles [t0, t0+nt) (operand fragments and
+// norms) from global memory straight into one LDS stage buffer.  Each wave
+// instruction moves 64 lanes x 16 bytes; completion is tracked by vmcnt.
+__device__ __forceinline__ void stage_tiles_async(const uint4* fslice, const float* cslice, int t0, int nt,
+                                                  char* buf, int wave, int lane) {
+  const int n_inst = nt * (kBf16TileU4 / 64);
+  for (int i = wave; i < n_inst; i += kBf16Waves)
+    __builtin_amdgcn_global_load_lds(fslice + (size_t)t0 * kBf16TileU4 + i * 64 + lane,
+                                     (lds_ptr_t)(buf + i * 1024), 16, 0, 0);
+  if (wave == 0) {
+    const int n_cn = nt * kTileC;
+    for (int i = 0; i < n_cn; i += 64)
+      if (i + lane < n_cn)
+        __builtin_amdgcn_global_load_lds(cslice + t0 * kTileC + i + lane,
+                                         (lds_ptr_t)(buf + kBf16StageTiles * kBf16TileU4 * 16 + i * 4), 4, 0, 0);
+  }
+}
+
+// Lowest-index argmin of the lane's 16 results of a tile (rows ascend with v),
+// as a 4-level tree so the compares are independent, then merged into the
+// running minimum (earlier tiles hold lower indices, so only a strictly smaller
+// value replaces it).
+// Tile epilogue of the running argmin.  The lane's 16 results of a tile
+// (rows ascending with v) are reduced to their minimum with min3 (8 ops); only
+// when that beats the running best does the lane search for the lowest row
+// holding it.  Because tiles are visited in ascending order and only a
+// strictly smaller value replaces the best, the result is the lowest index
+// among equal minima.  The search is skipped by a wave-uniform branch (taken
+// when any lane improved) and applied with per-lane selects, so EXEC is never
+// narrowed while matrix instructions are in flight.
+// Row of result register v within the lane's half of a 32x32 tile.
+#define LKV_ROW(v) (8 * ((v) >> 2) + ((v) & 3))
+
+__device__ __forceinline__ float tile_min(const floatx16& x) {
+  const float a = __builtin_fminf(__builtin_fminf(x[0], x[1]), x[2]);
+  const float b = __builtin_fminf(__builtin_fminf(x[3], x[4]), x[5]);
+  const float c = __builtin_fminf(__builtin_fminf(x[6], x[7]), x[8]);
+  const float d = __builtin_fminf(__builtin_fminf(x[9], x[10]), x[11]);
+  const float e = __builtin_fminf(__builtin_fminf(x[12], x[13]), x[14]);
+  const float f = __builtin_fminf(__builtin_fminf(a, b), c);
+  const float g = __builtin_fminf(__builtin_fminf(d, e), x[15]);
+  return __builtin_fminf(f, g);
+}
+
+// Lowest row of the tile holding the value m (the lane's minimum).
+__device__ __forceinline__ int tile_find(const floatx16& x, float m) {
+  int id = LKV_ROW(15);
+#define LKV_PICK(v) id = (x[v] == m) ? LKV_ROW(v) : id
+  LKV_PICK(14); LKV_PICK(13); LKV_PICK(12); LKV_PICK(11); LKV_PICK(10); LKV_PICK(9); LKV_PICK(8);
+  LKV_PICK(7); LKV_PICK(6); LKV_PICK(5); LKV_PICK(4); LKV_PICK(3); LKV_PICK(2); LKV_PICK(1); LKV_PICK(0);
+#undef LKV_PICK
+  return id;
+}
+
+constexpr int kBf16StageBytes = kBf16StageTiles * (kBf16TileU4 * 16 + kTileC * 4);
+
+// One LDS stage of the bf16 sweep: the stage's tiles are already in `cur`;
+// the next stage is copied asynchronously into `nxt` meanwhile.  `cur` and
+// `nxt` are distinct __shared__ objects so the compiler can tell the reads of
+// one from the DMA into the other and does not wait for the prefetch.
+template <int kKT>
+__device__ __forceinline__ void bf16_stage(const char* cur, char* nxt, const uint4* fslice, const float* cslice,
+                                           int st, int n_stages, int n_ctiles, int wave, int lane, int h,
+                                           const bf16x8_t (&b)[kKT][kBf16Steps], float (&best)[kKT], int (&bidx)[kKT]) {
+  const int t0 = st * kBf16StageTiles;
+  const int nt = min(kBf16StageTiles, n_ctiles - t0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();   // stage st is in LDS everywhere; the other buffer is free
+  if (st + 1 < n_stages)
+    stage_tiles_async(fslice, cslice, t0 + kBf16StageTiles, min(kBf16StageTiles, n_ctiles - t0 - kBf16StageTiles),
+                      nxt, wave, lane);
+  const uint4* s_frag = reinterpret_cast<const uint4*>(cur);
+  const float* s_cn = reinterpret_cast<const float*>(cur + kBf16StageTiles * kBf16TileU4 * 16);
+  for (int tt = 0; tt < nt; ++tt) {
+    bf16x8_t a[kBf16Steps];
+#pragma unroll
+    for (int s = 0; s < kBf16Steps; ++s)
+      a[s] = __builtin_bit_cast(bf16x8_t, s_frag[(tt * kBf16Steps + s) * 64 + lane]);
+    floatx16 cn;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const float4 x = *reinterpret_cast<const float4*>(&s_cn[tt * kTileC + 8 * g + 4 * h]);
+      cn[4 * g + 0] = x.x; cn[4 * g + 1] = x.y; cn[4 * g + 2] = x.z; cn[4 * g + 3] = x.w;
+    }
+    const int cbase = (t0 + tt) * kTileC + 4 * h;
+    // independent accumulation chains (one per key tile), interleaved step by
+    // step so consecutive MFMAs never wait on each other
+    floatx16 acc[kKT];
+#pragma unroll
+    for (int kt = 0; kt < kKT; ++kt)
+      acc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], b[kt][0], cn, 0, 0, 0);
+#pragma unroll
+    for (int s = 1; s < kBf16Steps; ++s)
+#pragma unroll
+      for (int kt = 0; kt < kKT; ++kt)
+        acc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s], b[kt][s], acc[kt], 0, 0, 0);
+#pragma unroll
+    for (int kt = 0; kt < kKT; ++kt) {
+      const float m = tile_min(acc[kt]);
+      const bool better = m < best[kt];
+      // wave-uniform branch: EXEC stays all-ones, lanes select their update.
+      // The predicate goes through an opaque register so the compiler cannot
+      // turn the selects back into an EXEC-masked block.
+      if (__builtin_amdgcn_ballot_w64(better)) {
+        int sel = better ? 1 : 0;
+        int id = cbase + tile_find(acc[kt], m);
+        asm volatile("" : "+v"(sel), "+v"(id));
+        bidx[kt] = sel ? id : bidx[kt];
+        best[kt] = sel ? m : best[kt];
+      }
+    }
+  }
+}
+
 // bf16 keys: each wave holds kBf16KeyTiles tiles of 32 keys as MFMA B operands
-// for the whole sweep; centroid tiles stream through LDS.  Lane l owns key
+// for the whole sweep; centroid tiles stream through two LDS stage buffers
+// (the next stage loads while the current one is used).  Lane l owns key
 // column l % 32 and rows 8*(v/4) + 4*(l/32) + (v%4) of each 32x32 result, so
 // the argmin over a tile is in-lane; the two lane halves merge at the end.
-__global__ __launch_bounds__(kAssignThreads, 2)
+__global__ __launch_bounds__(kBf16Threads, 8 / kBf16Waves)
 void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restrict__ frag,
                         const float* __restrict__ cnorm, int32_t* __restrict__ assign,
                         int32_t* __restrict__ counts, int n_tokens, int n_clusters, int n_ctiles,
                         int blocks_per_slice, int hist_in_lds) {
-  extern __shared__ __align__(16) char smem[];
-  uint4* s_frag = reinterpret_cast<uint4*>(smem);
-  float* s_cn = reinterpret_cast<float*>(smem + kBf16StageTiles * kBf16TileU4 * 16);
+  __shared__ __align__(16) char s_stage0[kBf16StageBytes];
+  __shared__ __align__(16) char s_stage1[kBf16StageBytes];
 
   const int slice = blockIdx.x / blocks_per_slice;
   const int kb = blockIdx.x - slice * blocks_per_slice;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, j = lane & 31;
   const int key_base = kb * kBf16KeysPerBlock + wave * (32 * kBf16KeyTiles);
   const uint16_t* kslice = keys + (size_t)slice * n_tokens * kHeadDim;
+  const uint4* fslice = frag + (size_t)slice * n_ctiles * kBf16TileU4;
+  const float* cslice = cnorm + (size_t)slice * n_ctiles * kTileC;
+  const int n_stages = (n_ctiles + kBf16StageTiles - 1) / kBf16StageTiles;
 
+  stage_tiles_async(fslice, cslice, 0, min(kBf16StageTiles, n_ctiles), s_stage0, wave, lane);
   bf16x8_t b[kBf16KeyTiles][kBf16Steps];
 #pragma unroll
   for (int kt = 0; kt < kBf16KeyTiles; ++kt) {
@@ -158,43 +289,14 @@ void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restri
 #pragma unroll
   for (int kt = 0; kt < kBf16KeyTiles; ++kt) {
     best[kt] = __builtin_inff();
-    bidx[kt] = 0;
+    bidx[kt] = -1;
   }
 
-  const uint4* fslice = frag + (size_t)slice * n_ctiles * kBf16TileU4;
-  const float* cslice = cnorm + (size_t)slice * n_ctiles * kTileC;
-  for (int t0 = 0; t0 < n_ctiles; t0 += kBf16StageTiles) {
-    const int nt = min(kBf16StageTiles, n_ctiles - t0);
-    __syncthreads();
-    for (int i = tid; i < nt * kBf16TileU4; i += kAssignThreads) s_frag[i] = fslice[(size_t)t0 * kBf16TileU4 + i];
-    for (int i = tid; i < nt * kTileC; i += kAssignThreads) s_cn[i] = cslice[t0 * kTileC + i];
-    __syncthreads();
-    for (int tt = 0; tt < nt; ++tt) {
-      bf16x8_t a[kBf16Steps];
-#pragma unroll
-      for (int s = 0; s < kBf16Steps; ++s)
-        a[s] = __builtin_bit_cast(bf16x8_t, s_frag[(tt * kBf16Steps + s) * 64 + lane]);
-      floatx16 cn;
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const float4 x = *reinterpret_cast<const float4*>(&s_cn[tt * kTileC + 8 * g + 4 * h]);
-        cn[4 * g + 0] = x.x; cn[4 * g + 1] = x.y; cn[4 * g + 2] = x.z; cn[4 * g + 3] = x.w;
-      }
-      const int cbase = (t0 + tt) * kTileC + 4 * h;
-#pragma unroll
-      for (int kt = 0; kt < kBf16KeyTiles; ++kt) {
-        floatx16 acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], b[kt][0], cn, 0, 0, 0);
-#pragma unroll
-        for (int s = 1; s < kBf16Steps; ++s)
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s], b[kt][s], acc, 0, 0, 0);
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float x = acc[v];
-          const int c = cbase + 8 * (v >> 2) + (v & 3);
-          if (x < best[kt]) { best[kt] = x; bidx[kt] = c; }
-        }
-      }
-    }
+  for (int st = 0; st < n_stages; st += 2) {
+    bf16_stage<kBf16KeyTiles>(s_stage0, s_stage1, fslice, cslice, st, n_stages, n_ctiles, wave, lane, h, b, best, bidx);
+    if (st + 1 < n_stages)
+      bf16_stage<kBf16KeyTiles>(s_stage1, s_stage0, fslice, cslice, st + 1, n_stages, n_ctiles, wave, lane, h, b, best,
+                                bidx);
   }
 
   int zi[kBf16KeyTiles];
@@ -203,7 +305,12 @@ void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restri
   for (int kt = 0; kt < kBf16KeyTiles; ++kt) {
     const float ob = __shfl_xor(best[kt], 32, kWave);
     const int oi = __shfl_xor(bidx[kt], 32, kWave);
-    if (ob < best[kt] || (ob == best[kt] && oi < bidx[kt])) { best[kt] = ob; bidx[kt] = oi; }
+    // a half that never saw a finite value holds index -1
+    if (bidx[kt] < 0 || (oi >= 0 && (ob < best[kt] || (ob == best[kt] && oi < bidx[kt])))) {
+      best[kt] = ob;
+      bidx[kt] = oi;
+    }
+    if (bidx[kt] < 0) bidx[kt] = 0;   // only reachable with non-finite inputs
     const int key = key_base + kt * 32 + j;
     zi[kt] = bidx[kt];
     zv[kt] = (h == 0) && key < n_tokens;
@@ -211,7 +318,7 @@ void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restri
   }
   if (counts) {
     __syncthreads();
-    block_histogram(reinterpret_cast<int*>(smem), hist_in_lds, n_clusters,
+    block_histogram(reinterpret_cast<int*>(s_stage0), hist_in_lds, n_clusters,
                     counts + (size_t)slice * n_clusters, zi, zv, kBf16KeyTiles);
   }
 }
@@ -548,10 +655,8 @@ int launch_assign(const void* keys, int dtype, int64_t S, int N, int C, const Ws
   const int n_ctiles = ceil_div(C, kTileC);
   if (dtype == LOUISKV_BF16) {
     const int bps = ceil_div(N, kBf16KeysPerBlock);
-    size_t lds = (size_t)kBf16StageTiles * (kBf16TileU4 * 16 + kTileC * 4);
-    const bool hist_lds = (size_t)C * 4 <= std::max(lds, kMaxHistLds);
-    if (with_counts && hist_lds) lds = std::max(lds, (size_t)C * 4);
-    assign_bf16_kernel<<<(unsigned)(S * bps), kAssignThreads, lds, st>>>(
+    const bool hist_lds = (size_t)C * 4 <= (size_t)kBf16StageBytes;
+    assign_bf16_kernel<<<(unsigned)(S * bps), kBf16Threads, 0, st>>>(
         static_cast<const uint16_t*>(keys), w.frag, w.cnorm, assign, with_counts ? w.counts : nullptr, N, C,
         n_ctiles, bps, hist_lds ? 1 : 0);
   } else {
