@@ -33,7 +33,7 @@ constexpr int kF32TileU4 = 16 * 64;                // uint4 per fp32 operand til
 #define LKV_BF16_KEY_TILES 4
 #endif
 #ifndef LKV_BF16_STAGE_TILES
-#define LKV_BF16_STAGE_TILES 4
+#define LKV_BF16_STAGE_TILES 2
 #endif
 #ifndef LKV_ASSIGN_WAVES
 #define LKV_ASSIGN_WAVES 4
@@ -48,6 +48,16 @@ constexpr int kF32KeysPerBlock = 4 * 32;           // one 32-key tile per wave
 constexpr int kF32StageTiles = 2;
 
 __host__ __device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// Workgroups are dealt to the 8 XCDs round-robin by block id.  Renumber the
+// first 8*floor(n/8) blocks so that consecutive logical blocks (the blocks of
+// one slice) run on the same XCD and share its L2; the tail keeps its id.
+constexpr int kXcds = 8;
+__device__ __forceinline__ int xcd_local_block(int b, int n) {
+  const int q = n / kXcds;
+  if (b >= q * kXcds) return b;
+  return (b % kXcds) * q + b / kXcds;
+}
 
 template <class T>
 __global__ void init_centroids_kernel(const T* __restrict__ keys, const int32_t* __restrict__ init_idx,
@@ -136,28 +146,49 @@ __device__ __forceinline__ void block_histogram(int* hist, bool lds_ok, int n_cl
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
-// Asynchronous copy of centroid tiles [t0, t0+nt) (operand fragments and
-// norms) from global memory straight into one LDS stage buffer.  Each wave
-// instruction moves 64 lanes x 16 bytes; completion is tracked by vmcnt.
-__device__ __forceinline__ void stage_tiles_async(const uint4* fslice, const float* cslice, int t0, int nt,
-                                                  char* buf, int wave, int lane) {
-  const int n_inst = nt * (kBf16TileU4 / 64);
-  for (int i = wave; i < n_inst; i += kBf16Waves)
-    __builtin_amdgcn_global_load_lds(fslice + (size_t)t0 * kBf16TileU4 + i * 64 + lane,
-                                     (lds_ptr_t)(buf + i * 1024), 16, 0, 0);
-  if (wave == 0) {
-    const int n_cn = nt * kTileC;
-    for (int i = 0; i < n_cn; i += 64)
-      if (i + lane < n_cn)
-        __builtin_amdgcn_global_load_lds(cslice + t0 * kTileC + i + lane,
-                                         (lds_ptr_t)(buf + kBf16StageTiles * kBf16TileU4 * 16 + i * 4), 4, 0, 0);
+constexpr int kBf16Ring = 4;                          // LDS stage buffers in flight
+constexpr int kBf16StageBytes = kBf16StageTiles * kBf16TileU4 * 16 + 64 * 4;
+// DMA instructions each wave issues per stage: its share of the operand tiles
+// plus one copy of the stage's norms (every wave writes the same norms, so the
+// count is the same for all waves and vmcnt thresholds are uniform).
+constexpr int kBf16DmaPerWave = kBf16StageTiles * (kBf16TileU4 / 64) / kBf16Waves + 1;
+static_assert(kBf16StageTiles * (kBf16TileU4 / 64) % kBf16Waves == 0, "operand copies must split evenly");
+static_assert(kBf16StageTiles * kTileC <= 64, "one 64-lane copy carries a stage's norms");
+
+// Asynchronous copy of stage `st` (centroid operand tiles and their norms)
+// straight from global memory into an LDS stage buffer; 64 lanes x 16 bytes
+// per instruction, completion tracked by vmcnt.  The tile count is padded to
+// whole stages, so every stage copies the same amount.
+// Copies [q0, q1) of the wave's kBf16DmaPerWave instructions for stage st
+// (the last one carries the norms), so a stage's copy can be spread out.
+__device__ __forceinline__ void stage_async_part(const uint4* fslice, const float* cslice, int st, char* buf,
+                                                 int wave, int lane, int q0, int q1) {
+  const uint4* src = fslice + (size_t)st * kBf16StageTiles * kBf16TileU4;
+#pragma unroll
+  for (int q = 0; q < kBf16DmaPerWave - 1; ++q) {
+    if (q < q0 || q >= q1) continue;
+    const int i = wave + q * kBf16Waves;
+    __builtin_amdgcn_global_load_lds(src + i * 64 + lane, (lds_ptr_t)(buf + i * 1024), 16, 0, 0);
+  }
+  if (q1 == kBf16DmaPerWave) {
+    const int c = lane % (kBf16StageTiles * kTileC);
+    __builtin_amdgcn_global_load_lds(cslice + st * kBf16StageTiles * kTileC + c,
+                                     (lds_ptr_t)(buf + kBf16StageTiles * kBf16TileU4 * 16), 4, 0, 0);
   }
 }
 
-// Lowest-index argmin of the lane's 16 results of a tile (rows ascend with v),
-// as a 4-level tree so the compares are independent, then merged into the
-// running minimum (earlier tiles hold lower indices, so only a strictly smaller
-// value replaces it).
+__device__ __forceinline__ void stage_async(const uint4* fslice, const float* cslice, int st, char* buf, int wave,
+                                            int lane) {
+  stage_async_part(fslice, cslice, st, buf, wave, lane, 0, kBf16DmaPerWave);
+}
+
+__device__ __forceinline__ void wait_vm_stages(int k) {
+  // at most k later stages' copies may still be in flight
+  if (k >= 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kBf16DmaPerWave) : "memory");
+  else if (k == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kBf16DmaPerWave) : "memory");
+  else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
 // Tile epilogue of the running argmin.  The lane's 16 results of a tile
 // (rows ascending with v) are reduced to their minimum with min3 (8 ops); only
 // when that beats the running best does the lane search for the lowest row
@@ -190,26 +221,29 @@ __device__ __forceinline__ int tile_find(const floatx16& x, float m) {
   return id;
 }
 
-constexpr int kBf16StageBytes = kBf16StageTiles * (kBf16TileU4 * 16 + kTileC * 4);
-
-// One LDS stage of the bf16 sweep: the stage's tiles are already in `cur`;
-// the next stage is copied asynchronously into `nxt` meanwhile.  `cur` and
-// `nxt` are distinct __shared__ objects so the compiler can tell the reads of
-// one from the DMA into the other and does not wait for the prefetch.
+// One stage of the bf16 sweep.  `cur` holds stage st (its copy was waited
+// for); the copy of stage st + kBf16Ring - 1 goes into `nxt`, the buffer that
+// stage st - 1 used.
 template <int kKT>
-__device__ __forceinline__ void bf16_stage(const char* cur, char* nxt, const uint4* fslice, const float* cslice,
-                                           int st, int n_stages, int n_ctiles, int wave, int lane, int h,
-                                           const bf16x8_t (&b)[kKT][kBf16Steps], float (&best)[kKT], int (&bidx)[kKT]) {
-  const int t0 = st * kBf16StageTiles;
-  const int nt = min(kBf16StageTiles, n_ctiles - t0);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();   // stage st is in LDS everywhere; the other buffer is free
-  if (st + 1 < n_stages)
-    stage_tiles_async(fslice, cslice, t0 + kBf16StageTiles, min(kBf16StageTiles, n_ctiles - t0 - kBf16StageTiles),
-                      nxt, wave, lane);
+__device__ __forceinline__ void bf16_stage(const char* cur, char* nxt, const uint4* fslice,
+                                           const float* cslice, int st, int n_stages, int wave, int lane, int h,
+                                           const bf16x8_t (&b)[kKT][kBf16Steps], float (&best)[kKT],
+                                           int (&bidx)[kKT]) {
+  wait_vm_stages(min(kBf16Ring - 2, n_stages - 1 - st));
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();   // stage st is in LDS for all waves; stage st-1's buffer is free
+  const bool copy_next = st + kBf16Ring - 1 < n_stages;
   const uint4* s_frag = reinterpret_cast<const uint4*>(cur);
   const float* s_cn = reinterpret_cast<const float*>(cur + kBf16StageTiles * kBf16TileU4 * 16);
-  for (int tt = 0; tt < nt; ++tt) {
+  const int t0 = st * kBf16StageTiles;
+#pragma unroll
+  for (int tt = 0; tt < kBf16StageTiles; ++tt) {
+    // spread the copy of stage st + kBf16Ring - 1 over the stage's tiles
+    if (copy_next) {
+      const int per = (kBf16DmaPerWave + kBf16StageTiles - 1) / kBf16StageTiles;
+      stage_async_part(fslice, cslice, st + kBf16Ring - 1, nxt, wave, lane, tt * per,
+                       min(kBf16DmaPerWave, (tt + 1) * per));
+    }
     bf16x8_t a[kBf16Steps];
 #pragma unroll
     for (int s = 0; s < kBf16Steps; ++s)
@@ -250,29 +284,63 @@ __device__ __forceinline__ void bf16_stage(const char* cur, char* nxt, const uin
   }
 }
 
+// The whole sweep over the centroid stages.  The four ring buffers are
+// restrict parameters of this one inlined function, so every asynchronous
+// copy and every LDS read below carries alias scopes that tell the compiler
+// which buffer it touches; it then waits only where the code says so instead
+// of draining all copies in flight before each read.
+template <int kKT>
+__device__ __forceinline__ void bf16_sweep(char* __restrict__ r0, char* __restrict__ r1, char* __restrict__ r2,
+                                           char* __restrict__ r3, const uint4* fslice, const float* cslice,
+                                           int n_stages, int wave, int lane, int h,
+                                           const bf16x8_t (&b)[kKT][kBf16Steps], float (&best)[kKT],
+                                           int (&bidx)[kKT]) {
+  // prologue: the first kBf16Ring - 1 stages are copied before the sweep
+  stage_async(fslice, cslice, 0, r0, wave, lane);
+  if (n_stages > 1) stage_async(fslice, cslice, 1, r1, wave, lane);
+  if (n_stages > 2) stage_async(fslice, cslice, 2, r2, wave, lane);
+#pragma unroll
+  for (int kt = 0; kt < kKT; ++kt) {
+    best[kt] = __builtin_inff();
+    bidx[kt] = -1;
+  }
+  for (int st = 0; st < n_stages; st += kBf16Ring) {
+    bf16_stage<kKT>(r0, r3, fslice, cslice, st, n_stages, wave, lane, h, b, best, bidx);
+    if (st + 1 >= n_stages) break;
+    bf16_stage<kKT>(r1, r0, fslice, cslice, st + 1, n_stages, wave, lane, h, b, best, bidx);
+    if (st + 2 >= n_stages) break;
+    bf16_stage<kKT>(r2, r1, fslice, cslice, st + 2, n_stages, wave, lane, h, b, best, bidx);
+    if (st + 3 >= n_stages) break;
+    bf16_stage<kKT>(r3, r2, fslice, cslice, st + 3, n_stages, wave, lane, h, b, best, bidx);
+  }
+}
+
 // bf16 keys: each wave holds kBf16KeyTiles tiles of 32 keys as MFMA B operands
-// for the whole sweep; centroid tiles stream through two LDS stage buffers
-// (the next stage loads while the current one is used).  Lane l owns key
-// column l % 32 and rows 8*(v/4) + 4*(l/32) + (v%4) of each 32x32 result, so
-// the argmin over a tile is in-lane; the two lane halves merge at the end.
+// for the whole sweep; centroid tiles stream through a ring of kBf16Ring LDS
+// stage buffers, copied kBf16Ring - 1 stages ahead.  Lane l owns key column
+// l % 32 and rows 8*(v/4) + 4*(l/32) + (v%4) of each 32x32 result, so the
+// argmin over a tile is in-lane; the two lane halves merge at the end.
 __global__ __launch_bounds__(kBf16Threads, 8 / kBf16Waves)
 void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restrict__ frag,
                         const float* __restrict__ cnorm, int32_t* __restrict__ assign,
                         int32_t* __restrict__ counts, int n_tokens, int n_clusters, int n_ctiles,
                         int blocks_per_slice, int hist_in_lds) {
-  __shared__ __align__(16) char s_stage0[kBf16StageBytes];
-  __shared__ __align__(16) char s_stage1[kBf16StageBytes];
+  __shared__ __align__(16) char s_ring0[kBf16StageBytes];
+  __shared__ __align__(16) char s_ring1[kBf16StageBytes];
+  __shared__ __align__(16) char s_ring2[kBf16StageBytes];
+  __shared__ __align__(16) char s_ring3[kBf16StageBytes];
+  static_assert(kBf16Ring == 4, "the stage loop below is unrolled for four buffers");
 
-  const int slice = blockIdx.x / blocks_per_slice;
-  const int kb = blockIdx.x - slice * blocks_per_slice;
+  const int lb = xcd_local_block(blockIdx.x, gridDim.x);
+  const int slice = lb / blocks_per_slice;
+  const int kb = lb - slice * blocks_per_slice;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, j = lane & 31;
   const int key_base = kb * kBf16KeysPerBlock + wave * (32 * kBf16KeyTiles);
   const uint16_t* kslice = keys + (size_t)slice * n_tokens * kHeadDim;
   const uint4* fslice = frag + (size_t)slice * n_ctiles * kBf16TileU4;
   const float* cslice = cnorm + (size_t)slice * n_ctiles * kTileC;
-  const int n_stages = (n_ctiles + kBf16StageTiles - 1) / kBf16StageTiles;
+  const int n_stages = n_ctiles / kBf16StageTiles;   // n_ctiles is padded to whole stages
 
-  stage_tiles_async(fslice, cslice, 0, min(kBf16StageTiles, n_ctiles), s_stage0, wave, lane);
   bf16x8_t b[kBf16KeyTiles][kBf16Steps];
 #pragma unroll
   for (int kt = 0; kt < kBf16KeyTiles; ++kt) {
@@ -284,20 +352,13 @@ void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restri
       b[kt][s] = __builtin_bit_cast(bf16x8_t, v);
     }
   }
+  // the key operands are complete before the sweep starts, so no key load is
+  // pending inside the stage loop (the loop then only waits for its copies)
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   float best[kBf16KeyTiles];
   int bidx[kBf16KeyTiles];
-#pragma unroll
-  for (int kt = 0; kt < kBf16KeyTiles; ++kt) {
-    best[kt] = __builtin_inff();
-    bidx[kt] = -1;
-  }
-
-  for (int st = 0; st < n_stages; st += 2) {
-    bf16_stage<kBf16KeyTiles>(s_stage0, s_stage1, fslice, cslice, st, n_stages, n_ctiles, wave, lane, h, b, best, bidx);
-    if (st + 1 < n_stages)
-      bf16_stage<kBf16KeyTiles>(s_stage1, s_stage0, fslice, cslice, st + 1, n_stages, n_ctiles, wave, lane, h, b, best,
-                                bidx);
-  }
+  bf16_sweep<kBf16KeyTiles>(s_ring0, s_ring1, s_ring2, s_ring3, fslice, cslice, n_stages, wave, lane, h, b, best,
+                            bidx);
 
   int zi[kBf16KeyTiles];
   bool zv[kBf16KeyTiles];
@@ -318,7 +379,7 @@ void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restri
   }
   if (counts) {
     __syncthreads();
-    block_histogram(reinterpret_cast<int*>(s_stage0), hist_in_lds, n_clusters,
+    block_histogram(reinterpret_cast<int*>(s_ring0), hist_in_lds, n_clusters,
                     counts + (size_t)slice * n_clusters, zi, zv, kBf16KeyTiles);
   }
 }
@@ -618,9 +679,16 @@ struct Ws {
   size_t bytes;
 };
 
+// Centroid tiles per slice; bf16 pads to whole LDS stages (padding rows have a
+// zero operand and an infinite norm, so they never win).
+int n_ctiles_for(int n_clusters, int dtype) {
+  const int t = ceil_div(n_clusters, kTileC);
+  return dtype == LOUISKV_BF16 ? ceil_div(t, kBf16StageTiles) * kBf16StageTiles : t;
+}
+
 Ws carve(void* base, int64_t n_slices, int n_tokens, int n_clusters, int dtype) {
   Carver cv(base);
-  const int n_ctiles = ceil_div(n_clusters, kTileC);
+  const int n_ctiles = n_ctiles_for(n_clusters, dtype);
   const int tile_u4 = dtype == LOUISKV_BF16 ? kBf16TileU4 : kF32TileU4;
   Ws w;
   w.frag = cv.take<uint4>((size_t)n_slices * n_ctiles * tile_u4);
@@ -637,7 +705,7 @@ constexpr size_t kMaxHistLds = 64 * 1024;
 
 int launch_prep(const float* reps, int stride, int64_t S, int C, int dtype, const Ws& w, bool zero_counts,
                 hipStream_t st) {
-  const int n_ctiles = ceil_div(C, kTileC);
+  const int n_ctiles = n_ctiles_for(C, dtype);
   const int64_t rows = S * n_ctiles * kTileC;
   const int grid = (int)((rows + 3) / 4);
   if (dtype == LOUISKV_BF16)
@@ -652,7 +720,7 @@ int launch_prep(const float* reps, int stride, int64_t S, int C, int dtype, cons
 
 int launch_assign(const void* keys, int dtype, int64_t S, int N, int C, const Ws& w, int32_t* assign,
                   bool with_counts, hipStream_t st) {
-  const int n_ctiles = ceil_div(C, kTileC);
+  const int n_ctiles = n_ctiles_for(C, dtype);
   if (dtype == LOUISKV_BF16) {
     const int bps = ceil_div(N, kBf16KeysPerBlock);
     const bool hist_lds = (size_t)C * 4 <= (size_t)kBf16StageBytes;
