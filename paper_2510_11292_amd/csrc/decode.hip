@@ -361,29 +361,76 @@ void gather_kernel(const T* __restrict__ k_pool, const T* __restrict__ v_pool, i
 
 constexpr int kAttnChunk = 256;   // rows per split-KV block
 
-__device__ __forceinline__ void load8(const uint16_t* p, float* x) {
-  const uint4 v = *reinterpret_cast<const uint4*>(p);
-  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    x[2 * i] = __uint_as_float(w[i] << 16);
-    x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-  }
+// Sum over the 16 lanes of a DPP row, result in every lane of the row:
+// butterflies over lane^1, lane^2 (quad permutes), then the mirrored halves
+// of 8 and of 16 lanes.  All VALU, no LDS traffic.
+__device__ __forceinline__ float row16_sum(float x) {
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0xB1, 0xF, 0xF, false));
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x4E, 0xF, 0xF, false));
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x141, 0xF, 0xF, false));
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x140, 0xF, 0xF, false));
+  return x;
 }
-__device__ __forceinline__ void load8(const float* p, float* x) {
-  const float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
-  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// One lane's share (8 dims) of a K or V row, kept in storage format until used.
+template <class T> struct Raw8;
+template <> struct Raw8<uint16_t> {
+  uint32_t w[4];
+  __device__ __forceinline__ void load(const uint16_t* p) {
+    const uint4 v = *reinterpret_cast<const uint4*>(p);
+    w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+  }
+  __device__ __forceinline__ float at(int e) const {
+    return __uint_as_float((e & 1) ? (w[e >> 1] & 0xffff0000u) : (w[e >> 1] << 16));
+  }
+  // sum_e a[e] * this[e] with fp32 accumulation of the exact bf16 products
+  __device__ __forceinline__ float dot(const Raw8& a) const {
+    typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
+    float d = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      d = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf2, a.w[i]), __builtin_bit_cast(bf2, w[i]), d, false);
+    return d;
+  }
+};
+template <> struct Raw8<float> {
+  float x[8];
+  __device__ __forceinline__ void load(const float* p) {
+    const float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+  }
+  __device__ __forceinline__ float at(int e) const { return x[e]; }
+  __device__ __forceinline__ float dot(const Raw8& a) const {
+    float d = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) d = fmaf(a.x[e], x[e], d);
+    return d;
+  }
+};
+
+// Rows each 16-lane group keeps in flight: enough loads outstanding to cover
+// HBM latency at the occupancy the register footprint allows.
+template <class T, int G>
+constexpr int attn_rows_in_flight() {
+  return (sizeof(T) == 2 ? 4 : 2) / (G == 8 ? 2 : 1);
 }
 
 // Block (chunk, slice): online softmax over up to kAttnChunk rows for the G
-// query heads of the slice; 16 lanes per row, lane sub owns dims 8*sub..+7.
-// Writes (m, l, acc[128]) per head to the partial buffer.
+// query heads of the slice, in base 2 (logits scaled by log2 e / sqrt d);
+// 16 lanes per row, lane sub owns dims 8*sub..+7, and each 16-lane group takes
+// every 16th row, R rows per pass with all their loads issued up front.  The
+// running maximum and the rescale of the accumulators change only when some
+// lane's maximum grows (a wave-uniform branch with per-lane selects).  Writes
+// (m, l, acc[128]) per head, m in base 2.
 template <class T, int G>
 __global__ __launch_bounds__(256)
 void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, const T* __restrict__ k_buf,
                          const T* __restrict__ v_buf, const int32_t* __restrict__ n_sel, int buf_rows,
                          const T* __restrict__ k_local, const T* __restrict__ v_local, int window, int local_start,
                          int n_local, int n_chunks, float* __restrict__ part) {
+  constexpr int R = attn_rows_in_flight<T, G>();
   __shared__ float s_m[4][G], s_l[4][G];
   __shared__ float s_acc[4][G][kHeadDim];
   const int64_t s = blockIdx.x / n_chunks;
@@ -395,15 +442,13 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
   const int total = nsel + n_local;
   const int r0 = chunk * kAttnChunk;
   const int r1 = min(total, r0 + kAttnChunk);
+  const int n_pass = r1 > r0 ? (r1 - r0 + 16 * R - 1) / (16 * R) : 0;   // same for every lane of the block
 
-  float qv[G][8];
+  Raw8<T> qv[G];
   const size_t qbase = ((size_t)grp * n_kv_heads * G + (size_t)kvh * G) * kHeadDim + 8 * sub;
 #pragma unroll
-  for (int j = 0; j < G; ++j) {
-    load8(q + qbase + (size_t)j * kHeadDim, qv[j]);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) qv[j][e] *= scale;
-  }
+  for (int j = 0; j < G; ++j) qv[j].load(q + qbase + (size_t)j * kHeadDim);
+  const float qs = scale * kLog2e;
   float m[G], l[G], acc[G][8];
 #pragma unroll
   for (int j = 0; j < G; ++j) {
@@ -412,36 +457,68 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[j][e] = 0.f;
   }
-  for (int r = r0 + rg; r < r1; r += 16) {
-    const T* kr;
-    const T* vr;
-    if (r < nsel) {
-      kr = k_buf + ((size_t)s * buf_rows + r) * kHeadDim;
-      vr = v_buf + ((size_t)s * buf_rows + r) * kHeadDim;
-    } else {
-      const int slot = (local_start + (r - nsel)) % window;
-      kr = k_local + ((size_t)s * window + slot) * kHeadDim;
-      vr = v_local + ((size_t)s * window + slot) * kHeadDim;
+  const T* kb = k_buf + (size_t)s * buf_rows * kHeadDim + 8 * sub;
+  const T* vb = v_buf + (size_t)s * buf_rows * kHeadDim + 8 * sub;
+  const T* kl = k_local + (size_t)s * window * kHeadDim + 8 * sub;
+  const T* vl = v_local + (size_t)s * window * kHeadDim + 8 * sub;
+  for (int ps = 0; ps < n_pass; ++ps) {
+    Raw8<T> kx[R], vx[R];
+    bool valid[R];
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      const int r = r0 + rg + 16 * (ps * R + i);
+      valid[i] = r < r1;
+      const int rr = valid[i] ? r : r0;    // rows past the chunk re-read its first row and are masked
+      size_t off;
+      const T* kp;
+      const T* vp;
+      if (rr < nsel) {
+        off = (size_t)rr * kHeadDim;
+        kp = kb; vp = vb;
+      } else {
+        int slot = local_start + (rr - nsel);      // local_start < window and rr - nsel < n_local <= window
+        slot -= slot >= window ? window : 0;
+        off = (size_t)slot * kHeadDim;
+        kp = kl; vp = vl;
+      }
+      kx[i].load(kp + off);
+      vx[i].load(vp + off);
     }
-    float kx[8], vx[8];
-    load8(kr + 8 * sub, kx);
-    load8(vr + 8 * sub, vx);
+    __builtin_amdgcn_sched_barrier(0);   // keep every load of the pass ahead of its first use
+    float sc[R][G];
+    bool grow = false;
 #pragma unroll
-    for (int j = 0; j < G; ++j) {
-      float d = 0.f;
+    for (int i = 0; i < R; ++i) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) d = fmaf(qv[j][e], kx[e], d);
-      d += __shfl_xor(d, 8, kWave);
-      d += __shfl_xor(d, 4, kWave);
-      d += __shfl_xor(d, 2, kWave);
-      d += __shfl_xor(d, 1, kWave);
-      const float mn = fmaxf(m[j], d);
-      const float corr = expf(m[j] - mn);
-      const float p = expf(d - mn);
-      l[j] = l[j] * corr + p;
+      for (int j = 0; j < G; ++j) {
+        const float d = row16_sum(kx[i].dot(qv[j])) * qs;
+        sc[i][j] = valid[i] ? d : -__builtin_inff();
+        grow |= sc[i][j] > m[j];
+      }
+    }
+    // rescale only when some lane's running maximum grows
+    if (__builtin_amdgcn_ballot_w64(grow)) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[j][e] = fmaf(acc[j][e], corr, p * vx[e]);
-      m[j] = mn;
+      for (int j = 0; j < G; ++j) {
+        float mn = m[j];
+#pragma unroll
+        for (int i = 0; i < R; ++i) mn = fmaxf(mn, sc[i][j]);
+        const float corr = mn == -__builtin_inff() ? 1.f : __builtin_amdgcn_exp2f(m[j] - mn);
+        l[j] *= corr;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[j][e] *= corr;
+        m[j] = mn;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        const float p = valid[i] ? __builtin_amdgcn_exp2f(sc[i][j] - m[j]) : 0.f;
+        l[j] += p;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[j][e] = fmaf(p, vx[i].at(e), acc[j][e]);
+      }
     }
   }
   // merge the 4 row groups of each wave (lanes l, l^16, l^32, l^48 share sub)
@@ -452,8 +529,8 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
       const float mo = __shfl_xor(m[j], o, kWave);
       const float lo = __shfl_xor(l[j], o, kWave);
       const float mn = fmaxf(m[j], mo);
-      const float ca = mn == -__builtin_inff() ? 0.f : expf(m[j] - mn);
-      const float cb = mn == -__builtin_inff() ? 0.f : expf(mo - mn);
+      const float ca = mn == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(m[j] - mn);
+      const float cb = mn == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(mo - mn);
       l[j] = l[j] * ca + lo * cb;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -486,7 +563,7 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
     float ll = 0.f, aa = 0.f;
     if (mm != -__builtin_inff()) {
       for (int q2 = 0; q2 < 4; ++q2) {
-        const float c = expf(s_m[q2][j] - mm);
+        const float c = __builtin_amdgcn_exp2f(s_m[q2][j] - mm);
         ll += s_l[q2][j] * c;
         aa += s_acc[q2][j][k] * c;
       }
@@ -517,7 +594,7 @@ void attn_combine_kernel(const float* __restrict__ part, int n_chunks, int G, in
   if (mm != -__builtin_inff()) {
     for (int c = 0; c < n_chunks; ++c) {
       const float* pc = p + (size_t)c * G * pstride;
-      const float w = expf(pc[0] - mm);
+      const float w = __builtin_amdgcn_exp2f(pc[0] - mm);
       ll += pc[1] * w;
       a0 += pc[2 + 2 * lane] * w;
       a1 += pc[2 + 2 * lane + 1] * w;
@@ -527,7 +604,8 @@ void attn_combine_kernel(const float* __restrict__ part, int n_chunks, int G, in
   TO* o = out + (size_t)row * kHeadDim;
   store_from_f32(o, 2 * lane, a0 * inv);
   store_from_f32(o, 2 * lane + 1, a1 * inv);
-  if (lse_out && lane == 0) lse_out[row] = ll > 0.f ? mm + logf(ll) : -__builtin_inff();
+  // partial maxima are in base 2: lse = ln 2 * (m + log2 l)
+  if (lse_out && lane == 0) lse_out[row] = ll > 0.f ? 0.6931471805599453f * (mm + log2f(ll)) : -__builtin_inff();
 }
 
 int check_dtype(int dtype) {
