@@ -292,6 +292,9 @@ size_t louiskv_sparse_decode_attn_workspace_size(int64_t n_slices, int32_t group
  * lse_out    out [n_groups][n_kv_heads*group_size] float32 or NULL: natural log of
  *            each head's softmax denominator (max included); -inf and o = 0
  *            when a slice has no row.
+ * workspace  louiskv_sparse_decode_attn_workspace_size() bytes for split-KV
+ *            partials; the size is 0 (and workspace may be NULL) when there are
+ *            enough slices for one block per slice.
  */
 int louiskv_sparse_decode_attn(const void* q, int32_t dtype, int64_t n_slices,
                                int32_t n_kv_heads, int32_t group_size, int32_t d,

@@ -359,7 +359,13 @@ void gather_kernel(const T* __restrict__ k_pool, const T* __restrict__ v_pool, i
 
 // ------------------------------------------------------------------ attention
 
-constexpr int kAttnChunk = 256;   // rows per split-KV block
+// One block of 16 waves per CU (8 waves where the register footprint needs
+// more than 128 VGPRs).  A slice's rows go to one block when there are enough
+// slices to fill the chip; otherwise they are cut into n_chunks equal ranges
+// (split-KV), never below kAttnMinRows rows per block, and a second kernel
+// merges the chunk partials.
+constexpr int kAttnTargetBlocks = 256;
+constexpr int kAttnMinRows = 256;
 
 // Sum over the 16 lanes of a DPP row, result in every lane of the row:
 // butterflies over lane^1, lane^2 (quad permutes), then the mirrored halves
@@ -416,33 +422,84 @@ template <class T, int G>
 constexpr int attn_rows_in_flight() {
   return (sizeof(T) == 2 ? 4 : 2) / (G == 8 ? 2 : 1);
 }
-
-// Block (chunk, slice): online softmax over up to kAttnChunk rows for the G
-// query heads of the slice, in base 2 (logits scaled by log2 e / sqrt d);
-// 16 lanes per row, lane sub owns dims 8*sub..+7, and each 16-lane group takes
-// every 16th row, R rows per pass with all their loads issued up front.  The
-// running maximum and the rescale of the accumulators change only when some
-// lane's maximum grows (a wave-uniform branch with per-lane selects).  Writes
-// (m, l, acc[128]) per head, m in base 2.
 template <class T, int G>
-__global__ __launch_bounds__(256)
+constexpr int attn_waves() {
+  return sizeof(T) == 2 && G <= 4 ? 16 : 8;
+}
+
+// Merge NW wave states (base-2 maximum m and sum l per head, acc per head and
+// dim, all in LDS) into the block's result: the normalised output and lse when
+// the block covers the whole slice (n_chunks == 1), else the chunk partial
+// (m, l, acc[128]) per head for attn_combine_kernel.
+template <int G, int NW>
+__device__ __forceinline__ void attn_block_merge(const float (*s_m)[G], const float (*s_l)[G],
+                                                 const float (*s_acc)[G][kHeadDim], int tid, int64_t s, int chunk,
+                                                 int n_chunks, float* __restrict__ part, void* __restrict__ out,
+                                                 int out_bf16, float* __restrict__ lse_out) {
+  for (int i = tid; i < G * kHeadDim; i += NW * 64) {
+    const int j = i / kHeadDim, k = i % kHeadDim;
+    float mm = -__builtin_inff();
+    for (int q2 = 0; q2 < NW; ++q2) mm = fmaxf(mm, s_m[q2][j]);
+    float ll = 0.f, aa = 0.f;
+    if (mm != -__builtin_inff()) {
+      for (int q2 = 0; q2 < NW; ++q2) {
+        const float c = __builtin_amdgcn_exp2f(s_m[q2][j] - mm);
+        ll += s_l[q2][j] * c;
+        aa += s_acc[q2][j][k] * c;
+      }
+    }
+    if (n_chunks == 1) {
+      const size_t row = (size_t)s * G + j;    // (group, query head) row of the output
+      const float o = ll > 0.f ? aa / ll : 0.f;
+      if (out_bf16)
+        static_cast<uint16_t*>(out)[row * kHeadDim + k] = f32_to_bf16(o);
+      else
+        static_cast<float*>(out)[row * kHeadDim + k] = o;
+      // base-2 maxima: lse = ln 2 * (m + log2 l)
+      if (lse_out && k == 0) lse_out[row] = ll > 0.f ? 0.6931471805599453f * (mm + log2f(ll)) : -__builtin_inff();
+    } else {
+      const size_t pstride = 2 + kHeadDim;
+      float* pout = part + ((size_t)s * n_chunks + chunk) * G * pstride;
+      pout[j * pstride + 2 + k] = aa;
+      if (k == 0) {
+        pout[j * pstride + 0] = mm;
+        pout[j * pstride + 1] = ll;
+      }
+    }
+  }
+}
+
+// Block (chunk, slice): online softmax over the chunk's share of rows for the G
+// query heads of the slice, in base 2 (logits scaled by log2 e / sqrt d);
+// 16 lanes per row, lane sub owns dims 8*sub..+7, and each of the 64 row groups
+// takes every 64th row, R rows per pass with all their loads issued up front.
+// The running maximum and the rescale of the accumulators change only when
+// some lane's maximum grows (a wave-uniform branch with per-lane selects).
+// With one chunk the block writes the normalised output (and lse); otherwise
+// it writes (m, l, acc[128]) per head, m in base 2, for the merge kernel.
+template <class T, int G>
+__global__ __launch_bounds__((attn_waves<T, G>() * 64))
 void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, const T* __restrict__ k_buf,
                          const T* __restrict__ v_buf, const int32_t* __restrict__ n_sel, int buf_rows,
                          const T* __restrict__ k_local, const T* __restrict__ v_local, int window, int local_start,
-                         int n_local, int n_chunks, float* __restrict__ part) {
+                         int n_local, int n_chunks, float* __restrict__ part, void* __restrict__ out, int out_bf16,
+                         float* __restrict__ lse_out) {
   constexpr int R = attn_rows_in_flight<T, G>();
-  __shared__ float s_m[4][G], s_l[4][G];
-  __shared__ float s_acc[4][G][kHeadDim];
+  constexpr int kAttnWaves = attn_waves<T, G>();
+  constexpr int kAttnThreads = kAttnWaves * 64;
+  constexpr int kAttnGroups = kAttnWaves * 4;      // 16-lane row groups per block
+  __shared__ float s_m[kAttnWaves][G], s_l[kAttnWaves][G];
+  __shared__ float s_acc[kAttnWaves][G][kHeadDim];
   const int64_t s = blockIdx.x / n_chunks;
   const int chunk = (int)(blockIdx.x - s * n_chunks);
   const int64_t grp = s / n_kv_heads;
   const int kvh = (int)(s - grp * n_kv_heads);
-  const int tid = threadIdx.x, sub = tid & 15, rg = tid >> 4;   // 16 row groups of 16 lanes
+  const int tid = threadIdx.x, sub = tid & 15, rg = tid >> 4;   // 64 row groups of 16 lanes
   const int nsel = max(0, min(n_sel[s], buf_rows));
   const int total = nsel + n_local;
-  const int r0 = chunk * kAttnChunk;
-  const int r1 = min(total, r0 + kAttnChunk);
-  const int n_pass = r1 > r0 ? (r1 - r0 + 16 * R - 1) / (16 * R) : 0;   // same for every lane of the block
+  const int r0 = (int)((int64_t)total * chunk / n_chunks);
+  const int r1 = (int)((int64_t)total * (chunk + 1) / n_chunks);
+  const int n_pass = r1 > r0 ? (r1 - r0 + kAttnGroups * R - 1) / (kAttnGroups * R) : 0;   // block-uniform
 
   Raw8<T> qv[G];
   const size_t qbase = ((size_t)grp * n_kv_heads * G + (size_t)kvh * G) * kHeadDim + 8 * sub;
@@ -461,14 +518,14 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
   const T* vb = v_buf + (size_t)s * buf_rows * kHeadDim + 8 * sub;
   const T* kl = k_local + (size_t)s * window * kHeadDim + 8 * sub;
   const T* vl = v_local + (size_t)s * window * kHeadDim + 8 * sub;
-  for (int ps = 0; ps < n_pass; ++ps) {
-    Raw8<T> kx[R], vx[R];
-    bool valid[R];
+  // Issue the loads of pass ps; rows past the chunk re-read its first row and
+  // are masked.
+  auto load_pass = [&](int ps, Raw8<T>* kx, Raw8<T>* vx, bool* valid) {
 #pragma unroll
     for (int i = 0; i < R; ++i) {
-      const int r = r0 + rg + 16 * (ps * R + i);
+      const int r = r0 + rg + kAttnGroups * (ps * R + i);
       valid[i] = r < r1;
-      const int rr = valid[i] ? r : r0;    // rows past the chunk re-read its first row and are masked
+      const int rr = valid[i] ? r : r0;
       size_t off;
       const T* kp;
       const T* vp;
@@ -484,7 +541,8 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
       kx[i].load(kp + off);
       vx[i].load(vp + off);
     }
-    __builtin_amdgcn_sched_barrier(0);   // keep every load of the pass ahead of its first use
+  };
+  auto compute_pass = [&](const Raw8<T>* kx, const Raw8<T>* vx, const bool* valid) {
     float sc[R][G];
     bool grow = false;
 #pragma unroll
@@ -520,6 +578,13 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
         for (int e = 0; e < 8; ++e) acc[j][e] = fmaf(p, vx[i].at(e), acc[j][e]);
       }
     }
+  };
+  for (int ps = 0; ps < n_pass; ++ps) {
+    Raw8<T> kx[R], vx[R];
+    bool valid[R];
+    load_pass(ps, kx, vx, valid);
+    __builtin_amdgcn_sched_barrier(0);   // keep every load of the pass ahead of its first use
+    compute_pass(kx, vx, valid);
   }
   // merge the 4 row groups of each wave (lanes l, l^16, l^32, l^48 share sub)
 #pragma unroll
@@ -553,27 +618,197 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
     }
   }
   __syncthreads();
-  // merge the 4 waves and write the block's partial
-  const size_t pstride = 2 + kHeadDim;
-  float* out = part + ((size_t)s * n_chunks + chunk) * G * pstride;
-  for (int i = tid; i < G * kHeadDim; i += 256) {
-    const int j = i / kHeadDim, k = i % kHeadDim;
-    float mm = -__builtin_inff();
-    for (int q2 = 0; q2 < 4; ++q2) mm = fmaxf(mm, s_m[q2][j]);
-    float ll = 0.f, aa = 0.f;
-    if (mm != -__builtin_inff()) {
-      for (int q2 = 0; q2 < 4; ++q2) {
-        const float c = __builtin_amdgcn_exp2f(s_m[q2][j] - mm);
-        ll += s_l[q2][j] * c;
-        aa += s_acc[q2][j][k] * c;
+  attn_block_merge<G, kAttnWaves>(s_m, s_l, s_acc, tid, s, chunk, n_chunks, part, out, out_bf16, lse_out);
+}
+
+// ---- bf16: scores on the matrix cores
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 attn_bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float attn_floatx4;
+
+__device__ __forceinline__ float row16_max(float x) {
+  x = fmaxf(x, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0xB1, 0xF, 0xF, false)));
+  x = fmaxf(x, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x4E, 0xF, 0xF, false)));
+  x = fmaxf(x, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x141, 0xF, 0xF, false)));
+  x = fmaxf(x, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x140, 0xF, 0xF, false)));
+  return x;
+}
+
+template <int G>
+constexpr int attn_mfma_waves() {
+  return G == 8 ? 8 : 16;
+}
+
+// Block (chunk, slice) for bf16 K/V.  A wave takes 16-row tiles t = w, w+NW, ...
+// of the chunk.  Scores S = Q K^T come from v_mfma_f32_16x16x32_bf16 with the
+// tile's K rows as the B operand (lane l: row l%16, dims 32c+8(l/16)..+7 of
+// k-chunk c) and Q as the A operand, its g heads repeated over the 16 rows of
+// A, so that every lane receives the scores of its row (l%16) for all heads.
+// The base-2 online softmax runs per lane on those scores; the probabilities
+// go through a per-wave LDS slot to the V layout of the PV step, 16 lanes per
+// row (lane owns dims 8(l%16)..+7, rows 4k + l/16 of the tile for k = 0..3),
+// where P V accumulates in float32 on the vector ALUs.  Output and partials as
+// attn_partial_kernel.
+template <int G>
+__global__ __launch_bounds__((attn_mfma_waves<G>() * 64))
+void attn_mfma_kernel(const uint16_t* __restrict__ q, int n_kv_heads, float scale, const uint16_t* __restrict__ k_buf,
+                      const uint16_t* __restrict__ v_buf, const int32_t* __restrict__ n_sel, int buf_rows,
+                      const uint16_t* __restrict__ k_local, const uint16_t* __restrict__ v_local, int window,
+                      int local_start, int n_local, int n_chunks, float* __restrict__ part, void* __restrict__ out,
+                      int out_bf16, float* __restrict__ lse_out) {
+  constexpr int NW = attn_mfma_waves<G>();
+  constexpr int NM = G == 8 ? 2 : 1;        // matrix ops per k-chunk, 4 heads each
+  constexpr int GA = G < 4 ? G : 4;         // distinct heads in one op's output
+  __shared__ float4 s_p[NW][NM][64];
+  __shared__ float s_m[NW][G], s_l[NW][G];
+  __shared__ float s_acc[NW][G][kHeadDim];
+  const int64_t s = blockIdx.x / n_chunks;
+  const int chunk = (int)(blockIdx.x - s * n_chunks);
+  const int64_t grp = s / n_kv_heads;
+  const int kvh = (int)(s - grp * n_kv_heads);
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, p16 = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);    // wave-uniform, kept in a scalar register
+  const int nsel = max(0, min(n_sel[s], buf_rows));
+  const int total = nsel + n_local;
+  const int r0 = (int)((int64_t)total * chunk / n_chunks);
+  const int r1 = (int)((int64_t)total * (chunk + 1) / n_chunks);
+  const int n_tiles = (r1 - r0 + 15) / 16;   // block-uniform
+
+  // A operand: row m = l%16 holds head 4*mi + m % GA; k-chunk c covers dims 32c..32c+31
+  attn_bf16x8 qa[NM][4];
+  const uint16_t* qs0 = q + ((size_t)grp * n_kv_heads + kvh) * G * kHeadDim;
+#pragma unroll
+  for (int mi = 0; mi < NM; ++mi)
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      qa[mi][c] = __builtin_bit_cast(
+          attn_bf16x8, *reinterpret_cast<const uint4*>(qs0 + (size_t)(4 * mi + p16 % GA) * kHeadDim + 32 * c + 8 * g));
+  const float qscale = scale * kLog2e;
+  float m[G], l[G], acc[G][8];
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    m[j] = -__builtin_inff();
+    l[j] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[j][e] = 0.f;
+  }
+  const uint16_t* kb = k_buf + (size_t)s * buf_rows * kHeadDim;
+  const uint16_t* vb = v_buf + (size_t)s * buf_rows * kHeadDim;
+  const uint16_t* kl = k_local + (size_t)s * window * kHeadDim;
+  const uint16_t* vl = v_local + (size_t)s * window * kHeadDim;
+  // element offset of row r (valid) in its region, and which region
+  auto row_off = [&](int r, bool& local) -> size_t {
+    local = r >= nsel;
+    int slot = local_start + (r - nsel);        // local_start < window and r - nsel < n_local <= window
+    slot -= slot >= window ? window : 0;
+    return (size_t)(local ? slot : r) * kHeadDim;
+  };
+
+  for (int t = w; t < n_tiles; t += NW) {
+    const int tb = r0 + 16 * t;
+    // K rows for the B operand; rows past the chunk re-read its first row and are masked
+    const int kr = tb + p16;
+    const bool kvalid = kr < r1;
+    bool kloc;
+    const size_t koff = row_off(kvalid ? kr : r0, kloc);
+    const uint16_t* kp = (kloc ? kl : kb) + koff + 8 * g;
+    uint4 kx[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) kx[c] = *reinterpret_cast<const uint4*>(kp + 32 * c);
+    uint4 vx[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int vr = tb + 4 * k + g;
+      bool vloc;
+      const size_t voff = row_off(vr < r1 ? vr : r0, vloc);
+      vx[k] = *reinterpret_cast<const uint4*>((vloc ? vl : vb) + voff + 8 * p16);
+    }
+    __builtin_amdgcn_sched_barrier(0);   // keep the tile's loads ahead of their first use
+    attn_floatx4 sacc[NM];
+#pragma unroll
+    for (int mi = 0; mi < NM; ++mi) {
+      sacc[mi] = attn_floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        sacc[mi] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[mi][c], __builtin_bit_cast(attn_bf16x8, kx[c]), sacc[mi],
+                                                          0, 0, 0);
+    }
+    float sc[G];
+    bool grow = false;
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      const float x = sacc[j / 4][j % 4] * qscale;    // head j of row kr (regs i >= GA repeat heads)
+      sc[j] = kvalid ? x : -__builtin_inff();
+      grow |= sc[j] > m[j];
+    }
+    // rescale only when some row's score exceeds its head's running maximum
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        const float mn = fmaxf(m[j], row16_max(sc[j]));
+        const float corr = mn == -__builtin_inff() ? 1.f : __builtin_amdgcn_exp2f(m[j] - mn);
+        l[j] *= corr;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[j][e] *= corr;
+        m[j] = mn;
       }
     }
-    out[j * pstride + 2 + k] = aa;
-    if (k == 0) {
-      out[j * pstride + 0] = mm;
-      out[j * pstride + 1] = ll;
+    float pr[NM * 4];
+#pragma unroll
+    for (int j = 0; j < NM * 4; ++j) pr[j] = 0.f;
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      pr[j] = kvalid ? __builtin_amdgcn_exp2f(sc[j] - m[j]) : 0.f;
+      l[j] += pr[j];
+    }
+    // probabilities of row p16 to the lanes that hold its V row
+#pragma unroll
+    for (int mi = 0; mi < NM; ++mi)
+      s_p[w][mi][lane] = make_float4(pr[4 * mi], pr[4 * mi + 1], pr[4 * mi + 2], pr[4 * mi + 3]);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      float pk[NM * 4];
+#pragma unroll
+      for (int mi = 0; mi < NM; ++mi) {
+        const float4 f = s_p[w][mi][4 * k + g + 16 * g];
+        pk[4 * mi] = f.x; pk[4 * mi + 1] = f.y; pk[4 * mi + 2] = f.z; pk[4 * mi + 3] = f.w;
+      }
+      float vf[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t wv = (&vx[k].x)[i];
+        vf[2 * i] = __uint_as_float(wv << 16);
+        vf[2 * i + 1] = __uint_as_float(wv & 0xffff0000u);
+      }
+#pragma unroll
+      for (int j = 0; j < G; ++j)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[j][e] = fmaf(pk[j], vf[e], acc[j][e]);
     }
   }
+  // wave totals: l over the 16 row positions, acc over the 4 lane groups (m is wave-uniform)
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    l[j] = row16_sum(l[j]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      acc[j][e] += __shfl_xor(acc[j][e], 16, kWave);
+      acc[j][e] += __shfl_xor(acc[j][e], 32, kWave);
+    }
+  }
+  if (lane < 16) {
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      if (lane == 0) {
+        s_m[w][j] = m[j];
+        s_l[w][j] = l[j];
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s_acc[w][j][8 * p16 + e] = acc[j][e];
+    }
+  }
+  __syncthreads();
+  attn_block_merge<G, NW>(s_m, s_l, s_acc, tid, s, chunk, n_chunks, part, out, out_bf16, lse_out);
 }
 
 // One wave per (slice, head): merge the chunk partials.
@@ -620,10 +855,16 @@ size_t retrieve_ws_bytes(int64_t S, int units_cap, int budget, int G) {
   return align_up(cv.used, 256);
 }
 
-int attn_chunks(int buf_rows, int window) { return std::max(1, (buf_rows + window + kAttnChunk - 1) / kAttnChunk); }
+int attn_chunks(int64_t S, int buf_rows, int window) {
+  const int64_t cap = (int64_t)buf_rows + window;
+  const int64_t by_rows = std::max<int64_t>(1, (cap + kAttnMinRows - 1) / kAttnMinRows);
+  const int64_t by_grid = std::max<int64_t>(1, (kAttnTargetBlocks + S - 1) / S);
+  return (int)std::min(by_rows, by_grid);
+}
 
 size_t attn_ws_bytes(int64_t S, int G, int buf_rows, int window) {
-  return align_up((size_t)S * attn_chunks(buf_rows, window) * G * (2 + kHeadDim) * sizeof(float), 256);
+  const int nc = attn_chunks(S, buf_rows, window);
+  return nc == 1 ? 0 : align_up((size_t)S * nc * G * (2 + kHeadDim) * sizeof(float), 256);
 }
 
 }  // namespace
@@ -765,12 +1006,23 @@ extern "C" size_t louiskv_sparse_decode_attn_workspace_size(int64_t n_slices, in
 template <class T, int G>
 static void launch_attn_partial(const void* q, int n_kv_heads, float scale, const void* k_buf, const void* v_buf,
                                 const int32_t* n_sel, int buf_rows, const void* k_local, const void* v_local,
-                                int window, int local_start, int n_local, int n_chunks, float* part, unsigned grid,
-                                hipStream_t s) {
-  attn_partial_kernel<T, G><<<grid, 256, 0, s>>>(
+                                int window, int local_start, int n_local, int n_chunks, float* part, void* out,
+                                int out_bf16, float* lse_out, unsigned grid, hipStream_t s) {
+  attn_partial_kernel<T, G><<<grid, attn_waves<T, G>() * 64, 0, s>>>(
       static_cast<const T*>(q), n_kv_heads, scale, static_cast<const T*>(k_buf), static_cast<const T*>(v_buf), n_sel,
       buf_rows, static_cast<const T*>(k_local), static_cast<const T*>(v_local), window, local_start, n_local, n_chunks,
-      part);
+      part, out, out_bf16, lse_out);
+}
+
+template <int G>
+static void launch_attn_mfma(const void* q, int n_kv_heads, float scale, const void* k_buf, const void* v_buf,
+                             const int32_t* n_sel, int buf_rows, const void* k_local, const void* v_local, int window,
+                             int local_start, int n_local, int n_chunks, float* part, void* out, int out_bf16,
+                             float* lse_out, unsigned grid, hipStream_t s) {
+  attn_mfma_kernel<G><<<grid, attn_mfma_waves<G>() * 64, 0, s>>>(
+      static_cast<const uint16_t*>(q), n_kv_heads, scale, static_cast<const uint16_t*>(k_buf),
+      static_cast<const uint16_t*>(v_buf), n_sel, buf_rows, static_cast<const uint16_t*>(k_local),
+      static_cast<const uint16_t*>(v_local), window, local_start, n_local, n_chunks, part, out, out_bf16, lse_out);
 }
 
 extern "C" int louiskv_sparse_decode_attn(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads,
@@ -794,10 +1046,10 @@ extern "C" int louiskv_sparse_decode_attn(const void* q, int32_t dtype, int64_t 
   if (buf_rows < 0 || window < 0 || n_local < 0 || n_local > window || (window > 0 && (local_start < 0 || local_start >= window)))
     return fail(LOUISKV_ERR_SHAPE, "buf_rows=%d window=%d local_start=%d n_local=%d", buf_rows, window, local_start,
                 n_local);
-  const int n_chunks = attn_chunks(buf_rows, window);
+  const int n_chunks = attn_chunks(n_slices, buf_rows, window);
   if ((int64_t)n_slices * n_chunks > INT32_MAX) return fail(LOUISKV_ERR_SHAPE, "problem too large for one launch");
   const size_t need = attn_ws_bytes(n_slices, group_size, buf_rows, window);
-  if (!workspace || workspace_bytes < need)
+  if (need > 0 && (!workspace || workspace_bytes < need))
     return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
   float* part = static_cast<float*>(workspace);
   hipStream_t s = as_stream(stream);
@@ -806,13 +1058,16 @@ extern "C" int louiskv_sparse_decode_attn(const void* q, int32_t dtype, int64_t 
   const int lstart = window > 0 ? local_start : 0;
 #define LKV_ATTN(T, G) \
   launch_attn_partial<T, G>(q, n_kv_heads, scale, k_buf, v_buf, n_sel, buf_rows, k_local, v_local, win, lstart, n_local, \
-                            n_chunks, part, grid, s)
+                            n_chunks, part, out, out_dtype == LOUISKV_BF16, lse_out, grid, s)
+#define LKV_ATTN_MFMA(G) \
+  launch_attn_mfma<G>(q, n_kv_heads, scale, k_buf, v_buf, n_sel, buf_rows, k_local, v_local, win, lstart, n_local, \
+                      n_chunks, part, out, out_dtype == LOUISKV_BF16, lse_out, grid, s)
   if (dtype == LOUISKV_BF16) {
     switch (group_size) {
-      case 1: LKV_ATTN(uint16_t, 1); break;
-      case 2: LKV_ATTN(uint16_t, 2); break;
-      case 4: LKV_ATTN(uint16_t, 4); break;
-      default: LKV_ATTN(uint16_t, 8); break;
+      case 1: LKV_ATTN_MFMA(1); break;
+      case 2: LKV_ATTN_MFMA(2); break;
+      case 4: LKV_ATTN_MFMA(4); break;
+      default: LKV_ATTN_MFMA(8); break;
     }
   } else {
     switch (group_size) {
@@ -823,7 +1078,9 @@ extern "C" int louiskv_sparse_decode_attn(const void* q, int32_t dtype, int64_t 
     }
   }
 #undef LKV_ATTN
+#undef LKV_ATTN_MFMA
   LKV_CHECK_LAUNCH();
+  if (n_chunks == 1) return LOUISKV_OK;     // the blocks wrote the output themselves
   const int64_t rows = n_slices * group_size;
   const int cgrid = (int)((rows + 3) / 4);
   if (out_dtype == LOUISKV_BF16)

@@ -173,6 +173,12 @@ ATTN_CASES = [
     (torch.bfloat16, torch.float32, 2, 4, 8, 100, 32, 0, 0),
     (torch.float32, torch.float32, 3, 2, 1, 77, 16, 16, 5),
     (torch.bfloat16, torch.float32, 1, 8, 2, 4096, 128, 1, 127),
+    # 256 slices and more: one block per slice writes the output directly
+    (torch.bfloat16, torch.float32, 32, 8, 4, 2048, 128, 128, 17),
+    (torch.bfloat16, torch.bfloat16, 32, 8, 4, 700, 128, 50, 100),
+    (torch.float32, torch.float32, 64, 4, 4, 300, 64, 64, 3),
+    (torch.bfloat16, torch.float32, 64, 4, 8, 500, 32, 32, 31),
+    (torch.bfloat16, torch.float32, 40, 8, 4, 1000, 128, 0, 0),
 ]
 
 
