@@ -112,5 +112,7 @@ def test_validation_errors_return_before_launch(lib):
 def test_workspace_sizes_are_positive(lib):
     assert lib.louiskv_cluster_prefill_workspace_size(256, 32768, 128, 1024, 1) > 256 * 32768 * 4
     assert lib.louiskv_retrieve_workspace_size(256, 1024, 2048) > 0
-    assert lib.louiskv_sparse_decode_attn_workspace_size(256, 4, 128, 2048, 128) > 0
+    # one block per slice once there are enough slices: no split-KV partials
+    assert lib.louiskv_sparse_decode_attn_workspace_size(256, 4, 128, 2048, 128) == 0
+    assert lib.louiskv_sparse_decode_attn_workspace_size(8, 4, 128, 2048, 128) > 0
     assert lib.louiskv_cluster_prefill_workspace_size(0, 1, 128, 1, 1) == 0
