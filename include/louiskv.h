@@ -244,7 +244,8 @@ size_t louiskv_retrieve_workspace_size(int64_t n_slices, int32_t units_cap,
  * Algorithm 1 Retrieve with the group-consistent score of Appendix B, for the
  * slices whose group fired (all slices when fire is NULL):
  *   A_u = (1/g) sum_j softmax_u(q_j . reps_u * scale) over units 0..n_units-1
- *   (float64), units ranked by A descending, equal scores by lower unit id;
+ *   (float64), units ranked by A descending, equal scores by lower unit id
+ *   (scores within 2^-39 of each other count as equal);
  *   the longest prefix of the ranking whose total unit_size is <= budget is
  *   selected (Section 3.1 constraint |I_t| <= B); the rows of the selected
  *   units, in rank order and ascending inside a unit, are copied from the
@@ -263,7 +264,7 @@ size_t louiskv_retrieve_workspace_size(int64_t n_slices, int32_t units_cap,
  * n_sel        out [n_slices] int32, selected tokens (<= budget).
  * k_buf, v_buf out [n_slices][budget][d] dtype, rows 0..n_sel-1 written.
  * scores_out   out [n_slices][units_cap] float64 or NULL.
- * Requires 1 <= n_units <= 16384, budget >= 0.
+ * Requires 1 <= group_size <= 8, 1 <= n_units <= 8192, budget >= 0.
  */
 int louiskv_retrieve(const void* q, int32_t dtype, int64_t n_slices,
                      int32_t n_kv_heads, int32_t group_size, int32_t d, double scale,

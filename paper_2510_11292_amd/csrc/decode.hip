@@ -110,82 +110,129 @@ void store_decode_kernel(const T* __restrict__ k_new, const T* __restrict__ v_ne
 
 // ------------------------------------------------------------------ retrieve
 
-constexpr int kSelThreads = 512;
+#ifndef LKV_SEL_THREADS
+#define LKV_SEL_THREADS 512
+#endif
+#ifndef LKV_SEL_BATCH
+#define LKV_SEL_BATCH 4
+#endif
+constexpr int kSelThreads = LKV_SEL_THREADS;
+constexpr int kSelWaves = kSelThreads / 64;
+constexpr int kSelBatch = LKV_SEL_BATCH;   // unit quads per wave with loads in flight
+constexpr int kUnitIdBits = 13;       // kMaxUnits = 2^13
 
-__device__ __forceinline__ bool ranks_before(double sa, int ia, double sb, int ib) {
-  return sa > sb || (sa == sb && ia < ib);
+// Sum over the 16 lanes of a DPP row for a float64 (two 32-bit DPP moves per step).
+__device__ __forceinline__ double row16_sum_f64(double x) {
+#define LKV_DPP64(ctrl)                                                                                   \
+  {                                                                                                       \
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)__double2loint(x), ctrl, 0xF, 0xF, false);        \
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)__double2hiint(x), ctrl, 0xF, 0xF, false);        \
+    x += __hiloint2double(hi, lo);                                                                        \
+  }
+  LKV_DPP64(0xB1) LKV_DPP64(0x4E) LKV_DPP64(0x141) LKV_DPP64(0x140)
+#undef LKV_DPP64
+  return x;
 }
 
-// One block per fired slice: float64 group-consistent scores, LDS bitonic sort
-// by (score desc, id asc), prefix-stop under the budget, selected unit list and
-// the pool-row list that the gather kernel copies.
-template <class T>
+// Sort key of a unit: larger is ranked first.  The score (a non-negative
+// double, whose bit pattern orders like its value) keeps its top 51 bits and
+// the low 13 bits hold (kMaxUnits - 1 - id), so equal keys rank the lower id
+// first.  Scores closer than 2^-39 relative order by id.
+__device__ __forceinline__ uint64_t unit_key(double a, int id) {
+  const uint64_t bits = (uint64_t)__double_as_longlong(a);
+  return (bits >> kUnitIdBits << kUnitIdBits) | (uint64_t)(kMaxUnits - 1 - id);
+}
+__device__ __forceinline__ int key_unit(uint64_t k) { return kMaxUnits - 1 - (int)(k & (kMaxUnits - 1)); }
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
+  const int lo = __shfl_xor((int)(uint32_t)v, m, kWave);
+  const int hi = __shfl_xor((int)(uint32_t)(v >> 32), m, kWave);
+  return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+
+// Bitonic merge steps jj = jj0, jj0/2, .., 1 of stage k on one key per lane,
+// element index i = 64*chunk + lane; partners are in the same wave.
+__device__ __forceinline__ uint64_t bitonic_in_wave(uint64_t v, int i, int k, int jj0) {
+  for (int jj = jj0; jj > 0; jj >>= 1) {
+    const uint64_t o = shfl_xor_u64(v, jj);
+    const bool desc = (i & k) == 0;
+    const bool lower = (i & jj) == 0;
+    v = (desc == lower) ? (v > o ? v : o) : (v < o ? v : o);
+  }
+  return v;
+}
+
+// One block per fired slice: float64 group-consistent scores (Appendix B),
+// a descending bitonic sort of the unit keys, prefix-stop under the budget,
+// the selected unit list and the pool-row list that the gather kernel copies.
+//  pass 1  logits l_ju = q_j . rep_u * scale and their maxima M_j, 16 lanes
+//          per unit (lane sub holds dims 8*sub..+7 of the G queries in float64
+//          registers), kSelBatch quads of units in flight per wave; the unit
+//          sizes go to LDS.
+//  pass 2  e_ju = exp(l_ju - M_j) and Z_j = sum_u e_ju.
+//  pass 3  A_u = (1/g) sum_j e_ju / Z_j and the sort keys.
+//  sort    64-key chunks in registers for merge distances below 64 (no
+//          barrier), LDS steps with a barrier for the longer ones.
+template <class T, int G>
 __global__ __launch_bounds__(kSelThreads)
-void score_select_kernel(const T* __restrict__ q, int n_kv_heads, int group_size, double scale,
-                         const float* __restrict__ reps, const int32_t* __restrict__ unit_start,
-                         const int32_t* __restrict__ unit_size, int units_cap, int n_units, int budget,
-                         const uint8_t* __restrict__ fire, int32_t* __restrict__ sel_units,
-                         int32_t* __restrict__ n_sel_units, int32_t* __restrict__ n_sel,
-                         double* __restrict__ scores_out, double* __restrict__ logit_ws,
-                         int32_t* __restrict__ row_ws, int n_pad) {
+void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, const float* __restrict__ reps,
+                         const int32_t* __restrict__ unit_start, const int32_t* __restrict__ unit_size,
+                         int units_cap, int n_units, int budget, const uint8_t* __restrict__ fire,
+                         int32_t* __restrict__ sel_units, int32_t* __restrict__ n_sel_units,
+                         int32_t* __restrict__ n_sel, double* __restrict__ scores_out,
+                         double* __restrict__ logit_ws, int32_t* __restrict__ row_ws, int n_pad) {
   extern __shared__ __align__(16) char smem[];
-  double* s_sc = reinterpret_cast<double*>(smem);                // [n_pad]
-  int* s_id = reinterpret_cast<int*>(s_sc + n_pad);              // [n_pad]
-  __shared__ double s_q[kMaxGroupSize][kHeadDim];
-  __shared__ double s_red[kMaxGroupSize][kSelThreads / 64];
-  __shared__ double s_m[kMaxGroupSize], s_z[kMaxGroupSize];
-  __shared__ int s_ntake, s_nsel;
-  __shared__ int s_wsum[kSelThreads / 64];
+  uint64_t* s_key = reinterpret_cast<uint64_t*>(smem);            // [n_pad]
+  int* s_size = reinterpret_cast<int*>(s_key + n_pad);            // [n_pad] unit sizes by unit id
+  int* s_incl = s_size + n_pad;                                    // [n_pad] inclusive size sums by rank
+  __shared__ double s_rm[G][kSelWaves], s_rz[G][kSelWaves];
+  __shared__ double s_m[G], s_z[G];
+  __shared__ int s_ntake;
+  __shared__ int s_wsum[kSelWaves];
 
   const int64_t s = blockIdx.x;
   const int64_t grp = s / n_kv_heads;
   if (fire && !fire[grp]) return;
   const int kvh = (int)(s - grp * n_kv_heads);
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-  const int G = group_size;
-  const int n_q_heads = n_kv_heads * G;
-
-  for (int i = tid; i < G * kHeadDim; i += kSelThreads) {
-    const int j = i / kHeadDim, k = i % kHeadDim;
-    s_q[j][k] = load_as_f32(q, ((size_t)grp * n_q_heads + (size_t)kvh * G + j) * kHeadDim + k);
-  }
-  __syncthreads();
-
-  // pass 1: logits, 16 lanes per unit, each lane 8 dims
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int sub = lane & 15, quad = lane >> 4;
-  double mx[kMaxGroupSize];
+  const int n_q_heads = n_kv_heads * G;
+  const int32_t* us = unit_size + (size_t)s * units_cap;
+  for (int u = tid; u < n_units; u += kSelThreads) s_size[u] = max(us[u], 0);
+
+  double qd[G][8];
 #pragma unroll
-  for (int j = 0; j < kMaxGroupSize; ++j) mx[j] = -__builtin_inf();
+  for (int j = 0; j < G; ++j)
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      qd[j][e] = (double)load_as_f32(q, ((size_t)grp * n_q_heads + (size_t)kvh * G + j) * kHeadDim + 8 * sub + e);
+
+  // pass 1
+  double mx[G];
+#pragma unroll
+  for (int j = 0; j < G; ++j) mx[j] = -__builtin_inf();
   double* lg = logit_ws + (size_t)s * units_cap * G;
   const float* rs = reps + (size_t)s * units_cap * kHeadDim;
-  for (int u0 = w * 4; u0 < n_units; u0 += (kSelThreads / 64) * 4) {
-    const int u = u0 + quad;
-    double part[kMaxGroupSize];
+  for (int u0 = w * 4 * kSelBatch; u0 < n_units; u0 += kSelWaves * 4 * kSelBatch) {
+    float4 x[kSelBatch][2];
 #pragma unroll
-    for (int j = 0; j < kMaxGroupSize; ++j) part[j] = 0.0;
-    if (u < n_units) {
+    for (int i = 0; i < kSelBatch; ++i) {
+      const int u = min(u0 + 4 * i + quad, n_units - 1);   // past the end: re-read the last unit, unused
       const float4* r4 = reinterpret_cast<const float4*>(rs + (size_t)u * kHeadDim + 8 * sub);
-      const float4 x0 = r4[0], x1 = r4[1];
-      const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-#pragma unroll
-      for (int j = 0; j < kMaxGroupSize; ++j) {
-        if (j < G) {
-          double a = 0.0;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) a += s_q[j][8 * sub + e] * (double)x[e];
-          part[j] = a;
-        }
-      }
+      x[i][0] = r4[0];
+      x[i][1] = r4[1];
     }
 #pragma unroll
-    for (int j = 0; j < kMaxGroupSize; ++j) {
-      if (j < G) {
-        double a = part[j];
-        a += __shfl_xor(a, 8, kWave);
-        a += __shfl_xor(a, 4, kWave);
-        a += __shfl_xor(a, 2, kWave);
-        a += __shfl_xor(a, 1, kWave);
-        a *= scale;
+    for (int i = 0; i < kSelBatch; ++i) {
+      const int u = u0 + 4 * i + quad;
+      const double xd[8] = {x[i][0].x, x[i][0].y, x[i][0].z, x[i][0].w, x[i][1].x, x[i][1].y, x[i][1].z, x[i][1].w};
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        double a = 0.0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) a = fma(qd[j][e], xd[e], a);
+        a = row16_sum_f64(a) * scale;
         if (u < n_units) {
           mx[j] = fmax(mx[j], a);
           if (sub == j) lg[(size_t)u * G + j] = a;
@@ -194,96 +241,95 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, int group_size
     }
   }
 #pragma unroll
-  for (int j = 0; j < kMaxGroupSize; ++j) {
-    if (j < G) {
-      const double m = wave_max(mx[j]);
-      if (lane == 0) s_red[j][w] = m;
-    }
+  for (int j = 0; j < G; ++j) {
+    const double m = wave_max(mx[j]);
+    if (lane == 0) s_rm[j][w] = m;
   }
   __syncthreads();
   if (tid < G) {
-    double m = s_red[tid][0];
-    for (int q2 = 1; q2 < kSelThreads / 64; ++q2) m = fmax(m, s_red[tid][q2]);
+    double m = s_rm[tid][0];
+    for (int q2 = 1; q2 < kSelWaves; ++q2) m = fmax(m, s_rm[tid][q2]);
     s_m[tid] = m;
   }
   __syncthreads();
 
-  // pass 2: exponentials and their sums per head
-  double zs[kMaxGroupSize];
+  // pass 2: exponentials (kept in the logit workspace) and their sums per head
+  double zs[G];
 #pragma unroll
-  for (int j = 0; j < kMaxGroupSize; ++j) zs[j] = 0.0;
+  for (int j = 0; j < G; ++j) zs[j] = 0.0;
   for (int u = tid; u < n_units; u += kSelThreads) {
 #pragma unroll
-    for (int j = 0; j < kMaxGroupSize; ++j) {
-      if (j < G) {
-        const double e = exp(lg[(size_t)u * G + j] - s_m[j]);
-        lg[(size_t)u * G + j] = e;
-        zs[j] += e;
-      }
+    for (int j = 0; j < G; ++j) {
+      const double e = exp(lg[(size_t)u * G + j] - s_m[j]);
+      lg[(size_t)u * G + j] = e;
+      zs[j] += e;
     }
   }
 #pragma unroll
-  for (int j = 0; j < kMaxGroupSize; ++j) {
-    if (j < G) {
-      const double z = wave_sum(zs[j]);
-      if (lane == 0) s_red[j][w] = z;
-    }
+  for (int j = 0; j < G; ++j) {
+    const double z = wave_sum(zs[j]);
+    if (lane == 0) s_rz[j][w] = z;
   }
   __syncthreads();
   if (tid < G) {
     double z = 0.0;
-    for (int q2 = 0; q2 < kSelThreads / 64; ++q2) z += s_red[tid][q2];
+    for (int q2 = 0; q2 < kSelWaves; ++q2) z += s_rz[tid][q2];
     s_z[tid] = z;
   }
   __syncthreads();
 
-  // pass 3: averaged probabilities as sort keys
+  // pass 3: averaged probabilities and sort keys (padding keys 0 rank last)
   for (int u = tid; u < n_pad; u += kSelThreads) {
+    uint64_t key = 0;
     if (u < n_units) {
       double a = 0.0;
+#pragma unroll
       for (int j = 0; j < G; ++j) a += lg[(size_t)u * G + j] / s_z[j];
       a /= (double)G;
-      s_sc[u] = a;
-      s_id[u] = u;
+      key = unit_key(a, u);
       if (scores_out) scores_out[(size_t)s * units_cap + u] = a;
-    } else {
-      s_sc[u] = -1.0;
-      s_id[u] = 0x7fffffff;
     }
+    s_key[u] = key;
   }
   __syncthreads();
 
-  // bitonic sort, first in rank order
-  for (int k = 2; k <= n_pad; k <<= 1) {
-    for (int jj = k >> 1; jj > 0; jj >>= 1) {
+  // bitonic sort, descending keys (n_pad >= 64)
+  const int n_chunk = n_pad / 64;
+  for (int c = w; c < n_chunk; c += kSelWaves) {
+    const int i = 64 * c + lane;
+    uint64_t v = s_key[i];
+    for (int k = 2; k <= 64; k <<= 1) v = bitonic_in_wave(v, i, k, k >> 1);
+    s_key[i] = v;
+  }
+  __syncthreads();
+  for (int k = 128; k <= n_pad; k <<= 1) {
+    for (int jj = k >> 1; jj >= 64; jj >>= 1) {
       for (int i = tid; i < n_pad; i += kSelThreads) {
         const int p = i ^ jj;
         if (p > i) {
-          const bool up = (i & k) == 0;
-          const double si = s_sc[i], sp = s_sc[p];
-          const int ii = s_id[i], ip = s_id[p];
-          const bool swap = up ? ranks_before(sp, ip, si, ii) : ranks_before(si, ii, sp, ip);
-          if (swap) {
-            s_sc[i] = sp; s_sc[p] = si;
-            s_id[i] = ip; s_id[p] = ii;
+          const uint64_t a = s_key[i], b = s_key[p];
+          const bool desc = (i & k) == 0;
+          if (desc ? a < b : a > b) {
+            s_key[i] = b;
+            s_key[p] = a;
           }
         }
       }
       __syncthreads();
     }
+    for (int c = w; c < n_chunk; c += kSelWaves) {
+      const int i = 64 * c + lane;
+      s_key[i] = bitonic_in_wave(s_key[i], i, k, 32);
+    }
+    __syncthreads();
   }
 
   // prefix stop: count ranks whose inclusive size sum stays within the budget
-  if (tid == 0) { s_ntake = 0; s_nsel = 0; }
-  __syncthreads();
-  const int32_t* us = unit_size + (size_t)s * units_cap;
+  if (tid == 0) s_ntake = 0;
   int carry = 0;
-  double* incl_d = s_sc;   // reuse the score array as int storage for inclusive sums
-  int* incl = reinterpret_cast<int*>(incl_d);
   for (int base = 0; base < n_units; base += kSelThreads) {
     const int p = base + tid;
-    const int id = p < n_units ? s_id[p] : -1;
-    const int v = (id >= 0 && id < n_units) ? max(us[id], 0) : 0;
+    const int v = p < n_units ? s_size[key_unit(s_key[p])] : 0;
     int x = v;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
@@ -296,27 +342,26 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, int group_size
     for (int q2 = 0; q2 < w; ++q2) wp += s_wsum[q2];
     const long long inc = (long long)carry + wp + x;
     if (p < n_units) {
-      incl[p] = inc > 0x3fffffff ? 0x3fffffff : (int)inc;
+      s_incl[p] = inc > 0x3fffffff ? 0x3fffffff : (int)inc;   // sums past the budget are never read
       if (inc <= budget) atomicAdd(&s_ntake, 1);
     }
     int tot = 0;
-    for (int q2 = 0; q2 < kSelThreads / 64; ++q2) tot += s_wsum[q2];
+    for (int q2 = 0; q2 < kSelWaves; ++q2) tot += s_wsum[q2];
     carry = (int)std::min<long long>((long long)carry + tot, 0x3fffffff);
     __syncthreads();
   }
-  __syncthreads();
   const int ntake = s_ntake;
-  const int nsel = ntake > 0 ? incl[ntake - 1] : 0;
+  const int nsel = ntake > 0 ? s_incl[ntake - 1] : 0;
   const int32_t* ustart = unit_start + (size_t)s * units_cap;
   int32_t* rows = row_ws + (size_t)s * budget;
-  for (int p = tid; p < ntake; p += kSelThreads) {
-    const int u = s_id[p];
-    const bool real = u >= 0 && u < n_units;
-    sel_units[(size_t)s * units_cap + p] = real ? u : -1;
-    const int sz = real ? max(us[u], 0) : 0;
-    const int ex = incl[p] - sz;
-    const int st0 = real ? ustart[u] : 0;
-    for (int i = 0; i < sz; ++i) rows[ex + i] = st0 + i;
+  // one wave per selected unit: its rank in the list, then its rows in order
+  for (int p = w; p < ntake; p += kSelWaves) {
+    const int u = key_unit(s_key[p]);
+    const int sz = s_size[u];
+    const int ex = s_incl[p] - sz;
+    const int st0 = ustart[u];
+    if (lane == 0) sel_units[(size_t)s * units_cap + p] = u;
+    for (int i = lane; i < sz; i += kWave) rows[ex + i] = st0 + i;
   }
   if (tid == 0) {
     n_sel_units[s] = ntake;
@@ -965,18 +1010,32 @@ extern "C" int louiskv_retrieve(const void* q, int32_t dtype, int64_t n_slices, 
   Carver cv(workspace);
   double* logit_ws = cv.take<double>((size_t)n_slices * units_cap * kMaxGroupSize);
   int32_t* row_ws = cv.take<int32_t>((size_t)n_slices * std::max(budget, 1));
-  int n_pad = 1;
+  int n_pad = 64;                     // whole 64-key chunks for the in-wave sort steps
   while (n_pad < n_units) n_pad <<= 1;
-  const size_t lds = (size_t)n_pad * (sizeof(double) + sizeof(int));
+  const size_t lds = (size_t)n_pad * (sizeof(uint64_t) + 2 * sizeof(int));
   hipStream_t s = as_stream(stream);
-  if (dtype == LOUISKV_BF16)
-    score_select_kernel<uint16_t><<<(unsigned)n_slices, kSelThreads, lds, s>>>(
-        static_cast<const uint16_t*>(q), n_kv_heads, group_size, scale, reps, unit_start, unit_size, units_cap, n_units,
-        budget, fire, sel_units, n_sel_units, n_sel, scores_out, logit_ws, row_ws, n_pad);
-  else
-    score_select_kernel<float><<<(unsigned)n_slices, kSelThreads, lds, s>>>(
-        static_cast<const float*>(q), n_kv_heads, group_size, scale, reps, unit_start, unit_size, units_cap, n_units,
-        budget, fire, sel_units, n_sel_units, n_sel, scores_out, logit_ws, row_ws, n_pad);
+#define LKV_SEL(T, G)                                                                                                  \
+  score_select_kernel<T, G><<<(unsigned)n_slices, kSelThreads, lds, s>>>(                                              \
+      static_cast<const T*>(q), n_kv_heads, scale, reps, unit_start, unit_size, units_cap, n_units, budget, fire,    \
+      sel_units, n_sel_units, n_sel, scores_out, logit_ws, row_ws, n_pad)
+#define LKV_SEL_G(T)                  \
+  switch (group_size) {               \
+    case 1: LKV_SEL(T, 1); break;     \
+    case 2: LKV_SEL(T, 2); break;     \
+    case 3: LKV_SEL(T, 3); break;     \
+    case 4: LKV_SEL(T, 4); break;     \
+    case 5: LKV_SEL(T, 5); break;     \
+    case 6: LKV_SEL(T, 6); break;     \
+    case 7: LKV_SEL(T, 7); break;     \
+    default: LKV_SEL(T, 8); break;    \
+  }
+  if (dtype == LOUISKV_BF16) {
+    LKV_SEL_G(uint16_t)
+  } else {
+    LKV_SEL_G(float)
+  }
+#undef LKV_SEL_G
+#undef LKV_SEL
   LKV_CHECK_LAUNCH();
   if (budget > 0) {
     const int rpb = 128;

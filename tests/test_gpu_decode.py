@@ -118,6 +118,9 @@ RETRIEVE_CASES = [
     (torch.bfloat16, 2, 4, 1, 17, 100, 30),
     (torch.float32, 1, 8, 4, 50, 0, 10),          # zero budget: nothing selected
     (torch.bfloat16, 1, 8, 4, 64, 10 ** 6, 40),   # budget covers everything
+    (torch.bfloat16, 2, 8, 4, 4348, 4096, 40),    # 131K-prompt unit count: 8192-entry sort
+    (torch.float32, 2, 2, 3, 200, 300, 15),       # group size that is not a power of two
+    (torch.bfloat16, 1, 8, 4, 1, 64, 40),         # a single unit
 ]
 
 
