@@ -32,7 +32,9 @@
  * Pointers    Device pointers, except KV pools that the caller declares host
  *             resident (pool_on_host = 1): those must be pinned, device-mapped
  *             host memory (hipHostMalloc), which kernels read and write
- *             directly over the host link.
+ *             directly over the host link.  Such pools are checked with
+ *             hipPointerGetAttributes; any other pointer is refused with
+ *             LOUISKV_ERR_UNSUPPORTED before anything is launched.
  * Streams     `stream` is a hipStream_t (NULL = the legacy default stream).
  *             Arguments are validated on the host; the work is then enqueued
  *             and the call returns without synchronising.

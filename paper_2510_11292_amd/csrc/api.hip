@@ -24,6 +24,22 @@ int fail(int status, const char* fmt, ...) {
   return status;
 }
 
+int device_view_of_host_pool(const void* p, void** dev) {
+  if (!p) {
+    *dev = nullptr;
+    return LOUISKV_OK;
+  }
+  hipPointerAttribute_t attr;
+  const hipError_t e = hipPointerGetAttributes(&attr, p);
+  if (e != hipSuccess || attr.type != hipMemoryTypeHost || attr.devicePointer == nullptr) {
+    (void)hipGetLastError();   // clear the lookup's error so that later calls do not report it
+    return fail(LOUISKV_ERR_UNSUPPORTED,
+                "pool_on_host=1 needs pinned, device-mapped host memory (hipHostMalloc); %p is not", p);
+  }
+  *dev = attr.devicePointer;
+  return LOUISKV_OK;
+}
+
 }  // namespace louiskv
 
 extern "C" int louiskv_abi_version(void) { return LOUISKV_ABI_VERSION; }

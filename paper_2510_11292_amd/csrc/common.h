@@ -19,6 +19,9 @@ constexpr int kWave = 64;       // CDNA wavefront width
 void set_error(const char* fmt, ...);
 const char* g_err_text();
 int fail(int status, const char* fmt, ...);   // records the message, returns status
+// Device address of a pinned, device-mapped host allocation (NULL stays NULL);
+// LOUISKV_ERR_UNSUPPORTED for any other pointer.
+int device_view_of_host_pool(const void* p, void** dev);
 
 #define LKV_CHECK_HIP(expr)                                                        \
   do {                                                                             \

@@ -945,10 +945,11 @@ extern "C" int louiskv_segment_output(const void* k_new, const void* v_new, int3
                                       float* reps, int32_t* unit_start, int32_t* unit_size, int32_t units_cap,
                                       int32_t n_clusters, void* k_pool, void* v_pool, int64_t pool_rows,
                                       int32_t prompt_len, int32_t pool_on_host, void* stream) {
-  (void)pool_on_host;
   if (!k_new || !v_new || !k_local || !v_local) return fail(LOUISKV_ERR_NULL, "k_new, v_new, k_local, v_local required");
   int st = check_dtype(dtype);
   if (st) return st;
+  if (pool_on_host && ((st = device_view_of_host_pool(k_pool, &k_pool)) || (st = device_view_of_host_pool(v_pool, &v_pool))))
+    return st;
   if (d != kHeadDim) return fail(LOUISKV_ERR_UNSUPPORTED, "head dim %d not supported (only 128)", d);
   if (n_slices < 1 || n_slices > INT32_MAX) return fail(LOUISKV_ERR_SHAPE, "n_slices=%lld", (long long)n_slices);
   int32_t ev = -1, n_ev = 0;
@@ -989,12 +990,15 @@ extern "C" int louiskv_retrieve(const void* q, int32_t dtype, int64_t n_slices, 
                                 const uint8_t* fire, int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel,
                                 void* k_buf, void* v_buf, double* scores_out, void* workspace, size_t workspace_bytes,
                                 void* stream) {
-  (void)pool_on_host;
   if (!q || !reps || !unit_start || !unit_size || !k_pool || !v_pool || !sel_units || !n_sel_units || !n_sel || !k_buf ||
       !v_buf)
     return fail(LOUISKV_ERR_NULL, "a required pointer of louiskv_retrieve is NULL");
   int st = check_dtype(dtype);
   if (st) return st;
+  void* kpd = const_cast<void*>(k_pool);
+  void* vpd = const_cast<void*>(v_pool);
+  if (pool_on_host && ((st = device_view_of_host_pool(k_pool, &kpd)) || (st = device_view_of_host_pool(v_pool, &vpd))))
+    return st;
   if (d != kHeadDim) return fail(LOUISKV_ERR_UNSUPPORTED, "head dim %d not supported (only 128)", d);
   if (n_kv_heads < 1 || n_slices < 1 || n_slices % n_kv_heads != 0 || n_slices > INT32_MAX)
     return fail(LOUISKV_ERR_SHAPE, "n_slices=%lld must be a positive multiple of n_kv_heads=%d", (long long)n_slices,
@@ -1042,12 +1046,12 @@ extern "C" int louiskv_retrieve(const void* q, int32_t dtype, int64_t n_slices, 
     const int bps = (budget + rpb - 1) / rpb;
     const unsigned grid = (unsigned)(n_slices * bps);
     if (dtype == LOUISKV_BF16)
-      gather_kernel<uint16_t><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(k_pool),
-                                                   static_cast<const uint16_t*>(v_pool), pool_rows, row_ws, n_sel, fire,
+      gather_kernel<uint16_t><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(kpd),
+                                                   static_cast<const uint16_t*>(vpd), pool_rows, row_ws, n_sel, fire,
                                                    n_kv_heads, budget, bps, rpb, static_cast<uint16_t*>(k_buf),
                                                    static_cast<uint16_t*>(v_buf));
     else
-      gather_kernel<float><<<grid, 256, 0, s>>>(static_cast<const float*>(k_pool), static_cast<const float*>(v_pool),
+      gather_kernel<float><<<grid, 256, 0, s>>>(static_cast<const float*>(kpd), static_cast<const float*>(vpd),
                                                 pool_rows, row_ws, n_sel, fire, n_kv_heads, budget, bps, rpb,
                                                 static_cast<float*>(k_buf), static_cast<float*>(v_buf));
     LKV_CHECK_LAUNCH();

@@ -805,7 +805,8 @@ extern "C" int louiskv_cluster_prefill(const void* keys, int32_t dtype, int64_t 
   if (v_pool && !values) return fail(LOUISKV_ERR_NULL, "v_pool given without values");
   if ((k_pool || v_pool) && pool_rows < n_tokens)
     return fail(LOUISKV_ERR_SHAPE, "pool_rows=%lld < n_tokens=%d", (long long)pool_rows, n_tokens);
-  (void)pool_on_host;
+  if (pool_on_host && ((st = device_view_of_host_pool(k_pool, &k_pool)) || (st = device_view_of_host_pool(v_pool, &v_pool))))
+    return st;
   const Ws need = carve(nullptr, n_slices, n_tokens, n_clusters, dtype);
   if (!workspace || workspace_bytes < need.bytes)
     return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need.bytes, workspace_bytes);

@@ -227,14 +227,15 @@ def test_sparse_decode_attn(dtype, odt, G, H, g, BR, W, nl, ls):
 
 # ------------------------------------------------------------------ whole decode loop
 
-def _run_loop(wl, n_groups, steps, mode):
+def _run_loop(wl, n_groups, steps, mode, pool_on_host=False):
     """Prefill on the GPU, then `steps` decode steps on the GPU and in the
     oracle (started from the GPU's prefill state), step-locked."""
     from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
     data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(n_groups)], gen_len=steps)
     cfg = config_from_workload(wl, n_groups=n_groups, mode=mode, gen_len=steps)
     odt = torch.float32
-    eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, keep_scores=True, out_dtype=odt)
+    eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, pool_on_host=pool_on_host, keep_scores=True,
+                        out_dtype=odt)
     eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
     torch.cuda.synchronize()
     H, g = wl.n_kv_heads, wl.group_size
@@ -307,3 +308,33 @@ def test_decode_loop_bf16_with_evictions():
     wl = synth.get_workload("si-lo-16k").replace(prompt_len=2048, n_clusters=64, budget=512, name="si-lo-16k")
     st = _run_loop(wl, 2, 300, mode=1)
     assert st["fires"] > 40
+
+
+def test_decode_loop_host_pool():
+    """The same reduction with the KV pool in pinned host memory: prefill packs
+    into it, evictions append to it and retrieval gathers from it over the
+    host link."""
+    wl = synth.get_workload("host-131k").replace(prompt_len=2048, n_clusters=64, budget=512, name="host-131k")
+    st = _run_loop(wl, 1, 200, mode=1, pool_on_host=True)
+    assert st["fires"] > 20
+
+
+def test_host_pool_flag_rejects_device_memory():
+    """pool_on_host=1 with device tensors is refused on the host, before any launch."""
+    L = _L()
+    from paper_2510_11292_amd.louiskv import LouisKVError
+    S, U, B = 8, 16, 64
+    q = torch.zeros(1, 32, 128, dtype=torch.bfloat16, device=DEV)
+    reps = torch.zeros(S, U, 128, device=DEV)
+    sizes = torch.full((S, U), 4, dtype=torch.int32, device=DEV)
+    starts = (torch.arange(U, dtype=torch.int32, device=DEV) * 4).repeat(S, 1)
+    kp = torch.zeros(S, 4 * U, 128, dtype=torch.bfloat16, device=DEV)
+    kb = torch.full((S, B, 128), 7, dtype=torch.bfloat16, device=DEV)
+    sel = torch.zeros(S, U, dtype=torch.int32, device=DEV)
+    nsu = torch.full((S,), -5, dtype=torch.int32, device=DEV)
+    nsel = torch.full((S,), -5, dtype=torch.int32, device=DEV)
+    with pytest.raises(LouisKVError) as ei:
+        L.retrieve(q, 8, reps, starts, sizes, U, kp, kp, B, sel, nsu, nsel, kb, kb.clone(), pool_on_host=True)
+    assert ei.value.status == 4
+    torch.cuda.synchronize()
+    assert torch.all(nsel == -5) and torch.all(kb == 7)

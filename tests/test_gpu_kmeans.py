@@ -194,41 +194,3 @@ def test_empty_cluster_keeps_centroid():
         res = oracle.kmeans(to64(keys)[s], to_np(init)[s], 1, bf16_operand=True)
         assert np.array_equal(to_np(assign)[s], res.z)
         assert np.array_equal(to64(reps)[s], res.centroids)
-
-
-@pytest.mark.slow
-def test_cluster_prefill_full_shape_sampled():
-    """li-so-32k at full shape (256 slices, P=32768, C=1024, 10 iterations,
-    bf16), the launch the benchmark times.  Checked on sampled slices: the
-    tenth assignment against the oracle's argmin from the ninth centroids (on
-    sampled keys), and the tenth centroids as exact means of that assignment."""
-    L = _L()
-    wl = synth.get_workload("li-so-32k")
-    S, P, C = wl.n_slices, wl.prompt_len, wl.n_clusters
-    keys = torch.empty(S, P, 128, dtype=torch.bfloat16, device=DEV)
-    init = torch.empty(S, C, dtype=torch.int32)
-    for s in range(S):
-        layer, h = divmod(s, wl.n_kv_heads)
-        keys[s] = synth.slice_keys_values(wl, 0, layer, h, DEV, n_tokens=P)[0]
-        init[s] = synth.init_indices(wl, 0, layer, h)
-    init = init.to(DEV)
-    outs = {}
-    for iters in (wl.n_iters - 1, wl.n_iters):
-        reps = torch.empty(S, C, 128, device=DEV)
-        ustart = torch.empty(S, C, dtype=torch.int32, device=DEV)
-        usize = torch.empty_like(ustart)
-        assign = torch.empty(S, P, dtype=torch.int32, device=DEV)
-        perm = torch.empty_like(assign)
-        L.cluster_prefill(keys, C, iters, init, reps, ustart, usize, assign, perm)
-        torch.cuda.synchronize()
-        outs[iters] = (reps, assign, usize)
-    rng = np.random.default_rng(0)
-    for s in (0, 77, 255):
-        k64 = to64(keys[s])
-        c9 = to64(outs[wl.n_iters - 1][0][s])
-        z10 = to_np(outs[wl.n_iters][1][s])
-        sample = rng.choice(P, 2048, replace=False)
-        check_assignment(k64[sample], oracle.round_to_bf16(c9), z10[sample])
-        ref, cnt = oracle.kmeans_update(k64, z10, c9)
-        assert np.array_equal(to_np(outs[wl.n_iters][2][s]), cnt)
-        assert np.array_equal(to64(outs[wl.n_iters][0][s]), ref)
