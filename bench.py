@@ -32,6 +32,8 @@ if ROOT not in sys.path:
 METRIC = "prompt keys clustered/s; retrieval+sparse-attn decode steps/s at 32K ctx"
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "kmeans_assign_traffic_li-so-32k.md")
+ASSIGN_SOURCES = [os.path.join(ROOT, "paper_2510_11292_amd", "csrc", f) for f in ("kmeans.hip", "common.h")]
 
 
 def log(msg: str) -> None:
@@ -46,6 +48,80 @@ def make_inputs(wl, device):
     torch.cuda.synchronize()
     log(f"generated inputs for {data.n_slices} slices in {time.time() - t0:.1f}s")
     return data
+
+
+def sources_sha256(paths) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for p in paths:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per assignment launch from the committed counter summary
+    (FETCH_SIZE + WRITE_SIZE, calibrated on a plain copy), or None when the
+    summary is missing, covers another workload, or the kernel's sources have
+    changed since the counters were taken."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    fields = {}
+    with open(TRAFFIC_FILE) as f:
+        for line in f:
+            if line.startswith("- ") and ": " in line:
+                k, v = line[2:].split(": ", 1)
+                fields[k.strip()] = v.strip().strip("`")
+    try:
+        if fields.get("workload") != workload or fields.get("kernel_sources_sha256") != sources_sha256(ASSIGN_SOURCES):
+            return None
+        return float(fields["fetch_bytes_per_launch"]) + float(fields["write_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def time_attention(eng, wl, reps=20):
+    """Average duration of louiskv_sparse_decode_attn on the engine's final
+    decode state, timed with HIP events on the stream it is launched on."""
+    import torch
+    from paper_2510_11292_amd import louiskv as L
+    c = eng.cfg
+    t = c.gen_len - 1
+    _, _, n_local, local_start = L.window_info(t, c.window, c.seg_len)
+    q = torch.randn(c.n_groups, c.n_q_heads, c.head_dim, device=eng.device).to(eng.dtype)
+    st = torch.cuda.current_stream()
+
+    def launch():
+        L.sparse_decode_attn(q, c.n_kv_heads, eng.k_buf, eng.v_buf, eng.n_sel, eng.k_local, eng.v_local,
+                             local_start, n_local, eng.out, eng.lse, workspace=eng.ws_attn, stream=st)
+    for _ in range(3):
+        launch()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(st)
+    for _ in range(reps):
+        launch()
+    e1.record(st)
+    torch.cuda.synchronize()
+    sec = e0.elapsed_time(e1) / reps / 1e3
+    esz = eng.k_buf.element_size()
+    rows = int(eng.n_sel.sum()) + c.n_slices * n_local
+    nbytes = rows * 2 * c.head_dim * esz + 2 * c.n_groups * c.n_q_heads * c.head_dim * esz
+    return sec, nbytes
+
+
+def copy_calibration(mib: int):
+    """A streaming copy kernel of a known size (outside the timed region): the
+    reference for scaling the HBM byte counters.  torch.mul(x, 1) reads and
+    writes `mib` MiB once each (a same-type copy_ would become a DMA transfer
+    rather than a kernel)."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    log(f"copy calibration: 3 copy kernels of {mib} MiB")
 
 
 def cpu_baseline(wl, data, budget_s: float):
@@ -63,12 +139,17 @@ def cpu_baseline(wl, data, budget_s: float):
     def f64(t):
         return t.detach().float().cpu().numpy().astype(np.float64)
 
-    keys0 = f64(data.prompt_keys[0])
-    init0 = data.init_idx[0].cpu().numpy()
-    t0 = time.time()
-    res = oracle.kmeans(keys0, init0, wl.n_iters, bf16_operand=(wl.dtype == "bf16"))
-    t_km = time.time() - t0
-    keys_per_s = wl.prompt_len / t_km       # one slice; every slice costs the same
+    km_slices = 2
+    t_km = 0.0
+    for sl in range(km_slices):
+        keys_s = f64(data.prompt_keys[sl])
+        init_s = data.init_idx[sl].cpu().numpy()
+        t0 = time.time()
+        r = oracle.kmeans(keys_s, init_s, wl.n_iters, bf16_operand=(wl.dtype == "bf16"))
+        t_km += time.time() - t0
+        if sl == 0:
+            res = r
+    keys_per_s = km_slices * wl.prompt_len / t_km       # every slice costs the same
 
     # decode: one group, steps until the time budget is used
     H = wl.n_kv_heads
@@ -87,7 +168,7 @@ def cpu_baseline(wl, data, budget_s: float):
     return {
         "value": keys_per_s, "unit": "keys/s", "cores": int(blas_threads), "kind": "oracle",
         "decode_steps_per_s": steps_per_s,
-        "sample": (f"k-means of 1 of {wl.n_slices} slices ({wl.prompt_len} keys, C={wl.n_clusters}, "
+        "sample": (f"k-means of {km_slices} of {wl.n_slices} slices ({wl.prompt_len} keys, C={wl.n_clusters}, "
                    f"{wl.n_iters} iterations) in {t_km:.1f}s, scaled linearly; decode: {n} of {wl.gen_len} steps "
                    f"of 1 of {wl.n_groups} layer groups in {t_dec * n:.1f}s, scaled by the group count"),
         "host_cpus": len(os.sched_getaffinity(0)), "cpu": platform.processor() or platform.machine(),
@@ -105,6 +186,8 @@ def main() -> int:
                     help="seconds of oracle decode steps in the CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="launch decode steps one by one (no HIP graph)")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="after the run, copy this many MiB three times (counter calibration for profiles)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -186,6 +269,8 @@ def main() -> int:
     ms_per_step = wall / args.steps * 1e3
     fire_rate = float(eng.fire.float().mean())  # last step's groups (informational)
     achieved = flops_per_launch / t_assign / 1e12
+    t_attn, attn_bytes = time_attention(eng, wl)
+    traffic = measured_traffic(wl.name)
     out = {
         "metric": METRIC,
         "value": keys / t_pre,
@@ -212,12 +297,21 @@ def main() -> int:
         "roofline": {
             "kernel": "kmeans_assign (bf16 MFMA, fused argmin)",
             "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+            "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
             "avg_launch_ms": t_assign * 1e3, "flops_per_launch": flops_per_launch,
+        },
+        "attention_roofline": {
+            "kernel": "sparse_decode_attn (bf16 MFMA scores, all slices)", "bound": "hbm",
+            "achieved": attn_bytes / t_attn / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": attn_bytes / t_attn / 1e9 / PEAK_HBM_GBS, "avg_launch_us": t_attn * 1e6,
+            "bytes_per_launch": attn_bytes,
         },
     }
     log(f"prefill {t_pre * 1e3:.2f} ms, decode {t_dec * 1e3:.2f} ms ({wl.gen_len / t_dec:.0f} steps/s), "
         f"assign {t_assign * 1e3:.3f} ms/launch = {achieved:.1f} TFLOP/s, last-step fire rate {fire_rate:.2f}")
+    log(f"attention {t_attn * 1e6:.1f} us/launch = {attn_bytes / t_attn / 1e9:.0f} GB/s")
+    if args.copy_mib > 0:
+        copy_calibration(args.copy_mib)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(wl, data, args.cpu_budget_s)
