@@ -125,9 +125,10 @@ def copy_calibration(mib: int):
 
 
 def cpu_baseline(wl, data, budget_s: float):
-    """The oracle on a bounded sample: k-means of one slice and the decode loop
-    of one (sequence, layer) group for a prefix of the decode steps, scaled to
-    the whole workload."""
+    """The oracle on a bounded sample: k-means of the KV-head slices of one
+    (sequence, layer) group (full iterations, until the time budget is used),
+    then the decode loop of that group over the decode steps (until the budget
+    is used), each scaled to the whole workload."""
     import numpy as np
     import oracle
     try:
@@ -139,22 +140,22 @@ def cpu_baseline(wl, data, budget_s: float):
     def f64(t):
         return t.detach().float().cpu().numpy().astype(np.float64)
 
-    km_slices = 2
-    t_km = 0.0
-    for sl in range(km_slices):
-        keys_s = f64(data.prompt_keys[sl])
-        init_s = data.init_idx[sl].cpu().numpy()
-        t0 = time.time()
-        r = oracle.kmeans(keys_s, init_s, wl.n_iters, bf16_operand=(wl.dtype == "bf16"))
-        t_km += time.time() - t0
-        if sl == 0:
-            res = r
-    keys_per_s = km_slices * wl.prompt_len / t_km       # every slice costs the same
-
-    # decode: one group, steps until the time budget is used
     H = wl.n_kv_heads
-    results = [res] + [oracle.kmeans(f64(data.prompt_keys[h]), data.init_idx[h].cpu().numpy(), 1,
-                                     wl.dtype == "bf16") for h in range(1, H)]
+    bf16 = wl.dtype == "bf16"
+    results = []
+    t_km = 0.0
+    for h in range(H):
+        if results and t_km >= budget_s:
+            break
+        t0 = time.time()
+        results.append(oracle.kmeans(f64(data.prompt_keys[h]), data.init_idx[h].cpu().numpy(), wl.n_iters, bf16))
+        t_km += time.time() - t0
+    km_slices = len(results)
+    keys_per_s = km_slices * wl.prompt_len / t_km       # every slice costs the same
+    # heads past the budget start decoding from one Lloyd iteration (same unit count and sizes scale)
+    results += [oracle.kmeans(f64(data.prompt_keys[h]), data.init_idx[h].cpu().numpy(), 1, bf16)
+                for h in range(km_slices, H)]
+
     st = oracle.prefill_state_from_kmeans([f64(data.prompt_keys[h]) for h in range(H)],
                                           [f64(data.prompt_values[h]) for h in range(H)], results)
     dec = oracle.GroupDecoder(st, wl.n_q_heads, wl.budget, wl.window, wl.seg_len, wl.tau, "anchor")
@@ -183,7 +184,7 @@ def main() -> int:
     ap.add_argument("--workload", default="li-so-32k")
     ap.add_argument("--mode", default="anchor", choices=["anchor", "prev"])
     ap.add_argument("--cpu-budget-s", type=float, default=12.0,
-                    help="seconds of oracle decode steps in the CPU baseline sample")
+                    help="seconds of oracle k-means, and again of oracle decode steps, in the CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="launch decode steps one by one (no HIP graph)")
     ap.add_argument("--copy-mib", type=int, default=0,
