@@ -13,36 +13,86 @@ constexpr int kMaxUnits = 8192;
 
 // ------------------------------------------------------------------ boundary
 
-// One block of 4 waves per group.  Each wave takes heads w, w+4, ...; a head's
-// 128 dims are 2 per lane.  Cosines in float64.
+// Sum over the 16 lanes of a DPP row for a float64 (two 32-bit DPP moves per step).
+__device__ __forceinline__ double row16_sum_f64(double x) {
+#define LKV_DPP64(ctrl)                                                                                   \
+  {                                                                                                       \
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)__double2loint(x), ctrl, 0xF, 0xF, false);        \
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)__double2hiint(x), ctrl, 0xF, 0xF, false);        \
+    x += __hiloint2double(hi, lo);                                                                        \
+  }
+  LKV_DPP64(0xB1) LKV_DPP64(0x4E) LKV_DPP64(0x141) LKV_DPP64(0x140)
+#undef LKV_DPP64
+  return x;
+}
+
+// Eight consecutive elements of a row as float (16 B of bf16, 32 B of fp32).
+__device__ __forceinline__ void load_row8(const uint16_t* p, float* x) {
+  const uint4 v = *reinterpret_cast<const uint4*>(p);
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[2 * i] = __uint_as_float(w[i] << 16);
+    x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ void load_row8(const float* p, float* x) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+
+constexpr int kBndHeadsPerPass = 32;   // 16 lane groups x 2 heads, all loads issued together
+
+// One block of 4 waves per group.  16 lanes per head (lane sub holds dims
+// 8*sub..+7), each 16-lane group takes two heads per pass; the float64 dot
+// product and norms of a head are DPP row sums.  Cosines in float64.
 template <class T>
 __global__ __launch_bounds__(256)
 void boundary_kernel(const T* __restrict__ q, T* __restrict__ q_ref, int n_heads, double tau, int mode,
                      int first, double* __restrict__ r_out, uint8_t* __restrict__ fire_out) {
-  __shared__ double s_part[4];
+  __shared__ double s_part[16];
   __shared__ int s_fire;
   const int g = blockIdx.x;
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, sub = tid & 15, hg = tid >> 4;
   const size_t base = (size_t)g * n_heads * kHeadDim;
   double acc = 0.0;
   if (!first) {
-    for (int hh = w; hh < n_heads; hh += 4) {
-      const size_t o = base + (size_t)hh * kHeadDim + 2 * lane;
-      const double a0 = load_as_f32(q, o), a1 = load_as_f32(q, o + 1);
-      const double b0 = load_as_f32(q_ref, o), b1 = load_as_f32(q_ref, o + 1);
-      const double dot = wave_sum(a0 * b0 + a1 * b1);
-      const double na = wave_sum(a0 * a0 + a1 * a1);
-      const double nb = wave_sum(b0 * b0 + b1 * b1);
-      acc += dot / fmax(sqrt(na) * sqrt(nb), 1e-30);
+    for (int p = 0; p < n_heads; p += kBndHeadsPerPass) {
+      float a[2][8], b[2][8];
+      bool ok[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int h = p + hg + 16 * i;
+        ok[i] = h < n_heads;
+        const size_t o = base + (size_t)(ok[i] ? h : 0) * kHeadDim + 8 * sub;
+        load_row8(q + o, a[i]);
+        load_row8(q_ref + o, b[i]);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        double dot = 0.0, na = 0.0, nb = 0.0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          dot = fma((double)a[i][e], (double)b[i][e], dot);
+          na = fma((double)a[i][e], (double)a[i][e], na);
+          nb = fma((double)b[i][e], (double)b[i][e], nb);
+        }
+        dot = row16_sum_f64(dot);
+        na = row16_sum_f64(na);
+        nb = row16_sum_f64(nb);
+        if (ok[i]) acc += dot / fmax(sqrt(na) * sqrt(nb), 1e-30);
+      }
     }
   }
-  if (lane == 0) s_part[w] = acc;
+  if (sub == 0) s_part[hg] = acc;
   __syncthreads();
   if (tid == 0) {
     double r = __builtin_nan("");
     int fire = 1;
     if (!first) {
-      r = (s_part[0] + s_part[1] + s_part[2] + s_part[3]) / (double)n_heads;
+      r = 0.0;
+      for (int i = 0; i < 16; ++i) r += s_part[i];
+      r /= (double)n_heads;
       fire = r < tau ? 1 : 0;
     }
     if (r_out) r_out[g] = r;
@@ -120,19 +170,6 @@ constexpr int kSelThreads = LKV_SEL_THREADS;
 constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kSelBatch = LKV_SEL_BATCH;   // unit quads per wave with loads in flight
 constexpr int kUnitIdBits = 13;       // kMaxUnits = 2^13
-
-// Sum over the 16 lanes of a DPP row for a float64 (two 32-bit DPP moves per step).
-__device__ __forceinline__ double row16_sum_f64(double x) {
-#define LKV_DPP64(ctrl)                                                                                   \
-  {                                                                                                       \
-    const int lo = __builtin_amdgcn_update_dpp(0, (int)__double2loint(x), ctrl, 0xF, 0xF, false);        \
-    const int hi = __builtin_amdgcn_update_dpp(0, (int)__double2hiint(x), ctrl, 0xF, 0xF, false);        \
-    x += __hiloint2double(hi, lo);                                                                        \
-  }
-  LKV_DPP64(0xB1) LKV_DPP64(0x4E) LKV_DPP64(0x141) LKV_DPP64(0x140)
-#undef LKV_DPP64
-  return x;
-}
 
 // Sort key of a unit: larger is ranked first.  The score (a non-negative
 // double, whose bit pattern orders like its value) keeps its top 51 bits and
