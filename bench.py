@@ -8,13 +8,16 @@ retrieval at boundaries (budget 2048), window store and sparse attention for
 all layers):
 
   prefill   louiskv_cluster_prefill (k-means + cluster-packed K/V pool)
-  decode    128 x [boundary_check, retrieve, segment_output, sparse_decode_attn]
+  decode    128 x [boundary_check, retrieve_rows, segment_output,
+                   sparse_decode_attn_rows]   (KV_critical as a pool row list)
 
 Inputs are seeded synthetic tensors already resident in HBM before timing.
 Prints one JSON line: value = prompt keys clustered per second; the decode
-rate is reported alongside; `roofline` covers the dominant kernel (the MFMA
-k-means assignment), timed with HIP events on the stream it runs on;
-`cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
+rate is reported alongside, and the decode rate with the gathered (copied)
+KV_critical of louiskv_retrieve + louiskv_sparse_decode_attn after it;
+`roofline` covers the dominant kernel (the MFMA k-means assignment), timed
+with HIP events on the stream it runs on; `cpu_baseline` times the CPU oracle
+on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -92,8 +95,13 @@ def time_attention(eng, wl, reps=20):
     st = torch.cuda.current_stream()
 
     def launch():
-        L.sparse_decode_attn(q, c.n_kv_heads, eng.k_buf, eng.v_buf, eng.n_sel, eng.k_local, eng.v_local,
-                             local_start, n_local, eng.out, eng.lse, workspace=eng.ws_attn, stream=st)
+        if eng.zero_copy:
+            L.sparse_decode_attn_rows(q, c.n_kv_heads, eng.k_pool, eng.v_pool, eng.sel_rows, eng.n_sel,
+                                      eng.k_local, eng.v_local, local_start, n_local, eng.out, eng.lse,
+                                      workspace=eng.ws_attn, stream=st)
+        else:
+            L.sparse_decode_attn(q, c.n_kv_heads, eng.k_buf, eng.v_buf, eng.n_sel, eng.k_local, eng.v_local,
+                                 local_start, n_local, eng.out, eng.lse, workspace=eng.ws_attn, stream=st)
     for _ in range(3):
         launch()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -103,10 +111,49 @@ def time_attention(eng, wl, reps=20):
     e1.record(st)
     torch.cuda.synchronize()
     sec = e0.elapsed_time(e1) / reps / 1e3
-    esz = eng.k_buf.element_size()
-    rows = int(eng.n_sel.sum()) + c.n_slices * n_local
+    esz = eng.k_local.element_size()
+    n_sel = int(eng.n_sel.sum())
+    rows = n_sel + c.n_slices * n_local
     nbytes = rows * 2 * c.head_dim * esz + 2 * c.n_groups * c.n_q_heads * c.head_dim * esz
+    if eng.zero_copy:
+        nbytes += 4 * n_sel            # the row list
     return sec, nbytes
+
+
+def dense_decode_ms(wl, data, cfg, dtype, reps=2):
+    """Decode loop with the dense KV_critical (louiskv_retrieve gathers the
+    selected rows, louiskv_sparse_decode_attn reads the copies), as one HIP
+    graph after a fresh prefill; mean replay time in ms."""
+    import torch
+    from paper_2510_11292_amd.engine import LouisKVEngine
+    eng = LouisKVEngine(cfg, dtype, "cuda", pool_on_host=wl.pool_on_host, zero_copy=False)
+
+    def decode_all():
+        for t in range(wl.gen_len):
+            eng.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+    eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        decode_all()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    eng.t = 0
+    with torch.cuda.graph(graph):
+        decode_all()
+    ms = 0.0
+    for _ in range(reps):
+        eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ms += e0.elapsed_time(e1)
+    del graph, eng
+    torch.cuda.empty_cache()
+    return ms / reps
 
 
 def copy_calibration(mib: int):
@@ -272,6 +319,9 @@ def main() -> int:
     achieved = flops_per_launch / t_assign / 1e12
     t_attn, attn_bytes = time_attention(eng, wl)
     traffic = measured_traffic(wl.name)
+    dense_ms = None
+    if eng.zero_copy and not args.eager:
+        dense_ms = dense_decode_ms(wl, data, cfg, dtype)
     out = {
         "metric": METRIC,
         "value": keys / t_pre,
@@ -291,8 +341,10 @@ def main() -> int:
             "clusters": wl.n_clusters, "lloyd_iters": wl.n_iters, "decode_steps": wl.gen_len,
             "budget": wl.budget, "window": wl.window, "segment": wl.seg_len, "tau": wl.tau,
             "ref_mode": args.mode, "decode_launch": "eager" if graph is None else "hip_graph",
+            "kv_critical": "pool row list (zero-copy)" if eng.zero_copy else "gathered copy",
         },
         "decode_steps_per_s": wl.gen_len / t_dec,
+        "decode_steps_per_s_gathered_kv_critical": (wl.gen_len / (dense_ms / 1e3)) if dense_ms else None,
         "prefill_ms": t_pre * 1e3,
         "decode_ms": t_dec * 1e3,
         "roofline": {
@@ -302,7 +354,8 @@ def main() -> int:
             "avg_launch_ms": t_assign * 1e3, "flops_per_launch": flops_per_launch,
         },
         "attention_roofline": {
-            "kernel": "sparse_decode_attn (bf16 MFMA scores, all slices)", "bound": "hbm",
+            "kernel": ("sparse_decode_attn_rows" if eng.zero_copy else "sparse_decode_attn")
+            + " (bf16 MFMA scores, all slices)", "bound": "hbm",
             "achieved": attn_bytes / t_attn / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": attn_bytes / t_attn / 1e9 / PEAK_HBM_GBS, "avg_launch_us": t_attn * 1e6,
             "bytes_per_launch": attn_bytes,
@@ -311,6 +364,8 @@ def main() -> int:
     log(f"prefill {t_pre * 1e3:.2f} ms, decode {t_dec * 1e3:.2f} ms ({wl.gen_len / t_dec:.0f} steps/s), "
         f"assign {t_assign * 1e3:.3f} ms/launch = {achieved:.1f} TFLOP/s, last-step fire rate {fire_rate:.2f}")
     log(f"attention {t_attn * 1e6:.1f} us/launch = {attn_bytes / t_attn / 1e9:.0f} GB/s")
+    if dense_ms:
+        log(f"decode with the gathered KV_critical: {dense_ms:.2f} ms ({wl.gen_len / (dense_ms / 1e3):.0f} steps/s)")
     if args.copy_mib > 0:
         copy_calibration(args.copy_mib)
     if not args.no_cpu_baseline:

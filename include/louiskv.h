@@ -20,7 +20,10 @@
  *                                                   (Appendix B equation for A_t;
  *                                                    Section 3.1 budget;
  *                                                    Algorithm 1 Retrieve)
+ *   louiskv_retrieve_rows       the same selection as a list of pool rows
+ *                               (zero-copy KV_critical for device pools)
  *   louiskv_sparse_decode_attn  attention over [KV_critical : KV_local]
+ *   louiskv_sparse_decode_attn_rows  the same over listed pool rows
  *                                                   (Section 3.1 attention;
  *                                                    Algorithm 1 decode loop)
  *
@@ -278,6 +281,32 @@ int louiskv_retrieve(const void* q, int32_t dtype, int64_t n_slices,
                      void* k_buf, void* v_buf, double* scores_out,
                      void* workspace, size_t workspace_bytes, void* stream);
 
+size_t louiskv_retrieve_rows_workspace_size(int64_t n_slices, int32_t units_cap);
+
+/*
+ * louiskv_retrieve without the copy (zero-copy retrieval for pools in device
+ * memory): the same scores, ranking and prefix-stop selection (Appendix B;
+ * Section 3.1 budget; Algorithm 1 Retrieve), but instead of gathering K/V rows
+ * into KV_critical it writes, per fired slice, the list of the selected pool
+ * rows (rank order, ascending inside a unit).  louiskv_sparse_decode_attn_rows
+ * then reads those rows from the pool directly: KV_critical becomes a list of
+ * row indices rather than a copy.  Slices whose group did not fire keep their
+ * previous list.
+ *
+ * sel_rows   out [n_slices][budget] int32, entries 0..n_sel-1 written
+ *            (may be NULL when budget == 0).
+ * Other arguments as louiskv_retrieve; the workspace is
+ * louiskv_retrieve_rows_workspace_size() bytes.
+ */
+int louiskv_retrieve_rows(const void* q, int32_t dtype, int64_t n_slices,
+                          int32_t n_kv_heads, int32_t group_size, int32_t d, double scale,
+                          const float* reps, const int32_t* unit_start,
+                          const int32_t* unit_size, int32_t units_cap, int32_t n_units,
+                          int32_t budget, const uint8_t* fire, int32_t* sel_units,
+                          int32_t* n_sel_units, int32_t* n_sel, int32_t* sel_rows,
+                          double* scores_out, void* workspace, size_t workspace_bytes,
+                          void* stream);
+
 size_t louiskv_sparse_decode_attn_workspace_size(int64_t n_slices, int32_t group_size,
                                                  int32_t d, int32_t buf_rows,
                                                  int32_t window);
@@ -307,6 +336,30 @@ int louiskv_sparse_decode_attn(const void* q, int32_t dtype, int64_t n_slices,
                                int32_t window, int32_t local_start, int32_t n_local,
                                void* out, int32_t out_dtype, float* lse_out,
                                void* workspace, size_t workspace_bytes, void* stream);
+
+size_t louiskv_sparse_decode_attn_rows_workspace_size(int64_t n_slices, int32_t group_size,
+                                                      int32_t d, int32_t budget,
+                                                      int32_t window);
+
+/*
+ * louiskv_sparse_decode_attn over rows read straight from the pool: the
+ * attended rows are the pool rows sel_rows[s][0..n_sel[s]-1] (as written by
+ * louiskv_retrieve_rows) followed by the live rows of the local ring.  Same
+ * arithmetic, layouts and outputs as louiskv_sparse_decode_attn.
+ *
+ * k_pool, v_pool  [n_slices][pool_rows][d] dtype, device memory.
+ * sel_rows   [n_slices][budget] int32; entries are clamped into [0, pool_rows).
+ * n_sel      [n_slices] int32 (<= budget).
+ */
+int louiskv_sparse_decode_attn_rows(const void* q, int32_t dtype, int64_t n_slices,
+                                    int32_t n_kv_heads, int32_t group_size, int32_t d,
+                                    float scale, const void* k_pool, const void* v_pool,
+                                    int64_t pool_rows, const int32_t* sel_rows,
+                                    const int32_t* n_sel, int32_t budget,
+                                    const void* k_local, const void* v_local,
+                                    int32_t window, int32_t local_start, int32_t n_local,
+                                    void* out, int32_t out_dtype, float* lse_out,
+                                    void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -441,6 +441,17 @@ void gather_kernel(const T* __restrict__ k_pool, const T* __restrict__ v_pool, i
 
 // ------------------------------------------------------------------ attention
 
+// Zero-copy retrieval: the selected rows are read straight from the pool
+// through the slice's row list.  A block copies its chunk's entries
+// [lo, hi) of the list into LDS, clamped into the pool so that a malformed
+// list cannot address memory outside it, and waits for the copy.
+__device__ __forceinline__ void stage_row_list(const int32_t* __restrict__ list, int lo, int hi, int64_t src_rows,
+                                               int* s_rows, int tid, int n_threads) {
+  for (int i = lo + tid; i < hi; i += n_threads)
+    s_rows[i - lo] = (int)min<int64_t>(max(list[i], 0), src_rows - 1);
+  __syncthreads();
+}
+
 // One block of 16 waves per CU (8 waves where the register footprint needs
 // more than 128 VGPRs).  A slice's rows go to one block when there are enough
 // slices to fill the chip; otherwise they are cut into n_chunks equal ranges
@@ -559,13 +570,15 @@ __device__ __forceinline__ void attn_block_merge(const float (*s_m)[G], const fl
 // some lane's maximum grows (a wave-uniform branch with per-lane selects).
 // With one chunk the block writes the normalised output (and lse); otherwise
 // it writes (m, l, acc[128]) per head, m in base 2, for the merge kernel.
-template <class T, int G>
+template <class T, int G, bool kIdx>
 __global__ __launch_bounds__((attn_waves<T, G>() * 64))
 void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, const T* __restrict__ k_buf,
                          const T* __restrict__ v_buf, const int32_t* __restrict__ n_sel, int buf_rows,
+                         const int32_t* __restrict__ rows, int64_t src_rows,
                          const T* __restrict__ k_local, const T* __restrict__ v_local, int window, int local_start,
                          int n_local, int n_chunks, float* __restrict__ part, void* __restrict__ out, int out_bf16,
                          float* __restrict__ lse_out) {
+  extern __shared__ int s_rows[];     // kIdx: the chunk's entries of the row list
   constexpr int R = attn_rows_in_flight<T, G>();
   constexpr int kAttnWaves = attn_waves<T, G>();
   constexpr int kAttnThreads = kAttnWaves * 64;
@@ -596,10 +609,11 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[j][e] = 0.f;
   }
-  const T* kb = k_buf + (size_t)s * buf_rows * kHeadDim + 8 * sub;
-  const T* vb = v_buf + (size_t)s * buf_rows * kHeadDim + 8 * sub;
+  const T* kb = k_buf + (size_t)s * src_rows * kHeadDim + 8 * sub;
+  const T* vb = v_buf + (size_t)s * src_rows * kHeadDim + 8 * sub;
   const T* kl = k_local + (size_t)s * window * kHeadDim + 8 * sub;
   const T* vl = v_local + (size_t)s * window * kHeadDim + 8 * sub;
+  if (kIdx) stage_row_list(rows + (size_t)s * buf_rows, r0, min(r1, nsel), src_rows, s_rows, tid, kAttnThreads);
   // Issue the loads of pass ps; rows past the chunk re-read its first row and
   // are masked.
   auto load_pass = [&](int ps, Raw8<T>* kx, Raw8<T>* vx, bool* valid) {
@@ -612,7 +626,7 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
       const T* kp;
       const T* vp;
       if (rr < nsel) {
-        off = (size_t)rr * kHeadDim;
+        off = (size_t)(kIdx ? s_rows[rr - r0] : rr) * kHeadDim;
         kp = kb; vp = vb;
       } else {
         int slot = local_start + (rr - nsel);      // local_start < window and rr - nsel < n_local <= window
@@ -731,13 +745,15 @@ constexpr int attn_mfma_waves() {
 // row (lane owns dims 8(l%16)..+7, rows 4k + l/16 of the tile for k = 0..3),
 // where P V accumulates in float32 on the vector ALUs.  Output and partials as
 // attn_partial_kernel.
-template <int G>
+template <int G, bool kIdx>
 __global__ __launch_bounds__((attn_mfma_waves<G>() * 64))
 void attn_mfma_kernel(const uint16_t* __restrict__ q, int n_kv_heads, float scale, const uint16_t* __restrict__ k_buf,
                       const uint16_t* __restrict__ v_buf, const int32_t* __restrict__ n_sel, int buf_rows,
+                      const int32_t* __restrict__ rows, int64_t src_rows,
                       const uint16_t* __restrict__ k_local, const uint16_t* __restrict__ v_local, int window,
                       int local_start, int n_local, int n_chunks, float* __restrict__ part, void* __restrict__ out,
                       int out_bf16, float* __restrict__ lse_out) {
+  extern __shared__ int s_rows[];     // kIdx: the chunk's entries of the row list
   constexpr int NW = attn_mfma_waves<G>();
   constexpr int NM = G == 8 ? 2 : 1;        // matrix ops per k-chunk, 4 heads each
   constexpr int GA = G < 4 ? G : 4;         // distinct heads in one op's output
@@ -774,16 +790,18 @@ void attn_mfma_kernel(const uint16_t* __restrict__ q, int n_kv_heads, float scal
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[j][e] = 0.f;
   }
-  const uint16_t* kb = k_buf + (size_t)s * buf_rows * kHeadDim;
-  const uint16_t* vb = v_buf + (size_t)s * buf_rows * kHeadDim;
+  const uint16_t* kb = k_buf + (size_t)s * src_rows * kHeadDim;
+  const uint16_t* vb = v_buf + (size_t)s * src_rows * kHeadDim;
   const uint16_t* kl = k_local + (size_t)s * window * kHeadDim;
   const uint16_t* vl = v_local + (size_t)s * window * kHeadDim;
+  if (kIdx) stage_row_list(rows + (size_t)s * buf_rows, r0, min(r1, nsel), src_rows, s_rows, tid, NW * 64);
   // element offset of row r (valid) in its region, and which region
   auto row_off = [&](int r, bool& local) -> size_t {
     local = r >= nsel;
     int slot = local_start + (r - nsel);        // local_start < window and r - nsel < n_local <= window
     slot -= slot >= window ? window : 0;
-    return (size_t)(local ? slot : r) * kHeadDim;
+    const int sel = kIdx ? s_rows[max(0, min(r, nsel - 1) - r0)] : r;   // index stays inside the staged chunk
+    return (size_t)(local ? slot : sel) * kHeadDim;
   };
 
   for (int t = w; t < n_tiles; t += NW) {
@@ -937,15 +955,19 @@ size_t retrieve_ws_bytes(int64_t S, int units_cap, int budget, int G) {
   return align_up(cv.used, 256);
 }
 
-int attn_chunks(int64_t S, int buf_rows, int window) {
+constexpr int kAttnMaxListRows = 8192;   // row-list entries one block stages in LDS (32 KB)
+
+int attn_chunks(int64_t S, int buf_rows, int window, bool indexed) {
   const int64_t cap = (int64_t)buf_rows + window;
   const int64_t by_rows = std::max<int64_t>(1, (cap + kAttnMinRows - 1) / kAttnMinRows);
   const int64_t by_grid = std::max<int64_t>(1, (kAttnTargetBlocks + S - 1) / S);
-  return (int)std::min(by_rows, by_grid);
+  int64_t nc = std::min(by_rows, by_grid);
+  if (indexed) nc = std::max<int64_t>(nc, (cap + kAttnMaxListRows - 1) / kAttnMaxListRows);
+  return (int)nc;
 }
 
-size_t attn_ws_bytes(int64_t S, int G, int buf_rows, int window) {
-  const int nc = attn_chunks(S, buf_rows, window);
+size_t attn_ws_bytes(int64_t S, int G, int buf_rows, int window, bool indexed) {
+  const int nc = attn_chunks(S, buf_rows, window, indexed);
   return nc == 1 ? 0 : align_up((size_t)S * nc * G * (2 + kHeadDim) * sizeof(float), 256);
 }
 
@@ -1020,45 +1042,26 @@ extern "C" size_t louiskv_retrieve_workspace_size(int64_t n_slices, int32_t unit
   return retrieve_ws_bytes(n_slices, units_cap, budget, kMaxGroupSize);
 }
 
-extern "C" int louiskv_retrieve(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads, int32_t group_size,
-                                int32_t d, double scale, const float* reps, const int32_t* unit_start,
-                                const int32_t* unit_size, int32_t units_cap, int32_t n_units, const void* k_pool,
-                                const void* v_pool, int64_t pool_rows, int32_t pool_on_host, int32_t budget,
-                                const uint8_t* fire, int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel,
-                                void* k_buf, void* v_buf, double* scores_out, void* workspace, size_t workspace_bytes,
-                                void* stream) {
-  if (!q || !reps || !unit_start || !unit_size || !k_pool || !v_pool || !sel_units || !n_sel_units || !n_sel || !k_buf ||
-      !v_buf)
-    return fail(LOUISKV_ERR_NULL, "a required pointer of louiskv_retrieve is NULL");
-  int st = check_dtype(dtype);
-  if (st) return st;
-  void* kpd = const_cast<void*>(k_pool);
-  void* vpd = const_cast<void*>(v_pool);
-  if (pool_on_host && ((st = device_view_of_host_pool(k_pool, &kpd)) || (st = device_view_of_host_pool(v_pool, &vpd))))
-    return st;
-  if (d != kHeadDim) return fail(LOUISKV_ERR_UNSUPPORTED, "head dim %d not supported (only 128)", d);
-  if (n_kv_heads < 1 || n_slices < 1 || n_slices % n_kv_heads != 0 || n_slices > INT32_MAX)
-    return fail(LOUISKV_ERR_SHAPE, "n_slices=%lld must be a positive multiple of n_kv_heads=%d", (long long)n_slices,
-                n_kv_heads);
-  if (group_size < 1 || group_size > kMaxGroupSize)
-    return fail(LOUISKV_ERR_UNSUPPORTED, "group_size=%d must be in [1, %d]", group_size, kMaxGroupSize);
+namespace louiskv {
+namespace {
+
+// Arguments shared by both retrieval entry points, then the scoring/selection
+// kernel, whose pool-row list goes to `rows` ([n_slices][budget]).
+int score_and_select(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads, int32_t group_size, int32_t d,
+                     double scale, const float* reps, const int32_t* unit_start, const int32_t* unit_size,
+                     int32_t units_cap, int32_t n_units, int32_t budget, const uint8_t* fire, int32_t* sel_units,
+                     int32_t* n_sel_units, int32_t* n_sel, int32_t* rows, double* scores_out, double* logit_ws,
+                     hipStream_t s) {
   if (n_units < 1 || n_units > units_cap || n_units > kMaxUnits)
     return fail(LOUISKV_ERR_SHAPE, "n_units=%d must be in [1, min(units_cap=%d, %d)]", n_units, units_cap, kMaxUnits);
-  if (budget < 0) return fail(LOUISKV_ERR_SHAPE, "budget=%d < 0", budget);
-  const size_t need = retrieve_ws_bytes(n_slices, units_cap, budget, kMaxGroupSize);
-  if (!workspace || workspace_bytes < need)
-    return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
-  Carver cv(workspace);
-  double* logit_ws = cv.take<double>((size_t)n_slices * units_cap * kMaxGroupSize);
-  int32_t* row_ws = cv.take<int32_t>((size_t)n_slices * std::max(budget, 1));
   int n_pad = 64;                     // whole 64-key chunks for the in-wave sort steps
   while (n_pad < n_units) n_pad <<= 1;
   const size_t lds = (size_t)n_pad * (sizeof(uint64_t) + 2 * sizeof(int));
-  hipStream_t s = as_stream(stream);
+  (void)d;
 #define LKV_SEL(T, G)                                                                                                  \
   score_select_kernel<T, G><<<(unsigned)n_slices, kSelThreads, lds, s>>>(                                              \
       static_cast<const T*>(q), n_kv_heads, scale, reps, unit_start, unit_size, units_cap, n_units, budget, fire,    \
-      sel_units, n_sel_units, n_sel, scores_out, logit_ws, row_ws, n_pad)
+      sel_units, n_sel_units, n_sel, scores_out, logit_ws, rows, n_pad)
 #define LKV_SEL_G(T)                  \
   switch (group_size) {               \
     case 1: LKV_SEL(T, 1); break;     \
@@ -1078,6 +1081,58 @@ extern "C" int louiskv_retrieve(const void* q, int32_t dtype, int64_t n_slices, 
 #undef LKV_SEL_G
 #undef LKV_SEL
   LKV_CHECK_LAUNCH();
+  return LOUISKV_OK;
+}
+
+int check_retrieve_common(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads, int32_t group_size,
+                          int32_t d, const float* reps, const int32_t* unit_start, const int32_t* unit_size,
+                          int32_t units_cap, int32_t n_units, int32_t budget, const int32_t* sel_units,
+                          const int32_t* n_sel_units, const int32_t* n_sel) {
+  if (!q || !reps || !unit_start || !unit_size || !sel_units || !n_sel_units || !n_sel)
+    return fail(LOUISKV_ERR_NULL, "q, reps, unit tables and selection outputs are required");
+  int st = check_dtype(dtype);
+  if (st) return st;
+  if (d != kHeadDim) return fail(LOUISKV_ERR_UNSUPPORTED, "head dim %d not supported (only 128)", d);
+  if (n_kv_heads < 1 || n_slices < 1 || n_slices % n_kv_heads != 0 || n_slices > INT32_MAX)
+    return fail(LOUISKV_ERR_SHAPE, "n_slices=%lld must be a positive multiple of n_kv_heads=%d", (long long)n_slices,
+                n_kv_heads);
+  if (group_size < 1 || group_size > kMaxGroupSize)
+    return fail(LOUISKV_ERR_UNSUPPORTED, "group_size=%d must be in [1, %d]", group_size, kMaxGroupSize);
+  if (n_units < 1 || n_units > units_cap || n_units > kMaxUnits)
+    return fail(LOUISKV_ERR_SHAPE, "n_units=%d must be in [1, min(units_cap=%d, %d)]", n_units, units_cap, kMaxUnits);
+  if (budget < 0) return fail(LOUISKV_ERR_SHAPE, "budget=%d < 0", budget);
+  return LOUISKV_OK;
+}
+
+}  // namespace
+}  // namespace louiskv
+
+extern "C" int louiskv_retrieve(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads, int32_t group_size,
+                                int32_t d, double scale, const float* reps, const int32_t* unit_start,
+                                const int32_t* unit_size, int32_t units_cap, int32_t n_units, const void* k_pool,
+                                const void* v_pool, int64_t pool_rows, int32_t pool_on_host, int32_t budget,
+                                const uint8_t* fire, int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel,
+                                void* k_buf, void* v_buf, double* scores_out, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  int st = check_retrieve_common(q, dtype, n_slices, n_kv_heads, group_size, d, reps, unit_start, unit_size, units_cap,
+                                 n_units, budget, sel_units, n_sel_units, n_sel);
+  if (st) return st;
+  if (!k_pool || !v_pool || !k_buf || !v_buf) return fail(LOUISKV_ERR_NULL, "k_pool, v_pool, k_buf, v_buf required");
+  void* kpd = const_cast<void*>(k_pool);
+  void* vpd = const_cast<void*>(v_pool);
+  if (pool_on_host && ((st = device_view_of_host_pool(k_pool, &kpd)) || (st = device_view_of_host_pool(v_pool, &vpd))))
+    return st;
+  const size_t need = retrieve_ws_bytes(n_slices, units_cap, budget, kMaxGroupSize);
+  if (!workspace || workspace_bytes < need)
+    return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  Carver cv(workspace);
+  double* logit_ws = cv.take<double>((size_t)n_slices * units_cap * kMaxGroupSize);
+  int32_t* row_ws = cv.take<int32_t>((size_t)n_slices * std::max(budget, 1));
+  hipStream_t s = as_stream(stream);
+  if ((st = score_and_select(q, dtype, n_slices, n_kv_heads, group_size, d, scale, reps, unit_start, unit_size,
+                             units_cap, n_units, budget, fire, sel_units, n_sel_units, n_sel, row_ws, scores_out,
+                             logit_ws, s)))
+    return st;
   if (budget > 0) {
     const int rpb = 128;
     const int bps = (budget + rpb - 1) / rpb;
@@ -1096,43 +1151,115 @@ extern "C" int louiskv_retrieve(const void* q, int32_t dtype, int64_t n_slices, 
   return LOUISKV_OK;
 }
 
+extern "C" size_t louiskv_retrieve_rows_workspace_size(int64_t n_slices, int32_t units_cap) {
+  if (n_slices < 1 || units_cap < 1) return 0;
+  return align_up((size_t)n_slices * units_cap * kMaxGroupSize * sizeof(double), 256);
+}
+
+extern "C" int louiskv_retrieve_rows(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads,
+                                     int32_t group_size, int32_t d, double scale, const float* reps,
+                                     const int32_t* unit_start, const int32_t* unit_size, int32_t units_cap,
+                                     int32_t n_units, int32_t budget, const uint8_t* fire, int32_t* sel_units,
+                                     int32_t* n_sel_units, int32_t* n_sel, int32_t* sel_rows, double* scores_out,
+                                     void* workspace, size_t workspace_bytes, void* stream) {
+  int st = check_retrieve_common(q, dtype, n_slices, n_kv_heads, group_size, d, reps, unit_start, unit_size, units_cap,
+                                 n_units, budget, sel_units, n_sel_units, n_sel);
+  if (st) return st;
+  if (budget > 0 && !sel_rows) return fail(LOUISKV_ERR_NULL, "sel_rows is required when budget > 0");
+  const size_t need = louiskv_retrieve_rows_workspace_size(n_slices, units_cap);
+  if (!workspace || workspace_bytes < need)
+    return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  return score_and_select(q, dtype, n_slices, n_kv_heads, group_size, d, scale, reps, unit_start, unit_size, units_cap,
+                          n_units, budget, fire, sel_units, n_sel_units, n_sel, sel_rows, scores_out,
+                          static_cast<double*>(workspace), as_stream(stream));
+}
+
 extern "C" size_t louiskv_sparse_decode_attn_workspace_size(int64_t n_slices, int32_t group_size, int32_t d,
                                                             int32_t buf_rows, int32_t window) {
   (void)d;
   if (n_slices < 1 || group_size < 1 || buf_rows < 0 || window < 0) return 0;
-  return attn_ws_bytes(n_slices, group_size, buf_rows, window);
+  return attn_ws_bytes(n_slices, group_size, buf_rows, window, false);
 }
 
-template <class T, int G>
-static void launch_attn_partial(const void* q, int n_kv_heads, float scale, const void* k_buf, const void* v_buf,
-                                const int32_t* n_sel, int buf_rows, const void* k_local, const void* v_local,
-                                int window, int local_start, int n_local, int n_chunks, float* part, void* out,
-                                int out_bf16, float* lse_out, unsigned grid, hipStream_t s) {
-  attn_partial_kernel<T, G><<<grid, attn_waves<T, G>() * 64, 0, s>>>(
-      static_cast<const T*>(q), n_kv_heads, scale, static_cast<const T*>(k_buf), static_cast<const T*>(v_buf), n_sel,
-      buf_rows, static_cast<const T*>(k_local), static_cast<const T*>(v_local), window, local_start, n_local, n_chunks,
-      part, out, out_bf16, lse_out);
+extern "C" size_t louiskv_sparse_decode_attn_rows_workspace_size(int64_t n_slices, int32_t group_size, int32_t d,
+                                                                 int32_t budget, int32_t window) {
+  (void)d;
+  if (n_slices < 1 || group_size < 1 || budget < 0 || window < 0) return 0;
+  return attn_ws_bytes(n_slices, group_size, budget, window, true);
 }
 
-template <int G>
-static void launch_attn_mfma(const void* q, int n_kv_heads, float scale, const void* k_buf, const void* v_buf,
-                             const int32_t* n_sel, int buf_rows, const void* k_local, const void* v_local, int window,
-                             int local_start, int n_local, int n_chunks, float* part, void* out, int out_bf16,
-                             float* lse_out, unsigned grid, hipStream_t s) {
-  attn_mfma_kernel<G><<<grid, attn_mfma_waves<G>() * 64, 0, s>>>(
-      static_cast<const uint16_t*>(q), n_kv_heads, scale, static_cast<const uint16_t*>(k_buf),
-      static_cast<const uint16_t*>(v_buf), n_sel, buf_rows, static_cast<const uint16_t*>(k_local),
-      static_cast<const uint16_t*>(v_local), window, local_start, n_local, n_chunks, part, out, out_bf16, lse_out);
+namespace louiskv {
+namespace {
+
+struct AttnArgs {
+  const void* q;
+  int n_kv_heads;
+  float scale;
+  const void* k_src;
+  const void* v_src;
+  const int32_t* n_sel;
+  int buf_rows;            // KV_critical rows per slice, or row-list entries per slice
+  const int32_t* rows;     // row list, or NULL for the dense KV_critical
+  int64_t src_rows;        // rows per slice of k_src/v_src
+  const void* k_local;
+  const void* v_local;
+  int window, local_start, n_local, n_chunks;
+  float* part;
+  void* out;
+  int out_bf16;
+  float* lse_out;
+  unsigned grid;
+  size_t lds;              // dynamic LDS for the staged row list
+};
+
+template <class T, int G, bool kIdx>
+void launch_attn_partial(const AttnArgs& a, hipStream_t s) {
+  attn_partial_kernel<T, G, kIdx><<<a.grid, attn_waves<T, G>() * 64, a.lds, s>>>(
+      static_cast<const T*>(a.q), a.n_kv_heads, a.scale, static_cast<const T*>(a.k_src), static_cast<const T*>(a.v_src),
+      a.n_sel, a.buf_rows, a.rows, a.src_rows, static_cast<const T*>(a.k_local), static_cast<const T*>(a.v_local),
+      a.window, a.local_start, a.n_local, a.n_chunks, a.part, a.out, a.out_bf16, a.lse_out);
 }
 
-extern "C" int louiskv_sparse_decode_attn(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads,
-                                          int32_t group_size, int32_t d, float scale, const void* k_buf,
-                                          const void* v_buf, const int32_t* n_sel, int32_t buf_rows,
-                                          const void* k_local, const void* v_local, int32_t window,
-                                          int32_t local_start, int32_t n_local, void* out, int32_t out_dtype,
-                                          float* lse_out, void* workspace, size_t workspace_bytes, void* stream) {
+template <int G, bool kIdx>
+void launch_attn_mfma(const AttnArgs& a, hipStream_t s) {
+  attn_mfma_kernel<G, kIdx><<<a.grid, attn_mfma_waves<G>() * 64, a.lds, s>>>(
+      static_cast<const uint16_t*>(a.q), a.n_kv_heads, a.scale, static_cast<const uint16_t*>(a.k_src),
+      static_cast<const uint16_t*>(a.v_src), a.n_sel, a.buf_rows, a.rows, a.src_rows,
+      static_cast<const uint16_t*>(a.k_local), static_cast<const uint16_t*>(a.v_local), a.window, a.local_start,
+      a.n_local, a.n_chunks, a.part, a.out, a.out_bf16, a.lse_out);
+}
+
+template <bool kIdx>
+void launch_attn(int dtype, int group_size, const AttnArgs& a, hipStream_t s) {
+  if (dtype == LOUISKV_BF16) {
+    switch (group_size) {
+      case 1: launch_attn_mfma<1, kIdx>(a, s); break;
+      case 2: launch_attn_mfma<2, kIdx>(a, s); break;
+      case 4: launch_attn_mfma<4, kIdx>(a, s); break;
+      default: launch_attn_mfma<8, kIdx>(a, s); break;
+    }
+  } else {
+    switch (group_size) {
+      case 1: launch_attn_partial<float, 1, kIdx>(a, s); break;
+      case 2: launch_attn_partial<float, 2, kIdx>(a, s); break;
+      case 4: launch_attn_partial<float, 4, kIdx>(a, s); break;
+      default: launch_attn_partial<float, 8, kIdx>(a, s); break;
+    }
+  }
+}
+
+// Validation and launch shared by the dense (KV_critical) and the row-list
+// entry points.
+int sparse_decode_attn(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads, int32_t group_size,
+                       int32_t d, float scale, const void* k_src, const void* v_src, const int32_t* n_sel,
+                       int32_t buf_rows, const int32_t* rows, int64_t src_rows, const void* k_local,
+                       const void* v_local, int32_t window, int32_t local_start, int32_t n_local, void* out,
+                       int32_t out_dtype, float* lse_out, void* workspace, size_t workspace_bytes, void* stream) {
+  const bool indexed = rows != nullptr;
   if (!q || !out || !n_sel) return fail(LOUISKV_ERR_NULL, "q, out and n_sel are required");
-  if (buf_rows > 0 && (!k_buf || !v_buf)) return fail(LOUISKV_ERR_NULL, "k_buf/v_buf required when buf_rows > 0");
+  if (buf_rows > 0 && (!k_src || !v_src))
+    return fail(LOUISKV_ERR_NULL, indexed ? "k_pool/v_pool required when budget > 0"
+                                          : "k_buf/v_buf required when buf_rows > 0");
   if (n_local > 0 && (!k_local || !v_local)) return fail(LOUISKV_ERR_NULL, "k_local/v_local required when n_local > 0");
   int st = check_dtype(dtype);
   if (st) return st;
@@ -1146,49 +1273,66 @@ extern "C" int louiskv_sparse_decode_attn(const void* q, int32_t dtype, int64_t 
   if (buf_rows < 0 || window < 0 || n_local < 0 || n_local > window || (window > 0 && (local_start < 0 || local_start >= window)))
     return fail(LOUISKV_ERR_SHAPE, "buf_rows=%d window=%d local_start=%d n_local=%d", buf_rows, window, local_start,
                 n_local);
-  const int n_chunks = attn_chunks(n_slices, buf_rows, window);
+  if (indexed && buf_rows > 0 && src_rows < 1) return fail(LOUISKV_ERR_SHAPE, "pool_rows=%lld", (long long)src_rows);
+  const int n_chunks = attn_chunks(n_slices, buf_rows, window, indexed);
   if ((int64_t)n_slices * n_chunks > INT32_MAX) return fail(LOUISKV_ERR_SHAPE, "problem too large for one launch");
-  const size_t need = attn_ws_bytes(n_slices, group_size, buf_rows, window);
+  const size_t need = attn_ws_bytes(n_slices, group_size, buf_rows, window, indexed);
   if (need > 0 && (!workspace || workspace_bytes < need))
     return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
-  float* part = static_cast<float*>(workspace);
+  AttnArgs a;
+  a.q = q; a.n_kv_heads = n_kv_heads; a.scale = scale; a.k_src = k_src; a.v_src = v_src; a.n_sel = n_sel;
+  a.buf_rows = buf_rows; a.rows = rows; a.src_rows = indexed ? src_rows : buf_rows;
+  a.k_local = k_local; a.v_local = v_local;
+  a.window = window > 0 ? window : 1;
+  a.local_start = window > 0 ? local_start : 0;
+  a.n_local = n_local; a.n_chunks = n_chunks;
+  a.part = static_cast<float*>(workspace);
+  a.out = out; a.out_bf16 = out_dtype == LOUISKV_BF16; a.lse_out = lse_out;
+  a.grid = (unsigned)(n_slices * n_chunks);
+  // a chunk spans at most ceil(total / n_chunks) <= ceil((buf_rows + window) / n_chunks) rows
+  a.lds = indexed ? (size_t)(((int64_t)buf_rows + window + n_chunks - 1) / n_chunks + 1) * sizeof(int) : 0;
   hipStream_t s = as_stream(stream);
-  const unsigned grid = (unsigned)(n_slices * n_chunks);
-  const int win = window > 0 ? window : 1;
-  const int lstart = window > 0 ? local_start : 0;
-#define LKV_ATTN(T, G) \
-  launch_attn_partial<T, G>(q, n_kv_heads, scale, k_buf, v_buf, n_sel, buf_rows, k_local, v_local, win, lstart, n_local, \
-                            n_chunks, part, out, out_dtype == LOUISKV_BF16, lse_out, grid, s)
-#define LKV_ATTN_MFMA(G) \
-  launch_attn_mfma<G>(q, n_kv_heads, scale, k_buf, v_buf, n_sel, buf_rows, k_local, v_local, win, lstart, n_local, \
-                      n_chunks, part, out, out_dtype == LOUISKV_BF16, lse_out, grid, s)
-  if (dtype == LOUISKV_BF16) {
-    switch (group_size) {
-      case 1: LKV_ATTN_MFMA(1); break;
-      case 2: LKV_ATTN_MFMA(2); break;
-      case 4: LKV_ATTN_MFMA(4); break;
-      default: LKV_ATTN_MFMA(8); break;
-    }
-  } else {
-    switch (group_size) {
-      case 1: LKV_ATTN(float, 1); break;
-      case 2: LKV_ATTN(float, 2); break;
-      case 4: LKV_ATTN(float, 4); break;
-      default: LKV_ATTN(float, 8); break;
-    }
-  }
-#undef LKV_ATTN
-#undef LKV_ATTN_MFMA
+  if (indexed)
+    launch_attn<true>(dtype, group_size, a, s);
+  else
+    launch_attn<false>(dtype, group_size, a, s);
   LKV_CHECK_LAUNCH();
   if (n_chunks == 1) return LOUISKV_OK;     // the blocks wrote the output themselves
-  const int64_t rows = n_slices * group_size;
-  const int cgrid = (int)((rows + 3) / 4);
+  const int64_t n_rows = n_slices * group_size;
+  const int cgrid = (int)((n_rows + 3) / 4);
   if (out_dtype == LOUISKV_BF16)
-    attn_combine_kernel<uint16_t><<<cgrid, 256, 0, s>>>(part, n_chunks, group_size, rows, static_cast<uint16_t*>(out),
-                                                        lse_out);
+    attn_combine_kernel<uint16_t><<<cgrid, 256, 0, s>>>(a.part, n_chunks, group_size, n_rows,
+                                                        static_cast<uint16_t*>(out), lse_out);
   else
-    attn_combine_kernel<float><<<cgrid, 256, 0, s>>>(part, n_chunks, group_size, rows, static_cast<float*>(out),
+    attn_combine_kernel<float><<<cgrid, 256, 0, s>>>(a.part, n_chunks, group_size, n_rows, static_cast<float*>(out),
                                                      lse_out);
   LKV_CHECK_LAUNCH();
   return LOUISKV_OK;
+}
+
+}  // namespace
+}  // namespace louiskv
+
+extern "C" int louiskv_sparse_decode_attn(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads,
+                                          int32_t group_size, int32_t d, float scale, const void* k_buf,
+                                          const void* v_buf, const int32_t* n_sel, int32_t buf_rows,
+                                          const void* k_local, const void* v_local, int32_t window,
+                                          int32_t local_start, int32_t n_local, void* out, int32_t out_dtype,
+                                          float* lse_out, void* workspace, size_t workspace_bytes, void* stream) {
+  return sparse_decode_attn(q, dtype, n_slices, n_kv_heads, group_size, d, scale, k_buf, v_buf, n_sel, buf_rows,
+                            nullptr, buf_rows, k_local, v_local, window, local_start, n_local, out, out_dtype,
+                            lse_out, workspace, workspace_bytes, stream);
+}
+
+extern "C" int louiskv_sparse_decode_attn_rows(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads,
+                                               int32_t group_size, int32_t d, float scale, const void* k_pool,
+                                               const void* v_pool, int64_t pool_rows, const int32_t* sel_rows,
+                                               const int32_t* n_sel, int32_t budget, const void* k_local,
+                                               const void* v_local, int32_t window, int32_t local_start,
+                                               int32_t n_local, void* out, int32_t out_dtype, float* lse_out,
+                                               void* workspace, size_t workspace_bytes, void* stream) {
+  if (!sel_rows) return fail(LOUISKV_ERR_NULL, "sel_rows is required");
+  return sparse_decode_attn(q, dtype, n_slices, n_kv_heads, group_size, d, scale, k_pool, v_pool, n_sel, budget,
+                            sel_rows, pool_rows, k_local, v_local, window, local_start, n_local, out, out_dtype,
+                            lse_out, workspace, workspace_bytes, stream);
 }

@@ -12,6 +12,12 @@ paper's Algorithm 1:
              oldest-segment eviction), louiskv_sparse_decode_attn over
              [KV_critical : KV_local].
 
+With the pool in device memory the engine runs zero-copy by default:
+louiskv_retrieve_rows keeps KV_critical as a list of pool rows and
+louiskv_sparse_decode_attn_rows reads them from the pool, so a fired step
+copies nothing.  A pool in pinned host memory (or zero_copy=False) uses the
+dense KV_critical buffers that louiskv_retrieve gathers.
+
 Python only allocates tensors and passes pointers; every step of the path
 runs in the library's kernels.
 """
@@ -67,11 +73,15 @@ def config_from_workload(wl, n_groups: Optional[int] = None, mode: int = L.REF_A
 
 class LouisKVEngine:
     def __init__(self, cfg: EngineConfig, dtype: torch.dtype, device="cuda", pool_on_host: bool = False,
-                 keep_scores: bool = False, out_dtype: Optional[torch.dtype] = None):
+                 keep_scores: bool = False, out_dtype: Optional[torch.dtype] = None,
+                 zero_copy: Optional[bool] = None):
         self.cfg = cfg
         self.dtype = dtype
         self.device = torch.device(device)
         self.pool_on_host = pool_on_host
+        if zero_copy and pool_on_host:
+            raise ValueError("zero-copy retrieval reads the pool from device memory; use zero_copy=False")
+        self.zero_copy = (not pool_on_host) if zero_copy is None else bool(zero_copy)
         S, d, cap, G = cfg.n_slices, cfg.head_dim, cfg.units_cap, cfg.n_groups
         dev = self.device
         i32 = dict(dtype=torch.int32, device=dev)
@@ -88,8 +98,13 @@ class LouisKVEngine:
             self.v_pool = torch.empty(S, cfg.pool_rows, d, dtype=dtype, device=dev)
         self.k_local = torch.zeros(S, cfg.window, d, dtype=dtype, device=dev)
         self.v_local = torch.zeros(S, cfg.window, d, dtype=dtype, device=dev)
-        self.k_buf = torch.zeros(S, max(cfg.budget, 1), d, dtype=dtype, device=dev)
-        self.v_buf = torch.zeros(S, max(cfg.budget, 1), d, dtype=dtype, device=dev)
+        if self.zero_copy:
+            self.sel_rows = torch.zeros(S, max(cfg.budget, 1), **i32)
+            self.k_buf = self.v_buf = None
+        else:
+            self.sel_rows = None
+            self.k_buf = torch.zeros(S, max(cfg.budget, 1), d, dtype=dtype, device=dev)
+            self.v_buf = torch.zeros(S, max(cfg.budget, 1), d, dtype=dtype, device=dev)
         self.sel_units = torch.zeros(S, cap, **i32)
         self.n_sel_units = torch.zeros(S, **i32)
         self.n_sel = torch.zeros(S, **i32)
@@ -102,10 +117,14 @@ class LouisKVEngine:
         dc = L.BF16 if dtype == torch.bfloat16 else L.F32
         u8 = dict(dtype=torch.uint8, device=dev)
         self.ws_prefill = torch.empty(L.cluster_prefill_workspace_size(S, cfg.prompt_len, cfg.n_clusters, dc), **u8)
-        self.ws_retrieve = torch.empty(L.retrieve_workspace_size(S, cap, cfg.budget), **u8)
-        self.ws_attn = torch.empty(
-            L.sparse_decode_attn_workspace_size(S, cfg.n_q_heads // cfg.n_kv_heads, self.k_buf.shape[1],
-                                                cfg.window), **u8)
+        g = cfg.n_q_heads // cfg.n_kv_heads
+        rows = max(cfg.budget, 1)
+        if self.zero_copy:
+            self.ws_retrieve = torch.empty(L.retrieve_rows_workspace_size(S, cap), **u8)
+            self.ws_attn = torch.empty(max(L.sparse_decode_attn_rows_workspace_size(S, g, rows, cfg.window), 1), **u8)
+        else:
+            self.ws_retrieve = torch.empty(L.retrieve_workspace_size(S, cap, cfg.budget), **u8)
+            self.ws_attn = torch.empty(max(L.sparse_decode_attn_workspace_size(S, g, rows, cfg.window), 1), **u8)
         self.t = 0
 
     # ---------------------------------------------------------------- prefill
@@ -130,14 +149,24 @@ class LouisKVEngine:
         c = self.cfg
         t = self.t
         L.boundary_check(q_t, self.q_ref, c.tau, c.mode, t == 0, self.fire, self.r)
-        L.retrieve(q_t, c.n_kv_heads, self.reps, self.unit_start, self.unit_size, self.n_units_before(t),
-                   self.k_pool, self.v_pool, c.budget, self.sel_units, self.n_sel_units, self.n_sel,
-                   self.k_buf, self.v_buf, fire=self.fire, pool_on_host=self.pool_on_host,
-                   scores_out=self.scores, workspace=self.ws_retrieve)
+        if self.zero_copy:
+            L.retrieve_rows(q_t, c.n_kv_heads, self.reps, self.unit_start, self.unit_size, self.n_units_before(t),
+                            c.budget, self.sel_units, self.n_sel_units, self.n_sel, self.sel_rows, fire=self.fire,
+                            scores_out=self.scores, workspace=self.ws_retrieve)
+        else:
+            L.retrieve(q_t, c.n_kv_heads, self.reps, self.unit_start, self.unit_size, self.n_units_before(t),
+                       self.k_pool, self.v_pool, c.budget, self.sel_units, self.n_sel_units, self.n_sel,
+                       self.k_buf, self.v_buf, fire=self.fire, pool_on_host=self.pool_on_host,
+                       scores_out=self.scores, workspace=self.ws_retrieve)
         L.segment_output(k_t, v_t, self.k_local, self.v_local, t, c.seg_len, self.reps, self.unit_start,
                          self.unit_size, c.n_clusters, self.k_pool, self.v_pool, c.prompt_len,
                          pool_on_host=self.pool_on_host)
         _, _, n_local, local_start = L.window_info(t, c.window, c.seg_len)
-        L.sparse_decode_attn(q_t, c.n_kv_heads, self.k_buf, self.v_buf, self.n_sel, self.k_local, self.v_local,
-                             local_start, n_local, self.out, self.lse, workspace=self.ws_attn)
+        if self.zero_copy:
+            L.sparse_decode_attn_rows(q_t, c.n_kv_heads, self.k_pool, self.v_pool, self.sel_rows, self.n_sel,
+                                      self.k_local, self.v_local, local_start, n_local, self.out, self.lse,
+                                      workspace=self.ws_attn)
+        else:
+            L.sparse_decode_attn(q_t, c.n_kv_heads, self.k_buf, self.v_buf, self.n_sel, self.k_local,
+                                 self.v_local, local_start, n_local, self.out, self.lse, workspace=self.ws_attn)
         self.t += 1

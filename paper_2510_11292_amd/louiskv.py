@@ -48,6 +48,16 @@ _SIGS = {
         _P, _P, _P, _I32, _I32,
         _P, _P, _I64, _I32, _I32, _P,
         _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "louiskv_retrieve_rows_workspace_size": (_SZ, [_I64, _I32]),
+    "louiskv_retrieve_rows": (ctypes.c_int, [
+        _P, _I32, _I64, _I32, _I32, _I32, _D,
+        _P, _P, _P, _I32, _I32, _I32, _P,
+        _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "louiskv_sparse_decode_attn_rows_workspace_size": (_SZ, [_I64, _I32, _I32, _I32, _I32]),
+    "louiskv_sparse_decode_attn_rows": (ctypes.c_int, [
+        _P, _I32, _I64, _I32, _I32, _I32, _F,
+        _P, _P, _I64, _P, _P, _I32, _P, _P, _I32, _I32, _I32,
+        _P, _I32, _P, _P, _SZ, _P]),
     "louiskv_sparse_decode_attn_workspace_size": (_SZ, [_I64, _I32, _I32, _I32, _I32]),
     "louiskv_sparse_decode_attn": (ctypes.c_int, [
         _P, _I32, _I64, _I32, _I32, _I32, _F,
@@ -224,3 +234,44 @@ def sparse_decode_attn(q, n_kv_heads: int, k_buf, v_buf, n_sel, k_local, v_local
         _ptr(q), _dtype_code(q), s, n_kv_heads, gs, d, float(sc), _ptr(k_buf), _ptr(v_buf), _ptr(n_sel), buf_rows,
         _ptr(k_local), _ptr(v_local), window, local_start, n_local, _ptr(out), _dtype_code(out), _ptr(lse_out),
         _ptr(ws), wsb, _stream(stream)))
+
+
+def retrieve_rows_workspace_size(n_slices, units_cap) -> int:
+    return load_library().louiskv_retrieve_rows_workspace_size(n_slices, units_cap)
+
+
+def retrieve_rows(q, n_kv_heads: int, reps, unit_start, unit_size, n_units: int, budget: int, sel_units,
+                  n_sel_units, n_sel, sel_rows, fire=None, scale: Optional[float] = None, scores_out=None,
+                  workspace=None, stream=None):
+    """Selection as a list of pool rows (no copy); sel_rows is [S][budget] int32."""
+    g, hq, d = q.shape
+    s = reps.shape[0]
+    cap = reps.shape[1]
+    ws, wsb = _ws(retrieve_rows_workspace_size(s, cap), q.device, workspace)
+    sc = (1.0 / d ** 0.5) if scale is None else scale
+    _check(load_library().louiskv_retrieve_rows(
+        _ptr(q), _dtype_code(q), s, n_kv_heads, hq // n_kv_heads, d, float(sc),
+        _ptr(reps), _ptr(unit_start), _ptr(unit_size), cap, n_units, budget, _ptr(fire),
+        _ptr(sel_units), _ptr(n_sel_units), _ptr(n_sel), _ptr(sel_rows), _ptr(scores_out),
+        _ptr(ws), wsb, _stream(stream)))
+
+
+def sparse_decode_attn_rows_workspace_size(n_slices, group_size, budget, window, d=128) -> int:
+    return load_library().louiskv_sparse_decode_attn_rows_workspace_size(n_slices, group_size, d, budget, window)
+
+
+def sparse_decode_attn_rows(q, n_kv_heads: int, k_pool, v_pool, sel_rows, n_sel, k_local, v_local,
+                            local_start: int, n_local: int, out, lse_out=None, scale: Optional[float] = None,
+                            workspace=None, stream=None):
+    """Attention over the listed pool rows followed by the local window."""
+    g, hq, d = q.shape
+    s = n_sel.shape[0]
+    gs = hq // n_kv_heads
+    budget = sel_rows.shape[1]
+    window = k_local.shape[1] if k_local is not None else 0
+    ws, wsb = _ws(sparse_decode_attn_rows_workspace_size(s, gs, budget, window, d), q.device, workspace)
+    sc = (1.0 / d ** 0.5) if scale is None else scale
+    _check(load_library().louiskv_sparse_decode_attn_rows(
+        _ptr(q), _dtype_code(q), s, n_kv_heads, gs, d, float(sc), _ptr(k_pool), _ptr(v_pool), k_pool.shape[1],
+        _ptr(sel_rows), _ptr(n_sel), budget, _ptr(k_local), _ptr(v_local), window, local_start, n_local,
+        _ptr(out), _dtype_code(out), _ptr(lse_out), _ptr(ws), wsb, _stream(stream)))

@@ -225,9 +225,121 @@ def test_sparse_decode_attn(dtype, odt, G, H, g, BR, W, nl, ls):
         np.testing.assert_allclose(to64(lse[grp, h * g:(h + 1) * g]), l, rtol=1e-5, atol=1e-5)
 
 
+@pytest.mark.parametrize("dtype,G,H,g,U,B,maxsz", RETRIEVE_CASES)
+def test_retrieve_rows(dtype, G, H, g, U, B, maxsz):
+    """Zero-copy retrieval: the same selection as a list of pool rows."""
+    L = _L()
+    S = G * H
+    gen = _gen(U + B + 1)
+    q = torch.randn(G, H * g, 128, generator=gen, device=DEV).mul(2).to(dtype)
+    reps = torch.randn(S, U + 3, 128, generator=gen, device=DEV)
+    sizes = torch.randint(0, maxsz + 1, (S, U + 3), generator=gen, device=DEV, dtype=torch.int32)
+    starts = torch.zeros_like(sizes)
+    starts[:, 1:] = torch.cumsum(sizes, 1)[:, :-1].to(torch.int32)
+    rows_cap = int(sizes.sum(1).max()) + 5
+    fire = (torch.arange(G, device=DEV) % 3 != 1).to(torch.uint8)
+    Bcall = min(B, rows_cap) if B > 0 else 0
+    sel_rows = torch.full((S, max(Bcall, 1)), -7, dtype=torch.int32, device=DEV)
+    sel = torch.full((S, U + 3), -1, dtype=torch.int32, device=DEV)
+    nsu = torch.full((S,), -1, dtype=torch.int32, device=DEV)
+    nsel = torch.full((S,), -1, dtype=torch.int32, device=DEV)
+    L.retrieve_rows(q, H, reps, starts, sizes, U, Bcall, sel, nsu, nsel, sel_rows, fire=fire)
+    torch.cuda.synchronize()
+    q64, r64, sz, st = to64(q), to64(reps), to_np(sizes), to_np(starts)
+    for s in range(S):
+        grp, h = divmod(s, H)
+        if not fire[grp]:
+            assert int(nsel[s]) == -1 and torch.all(sel_rows[s] == -7)
+            continue
+        a = oracle.group_scores(q64[grp, h * g:(h + 1) * g], r64[s, :U], 1 / np.sqrt(128))
+        got = to_np(sel[s, :int(nsu[s])]).tolist()
+        selection_matches(a, sz[s, :U], Bcall, got)
+        idx = [r for u in got for r in range(int(st[s, u]), int(st[s, u] + sz[s, u]))]
+        assert int(nsel[s]) == len(idx) <= max(Bcall, 0)
+        assert to_np(sel_rows[s, :len(idx)]).tolist() == idx
+
+
+ROWS_ATTN_CASES = [
+    # (dtype, out dtype, n_groups, n_kv, g, budget, pool rows, window, n_local, local_start)
+    (torch.bfloat16, torch.float32, 32, 8, 4, 2048, 6000, 128, 128, 17),   # one block per slice
+    (torch.bfloat16, torch.float32, 2, 8, 4, 700, 3000, 64, 40, 60),       # split-KV
+    (torch.bfloat16, torch.bfloat16, 1, 8, 8, 300, 1000, 32, 32, 5),
+    (torch.float32, torch.float32, 1, 8, 4, 512, 2000, 128, 97, 32),
+    (torch.float32, torch.float32, 64, 4, 4, 300, 900, 64, 64, 3),
+]
+
+
+@pytest.mark.parametrize("dtype,odt,G,H,g,B,PR,W,nl,ls", ROWS_ATTN_CASES)
+def test_sparse_decode_attn_rows(dtype, odt, G, H, g, B, PR, W, nl, ls):
+    """Attention over listed pool rows (random rows, ragged counts, empty
+    slices) then the local window, against the oracle on the same rows."""
+    L = _L()
+    S = G * H
+    gen = _gen(B + PR + nl)
+    q = torch.randn(G, H * g, 128, generator=gen, device=DEV).mul(1.5).to(dtype)
+    kp = torch.randn(S, PR, 128, generator=gen, device=DEV).mul(2).to(dtype)
+    vp = torch.randn(S, PR, 128, generator=gen, device=DEV).to(dtype)
+    kl = torch.randn(S, W, 128, generator=gen, device=DEV).mul(2).to(dtype)
+    vl = torch.randn(S, W, 128, generator=gen, device=DEV).to(dtype)
+    rows = torch.stack([torch.randperm(PR, generator=torch.Generator().manual_seed(s))[:B] for s in range(S)])
+    rows = rows.to(torch.int32).to(DEV)
+    nsel = torch.randint(0, B + 1, (S,), generator=gen, device=DEV, dtype=torch.int32)
+    nsel[0] = B
+    nsel[-1] = 0
+    out = torch.empty(G, H * g, 128, dtype=odt, device=DEV)
+    lse = torch.empty(G, H * g, dtype=torch.float32, device=DEV)
+    L.sparse_decode_attn_rows(q, H, kp, vp, rows, nsel, kl, vl, ls, nl, out, lse)
+    torch.cuda.synchronize()
+    q64 = to64(q)
+    for s in range(S):
+        grp, h = divmod(s, H)
+        n = int(nsel[s])
+        idx = rows[s, :n].long()
+        slots = [(ls + i) % W for i in range(nl)]
+        kk = np.concatenate([to64(kp[s, idx]), to64(kl[s, slots])])
+        vv = np.concatenate([to64(vp[s, idx]), to64(vl[s, slots])])
+        got = to64(out[grp, h * g:(h + 1) * g])
+        if kk.shape[0] == 0:
+            assert np.all(got == 0)
+            continue
+        o, l = oracle.attention(q64[grp, h * g:(h + 1) * g], kk, vv, 1 / np.sqrt(128))
+        if odt == torch.bfloat16:
+            ref = oracle.round_to_bf16(o)
+            assert np.all(np.abs(got - ref) <= np.abs(ref) * 2.0 ** -7 + 1e-6)
+        elif dtype == torch.float32:
+            check_rows_rel(got, o, 1e-5, "fp32 attention over listed rows")
+        else:
+            assert np.abs(got - o).max() <= 2e-3
+        np.testing.assert_allclose(to64(lse[grp, h * g:(h + 1) * g]), l, rtol=1e-5, atol=1e-5)
+
+
+def test_sparse_decode_attn_rows_clamps_list_entries():
+    """Entries outside [0, pool_rows) are clamped into the pool by the kernel."""
+    L = _L()
+    S, H, g, B, PR, W = 8, 8, 4, 64, 200, 32
+    gen = _gen(99)
+    q = torch.randn(1, H * g, 128, generator=gen, device=DEV).to(torch.bfloat16)
+    kp = torch.randn(S, PR, 128, generator=gen, device=DEV).to(torch.bfloat16)
+    vp = torch.randn(S, PR, 128, generator=gen, device=DEV).to(torch.bfloat16)
+    kl = torch.zeros(S, W, 128, dtype=torch.bfloat16, device=DEV)
+    rows = torch.randint(0, PR, (S, B), generator=gen, device=DEV, dtype=torch.int32)
+    rows[:, 3] = -5
+    rows[:, 9] = PR + 10
+    nsel = torch.full((S,), B, dtype=torch.int32, device=DEV)
+    out = torch.empty(1, H * g, 128, dtype=torch.float32, device=DEV)
+    L.sparse_decode_attn_rows(q, H, kp, vp, rows, nsel, kl, kl, 0, 0, out)
+    torch.cuda.synchronize()
+    clamped = rows.clamp(0, PR - 1).long()
+    q64 = to64(q)
+    for s in range(S):
+        o, _ = oracle.attention(q64[0, s * g:(s + 1) * g], to64(kp[s, clamped[s]]), to64(vp[s, clamped[s]]),
+                                1 / np.sqrt(128))
+        assert np.abs(to64(out[0, s * g:(s + 1) * g]) - o).max() <= 2e-3
+
+
 # ------------------------------------------------------------------ whole decode loop
 
-def _run_loop(wl, n_groups, steps, mode, pool_on_host=False):
+def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None):
     """Prefill on the GPU, then `steps` decode steps on the GPU and in the
     oracle (started from the GPU's prefill state), step-locked."""
     from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
@@ -235,7 +347,7 @@ def _run_loop(wl, n_groups, steps, mode, pool_on_host=False):
     cfg = config_from_workload(wl, n_groups=n_groups, mode=mode, gen_len=steps)
     odt = torch.float32
     eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, pool_on_host=pool_on_host, keep_scores=True,
-                        out_dtype=odt)
+                        out_dtype=odt, zero_copy=zero_copy)
     eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
     torch.cuda.synchronize()
     H, g = wl.n_kv_heads, wl.group_size
@@ -297,16 +409,19 @@ def test_decode_loop_tiny_workload_anchor():
 
 
 def test_decode_loop_tiny_workload_prev():
+    """PREV mode, with the dense (gathered) KV_critical."""
     wl = synth.get_workload("tiny-4k")
-    st = _run_loop(wl, 1, wl.gen_len, mode=0)
+    st = _run_loop(wl, 1, wl.gen_len, mode=0, zero_copy=False)
     assert st["fires"] >= 1
 
 
-def test_decode_loop_bf16_with_evictions():
+@pytest.mark.parametrize("zero_copy", [True, False])
+def test_decode_loop_bf16_with_evictions(zero_copy):
     """A bf16 reduction of the long-output shape: 2 groups, P=2048, C=64,
-    300 steps so several segments are evicted and later retrieved."""
+    300 steps so several segments are evicted and later retrieved; with
+    KV_critical as a row list (zero-copy) and as gathered copies."""
     wl = synth.get_workload("si-lo-16k").replace(prompt_len=2048, n_clusters=64, budget=512, name="si-lo-16k")
-    st = _run_loop(wl, 2, 300, mode=1)
+    st = _run_loop(wl, 2, 300, mode=1, zero_copy=zero_copy)
     assert st["fires"] > 40
 
 

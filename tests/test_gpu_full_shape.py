@@ -11,7 +11,8 @@ sampled outputs are checked against the oracle one by one.
                of two groups the step's outputs are recomputed by the oracle
                from the state the GPU held before the step: the boundary value
                and decision, the scores and the budgeted selection when the
-               group fired, KV_critical against the pool rows of the selection,
+               group fired, KV_critical (copied rows or the row list) against
+               the pool rows of the selection,
                the local window and any evicted segment (mean and pool rows),
                and the attention output.
 """
@@ -112,13 +113,17 @@ def _check_step(eng, data, wl, t, gi, q_ref_before, stats):
             np.testing.assert_allclose(to_np(eng.scores[s, :n_units]), a, rtol=1e-12, atol=1e-300)
             stats["excused"] += selection_matches(a, sizes, wl.budget, got)
             assert nsel == int(sizes[got].sum()) <= wl.budget
-        # KV_critical holds the rows of the current selection, in rank order
+        # KV_critical holds the rows of the current selection, in rank order: as
+        # copies (dense) or as the list of their pool rows (zero-copy)
         idx = [rr for u in got for rr in range(int(starts[u]), int(starts[u] + sizes[u]))]
         assert len(idx) == nsel
         rows = torch.as_tensor(idx, dtype=torch.long)
         kp = eng.k_pool[s].index_select(0, rows.to(eng.k_pool.device))
         vp = eng.v_pool[s].index_select(0, rows.to(eng.v_pool.device))
-        assert torch.equal(eng.k_buf[s, :nsel].cpu(), kp.cpu()) and torch.equal(eng.v_buf[s, :nsel].cpu(), vp.cpu())
+        if eng.zero_copy:
+            assert to_np(eng.sel_rows[s, :nsel]).tolist() == idx
+        else:
+            assert torch.equal(eng.k_buf[s, :nsel].cpu(), kp.cpu()) and torch.equal(eng.v_buf[s, :nsel].cpu(), vp.cpu())
         # local window after the append: tokens nev*seg .. t in their ring slots
         slots = [(local_start + i) % W for i in range(n_local)]
         toks = list(range(nev * seg, t + 1))
@@ -147,15 +152,21 @@ def _sample_steps(wl):
     return {t for t in base if 0 <= t < T}
 
 
-@pytest.mark.parametrize("name", LARGE)
-def test_decode_full_shape_sampled(name):
+# The engine's default retrieval (zero-copy rows for device pools, the dense
+# KV_critical gather for the host pool), plus the dense gather on the
+# benchmark workload.
+DECODE_CASES = [(n, None) for n in LARGE] + [("li-so-32k", "dense")]
+
+
+@pytest.mark.parametrize("name,retrieval", DECODE_CASES)
+def test_decode_full_shape_sampled(name, retrieval):
     from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
     L = _L()
     wl = synth.get_workload(name)
     data = synth.make_slices(wl, DEV)
     cfg = config_from_workload(wl, mode=L.REF_ANCHOR)
     eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, pool_on_host=wl.pool_on_host, keep_scores=True,
-                        out_dtype=torch.float32)
+                        out_dtype=torch.float32, zero_copy=False if retrieval == "dense" else None)
     eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
     torch.cuda.synchronize()
     groups = (0, wl.n_groups - 1)
