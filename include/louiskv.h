@@ -168,6 +168,24 @@ int louiskv_cluster_prefill(const void* keys, int32_t dtype, int64_t n_slices,
                             void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * The pool write of louiskv_cluster_prefill on its own (Algorithm 1 offload of
+ * the prompt K/V): rows 0..n_tokens-1 of each slice's pools receive the keys
+ * (and values) in perm order, so that each cluster is one contiguous run.
+ * Lets a caller run the clustering without a pool and write the pool later,
+ * on another stream, or time the two apart.
+ *
+ * keys, values [n_slices][n_tokens][d] dtype (values may be NULL when v_pool is).
+ * perm        [n_slices][n_tokens] int32 as written by louiskv_cluster_prefill;
+ *             entries are clamped into [0, n_tokens).
+ * k_pool, v_pool  out [n_slices][pool_rows][d] dtype (v_pool may be NULL);
+ *             pool_on_host: see Pointers.  Requires pool_rows >= n_tokens.
+ */
+int louiskv_pack_pool(const void* keys, const void* values, int32_t dtype,
+                      int64_t n_slices, int32_t n_tokens, int32_t d,
+                      const int32_t* perm, void* k_pool, void* v_pool,
+                      int64_t pool_rows, int32_t pool_on_host, void* stream);
+
+/*
  * One assignment step alone (the first half of a Lloyd iteration above), for
  * step-by-step checking: assign[s][i] = argmin_c ||keys[s][i] - op(c)||^2 over
  * the n_clusters float32 centroids at centroids[s][0..C-1] (slice stride

@@ -659,7 +659,7 @@ __global__ void pack_pool_kernel(const T* __restrict__ src, const int32_t* __res
   const int sub = threadIdx.x & 15;
   const int64_t s = g / n_tokens;
   const int r = (int)(g - s * n_tokens);
-  const int tok = perm[s * n_tokens + r];
+  const int tok = min(max(perm[s * n_tokens + r], 0), n_tokens - 1);   // perm may come from the caller
   constexpr int kU4 = kHeadDim * sizeof(T) / 16;
   const uint4* a = reinterpret_cast<const uint4*>(src + ((size_t)s * n_tokens + tok) * kHeadDim);
   uint4* b = reinterpret_cast<uint4*>(pool + ((size_t)s * pool_rows + r) * kHeadDim);
@@ -765,6 +765,26 @@ int launch_sum(const void* keys, int dtype, int64_t S, int N, int C, const Ws& w
   return LOUISKV_OK;
 }
 
+// Prompt K/V rows in perm order into the pools (each cluster one contiguous run).
+int launch_pack(const void* keys, const void* values, int dtype, int64_t S, int N, const int32_t* perm, void* k_pool,
+                void* v_pool, int64_t pool_rows, hipStream_t s) {
+  const int64_t prow = S * N;
+  const int pgrid = (int)((prow + 15) / 16);
+  for (int which = 0; which < 2; ++which) {
+    void* pool = which == 0 ? k_pool : v_pool;
+    const void* src = which == 0 ? keys : values;
+    if (!pool) continue;
+    if (dtype == LOUISKV_BF16)
+      pack_pool_kernel<uint16_t><<<pgrid, 256, 0, s>>>(static_cast<const uint16_t*>(src), perm,
+                                                        static_cast<uint16_t*>(pool), pool_rows, N, prow);
+    else
+      pack_pool_kernel<float><<<pgrid, 256, 0, s>>>(static_cast<const float*>(src), perm, static_cast<float*>(pool),
+                                                     pool_rows, N, prow);
+    LKV_CHECK_LAUNCH();
+  }
+  return LOUISKV_OK;
+}
+
 int check_common(const void* keys, int dtype, int64_t S, int N, int d, int C) {
   if (!keys) return fail(LOUISKV_ERR_NULL, "keys is NULL");
   if (dtype != LOUISKV_F32 && dtype != LOUISKV_BF16) return fail(LOUISKV_ERR_DTYPE, "unknown dtype %d", dtype);
@@ -838,21 +858,23 @@ extern "C" int louiskv_cluster_prefill(const void* keys, int32_t dtype, int64_t 
                                                           unit_size, units_cap, n_tokens, n_clusters, rows);
     LKV_CHECK_LAUNCH();
   }
-  const int64_t prow = n_slices * n_tokens;
-  const int pgrid = (int)((prow + 15) / 16);
-  for (int which = 0; which < 2; ++which) {
-    void* pool = which == 0 ? k_pool : v_pool;
-    const void* src = which == 0 ? keys : values;
-    if (!pool) continue;
-    if (dtype == LOUISKV_BF16)
-      pack_pool_kernel<uint16_t><<<pgrid, 256, 0, s>>>(static_cast<const uint16_t*>(src), perm,
-                                                        static_cast<uint16_t*>(pool), pool_rows, n_tokens, prow);
-    else
-      pack_pool_kernel<float><<<pgrid, 256, 0, s>>>(static_cast<const float*>(src), perm, static_cast<float*>(pool),
-                                                     pool_rows, n_tokens, prow);
-    LKV_CHECK_LAUNCH();
-  }
-  return LOUISKV_OK;
+  return launch_pack(keys, values, dtype, n_slices, n_tokens, perm, k_pool, v_pool, pool_rows, s);
+}
+
+extern "C" int louiskv_pack_pool(const void* keys, const void* values, int32_t dtype, int64_t n_slices,
+                                 int32_t n_tokens, int32_t d, const int32_t* perm, void* k_pool, void* v_pool,
+                                 int64_t pool_rows, int32_t pool_on_host, void* stream) {
+  if (!keys || !perm || !k_pool) return fail(LOUISKV_ERR_NULL, "keys, perm and k_pool are required");
+  if (v_pool && !values) return fail(LOUISKV_ERR_NULL, "v_pool given without values");
+  if (dtype != LOUISKV_F32 && dtype != LOUISKV_BF16) return fail(LOUISKV_ERR_DTYPE, "unknown dtype %d", dtype);
+  if (d != kHeadDim) return fail(LOUISKV_ERR_UNSUPPORTED, "head dim %d not supported (only 128)", d);
+  if (n_slices < 1 || n_tokens < 1 || pool_rows < n_tokens)
+    return fail(LOUISKV_ERR_SHAPE, "n_slices=%lld n_tokens=%d pool_rows=%lld", (long long)n_slices, n_tokens,
+                (long long)pool_rows);
+  int st;
+  if (pool_on_host && ((st = device_view_of_host_pool(k_pool, &k_pool)) || (st = device_view_of_host_pool(v_pool, &v_pool))))
+    return st;
+  return launch_pack(keys, values, dtype, n_slices, n_tokens, perm, k_pool, v_pool, pool_rows, as_stream(stream));
 }
 
 extern "C" int louiskv_kmeans_assign(const void* keys, int32_t dtype, int64_t n_slices, int32_t n_tokens, int32_t d,

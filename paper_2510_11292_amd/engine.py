@@ -5,7 +5,8 @@ LouisKVEngine owns the device (or pinned-host) tensors of one batch of
 paper's Algorithm 1:
 
   prefill()  louiskv_cluster_prefill: k-means per slice, centroids as unit
-             index vectors, prompt K/V packed cluster by cluster into the pool.
+             index vectors; louiskv_pack_pool: prompt K/V packed cluster by
+             cluster into the pool.
   step()     one decode step for every group: louiskv_boundary_check, then
              louiskv_retrieve for the groups that fired (scores see the units
              evicted before this step), louiskv_segment_output (window append,
@@ -129,12 +130,18 @@ class LouisKVEngine:
 
     # ---------------------------------------------------------------- prefill
     def prefill(self, prompt_keys: torch.Tensor, prompt_values: torch.Tensor, init_idx: torch.Tensor,
-                iter_events=None) -> None:
+                iter_events=None, pack_event=None) -> None:
+        """k-means of the prompt keys (louiskv_cluster_prefill), then the pool
+        write (louiskv_pack_pool).  pack_event, if given, is recorded between
+        the two on the current stream."""
         c = self.cfg
         L.cluster_prefill(prompt_keys, c.n_clusters, c.n_iters, init_idx, self.reps, self.unit_start,
-                          self.unit_size, self.assign, self.perm, values=prompt_values, k_pool=self.k_pool,
-                          v_pool=self.v_pool, pool_on_host=self.pool_on_host, iter_events=iter_events,
+                          self.unit_size, self.assign, self.perm, iter_events=iter_events,
                           workspace=self.ws_prefill)
+        if pack_event is not None:
+            pack_event.record()
+        L.pack_pool(prompt_keys, prompt_values, self.perm, self.k_pool, self.v_pool,
+                    pool_on_host=self.pool_on_host)
         self.t = 0
 
     # ---------------------------------------------------------------- decode

@@ -36,6 +36,7 @@ _SIGS = {
         _P, _I32, _I64, _I32, _I32, _I32, _I32, _P,
         _P, _I32, _P, _P, _P, _P,
         _P, _P, _P, _I64, _I32, _P, _P, _SZ, _P]),
+    "louiskv_pack_pool": (ctypes.c_int, [_P, _P, _I32, _I64, _I32, _I32, _P, _P, _P, _I64, _I32, _P]),
     "louiskv_kmeans_assign": (ctypes.c_int, [_P, _I32, _I64, _I32, _I32, _I32, _P, _I32, _P, _P, _SZ, _P]),
     "louiskv_kmeans_update": (ctypes.c_int, [_P, _I32, _I64, _I32, _I32, _I32, _P, _P, _P, _I32, _P, _P, _SZ, _P]),
     "louiskv_segment_output": (ctypes.c_int, [
@@ -275,3 +276,11 @@ def sparse_decode_attn_rows(q, n_kv_heads: int, k_pool, v_pool, sel_rows, n_sel,
         _ptr(q), _dtype_code(q), s, n_kv_heads, gs, d, float(sc), _ptr(k_pool), _ptr(v_pool), k_pool.shape[1],
         _ptr(sel_rows), _ptr(n_sel), budget, _ptr(k_local), _ptr(v_local), window, local_start, n_local,
         _ptr(out), _dtype_code(out), _ptr(lse_out), _ptr(ws), wsb, _stream(stream)))
+
+
+def pack_pool(keys, values, perm, k_pool, v_pool=None, pool_on_host: bool = False, stream=None):
+    """Prompt K/V rows into the pools in perm order (each cluster contiguous)."""
+    s, n, d = keys.shape
+    _check(load_library().louiskv_pack_pool(
+        _ptr(keys), _ptr(values), _dtype_code(keys), s, n, d, _ptr(perm), _ptr(k_pool), _ptr(v_pool),
+        k_pool.shape[1], int(pool_on_host), _stream(stream)))

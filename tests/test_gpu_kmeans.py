@@ -194,3 +194,27 @@ def test_empty_cluster_keeps_centroid():
         res = oracle.kmeans(to64(keys)[s], to_np(init)[s], 1, bf16_operand=True)
         assert np.array_equal(to_np(assign)[s], res.z)
         assert np.array_equal(to64(reps)[s], res.centroids)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_pack_pool_writes_rows_in_perm_order(dtype):
+    """louiskv_pack_pool: pool row r of a slice holds token perm[r] (entries
+    clamped into [0, n_tokens)); rows past n_tokens are left alone."""
+    L = _L()
+    S, N, extra = 3, 300, 20
+    g = torch.Generator(device=DEV).manual_seed(31)
+    keys = torch.randn(S, N, 128, generator=g, device=DEV).to(dtype)
+    values = torch.randn(S, N, 128, generator=g, device=DEV).to(dtype)
+    perm = torch.stack([torch.randperm(N, generator=torch.Generator().manual_seed(s)) for s in range(S)])
+    perm = perm.to(torch.int32).to(DEV)
+    perm[1, 5] = -3
+    perm[2, 7] = N + 7
+    kp = torch.full((S, N + extra, 128), 5, dtype=dtype, device=DEV)
+    vp = torch.full_like(kp, 6)
+    L.pack_pool(keys, values, perm, kp, vp)
+    torch.cuda.synchronize()
+    idx = perm.clamp(0, N - 1).long()
+    for s in range(S):
+        assert torch.equal(kp[s, :N], keys[s, idx[s]])
+        assert torch.equal(vp[s, :N], values[s, idx[s]])
+        assert torch.all(kp[s, N:] == 5) and torch.all(vp[s, N:] == 6)
