@@ -14,6 +14,11 @@
 //   sum      centroid = float64 sum of members / count, rounded once to fp32;
 //            empty clusters keep their centroid.  Sums of bf16 or fp32 inputs
 //            are exact in float64 at these sizes, so the order is irrelevant.
+//            The same kernel writes the next iteration's operand and clears
+//            the counts (prep runs once, before the first iteration).
+// From the second iteration on, the assignment starts each key's running
+// minimum at a bound from its previous centroid, so the index search runs
+// only for tiles that hold a closer centroid.
 // After the last iteration, finalize sorts each member range ascending (the
 // perm output), writes the unit table, and pack copies K/V rows into the pool.
 #include "common.h"
@@ -161,19 +166,36 @@ static_assert(kBf16StageTiles * kTileC <= 64, "one 64-lane copy carries a stage'
 // whole stages, so every stage copies the same amount.
 // Copies [q0, q1) of the wave's kBf16DmaPerWave instructions for stage st
 // (the last one carries the norms), so a stage's copy can be spread out.
+//
+// The copies are written as inline assembly (scalar base address, per-lane
+// offset, LDS destination in M0) rather than with the compiler builtin: the
+// builtin makes the compiler track the LDS writes itself, and at the loop
+// header it cannot tell the ring buffers apart and drains every copy in
+// flight (vmcnt(0)) once per pass of the ring.  Written this way the compiler
+// sees no memory operation, and the sweep's explicit vmcnt waits and barriers
+// are the only synchronisation, as intended.
+__device__ __forceinline__ void dma_16b(const void* base, uint32_t lane_off, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(lane_off), "s"(base), "s"(lds_addr)
+               : "memory", "m0");
+}
+__device__ __forceinline__ void dma_4b(const void* base, uint32_t lane_off, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1" ::"v"(lane_off), "s"(base), "s"(lds_addr)
+               : "memory", "m0");
+}
+
 __device__ __forceinline__ void stage_async_part(const uint4* fslice, const float* cslice, int st, char* buf,
                                                  int wave, int lane, int q0, int q1) {
   const uint4* src = fslice + (size_t)st * kBf16StageTiles * kBf16TileU4;
 #pragma unroll
   for (int q = 0; q < kBf16DmaPerWave - 1; ++q) {
     if (q < q0 || q >= q1) continue;
-    const int i = wave + q * kBf16Waves;
-    __builtin_amdgcn_global_load_lds(src + i * 64 + lane, (lds_ptr_t)(buf + i * 1024), 16, 0, 0);
+    const int i = wave + q * kBf16Waves;   // wave-uniform
+    dma_16b(src + i * 64, lane * 16, (uint32_t)(uintptr_t)(buf + i * 1024));
   }
   if (q1 == kBf16DmaPerWave) {
     const int c = lane % (kBf16StageTiles * kTileC);
-    __builtin_amdgcn_global_load_lds(cslice + st * kBf16StageTiles * kTileC + c,
-                                     (lds_ptr_t)(buf + kBf16StageTiles * kBf16TileU4 * 16), 4, 0, 0);
+    dma_4b(cslice + st * kBf16StageTiles * kTileC, c * 4,
+           (uint32_t)(uintptr_t)(buf + kBf16StageTiles * kBf16TileU4 * 16));
   }
 }
 
@@ -211,15 +233,25 @@ __device__ __forceinline__ float tile_min(const floatx16& x) {
   return __builtin_fminf(f, g);
 }
 
-// Lowest row of the tile holding the value m (the lane's minimum).
+// Lowest row of the tile holding the value m (the lane's minimum).  All
+// compares go first, each into its own SGPR pair, then the selects from the
+// highest row down; written as a plain select chain the compiler pairs every
+// compare with its select through VCC and pads each pair with wait states.
+#define LKV_CMP(v) asm("v_cmp_eq_f32_e64 %0, %1, %2" : "=s"(e##v) : "v"(x[v]), "v"(m))
+#define LKV_CND(v, row) asm("v_cndmask_b32_e64 %0, %1, " #row ", %2" : "=v"(id) : "v"(id), "s"(e##v))
 __device__ __forceinline__ int tile_find(const floatx16& x, float m) {
+  uint64_t e0, e1, e2, e3, e4, e5, e6, e7, e8, e9, e10, e11, e12, e13, e14;
+  LKV_CMP(0); LKV_CMP(1); LKV_CMP(2); LKV_CMP(3); LKV_CMP(4); LKV_CMP(5); LKV_CMP(6); LKV_CMP(7);
+  LKV_CMP(8); LKV_CMP(9); LKV_CMP(10); LKV_CMP(11); LKV_CMP(12); LKV_CMP(13); LKV_CMP(14);
   int id = LKV_ROW(15);
-#define LKV_PICK(v) id = (x[v] == m) ? LKV_ROW(v) : id
-  LKV_PICK(14); LKV_PICK(13); LKV_PICK(12); LKV_PICK(11); LKV_PICK(10); LKV_PICK(9); LKV_PICK(8);
-  LKV_PICK(7); LKV_PICK(6); LKV_PICK(5); LKV_PICK(4); LKV_PICK(3); LKV_PICK(2); LKV_PICK(1); LKV_PICK(0);
-#undef LKV_PICK
+  // rows LKV_ROW(14..0) = 26 25 24 19 18 17 16 11 10 9 8 3 2 1 0
+  LKV_CND(14, 26); LKV_CND(13, 25); LKV_CND(12, 24); LKV_CND(11, 19); LKV_CND(10, 18); LKV_CND(9, 17);
+  LKV_CND(8, 16); LKV_CND(7, 11); LKV_CND(6, 10); LKV_CND(5, 9); LKV_CND(4, 8); LKV_CND(3, 3); LKV_CND(2, 2);
+  LKV_CND(1, 1); LKV_CND(0, 0);
   return id;
 }
+#undef LKV_CMP
+#undef LKV_CND
 
 // One stage of the bf16 sweep.  `cur` holds stage st (its copy was waited
 // for); the copy of stage st + kBf16Ring - 1 goes into `nxt`, the buffer that
@@ -288,7 +320,8 @@ __device__ __forceinline__ void bf16_stage(const char* cur, char* nxt, const uin
 // restrict parameters of this one inlined function, so every asynchronous
 // copy and every LDS read below carries alias scopes that tell the compiler
 // which buffer it touches; it then waits only where the code says so instead
-// of draining all copies in flight before each read.
+// of draining all copies in flight before each read.  best/bidx come in
+// holding the starting bound (and -1).
 template <int kKT>
 __device__ __forceinline__ void bf16_sweep(char* __restrict__ r0, char* __restrict__ r1, char* __restrict__ r2,
                                            char* __restrict__ r3, const uint4* fslice, const float* cslice,
@@ -299,11 +332,6 @@ __device__ __forceinline__ void bf16_sweep(char* __restrict__ r0, char* __restri
   stage_async(fslice, cslice, 0, r0, wave, lane);
   if (n_stages > 1) stage_async(fslice, cslice, 1, r1, wave, lane);
   if (n_stages > 2) stage_async(fslice, cslice, 2, r2, wave, lane);
-#pragma unroll
-  for (int kt = 0; kt < kKT; ++kt) {
-    best[kt] = __builtin_inff();
-    bidx[kt] = -1;
-  }
   for (int st = 0; st < n_stages; st += kBf16Ring) {
     bf16_stage<kKT>(r0, r3, fslice, cslice, st, n_stages, wave, lane, h, b, best, bidx);
     if (st + 1 >= n_stages) break;
@@ -324,7 +352,7 @@ __global__ __launch_bounds__(kBf16Threads, 8 / kBf16Waves)
 void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restrict__ frag,
                         const float* __restrict__ cnorm, int32_t* __restrict__ assign,
                         int32_t* __restrict__ counts, int n_tokens, int n_clusters, int n_ctiles,
-                        int blocks_per_slice, int hist_in_lds) {
+                        int blocks_per_slice, int hist_in_lds, int use_bound) {
   __shared__ __align__(16) char s_ring0[kBf16StageBytes];
   __shared__ __align__(16) char s_ring1[kBf16StageBytes];
   __shared__ __align__(16) char s_ring2[kBf16StageBytes];
@@ -334,7 +362,9 @@ void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restri
   const int lb = xcd_local_block(blockIdx.x, gridDim.x);
   const int slice = lb / blocks_per_slice;
   const int kb = lb - slice * blocks_per_slice;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, j = lane & 31;
+  // the wave index lives in an SGPR (it addresses the copies every stage)
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, h = lane >> 5,
+            j = lane & 31;
   const int key_base = kb * kBf16KeysPerBlock + wave * (32 * kBf16KeyTiles);
   const uint16_t* kslice = keys + (size_t)slice * n_tokens * kHeadDim;
   const uint4* fslice = frag + (size_t)slice * n_ctiles * kBf16TileU4;
@@ -353,10 +383,58 @@ void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restri
     }
   }
   // the key operands are complete before the sweep starts, so no key load is
-  // pending inside the stage loop (the loop then only waits for its copies)
+  // pending inside the stage loop (the loop then only waits for its copies);
+  // the compiler does not read that wait, so every key register is also used
+  // here, which makes it complete the loads before the loop, not inside it
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int kt = 0; kt < kBf16KeyTiles; ++kt)
+#pragma unroll
+    for (int s = 0; s < kBf16Steps; ++s) asm volatile("" ::"v"(b[kt][s]));
+
+  // Starting bound.  From the second Lloyd iteration on, assign holds the
+  // previous assignment; the key's distance to that centroid (computed on the
+  // VALU over the same bf16 operands) plus a margin is an upper bound on the
+  // matrix-core value of its nearest centroid: both evaluations of D differ
+  // from the exact value by at most ~60 x 2^-24 x (||c||^2 + 2 sum|c_i k_i|)
+  // <= 7.2e-6 (||c||^2 + ||k||^2), and the margin is 3e-5 of that.  Tiles whose
+  // minimum does not beat the bound skip the index search; the nearest
+  // centroid's value is strictly below it, so the result is unchanged.
   float best[kBf16KeyTiles];
   int bidx[kBf16KeyTiles];
+#pragma unroll
+  for (int kt = 0; kt < kBf16KeyTiles; ++kt) {
+    bidx[kt] = -1;
+    best[kt] = __builtin_inff();
+    const int key = key_base + kt * 32 + j;
+    const int zp = (use_bound && key < n_tokens) ? assign[(size_t)slice * n_tokens + key] : -1;
+    const bool have = zp >= 0 && zp < n_clusters;
+    if (__builtin_amdgcn_ballot_w64(have)) {
+      typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+      const int zc = have ? zp : 0;
+      // the lane's 64 dimensions of -2 op(c): A-fragment row zc % 32, half h
+      const uint4* f = fslice + (size_t)(zc / kTileC) * kBf16TileU4 + (zc % kTileC) + 32 * h;
+      float p = 0.f, kk = 0.f;
+#pragma unroll
+      for (int s = 0; s < kBf16Steps; ++s) {
+        const uint4 fa = f[s * 64];
+        const uint4 kv = __builtin_bit_cast(uint4, b[kt][s]);
+        const uint32_t fw[4] = {fa.x, fa.y, fa.z, fa.w};
+        const uint32_t kw[4] = {kv.x, kv.y, kv.z, kv.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const bf16x2_t kq = __builtin_bit_cast(bf16x2_t, kw[q]);
+          p = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, fw[q]), kq, p, false);
+          kk = __builtin_amdgcn_fdot2_f32_bf16(kq, kq, kk, false);
+        }
+      }
+      p += __shfl_xor(p, 32, kWave);
+      kk += __shfl_xor(kk, 32, kWave);
+      const float cn = cslice[zc];
+      const float u = cn + p + 3e-5f * (cn + kk);
+      if (have && u < __builtin_inff()) best[kt] = u;   // false for NaN
+    }
+  }
   bf16_sweep<kBf16KeyTiles>(s_ring0, s_ring1, s_ring2, s_ring3, fslice, cslice, n_stages, wave, lane, h, b, best,
                             bidx);
 
@@ -366,7 +444,7 @@ void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restri
   for (int kt = 0; kt < kBf16KeyTiles; ++kt) {
     const float ob = __shfl_xor(best[kt], 32, kWave);
     const int oi = __shfl_xor(bidx[kt], 32, kWave);
-    // a half that never saw a finite value holds index -1
+    // a half with no value below its starting bound holds index -1
     if (bidx[kt] < 0 || (oi >= 0 && (ob < best[kt] || (ob == best[kt] && oi < bidx[kt])))) {
       best[kt] = ob;
       bidx[kt] = oi;
@@ -562,11 +640,23 @@ __global__ void scatter_kernel(const int32_t* __restrict__ assign, int32_t* __re
 }
 
 // One wave per (slice, cluster): mean of the member keys, float64 sum.
+// A key row is read as 16-byte pieces: kLpr lanes per row, so one wave load
+// covers kRpl rows and four loads are in flight; each lane accumulates its
+// dims in float64 and the row groups are summed across lanes at the end.
+// With frag given, the wave also writes the next iteration's matrix operand
+// for this centroid (-2 op(c) in A-fragment order, and ||op(c)||^2), the work
+// prep_operand_kernel does for the first iteration; with zero_counts it
+// clears the cluster's count for the next assignment.
 template <class T>
-__global__ void centroid_sum_kernel(const T* __restrict__ keys, const int32_t* __restrict__ members,
-                                    const int32_t* __restrict__ offsets, const int32_t* __restrict__ counts,
-                                    const float* centroids_in, float* centroids_out, int stride,
-                                    int n_tokens, int n_clusters, int64_t n_rows) {
+__global__ void centroid_update_kernel(const T* __restrict__ keys, const int32_t* __restrict__ members,
+                                       const int32_t* __restrict__ offsets, int32_t* __restrict__ counts,
+                                       const float* centroids_in, float* centroids_out, int stride, int n_tokens,
+                                       int n_clusters, int64_t n_rows, uint4* __restrict__ frag,
+                                       float* __restrict__ cnorm, int n_ctiles, int zero_counts) {
+  constexpr int kDims = 16 / sizeof(T);          // dims per 16-byte piece (8 bf16, 4 fp32)
+  constexpr int kLpr = kHeadDim / kDims;         // lanes per row
+  constexpr int kRpl = kWave / kLpr;             // rows per wave load
+  constexpr int kUnroll = 4;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= n_rows) return;
   const int lane = threadIdx.x & 63;
@@ -575,6 +665,7 @@ __global__ void centroid_sum_kernel(const T* __restrict__ keys, const int32_t* _
   const int n = counts[s * n_clusters + c];
   float* dst = centroids_out + ((size_t)s * stride + c) * kHeadDim;
   if (n == 0) {
+    // empty: the centroid (and its operand from the previous preparation) stay
     if (centroids_in != centroids_out) {
       const float* src = centroids_in + ((size_t)s * stride + c) * kHeadDim;
       dst[2 * lane] = src[2 * lane];
@@ -585,35 +676,70 @@ __global__ void centroid_sum_kernel(const T* __restrict__ keys, const int32_t* _
   const int off = offsets[s * (n_clusters + 1) + c];
   const int32_t* mem = members + (size_t)s * n_tokens + off;
   const T* kslice = keys + (size_t)s * n_tokens * kHeadDim;
-  double a0 = 0.0, a1 = 0.0;
-  for (int m0 = 0; m0 < n; m0 += 64) {
+  const int sub = lane % kLpr, grp = lane / kLpr;
+  double acc[kDims];
+#pragma unroll
+  for (int e = 0; e < kDims; ++e) acc[e] = 0.0;
+  for (int m0 = 0; m0 < n; m0 += kWave) {
     const int mine = (m0 + lane < n) ? mem[m0 + lane] : 0;
-    const int cnt = min(64, n - m0);
-    int q = 0;
-    for (; q + 4 <= cnt; q += 4) {
-      float x[4][2];
+    const int cnt = min(kWave, n - m0);
+    for (int q = 0; q < cnt; q += kRpl * kUnroll) {
+      uint4 x[kUnroll];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int tok = __shfl(mine, q + u, kWave);
-        const T* r = kslice + (size_t)tok * kHeadDim;
-        x[u][0] = load_as_f32(r, 2 * lane);
-        x[u][1] = load_as_f32(r, 2 * lane + 1);
+      for (int u = 0; u < kUnroll; ++u) {
+        const int r = q + u * kRpl + grp;
+        const int tok = __shfl(mine, r & (kWave - 1), kWave);
+        x[u] = r < cnt ? reinterpret_cast<const uint4*>(kslice + (size_t)tok * kHeadDim)[sub]
+                       : make_uint4(0, 0, 0, 0);
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        a0 += (double)x[u][0];
-        a1 += (double)x[u][1];
+      for (int u = 0; u < kUnroll; ++u) {
+        const T* v = reinterpret_cast<const T*>(&x[u]);
+#pragma unroll
+        for (int e = 0; e < kDims; ++e) acc[e] += (double)load_as_f32(v, e);
       }
-    }
-    for (; q < cnt; ++q) {
-      const int tok = __shfl(mine, q, kWave);
-      const T* r = kslice + (size_t)tok * kHeadDim;
-      a0 += (double)load_as_f32(r, 2 * lane);
-      a1 += (double)load_as_f32(r, 2 * lane + 1);
     }
   }
-  dst[2 * lane] = (float)(a0 / (double)n);
-  dst[2 * lane + 1] = (float)(a1 / (double)n);
+#pragma unroll
+  for (int o = kLpr; o < kWave; o <<= 1)
+#pragma unroll
+    for (int e = 0; e < kDims; ++e) acc[e] += __shfl_xor(acc[e], o, kWave);
+  if (grp != 0) return;
+  // lanes 0..kLpr-1 hold dims kDims*lane ..
+  float mean[kDims];
+#pragma unroll
+  for (int e = 0; e < kDims; ++e) mean[e] = (float)(acc[e] / (double)n);
+  float4* d4 = reinterpret_cast<float4*>(dst + kDims * sub);
+#pragma unroll
+  for (int e = 0; e < kDims; e += 4) d4[e / 4] = make_float4(mean[e], mean[e + 1], mean[e + 2], mean[e + 3]);
+  if (zero_counts && sub == 0) counts[s * n_clusters + c] = 0;
+  if (!frag) return;
+  // next iteration's operand: same layout and values as prep_operand_kernel
+  const int t = c / kTileC, ci = c % kTileC;
+  const int d0 = kDims * sub, hh = d0 >> 6;
+  const int flane = hh * 32 + ci;
+  double nrm = 0.0;
+  if (sizeof(T) == 2) {
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) {
+      const float o0 = bf16_to_f32(f32_to_bf16(mean[e])), o1 = bf16_to_f32(f32_to_bf16(mean[e + 1]));
+      nrm += (double)o0 * o0 + (double)o1 * o1;
+      w[e / 2] = (uint32_t)f32_to_bf16(-2.f * o0) | ((uint32_t)f32_to_bf16(-2.f * o1) << 16);
+    }
+    const int step = (d0 & 63) >> 3;
+    frag[((size_t)s * n_ctiles + t) * kBf16TileU4 + step * 64 + flane] = make_uint4(w[0], w[1], w[2], w[3]);
+  } else {
+#pragma unroll
+    for (int e = 0; e < kDims; ++e) nrm += (double)mean[e] * mean[e];
+    const int step = d0 & 63;   // 4 consecutive steps, one float4 of the fp32 layout
+    float* f = reinterpret_cast<float*>(frag + ((size_t)s * n_ctiles + t) * kF32TileU4);
+    *reinterpret_cast<float4*>(f + ((size_t)(step >> 2) * 64 + flane) * 4) =
+        make_float4(-2.f * mean[0], -2.f * mean[1], -2.f * mean[2], -2.f * mean[3]);
+  }
+#pragma unroll
+  for (int o = 1; o < kLpr; o <<= 1) nrm += __shfl_xor(nrm, o, kWave);
+  if (sub == 0) cnorm[(size_t)s * n_ctiles * kTileC + c] = (float)nrm;
 }
 
 // One wave per (slice, cluster): member ids sorted ascending into perm (rank =
@@ -718,15 +844,16 @@ int launch_prep(const float* reps, int stride, int64_t S, int C, int dtype, cons
   return LOUISKV_OK;
 }
 
+// use_bound: assign holds a valid previous assignment (bf16 path only).
 int launch_assign(const void* keys, int dtype, int64_t S, int N, int C, const Ws& w, int32_t* assign,
-                  bool with_counts, hipStream_t st) {
+                  bool with_counts, bool use_bound, hipStream_t st) {
   const int n_ctiles = n_ctiles_for(C, dtype);
   if (dtype == LOUISKV_BF16) {
     const int bps = ceil_div(N, kBf16KeysPerBlock);
     const bool hist_lds = (size_t)C * 4 <= (size_t)kBf16StageBytes;
     assign_bf16_kernel<<<(unsigned)(S * bps), kBf16Threads, 0, st>>>(
         static_cast<const uint16_t*>(keys), w.frag, w.cnorm, assign, with_counts ? w.counts : nullptr, N, C,
-        n_ctiles, bps, hist_lds ? 1 : 0);
+        n_ctiles, bps, hist_lds ? 1 : 0, use_bound ? 1 : 0);
   } else {
     const int bps = ceil_div(N, kF32KeysPerBlock);
     size_t lds = (size_t)kF32StageTiles * (kF32TileU4 * 16 + kTileC * 4);
@@ -751,16 +878,22 @@ int launch_scan_scatter(const int32_t* assign, int64_t S, int N, int C, const Ws
   return LOUISKV_OK;
 }
 
+// Centroid update; with prep_next, also the next iteration's operand and
+// cleared counts (the work of launch_prep for the iterations after the first).
 int launch_sum(const void* keys, int dtype, int64_t S, int N, int C, const Ws& w, const float* cin, float* cout,
-               int stride, hipStream_t st) {
+               int stride, bool prep_next, hipStream_t st) {
   const int64_t rows = S * C;
   const int grid = (int)((rows + 3) / 4);
+  const int n_ctiles = n_ctiles_for(C, dtype);
+  uint4* frag = prep_next ? w.frag : nullptr;
   if (dtype == LOUISKV_BF16)
-    centroid_sum_kernel<uint16_t><<<grid, 256, 0, st>>>(static_cast<const uint16_t*>(keys), w.members, w.offsets,
-                                                         w.counts, cin, cout, stride, N, C, rows);
+    centroid_update_kernel<uint16_t><<<grid, 256, 0, st>>>(static_cast<const uint16_t*>(keys), w.members,
+                                                            w.offsets, w.counts, cin, cout, stride, N, C, rows, frag,
+                                                            w.cnorm, n_ctiles, prep_next ? 1 : 0);
   else
-    centroid_sum_kernel<float><<<grid, 256, 0, st>>>(static_cast<const float*>(keys), w.members, w.offsets,
-                                                      w.counts, cin, cout, stride, N, C, rows);
+    centroid_update_kernel<float><<<grid, 256, 0, st>>>(static_cast<const float*>(keys), w.members, w.offsets,
+                                                         w.counts, cin, cout, stride, N, C, rows, frag, w.cnorm,
+                                                         n_ctiles, prep_next ? 1 : 0);
   LKV_CHECK_LAUNCH();
   return LOUISKV_OK;
 }
@@ -844,13 +977,16 @@ extern "C" int louiskv_cluster_prefill(const void* keys, int32_t dtype, int64_t 
                                                          n_clusters, units_cap, rows);
     LKV_CHECK_LAUNCH();
   }
+  // the first operand comes from the initial centroids; after that each
+  // update writes the next one (and clears the counts) as it goes
+  if ((st = launch_prep(reps, units_cap, n_slices, n_clusters, dtype, w, true, s))) return st;
   for (int it = 0; it < n_iters; ++it) {
-    if ((st = launch_prep(reps, units_cap, n_slices, n_clusters, dtype, w, true, s))) return st;
     if (iter_events) LKV_CHECK_HIP(hipEventRecord(reinterpret_cast<hipEvent_t>(iter_events[2 * it]), s));
-    if ((st = launch_assign(keys, dtype, n_slices, n_tokens, n_clusters, w, assign, true, s))) return st;
+    if ((st = launch_assign(keys, dtype, n_slices, n_tokens, n_clusters, w, assign, true, it > 0, s))) return st;
     if (iter_events) LKV_CHECK_HIP(hipEventRecord(reinterpret_cast<hipEvent_t>(iter_events[2 * it + 1]), s));
     if ((st = launch_scan_scatter(assign, n_slices, n_tokens, n_clusters, w, s))) return st;
-    if ((st = launch_sum(keys, dtype, n_slices, n_tokens, n_clusters, w, reps, reps, units_cap, s))) return st;
+    if ((st = launch_sum(keys, dtype, n_slices, n_tokens, n_clusters, w, reps, reps, units_cap, it + 1 < n_iters, s)))
+      return st;
   }
   {
     const int64_t rows = n_slices * n_clusters;
@@ -890,7 +1026,7 @@ extern "C" int louiskv_kmeans_assign(const void* keys, int32_t dtype, int64_t n_
   const Ws w = carve(workspace, n_slices, n_tokens, n_clusters, dtype);
   hipStream_t s = as_stream(stream);
   if ((st = launch_prep(centroids, centroid_stride, n_slices, n_clusters, dtype, w, false, s))) return st;
-  return launch_assign(keys, dtype, n_slices, n_tokens, n_clusters, w, assign, false, s);
+  return launch_assign(keys, dtype, n_slices, n_tokens, n_clusters, w, assign, false, false, s);
 }
 
 extern "C" int louiskv_kmeans_update(const void* keys, int32_t dtype, int64_t n_slices, int32_t n_tokens, int32_t d,
@@ -914,7 +1050,7 @@ extern "C" int louiskv_kmeans_update(const void* keys, int32_t dtype, int64_t n_
   LKV_CHECK_LAUNCH();
   if ((st = launch_scan_scatter(assign, n_slices, n_tokens, n_clusters, w, s))) return st;
   if ((st = launch_sum(keys, dtype, n_slices, n_tokens, n_clusters, w, centroids_in, centroids_out,
-                       centroid_stride, s)))
+                       centroid_stride, false, s)))
     return st;
   if (counts)
     LKV_CHECK_HIP(hipMemcpyAsync(counts, w.counts, sizeof(int32_t) * n_slices * n_clusters,
