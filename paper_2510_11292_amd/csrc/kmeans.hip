@@ -328,10 +328,7 @@ __device__ __forceinline__ void bf16_sweep(char* __restrict__ r0, char* __restri
                                            int n_stages, int wave, int lane, int h,
                                            const bf16x8_t (&b)[kKT][kBf16Steps], float (&best)[kKT],
                                            int (&bidx)[kKT]) {
-  // prologue: the first kBf16Ring - 1 stages are copied before the sweep
-  stage_async(fslice, cslice, 0, r0, wave, lane);
-  if (n_stages > 1) stage_async(fslice, cslice, 1, r1, wave, lane);
-  if (n_stages > 2) stage_async(fslice, cslice, 2, r2, wave, lane);
+  // the first kBf16Ring - 1 stages were copied by the caller (bf16_prologue)
   for (int st = 0; st < n_stages; st += kBf16Ring) {
     bf16_stage<kKT>(r0, r3, fslice, cslice, st, n_stages, wave, lane, h, b, best, bidx);
     if (st + 1 >= n_stages) break;
@@ -343,6 +340,16 @@ __device__ __forceinline__ void bf16_sweep(char* __restrict__ r0, char* __restri
   }
 }
 
+// Copies of the first kBf16Ring - 1 stages, issued before anything else the
+// block loads, so their latency overlaps the key loads and the bound.
+__device__ __forceinline__ void bf16_prologue(char* __restrict__ r0, char* __restrict__ r1, char* __restrict__ r2,
+                                              const uint4* fslice, const float* cslice, int n_stages, int wave,
+                                              int lane) {
+  stage_async(fslice, cslice, 0, r0, wave, lane);
+  if (n_stages > 1) stage_async(fslice, cslice, 1, r1, wave, lane);
+  if (n_stages > 2) stage_async(fslice, cslice, 2, r2, wave, lane);
+}
+
 // bf16 keys: each wave holds kBf16KeyTiles tiles of 32 keys as MFMA B operands
 // for the whole sweep; centroid tiles stream through a ring of kBf16Ring LDS
 // stage buffers, copied kBf16Ring - 1 stages ahead.  Lane l owns key column
@@ -352,7 +359,8 @@ __global__ __launch_bounds__(kBf16Threads, 8 / kBf16Waves)
 void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restrict__ frag,
                         const float* __restrict__ cnorm, int32_t* __restrict__ assign,
                         int32_t* __restrict__ counts, int n_tokens, int n_clusters, int n_ctiles,
-                        int blocks_per_slice, int hist_in_lds, int use_bound) {
+                        int blocks_per_slice, int hist_in_lds, int use_bound, uint4* __restrict__ kswz,
+                        int kswz_mode) {
   __shared__ __align__(16) char s_ring0[kBf16StageBytes];
   __shared__ __align__(16) char s_ring1[kBf16StageBytes];
   __shared__ __align__(16) char s_ring2[kBf16StageBytes];
@@ -371,27 +379,46 @@ void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restri
   const float* cslice = cnorm + (size_t)slice * n_ctiles * kTileC;
   const int n_stages = n_ctiles / kBf16StageTiles;   // n_ctiles is padded to whole stages
 
-  bf16x8_t b[kBf16KeyTiles][kBf16Steps];
+  // Start-up latency is the block's fixed cost, so the loads that do not
+  // depend on each other are issued together: the ring's first copies, the
+  // previous assignment (for the bound), then the keys.
+  bf16_prologue(s_ring0, s_ring1, s_ring2, fslice, cslice, n_stages, wave, lane);
+  int zp[kBf16KeyTiles];
 #pragma unroll
   for (int kt = 0; kt < kBf16KeyTiles; ++kt) {
     const int key = key_base + kt * 32 + j;
-    const uint4* src = reinterpret_cast<const uint4*>(kslice + (size_t)key * kHeadDim + 64 * h);
+    zp[kt] = (use_bound && key < n_tokens) ? assign[(size_t)slice * n_tokens + key] : -1;
+  }
+  // Key operands.  In B-operand order a load instruction touches 64 rows
+  // (16 bytes of each), which makes the block's start slow; so the first
+  // iteration of a prefill also stores the operands in that order (kswz_mode
+  // 1, one contiguous KiB per instruction, padding keys zero), and the later
+  // iterations read them back contiguously (kswz_mode 2).
+  bf16x8_t b[kBf16KeyTiles][kBf16Steps];
+  uint4* zs = kswz + (((size_t)slice * blocks_per_slice + kb) * kBf16Waves + wave) * (kBf16KeyTiles * kBf16Steps * 64);
+  if (kswz_mode == 2) {
 #pragma unroll
-    for (int s = 0; s < kBf16Steps; ++s) {
-      uint4 v = key < n_tokens ? src[s] : make_uint4(0, 0, 0, 0);
-      b[kt][s] = __builtin_bit_cast(bf16x8_t, v);
+    for (int kt = 0; kt < kBf16KeyTiles; ++kt)
+#pragma unroll
+      for (int s = 0; s < kBf16Steps; ++s) b[kt][s] = __builtin_bit_cast(bf16x8_t, zs[(kt * kBf16Steps + s) * 64 + lane]);
+  } else {
+#pragma unroll
+    for (int kt = 0; kt < kBf16KeyTiles; ++kt) {
+      const int key = key_base + kt * 32 + j;
+      const uint4* src = reinterpret_cast<const uint4*>(kslice + (size_t)key * kHeadDim + 64 * h);
+#pragma unroll
+      for (int s = 0; s < kBf16Steps; ++s) {
+        uint4 v = key < n_tokens ? src[s] : make_uint4(0, 0, 0, 0);
+        b[kt][s] = __builtin_bit_cast(bf16x8_t, v);
+      }
+    }
+    if (kswz_mode == 1) {
+#pragma unroll
+      for (int kt = 0; kt < kBf16KeyTiles; ++kt)
+#pragma unroll
+        for (int s = 0; s < kBf16Steps; ++s) zs[(kt * kBf16Steps + s) * 64 + lane] = __builtin_bit_cast(uint4, b[kt][s]);
     }
   }
-  // the key operands are complete before the sweep starts, so no key load is
-  // pending inside the stage loop (the loop then only waits for its copies);
-  // the compiler does not read that wait, so every key register is also used
-  // here, which makes it complete the loads before the loop, not inside it
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-#pragma unroll
-  for (int kt = 0; kt < kBf16KeyTiles; ++kt)
-#pragma unroll
-    for (int s = 0; s < kBf16Steps; ++s) asm volatile("" ::"v"(b[kt][s]));
-
   // Starting bound.  From the second Lloyd iteration on, assign holds the
   // previous assignment; the key's distance to that centroid (computed on the
   // VALU over the same bf16 operands) plus a margin is an upper bound on the
@@ -406,12 +433,10 @@ void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restri
   for (int kt = 0; kt < kBf16KeyTiles; ++kt) {
     bidx[kt] = -1;
     best[kt] = __builtin_inff();
-    const int key = key_base + kt * 32 + j;
-    const int zp = (use_bound && key < n_tokens) ? assign[(size_t)slice * n_tokens + key] : -1;
-    const bool have = zp >= 0 && zp < n_clusters;
+    const bool have = zp[kt] >= 0 && zp[kt] < n_clusters;
     if (__builtin_amdgcn_ballot_w64(have)) {
       typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
-      const int zc = have ? zp : 0;
+      const int zc = have ? zp[kt] : 0;
       // the lane's 64 dimensions of -2 op(c): A-fragment row zc % 32, half h
       const uint4* f = fslice + (size_t)(zc / kTileC) * kBf16TileU4 + (zc % kTileC) + 32 * h;
       float p = 0.f, kk = 0.f;
@@ -435,6 +460,15 @@ void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restri
       if (have && u < __builtin_inff()) best[kt] = u;   // false for NaN
     }
   }
+  // the key operands are complete before the sweep starts, so no key load is
+  // pending inside the stage loop (the loop then only waits for its copies);
+  // the compiler does not read that wait, so every key register is also used
+  // here, which makes it complete the loads before the loop, not inside it
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int kt = 0; kt < kBf16KeyTiles; ++kt)
+#pragma unroll
+    for (int s = 0; s < kBf16Steps; ++s) asm volatile("" ::"v"(b[kt][s]));
   bf16_sweep<kBf16KeyTiles>(s_ring0, s_ring1, s_ring2, s_ring3, fslice, cslice, n_stages, wave, lane, h, b, best,
                             bidx);
 
@@ -802,6 +836,7 @@ struct Ws {
   int32_t* offsets;
   int32_t* cursor;
   int32_t* members;
+  uint4* kswz;   // bf16 key operands in B-operand order (kswz_mode of the assignment)
   size_t bytes;
 };
 
@@ -823,6 +858,9 @@ Ws carve(void* base, int64_t n_slices, int n_tokens, int n_clusters, int dtype) 
   w.offsets = cv.take<int32_t>((size_t)n_slices * (n_clusters + 1));
   w.cursor = cv.take<int32_t>((size_t)n_slices * n_clusters);
   w.members = cv.take<int32_t>((size_t)n_slices * n_tokens);
+  w.kswz = dtype == LOUISKV_BF16
+               ? cv.take<uint4>((size_t)n_slices * ceil_div(n_tokens, kBf16KeysPerBlock) * kBf16KeysPerBlock * 16)
+               : nullptr;
   w.bytes = align_up(cv.used, 256);
   return w;
 }
@@ -844,16 +882,17 @@ int launch_prep(const float* reps, int stride, int64_t S, int C, int dtype, cons
   return LOUISKV_OK;
 }
 
-// use_bound: assign holds a valid previous assignment (bf16 path only).
+// use_bound: assign holds a valid previous assignment; kswz_mode: 0 keys only,
+// 1 keys and store the operand copy, 2 read the copy (bf16 path only).
 int launch_assign(const void* keys, int dtype, int64_t S, int N, int C, const Ws& w, int32_t* assign,
-                  bool with_counts, bool use_bound, hipStream_t st) {
+                  bool with_counts, bool use_bound, int kswz_mode, hipStream_t st) {
   const int n_ctiles = n_ctiles_for(C, dtype);
   if (dtype == LOUISKV_BF16) {
     const int bps = ceil_div(N, kBf16KeysPerBlock);
     const bool hist_lds = (size_t)C * 4 <= (size_t)kBf16StageBytes;
     assign_bf16_kernel<<<(unsigned)(S * bps), kBf16Threads, 0, st>>>(
         static_cast<const uint16_t*>(keys), w.frag, w.cnorm, assign, with_counts ? w.counts : nullptr, N, C,
-        n_ctiles, bps, hist_lds ? 1 : 0, use_bound ? 1 : 0);
+        n_ctiles, bps, hist_lds ? 1 : 0, use_bound ? 1 : 0, w.kswz, kswz_mode);
   } else {
     const int bps = ceil_div(N, kF32KeysPerBlock);
     size_t lds = (size_t)kF32StageTiles * (kF32TileU4 * 16 + kTileC * 4);
@@ -982,7 +1021,8 @@ extern "C" int louiskv_cluster_prefill(const void* keys, int32_t dtype, int64_t 
   if ((st = launch_prep(reps, units_cap, n_slices, n_clusters, dtype, w, true, s))) return st;
   for (int it = 0; it < n_iters; ++it) {
     if (iter_events) LKV_CHECK_HIP(hipEventRecord(reinterpret_cast<hipEvent_t>(iter_events[2 * it]), s));
-    if ((st = launch_assign(keys, dtype, n_slices, n_tokens, n_clusters, w, assign, true, it > 0, s))) return st;
+    if ((st = launch_assign(keys, dtype, n_slices, n_tokens, n_clusters, w, assign, true, it > 0, it == 0 ? 1 : 2, s)))
+      return st;
     if (iter_events) LKV_CHECK_HIP(hipEventRecord(reinterpret_cast<hipEvent_t>(iter_events[2 * it + 1]), s));
     if ((st = launch_scan_scatter(assign, n_slices, n_tokens, n_clusters, w, s))) return st;
     if ((st = launch_sum(keys, dtype, n_slices, n_tokens, n_clusters, w, reps, reps, units_cap, it + 1 < n_iters, s)))
@@ -1026,7 +1066,7 @@ extern "C" int louiskv_kmeans_assign(const void* keys, int32_t dtype, int64_t n_
   const Ws w = carve(workspace, n_slices, n_tokens, n_clusters, dtype);
   hipStream_t s = as_stream(stream);
   if ((st = launch_prep(centroids, centroid_stride, n_slices, n_clusters, dtype, w, false, s))) return st;
-  return launch_assign(keys, dtype, n_slices, n_tokens, n_clusters, w, assign, false, false, s);
+  return launch_assign(keys, dtype, n_slices, n_tokens, n_clusters, w, assign, false, false, 0, s);
 }
 
 extern "C" int louiskv_kmeans_update(const void* keys, int32_t dtype, int64_t n_slices, int32_t n_tokens, int32_t d,
