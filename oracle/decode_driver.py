@@ -12,8 +12,13 @@ Per decode step t, in the order of Algorithm 1's decode phase:
      gather of the selected rows into KV_critical;
   3. store_cache for the decode stage: the new (k_t, v_t) enters the local
      window.  If the window already holds `window` tokens, its oldest
-     `seg_len` tokens leave first: their mean key becomes a new unit's index
-     vector and their rows are appended to the pool (Section 4.2 decode stage);
+     segment leaves first: its mean key becomes a new unit's index vector and
+     its rows are appended to the pool (Section 4.2 decode stage).  Segments
+     are either fixed runs of `seg_len` tokens (segments="fixed") or
+     delimited by the boundaries of step 1 (segments="boundary": Section 4.2
+     partitions the generated KV at the semantic boundaries of Section 4.1;
+     a segment also closes once it holds `seg_len` tokens, so that a full
+     window always holds a closed segment, and seg_len < window is required);
   4. attention of each query head over [KV_critical : KV_local], the current
      token included.
 KV_critical is kept unchanged between boundaries.
@@ -57,6 +62,14 @@ def prefill_state_from_kmeans(prompt_keys: Sequence, prompt_values: Sequence,
     return PrefillState(reps, starts, sizes, kp, vp)
 
 
+def opens_segment(fire: bool, gen: int, open_first: Optional[int], seg_max: int) -> bool:
+    """Boundary-delimited segments: token `gen` starts a new segment when there
+    is no open one, when this step is a semantic boundary (Section 4.1, the
+    is_new_segment of Algorithm 1), or when the open segment (first token
+    open_first) already holds seg_max tokens."""
+    return open_first is None or fire or gen - open_first >= seg_max
+
+
 @dataclass
 class StepRecord:
     t: int
@@ -73,9 +86,15 @@ class StepRecord:
 class GroupDecoder:
     def __init__(self, prefill: PrefillState, n_q_heads: int, budget: int,
                  window: int, seg_len: int, tau: float, mode: str = "anchor",
-                 scale: Optional[float] = None):
+                 scale: Optional[float] = None, segments: str = "fixed"):
         if mode not in ("prev", "anchor"):
             raise ValueError(mode)
+        if segments not in ("fixed", "boundary"):
+            raise ValueError(segments)
+        if segments == "boundary" and not 1 <= seg_len < window:
+            raise ValueError("boundary segments need 1 <= seg_len < window")
+        self.segments = segments
+        self.seg_first = deque()   # boundary mode: first generation index of each segment in the window
         self.h_kv = len(prefill.reps)
         self.g = n_q_heads // self.h_kv
         self.d = prefill.reps[0].shape[1]
@@ -136,20 +155,31 @@ class GroupDecoder:
                 sels.append(chosen)
 
         evicted = None
+        gen = self.t - 1                      # generation index of this step's token
+        new_segment = False
+        if self.segments == "boundary":
+            new_segment = opens_segment(fire, gen, self.seg_first[-1] if self.seg_first else None, self.seg_len)
         if len(self.local[0]) >= self.window:
             evicted = self.n_units()
+            if self.segments == "fixed":
+                n_leave = self.seg_len
+            else:
+                first = self.seg_first.popleft()
+                n_leave = (self.seg_first[0] if self.seg_first else gen) - first
             for h in range(self.h_kv):
-                seg = [self.local[h].popleft() for _ in range(self.seg_len)]
+                seg = [self.local[h].popleft() for _ in range(n_leave)]
                 seg_k = np.stack([s[1] for s in seg])
                 seg_v = np.stack([s[2] for s in seg])
                 self.reps[h].append(segment_mean(seg_k))
                 self.unit_start[h].append(self.n_prompt + seg[0][0])
-                self.unit_size[h].append(self.seg_len)
+                self.unit_size[h].append(n_leave)
                 self.k_pool[h].extend(list(seg_k))
                 self.v_pool[h].extend(list(seg_v))
             self.n_evicted += 1
+        if new_segment:
+            self.seg_first.append(gen)
         for h in range(self.h_kv):
-            self.local[h].append((self.t - 1, k_t[h], v_t[h]))
+            self.local[h].append((gen, k_t[h], v_t[h]))
 
         out = np.zeros((self.h_kv * self.g, self.d))
         lse = np.zeros(self.h_kv * self.g)

@@ -399,5 +399,62 @@ def pin_decode_boundary_modes(orc):
     assert 0.18 < rates["anchor"] < 0.35, rates
 
 
-DECODE_PINS = [pin_decode_dense_special_case, pin_decode_frozen_and_schedule, pin_decode_boundary_modes]
+def pin_decode_boundary_segments(orc):
+    """Boundary-delimited segments.  (1) When only the first step fires, the
+    segments are the seg_len-token runs of the fixed scheme, so the two
+    decoders agree step for step.  (2) When every step fires, every segment is
+    one token: from step W+1 on each step evicts the token W steps back, as a
+    unit of size 1 whose index vector is that key.  (3) For an arbitrary fire
+    pattern the evicted units tile the generated tokens in order, none is
+    longer than seg_len, each starts at a fired step or right after a unit of
+    exactly seg_len tokens, the window never holds more than W tokens, a
+    segment leaves exactly when the window held W tokens before the step, and
+    every index vector is the mean of its unit's rows."""
+    pk, pv, gk, gv, q = _tiny_group(22, t=120)
+    h_kv, p, d = pk.shape
+    # (1)
+    a = orc.GroupDecoder(_prefill(orc, pk, pv, 8), q.shape[1], 40, 32, 8, -1.5, "anchor")
+    b = orc.GroupDecoder(_prefill(orc, pk, pv, 8), q.shape[1], 40, 32, 8, -1.5, "anchor", segments="boundary")
+    for t in range(q.shape[0]):
+        ra, rb = a.step(q[t], gk[t], gv[t]), b.step(q[t], gk[t], gv[t])
+        assert ra.evicted_unit == rb.evicted_unit and np.array_equal(ra.out, rb.out)
+    assert a.unit_size == b.unit_size and a.unit_start == b.unit_start
+    # (2)
+    dec = orc.GroupDecoder(_prefill(orc, pk, pv, 8), q.shape[1], 40, 16, 4, 1.5, "prev", segments="boundary")
+    for t in range(q.shape[0]):
+        rec = dec.step(q[t], gk[t], gv[t])
+        assert rec.fire
+        if t < 16:
+            assert rec.evicted_unit is None
+        else:
+            u = rec.evicted_unit
+            assert u == 8 + t - 16
+            for h in range(h_kv):
+                assert dec.unit_size[h][u] == 1 and dec.unit_start[h][u] == p + t - 16
+                assert np.array_equal(dec.reps[h][u], gk[t - 16, h].astype(np.float32))
+    # (3)
+    rng = RNG(23)
+    W, smax = 24, 5
+    fires = rng.random(q.shape[0]) < 0.3
+    dec = orc.GroupDecoder(_prefill(orc, pk, pv, 8), q.shape[1], 40, W, smax, 0.9, "anchor", segments="boundary")
+    for t in range(q.shape[0]):
+        before = len(dec.local[0])
+        rec = dec.step(q[t], gk[t], gv[t], fire_override=bool(fires[t]) or t == 0)
+        assert len(dec.local[0]) <= W
+        assert (rec.evicted_unit is not None) == (before == W)
+        left = dec.unit_size[0][rec.evicted_unit] if rec.evicted_unit is not None else 0
+        assert len(dec.local[0]) == before - left + 1
+    for h in range(h_kv):
+        starts, sizes = dec.unit_start[h][8:], dec.unit_size[h][8:]
+        assert starts[0] == p and all(x + n == y for x, n, y in zip(starts, sizes, starts[1:]))
+        assert all(1 <= n <= smax for n in sizes)
+        for i, (st, n) in enumerate(zip(starts, sizes)):
+            g0 = st - p
+            assert g0 == 0 or fires[g0] or sizes[i - 1] == smax
+            assert np.array_equal(dec.reps[h][8 + i], gk[g0:g0 + n, h].mean(0).astype(np.float32))
+        assert starts[-1] + sizes[-1] - p + len(dec.local[h]) == q.shape[0]
+
+
+DECODE_PINS = [pin_decode_dense_special_case, pin_decode_frozen_and_schedule, pin_decode_boundary_modes,
+               pin_decode_boundary_segments]
 ALL_PINS = ALL_PINS + DECODE_PINS

@@ -105,6 +105,18 @@ def _segment_mean_f64(rows):
     return r.sum(0) / (r.shape[0] - 1)
 
 
+def _opens_no_cap(fire, gen, open_first, seg_max):
+    return open_first is None or fire
+
+
+def _opens_cap_late(fire, gen, open_first, seg_max):
+    return open_first is None or fire or gen - open_first > seg_max
+
+
+def _opens_ignores_fire(fire, gen, open_first, seg_max):
+    return open_first is None or gen - open_first >= seg_max
+
+
 MUTATIONS = {
     "distance_cross_term_sign": ("squared_distances", _sqdist_plus),
     "distance_dropped_centroid_norm": ("squared_distances", _sqdist_no_cnorm),
@@ -121,6 +133,9 @@ MUTATIONS = {
     "attention_keys_as_values": ("attention", _attention_k_as_v),
     "attention_scale_dropped": ("attention", _attention_no_scale),
     "segment_mean_wrong_count": ("segment_mean", _segment_mean_f64),
+    "segment_without_length_cap": ("opens_segment", _opens_no_cap),
+    "segment_cap_one_late": ("opens_segment", _opens_cap_late),
+    "segment_ignores_boundary": ("opens_segment", _opens_ignores_fire),
 }
 
 
