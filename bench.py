@@ -98,7 +98,15 @@ def time_attention(eng, wl, reps=20):
     st = torch.cuda.current_stream()
 
     def launch():
-        if eng.zero_copy:
+        if eng.seg_state is not None:
+            if eng.zero_copy:
+                L.sparse_decode_attn_rows_seg(q, c.n_kv_heads, eng.k_pool, eng.v_pool, eng.sel_rows, eng.n_sel,
+                                              eng.k_local, eng.v_local, eng.seg_state, t + 1, eng.out, eng.lse,
+                                              workspace=eng.ws_attn, stream=st)
+            else:
+                L.sparse_decode_attn_seg(q, c.n_kv_heads, eng.k_buf, eng.v_buf, eng.n_sel, eng.k_local, eng.v_local,
+                                         eng.seg_state, t + 1, eng.out, eng.lse, workspace=eng.ws_attn, stream=st)
+        elif eng.zero_copy:
             L.sparse_decode_attn_rows(q, c.n_kv_heads, eng.k_pool, eng.v_pool, eng.sel_rows, eng.n_sel,
                                       eng.k_local, eng.v_local, local_start, n_local, eng.out, eng.lse,
                                       workspace=eng.ws_attn, stream=st)
@@ -116,7 +124,10 @@ def time_attention(eng, wl, reps=20):
     sec = e0.elapsed_time(e1) / reps / 1e3
     esz = eng.k_local.element_size()
     n_sel = int(eng.n_sel.sum())
-    rows = n_sel + c.n_slices * n_local
+    if eng.seg_state is not None:   # each slice's window from its first live token
+        rows = n_sel + int((t + 1 - eng.seg_state[:, 1].long()).clamp(0, c.window).sum())
+    else:
+        rows = n_sel + c.n_slices * n_local
     nbytes = rows * 2 * c.head_dim * esz + 2 * c.n_groups * c.n_q_heads * c.head_dim * esz
     if eng.zero_copy:
         nbytes += 4 * n_sel            # the row list
@@ -233,6 +244,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="li-so-32k")
     ap.add_argument("--mode", default="anchor", choices=["anchor", "prev"])
+    ap.add_argument("--segments", default="fixed", choices=["fixed", "boundary"],
+                    help="output segments: fixed runs (the workload's definition) or delimited by the boundaries")
     ap.add_argument("--cpu-budget-s", type=float, default=12.0,
                     help="seconds of oracle k-means, and again of oracle decode steps, in the CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -260,7 +273,7 @@ def main() -> int:
     wl = synth.get_workload(args.workload)
     mode = L.REF_ANCHOR if args.mode == "anchor" else L.REF_PREV
     data = make_inputs(wl, dev)
-    cfg = config_from_workload(wl, mode=mode)
+    cfg = config_from_workload(wl, mode=mode, segments=args.segments)
     dtype = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
     eng = LouisKVEngine(cfg, dtype, dev, pool_on_host=wl.pool_on_host)
 
@@ -346,7 +359,8 @@ def main() -> int:
             "q_heads": wl.n_q_heads, "head_dim": wl.head_dim, "prompt_tokens": wl.prompt_len,
             "clusters": wl.n_clusters, "lloyd_iters": wl.n_iters, "decode_steps": wl.gen_len,
             "budget": wl.budget, "window": wl.window, "segment": wl.seg_len, "tau": wl.tau,
-            "ref_mode": args.mode, "decode_launch": "eager" if graph is None else "hip_graph",
+            "ref_mode": args.mode, "segments": args.segments,
+            "decode_launch": "eager" if graph is None else "hip_graph",
             "kv_critical": "pool row list (zero-copy)" if eng.zero_copy else "gathered copy",
         },
         "decode_steps_per_s": wl.gen_len / t_dec,

@@ -379,6 +379,124 @@ int louiskv_sparse_decode_attn_rows(const void* q, int32_t dtype, int64_t n_slic
                                     void* out, int32_t out_dtype, float* lse_out,
                                     void* workspace, size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------------ */
+/* Decode stage with boundary-delimited segments                             */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Section 4.2 (decode stage) partitions the generated KV cache into temporal
+ * segments at the semantic boundaries of Section 4.1 (Algorithm 1's
+ * is_new_segment); these calls implement that variant of store_cache,
+ * Retrieve and attention.  A token starts a new segment when its group fired
+ * this step, when no segment is open, or when the open segment already holds
+ * seg_max tokens (the cap keeps a closed segment in every full window;
+ * 1 <= seg_max < window).  Before a token is stored, if the window already
+ * holds `window` tokens, its oldest segment leaves: it becomes the next unit
+ * (index vector = mean key, float64 sum with one rounding to float32) and its
+ * rows go to the pool.  Segment boundaries are per (sequence, layer) group,
+ * so every slice of a group has the same segments.
+ *
+ * seg_state  [n_slices][louiskv_segment_state_ints(window)] int32, owned by
+ *            the caller and private to the library: the window bounds, the
+ *            unit count and the open segments of each slice.  Set it up with
+ *            louiskv_segment_state_init after the prefill, before step 0.
+ *            Entry 0 of a slice is its unit count (clusters plus segments
+ *            evicted so far), entry 4 is 1 if a segment could not become a
+ *            unit because units_cap or pool_rows was exhausted (its tokens
+ *            are then no longer attended).
+ */
+size_t louiskv_segment_state_ints(int32_t window);
+
+/*
+ * The segment state before the first decode step: n_clusters units (the
+ * clusters of the prefill), an empty window.  Enqueued on `stream`.
+ */
+int louiskv_segment_state_init(int32_t* seg_state, int64_t n_slices, int32_t window,
+                               int32_t n_clusters, void* stream);
+
+/*
+ * Algorithm 1 store_cache(decode) with boundary-delimited segments (see
+ * above), for every slice at decode step `step` (0-based; steps must be
+ * issued in order, starting from 0).
+ * fire       [n_groups] uint8, this step's boundary decisions
+ *            (louiskv_boundary_check), n_groups = n_slices / n_kv_heads; NULL
+ *            means no group fired (step 0 always opens a segment).
+ * A unit created here has unit_start = prompt_len + (generation index of its
+ * first token) and unit_size = its token count; the pool needs
+ * pool_rows >= prompt_len + step + 1.  Other arguments as
+ * louiskv_segment_output.
+ */
+int louiskv_segment_output_boundary(const void* k_new, const void* v_new, int32_t dtype,
+                                    int64_t n_slices, int32_t n_kv_heads, int32_t d,
+                                    void* k_local, void* v_local, int32_t window,
+                                    int32_t step, int32_t seg_max, const uint8_t* fire,
+                                    int32_t* seg_state, float* reps, int32_t* unit_start,
+                                    int32_t* unit_size, int32_t units_cap, int32_t n_clusters,
+                                    void* k_pool, void* v_pool, int64_t pool_rows,
+                                    int32_t prompt_len, int32_t pool_on_host, void* stream);
+
+/*
+ * louiskv_retrieve (Appendix B scores, Section 3.1 budget, Algorithm 1
+ * Retrieve) where each slice scores its own units 0 .. n_units[s]-1, the
+ * count kept in seg_state; max_units bounds those counts for every slice
+ * (1 <= max_units <= min(units_cap, 8192)) and sizes the sort.  Workspace as
+ * louiskv_retrieve_workspace_size().
+ */
+int louiskv_retrieve_seg(const void* q, int32_t dtype, int64_t n_slices,
+                         int32_t n_kv_heads, int32_t group_size, int32_t d, double scale,
+                         const float* reps, const int32_t* unit_start,
+                         const int32_t* unit_size, int32_t units_cap, int32_t max_units,
+                         const int32_t* seg_state, int32_t window,
+                         const void* k_pool, const void* v_pool, int64_t pool_rows,
+                         int32_t pool_on_host, int32_t budget, const uint8_t* fire,
+                         int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel,
+                         void* k_buf, void* v_buf, double* scores_out,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * louiskv_retrieve_rows with per-slice unit counts from seg_state (as
+ * louiskv_retrieve_seg).  Workspace as louiskv_retrieve_rows_workspace_size().
+ */
+int louiskv_retrieve_rows_seg(const void* q, int32_t dtype, int64_t n_slices,
+                              int32_t n_kv_heads, int32_t group_size, int32_t d, double scale,
+                              const float* reps, const int32_t* unit_start,
+                              const int32_t* unit_size, int32_t units_cap, int32_t max_units,
+                              const int32_t* seg_state, int32_t window, int32_t budget,
+                              const uint8_t* fire, int32_t* sel_units, int32_t* n_sel_units,
+                              int32_t* n_sel, int32_t* sel_rows, double* scores_out,
+                              void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * louiskv_sparse_decode_attn (Section 3.1 over [KV_critical : KV_local]) where
+ * each slice's live window comes from seg_state: the tokens from its first
+ * live token up to n_tokens - 1, with n_tokens the number of generated
+ * tokens stored so far (step + 1 after this step's store).  Workspace as
+ * louiskv_sparse_decode_attn_workspace_size().
+ */
+int louiskv_sparse_decode_attn_seg(const void* q, int32_t dtype, int64_t n_slices,
+                                   int32_t n_kv_heads, int32_t group_size, int32_t d,
+                                   float scale, const void* k_buf, const void* v_buf,
+                                   const int32_t* n_sel, int32_t buf_rows,
+                                   const void* k_local, const void* v_local, int32_t window,
+                                   const int32_t* seg_state, int32_t n_tokens,
+                                   void* out, int32_t out_dtype, float* lse_out,
+                                   void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * louiskv_sparse_decode_attn_rows with per-slice windows from seg_state (as
+ * louiskv_sparse_decode_attn_seg).  Workspace as
+ * louiskv_sparse_decode_attn_rows_workspace_size().
+ */
+int louiskv_sparse_decode_attn_rows_seg(const void* q, int32_t dtype, int64_t n_slices,
+                                        int32_t n_kv_heads, int32_t group_size, int32_t d,
+                                        float scale, const void* k_pool, const void* v_pool,
+                                        int64_t pool_rows, const int32_t* sel_rows,
+                                        const int32_t* n_sel, int32_t budget,
+                                        const void* k_local, const void* v_local, int32_t window,
+                                        const int32_t* seg_state, int32_t n_tokens,
+                                        void* out, int32_t out_dtype, float* lse_out,
+                                        void* workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

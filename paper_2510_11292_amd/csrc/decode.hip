@@ -11,6 +11,13 @@ namespace {
 constexpr int kMaxGroupSize = 8;
 constexpr int kMaxUnits = 8192;
 
+// Per-slice state of a local window with boundary-delimited segments (int32):
+// units so far, first token (generation index) in the window, the ring of
+// segment first tokens (oldest at head, count entries, the last one open),
+// and a flag set when a segment could not become a unit (unit table full).
+constexpr int kSegNUnits = 0, kSegWinFirst = 1, kSegHead = 2, kSegCount = 3, kSegOverflow = 4;
+constexpr int kSegRing = 8;   // the ring of `window` entries starts here
+
 // ------------------------------------------------------------------ boundary
 
 // Sum over the 16 lanes of a DPP row for a float64 (two 32-bit DPP moves per step).
@@ -158,6 +165,101 @@ void store_decode_kernel(const T* __restrict__ k_new, const T* __restrict__ v_ne
   v_local[o + 1] = v_new[n + 1];
 }
 
+// store_cache(decode) with boundary-delimited segments, one wave per slice.
+// Token `step` opens a new segment when its group fired, when no segment is
+// open, or when the open one already holds seg_max tokens.  If the window
+// already holds `window` tokens, the oldest segment (closed: seg_max < window)
+// leaves first: its mean key (float64 sum, one rounding) becomes unit
+// n_units with pool rows prompt_len + its first token .. (tokens leave in
+// order, so a token's pool row is prompt_len + its generation index).  Then
+// the token goes to ring slot step % window.  The state starts from
+// seg_state_init_kernel.
+template <class T>
+__global__ __launch_bounds__(64)
+void store_segmented_kernel(const T* __restrict__ k_new, const T* __restrict__ v_new, T* __restrict__ k_local,
+                            T* __restrict__ v_local, int window, int step, int seg_max,
+                            const uint8_t* __restrict__ fire, int n_kv_heads, int32_t* __restrict__ state,
+                            float* __restrict__ reps, int32_t* __restrict__ unit_start,
+                            int32_t* __restrict__ unit_size, int units_cap, int n_clusters, T* __restrict__ k_pool,
+                            T* __restrict__ v_pool, int64_t pool_rows, int prompt_len) {
+  const int64_t s = blockIdx.x;
+  const int lane = threadIdx.x;
+  int32_t* st = state + s * (kSegRing + window);
+  int32_t* ring = st + kSegRing;
+  int n_units = st[kSegNUnits], win_first = st[kSegWinFirst], head = st[kSegHead], count = st[kSegCount],
+      overflow = st[kSegOverflow];
+  const bool fired = fire && fire[s / n_kv_heads] != 0;
+  const int open_first = count > 0 ? ring[(head + count - 1) % window] : -1;
+  const bool opens = count == 0 || fired || step - open_first >= seg_max;
+  const size_t lbase = (size_t)s * window * kHeadDim;
+  if (step - win_first >= window && count > 0) {
+    const int a = ring[head];
+    const int b = count > 1 ? ring[(head + 1) % window] : step;
+    const int len = b - a;
+    const int64_t prow = (int64_t)prompt_len + a;
+    const bool room = n_units < units_cap && prow + len <= pool_rows;
+    double a0 = 0.0, a1 = 0.0;
+    for (int r = 0; r < len; ++r) {
+      const size_t o = lbase + (size_t)((a + r) % window) * kHeadDim + 2 * lane;
+      const T k0 = k_local[o], k1 = k_local[o + 1];
+      a0 += (double)load_as_f32(&k0, 0);
+      a1 += (double)load_as_f32(&k1, 0);
+      if (k_pool && room) {
+        const size_t po = ((size_t)s * pool_rows + prow + r) * kHeadDim + 2 * lane;
+        k_pool[po] = k0;
+        k_pool[po + 1] = k1;
+        if (v_pool) {
+          v_pool[po] = v_local[o];
+          v_pool[po + 1] = v_local[o + 1];
+        }
+      }
+    }
+    if (room) {
+      float* rep = reps + ((size_t)s * units_cap + n_units) * kHeadDim;
+      rep[2 * lane] = (float)(a0 / (double)len);
+      rep[2 * lane + 1] = (float)(a1 / (double)len);
+      if (lane == 0) {
+        unit_start[s * units_cap + n_units] = (int32_t)prow;
+        unit_size[s * units_cap + n_units] = len;
+      }
+      ++n_units;
+    } else {
+      overflow = 1;   // no room for the unit: its tokens are no longer attended
+    }
+    head = (head + 1) % window;
+    --count;
+    win_first = b;
+    __syncthreads();   // the evicted rows are read before the new token overwrites the first slot
+  }
+  if (opens) {
+    if (lane == 0) ring[(head + count) % window] = step;
+    ++count;
+  }
+  const int slot = step % window;
+  const size_t o = lbase + (size_t)slot * kHeadDim + 2 * lane;
+  const size_t n = (size_t)s * kHeadDim + 2 * lane;
+  k_local[o] = k_new[n];
+  k_local[o + 1] = k_new[n + 1];
+  v_local[o] = v_new[n];
+  v_local[o + 1] = v_new[n + 1];
+  if (lane == 0) {
+    st[kSegNUnits] = n_units;
+    st[kSegWinFirst] = win_first;
+    st[kSegHead] = head;
+    st[kSegCount] = count;
+    st[kSegOverflow] = overflow;
+  }
+}
+
+// The state before the first decode step: the clusters are the only units,
+// the window is empty.
+__global__ void seg_state_init_kernel(int32_t* __restrict__ state, int64_t n_slices, int stride, int n_clusters) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_slices * stride) return;
+  const int e = (int)(i % stride);
+  state[i] = e == kSegNUnits ? n_clusters : 0;
+}
+
 // ------------------------------------------------------------------ retrieve
 
 #ifndef LKV_SEL_THREADS
@@ -214,14 +316,15 @@ template <class T, int G>
 __global__ __launch_bounds__(kSelThreads)
 void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, const float* __restrict__ reps,
                          const int32_t* __restrict__ unit_start, const int32_t* __restrict__ unit_size,
-                         int units_cap, int n_units, int budget, const uint8_t* __restrict__ fire,
+                         int units_cap, int n_units_arg, int budget, const uint8_t* __restrict__ fire,
                          int32_t* __restrict__ sel_units, int32_t* __restrict__ n_sel_units,
                          int32_t* __restrict__ n_sel, double* __restrict__ scores_out,
-                         double* __restrict__ logit_ws, int32_t* __restrict__ row_ws, int n_pad) {
+                         double* __restrict__ logit_ws, int32_t* __restrict__ row_ws, int n_pad_arg,
+                         const int32_t* __restrict__ seg_state, int seg_stride) {
   extern __shared__ __align__(16) char smem[];
-  uint64_t* s_key = reinterpret_cast<uint64_t*>(smem);            // [n_pad]
-  int* s_size = reinterpret_cast<int*>(s_key + n_pad);            // [n_pad] unit sizes by unit id
-  int* s_incl = s_size + n_pad;                                    // [n_pad] inclusive size sums by rank
+  uint64_t* s_key = reinterpret_cast<uint64_t*>(smem);            // [n_pad_arg]
+  int* s_size = reinterpret_cast<int*>(s_key + n_pad_arg);        // [n_pad_arg] unit sizes by unit id
+  int* s_incl = s_size + n_pad_arg;                                // [n_pad_arg] inclusive size sums by rank
   __shared__ double s_rm[G][kSelWaves], s_rz[G][kSelWaves];
   __shared__ double s_m[G], s_z[G];
   __shared__ int s_ntake;
@@ -230,6 +333,14 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
   const int64_t s = blockIdx.x;
   const int64_t grp = s / n_kv_heads;
   if (fire && !fire[grp]) return;
+  // with boundary-delimited segments each slice has its own unit count (the
+  // argument is then an upper bound that sized the LDS)
+  int n_units = n_units_arg, n_pad = n_pad_arg;
+  if (seg_state) {
+    n_units = min(max(seg_state[s * seg_stride + kSegNUnits], 1), n_units_arg);
+    n_pad = 64;
+    while (n_pad < n_units) n_pad <<= 1;
+  }
   const int kvh = (int)(s - grp * n_kv_heads);
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -562,6 +673,16 @@ __device__ __forceinline__ void attn_block_merge(const float (*s_m)[G], const fl
   }
 }
 
+// With boundary-delimited segments the window of slice s holds the tokens
+// from its first token (state) to n_tokens - 1; otherwise the arguments hold.
+__device__ __forceinline__ void slice_window(const int32_t* seg_state, int seg_stride, int64_t s, int window,
+                                             int n_tokens, int& local_start, int& n_local) {
+  if (!seg_state) return;
+  const int wf = seg_state[s * seg_stride + kSegWinFirst];
+  n_local = min(max(n_tokens - wf, 0), window);
+  local_start = wf >= 0 ? wf % window : 0;
+}
+
 // Block (chunk, slice): online softmax over the chunk's share of rows for the G
 // query heads of the slice, in base 2 (logits scaled by log2 e / sqrt d);
 // 16 lanes per row, lane sub owns dims 8*sub..+7, and each of the 64 row groups
@@ -575,9 +696,10 @@ __global__ __launch_bounds__((attn_waves<T, G>() * 64))
 void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, const T* __restrict__ k_buf,
                          const T* __restrict__ v_buf, const int32_t* __restrict__ n_sel, int buf_rows,
                          const int32_t* __restrict__ rows, int64_t src_rows,
-                         const T* __restrict__ k_local, const T* __restrict__ v_local, int window, int local_start,
-                         int n_local, int n_chunks, float* __restrict__ part, void* __restrict__ out, int out_bf16,
-                         float* __restrict__ lse_out) {
+                         const T* __restrict__ k_local, const T* __restrict__ v_local, int window, int local_start_arg,
+                         int n_local_arg, int n_chunks, float* __restrict__ part, void* __restrict__ out, int out_bf16,
+                         float* __restrict__ lse_out, const int32_t* __restrict__ seg_state, int seg_stride,
+                         int n_tokens) {
   extern __shared__ int s_rows[];     // kIdx: the chunk's entries of the row list
   constexpr int R = attn_rows_in_flight<T, G>();
   constexpr int kAttnWaves = attn_waves<T, G>();
@@ -590,6 +712,8 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
   const int64_t grp = s / n_kv_heads;
   const int kvh = (int)(s - grp * n_kv_heads);
   const int tid = threadIdx.x, sub = tid & 15, rg = tid >> 4;   // 64 row groups of 16 lanes
+  int local_start = local_start_arg, n_local = n_local_arg;
+  slice_window(seg_state, seg_stride, s, window, n_tokens, local_start, n_local);
   const int nsel = max(0, min(n_sel[s], buf_rows));
   const int total = nsel + n_local;
   const int r0 = (int)((int64_t)total * chunk / n_chunks);
@@ -751,8 +875,9 @@ void attn_mfma_kernel(const uint16_t* __restrict__ q, int n_kv_heads, float scal
                       const uint16_t* __restrict__ v_buf, const int32_t* __restrict__ n_sel, int buf_rows,
                       const int32_t* __restrict__ rows, int64_t src_rows,
                       const uint16_t* __restrict__ k_local, const uint16_t* __restrict__ v_local, int window,
-                      int local_start, int n_local, int n_chunks, float* __restrict__ part, void* __restrict__ out,
-                      int out_bf16, float* __restrict__ lse_out) {
+                      int local_start_arg, int n_local_arg, int n_chunks, float* __restrict__ part,
+                      void* __restrict__ out, int out_bf16, float* __restrict__ lse_out,
+                      const int32_t* __restrict__ seg_state, int seg_stride, int n_tokens) {
   extern __shared__ int s_rows[];     // kIdx: the chunk's entries of the row list
   constexpr int NW = attn_mfma_waves<G>();
   constexpr int NM = G == 8 ? 2 : 1;        // matrix ops per k-chunk, 4 heads each
@@ -766,6 +891,8 @@ void attn_mfma_kernel(const uint16_t* __restrict__ q, int n_kv_heads, float scal
   const int kvh = (int)(s - grp * n_kv_heads);
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, p16 = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);    // wave-uniform, kept in a scalar register
+  int local_start = local_start_arg, n_local = n_local_arg;
+  slice_window(seg_state, seg_stride, s, window, n_tokens, local_start, n_local);
   const int nsel = max(0, min(n_sel[s], buf_rows));
   const int total = nsel + n_local;
   const int r0 = (int)((int64_t)total * chunk / n_chunks);
@@ -1037,6 +1164,65 @@ extern "C" int louiskv_segment_output(const void* k_new, const void* v_new, int3
   return LOUISKV_OK;
 }
 
+extern "C" size_t louiskv_segment_state_ints(int32_t window) {
+  return window >= 2 ? (size_t)(kSegRing + window) : 0;
+}
+
+extern "C" int louiskv_segment_state_init(int32_t* seg_state, int64_t n_slices, int32_t window, int32_t n_clusters,
+                                          void* stream) {
+  if (!seg_state) return fail(LOUISKV_ERR_NULL, "seg_state is required");
+  if (window < 2 || n_slices < 1 || n_clusters < 1)
+    return fail(LOUISKV_ERR_SHAPE, "window=%d n_slices=%lld n_clusters=%d", window, (long long)n_slices, n_clusters);
+  const int stride = kSegRing + window;
+  const int64_t n = n_slices * stride;
+  seg_state_init_kernel<<<(unsigned)((n + 255) / 256), 256, 0, as_stream(stream)>>>(seg_state, n_slices, stride,
+                                                                                   n_clusters);
+  LKV_CHECK_LAUNCH();
+  return LOUISKV_OK;
+}
+
+extern "C" int louiskv_segment_output_boundary(const void* k_new, const void* v_new, int32_t dtype, int64_t n_slices,
+                                               int32_t n_kv_heads, int32_t d, void* k_local, void* v_local,
+                                               int32_t window, int32_t step, int32_t seg_max, const uint8_t* fire,
+                                               int32_t* seg_state, float* reps, int32_t* unit_start,
+                                               int32_t* unit_size, int32_t units_cap, int32_t n_clusters,
+                                               void* k_pool, void* v_pool, int64_t pool_rows, int32_t prompt_len,
+                                               int32_t pool_on_host, void* stream) {
+  if (!k_new || !v_new || !k_local || !v_local || !seg_state)
+    return fail(LOUISKV_ERR_NULL, "k_new, v_new, k_local, v_local and seg_state are required");
+  if (!reps || !unit_start || !unit_size) return fail(LOUISKV_ERR_NULL, "unit tables are required");
+  if (v_pool && !k_pool) return fail(LOUISKV_ERR_NULL, "v_pool given without k_pool");
+  int st = check_dtype(dtype);
+  if (st) return st;
+  if (pool_on_host && ((st = device_view_of_host_pool(k_pool, &k_pool)) || (st = device_view_of_host_pool(v_pool, &v_pool))))
+    return st;
+  if (d != kHeadDim) return fail(LOUISKV_ERR_UNSUPPORTED, "head dim %d not supported (only 128)", d);
+  if (n_kv_heads < 1 || n_slices < 1 || n_slices % n_kv_heads != 0 || n_slices > INT32_MAX)
+    return fail(LOUISKV_ERR_SHAPE, "n_slices=%lld must be a positive multiple of n_kv_heads=%d", (long long)n_slices,
+                n_kv_heads);
+  if (window < 2 || seg_max < 1 || seg_max >= window)
+    return fail(LOUISKV_ERR_SHAPE, "need 1 <= seg_max=%d < window=%d", seg_max, window);
+  if (step < 0) return fail(LOUISKV_ERR_SHAPE, "step=%d < 0", step);
+  if (n_clusters < 1 || n_clusters > units_cap)
+    return fail(LOUISKV_ERR_SHAPE, "n_clusters=%d must be in [1, units_cap=%d]", n_clusters, units_cap);
+  if (prompt_len < 0 || ((k_pool || v_pool) && pool_rows < prompt_len))
+    return fail(LOUISKV_ERR_SHAPE, "prompt_len=%d pool_rows=%lld", prompt_len, (long long)pool_rows);
+  hipStream_t s = as_stream(stream);
+  if (dtype == LOUISKV_BF16)
+    store_segmented_kernel<uint16_t><<<(unsigned)n_slices, 64, 0, s>>>(
+        static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new), static_cast<uint16_t*>(k_local),
+        static_cast<uint16_t*>(v_local), window, step, seg_max, fire, n_kv_heads, seg_state, reps, unit_start,
+        unit_size, units_cap, n_clusters, static_cast<uint16_t*>(k_pool), static_cast<uint16_t*>(v_pool), pool_rows,
+        prompt_len);
+  else
+    store_segmented_kernel<float><<<(unsigned)n_slices, 64, 0, s>>>(
+        static_cast<const float*>(k_new), static_cast<const float*>(v_new), static_cast<float*>(k_local),
+        static_cast<float*>(v_local), window, step, seg_max, fire, n_kv_heads, seg_state, reps, unit_start, unit_size,
+        units_cap, n_clusters, static_cast<float*>(k_pool), static_cast<float*>(v_pool), pool_rows, prompt_len);
+  LKV_CHECK_LAUNCH();
+  return LOUISKV_OK;
+}
+
 extern "C" size_t louiskv_retrieve_workspace_size(int64_t n_slices, int32_t units_cap, int32_t budget) {
   if (n_slices < 1 || units_cap < 1 || budget < 0) return 0;
   return retrieve_ws_bytes(n_slices, units_cap, budget, kMaxGroupSize);
@@ -1051,7 +1237,7 @@ int score_and_select(const void* q, int32_t dtype, int64_t n_slices, int32_t n_k
                      double scale, const float* reps, const int32_t* unit_start, const int32_t* unit_size,
                      int32_t units_cap, int32_t n_units, int32_t budget, const uint8_t* fire, int32_t* sel_units,
                      int32_t* n_sel_units, int32_t* n_sel, int32_t* rows, double* scores_out, double* logit_ws,
-                     hipStream_t s) {
+                     const int32_t* seg_state, int32_t seg_stride, hipStream_t s) {
   if (n_units < 1 || n_units > units_cap || n_units > kMaxUnits)
     return fail(LOUISKV_ERR_SHAPE, "n_units=%d must be in [1, min(units_cap=%d, %d)]", n_units, units_cap, kMaxUnits);
   int n_pad = 64;                     // whole 64-key chunks for the in-wave sort steps
@@ -1061,7 +1247,7 @@ int score_and_select(const void* q, int32_t dtype, int64_t n_slices, int32_t n_k
 #define LKV_SEL(T, G)                                                                                                  \
   score_select_kernel<T, G><<<(unsigned)n_slices, kSelThreads, lds, s>>>(                                              \
       static_cast<const T*>(q), n_kv_heads, scale, reps, unit_start, unit_size, units_cap, n_units, budget, fire,    \
-      sel_units, n_sel_units, n_sel, scores_out, logit_ws, rows, n_pad)
+      sel_units, n_sel_units, n_sel, scores_out, logit_ws, rows, n_pad, seg_state, seg_stride)
 #define LKV_SEL_G(T)                  \
   switch (group_size) {               \
     case 1: LKV_SEL(T, 1); break;     \
@@ -1107,13 +1293,15 @@ int check_retrieve_common(const void* q, int32_t dtype, int64_t n_slices, int32_
 }  // namespace
 }  // namespace louiskv
 
-extern "C" int louiskv_retrieve(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads, int32_t group_size,
-                                int32_t d, double scale, const float* reps, const int32_t* unit_start,
-                                const int32_t* unit_size, int32_t units_cap, int32_t n_units, const void* k_pool,
-                                const void* v_pool, int64_t pool_rows, int32_t pool_on_host, int32_t budget,
-                                const uint8_t* fire, int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel,
-                                void* k_buf, void* v_buf, double* scores_out, void* workspace, size_t workspace_bytes,
-                                void* stream) {
+namespace louiskv {
+namespace {
+int retrieve_gather(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads, int32_t group_size, int32_t d,
+                    double scale, const float* reps, const int32_t* unit_start, const int32_t* unit_size,
+                    int32_t units_cap, int32_t n_units, const void* k_pool, const void* v_pool, int64_t pool_rows,
+                    int32_t pool_on_host, int32_t budget, const uint8_t* fire, int32_t* sel_units,
+                    int32_t* n_sel_units, int32_t* n_sel, void* k_buf, void* v_buf, double* scores_out,
+                    void* workspace, size_t workspace_bytes, const int32_t* seg_state, int32_t seg_stride,
+                    void* stream) {
   int st = check_retrieve_common(q, dtype, n_slices, n_kv_heads, group_size, d, reps, unit_start, unit_size, units_cap,
                                  n_units, budget, sel_units, n_sel_units, n_sel);
   if (st) return st;
@@ -1131,7 +1319,7 @@ extern "C" int louiskv_retrieve(const void* q, int32_t dtype, int64_t n_slices, 
   hipStream_t s = as_stream(stream);
   if ((st = score_and_select(q, dtype, n_slices, n_kv_heads, group_size, d, scale, reps, unit_start, unit_size,
                              units_cap, n_units, budget, fire, sel_units, n_sel_units, n_sel, row_ws, scores_out,
-                             logit_ws, s)))
+                             logit_ws, seg_state, seg_stride, s)))
     return st;
   if (budget > 0) {
     const int rpb = 128;
@@ -1151,6 +1339,59 @@ extern "C" int louiskv_retrieve(const void* q, int32_t dtype, int64_t n_slices, 
   return LOUISKV_OK;
 }
 
+int retrieve_rows(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads, int32_t group_size, int32_t d,
+                  double scale, const float* reps, const int32_t* unit_start, const int32_t* unit_size,
+                  int32_t units_cap, int32_t n_units, int32_t budget, const uint8_t* fire, int32_t* sel_units,
+                  int32_t* n_sel_units, int32_t* n_sel, int32_t* sel_rows, double* scores_out, void* workspace,
+                  size_t workspace_bytes, const int32_t* seg_state, int32_t seg_stride, void* stream) {
+  int st = check_retrieve_common(q, dtype, n_slices, n_kv_heads, group_size, d, reps, unit_start, unit_size, units_cap,
+                                 n_units, budget, sel_units, n_sel_units, n_sel);
+  if (st) return st;
+  if (budget > 0 && !sel_rows) return fail(LOUISKV_ERR_NULL, "sel_rows is required when budget > 0");
+  const size_t need = align_up((size_t)n_slices * units_cap * kMaxGroupSize * sizeof(double), 256);
+  if (!workspace || workspace_bytes < need)
+    return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  return score_and_select(q, dtype, n_slices, n_kv_heads, group_size, d, scale, reps, unit_start, unit_size, units_cap,
+                          n_units, budget, fire, sel_units, n_sel_units, n_sel, sel_rows, scores_out,
+                          static_cast<double*>(workspace), seg_state, seg_stride, as_stream(stream));
+}
+
+int check_seg_state(const int32_t* seg_state, int32_t window) {
+  if (!seg_state) return fail(LOUISKV_ERR_NULL, "seg_state is required");
+  if (window < 2) return fail(LOUISKV_ERR_SHAPE, "window=%d must be >= 2", window);
+  return LOUISKV_OK;
+}
+}  // namespace
+}  // namespace louiskv
+
+extern "C" int louiskv_retrieve(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads, int32_t group_size,
+                                int32_t d, double scale, const float* reps, const int32_t* unit_start,
+                                const int32_t* unit_size, int32_t units_cap, int32_t n_units, const void* k_pool,
+                                const void* v_pool, int64_t pool_rows, int32_t pool_on_host, int32_t budget,
+                                const uint8_t* fire, int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel,
+                                void* k_buf, void* v_buf, double* scores_out, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  return retrieve_gather(q, dtype, n_slices, n_kv_heads, group_size, d, scale, reps, unit_start, unit_size, units_cap,
+                         n_units, k_pool, v_pool, pool_rows, pool_on_host, budget, fire, sel_units, n_sel_units, n_sel,
+                         k_buf, v_buf, scores_out, workspace, workspace_bytes, nullptr, 0, stream);
+}
+
+extern "C" int louiskv_retrieve_seg(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads,
+                                    int32_t group_size, int32_t d, double scale, const float* reps,
+                                    const int32_t* unit_start, const int32_t* unit_size, int32_t units_cap,
+                                    int32_t max_units, const int32_t* seg_state, int32_t window, const void* k_pool,
+                                    const void* v_pool, int64_t pool_rows, int32_t pool_on_host, int32_t budget,
+                                    const uint8_t* fire, int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel,
+                                    void* k_buf, void* v_buf, double* scores_out, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  int st = check_seg_state(seg_state, window);
+  if (st) return st;
+  return retrieve_gather(q, dtype, n_slices, n_kv_heads, group_size, d, scale, reps, unit_start, unit_size, units_cap,
+                         max_units, k_pool, v_pool, pool_rows, pool_on_host, budget, fire, sel_units, n_sel_units,
+                         n_sel, k_buf, v_buf, scores_out, workspace, workspace_bytes, seg_state, kSegRing + window,
+                         stream);
+}
+
 extern "C" size_t louiskv_retrieve_rows_workspace_size(int64_t n_slices, int32_t units_cap) {
   if (n_slices < 1 || units_cap < 1) return 0;
   return align_up((size_t)n_slices * units_cap * kMaxGroupSize * sizeof(double), 256);
@@ -1162,16 +1403,23 @@ extern "C" int louiskv_retrieve_rows(const void* q, int32_t dtype, int64_t n_sli
                                      int32_t n_units, int32_t budget, const uint8_t* fire, int32_t* sel_units,
                                      int32_t* n_sel_units, int32_t* n_sel, int32_t* sel_rows, double* scores_out,
                                      void* workspace, size_t workspace_bytes, void* stream) {
-  int st = check_retrieve_common(q, dtype, n_slices, n_kv_heads, group_size, d, reps, unit_start, unit_size, units_cap,
-                                 n_units, budget, sel_units, n_sel_units, n_sel);
+  return retrieve_rows(q, dtype, n_slices, n_kv_heads, group_size, d, scale, reps, unit_start, unit_size, units_cap,
+                       n_units, budget, fire, sel_units, n_sel_units, n_sel, sel_rows, scores_out, workspace,
+                       workspace_bytes, nullptr, 0, stream);
+}
+
+extern "C" int louiskv_retrieve_rows_seg(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads,
+                                         int32_t group_size, int32_t d, double scale, const float* reps,
+                                         const int32_t* unit_start, const int32_t* unit_size, int32_t units_cap,
+                                         int32_t max_units, const int32_t* seg_state, int32_t window, int32_t budget,
+                                         const uint8_t* fire, int32_t* sel_units, int32_t* n_sel_units,
+                                         int32_t* n_sel, int32_t* sel_rows, double* scores_out, void* workspace,
+                                         size_t workspace_bytes, void* stream) {
+  int st = check_seg_state(seg_state, window);
   if (st) return st;
-  if (budget > 0 && !sel_rows) return fail(LOUISKV_ERR_NULL, "sel_rows is required when budget > 0");
-  const size_t need = louiskv_retrieve_rows_workspace_size(n_slices, units_cap);
-  if (!workspace || workspace_bytes < need)
-    return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
-  return score_and_select(q, dtype, n_slices, n_kv_heads, group_size, d, scale, reps, unit_start, unit_size, units_cap,
-                          n_units, budget, fire, sel_units, n_sel_units, n_sel, sel_rows, scores_out,
-                          static_cast<double*>(workspace), as_stream(stream));
+  return retrieve_rows(q, dtype, n_slices, n_kv_heads, group_size, d, scale, reps, unit_start, unit_size, units_cap,
+                       max_units, budget, fire, sel_units, n_sel_units, n_sel, sel_rows, scores_out, workspace,
+                       workspace_bytes, seg_state, kSegRing + window, stream);
 }
 
 extern "C" size_t louiskv_sparse_decode_attn_workspace_size(int64_t n_slices, int32_t group_size, int32_t d,
@@ -1208,6 +1456,8 @@ struct AttnArgs {
   void* out;
   int out_bf16;
   float* lse_out;
+  const int32_t* seg_state;   // per-slice windows (boundary-delimited segments) or NULL
+  int seg_stride, n_tokens;
   unsigned grid;
   size_t lds;              // dynamic LDS for the staged row list
 };
@@ -1217,7 +1467,8 @@ void launch_attn_partial(const AttnArgs& a, hipStream_t s) {
   attn_partial_kernel<T, G, kIdx><<<a.grid, attn_waves<T, G>() * 64, a.lds, s>>>(
       static_cast<const T*>(a.q), a.n_kv_heads, a.scale, static_cast<const T*>(a.k_src), static_cast<const T*>(a.v_src),
       a.n_sel, a.buf_rows, a.rows, a.src_rows, static_cast<const T*>(a.k_local), static_cast<const T*>(a.v_local),
-      a.window, a.local_start, a.n_local, a.n_chunks, a.part, a.out, a.out_bf16, a.lse_out);
+      a.window, a.local_start, a.n_local, a.n_chunks, a.part, a.out, a.out_bf16, a.lse_out, a.seg_state,
+      a.seg_stride, a.n_tokens);
 }
 
 template <int G, bool kIdx>
@@ -1226,7 +1477,7 @@ void launch_attn_mfma(const AttnArgs& a, hipStream_t s) {
       static_cast<const uint16_t*>(a.q), a.n_kv_heads, a.scale, static_cast<const uint16_t*>(a.k_src),
       static_cast<const uint16_t*>(a.v_src), a.n_sel, a.buf_rows, a.rows, a.src_rows,
       static_cast<const uint16_t*>(a.k_local), static_cast<const uint16_t*>(a.v_local), a.window, a.local_start,
-      a.n_local, a.n_chunks, a.part, a.out, a.out_bf16, a.lse_out);
+      a.n_local, a.n_chunks, a.part, a.out, a.out_bf16, a.lse_out, a.seg_state, a.seg_stride, a.n_tokens);
 }
 
 template <bool kIdx>
@@ -1254,7 +1505,8 @@ int sparse_decode_attn(const void* q, int32_t dtype, int64_t n_slices, int32_t n
                        int32_t d, float scale, const void* k_src, const void* v_src, const int32_t* n_sel,
                        int32_t buf_rows, const int32_t* rows, int64_t src_rows, const void* k_local,
                        const void* v_local, int32_t window, int32_t local_start, int32_t n_local, void* out,
-                       int32_t out_dtype, float* lse_out, void* workspace, size_t workspace_bytes, void* stream) {
+                       int32_t out_dtype, float* lse_out, void* workspace, size_t workspace_bytes, void* stream,
+                       const int32_t* seg_state = nullptr, int32_t n_tokens = 0) {
   const bool indexed = rows != nullptr;
   if (!q || !out || !n_sel) return fail(LOUISKV_ERR_NULL, "q, out and n_sel are required");
   if (buf_rows > 0 && (!k_src || !v_src))
@@ -1288,6 +1540,7 @@ int sparse_decode_attn(const void* q, int32_t dtype, int64_t n_slices, int32_t n
   a.n_local = n_local; a.n_chunks = n_chunks;
   a.part = static_cast<float*>(workspace);
   a.out = out; a.out_bf16 = out_dtype == LOUISKV_BF16; a.lse_out = lse_out;
+  a.seg_state = seg_state; a.seg_stride = kSegRing + window; a.n_tokens = n_tokens;
   a.grid = (unsigned)(n_slices * n_chunks);
   // a chunk spans at most ceil(total / n_chunks) <= ceil((buf_rows + window) / n_chunks) rows
   a.lds = indexed ? (size_t)(((int64_t)buf_rows + window + n_chunks - 1) / n_chunks + 1) * sizeof(int) : 0;
@@ -1335,4 +1588,36 @@ extern "C" int louiskv_sparse_decode_attn_rows(const void* q, int32_t dtype, int
   return sparse_decode_attn(q, dtype, n_slices, n_kv_heads, group_size, d, scale, k_pool, v_pool, n_sel, budget,
                             sel_rows, pool_rows, k_local, v_local, window, local_start, n_local, out, out_dtype,
                             lse_out, workspace, workspace_bytes, stream);
+}
+
+extern "C" int louiskv_sparse_decode_attn_seg(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads,
+                                              int32_t group_size, int32_t d, float scale, const void* k_buf,
+                                              const void* v_buf, const int32_t* n_sel, int32_t buf_rows,
+                                              const void* k_local, const void* v_local, int32_t window,
+                                              const int32_t* seg_state, int32_t n_tokens, void* out,
+                                              int32_t out_dtype, float* lse_out, void* workspace,
+                                              size_t workspace_bytes, void* stream) {
+  int st = check_seg_state(seg_state, window);
+  if (st) return st;
+  if (n_tokens < 1) return fail(LOUISKV_ERR_SHAPE, "n_tokens=%d must be >= 1", n_tokens);
+  return sparse_decode_attn(q, dtype, n_slices, n_kv_heads, group_size, d, scale, k_buf, v_buf, n_sel, buf_rows,
+                            nullptr, buf_rows, k_local, v_local, window, 0, window, out, out_dtype, lse_out,
+                            workspace, workspace_bytes, stream, seg_state, n_tokens);
+}
+
+extern "C" int louiskv_sparse_decode_attn_rows_seg(const void* q, int32_t dtype, int64_t n_slices,
+                                                   int32_t n_kv_heads, int32_t group_size, int32_t d, float scale,
+                                                   const void* k_pool, const void* v_pool, int64_t pool_rows,
+                                                   const int32_t* sel_rows, const int32_t* n_sel, int32_t budget,
+                                                   const void* k_local, const void* v_local, int32_t window,
+                                                   const int32_t* seg_state, int32_t n_tokens, void* out,
+                                                   int32_t out_dtype, float* lse_out, void* workspace,
+                                                   size_t workspace_bytes, void* stream) {
+  if (!sel_rows) return fail(LOUISKV_ERR_NULL, "sel_rows is required");
+  int st = check_seg_state(seg_state, window);
+  if (st) return st;
+  if (n_tokens < 1) return fail(LOUISKV_ERR_SHAPE, "n_tokens=%d must be >= 1", n_tokens);
+  return sparse_decode_attn(q, dtype, n_slices, n_kv_heads, group_size, d, scale, k_pool, v_pool, n_sel, budget,
+                            sel_rows, pool_rows, k_local, v_local, window, 0, window, out, out_dtype, lse_out,
+                            workspace, workspace_bytes, stream, seg_state, n_tokens);
 }

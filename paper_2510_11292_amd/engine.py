@@ -11,7 +11,10 @@ paper's Algorithm 1:
              louiskv_retrieve for the groups that fired (scores see the units
              evicted before this step), louiskv_segment_output (window append,
              oldest-segment eviction), louiskv_sparse_decode_attn over
-             [KV_critical : KV_local].
+             [KV_critical : KV_local].  With segments="boundary" the output
+             segments are delimited by the fired boundaries (the *_seg and
+             louiskv_segment_output_boundary calls, per-slice window state
+             on the device).
 
 With the pool in device memory the engine runs zero-copy by default:
 louiskv_retrieve_rows keeps KV_critical as a list of pool rows and
@@ -31,6 +34,8 @@ import torch
 
 from . import louiskv as L
 
+MAX_UNITS = 8192   # units one slice's retrieval scores (the library's limit)
+
 
 @dataclass(frozen=True)
 class EngineConfig:
@@ -47,6 +52,7 @@ class EngineConfig:
     tau: float
     mode: int = L.REF_ANCHOR
     head_dim: int = 128
+    segments: str = "fixed"    # "fixed" seg_len-token runs, or "boundary" (seg_len is then the cap)
 
     @property
     def n_groups(self) -> int:
@@ -54,6 +60,10 @@ class EngineConfig:
 
     @property
     def units_cap(self) -> int:
+        if self.segments == "boundary":
+            # at most one segment leaves per step once the window is full; the
+            # scorer handles at most MAX_UNITS units per slice
+            return min(self.n_clusters + max(0, self.gen_len - self.window), MAX_UNITS)
         ev = 0 if self.gen_len <= self.window else (self.gen_len - self.window + self.seg_len - 1) // self.seg_len
         return self.n_clusters + ev
 
@@ -115,6 +125,10 @@ class LouisKVEngine:
         self.out = torch.zeros(G, cfg.n_q_heads, d, dtype=out_dtype or dtype, device=dev)
         self.lse = torch.zeros(G, cfg.n_q_heads, dtype=torch.float32, device=dev)
         self.scores = torch.zeros(S, cap, dtype=torch.float64, device=dev) if keep_scores else None
+        if cfg.segments not in ("fixed", "boundary"):
+            raise ValueError(cfg.segments)
+        self.seg_state = (torch.zeros(S, L.segment_state_ints(cfg.window), **i32)
+                          if cfg.segments == "boundary" else None)
         dc = L.BF16 if dtype == torch.bfloat16 else L.F32
         u8 = dict(dtype=torch.uint8, device=dev)
         self.ws_prefill = torch.empty(L.cluster_prefill_workspace_size(S, cfg.prompt_len, cfg.n_clusters, dc), **u8)
@@ -142,6 +156,8 @@ class LouisKVEngine:
             pack_event.record()
         L.pack_pool(prompt_keys, prompt_values, self.perm, self.k_pool, self.v_pool,
                     pool_on_host=self.pool_on_host)
+        if self.seg_state is not None:
+            L.segment_state_init(self.seg_state, c.window, c.n_clusters)
         self.t = 0
 
     # ---------------------------------------------------------------- decode
@@ -156,6 +172,9 @@ class LouisKVEngine:
         c = self.cfg
         t = self.t
         L.boundary_check(q_t, self.q_ref, c.tau, c.mode, t == 0, self.fire, self.r)
+        if self.seg_state is not None:
+            self._step_boundary_segments(q_t, k_t, v_t)
+            return
         if self.zero_copy:
             L.retrieve_rows(q_t, c.n_kv_heads, self.reps, self.unit_start, self.unit_size, self.n_units_before(t),
                             c.budget, self.sel_units, self.n_sel_units, self.n_sel, self.sel_rows, fire=self.fire,
@@ -176,4 +195,33 @@ class LouisKVEngine:
         else:
             L.sparse_decode_attn(q_t, c.n_kv_heads, self.k_buf, self.v_buf, self.n_sel, self.k_local,
                                  self.v_local, local_start, n_local, self.out, self.lse, workspace=self.ws_attn)
+        self.t += 1
+
+    def _step_boundary_segments(self, q_t, k_t, v_t) -> None:
+        """The rest of step() with boundary-delimited segments: unit counts and
+        windows are per slice, kept on the device in seg_state."""
+        c = self.cfg
+        t = self.t
+        # units that can exist before this step: clusters plus one per step
+        # since the window first filled
+        bound = min(c.units_cap, c.n_clusters + max(0, t - c.window))
+        if self.zero_copy:
+            L.retrieve_rows_seg(q_t, c.n_kv_heads, self.reps, self.unit_start, self.unit_size, bound,
+                                self.seg_state, c.window, c.budget, self.sel_units, self.n_sel_units, self.n_sel,
+                                self.sel_rows, fire=self.fire, scores_out=self.scores, workspace=self.ws_retrieve)
+        else:
+            L.retrieve_seg(q_t, c.n_kv_heads, self.reps, self.unit_start, self.unit_size, bound, self.seg_state,
+                           c.window, self.k_pool, self.v_pool, c.budget, self.sel_units, self.n_sel_units,
+                           self.n_sel, self.k_buf, self.v_buf, fire=self.fire, pool_on_host=self.pool_on_host,
+                           scores_out=self.scores, workspace=self.ws_retrieve)
+        L.segment_output_boundary(k_t, v_t, self.k_local, self.v_local, t, c.seg_len, self.fire, self.seg_state,
+                                  self.reps, self.unit_start, self.unit_size, c.n_clusters, c.n_kv_heads,
+                                  self.k_pool, self.v_pool, c.prompt_len, pool_on_host=self.pool_on_host)
+        if self.zero_copy:
+            L.sparse_decode_attn_rows_seg(q_t, c.n_kv_heads, self.k_pool, self.v_pool, self.sel_rows, self.n_sel,
+                                          self.k_local, self.v_local, self.seg_state, t + 1, self.out, self.lse,
+                                          workspace=self.ws_attn)
+        else:
+            L.sparse_decode_attn_seg(q_t, c.n_kv_heads, self.k_buf, self.v_buf, self.n_sel, self.k_local,
+                                     self.v_local, self.seg_state, t + 1, self.out, self.lse, workspace=self.ws_attn)
         self.t += 1

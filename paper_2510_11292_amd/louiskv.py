@@ -64,6 +64,28 @@ _SIGS = {
         _P, _I32, _I64, _I32, _I32, _I32, _F,
         _P, _P, _P, _I32, _P, _P, _I32, _I32, _I32,
         _P, _I32, _P, _P, _SZ, _P]),
+    "louiskv_segment_state_ints": (_SZ, [_I32]),
+    "louiskv_segment_state_init": (ctypes.c_int, [_P, _I64, _I32, _I32, _P]),
+    "louiskv_segment_output_boundary": (ctypes.c_int, [
+        _P, _P, _I32, _I64, _I32, _I32, _P, _P, _I32, _I32, _I32, _P, _P,
+        _P, _P, _P, _I32, _I32, _P, _P, _I64, _I32, _I32, _P]),
+    "louiskv_retrieve_seg": (ctypes.c_int, [
+        _P, _I32, _I64, _I32, _I32, _I32, _D,
+        _P, _P, _P, _I32, _I32, _P, _I32,
+        _P, _P, _I64, _I32, _I32, _P,
+        _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "louiskv_retrieve_rows_seg": (ctypes.c_int, [
+        _P, _I32, _I64, _I32, _I32, _I32, _D,
+        _P, _P, _P, _I32, _I32, _P, _I32, _I32, _P,
+        _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "louiskv_sparse_decode_attn_seg": (ctypes.c_int, [
+        _P, _I32, _I64, _I32, _I32, _I32, _F,
+        _P, _P, _P, _I32, _P, _P, _I32, _P, _I32,
+        _P, _I32, _P, _P, _SZ, _P]),
+    "louiskv_sparse_decode_attn_rows_seg": (ctypes.c_int, [
+        _P, _I32, _I64, _I32, _I32, _I32, _F,
+        _P, _P, _I64, _P, _P, _I32, _P, _P, _I32, _P, _I32,
+        _P, _I32, _P, _P, _SZ, _P]),
 }
 
 EXPORTED = sorted(_SIGS)
@@ -275,6 +297,94 @@ def sparse_decode_attn_rows(q, n_kv_heads: int, k_pool, v_pool, sel_rows, n_sel,
     _check(load_library().louiskv_sparse_decode_attn_rows(
         _ptr(q), _dtype_code(q), s, n_kv_heads, gs, d, float(sc), _ptr(k_pool), _ptr(v_pool), k_pool.shape[1],
         _ptr(sel_rows), _ptr(n_sel), budget, _ptr(k_local), _ptr(v_local), window, local_start, n_local,
+        _ptr(out), _dtype_code(out), _ptr(lse_out), _ptr(ws), wsb, _stream(stream)))
+
+
+# ------------------------------------------------ boundary-delimited segments
+
+def segment_state_ints(window: int) -> int:
+    """int32 entries per slice of the segment state (louiskv_segment_state_ints)."""
+    return load_library().louiskv_segment_state_ints(window)
+
+
+def segment_state_init(seg_state, window: int, n_clusters: int, stream=None):
+    """Segment state before decode step 0 (clusters only, empty window)."""
+    _check(load_library().louiskv_segment_state_init(_ptr(seg_state), seg_state.shape[0], window, n_clusters,
+                                                     _stream(stream)))
+
+
+def segment_output_boundary(k_new, v_new, k_local, v_local, step: int, seg_max: int, fire, seg_state, reps,
+                            unit_start, unit_size, n_clusters: int, n_kv_heads: int, k_pool=None, v_pool=None,
+                            prompt_len: int = 0, pool_on_host: bool = False, stream=None):
+    s, d = k_new.shape
+    pool_rows = k_pool.shape[1] if k_pool is not None else 0
+    _check(load_library().louiskv_segment_output_boundary(
+        _ptr(k_new), _ptr(v_new), _dtype_code(k_new), s, n_kv_heads, d, _ptr(k_local), _ptr(v_local),
+        k_local.shape[1], step, seg_max, _ptr(fire), _ptr(seg_state), _ptr(reps), _ptr(unit_start),
+        _ptr(unit_size), reps.shape[1], n_clusters, _ptr(k_pool), _ptr(v_pool), pool_rows, prompt_len,
+        int(pool_on_host), _stream(stream)))
+
+
+def retrieve_seg(q, n_kv_heads: int, reps, unit_start, unit_size, max_units: int, seg_state, window: int, k_pool,
+                 v_pool, budget: int, sel_units, n_sel_units, n_sel, k_buf, v_buf, fire=None,
+                 scale: Optional[float] = None, pool_on_host: bool = False, scores_out=None, workspace=None,
+                 stream=None):
+    g, hq, d = q.shape
+    s = reps.shape[0]
+    cap = reps.shape[1]
+    ws, wsb = _ws(retrieve_workspace_size(s, cap, budget), q.device, workspace)
+    sc = (1.0 / d ** 0.5) if scale is None else scale
+    _check(load_library().louiskv_retrieve_seg(
+        _ptr(q), _dtype_code(q), s, n_kv_heads, hq // n_kv_heads, d, float(sc),
+        _ptr(reps), _ptr(unit_start), _ptr(unit_size), cap, max_units, _ptr(seg_state), window,
+        _ptr(k_pool), _ptr(v_pool), k_pool.shape[1], int(pool_on_host), budget, _ptr(fire),
+        _ptr(sel_units), _ptr(n_sel_units), _ptr(n_sel), _ptr(k_buf), _ptr(v_buf), _ptr(scores_out),
+        _ptr(ws), wsb, _stream(stream)))
+
+
+def retrieve_rows_seg(q, n_kv_heads: int, reps, unit_start, unit_size, max_units: int, seg_state, window: int,
+                      budget: int, sel_units, n_sel_units, n_sel, sel_rows, fire=None, scale: Optional[float] = None,
+                      scores_out=None, workspace=None, stream=None):
+    g, hq, d = q.shape
+    s = reps.shape[0]
+    cap = reps.shape[1]
+    ws, wsb = _ws(retrieve_rows_workspace_size(s, cap), q.device, workspace)
+    sc = (1.0 / d ** 0.5) if scale is None else scale
+    _check(load_library().louiskv_retrieve_rows_seg(
+        _ptr(q), _dtype_code(q), s, n_kv_heads, hq // n_kv_heads, d, float(sc),
+        _ptr(reps), _ptr(unit_start), _ptr(unit_size), cap, max_units, _ptr(seg_state), window, budget,
+        _ptr(fire), _ptr(sel_units), _ptr(n_sel_units), _ptr(n_sel), _ptr(sel_rows), _ptr(scores_out),
+        _ptr(ws), wsb, _stream(stream)))
+
+
+def sparse_decode_attn_seg(q, n_kv_heads: int, k_buf, v_buf, n_sel, k_local, v_local, seg_state, n_tokens: int,
+                           out, lse_out=None, scale: Optional[float] = None, workspace=None, stream=None):
+    g, hq, d = q.shape
+    s = n_sel.shape[0]
+    gs = hq // n_kv_heads
+    buf_rows = k_buf.shape[1] if k_buf is not None else 0
+    window = k_local.shape[1]
+    ws, wsb = _ws(sparse_decode_attn_workspace_size(s, gs, buf_rows, window, d), q.device, workspace)
+    sc = (1.0 / d ** 0.5) if scale is None else scale
+    _check(load_library().louiskv_sparse_decode_attn_seg(
+        _ptr(q), _dtype_code(q), s, n_kv_heads, gs, d, float(sc), _ptr(k_buf), _ptr(v_buf), _ptr(n_sel), buf_rows,
+        _ptr(k_local), _ptr(v_local), window, _ptr(seg_state), n_tokens, _ptr(out), _dtype_code(out),
+        _ptr(lse_out), _ptr(ws), wsb, _stream(stream)))
+
+
+def sparse_decode_attn_rows_seg(q, n_kv_heads: int, k_pool, v_pool, sel_rows, n_sel, k_local, v_local, seg_state,
+                                n_tokens: int, out, lse_out=None, scale: Optional[float] = None, workspace=None,
+                                stream=None):
+    g, hq, d = q.shape
+    s = n_sel.shape[0]
+    gs = hq // n_kv_heads
+    budget = sel_rows.shape[1]
+    window = k_local.shape[1]
+    ws, wsb = _ws(sparse_decode_attn_rows_workspace_size(s, gs, budget, window, d), q.device, workspace)
+    sc = (1.0 / d ** 0.5) if scale is None else scale
+    _check(load_library().louiskv_sparse_decode_attn_rows_seg(
+        _ptr(q), _dtype_code(q), s, n_kv_heads, gs, d, float(sc), _ptr(k_pool), _ptr(v_pool), k_pool.shape[1],
+        _ptr(sel_rows), _ptr(n_sel), budget, _ptr(k_local), _ptr(v_local), window, _ptr(seg_state), n_tokens,
         _ptr(out), _dtype_code(out), _ptr(lse_out), _ptr(ws), wsb, _stream(stream)))
 
 

@@ -109,6 +109,34 @@ def test_validation_errors_return_before_launch(lib):
                                       None, None, 0, 0, 0, None) == 2
 
 
+def test_boundary_segment_calls_validate_on_the_host(lib):
+    """The boundary-delimited segment calls refuse a missing state, a cap not
+    below the window and a state for a window too small, before any launch."""
+    P = ctypes.c_void_p
+    dummy = P(16)
+    assert lib.louiskv_segment_state_ints(64) == 8 + 64
+    assert lib.louiskv_segment_state_ints(1) == 0
+    base = [dummy, dummy, 1, 8, 8, 128, dummy, dummy, 64, 0, 16, None, dummy, dummy, dummy, dummy, 200, 64,
+            None, None, 0, 0, 0, None]
+    # missing state
+    a = list(base); a[12] = None
+    assert lib.louiskv_segment_output_boundary(*a) == 1
+    # cap not below the window
+    a = list(base); a[10] = 64
+    assert lib.louiskv_segment_output_boundary(*a) == 2
+    a = list(base); a[10] = 0
+    assert lib.louiskv_segment_output_boundary(*a) == 2
+    # more clusters than unit slots
+    a = list(base); a[17] = 201
+    assert lib.louiskv_segment_output_boundary(*a) == 2
+    # retrieval and attention need the state
+    assert lib.louiskv_retrieve_rows_seg(dummy, 1, 8, 8, 4, 128, 0.088, dummy, dummy, dummy, 100, 50, None, 64, 64,
+                                         None, dummy, dummy, dummy, dummy, None, dummy, 1 << 30, None) == 1
+    assert lib.louiskv_sparse_decode_attn_rows_seg(dummy, 1, 8, 8, 4, 128, 0.088, dummy, dummy, 1000, dummy, dummy,
+                                                   64, dummy, dummy, 64, dummy, 0, dummy, 1, None, dummy, 1 << 30,
+                                                   None) == 2
+
+
 def test_workspace_sizes_are_positive(lib):
     assert lib.louiskv_cluster_prefill_workspace_size(256, 32768, 128, 1024, 1) > 256 * 32768 * 4
     assert lib.louiskv_retrieve_workspace_size(256, 1024, 2048) > 0

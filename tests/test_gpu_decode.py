@@ -339,12 +339,12 @@ def test_sparse_decode_attn_rows_clamps_list_entries():
 
 # ------------------------------------------------------------------ whole decode loop
 
-def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None):
+def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, segments="fixed"):
     """Prefill on the GPU, then `steps` decode steps on the GPU and in the
     oracle (started from the GPU's prefill state), step-locked."""
     from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
     data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(n_groups)], gen_len=steps)
-    cfg = config_from_workload(wl, n_groups=n_groups, mode=mode, gen_len=steps)
+    cfg = config_from_workload(wl, n_groups=n_groups, mode=mode, gen_len=steps, segments=segments)
     odt = torch.float32
     eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, pool_on_host=pool_on_host, keep_scores=True,
                         out_dtype=odt, zero_copy=zero_copy)
@@ -361,8 +361,8 @@ def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None):
             k_pool=list(to64(eng.k_pool[sl, :wl.prompt_len])),
             v_pool=list(to64(eng.v_pool[sl, :wl.prompt_len])))
         decs.append(oracle.GroupDecoder(st, wl.n_q_heads, wl.budget, wl.window, wl.seg_len, wl.tau,
-                                        "prev" if mode == 0 else "anchor"))
-    stats = dict(fires=0, excused=0)
+                                        "prev" if mode == 0 else "anchor", segments=segments))
+    stats = dict(fires=0, excused=0, evictions=0, sizes=set())
     for t in range(steps):
         eng.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
         torch.cuda.synchronize()
@@ -396,8 +396,17 @@ def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None):
                 assert np.abs(got - rec.out).max() <= 2e-3, (t, np.abs(got - rec.out).max())
             if rec.evicted_unit is not None:
                 u = rec.evicted_unit
+                stats["evictions"] += 1
+                stats["sizes"].add(dec.unit_size[0][u])
                 for h in range(H):
                     assert np.array_equal(to64(eng.reps[gi * H + h, u]), dec.reps[h][u])
+                    assert int(eng.unit_start[gi * H + h, u]) == dec.unit_start[h][u]
+                    assert int(eng.unit_size[gi * H + h, u]) == dec.unit_size[h][u]
+            if segments == "boundary":
+                stt = to_np(eng.seg_state[gi * H:(gi + 1) * H])
+                assert (stt[:, 0] == dec.n_units()).all(), (t, stt[:, 0], dec.n_units())
+                assert (stt[:, 1] == dec.local[0][0][0]).all(), (t, stt[:, 1], dec.local[0][0][0])
+                assert (stt[:, 4] == 0).all()
     return stats
 
 
@@ -432,6 +441,34 @@ def test_decode_loop_host_pool():
     wl = synth.get_workload("host-131k").replace(prompt_len=2048, n_clusters=64, budget=512, name="host-131k")
     st = _run_loop(wl, 1, 200, mode=1, pool_on_host=True)
     assert st["fires"] > 20
+
+
+@pytest.mark.parametrize("zero_copy", [True, False])
+def test_decode_loop_boundary_segments(zero_copy):
+    """Boundary-delimited segments (anchor mode fires every few steps, so the
+    segments are short and of varied length) on the bf16 long-output
+    reduction: units, windows and attention step-locked with the oracle."""
+    wl = synth.get_workload("si-lo-16k").replace(prompt_len=2048, n_clusters=64, budget=512, window=64,
+                                                 seg_len=16, name="si-lo-16k")
+    st = _run_loop(wl, 2, 300, mode=1, zero_copy=zero_copy, segments="boundary")
+    assert st["fires"] > 40 and st["evictions"] > 40 and len(st["sizes"]) >= 2
+
+
+def test_decode_loop_boundary_segments_prev_fp32():
+    """The tiny fp32 workload with boundary segments in previous-query mode:
+    boundaries only at query jumps, so most segments end at the length cap."""
+    wl = synth.get_workload("tiny-4k").replace(window=64, seg_len=12)
+    st = _run_loop(wl, 1, wl.gen_len, mode=0, segments="boundary")
+    assert st["evictions"] > 10 and 12 in st["sizes"]
+
+
+def test_decode_loop_boundary_segments_host_pool():
+    """Boundary segments with the pool in pinned host memory (gathered
+    KV_critical over the host link)."""
+    wl = synth.get_workload("host-131k").replace(prompt_len=2048, n_clusters=64, budget=512, window=64, seg_len=16,
+                                                 name="host-131k")
+    st = _run_loop(wl, 1, 200, mode=1, pool_on_host=True, segments="boundary")
+    assert st["fires"] > 20 and st["evictions"] > 10
 
 
 def test_host_pool_flag_rejects_device_memory():

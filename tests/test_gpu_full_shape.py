@@ -200,3 +200,108 @@ def test_decode_full_shape_sampled(name, retrieval):
                 last_fire[gi] = t
     assert stats["fires"] > 0
     assert stats["checked"] >= 2 * len(steps)
+
+
+def _check_step_boundary(eng, data, wl, t, gi, q_ref_before, before, fires, stats):
+    """Step t of group gi with boundary-delimited segments, recomputed from the
+    GPU's state: the boundary, the scores and selection over the slice's own
+    unit count, KV_critical, the window from its first live token, the segment
+    that left (if any: the oldest tokens, a fired step or a full-length
+    segment before it, mean and pool rows), and the attention output."""
+    H, g, W, smax, P = wl.n_kv_heads, wl.group_size, wl.window, wl.seg_len, wl.prompt_len
+    scale = 1 / np.sqrt(128)
+    q64 = to64(data.queries[t, gi])
+    fire = bool(to_np(eng.fire)[gi])
+    if t == 0:
+        assert fire
+    else:
+        r_ref = oracle.query_similarity(q64, q_ref_before)
+        if fire != oracle.boundary_fires(r_ref, wl.tau, False):
+            assert abs(r_ref - wl.tau) <= REL * max(abs(r_ref), wl.tau), (t, gi, r_ref)
+            stats["excused"] += 1
+    after = to_np(eng.seg_state[gi * H:(gi + 1) * H])
+    for h in range(H):
+        s = gi * H + h
+        n_units, win0 = int(before[h, 0]), int(before[h, 1])
+        assert after[h, 4] == 0
+        sizes = to_np(eng.unit_size[s, :n_units]).astype(np.int64)
+        starts = to_np(eng.unit_start[s, :n_units]).astype(np.int64)
+        got = to_np(eng.sel_units[s, :int(eng.n_sel_units[s])]).tolist()
+        nsel = int(eng.n_sel[s])
+        if fire:
+            stats["fires"] += 1
+            a = oracle.group_scores(q64[h * g:(h + 1) * g], to64(eng.reps[s, :n_units]), scale)
+            np.testing.assert_allclose(to_np(eng.scores[s, :n_units]), a, rtol=1e-12, atol=1e-300)
+            stats["excused"] += selection_matches(a, sizes, wl.budget, got)
+            assert nsel == int(sizes[got].sum()) <= wl.budget
+        idx = [rr for u in got for rr in range(int(starts[u]), int(starts[u] + sizes[u]))]
+        rows = torch.as_tensor(idx, dtype=torch.long)
+        kp = eng.k_pool[s].index_select(0, rows.to(eng.k_pool.device))
+        vp = eng.v_pool[s].index_select(0, rows.to(eng.v_pool.device))
+        if eng.zero_copy:
+            assert to_np(eng.sel_rows[s, :nsel]).tolist() == idx
+        else:
+            assert torch.equal(eng.k_buf[s, :nsel].cpu(), kp.cpu()) and torch.equal(eng.v_buf[s, :nsel].cpu(), vp.cpu())
+        n_after, win1 = int(after[h, 0]), int(after[h, 1])
+        if n_after > n_units:
+            assert n_after == n_units + 1 and t - win0 == W
+            u = n_units
+            a0, n = int(eng.unit_start[s, u]) - P, int(eng.unit_size[s, u])
+            assert a0 == win0 and win1 == a0 + n and 1 <= n <= smax
+            assert a0 == 0 or fires[gi][a0] or int(eng.unit_size[s, u - 1]) == smax
+            seg_keys = data.gen_keys[a0:a0 + n, s]
+            assert torch.equal(eng.k_pool[s, P + a0:P + a0 + n].cpu(), seg_keys.cpu())
+            assert torch.equal(eng.v_pool[s, P + a0:P + a0 + n].cpu(), data.gen_values[a0:a0 + n, s].cpu())
+            assert np.array_equal(to64(eng.reps[s, u]), oracle.segment_mean(to64(seg_keys)))
+            stats["evictions"] += 1
+        else:
+            assert win1 == win0 and t - win0 < W
+        slots = [j % W for j in range(win1, t + 1)]
+        assert torch.equal(eng.k_local[s, slots].cpu(), data.gen_keys[win1:t + 1, s].cpu())
+        assert torch.equal(eng.v_local[s, slots].cpu(), data.gen_values[win1:t + 1, s].cpu())
+        kk = np.concatenate([to64(kp), to64(eng.k_local[s, slots])])
+        vv = np.concatenate([to64(vp), to64(eng.v_local[s, slots])])
+        o, _ = oracle.attention(q64[h * g:(h + 1) * g], kk, vv, scale)
+        err = np.abs(to64(eng.out[gi, h * g:(h + 1) * g]) - o).max()
+        assert err <= 2e-3, (t, s, err)
+    stats["checked"] += 1
+
+
+@pytest.mark.parametrize("name", ["si-lo-16k", "li-lo-32k-b4"])
+def test_decode_full_shape_boundary_segments(name):
+    """Every decode step of the full workload with boundary-delimited segments
+    (segment cap = the workload's segment length); sampled steps of two groups,
+    plus the first evictions, are recomputed from the GPU's state."""
+    from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
+    L = _L()
+    wl = synth.get_workload(name)
+    data = synth.make_slices(wl, DEV)
+    cfg = config_from_workload(wl, mode=L.REF_ANCHOR, segments="boundary")
+    eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, pool_on_host=wl.pool_on_host, keep_scores=True,
+                        out_dtype=torch.float32)
+    eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    torch.cuda.synchronize()
+    H = wl.n_kv_heads
+    groups = (0, wl.n_groups - 1)
+    steps = _sample_steps(wl) | set(range(wl.window, wl.window + 12))
+    last_fire = {gi: None for gi in groups}
+    fires = {gi: np.zeros(wl.gen_len, dtype=bool) for gi in groups}
+    stats = dict(fires=0, excused=0, checked=0, evictions=0)
+    for t in range(wl.gen_len):
+        q_ref = {gi: (None if last_fire[gi] is None else to64(data.queries[last_fire[gi], gi])) for gi in groups}
+        check = t in steps
+        before = {gi: to_np(eng.seg_state[gi * H:(gi + 1) * H]) for gi in groups} if check else None
+        eng.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        fire = to_np(eng.fire)
+        for gi in groups:
+            fires[gi][t] = bool(fire[gi])
+        if check:
+            for gi in groups:
+                _check_step_boundary(eng, data, wl, t, gi, q_ref[gi], before[gi], fires, stats)
+        for gi in groups:
+            if fire[gi]:
+                last_fire[gi] = t
+    st = to_np(eng.seg_state)
+    assert (st[:, 4] == 0).all()
+    assert stats["fires"] > 0 and stats["evictions"] > 0
+    assert stats["checked"] >= 2 * len(steps)
