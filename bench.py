@@ -135,12 +135,12 @@ def time_attention(eng, wl, reps=20):
 
 
 def dense_decode_ms(wl, data, cfg, dtype, reps=2):
-    """Decode loop with the dense KV_critical (louiskv_retrieve gathers the
-    selected rows, louiskv_sparse_decode_attn reads the copies), as one HIP
+    """Decode loop with the dense KV_critical (louiskv_retrieve gathers every
+    selected row, louiskv_sparse_decode_attn reads the copies), as one HIP
     graph after a fresh prefill; mean replay time in ms."""
     import torch
     from paper_2510_11292_amd.engine import LouisKVEngine
-    eng = LouisKVEngine(cfg, dtype, "cuda", pool_on_host=wl.pool_on_host, zero_copy=False)
+    eng = LouisKVEngine(cfg, dtype, "cuda", pool_on_host=wl.pool_on_host, zero_copy=False, delta=False)
 
     def decode_all():
         for t in range(wl.gen_len):
@@ -289,6 +289,18 @@ def main() -> int:
         for t in range(wl.gen_len):
             eng.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
 
+    # rows copied by the delta retrieval, against rows selected, over the
+    # fired slices of one pass (counted on the device, eager pass only)
+    moved = torch.zeros(2, dtype=torch.int64, device=dev)
+
+    def decode_all_counting():
+        for t in range(wl.gen_len):
+            eng.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+            if eng.delta:
+                fired = eng.fire.repeat_interleave(wl.n_kv_heads).bool()
+                moved[0] += eng.n_fetched.sum()
+                moved[1] += torch.where(fired, eng.n_sel, 0).sum()
+
     graph = None
     if not args.eager:
         # capture the whole decode loop once; replays follow a fresh prefill
@@ -296,7 +308,7 @@ def main() -> int:
         side = torch.cuda.Stream()
         side.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(side):
-            decode_all()
+            decode_all_counting()
         torch.cuda.current_stream().wait_stream(side)
         torch.cuda.synchronize()
         graph = torch.cuda.CUDAGraph()
@@ -339,7 +351,7 @@ def main() -> int:
     t_attn, attn_bytes = time_attention(eng, wl)
     traffic = measured_traffic(wl.name)
     dense_ms = None
-    if eng.zero_copy and not args.eager:
+    if (eng.zero_copy or eng.delta) and not args.eager:
         dense_ms = dense_decode_ms(wl, data, cfg, dtype)
     out = {
         "metric": METRIC,
@@ -361,10 +373,12 @@ def main() -> int:
             "budget": wl.budget, "window": wl.window, "segment": wl.seg_len, "tau": wl.tau,
             "ref_mode": args.mode, "segments": args.segments,
             "decode_launch": "eager" if graph is None else "hip_graph",
-            "kv_critical": "pool row list (zero-copy)" if eng.zero_copy else "gathered copy",
+            "kv_critical": ("pool row list (zero-copy)" if eng.zero_copy else
+                            "cache of pool rows (delta transfers)" if eng.delta else "gathered copy"),
         },
         "decode_steps_per_s": wl.gen_len / t_dec,
         "decode_steps_per_s_gathered_kv_critical": (wl.gen_len / (dense_ms / 1e3)) if dense_ms else None,
+        "delta_rows_moved_per_selected": (float(moved[0]) / max(float(moved[1]), 1.0)) if eng.delta else None,
         "prefill_ms": t_pre * 1e3,
         "cluster_ms": t_cluster * 1e3,
         "pool_pack_ms": t_pack * 1e3,

@@ -497,6 +497,48 @@ int louiskv_sparse_decode_attn_rows_seg(const void* q, int32_t dtype, int64_t n_
                                         void* out, int32_t out_dtype, float* lse_out,
                                         void* workspace, size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------------ */
+/* Retrieval with delta transfers (host-resident pools)                      */
+/* ------------------------------------------------------------------------ */
+
+size_t louiskv_retrieve_delta_workspace_size(int64_t n_slices, int32_t units_cap,
+                                             int32_t budget);
+
+/*
+ * Algorithm 1 Retrieve (scores of Appendix B, Section 3.1 budget) with
+ * KV_critical kept as a cache of pool rows, so that a retrieval moves only
+ * the rows the previous selection of the slice did not already hold (the
+ * transfer that Appendix A names as the remaining bottleneck).  For every
+ * fired slice: the same scores, ranking and prefix-stop selection as
+ * louiskv_retrieve; buffer slots whose row is selected again keep it, the
+ * others are freed; the newly selected rows (in rank order) go to the free
+ * slots (in slot order), copied from the pool; slot_list then lists the
+ * slots holding the selection.  Attend with louiskv_sparse_decode_attn_rows
+ * (or _rows_seg) over k_buf/v_buf as the pool, budget rows, slot_list as the
+ * row list.  Slices whose group did not fire are untouched.
+ * buf_row    in/out [n_slices][budget] int32: the pool row held by each
+ *            buffer slot, -1 when free; all -1 before the first retrieval.
+ * slot_list  out [n_slices][budget] int32, entries 0..n_sel-1 written.
+ * n_fetched  out [n_slices] int32 or NULL: rows copied this call (0 for
+ *            slices that did not fire).
+ * seg_state, window  NULL/ignored for fixed segments (n_units is then the
+ *            unit count of every slice); with boundary-delimited segments the
+ *            per-slice counts come from seg_state and n_units bounds them.
+ * k_buf, v_buf  [n_slices][budget][d] dtype.  Requires budget >= 1 and
+ *            pool_rows <= 524288.  Other arguments as louiskv_retrieve.
+ */
+int louiskv_retrieve_delta(const void* q, int32_t dtype, int64_t n_slices,
+                           int32_t n_kv_heads, int32_t group_size, int32_t d, double scale,
+                           const float* reps, const int32_t* unit_start,
+                           const int32_t* unit_size, int32_t units_cap, int32_t n_units,
+                           const int32_t* seg_state, int32_t window,
+                           const void* k_pool, const void* v_pool, int64_t pool_rows,
+                           int32_t pool_on_host, int32_t budget, const uint8_t* fire,
+                           int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel,
+                           void* k_buf, void* v_buf, int32_t* buf_row, int32_t* slot_list,
+                           int32_t* n_fetched, double* scores_out,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

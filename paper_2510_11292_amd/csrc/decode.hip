@@ -550,6 +550,165 @@ void gather_kernel(const T* __restrict__ k_pool, const T* __restrict__ v_pool, i
   }
 }
 
+// ------------------------------------------------------------------ delta gather
+//
+// KV_critical as a cache of pool rows (the delta transfer of a host-resident
+// pool).  buf_row[s][i] is the pool row held in buffer slot i (-1: free).  For
+// a fired slice the plan kernel keeps every slot whose row is selected again,
+// frees the others, and pairs the newly selected rows (selection order) with
+// the free slots (slot order); only those rows cross the host link (fetch
+// kernel).  slot_list then lists the n_sel slots holding the selection, which
+// the row-list attention reads from the buffers.
+
+constexpr int kPlanThreads = 1024;
+constexpr int64_t kDeltaMaxPoolRows = 512 * 1024;   // the plan's bitmap of pool rows fits 64 KiB of LDS
+constexpr int kPlanWaves = kPlanThreads / 64;
+
+// Exclusive block-wide prefix sum of one flag per thread; returns the total.
+__device__ __forceinline__ int block_scan_flag(int flag, int* s_w, int& excl) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const uint64_t m = __builtin_amdgcn_ballot_w64(flag != 0);
+  const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+  if (lane == 0) s_w[w] = __popcll(m);
+  __syncthreads();
+  int before = 0, total = 0;
+  for (int q = 0; q < kPlanWaves; ++q) {
+    const int c = s_w[q];
+    before += q < w ? c : 0;
+    total += c;
+  }
+  __syncthreads();
+  excl = before + below;
+  return total;
+}
+
+__global__ __launch_bounds__(kPlanThreads)
+void delta_plan_kernel(const int32_t* __restrict__ row_ws, const int32_t* __restrict__ n_sel,
+                       const uint8_t* __restrict__ fire, int n_kv_heads, int budget, int64_t pool_rows,
+                       int32_t* __restrict__ buf_row, int32_t* __restrict__ slot_list,
+                       int32_t* __restrict__ fetch_slot, int32_t* __restrict__ fetch_row,
+                       int32_t* __restrict__ n_fetch, int32_t* __restrict__ n_fetch_out) {
+  extern __shared__ uint32_t s_bits[];   // one bit per pool row
+  __shared__ int s_w[kPlanWaves];
+  __shared__ int s_base[3];
+  const int64_t s = blockIdx.x;
+  const int tid = threadIdx.x;
+  if (fire && !fire[s / n_kv_heads]) {
+    if (tid == 0) {
+      n_fetch[s] = 0;
+      if (n_fetch_out) n_fetch_out[s] = 0;
+    }
+    return;
+  }
+  const int n = min(max(n_sel[s], 0), budget);
+  const int words = (int)((pool_rows + 31) / 32);
+  const int32_t* rows = row_ws + (size_t)s * budget;
+  int32_t* brow = buf_row + (size_t)s * budget;
+  for (int i = tid; i < words; i += kPlanThreads) s_bits[i] = 0u;
+  __syncthreads();
+  for (int p = tid; p < n; p += kPlanThreads) {
+    const int r = rows[p];
+    if (r >= 0 && r < pool_rows) atomicOr(&s_bits[r >> 5], 1u << (r & 31));
+  }
+  __syncthreads();
+  // keep the slots whose row is selected again (test and clear its bit), free the rest
+  for (int i = tid; i < budget; i += kPlanThreads) {
+    const int r = brow[i];
+    bool keep = false;
+    if (r >= 0 && r < pool_rows) {
+      const uint32_t bit = 1u << (r & 31);
+      keep = (atomicAnd(&s_bits[r >> 5], ~bit) & bit) != 0;
+    }
+    if (!keep) brow[i] = -1;
+  }
+  __syncthreads();
+  // pair the k-th new row (selection order) with the k-th free slot (slot order)
+  if (tid == 0) { s_base[0] = 0; s_base[1] = 0; }
+  __syncthreads();
+  const int rounds = (budget + kPlanThreads - 1) / kPlanThreads;
+  for (int rd = 0; rd < rounds; ++rd) {
+    // free slots of this round
+    const int i = rd * kPlanThreads + tid;
+    const bool fr = i < budget && brow[i] < 0;
+    int ex;
+    const int tot = block_scan_flag(fr, s_w, ex);
+    if (fr) fetch_slot[(size_t)s * budget + s_base[1] + ex] = i;
+    __syncthreads();
+    if (tid == 0) s_base[1] += tot;
+    __syncthreads();
+  }
+  for (int rd = 0; rd < rounds; ++rd) {
+    const int p = rd * kPlanThreads + tid;
+    int r = -1;
+    bool nw = false;
+    if (p < n) {
+      r = rows[p];
+      nw = r >= 0 && r < pool_rows && (s_bits[r >> 5] >> (r & 31) & 1u);
+    }
+    int ex;
+    const int tot = block_scan_flag(nw, s_w, ex);
+    if (nw) {
+      const int k = s_base[0] + ex;            // k < number of free slots (the selection fits the buffer)
+      const int slot = fetch_slot[(size_t)s * budget + k];
+      fetch_row[(size_t)s * budget + k] = r;
+      brow[slot] = r;
+    }
+    __syncthreads();
+    if (tid == 0) s_base[0] += tot;
+    __syncthreads();
+  }
+  if (tid == 0) {
+    n_fetch[s] = s_base[0];
+    if (n_fetch_out) n_fetch_out[s] = s_base[0];
+  }
+  __syncthreads();
+  // the slots that hold the selection, in slot order
+  if (tid == 0) s_base[2] = 0;
+  __syncthreads();
+  for (int rd = 0; rd < rounds; ++rd) {
+    const int i = rd * kPlanThreads + tid;
+    const bool v = i < budget && brow[i] >= 0;
+    int ex;
+    const int tot = block_scan_flag(v, s_w, ex);
+    if (v) slot_list[(size_t)s * budget + s_base[2] + ex] = i;
+    __syncthreads();
+    if (tid == 0) s_base[2] += tot;
+    __syncthreads();
+  }
+}
+
+// Copy the planned rows pool -> buffer slot: 16 lanes per row, 16 rows per pass.
+template <class T>
+__global__ __launch_bounds__(256)
+void delta_fetch_kernel(const T* __restrict__ k_pool, const T* __restrict__ v_pool, int64_t pool_rows,
+                        const int32_t* __restrict__ fetch_slot, const int32_t* __restrict__ fetch_row,
+                        const int32_t* __restrict__ n_fetch, int budget, int blocks_per_slice, int rows_per_block,
+                        T* __restrict__ k_buf, T* __restrict__ v_buf) {
+  const int64_t s = blockIdx.x / blocks_per_slice;
+  const int b = (int)(blockIdx.x - s * blocks_per_slice);
+  const int n = n_fetch[s];
+  const int r0 = b * rows_per_block;
+  if (r0 >= n) return;
+  const int r1 = min(n, r0 + rows_per_block);
+  constexpr int kU4 = kHeadDim * sizeof(T) / 16;
+  const int sub = threadIdx.x & 15;
+  for (int k = r0 + (threadIdx.x >> 4); k < r1; k += 16) {
+    const int64_t pr = fetch_row[(size_t)s * budget + k];
+    const int slot = fetch_slot[(size_t)s * budget + k];
+    if (pr < 0 || pr >= pool_rows || slot < 0 || slot >= budget) continue;
+    const uint4* ks = reinterpret_cast<const uint4*>(k_pool + ((size_t)s * pool_rows + pr) * kHeadDim);
+    const uint4* vs = reinterpret_cast<const uint4*>(v_pool + ((size_t)s * pool_rows + pr) * kHeadDim);
+    uint4* kd = reinterpret_cast<uint4*>(k_buf + ((size_t)s * budget + slot) * kHeadDim);
+    uint4* vd = reinterpret_cast<uint4*>(v_buf + ((size_t)s * budget + slot) * kHeadDim);
+#pragma unroll
+    for (int q = sub; q < kU4; q += 16) {
+      const uint4 a = ks[q], c = vs[q];
+      kd[q] = a;
+      vd[q] = c;
+    }
+  }
+}
+
 // ------------------------------------------------------------------ attention
 
 // Zero-copy retrieval: the selected rows are read straight from the pool
@@ -1620,4 +1779,72 @@ extern "C" int louiskv_sparse_decode_attn_rows_seg(const void* q, int32_t dtype,
   return sparse_decode_attn(q, dtype, n_slices, n_kv_heads, group_size, d, scale, k_pool, v_pool, n_sel, budget,
                             sel_rows, pool_rows, k_local, v_local, window, 0, window, out, out_dtype, lse_out,
                             workspace, workspace_bytes, stream, seg_state, n_tokens);
+}
+
+extern "C" size_t louiskv_retrieve_delta_workspace_size(int64_t n_slices, int32_t units_cap, int32_t budget) {
+  if (n_slices < 1 || units_cap < 1 || budget < 1) return 0;
+  Carver cv(nullptr);
+  cv.take<double>((size_t)n_slices * units_cap * kMaxGroupSize);
+  cv.take<int32_t>((size_t)n_slices * budget);   // selected pool rows
+  cv.take<int32_t>((size_t)n_slices * budget);   // fetch slots
+  cv.take<int32_t>((size_t)n_slices * budget);   // fetch rows
+  cv.take<int32_t>((size_t)n_slices);            // fetch counts
+  return align_up(cv.used, 256);
+}
+
+extern "C" int louiskv_retrieve_delta(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads,
+                                      int32_t group_size, int32_t d, double scale, const float* reps,
+                                      const int32_t* unit_start, const int32_t* unit_size, int32_t units_cap,
+                                      int32_t n_units, const int32_t* seg_state, int32_t window,
+                                      const void* k_pool, const void* v_pool, int64_t pool_rows,
+                                      int32_t pool_on_host, int32_t budget, const uint8_t* fire,
+                                      int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel, void* k_buf,
+                                      void* v_buf, int32_t* buf_row, int32_t* slot_list, int32_t* n_fetched,
+                                      double* scores_out, void* workspace, size_t workspace_bytes, void* stream) {
+  int st = check_retrieve_common(q, dtype, n_slices, n_kv_heads, group_size, d, reps, unit_start, unit_size, units_cap,
+                                 n_units, budget, sel_units, n_sel_units, n_sel);
+  if (st) return st;
+  if (!k_pool || !v_pool || !k_buf || !v_buf || !buf_row || !slot_list)
+    return fail(LOUISKV_ERR_NULL, "k_pool, v_pool, k_buf, v_buf, buf_row and slot_list are required");
+  if (budget < 1) return fail(LOUISKV_ERR_SHAPE, "budget=%d must be >= 1", budget);
+  if (pool_rows < 1 || pool_rows > kDeltaMaxPoolRows)
+    return fail(LOUISKV_ERR_UNSUPPORTED, "pool_rows=%lld must be in [1, %lld]", (long long)pool_rows,
+                (long long)kDeltaMaxPoolRows);
+  if (seg_state && (st = check_seg_state(seg_state, window))) return st;
+  void* kpd = const_cast<void*>(k_pool);
+  void* vpd = const_cast<void*>(v_pool);
+  if (pool_on_host && ((st = device_view_of_host_pool(k_pool, &kpd)) || (st = device_view_of_host_pool(v_pool, &vpd))))
+    return st;
+  const size_t need = louiskv_retrieve_delta_workspace_size(n_slices, units_cap, budget);
+  if (!workspace || workspace_bytes < need)
+    return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  Carver cv(workspace);
+  double* logit_ws = cv.take<double>((size_t)n_slices * units_cap * kMaxGroupSize);
+  int32_t* row_ws = cv.take<int32_t>((size_t)n_slices * budget);
+  int32_t* fslot = cv.take<int32_t>((size_t)n_slices * budget);
+  int32_t* frow = cv.take<int32_t>((size_t)n_slices * budget);
+  int32_t* nfetch = cv.take<int32_t>((size_t)n_slices);
+  hipStream_t s = as_stream(stream);
+  if ((st = score_and_select(q, dtype, n_slices, n_kv_heads, group_size, d, scale, reps, unit_start, unit_size,
+                             units_cap, n_units, budget, fire, sel_units, n_sel_units, n_sel, row_ws, scores_out,
+                             logit_ws, seg_state, seg_state ? kSegRing + window : 0, s)))
+    return st;
+  const size_t lds = (size_t)((pool_rows + 31) / 32) * sizeof(uint32_t);
+  delta_plan_kernel<<<(unsigned)n_slices, kPlanThreads, lds, s>>>(row_ws, n_sel, fire, n_kv_heads, budget, pool_rows,
+                                                                  buf_row, slot_list, fslot, frow, nfetch, n_fetched);
+  LKV_CHECK_LAUNCH();
+  const int rpb = 128;
+  const int bps = (budget + rpb - 1) / rpb;
+  const unsigned grid = (unsigned)(n_slices * bps);
+  if (dtype == LOUISKV_BF16)
+    delta_fetch_kernel<uint16_t><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(kpd),
+                                                      static_cast<const uint16_t*>(vpd), pool_rows, fslot, frow, nfetch,
+                                                      budget, bps, rpb, static_cast<uint16_t*>(k_buf),
+                                                      static_cast<uint16_t*>(v_buf));
+  else
+    delta_fetch_kernel<float><<<grid, 256, 0, s>>>(static_cast<const float*>(kpd), static_cast<const float*>(vpd),
+                                                   pool_rows, fslot, frow, nfetch, budget, bps, rpb,
+                                                   static_cast<float*>(k_buf), static_cast<float*>(v_buf));
+  LKV_CHECK_LAUNCH();
+  return LOUISKV_OK;
 }

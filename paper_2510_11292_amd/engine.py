@@ -20,7 +20,9 @@ With the pool in device memory the engine runs zero-copy by default:
 louiskv_retrieve_rows keeps KV_critical as a list of pool rows and
 louiskv_sparse_decode_attn_rows reads them from the pool, so a fired step
 copies nothing.  A pool in pinned host memory (or zero_copy=False) uses the
-dense KV_critical buffers that louiskv_retrieve gathers.
+dense KV_critical buffers that louiskv_retrieve gathers; for a host pool the
+default keeps them as a cache of pool rows (louiskv_retrieve_delta), so a
+retrieval moves only the rows the previous selection did not hold.
 
 Python only allocates tensors and passes pointers; every step of the path
 runs in the library's kernels.
@@ -85,7 +87,7 @@ def config_from_workload(wl, n_groups: Optional[int] = None, mode: int = L.REF_A
 class LouisKVEngine:
     def __init__(self, cfg: EngineConfig, dtype: torch.dtype, device="cuda", pool_on_host: bool = False,
                  keep_scores: bool = False, out_dtype: Optional[torch.dtype] = None,
-                 zero_copy: Optional[bool] = None):
+                 zero_copy: Optional[bool] = None, delta: Optional[bool] = None):
         self.cfg = cfg
         self.dtype = dtype
         self.device = torch.device(device)
@@ -93,6 +95,11 @@ class LouisKVEngine:
         if zero_copy and pool_on_host:
             raise ValueError("zero-copy retrieval reads the pool from device memory; use zero_copy=False")
         self.zero_copy = (not pool_on_host) if zero_copy is None else bool(zero_copy)
+        if delta and self.zero_copy:
+            raise ValueError("delta transfers fill the KV_critical buffers; they need zero_copy=False")
+        # KV_critical as a cache of pool rows: the default for a host-resident pool
+        self.delta = (not self.zero_copy and pool_on_host) if delta is None else bool(delta)
+        self.delta = self.delta and cfg.budget >= 1
         S, d, cap, G = cfg.n_slices, cfg.head_dim, cfg.units_cap, cfg.n_groups
         dev = self.device
         i32 = dict(dtype=torch.int32, device=dev)
@@ -116,6 +123,10 @@ class LouisKVEngine:
             self.sel_rows = None
             self.k_buf = torch.zeros(S, max(cfg.budget, 1), d, dtype=dtype, device=dev)
             self.v_buf = torch.zeros(S, max(cfg.budget, 1), d, dtype=dtype, device=dev)
+        if self.delta:
+            self.buf_row = torch.full((S, max(cfg.budget, 1)), -1, **i32)
+            self.slot_list = torch.zeros(S, max(cfg.budget, 1), **i32)
+            self.n_fetched = torch.zeros(S, **i32)
         self.sel_units = torch.zeros(S, cap, **i32)
         self.n_sel_units = torch.zeros(S, **i32)
         self.n_sel = torch.zeros(S, **i32)
@@ -136,6 +147,9 @@ class LouisKVEngine:
         rows = max(cfg.budget, 1)
         if self.zero_copy:
             self.ws_retrieve = torch.empty(L.retrieve_rows_workspace_size(S, cap), **u8)
+            self.ws_attn = torch.empty(max(L.sparse_decode_attn_rows_workspace_size(S, g, rows, cfg.window), 1), **u8)
+        elif self.delta:
+            self.ws_retrieve = torch.empty(L.retrieve_delta_workspace_size(S, cap, rows), **u8)
             self.ws_attn = torch.empty(max(L.sparse_decode_attn_rows_workspace_size(S, g, rows, cfg.window), 1), **u8)
         else:
             self.ws_retrieve = torch.empty(L.retrieve_workspace_size(S, cap, cfg.budget), **u8)
@@ -158,6 +172,8 @@ class LouisKVEngine:
                     pool_on_host=self.pool_on_host)
         if self.seg_state is not None:
             L.segment_state_init(self.seg_state, c.window, c.n_clusters)
+        if self.delta:
+            self.buf_row.fill_(-1)
         self.t = 0
 
     # ---------------------------------------------------------------- decode
@@ -179,6 +195,8 @@ class LouisKVEngine:
             L.retrieve_rows(q_t, c.n_kv_heads, self.reps, self.unit_start, self.unit_size, self.n_units_before(t),
                             c.budget, self.sel_units, self.n_sel_units, self.n_sel, self.sel_rows, fire=self.fire,
                             scores_out=self.scores, workspace=self.ws_retrieve)
+        elif self.delta:
+            self._retrieve_delta(q_t, self.n_units_before(t), None)
         else:
             L.retrieve(q_t, c.n_kv_heads, self.reps, self.unit_start, self.unit_size, self.n_units_before(t),
                        self.k_pool, self.v_pool, c.budget, self.sel_units, self.n_sel_units, self.n_sel,
@@ -190,6 +208,10 @@ class LouisKVEngine:
         _, _, n_local, local_start = L.window_info(t, c.window, c.seg_len)
         if self.zero_copy:
             L.sparse_decode_attn_rows(q_t, c.n_kv_heads, self.k_pool, self.v_pool, self.sel_rows, self.n_sel,
+                                      self.k_local, self.v_local, local_start, n_local, self.out, self.lse,
+                                      workspace=self.ws_attn)
+        elif self.delta:
+            L.sparse_decode_attn_rows(q_t, c.n_kv_heads, self.k_buf, self.v_buf, self.slot_list, self.n_sel,
                                       self.k_local, self.v_local, local_start, n_local, self.out, self.lse,
                                       workspace=self.ws_attn)
         else:
@@ -209,6 +231,8 @@ class LouisKVEngine:
             L.retrieve_rows_seg(q_t, c.n_kv_heads, self.reps, self.unit_start, self.unit_size, bound,
                                 self.seg_state, c.window, c.budget, self.sel_units, self.n_sel_units, self.n_sel,
                                 self.sel_rows, fire=self.fire, scores_out=self.scores, workspace=self.ws_retrieve)
+        elif self.delta:
+            self._retrieve_delta(q_t, bound, self.seg_state)
         else:
             L.retrieve_seg(q_t, c.n_kv_heads, self.reps, self.unit_start, self.unit_size, bound, self.seg_state,
                            c.window, self.k_pool, self.v_pool, c.budget, self.sel_units, self.n_sel_units,
@@ -221,7 +245,21 @@ class LouisKVEngine:
             L.sparse_decode_attn_rows_seg(q_t, c.n_kv_heads, self.k_pool, self.v_pool, self.sel_rows, self.n_sel,
                                           self.k_local, self.v_local, self.seg_state, t + 1, self.out, self.lse,
                                           workspace=self.ws_attn)
+        elif self.delta:
+            L.sparse_decode_attn_rows_seg(q_t, c.n_kv_heads, self.k_buf, self.v_buf, self.slot_list, self.n_sel,
+                                          self.k_local, self.v_local, self.seg_state, t + 1, self.out, self.lse,
+                                          workspace=self.ws_attn)
         else:
             L.sparse_decode_attn_seg(q_t, c.n_kv_heads, self.k_buf, self.v_buf, self.n_sel, self.k_local,
                                      self.v_local, self.seg_state, t + 1, self.out, self.lse, workspace=self.ws_attn)
         self.t += 1
+
+    def _retrieve_delta(self, q_t, n_units: int, seg_state) -> None:
+        """Retrieval into KV_critical kept as a cache of pool rows (only the
+        rows the slice's previous selection lacks are copied)."""
+        c = self.cfg
+        L.retrieve_delta(q_t, c.n_kv_heads, self.reps, self.unit_start, self.unit_size, n_units, self.k_pool,
+                         self.v_pool, max(c.budget, 1), self.sel_units, self.n_sel_units, self.n_sel, self.k_buf,
+                         self.v_buf, self.buf_row, self.slot_list, fire=self.fire, seg_state=seg_state,
+                         window=c.window, n_fetched=self.n_fetched, pool_on_host=self.pool_on_host,
+                         scores_out=self.scores, workspace=self.ws_retrieve)

@@ -86,6 +86,12 @@ _SIGS = {
         _P, _I32, _I64, _I32, _I32, _I32, _F,
         _P, _P, _I64, _P, _P, _I32, _P, _P, _I32, _P, _I32,
         _P, _I32, _P, _P, _SZ, _P]),
+    "louiskv_retrieve_delta_workspace_size": (_SZ, [_I64, _I32, _I32]),
+    "louiskv_retrieve_delta": (ctypes.c_int, [
+        _P, _I32, _I64, _I32, _I32, _I32, _D,
+        _P, _P, _P, _I32, _I32, _P, _I32,
+        _P, _P, _I64, _I32, _I32, _P,
+        _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
 }
 
 EXPORTED = sorted(_SIGS)
@@ -386,6 +392,28 @@ def sparse_decode_attn_rows_seg(q, n_kv_heads: int, k_pool, v_pool, sel_rows, n_
         _ptr(q), _dtype_code(q), s, n_kv_heads, gs, d, float(sc), _ptr(k_pool), _ptr(v_pool), k_pool.shape[1],
         _ptr(sel_rows), _ptr(n_sel), budget, _ptr(k_local), _ptr(v_local), window, _ptr(seg_state), n_tokens,
         _ptr(out), _dtype_code(out), _ptr(lse_out), _ptr(ws), wsb, _stream(stream)))
+
+
+def retrieve_delta_workspace_size(n_slices, units_cap, budget) -> int:
+    return load_library().louiskv_retrieve_delta_workspace_size(n_slices, units_cap, budget)
+
+
+def retrieve_delta(q, n_kv_heads: int, reps, unit_start, unit_size, n_units: int, k_pool, v_pool, budget: int,
+                   sel_units, n_sel_units, n_sel, k_buf, v_buf, buf_row, slot_list, fire=None, seg_state=None,
+                   window: int = 0, n_fetched=None, scale: Optional[float] = None, pool_on_host: bool = False,
+                   scores_out=None, workspace=None, stream=None):
+    """Retrieval into KV_critical as a cache of pool rows (only new rows are copied)."""
+    g, hq, d = q.shape
+    s = reps.shape[0]
+    cap = reps.shape[1]
+    ws, wsb = _ws(retrieve_delta_workspace_size(s, cap, budget), q.device, workspace)
+    sc = (1.0 / d ** 0.5) if scale is None else scale
+    _check(load_library().louiskv_retrieve_delta(
+        _ptr(q), _dtype_code(q), s, n_kv_heads, hq // n_kv_heads, d, float(sc),
+        _ptr(reps), _ptr(unit_start), _ptr(unit_size), cap, n_units, _ptr(seg_state), window,
+        _ptr(k_pool), _ptr(v_pool), k_pool.shape[1], int(pool_on_host), budget, _ptr(fire),
+        _ptr(sel_units), _ptr(n_sel_units), _ptr(n_sel), _ptr(k_buf), _ptr(v_buf), _ptr(buf_row),
+        _ptr(slot_list), _ptr(n_fetched), _ptr(scores_out), _ptr(ws), wsb, _stream(stream)))
 
 
 def pack_pool(keys, values, perm, k_pool, v_pool=None, pool_on_host: bool = False, stream=None):

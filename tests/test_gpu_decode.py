@@ -339,7 +339,26 @@ def test_sparse_decode_attn_rows_clamps_list_entries():
 
 # ------------------------------------------------------------------ whole decode loop
 
-def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, segments="fixed"):
+def _check_delta_buffers(eng, gi, H):
+    """KV_critical kept as a cache of pool rows: the listed slots hold exactly
+    the selected rows (as copies of their pool rows), every slot at most once."""
+    for h in range(H):
+        s = gi * H + h
+        n = int(eng.n_sel[s])
+        slots = to_np(eng.slot_list[s, :n]).astype(np.int64)
+        assert len(set(slots.tolist())) == n
+        held = to_np(eng.buf_row[s])[slots].astype(np.int64)
+        units = to_np(eng.sel_units[s, :int(eng.n_sel_units[s])])
+        want = sorted(r for u in units for r in range(int(eng.unit_start[s, u]),
+                                                       int(eng.unit_start[s, u]) + int(eng.unit_size[s, u])))
+        assert sorted(held.tolist()) == want
+        assert (to_np(eng.buf_row[s]) >= 0).sum() == n
+        idx = torch.as_tensor(held, dtype=torch.long)
+        assert torch.equal(eng.k_buf[s, torch.as_tensor(slots)].cpu(), eng.k_pool[s].cpu()[idx])
+        assert torch.equal(eng.v_buf[s, torch.as_tensor(slots)].cpu(), eng.v_pool[s].cpu()[idx])
+
+
+def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, segments="fixed", delta=None):
     """Prefill on the GPU, then `steps` decode steps on the GPU and in the
     oracle (started from the GPU's prefill state), step-locked."""
     from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
@@ -347,7 +366,7 @@ def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, seg
     cfg = config_from_workload(wl, n_groups=n_groups, mode=mode, gen_len=steps, segments=segments)
     odt = torch.float32
     eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, pool_on_host=pool_on_host, keep_scores=True,
-                        out_dtype=odt, zero_copy=zero_copy)
+                        out_dtype=odt, zero_copy=zero_copy, delta=delta)
     eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
     torch.cuda.synchronize()
     H, g = wl.n_kv_heads, wl.group_size
@@ -362,7 +381,7 @@ def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, seg
             v_pool=list(to64(eng.v_pool[sl, :wl.prompt_len])))
         decs.append(oracle.GroupDecoder(st, wl.n_q_heads, wl.budget, wl.window, wl.seg_len, wl.tau,
                                         "prev" if mode == 0 else "anchor", segments=segments))
-    stats = dict(fires=0, excused=0, evictions=0, sizes=set())
+    stats = dict(fires=0, excused=0, evictions=0, sizes=set(), fetched=0, selected=0)
     for t in range(steps):
         eng.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
         torch.cuda.synchronize()
@@ -389,6 +408,10 @@ def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, seg
                            to64(data.gen_values[t, gi * H:(gi + 1) * H]), fire_override=bool(fire[gi]),
                            select_override=override)
             assert to_np(eng.n_sel[gi * H:(gi + 1) * H]).tolist() == rec.n_sel
+            if eng.delta and fire[gi]:
+                _check_delta_buffers(eng, gi, H)
+                stats["fetched"] += int(eng.n_fetched[gi * H:(gi + 1) * H].sum())
+                stats["selected"] += int(eng.n_sel[gi * H:(gi + 1) * H].sum())
             got = to64(eng.out[gi])
             if data.prompt_keys.dtype == torch.float32:
                 check_rows_rel(got, rec.out, 1e-5, f"step {t} attention")
@@ -434,13 +457,25 @@ def test_decode_loop_bf16_with_evictions(zero_copy):
     assert st["fires"] > 40
 
 
-def test_decode_loop_host_pool():
+@pytest.mark.parametrize("delta", [True, False])
+def test_decode_loop_host_pool(delta):
     """The same reduction with the KV pool in pinned host memory: prefill packs
-    into it, evictions append to it and retrieval gathers from it over the
-    host link."""
+    into it, evictions append to it and retrieval copies from it over the
+    host link, either every selected row (gather) or only the rows the
+    previous selection did not hold (delta, the engine's default there)."""
     wl = synth.get_workload("host-131k").replace(prompt_len=2048, n_clusters=64, budget=512, name="host-131k")
-    st = _run_loop(wl, 1, 200, mode=1, pool_on_host=True)
+    st = _run_loop(wl, 1, 200, mode=1, pool_on_host=True, delta=delta)
     assert st["fires"] > 20
+    if delta:
+        assert 0 < st["fetched"] < st["selected"]
+
+
+def test_decode_loop_delta_device_pool():
+    """Delta transfers over a pool in device memory (bf16 reduction with
+    evictions, two groups)."""
+    wl = synth.get_workload("si-lo-16k").replace(prompt_len=2048, n_clusters=64, budget=512, name="si-lo-16k")
+    st = _run_loop(wl, 2, 300, mode=1, zero_copy=False, delta=True)
+    assert st["fires"] > 40 and 0 < st["fetched"] < st["selected"]
 
 
 @pytest.mark.parametrize("zero_copy", [True, False])
