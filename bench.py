@@ -8,6 +8,9 @@ retrieval at boundaries (budget 2048), window store and sparse attention for
 all layers):
 
   prefill   louiskv_cluster_prefill (k-means + cluster-packed K/V pool)
+            (after the timed steps, the pipelined variant is timed apart:
+            louiskv_cluster_prefill_pipelined, one layer's slices per chunk,
+            each chunk's pool write overlapped with the next chunk's k-means)
   decode    128 x [boundary_check, retrieve_rows, segment_output,
                    sparse_decode_attn_rows]   (KV_critical as a pool row list)
 
@@ -237,6 +240,39 @@ def cpu_baseline(wl, data, budget_s: float):
     }
 
 
+def time_pipelined_prefill(eng, data, chunk: int, copy_engine: bool, reps: int = 3) -> float:
+    """Mean ms of louiskv_cluster_prefill_pipelined over the engine's buffers
+    (the clustering of each chunk of slices overlapped with the pool write of
+    the previous one), after one untimed call."""
+    import torch
+    from paper_2510_11292_amd import louiskv as L
+    c = eng.cfg
+    S = c.n_slices
+    chunk = max(1, min(chunk, S))
+    dc = L.BF16 if eng.dtype == torch.bfloat16 else L.F32
+    ws = torch.empty(L.cluster_prefill_pipelined_workspace_size(chunk, c.prompt_len, c.n_clusters, dc,
+                                                                eng.pool_on_host, copy_engine),
+                     dtype=torch.uint8, device=eng.device)
+    events = [torch.cuda.Event() for _ in range(-(-S // chunk) + 1)]
+    for e in events:
+        e.record()
+    copy_stream = torch.cuda.Stream()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    total = 0.0
+    for i in range(reps + 1):
+        t0.record()
+        L.cluster_prefill_pipelined(data.prompt_keys, c.n_clusters, c.n_iters, data.init_idx, eng.reps,
+                                    eng.unit_start, eng.unit_size, eng.assign, eng.perm, data.prompt_values,
+                                    eng.k_pool, eng.v_pool, chunk, events, copy_stream,
+                                    pool_on_host=eng.pool_on_host, copy_engine=copy_engine, workspace=ws)
+        t1.record()
+        torch.cuda.synchronize()
+        if i > 0:
+            total += t0.elapsed_time(t1)
+    del ws
+    return total / reps
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -250,6 +286,9 @@ def main() -> int:
                     help="seconds of oracle k-means, and again of oracle decode steps, in the CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="launch decode steps one by one (no HIP graph)")
+    ap.add_argument("--prefill-chunk", type=int, default=0,
+                    help="slices per chunk of the pipelined prefill that is timed after the run "
+                         "(default: one layer's KV heads; -1 skips it)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after the run, copy this many MiB three times (counter calibration for profiles)")
     args = ap.parse_args()
@@ -353,6 +392,20 @@ def main() -> int:
     dense_ms = None
     if (eng.zero_copy or eng.delta) and not args.eager:
         dense_ms = dense_decode_ms(wl, data, cfg, dtype)
+    pipelined = None
+    if args.prefill_chunk >= 0:
+        chunk = args.prefill_chunk or wl.n_kv_heads
+        pipelined = {"slices_per_chunk": chunk, "serial_ms": t_pre * 1e3}
+        pipelined["overlapped_ms"] = time_pipelined_prefill(eng, data, chunk, True)
+        if eng.pool_on_host:
+            pipelined["pool_write"] = "copy engines (HBM staging, pitched copy)"
+            pipelined["overlapped_ms_pack_kernel"] = time_pipelined_prefill(eng, data, chunk, False)
+        else:
+            pipelined["pool_write"] = "pack kernel on a second stream"
+        log(f"prefill: serial {t_pre * 1e3:.2f} ms; pipelined over chunks of {chunk} slices "
+            f"{pipelined['overlapped_ms']:.2f} ms"
+            + (f" (pack kernel instead of copy engines: {pipelined['overlapped_ms_pack_kernel']:.2f} ms)"
+               if eng.pool_on_host else ""))
     out = {
         "metric": METRIC,
         "value": keys / t_cluster,
@@ -383,6 +436,7 @@ def main() -> int:
         "cluster_ms": t_cluster * 1e3,
         "pool_pack_ms": t_pack * 1e3,
         "decode_ms": t_dec * 1e3,
+        "prefill_pipelined": pipelined,
         "roofline": {
             "kernel": "kmeans_assign (bf16 MFMA, fused argmin)",
             "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",

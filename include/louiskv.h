@@ -186,6 +186,52 @@ int louiskv_pack_pool(const void* keys, const void* values, int32_t dtype,
                       int64_t pool_rows, int32_t pool_on_host, void* stream);
 
 /*
+ * louiskv_cluster_prefill with the pool write overlapped (Section 4.2 prefill
+ * stage: clustering and offload run asynchronously; Algorithm 1
+ * store_cache(prefill), asynchronous offload of (K, V)).  The slices are
+ * taken in chunks of `slices_per_chunk` (one layer's KV heads is the natural
+ * chunk).  Each chunk is clustered on `stream`; its pool write then runs on
+ * `copy_stream`, beside the clustering of the following chunks.  Outputs and
+ * pool contents are those of louiskv_cluster_prefill, bit for bit.
+ *
+ * Arguments as louiskv_cluster_prefill, with k_pool required, plus:
+ * slices_per_chunk  >= 1; n_chunks = ceil(n_slices / min(slices_per_chunk, n_slices)).
+ * copy_engine  host pools only: 1 = permute each chunk into HBM staging (in the
+ *             workspace) and write it with the DMA copy engines
+ *             (hipMemcpy2DAsync), leaving the compute units to the clustering;
+ *             0 = a pack kernel on copy_stream writes the pool directly through
+ *             the mapping, with a bounded grid.  Device pools always use the
+ *             pack kernel.
+ * chunk_events  n_events >= n_chunks + 1 hipEvent_t created by the caller
+ *             (hipEventDisableTiming suffices); the library records event i on
+ *             `stream` after chunk i and the last one on `copy_stream` after the
+ *             last pool write, and makes `stream` wait for it, so that work
+ *             enqueued on `stream` after this call sees the whole pool.
+ * workspace   louiskv_cluster_prefill_pipelined_workspace_size(slices_per_chunk,
+ *             ...) bytes; reused by every chunk.
+ * stream, copy_stream  may be the same stream (no overlap).
+ * Errors as louiskv_cluster_prefill; a NULL event is ERR_NULL.
+ */
+size_t louiskv_cluster_prefill_pipelined_workspace_size(int64_t slices_per_chunk,
+                                                        int32_t n_tokens, int32_t d,
+                                                        int32_t n_clusters, int32_t dtype,
+                                                        int32_t pool_on_host,
+                                                        int32_t copy_engine);
+
+int louiskv_cluster_prefill_pipelined(const void* keys, int32_t dtype, int64_t n_slices,
+                                      int32_t n_tokens, int32_t d, int32_t n_clusters,
+                                      int32_t n_iters, const int32_t* init_idx,
+                                      float* reps, int32_t units_cap,
+                                      int32_t* unit_start, int32_t* unit_size,
+                                      int32_t* assign, int32_t* perm,
+                                      const void* values, void* k_pool, void* v_pool,
+                                      int64_t pool_rows, int32_t pool_on_host,
+                                      int64_t slices_per_chunk, int32_t copy_engine,
+                                      void* const* chunk_events, int64_t n_events,
+                                      void* workspace, size_t workspace_bytes,
+                                      void* stream, void* copy_stream);
+
+/*
  * One assignment step alone (the first half of a Lloyd iteration above), for
  * step-by-step checking: assign[s][i] = argmin_c ||keys[s][i] - op(c)||^2 over
  * the n_clusters float32 centroids at centroids[s][0..C-1] (slice stride

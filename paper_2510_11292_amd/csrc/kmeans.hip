@@ -814,17 +814,19 @@ __global__ void finalize_kernel(const int32_t* __restrict__ members, const int32
 template <class T>
 __global__ void pack_pool_kernel(const T* __restrict__ src, const int32_t* __restrict__ perm,
                                  T* __restrict__ pool, int64_t pool_rows, int n_tokens, int64_t n_rows) {
-  const int64_t g = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);   // 16 rows per block of 256
-  if (g >= n_rows) return;
+  // 16 rows per block of 256 per round; a grid smaller than n_rows / 16
+  // blocks strides over the rest (a pack that shares the chip with clustering)
   const int sub = threadIdx.x & 15;
-  const int64_t s = g / n_tokens;
-  const int r = (int)(g - s * n_tokens);
-  const int tok = min(max(perm[s * n_tokens + r], 0), n_tokens - 1);   // perm may come from the caller
-  constexpr int kU4 = kHeadDim * sizeof(T) / 16;
-  const uint4* a = reinterpret_cast<const uint4*>(src + ((size_t)s * n_tokens + tok) * kHeadDim);
-  uint4* b = reinterpret_cast<uint4*>(pool + ((size_t)s * pool_rows + r) * kHeadDim);
+  for (int64_t g = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4); g < n_rows; g += (int64_t)gridDim.x * 16) {
+    const int64_t s = g / n_tokens;
+    const int r = (int)(g - s * n_tokens);
+    const int tok = min(max(perm[s * n_tokens + r], 0), n_tokens - 1);   // perm may come from the caller
+    constexpr int kU4 = kHeadDim * sizeof(T) / 16;
+    const uint4* a = reinterpret_cast<const uint4*>(src + ((size_t)s * n_tokens + tok) * kHeadDim);
+    uint4* b = reinterpret_cast<uint4*>(pool + ((size_t)s * pool_rows + r) * kHeadDim);
 #pragma unroll
-  for (int q = sub; q < kU4; q += 16) b[q] = a[q];
+    for (int q = sub; q < kU4; q += 16) b[q] = a[q];
+  }
 }
 
 // ------------------------------------------------------------------ host side
@@ -939,9 +941,10 @@ int launch_sum(const void* keys, int dtype, int64_t S, int N, int C, const Ws& w
 
 // Prompt K/V rows in perm order into the pools (each cluster one contiguous run).
 int launch_pack(const void* keys, const void* values, int dtype, int64_t S, int N, const int32_t* perm, void* k_pool,
-                void* v_pool, int64_t pool_rows, hipStream_t s) {
+                void* v_pool, int64_t pool_rows, hipStream_t s, int max_grid = 0) {
   const int64_t prow = S * N;
-  const int pgrid = (int)((prow + 15) / 16);
+  int pgrid = (int)((prow + 15) / 16);
+  if (max_grid > 0) pgrid = std::min(pgrid, max_grid);
   for (int which = 0; which < 2; ++which) {
     void* pool = which == 0 ? k_pool : v_pool;
     const void* src = which == 0 ? keys : values;
@@ -952,6 +955,45 @@ int launch_pack(const void* keys, const void* values, int dtype, int64_t S, int 
     else
       pack_pool_kernel<float><<<pgrid, 256, 0, s>>>(static_cast<const float*>(src), perm, static_cast<float*>(pool),
                                                      pool_rows, N, prow);
+    LKV_CHECK_LAUNCH();
+  }
+  return LOUISKV_OK;
+}
+
+
+// Initial centroids, n_iters Lloyd iterations and the CSR/perm outputs, for
+// arguments already validated (no pool write).
+int run_cluster(const void* keys, int dtype, int64_t S, int N, int C, int n_iters, const int32_t* init_idx,
+                float* reps, int units_cap, int32_t* unit_start, int32_t* unit_size, int32_t* assign, int32_t* perm,
+                void* const* iter_events, const Ws& w, hipStream_t s) {
+  int st;
+  {
+    const int64_t rows = S * C;
+    const int grid = (int)((rows + 3) / 4);
+    if (dtype == LOUISKV_BF16)
+      init_centroids_kernel<uint16_t><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(keys), init_idx, reps,
+                                                            N, C, units_cap, rows);
+    else
+      init_centroids_kernel<float><<<grid, 256, 0, s>>>(static_cast<const float*>(keys), init_idx, reps, N,
+                                                         C, units_cap, rows);
+    LKV_CHECK_LAUNCH();
+  }
+  // the first operand comes from the initial centroids; after that each
+  // update writes the next one (and clears the counts) as it goes
+  if ((st = launch_prep(reps, units_cap, S, C, dtype, w, true, s))) return st;
+  for (int it = 0; it < n_iters; ++it) {
+    if (iter_events) LKV_CHECK_HIP(hipEventRecord(reinterpret_cast<hipEvent_t>(iter_events[2 * it]), s));
+    if ((st = launch_assign(keys, dtype, S, N, C, w, assign, true, it > 0, it == 0 ? 1 : 2, s)))
+      return st;
+    if (iter_events) LKV_CHECK_HIP(hipEventRecord(reinterpret_cast<hipEvent_t>(iter_events[2 * it + 1]), s));
+    if ((st = launch_scan_scatter(assign, S, N, C, w, s))) return st;
+    if ((st = launch_sum(keys, dtype, S, N, C, w, reps, reps, units_cap, it + 1 < n_iters, s)))
+      return st;
+  }
+  {
+    const int64_t rows = S * C;
+    finalize_kernel<<<(int)((rows + 3) / 4), 256, 0, s>>>(w.members, w.offsets, w.counts, perm, unit_start,
+                                                          unit_size, units_cap, N, C, rows);
     LKV_CHECK_LAUNCH();
   }
   return LOUISKV_OK;
@@ -1004,37 +1046,117 @@ extern "C" int louiskv_cluster_prefill(const void* keys, int32_t dtype, int64_t 
     return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need.bytes, workspace_bytes);
   const Ws w = carve(workspace, n_slices, n_tokens, n_clusters, dtype);
   hipStream_t s = as_stream(stream);
-
-  {
-    const int64_t rows = n_slices * n_clusters;
-    const int grid = (int)((rows + 3) / 4);
-    if (dtype == LOUISKV_BF16)
-      init_centroids_kernel<uint16_t><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(keys), init_idx, reps,
-                                                            n_tokens, n_clusters, units_cap, rows);
-    else
-      init_centroids_kernel<float><<<grid, 256, 0, s>>>(static_cast<const float*>(keys), init_idx, reps, n_tokens,
-                                                         n_clusters, units_cap, rows);
-    LKV_CHECK_LAUNCH();
-  }
-  // the first operand comes from the initial centroids; after that each
-  // update writes the next one (and clears the counts) as it goes
-  if ((st = launch_prep(reps, units_cap, n_slices, n_clusters, dtype, w, true, s))) return st;
-  for (int it = 0; it < n_iters; ++it) {
-    if (iter_events) LKV_CHECK_HIP(hipEventRecord(reinterpret_cast<hipEvent_t>(iter_events[2 * it]), s));
-    if ((st = launch_assign(keys, dtype, n_slices, n_tokens, n_clusters, w, assign, true, it > 0, it == 0 ? 1 : 2, s)))
-      return st;
-    if (iter_events) LKV_CHECK_HIP(hipEventRecord(reinterpret_cast<hipEvent_t>(iter_events[2 * it + 1]), s));
-    if ((st = launch_scan_scatter(assign, n_slices, n_tokens, n_clusters, w, s))) return st;
-    if ((st = launch_sum(keys, dtype, n_slices, n_tokens, n_clusters, w, reps, reps, units_cap, it + 1 < n_iters, s)))
-      return st;
-  }
-  {
-    const int64_t rows = n_slices * n_clusters;
-    finalize_kernel<<<(int)((rows + 3) / 4), 256, 0, s>>>(w.members, w.offsets, w.counts, perm, unit_start,
-                                                          unit_size, units_cap, n_tokens, n_clusters, rows);
-    LKV_CHECK_LAUNCH();
-  }
+  if ((st = run_cluster(keys, dtype, n_slices, n_tokens, n_clusters, n_iters, init_idx, reps, units_cap, unit_start,
+                        unit_size, assign, perm, iter_events, w, s)))
+    return st;
   return launch_pack(keys, values, dtype, n_slices, n_tokens, perm, k_pool, v_pool, pool_rows, s);
+}
+
+namespace louiskv {
+namespace {
+
+size_t esize_of(int dtype) { return dtype == LOUISKV_BF16 ? 2 : 4; }
+
+// Workspace of the pipelined prefill: the clustering workspace of one chunk,
+// then (copy-engine writes only) one chunk of staged pool rows.
+size_t pipelined_bytes(int64_t chunk, int N, int C, int dtype, bool staged) {
+  size_t b = carve(nullptr, chunk, N, C, dtype).bytes;
+  if (staged) b += align_up((size_t)chunk * N * kHeadDim * esize_of(dtype), 256);
+  return b;
+}
+
+// Largest pack grid while the pack shares the chip with the clustering of
+// the next chunk: enough rows in flight for the host link, few CUs held.
+constexpr int kOverlapPackGrid = 256;
+
+}  // namespace
+}  // namespace louiskv
+
+extern "C" size_t louiskv_cluster_prefill_pipelined_workspace_size(int64_t slices_per_chunk, int32_t n_tokens,
+                                                                   int32_t d, int32_t n_clusters, int32_t dtype,
+                                                                   int32_t pool_on_host, int32_t copy_engine) {
+  (void)d;
+  if (slices_per_chunk < 1 || n_tokens < 1 || n_clusters < 1) return 0;
+  const int dt = dtype == LOUISKV_BF16 ? LOUISKV_BF16 : LOUISKV_F32;
+  return pipelined_bytes(slices_per_chunk, n_tokens, n_clusters, dt, pool_on_host && copy_engine);
+}
+
+extern "C" int louiskv_cluster_prefill_pipelined(
+    const void* keys, int32_t dtype, int64_t n_slices, int32_t n_tokens, int32_t d, int32_t n_clusters,
+    int32_t n_iters, const int32_t* init_idx, float* reps, int32_t units_cap, int32_t* unit_start,
+    int32_t* unit_size, int32_t* assign, int32_t* perm, const void* values, void* k_pool, void* v_pool,
+    int64_t pool_rows, int32_t pool_on_host, int64_t slices_per_chunk, int32_t copy_engine,
+    void* const* chunk_events, int64_t n_events, void* workspace, size_t workspace_bytes, void* stream,
+    void* copy_stream) {
+  int st = check_common(keys, dtype, n_slices, n_tokens, d, n_clusters);
+  if (st) return st;
+  if (!init_idx || !reps || !unit_start || !unit_size || !assign || !perm || !k_pool)
+    return fail(LOUISKV_ERR_NULL, "init_idx, reps, unit_start, unit_size, assign, perm and k_pool are required");
+  if (n_iters < 1) return fail(LOUISKV_ERR_SHAPE, "n_iters=%d must be >= 1", n_iters);
+  if (units_cap < n_clusters) return fail(LOUISKV_ERR_SHAPE, "units_cap=%d < n_clusters=%d", units_cap, n_clusters);
+  if (v_pool && !values) return fail(LOUISKV_ERR_NULL, "v_pool given without values");
+  if (pool_rows < n_tokens)
+    return fail(LOUISKV_ERR_SHAPE, "pool_rows=%lld < n_tokens=%d", (long long)pool_rows, n_tokens);
+  if (slices_per_chunk < 1) return fail(LOUISKV_ERR_SHAPE, "slices_per_chunk=%lld must be >= 1",
+                                        (long long)slices_per_chunk);
+  const int64_t chunk = std::min(slices_per_chunk, n_slices);
+  const int64_t n_chunks = (n_slices + chunk - 1) / chunk;
+  if (!chunk_events || n_events < n_chunks + 1)
+    return fail(LOUISKV_ERR_NULL, "chunk_events must hold n_chunks + 1 = %lld events, got %lld",
+                (long long)(n_chunks + 1), (long long)n_events);
+  for (int64_t i = 0; i <= n_chunks; ++i)
+    if (!chunk_events[i]) return fail(LOUISKV_ERR_NULL, "chunk_events[%lld] is NULL", (long long)i);
+  void* k_dev = k_pool;
+  void* v_dev = v_pool;
+  if (pool_on_host && ((st = device_view_of_host_pool(k_pool, &k_dev)) || (st = device_view_of_host_pool(v_pool, &v_dev))))
+    return st;
+  const bool staged = pool_on_host && copy_engine;
+  const size_t need = pipelined_bytes(chunk, n_tokens, n_clusters, dtype, staged);
+  if (!workspace || workspace_bytes < need)
+    return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  const Ws w = carve(workspace, chunk, n_tokens, n_clusters, dtype);
+  void* staging = static_cast<char*>(workspace) + w.bytes;
+  hipStream_t s = as_stream(stream);
+  hipStream_t cp = as_stream(copy_stream);
+  const size_t es = esize_of(dtype);
+  const size_t row_bytes = (size_t)kHeadDim * es;
+  for (int64_t i = 0; i < n_chunks; ++i) {
+    const int64_t c0 = i * chunk;
+    const int64_t n = std::min(chunk, n_slices - c0);
+    const size_t kv_off = (size_t)c0 * n_tokens * row_bytes;
+    const size_t pool_off = (size_t)c0 * pool_rows * row_bytes;
+    const void* keys_c = static_cast<const char*>(keys) + kv_off;
+    const void* vals_c = values ? static_cast<const char*>(values) + kv_off : nullptr;
+    int32_t* perm_c = perm + c0 * n_tokens;
+    if ((st = run_cluster(keys_c, dtype, n, n_tokens, n_clusters, n_iters, init_idx + c0 * n_clusters,
+                          reps + c0 * units_cap * kHeadDim, units_cap, unit_start + c0 * units_cap,
+                          unit_size + c0 * units_cap, assign + c0 * n_tokens, perm_c, nullptr, w, s)))
+      return st;
+    // the pool write of this chunk waits for its clustering only and runs
+    // beside the clustering of the next chunks
+    LKV_CHECK_HIP(hipEventRecord(reinterpret_cast<hipEvent_t>(chunk_events[i]), s));
+    LKV_CHECK_HIP(hipStreamWaitEvent(cp, reinterpret_cast<hipEvent_t>(chunk_events[i]), 0));
+    if (!staged) {
+      if ((st = launch_pack(keys_c, vals_c, dtype, n, n_tokens, perm_c,
+                            static_cast<char*>(k_dev) + pool_off, v_dev ? static_cast<char*>(v_dev) + pool_off : nullptr,
+                            pool_rows, cp, kOverlapPackGrid)))
+        return st;
+      continue;
+    }
+    // copy engine: permute into HBM staging, then one pitched copy over the host link
+    for (int which = 0; which < 2; ++which) {
+      void* host = which == 0 ? k_pool : v_pool;
+      if (!host) continue;
+      const void* src = which == 0 ? keys_c : vals_c;
+      if ((st = launch_pack(src, nullptr, dtype, n, n_tokens, perm_c, staging, nullptr, n_tokens, cp))) return st;
+      LKV_CHECK_HIP(hipMemcpy2DAsync(static_cast<char*>(host) + pool_off, (size_t)pool_rows * row_bytes, staging,
+                                     (size_t)n_tokens * row_bytes, (size_t)n_tokens * row_bytes, (size_t)n,
+                                     hipMemcpyDeviceToHost, cp));
+    }
+  }
+  LKV_CHECK_HIP(hipEventRecord(reinterpret_cast<hipEvent_t>(chunk_events[n_chunks]), cp));
+  LKV_CHECK_HIP(hipStreamWaitEvent(s, reinterpret_cast<hipEvent_t>(chunk_events[n_chunks]), 0));
+  return LOUISKV_OK;
 }
 
 extern "C" int louiskv_pack_pool(const void* keys, const void* values, int32_t dtype, int64_t n_slices,

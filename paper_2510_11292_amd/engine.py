@@ -6,7 +6,10 @@ paper's Algorithm 1:
 
   prefill()  louiskv_cluster_prefill: k-means per slice, centroids as unit
              index vectors; louiskv_pack_pool: prompt K/V packed cluster by
-             cluster into the pool.
+             cluster into the pool.  With prefill_chunk set,
+             louiskv_cluster_prefill_pipelined clusters the slices chunk by
+             chunk and writes each chunk's pool rows on a second stream
+             while the next chunk is clustered.
   step()     one decode step for every group: louiskv_boundary_check, then
              louiskv_retrieve for the groups that fired (scores see the units
              evicted before this step), louiskv_segment_output (window append,
@@ -87,7 +90,8 @@ def config_from_workload(wl, n_groups: Optional[int] = None, mode: int = L.REF_A
 class LouisKVEngine:
     def __init__(self, cfg: EngineConfig, dtype: torch.dtype, device="cuda", pool_on_host: bool = False,
                  keep_scores: bool = False, out_dtype: Optional[torch.dtype] = None,
-                 zero_copy: Optional[bool] = None, delta: Optional[bool] = None):
+                 zero_copy: Optional[bool] = None, delta: Optional[bool] = None,
+                 prefill_chunk: Optional[int] = None, copy_engine: bool = True):
         self.cfg = cfg
         self.dtype = dtype
         self.device = torch.device(device)
@@ -142,7 +146,21 @@ class LouisKVEngine:
                           if cfg.segments == "boundary" else None)
         dc = L.BF16 if dtype == torch.bfloat16 else L.F32
         u8 = dict(dtype=torch.uint8, device=dev)
-        self.ws_prefill = torch.empty(L.cluster_prefill_workspace_size(S, cfg.prompt_len, cfg.n_clusters, dc), **u8)
+        # prefill_chunk: cluster that many slices at a time and write each
+        # chunk's pool rows on a second stream beside the next chunk's clustering
+        self.prefill_chunk = None if prefill_chunk is None else max(1, min(int(prefill_chunk), S))
+        self.copy_engine = bool(copy_engine)
+        if self.prefill_chunk is None:
+            self.ws_prefill = torch.empty(L.cluster_prefill_workspace_size(S, cfg.prompt_len, cfg.n_clusters, dc),
+                                          **u8)
+        else:
+            self.ws_prefill = torch.empty(L.cluster_prefill_pipelined_workspace_size(
+                self.prefill_chunk, cfg.prompt_len, cfg.n_clusters, dc, pool_on_host, self.copy_engine), **u8)
+            n_chunks = -(-S // self.prefill_chunk)
+            self.chunk_events = [torch.cuda.Event() for _ in range(n_chunks + 1)]
+            for e in self.chunk_events:
+                e.record()
+            self.copy_stream = torch.cuda.Stream(device=dev)
         g = cfg.n_q_heads // cfg.n_kv_heads
         rows = max(cfg.budget, 1)
         if self.zero_copy:
@@ -163,13 +181,22 @@ class LouisKVEngine:
         write (louiskv_pack_pool).  pack_event, if given, is recorded between
         the two on the current stream."""
         c = self.cfg
-        L.cluster_prefill(prompt_keys, c.n_clusters, c.n_iters, init_idx, self.reps, self.unit_start,
-                          self.unit_size, self.assign, self.perm, iter_events=iter_events,
-                          workspace=self.ws_prefill)
-        if pack_event is not None:
-            pack_event.record()
-        L.pack_pool(prompt_keys, prompt_values, self.perm, self.k_pool, self.v_pool,
-                    pool_on_host=self.pool_on_host)
+        if self.prefill_chunk is not None:
+            if iter_events is not None or pack_event is not None:
+                raise ValueError("the pipelined prefill takes no iteration or pack events")
+            L.cluster_prefill_pipelined(prompt_keys, c.n_clusters, c.n_iters, init_idx, self.reps, self.unit_start,
+                                        self.unit_size, self.assign, self.perm, prompt_values, self.k_pool,
+                                        self.v_pool, self.prefill_chunk, self.chunk_events, self.copy_stream,
+                                        pool_on_host=self.pool_on_host, copy_engine=self.copy_engine,
+                                        workspace=self.ws_prefill)
+        else:
+            L.cluster_prefill(prompt_keys, c.n_clusters, c.n_iters, init_idx, self.reps, self.unit_start,
+                              self.unit_size, self.assign, self.perm, iter_events=iter_events,
+                              workspace=self.ws_prefill)
+            if pack_event is not None:
+                pack_event.record()
+            L.pack_pool(prompt_keys, prompt_values, self.perm, self.k_pool, self.v_pool,
+                        pool_on_host=self.pool_on_host)
         if self.seg_state is not None:
             L.segment_state_init(self.seg_state, c.window, c.n_clusters)
         if self.delta:

@@ -37,6 +37,11 @@ _SIGS = {
         _P, _I32, _P, _P, _P, _P,
         _P, _P, _P, _I64, _I32, _P, _P, _SZ, _P]),
     "louiskv_pack_pool": (ctypes.c_int, [_P, _P, _I32, _I64, _I32, _I32, _P, _P, _P, _I64, _I32, _P]),
+    "louiskv_cluster_prefill_pipelined_workspace_size": (_SZ, [_I64, _I32, _I32, _I32, _I32, _I32, _I32]),
+    "louiskv_cluster_prefill_pipelined": (ctypes.c_int, [
+        _P, _I32, _I64, _I32, _I32, _I32, _I32, _P,
+        _P, _I32, _P, _P, _P, _P,
+        _P, _P, _P, _I64, _I32, _I64, _I32, _P, _I64, _P, _SZ, _P, _P]),
     "louiskv_kmeans_assign": (ctypes.c_int, [_P, _I32, _I64, _I32, _I32, _I32, _P, _I32, _P, _P, _SZ, _P]),
     "louiskv_kmeans_update": (ctypes.c_int, [_P, _I32, _I64, _I32, _I32, _I32, _P, _P, _P, _I32, _P, _P, _SZ, _P]),
     "louiskv_segment_output": (ctypes.c_int, [
@@ -187,6 +192,31 @@ def cluster_prefill(keys, n_clusters: int, n_iters: int, init_idx, reps, unit_st
         _ptr(reps), reps.shape[1], _ptr(unit_start), _ptr(unit_size), _ptr(assign), _ptr(perm),
         _ptr(values), _ptr(k_pool), _ptr(v_pool), pool_rows, int(pool_on_host), ev,
         _ptr(ws), wsb, _stream(stream)))
+
+
+def cluster_prefill_pipelined_workspace_size(slices_per_chunk, n_tokens, n_clusters, dtype_code, pool_on_host,
+                                             copy_engine, d=128) -> int:
+    return load_library().louiskv_cluster_prefill_pipelined_workspace_size(
+        slices_per_chunk, n_tokens, d, n_clusters, dtype_code, int(pool_on_host), int(copy_engine))
+
+
+def cluster_prefill_pipelined(keys, n_clusters: int, n_iters: int, init_idx, reps, unit_start, unit_size, assign,
+                              perm, values, k_pool, v_pool, slices_per_chunk: int, chunk_events: Sequence,
+                              copy_stream, pool_on_host: bool = False, copy_engine: bool = True, workspace=None,
+                              stream=None):
+    """louiskv_cluster_prefill_pipelined: chunk_events holds ceil(S / chunk) + 1
+    torch.cuda.Event objects (recorded once already, so that they exist)."""
+    s, n, d = keys.shape
+    dt = _dtype_code(keys)
+    ws, wsb = _ws(cluster_prefill_pipelined_workspace_size(min(slices_per_chunk, s), n, n_clusters, dt,
+                                                           pool_on_host, copy_engine, d), keys.device, workspace)
+    arr = (ctypes.c_void_p * len(chunk_events))(*[e.cuda_event for e in chunk_events])
+    _check(load_library().louiskv_cluster_prefill_pipelined(
+        _ptr(keys), dt, s, n, d, n_clusters, n_iters, _ptr(init_idx),
+        _ptr(reps), reps.shape[1], _ptr(unit_start), _ptr(unit_size), _ptr(assign), _ptr(perm),
+        _ptr(values), _ptr(k_pool), _ptr(v_pool), k_pool.shape[1], int(pool_on_host), slices_per_chunk,
+        int(copy_engine), ctypes.cast(arr, ctypes.c_void_p), len(chunk_events), _ptr(ws), wsb, _stream(stream),
+        _stream(copy_stream)))
 
 
 def kmeans_assign(keys, n_clusters: int, centroids, assign, workspace=None, stream=None):

@@ -137,6 +137,35 @@ def test_boundary_segment_calls_validate_on_the_host(lib):
                                                    None) == 2
 
 
+def test_pipelined_prefill_validates_on_the_host(lib):
+    """The pipelined prefill refuses a missing pool, a zero chunk and too few or
+    NULL events before any launch; its workspace is one chunk's."""
+    P = ctypes.c_void_p
+    dummy = P(16)
+    ev3 = (ctypes.c_void_p * 3)(16, 16, 16)
+    ev3_null = (ctypes.c_void_p * 3)(16, None, 16)
+
+    def call(k_pool=dummy, chunk=4, events=ev3, n_events=3, n_slices=8):
+        return lib.louiskv_cluster_prefill_pipelined(
+            dummy, 1, n_slices, 64, 128, 8, 1, dummy, dummy, 8, dummy, dummy, dummy, dummy,
+            None, k_pool, None, 64, 0, chunk, 1, ctypes.cast(events, P) if events is not None else None, n_events,
+            dummy, 1 << 30, None, None)
+
+    assert call(k_pool=None) == 1
+    assert call(chunk=0) == 2
+    assert call(events=None) == 1
+    assert call(n_events=2) == 1            # 8 slices in chunks of 4 need 3 events
+    assert call(chunk=3, n_events=3) == 1   # chunks of 3 need 4
+    assert call(events=ev3_null) == 1
+    one = lib.louiskv_cluster_prefill_workspace_size(8, 32768, 128, 1024, 1)
+    assert lib.louiskv_cluster_prefill_pipelined_workspace_size(8, 32768, 128, 1024, 1, 0, 1) == one
+    assert lib.louiskv_cluster_prefill_pipelined_workspace_size(8, 32768, 128, 1024, 1, 1, 0) == one
+    # host pool through the copy engines: plus one chunk of staged rows
+    assert lib.louiskv_cluster_prefill_pipelined_workspace_size(8, 32768, 128, 1024, 1, 1, 1) == \
+        one + 8 * 32768 * 256
+    assert lib.louiskv_cluster_prefill_pipelined_workspace_size(0, 32768, 128, 1024, 1, 1, 1) == 0
+
+
 def test_workspace_sizes_are_positive(lib):
     assert lib.louiskv_cluster_prefill_workspace_size(256, 32768, 128, 1024, 1) > 256 * 32768 * 4
     assert lib.louiskv_retrieve_workspace_size(256, 1024, 2048) > 0

@@ -218,3 +218,76 @@ def test_pack_pool_writes_rows_in_perm_order(dtype):
         assert torch.equal(kp[s, :N], keys[s, idx[s]])
         assert torch.equal(vp[s, :N], values[s, idx[s]])
         assert torch.all(kp[s, N:] == 5) and torch.all(vp[s, N:] == 6)
+
+
+PIPELINE_CASES = [
+    # (dtype, n_slices, n_tokens, n_clusters, slices_per_chunk, pool_on_host, copy_engine)
+    (torch.float32, 8, 4096, 64, 3, False, True),     # ragged last chunk (3, 3, 2)
+    (torch.bfloat16, 10, 5003, 77, 4, True, True),    # host pool through the copy engines
+    (torch.bfloat16, 10, 5003, 77, 4, True, False),   # host pool written by the pack kernel
+    (torch.bfloat16, 4, 4096, 128, 1, False, True),   # one slice per chunk
+    (torch.bfloat16, 4, 4096, 128, 8, True, True),    # one chunk holds every slice
+]
+
+
+@pytest.mark.parametrize("dtype,S,N,C,chunk,host,copy_engine", PIPELINE_CASES)
+def test_cluster_prefill_pipelined_equals_one_pass(dtype, S, N, C, chunk, host, copy_engine):
+    """louiskv_cluster_prefill_pipelined gives the outputs and pool contents of
+    louiskv_cluster_prefill bit for bit (the chunks are independent slices),
+    leaves the pool rows past the prompt alone, and orders work enqueued on the
+    calling stream after the whole pool write."""
+    L = _L()
+    keys = _keys(S, N, dtype, 700 + S)
+    g = torch.Generator(device=DEV).manual_seed(701)
+    values = torch.randn(S, N, 128, generator=g, device=DEV).to(dtype)
+    init = _init(S, N, C, 702)
+    cap, extra, iters = C + 5, 37, 4
+
+    def outputs():
+        return dict(reps=torch.zeros(S, cap, 128, device=DEV),
+                    ustart=torch.zeros(S, cap, dtype=torch.int32, device=DEV),
+                    usize=torch.zeros(S, cap, dtype=torch.int32, device=DEV),
+                    assign=torch.zeros(S, N, dtype=torch.int32, device=DEV),
+                    perm=torch.zeros(S, N, dtype=torch.int32, device=DEV))
+
+    def pools():
+        if host:
+            kp = torch.full((S, N + extra, 128), 5, dtype=dtype).pin_memory()
+            vp = torch.full((S, N + extra, 128), 6, dtype=dtype).pin_memory()
+        else:
+            kp = torch.full((S, N + extra, 128), 5, dtype=dtype, device=DEV)
+            vp = torch.full((S, N + extra, 128), 6, dtype=dtype, device=DEV)
+        return kp, vp
+
+    ref = outputs()
+    kr, vr = pools()
+    L.cluster_prefill(keys, C, iters, init, ref["reps"], ref["ustart"], ref["usize"], ref["assign"], ref["perm"],
+                      values=values, k_pool=kr, v_pool=vr, pool_on_host=host)
+    torch.cuda.synchronize()
+
+    out = outputs()
+    kp, vp = pools()
+    n_chunks = -(-S // min(chunk, S))
+    events = [torch.cuda.Event() for _ in range(n_chunks + 1)]
+    for e in events:
+        e.record()
+    copy_stream = torch.cuda.Stream()
+    print(f"pipelined prefill dtype={dtype} S={S} N={N} C={C} chunk={chunk} host={host} "
+          f"copy_engine={copy_engine}", flush=True)
+    L.cluster_prefill_pipelined(keys, C, iters, init, out["reps"], out["ustart"], out["usize"], out["assign"],
+                                out["perm"], values, kp, vp, chunk, events, copy_stream, pool_on_host=host,
+                                copy_engine=copy_engine)
+    # read the pools back with work on the calling stream, without a host sync
+    k_seen = kp.to(DEV, non_blocking=True) if host else kp.clone()
+    v_seen = vp.to(DEV, non_blocking=True) if host else vp.clone()
+    torch.cuda.synchronize()
+    for name in ref:
+        assert torch.equal(out[name], ref[name]), name
+    assert torch.equal(k_seen.cpu(), kr.cpu())
+    assert torch.equal(v_seen.cpu(), vr.cpu())
+    assert torch.all(k_seen[:, N:].cpu() == 5) and torch.all(v_seen[:, N:].cpu() == 6)
+    # the one-pass prefill is checked against the oracle elsewhere; here one
+    # slice again, directly: pool row r holds token perm[r]
+    idx = ref["perm"][S - 1].long()
+    assert torch.equal(k_seen[S - 1, :N], keys[S - 1, idx])
+    assert torch.equal(v_seen[S - 1, :N], values[S - 1, idx])
