@@ -13,6 +13,8 @@ all layers):
             each chunk's pool write overlapped with the next chunk's k-means)
   decode    128 x [boundary_check, retrieve_rows, segment_output,
                    sparse_decode_attn_rows]   (KV_critical as a pool row list)
+            launched for all layers at once; the same loop with one launch
+            sequence per layer (as a model runs) is timed apart
 
 Inputs are seeded synthetic tensors already resident in HBM before timing.
 Prints one JSON line: value = prompt keys clustered per second (the k-means
@@ -173,6 +175,44 @@ def dense_decode_ms(wl, data, cfg, dtype, reps=2):
     return ms / reps
 
 
+def layer_by_layer_decode_ms(eng, data, wl, reps=2):
+    """The decode loop with every step run group by group (one launch
+    sequence per layer of the sequence, the order in which a model produces
+    its queries), one HIP graph per decode step (as a serving loop captures
+    its steps), replayed after a fresh prefill; mean ms of the loop."""
+    import torch
+
+    def one_step(t):
+        eng.step_layer_by_layer(data.queries[t], data.gen_keys[t], data.gen_values[t])
+    eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for t in range(wl.gen_len):
+            one_step(t)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graphs = []
+    eng.t = 0
+    for t in range(wl.gen_len):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            one_step(t)
+        graphs.append(g)
+    ms = 0.0
+    for _ in range(reps):
+        eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for g in graphs:
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ms += e0.elapsed_time(e1)
+    del graphs
+    return ms / reps
+
+
 def copy_calibration(mib: int):
     """A streaming copy kernel of a known size (outside the timed region): the
     reference for scaling the HBM byte counters.  torch.mul(x, 1) reads and
@@ -289,6 +329,8 @@ def main() -> int:
     ap.add_argument("--prefill-chunk", type=int, default=0,
                     help="slices per chunk of the pipelined prefill that is timed after the run "
                          "(default: one layer's KV heads; -1 skips it)")
+    ap.add_argument("--no-layer-by-layer", action="store_true",
+                    help="skip the decode timing with one launch sequence per layer")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after the run, copy this many MiB three times (counter calibration for profiles)")
     args = ap.parse_args()
@@ -392,6 +434,16 @@ def main() -> int:
     dense_ms = None
     if (eng.zero_copy or eng.delta) and not args.eager:
         dense_ms = dense_decode_ms(wl, data, cfg, dtype)
+    layer_ms = None
+    if not args.eager and not args.no_layer_by_layer:
+        if eng.pool_on_host:
+            # not timed: capturing this path group by group (the whole loop
+            # as one graph) ended in a host segmentation fault whose cause
+            # is not established
+            log("decode layer by layer: not timed for a host-resident pool")
+        else:
+            layer_ms = layer_by_layer_decode_ms(eng, data, wl)
+            log(f"decode layer by layer: {layer_ms:.2f} ms ({wl.gen_len / (layer_ms / 1e3):.0f} steps/s)")
     pipelined = None
     if args.prefill_chunk >= 0:
         chunk = args.prefill_chunk or wl.n_kv_heads
@@ -431,6 +483,7 @@ def main() -> int:
         },
         "decode_steps_per_s": wl.gen_len / t_dec,
         "decode_steps_per_s_gathered_kv_critical": (wl.gen_len / (dense_ms / 1e3)) if dense_ms else None,
+        "decode_steps_per_s_layer_by_layer": (wl.gen_len / (layer_ms / 1e3)) if layer_ms else None,
         "delta_rows_moved_per_selected": (float(moved[0]) / max(float(moved[1]), 1.0)) if eng.delta else None,
         "prefill_ms": t_pre * 1e3,
         "cluster_ms": t_cluster * 1e3,

@@ -32,6 +32,7 @@ runs in the library's kernels.
 """
 from __future__ import annotations
 
+import dataclasses
 from dataclasses import dataclass
 from typing import Optional
 
@@ -202,6 +203,55 @@ class LouisKVEngine:
         if self.delta:
             self.buf_row.fill_(-1)
         self.t = 0
+
+    # ------------------------------------------------------- layer by layer
+    _PER_SLICE = ("reps", "unit_start", "unit_size", "assign", "perm", "k_pool", "v_pool", "k_local", "v_local",
+                  "sel_rows", "k_buf", "v_buf", "buf_row", "slot_list", "n_fetched", "sel_units", "n_sel_units",
+                  "n_sel", "scores", "seg_state")
+    _PER_GROUP = ("q_ref", "fire", "r", "out", "lse")
+
+    def group_view(self, g: int) -> "LouisKVEngine":
+        """An engine over group g alone (one layer of one sequence) that shares
+        this engine's storage: its calls read and write the same tensors, so a
+        decode step can run group by group, as a model runs its layers."""
+        import copy
+        c = self.cfg
+        if not 0 <= g < c.n_groups:
+            raise IndexError(g)
+        h = c.n_kv_heads
+        v = copy.copy(self)
+        v.cfg = dataclasses.replace(c, n_slices=h)
+        for name in self._PER_SLICE:
+            t = getattr(self, name, None)
+            if t is not None:
+                setattr(v, name, t[g * h:(g + 1) * h])
+        for name in self._PER_GROUP:
+            setattr(v, name, getattr(self, name)[g:g + 1])
+        # fewer slices per launch can take a larger workspace (split-KV
+        # attention partials); the views run one after another and share it
+        if not hasattr(self, "_view_ws_attn"):
+            gs = c.n_q_heads // h
+            rows = max(c.budget, 1)
+            if self.zero_copy or self.delta:
+                need = L.sparse_decode_attn_rows_workspace_size(h, gs, rows, c.window)
+            else:
+                need = L.sparse_decode_attn_workspace_size(h, gs, rows, c.window)
+            self._view_ws_attn = (self.ws_attn if need <= self.ws_attn.numel() else
+                                  torch.empty(need, dtype=torch.uint8, device=self.device))
+        v.ws_attn = self._view_ws_attn
+        return v
+
+    def step_layer_by_layer(self, q_t: torch.Tensor, k_t: torch.Tensor, v_t: torch.Tensor) -> None:
+        """One decode step run group by group (one launch sequence per layer,
+        the order in which a model produces its queries); results equal step()."""
+        c = self.cfg
+        h = c.n_kv_heads
+        if not hasattr(self, "_views"):
+            self._views = [self.group_view(g) for g in range(c.n_groups)]
+        for g, v in enumerate(self._views):
+            v.t = self.t
+            v.step(q_t[g:g + 1], k_t[g * h:(g + 1) * h], v_t[g * h:(g + 1) * h])
+        self.t += 1
 
     # ---------------------------------------------------------------- decode
     def n_units_before(self, t: int) -> int:

@@ -358,9 +358,12 @@ def _check_delta_buffers(eng, gi, H):
         assert torch.equal(eng.v_buf[s, torch.as_tensor(slots)].cpu(), eng.v_pool[s].cpu()[idx])
 
 
-def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, segments="fixed", delta=None):
+def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, segments="fixed", delta=None,
+              layer_by_layer=False):
     """Prefill on the GPU, then `steps` decode steps on the GPU and in the
-    oracle (started from the GPU's prefill state), step-locked."""
+    oracle (started from the GPU's prefill state), step-locked.  With
+    layer_by_layer each step runs group by group (one launch sequence per
+    layer) through views of the engine's tensors."""
     from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
     data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(n_groups)], gen_len=steps)
     cfg = config_from_workload(wl, n_groups=n_groups, mode=mode, gen_len=steps, segments=segments)
@@ -382,8 +385,13 @@ def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, seg
         decs.append(oracle.GroupDecoder(st, wl.n_q_heads, wl.budget, wl.window, wl.seg_len, wl.tau,
                                         "prev" if mode == 0 else "anchor", segments=segments))
     stats = dict(fires=0, excused=0, evictions=0, sizes=set(), fetched=0, selected=0)
+    if layer_by_layer and pool_on_host:
+        _require_interior_host_mapping(eng.k_pool, wl.n_kv_heads)
     for t in range(steps):
-        eng.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        if layer_by_layer:
+            eng.step_layer_by_layer(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        else:
+            eng.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
         torch.cuda.synchronize()
         fire, r = to_np(eng.fire), to_np(eng.r)
         for gi, dec in enumerate(decs):
@@ -504,6 +512,86 @@ def test_decode_loop_boundary_segments_host_pool():
                                                  name="host-131k")
     st = _run_loop(wl, 1, 200, mode=1, pool_on_host=True, segments="boundary")
     assert st["fires"] > 20 and st["evictions"] > 10
+
+
+def _require_interior_host_mapping(pool, rows_per_view):
+    """Group views of a pinned host pool hand the library interior pointers;
+    check (a runtime query, no kernel) that the device address the runtime
+    reports for one is the pool's device address plus the same offset."""
+    import ctypes
+
+    class Attr(ctypes.Structure):
+        _fields_ = [("type", ctypes.c_int), ("device", ctypes.c_int), ("devicePointer", ctypes.c_void_p),
+                    ("hostPointer", ctypes.c_void_p), ("isManaged", ctypes.c_int),
+                    ("allocationFlags", ctypes.c_uint)]
+
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipPointerGetAttributes.argtypes = [ctypes.POINTER(Attr), ctypes.c_void_p]
+    a, b = Attr(), Attr()
+    off = pool[rows_per_view].data_ptr() - pool.data_ptr()
+    assert hip.hipPointerGetAttributes(ctypes.byref(a), ctypes.c_void_p(pool.data_ptr())) == 0
+    assert hip.hipPointerGetAttributes(ctypes.byref(b), ctypes.c_void_p(pool.data_ptr() + off)) == 0
+    assert a.devicePointer and b.devicePointer
+    assert b.devicePointer - a.devicePointer == off, (hex(a.devicePointer), hex(b.devicePointer), off)
+
+
+def test_decode_loop_layer_by_layer():
+    """Each decode step run group by group (as a model runs its layers) over
+    views of one engine's tensors: the same oracle parity as the batched step,
+    with evictions (bf16 long-output reduction, three groups, zero-copy)."""
+    wl = synth.get_workload("si-lo-16k").replace(prompt_len=2048, n_clusters=64, budget=512, name="si-lo-16k")
+    st = _run_loop(wl, 3, 300, mode=1, layer_by_layer=True)
+    assert st["fires"] > 60 and st["evictions"] > 0
+
+
+def test_decode_loop_layer_by_layer_boundary_delta():
+    """Group-by-group steps with boundary segments and delta transfers over a
+    device pool (per-slice segment state and buffer rows seen through views)."""
+    wl = synth.get_workload("si-lo-16k").replace(prompt_len=2048, n_clusters=64, budget=512, window=64,
+                                                 seg_len=16, name="si-lo-16k")
+    st = _run_loop(wl, 2, 200, mode=1, zero_copy=False, delta=True, segments="boundary", layer_by_layer=True)
+    assert st["fires"] > 30 and st["evictions"] > 10 and 0 < st["fetched"] < st["selected"]
+
+
+def test_decode_loop_layer_by_layer_host_pool():
+    """Group-by-group steps with the pool in pinned host memory (delta
+    transfers): each group's calls take pointers into the middle of the pool."""
+    wl = synth.get_workload("host-131k").replace(prompt_len=2048, n_clusters=64, budget=512, name="host-131k")
+    st = _run_loop(wl, 2, 160, mode=1, pool_on_host=True, layer_by_layer=True)
+    assert st["fires"] > 20 and 0 < st["fetched"] < st["selected"]
+
+
+def test_layer_by_layer_equals_batched_at_full_layer_count():
+    """32 groups (one sequence of a 32-layer model; a reduced prompt so the
+    run is short): steps run group by group give the batched steps' fires,
+    selections and unit tables exactly, and the same attention outputs up to
+    the summation order (one launch per layer splits each slice's rows over
+    several blocks, the batched launch does not)."""
+    from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
+    wl = synth.get_workload("si-lo-16k").replace(prompt_len=512, n_clusters=16, budget=128, name="si-lo-16k")
+    G, steps = 32, 170
+    data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(G)], gen_len=steps)
+    cfg = config_from_workload(wl, n_groups=G, gen_len=steps)
+    engs = [LouisKVEngine(cfg, torch.bfloat16, DEV, out_dtype=torch.float32) for _ in range(2)]
+    for e in engs:
+        e.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    fires = 0
+    for t in range(steps):
+        engs[0].step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        engs[1].step_layer_by_layer(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        torch.cuda.synchronize()
+        a, b = engs
+        assert torch.equal(a.fire, b.fire), t
+        fires += int(a.fire.sum())
+        for name in ("n_sel", "n_sel_units", "sel_units", "unit_start", "unit_size", "reps"):
+            assert torch.equal(getattr(a, name), getattr(b, name)), (t, name)
+        for i in range(a.n_sel.shape[0]):
+            n = int(a.n_sel[i])
+            assert torch.equal(a.sel_rows[i, :n], b.sel_rows[i, :n]), (t, i)
+        err = (a.out - b.out).abs().max().item()
+        assert err <= 1e-5 * max(1.0, a.out.abs().max().item()), (t, err)
+        assert (a.lse - b.lse).abs().max().item() <= 1e-5, t
+    assert fires > G * steps // 8
 
 
 def test_host_pool_flag_rejects_device_memory():
