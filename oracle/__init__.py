@@ -16,19 +16,21 @@ from .louiskv_oracle import (
     KMeansResult,
     clustering_cost,
     segment_mean,
+    page_units,
     query_similarity,
     boundary_fires,
+    stride_fires,
     group_scores,
     select_budget,
     gather_units,
     attention,
 )
-from .decode_driver import PrefillState, GroupDecoder, prefill_state_from_kmeans
+from .decode_driver import PrefillState, GroupDecoder, prefill_state_from_kmeans, prefill_state_from_pages
 
 __all__ = [
     "round_to_bf16", "round_to_f32", "squared_distances", "kmeans_assign",
     "kmeans_update", "kmeans", "KMeansResult", "clustering_cost",
-    "segment_mean", "query_similarity", "boundary_fires", "group_scores",
-    "select_budget", "gather_units", "attention",
-    "PrefillState", "GroupDecoder", "prefill_state_from_kmeans",
+    "segment_mean", "page_units", "query_similarity", "boundary_fires", "stride_fires",
+    "group_scores", "select_budget", "gather_units", "attention",
+    "PrefillState", "GroupDecoder", "prefill_state_from_kmeans", "prefill_state_from_pages",
 ]

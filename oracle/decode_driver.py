@@ -22,6 +22,11 @@ Per decode step t, in the order of Algorithm 1's decode phase:
   4. attention of each query head over [KV_critical : KV_local], the current
      token included.
 KV_critical is kept unchanged between boundaries.
+
+Ablation baselines (Appendix D.3, Appendix B): a fixed-stride trigger in place
+of the boundary test, a page-level index in place of the prompt clusters
+(prefill_state_from_pages), and per-head selection in place of the
+group-consistent one.
 """
 from __future__ import annotations
 
@@ -32,8 +37,8 @@ from typing import List, Optional, Sequence
 import numpy as np
 
 from .louiskv_oracle import (
-    F64, attention, boundary_fires, gather_units, group_scores,
-    query_similarity, segment_mean, select_budget, KMeansResult,
+    F64, attention, boundary_fires, gather_units, group_scores, page_units,
+    query_similarity, segment_mean, select_budget, stride_fires, KMeansResult,
 )
 
 
@@ -62,6 +67,29 @@ def prefill_state_from_kmeans(prompt_keys: Sequence, prompt_values: Sequence,
     return PrefillState(reps, starts, sizes, kp, vp)
 
 
+def prefill_state_from_pages(prompt_keys: Sequence, prompt_values: Sequence, page_len: int) -> PrefillState:
+    """The page-level baseline's prefill (Appendix D.3): no clustering; the
+    pool holds the prompt in token order and each page of page_len tokens is
+    a unit indexed by its mean key."""
+    reps, starts, sizes, kp, vp = [], [], [], [], []
+    for k, v in zip(prompt_keys, prompt_values):
+        k = np.asarray(k, dtype=F64)
+        r, a, z = page_units(k, page_len)
+        reps.append(r)
+        starts.append(a)
+        sizes.append(z)
+        kp.append(k)
+        vp.append(np.asarray(v, dtype=F64))
+    return PrefillState(reps, starts, sizes, kp, vp)
+
+
+def head_scores(q_t, head: int, reps, scale: float) -> np.ndarray:
+    """Per-head selection (the baseline that group-consistent selection
+    replaces, Appendix B): query head `head` ranks the units of its KV head by
+    its own softmax alone, i.e. the group score with a group of one."""
+    return group_scores(np.asarray(q_t, dtype=F64)[head:head + 1], reps, scale)
+
+
 def opens_segment(fire: bool, gen: int, open_first: Optional[int], seg_max: int) -> bool:
     """Boundary-delimited segments: token `gen` starts a new segment when there
     is no open one, when this step is a semantic boundary (Section 4.1, the
@@ -75,9 +103,10 @@ class StepRecord:
     t: int
     r: float                      # NaN at t = 1
     fire: bool
-    scores: Optional[List[np.ndarray]]     # per KV head, when fired
-    sel_units: Optional[List[List[int]]]   # per KV head, when fired
-    n_sel: List[int]              # per KV head, current KV_critical size
+    scores: Optional[List[np.ndarray]]     # per selection list, when fired
+    sel_units: Optional[List[List[int]]]   # per selection list, when fired
+    n_sel: List[int]              # per selection list, current KV_critical size
+    # (a selection list is a KV head; with selection="per_head" a query head)
     evicted_unit: Optional[int]   # unit id created at this step, if any
     out: np.ndarray               # [H_q][d]
     lse: np.ndarray               # [H_q]
@@ -86,11 +115,22 @@ class StepRecord:
 class GroupDecoder:
     def __init__(self, prefill: PrefillState, n_q_heads: int, budget: int,
                  window: int, seg_len: int, tau: float, mode: str = "anchor",
-                 scale: Optional[float] = None, segments: str = "fixed"):
+                 scale: Optional[float] = None, segments: str = "fixed",
+                 trigger: str = "boundary", stride: int = 16, selection: str = "group"):
+        """trigger="stride" replaces the boundary test's decision by a
+        retrieval every `stride` steps (r is still computed and the reference
+        query still follows `mode`); selection="per_head" gives every query
+        head its own selection and KV_critical (the ablation baselines of
+        Appendix D.3 and Appendix B)."""
         if mode not in ("prev", "anchor"):
             raise ValueError(mode)
         if segments not in ("fixed", "boundary"):
             raise ValueError(segments)
+        if trigger not in ("boundary", "stride") or stride < 1:
+            raise ValueError((trigger, stride))
+        if selection not in ("group", "per_head"):
+            raise ValueError(selection)
+        self.trigger, self.stride, self.selection = trigger, stride, selection
         if segments == "boundary" and not 1 <= seg_len < window:
             raise ValueError("boundary segments need 1 <= seg_len < window")
         self.segments = segments
@@ -108,9 +148,11 @@ class GroupDecoder:
         self.k_pool = [list(np.asarray(k, dtype=F64)) for k in prefill.k_pool]
         self.v_pool = [list(np.asarray(v, dtype=F64)) for v in prefill.v_pool]
         self.local = [deque() for _ in range(self.h_kv)]   # (gen index, k, v)
-        self.crit_k = [np.zeros((0, self.d)) for _ in range(self.h_kv)]
-        self.crit_v = [np.zeros((0, self.d)) for _ in range(self.h_kv)]
-        self.crit_units: List[List[int]] = [[] for _ in range(self.h_kv)]
+        # one KV_critical per selection list: per KV head, or per query head
+        n_lists = self.h_kv * (self.g if selection == "per_head" else 1)
+        self.crit_k = [np.zeros((0, self.d)) for _ in range(n_lists)]
+        self.crit_v = [np.zeros((0, self.d)) for _ in range(n_lists)]
+        self.crit_units: List[List[int]] = [[] for _ in range(n_lists)]
         self.q_ref = None
         self.t = 0
         self.n_evicted = 0
@@ -131,7 +173,10 @@ class GroupDecoder:
         self.t += 1
         first = self.t == 1
         r = float("nan") if first else query_similarity(q_t, self.q_ref)
-        fire = boundary_fires(r, self.tau, first)
+        if self.trigger == "stride":
+            fire = stride_fires(self.t, self.stride)
+        else:
+            fire = boundary_fires(r, self.tau, first)
         if fire_override is not None:
             fire = bool(fire_override)
         if self.mode == "prev" or fire:
@@ -140,17 +185,23 @@ class GroupDecoder:
         scores = sels = None
         if fire:
             scores, sels = [], []
-            for h in range(self.h_kv):
-                a = group_scores(q_t[h * self.g:(h + 1) * self.g], np.asarray(self.reps[h]), self.scale)
+            per_head = self.selection == "per_head"
+            for li in range(len(self.crit_k)):
+                h = li // self.g if per_head else li
+                reps = np.asarray(self.reps[h])
+                if per_head:
+                    a = head_scores(q_t, li, reps, self.scale)
+                else:
+                    a = group_scores(q_t[h * self.g:(h + 1) * self.g], reps, self.scale)
                 if select_override is not None:
-                    chosen = [int(u) for u in select_override[h]]
+                    chosen = [int(u) for u in select_override[li]]
                 else:
                     chosen, _ = select_budget(a, self.unit_size[h], self.budget)
                 kp = np.asarray(self.k_pool[h])
                 vp = np.asarray(self.v_pool[h])
-                self.crit_k[h] = gather_units(kp, self.unit_start[h], self.unit_size[h], chosen)
-                self.crit_v[h] = gather_units(vp, self.unit_start[h], self.unit_size[h], chosen)
-                self.crit_units[h] = chosen
+                self.crit_k[li] = gather_units(kp, self.unit_start[h], self.unit_size[h], chosen)
+                self.crit_v[li] = gather_units(vp, self.unit_start[h], self.unit_size[h], chosen)
+                self.crit_units[li] = chosen
                 scores.append(a)
                 sels.append(chosen)
 
@@ -183,14 +234,17 @@ class GroupDecoder:
 
         out = np.zeros((self.h_kv * self.g, self.d))
         lse = np.zeros(self.h_kv * self.g)
-        for h in range(self.h_kv):
+        per_head = self.selection == "per_head"
+        for li in range(len(self.crit_k)):
+            h = li // self.g if per_head else li
+            heads = slice(li, li + 1) if per_head else slice(h * self.g, (h + 1) * self.g)
             lk = np.stack([x[1] for x in self.local[h]])
             lv = np.stack([x[2] for x in self.local[h]])
-            kk = np.concatenate([self.crit_k[h], lk])
-            vv = np.concatenate([self.crit_v[h], lv])
-            o, l = attention(q_t[h * self.g:(h + 1) * self.g], kk, vv, self.scale)
-            out[h * self.g:(h + 1) * self.g] = o
-            lse[h * self.g:(h + 1) * self.g] = l
+            kk = np.concatenate([self.crit_k[li], lk])
+            vv = np.concatenate([self.crit_v[li], lv])
+            o, l = attention(q_t[heads], kk, vv, self.scale)
+            out[heads] = o
+            lse[heads] = l
         return StepRecord(t=self.t, r=r, fire=fire, scores=scores, sel_units=sels,
                           n_sel=[int(x.shape[0]) for x in self.crit_k],
                           evicted_unit=evicted, out=out, lse=lse)

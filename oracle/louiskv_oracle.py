@@ -158,6 +158,22 @@ def segment_mean(rows) -> np.ndarray:
     return round_to_f32(r.sum(axis=0) / r.shape[0])
 
 
+def page_units(keys, page_len: int):
+    """Page-level index, the coarse-grained baseline of the management ablation
+    (Appendix D.3): the tokens are cut into consecutive pages of page_len (the
+    last one shorter when page_len does not divide the count), and each page
+    is a unit whose index vector is its mean key, computed as a segment mean.
+    Returns (reps [n_pages][d], starts [n_pages], sizes [n_pages])."""
+    k = np.asarray(keys, dtype=F64)
+    n = k.shape[0]
+    if page_len < 1:
+        raise ValueError("page_len must be >= 1")
+    starts = np.arange(0, n, page_len, dtype=np.int64)
+    sizes = np.minimum(page_len, n - starts)
+    reps = np.stack([segment_mean(k[a:a + z]) for a, z in zip(starts, sizes)])
+    return reps, starts, sizes
+
+
 # ---------------------------------------------------------------------------
 # semantic boundary test (Section 4.1 equation for r_t; Algorithm 1 decode loop)
 # ---------------------------------------------------------------------------
@@ -178,6 +194,12 @@ def query_similarity(q, q_ref) -> float:
 def boundary_fires(r: float, tau: float, first_step: bool) -> bool:
     """A new segment starts at the first step or when r drops strictly below tau."""
     return bool(first_step or r < tau)
+
+
+def stride_fires(t: int, stride: int) -> bool:
+    """The fixed-stride trigger of the retrieval ablation (Appendix D.3): a
+    retrieval at the first decode step (t = 1) and then every `stride` steps."""
+    return (t - 1) % stride == 0
 
 
 # ---------------------------------------------------------------------------

@@ -455,6 +455,114 @@ def pin_decode_boundary_segments(orc):
         assert starts[-1] + sizes[-1] - p + len(dec.local[h]) == q.shape[0]
 
 
+def pin_page_units(orc):
+    """Pages are consecutive runs of page_len tokens (the last one ragged),
+    each indexed by its mean key (numpy's mean, rounded to float32); one page
+    of every token is the global mean, pages of one token are the keys; the
+    page-level prefill keeps the prompt in token order, so always firing with
+    an unbounded budget is dense attention."""
+    rng = RNG(41)
+    k = rng.standard_normal((50, 8)) * 3
+    reps, starts, sizes = orc.page_units(k, 16)
+    assert starts.tolist() == [0, 16, 32, 48] and sizes.tolist() == [16, 16, 16, 2]
+    for i, (a, z) in enumerate(zip(starts, sizes)):
+        np.testing.assert_allclose(reps[i], np.mean(k[a:a + z], axis=0), rtol=1e-7, atol=0)
+        assert np.array_equal(reps[i], reps[i].astype(np.float32))
+    one, _, sz = orc.page_units(k, 50)
+    assert sz.tolist() == [50]
+    np.testing.assert_allclose(one[0], k.mean(0), rtol=1e-7, atol=0)
+    single, st1, sz1 = orc.page_units(k, 1)
+    assert np.array_equal(single, k.astype(np.float32)) and st1.tolist() == list(range(50))
+    big, _, szb = orc.page_units(k, 64)
+    assert szb.tolist() == [50]
+    # decode over pages: dense when every step fires with an unbounded budget
+    pk, pv, gk, gv, q = _tiny_group(43)
+    h_kv, p, d = pk.shape
+    g = q.shape[1] // h_kv
+    st = orc.prefill_state_from_pages(pk, pv, 16)
+    assert all(np.array_equal(st.k_pool[h], pk[h]) for h in range(h_kv))
+    dec = orc.GroupDecoder(st, q.shape[1], budget=10 ** 9, window=64, seg_len=16, tau=1.5, mode="prev")
+    s = 1 / np.sqrt(d)
+    for t in range(40):
+        rec = dec.step(q[t], gk[t], gv[t])
+        for h in range(h_kv):
+            kk = torch.from_numpy(np.concatenate([pk[h], gk[:t + 1, h]]))
+            vv = torch.from_numpy(np.concatenate([pv[h], gv[:t + 1, h]]))
+            qq = torch.from_numpy(q[t, h * g:(h + 1) * g])
+            ref = torch.nn.functional.scaled_dot_product_attention(
+                qq[None, :, None, :], kk[None, None].expand(1, g, -1, -1),
+                vv[None, None].expand(1, g, -1, -1), scale=s)[0, :, 0].numpy()
+            assert np.allclose(rec.out[h * g:(h + 1) * g], ref, rtol=1e-10, atol=1e-12)
+
+
+def pin_decode_stride_trigger(orc):
+    """The fixed-stride trigger fires at steps 1, 1 + s, 1 + 2s, ... whatever
+    the queries do; stride 1 behaves as a boundary test that always fires and
+    a stride past the last step as one that never fires after the first."""
+    pk, pv, gk, gv, q = _tiny_group(44, t=60)
+    st = _prefill(orc, pk, pv, 8)
+    dec = orc.GroupDecoder(st, q.shape[1], 40, 32, 8, 0.9, "anchor", trigger="stride", stride=5)
+    fired = [dec.step(q[t], gk[t], gv[t]).fire for t in range(q.shape[0])]
+    assert [t for t, f in enumerate(fired) if f] == list(range(0, q.shape[0], 5))
+    for stride, tau in ((1, 1.5), (1000, -2.0)):
+        a = orc.GroupDecoder(_prefill(orc, pk, pv, 8), q.shape[1], 40, 32, 8, 0.9, "anchor", trigger="stride",
+                             stride=stride)
+        b = orc.GroupDecoder(_prefill(orc, pk, pv, 8), q.shape[1], 40, 32, 8, tau, "anchor")
+        for t in range(q.shape[0]):
+            ra, rb = a.step(q[t], gk[t], gv[t]), b.step(q[t], gk[t], gv[t])
+            assert ra.fire == rb.fire and ra.sel_units == rb.sel_units
+            assert np.array_equal(ra.out, rb.out)
+
+
+def pin_decode_per_head(orc):
+    """Per-head selection: each query head's units are the budget prefix of
+    the ranking by its own softmax (scipy's, over its logits); with one query
+    head per KV head it is the group-consistent selection; with the heads of
+    a group given equal queries every head takes the group's selection; with
+    an unbounded budget every head attends to everything, as the group does."""
+    from scipy.special import softmax
+    pk, pv, gk, gv, q = _tiny_group(45, t=50)
+    h_kv, p, d = pk.shape
+    g = q.shape[1] // h_kv
+    s = 1 / np.sqrt(d)
+    # rankings of the units that exist before each step (its eviction comes
+    # after its retrieval)
+    dec = orc.GroupDecoder(_prefill(orc, pk, pv, 8), q.shape[1], 30, 32, 8, 1.5, "prev", selection="per_head")
+    for t in range(q.shape[0]):
+        reps_now = [np.asarray(r).copy() for r in dec.reps]
+        sizes_now = [list(z) for z in dec.unit_size]
+        rec = dec.step(q[t], gk[t], gv[t])
+        assert len(rec.sel_units) == h_kv * g
+        for li in range(h_kv * g):
+            h = li // g
+            a = softmax(q[t, li] @ reps_now[h].T * s)
+            assert rec.sel_units[li] == _select_by_sort(a, sizes_now[h], 30)[0]
+    heads_differ = any(len(set(map(tuple, rec.sel_units[h * g:(h + 1) * g]))) > 1 for h in range(h_kv))
+    assert heads_differ
+    # one query head per KV head
+    q1 = q[:, ::g]
+    a = orc.GroupDecoder(_prefill(orc, pk, pv, 8), h_kv, 30, 32, 8, 0.9, "anchor", selection="per_head")
+    b = orc.GroupDecoder(_prefill(orc, pk, pv, 8), h_kv, 30, 32, 8, 0.9, "anchor")
+    for t in range(q.shape[0]):
+        ra, rb = a.step(q1[t], gk[t], gv[t]), b.step(q1[t], gk[t], gv[t])
+        assert ra.fire == rb.fire and ra.sel_units == rb.sel_units and np.array_equal(ra.out, rb.out)
+    # equal queries within each group
+    qe = np.repeat(q[:, ::g], g, axis=1)
+    a = orc.GroupDecoder(_prefill(orc, pk, pv, 8), q.shape[1], 30, 32, 8, 0.9, "anchor", selection="per_head")
+    b = orc.GroupDecoder(_prefill(orc, pk, pv, 8), q.shape[1], 30, 32, 8, 0.9, "anchor")
+    for t in range(q.shape[0]):
+        ra, rb = a.step(qe[t], gk[t], gv[t]), b.step(qe[t], gk[t], gv[t])
+        if rb.fire:
+            assert ra.sel_units == [u for u in rb.sel_units for _ in range(g)]
+        assert np.allclose(ra.out, rb.out, rtol=1e-12, atol=1e-14)
+    # unbounded budget
+    a = orc.GroupDecoder(_prefill(orc, pk, pv, 8), q.shape[1], 10 ** 9, 32, 8, 1.5, "prev", selection="per_head")
+    b = orc.GroupDecoder(_prefill(orc, pk, pv, 8), q.shape[1], 10 ** 9, 32, 8, 1.5, "prev")
+    for t in range(q.shape[0]):
+        ra, rb = a.step(q[t], gk[t], gv[t]), b.step(q[t], gk[t], gv[t])
+        assert np.allclose(ra.out, rb.out, rtol=1e-10, atol=1e-12)
+
+
 DECODE_PINS = [pin_decode_dense_special_case, pin_decode_frozen_and_schedule, pin_decode_boundary_modes,
-               pin_decode_boundary_segments]
+               pin_decode_boundary_segments, pin_page_units, pin_decode_stride_trigger, pin_decode_per_head]
 ALL_PINS = ALL_PINS + DECODE_PINS

@@ -117,6 +117,28 @@ def _opens_ignores_fire(fire, gen, open_first, seg_max):
     return open_first is None or gen - open_first >= seg_max
 
 
+def _stride_late(t, stride):
+    return t % stride == 0
+
+
+def _pages_drop_tail(keys, page_len):
+    k = np.asarray(keys, F64)
+    n = k.shape[0] // page_len * page_len
+    starts = np.arange(0, n, page_len, dtype=np.int64)
+    sizes = np.full(len(starts), page_len, dtype=np.int64)
+    reps = np.stack([L.segment_mean(k[a:a + page_len]) for a in starts])
+    return reps, starts, sizes
+
+
+def _head_scores_first_head(q_t, head, reps, scale):
+    return L.group_scores(np.asarray(q_t, F64)[0:1], reps, scale)
+
+
+def _head_scores_group(q_t, head, reps, scale):
+    base = head - head % 2
+    return L.group_scores(np.asarray(q_t, F64)[base:base + 2], reps, scale)
+
+
 MUTATIONS = {
     "distance_cross_term_sign": ("squared_distances", _sqdist_plus),
     "distance_dropped_centroid_norm": ("squared_distances", _sqdist_no_cnorm),
@@ -136,6 +158,10 @@ MUTATIONS = {
     "segment_without_length_cap": ("opens_segment", _opens_no_cap),
     "segment_cap_one_late": ("opens_segment", _opens_cap_late),
     "segment_ignores_boundary": ("opens_segment", _opens_ignores_fire),
+    "stride_first_fire_late": ("stride_fires", _stride_late),
+    "pages_drop_ragged_tail": ("page_units", _pages_drop_tail),
+    "per_head_uses_first_head": ("head_scores", _head_scores_first_head),
+    "per_head_uses_group_average": ("head_scores", _head_scores_group),
 }
 
 
