@@ -585,6 +585,84 @@ int louiskv_retrieve_delta(const void* q, int32_t dtype, int64_t n_slices,
                            int32_t* n_fetched, double* scores_out,
                            void* workspace, size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------------ */
+/* Ablation baselines                                                        */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Fixed-stride trigger (the retrieval ablation's baseline, Appendix D.3): in
+ * place of louiskv_boundary_check, fire_out[g] = 1 for every group on the
+ * steps where step % stride == 0 (step is the 0-based decode step, so the
+ * first step fires), 0 otherwise.  fire_out [n_groups] uint8.
+ * Errors: NULL fire_out, n_groups < 1, step < 0 or stride < 1.
+ */
+int louiskv_fire_every(uint8_t* fire_out, int64_t n_groups, int32_t step,
+                       int32_t stride, void* stream);
+
+/*
+ * Page-level index for the prompt (the management ablation's coarse-grained
+ * baseline, Appendix D.3), in place of louiskv_cluster_prefill: the prompt
+ * of each slice is cut into pages of page_len tokens (the last page holds
+ * the remainder), page p is unit p with index vector the mean of its keys
+ * (float64 sum in row order, one rounding to float32), and the pool holds
+ * the prompt rows in token order.
+ *
+ * keys, values [n_slices][n_tokens][d] dtype (values may be NULL when v_pool is).
+ * reps        out [n_slices][units_cap][d] float32, rows 0..n_pages-1.
+ * unit_start, unit_size  out [n_slices][units_cap] int32: p * page_len and
+ *             min(page_len, n_tokens - p * page_len).
+ * k_pool, v_pool  out [n_slices][pool_rows][d] dtype or NULL (rows
+ *             0..n_tokens-1 written); pool_on_host as for louiskv_cluster_prefill.
+ * Requires n_pages = ceil(n_tokens / page_len) <= units_cap and
+ * pool_rows >= n_tokens when a pool is given.
+ */
+int louiskv_page_prefill(const void* keys, const void* values, int32_t dtype,
+                         int64_t n_slices, int32_t n_tokens, int32_t d, int32_t page_len,
+                         float* reps, int32_t units_cap, int32_t* unit_start,
+                         int32_t* unit_size, void* k_pool, void* v_pool,
+                         int64_t pool_rows, int32_t pool_on_host, void* stream);
+
+/*
+ * Per-head selection (the baseline that the group-consistent selection of
+ * Appendix B replaces): every query head ranks its KV head's units by its own
+ * softmax (the group score with a group of one) and takes its own budget
+ * prefix, so the g heads of a KV head attend to different rows.  Arguments
+ * as louiskv_retrieve_rows, but every per-list output has one list per query
+ * head, list index s * group_size + j for query head j of slice s:
+ * sel_units [n_slices * group_size][units_cap], n_sel_units and n_sel
+ * [n_slices * group_size], sel_rows [n_slices * group_size][budget],
+ * scores_out [n_slices * group_size][units_cap] or NULL.  Workspace:
+ * louiskv_retrieve_rows_workspace_size(n_slices * group_size, units_cap).
+ */
+int louiskv_retrieve_rows_per_head(const void* q, int32_t dtype, int64_t n_slices,
+                                   int32_t n_kv_heads, int32_t group_size, int32_t d,
+                                   double scale, const float* reps,
+                                   const int32_t* unit_start, const int32_t* unit_size,
+                                   int32_t units_cap, int32_t n_units, int32_t budget,
+                                   const uint8_t* fire, int32_t* sel_units,
+                                   int32_t* n_sel_units, int32_t* n_sel, int32_t* sel_rows,
+                                   double* scores_out, void* workspace,
+                                   size_t workspace_bytes, void* stream);
+
+/*
+ * Attention for per-head selections: query head j of slice s attends to the
+ * pool rows of list s * group_size + j (sel_rows, n_sel as written by
+ * louiskv_retrieve_rows_per_head) followed by the live rows of slice s's
+ * local window.  Other arguments, layouts and outputs as
+ * louiskv_sparse_decode_attn_rows.  Workspace:
+ * louiskv_sparse_decode_attn_rows_workspace_size(n_slices * group_size, 1,
+ * d, budget, window).
+ */
+int louiskv_sparse_decode_attn_rows_per_head(const void* q, int32_t dtype, int64_t n_slices,
+                                             int32_t n_kv_heads, int32_t group_size, int32_t d,
+                                             float scale, const void* k_pool, const void* v_pool,
+                                             int64_t pool_rows, const int32_t* sel_rows,
+                                             const int32_t* n_sel, int32_t budget,
+                                             const void* k_local, const void* v_local,
+                                             int32_t window, int32_t local_start, int32_t n_local,
+                                             void* out, int32_t out_dtype, float* lse_out,
+                                             void* workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -320,7 +320,7 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
                          int32_t* __restrict__ sel_units, int32_t* __restrict__ n_sel_units,
                          int32_t* __restrict__ n_sel, double* __restrict__ scores_out,
                          double* __restrict__ logit_ws, int32_t* __restrict__ row_ws, int n_pad_arg,
-                         const int32_t* __restrict__ seg_state, int seg_stride) {
+                         const int32_t* __restrict__ seg_state, int seg_stride, int slice_div) {
   extern __shared__ __align__(16) char smem[];
   uint64_t* s_key = reinterpret_cast<uint64_t*>(smem);            // [n_pad_arg]
   int* s_size = reinterpret_cast<int*>(s_key + n_pad_arg);        // [n_pad_arg] unit sizes by unit id
@@ -333,11 +333,14 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
   const int64_t s = blockIdx.x;
   const int64_t grp = s / n_kv_heads;
   if (fire && !fire[grp]) return;
+  // slice_div > 1: per-head selection, s is a query head and ps the slice of
+  // its KV head, whose units it ranks alone
+  const int64_t ps = s / slice_div;
   // with boundary-delimited segments each slice has its own unit count (the
   // argument is then an upper bound that sized the LDS)
   int n_units = n_units_arg, n_pad = n_pad_arg;
   if (seg_state) {
-    n_units = min(max(seg_state[s * seg_stride + kSegNUnits], 1), n_units_arg);
+    n_units = min(max(seg_state[ps * seg_stride + kSegNUnits], 1), n_units_arg);
     n_pad = 64;
     while (n_pad < n_units) n_pad <<= 1;
   }
@@ -346,7 +349,7 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int sub = lane & 15, quad = lane >> 4;
   const int n_q_heads = n_kv_heads * G;
-  const int32_t* us = unit_size + (size_t)s * units_cap;
+  const int32_t* us = unit_size + (size_t)ps * units_cap;
   for (int u = tid; u < n_units; u += kSelThreads) s_size[u] = max(us[u], 0);
 
   double qd[G][8];
@@ -361,7 +364,7 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
 #pragma unroll
   for (int j = 0; j < G; ++j) mx[j] = -__builtin_inf();
   double* lg = logit_ws + (size_t)s * units_cap * G;
-  const float* rs = reps + (size_t)s * units_cap * kHeadDim;
+  const float* rs = reps + (size_t)ps * units_cap * kHeadDim;
   for (int u0 = w * 4 * kSelBatch; u0 < n_units; u0 += kSelWaves * 4 * kSelBatch) {
     float4 x[kSelBatch][2];
 #pragma unroll
@@ -500,7 +503,7 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
   }
   const int ntake = s_ntake;
   const int nsel = ntake > 0 ? s_incl[ntake - 1] : 0;
-  const int32_t* ustart = unit_start + (size_t)s * units_cap;
+  const int32_t* ustart = unit_start + (size_t)ps * units_cap;
   int32_t* rows = row_ws + (size_t)s * budget;
   // one wave per selected unit: its rank in the list, then its rows in order
   for (int p = w; p < ntake; p += kSelWaves) {
@@ -858,7 +861,7 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
                          const T* __restrict__ k_local, const T* __restrict__ v_local, int window, int local_start_arg,
                          int n_local_arg, int n_chunks, float* __restrict__ part, void* __restrict__ out, int out_bf16,
                          float* __restrict__ lse_out, const int32_t* __restrict__ seg_state, int seg_stride,
-                         int n_tokens) {
+                         int n_tokens, int slice_div) {
   extern __shared__ int s_rows[];     // kIdx: the chunk's entries of the row list
   constexpr int R = attn_rows_in_flight<T, G>();
   constexpr int kAttnWaves = attn_waves<T, G>();
@@ -872,7 +875,9 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
   const int kvh = (int)(s - grp * n_kv_heads);
   const int tid = threadIdx.x, sub = tid & 15, rg = tid >> 4;   // 64 row groups of 16 lanes
   int local_start = local_start_arg, n_local = n_local_arg;
-  slice_window(seg_state, seg_stride, s, window, n_tokens, local_start, n_local);
+  // slice_div > 1: per-head lists, s is a query head and ps its KV head's slice
+  const int64_t ps = s / slice_div;
+  slice_window(seg_state, seg_stride, ps, window, n_tokens, local_start, n_local);
   const int nsel = max(0, min(n_sel[s], buf_rows));
   const int total = nsel + n_local;
   const int r0 = (int)((int64_t)total * chunk / n_chunks);
@@ -892,10 +897,10 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[j][e] = 0.f;
   }
-  const T* kb = k_buf + (size_t)s * src_rows * kHeadDim + 8 * sub;
-  const T* vb = v_buf + (size_t)s * src_rows * kHeadDim + 8 * sub;
-  const T* kl = k_local + (size_t)s * window * kHeadDim + 8 * sub;
-  const T* vl = v_local + (size_t)s * window * kHeadDim + 8 * sub;
+  const T* kb = k_buf + (size_t)ps * src_rows * kHeadDim + 8 * sub;
+  const T* vb = v_buf + (size_t)ps * src_rows * kHeadDim + 8 * sub;
+  const T* kl = k_local + (size_t)ps * window * kHeadDim + 8 * sub;
+  const T* vl = v_local + (size_t)ps * window * kHeadDim + 8 * sub;
   if (kIdx) stage_row_list(rows + (size_t)s * buf_rows, r0, min(r1, nsel), src_rows, s_rows, tid, kAttnThreads);
   // Issue the loads of pass ps; rows past the chunk re-read its first row and
   // are masked.
@@ -1036,7 +1041,7 @@ void attn_mfma_kernel(const uint16_t* __restrict__ q, int n_kv_heads, float scal
                       const uint16_t* __restrict__ k_local, const uint16_t* __restrict__ v_local, int window,
                       int local_start_arg, int n_local_arg, int n_chunks, float* __restrict__ part,
                       void* __restrict__ out, int out_bf16, float* __restrict__ lse_out,
-                      const int32_t* __restrict__ seg_state, int seg_stride, int n_tokens) {
+                      const int32_t* __restrict__ seg_state, int seg_stride, int n_tokens, int slice_div) {
   extern __shared__ int s_rows[];     // kIdx: the chunk's entries of the row list
   constexpr int NW = attn_mfma_waves<G>();
   constexpr int NM = G == 8 ? 2 : 1;        // matrix ops per k-chunk, 4 heads each
@@ -1051,7 +1056,9 @@ void attn_mfma_kernel(const uint16_t* __restrict__ q, int n_kv_heads, float scal
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, p16 = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);    // wave-uniform, kept in a scalar register
   int local_start = local_start_arg, n_local = n_local_arg;
-  slice_window(seg_state, seg_stride, s, window, n_tokens, local_start, n_local);
+  // slice_div > 1: per-head lists, s is a query head and ps its KV head's slice
+  const int64_t ps = s / slice_div;
+  slice_window(seg_state, seg_stride, ps, window, n_tokens, local_start, n_local);
   const int nsel = max(0, min(n_sel[s], buf_rows));
   const int total = nsel + n_local;
   const int r0 = (int)((int64_t)total * chunk / n_chunks);
@@ -1076,10 +1083,10 @@ void attn_mfma_kernel(const uint16_t* __restrict__ q, int n_kv_heads, float scal
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[j][e] = 0.f;
   }
-  const uint16_t* kb = k_buf + (size_t)s * src_rows * kHeadDim;
-  const uint16_t* vb = v_buf + (size_t)s * src_rows * kHeadDim;
-  const uint16_t* kl = k_local + (size_t)s * window * kHeadDim;
-  const uint16_t* vl = v_local + (size_t)s * window * kHeadDim;
+  const uint16_t* kb = k_buf + (size_t)ps * src_rows * kHeadDim;
+  const uint16_t* vb = v_buf + (size_t)ps * src_rows * kHeadDim;
+  const uint16_t* kl = k_local + (size_t)ps * window * kHeadDim;
+  const uint16_t* vl = v_local + (size_t)ps * window * kHeadDim;
   if (kIdx) stage_row_list(rows + (size_t)s * buf_rows, r0, min(r1, nsel), src_rows, s_rows, tid, NW * 64);
   // element offset of row r (valid) in its region, and which region
   auto row_off = [&](int r, bool& local) -> size_t {
@@ -1285,6 +1292,27 @@ extern "C" int louiskv_boundary_check(const void* q, void* q_ref, int32_t dtype,
   return LOUISKV_OK;
 }
 
+namespace louiskv {
+namespace {
+// Fixed-stride trigger: every group fires on the steps that are multiples of
+// the stride.
+__global__ void fire_every_kernel(uint8_t* __restrict__ fire, int64_t n_groups, uint8_t value) {
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g < n_groups) fire[g] = value;
+}
+}  // namespace
+}  // namespace louiskv
+
+extern "C" int louiskv_fire_every(uint8_t* fire_out, int64_t n_groups, int32_t step, int32_t stride, void* stream) {
+  if (!fire_out) return fail(LOUISKV_ERR_NULL, "fire_out is required");
+  if (n_groups < 1 || n_groups > INT32_MAX || step < 0 || stride < 1)
+    return fail(LOUISKV_ERR_SHAPE, "n_groups=%lld step=%d stride=%d", (long long)n_groups, step, stride);
+  fire_every_kernel<<<(unsigned)((n_groups + 255) / 256), 256, 0, as_stream(stream)>>>(
+      fire_out, n_groups, (uint8_t)(step % stride == 0 ? 1 : 0));
+  LKV_CHECK_LAUNCH();
+  return LOUISKV_OK;
+}
+
 extern "C" int louiskv_segment_output(const void* k_new, const void* v_new, int32_t dtype, int64_t n_slices, int32_t d,
                                       void* k_local, void* v_local, int32_t window, int32_t step, int32_t seg_len,
                                       float* reps, int32_t* unit_start, int32_t* unit_size, int32_t units_cap,
@@ -1396,7 +1424,7 @@ int score_and_select(const void* q, int32_t dtype, int64_t n_slices, int32_t n_k
                      double scale, const float* reps, const int32_t* unit_start, const int32_t* unit_size,
                      int32_t units_cap, int32_t n_units, int32_t budget, const uint8_t* fire, int32_t* sel_units,
                      int32_t* n_sel_units, int32_t* n_sel, int32_t* rows, double* scores_out, double* logit_ws,
-                     const int32_t* seg_state, int32_t seg_stride, hipStream_t s) {
+                     const int32_t* seg_state, int32_t seg_stride, hipStream_t s, int32_t slice_div = 1) {
   if (n_units < 1 || n_units > units_cap || n_units > kMaxUnits)
     return fail(LOUISKV_ERR_SHAPE, "n_units=%d must be in [1, min(units_cap=%d, %d)]", n_units, units_cap, kMaxUnits);
   int n_pad = 64;                     // whole 64-key chunks for the in-wave sort steps
@@ -1406,7 +1434,7 @@ int score_and_select(const void* q, int32_t dtype, int64_t n_slices, int32_t n_k
 #define LKV_SEL(T, G)                                                                                                  \
   score_select_kernel<T, G><<<(unsigned)n_slices, kSelThreads, lds, s>>>(                                              \
       static_cast<const T*>(q), n_kv_heads, scale, reps, unit_start, unit_size, units_cap, n_units, budget, fire,    \
-      sel_units, n_sel_units, n_sel, scores_out, logit_ws, rows, n_pad, seg_state, seg_stride)
+      sel_units, n_sel_units, n_sel, scores_out, logit_ws, rows, n_pad, seg_state, seg_stride, slice_div)
 #define LKV_SEL_G(T)                  \
   switch (group_size) {               \
     case 1: LKV_SEL(T, 1); break;     \
@@ -1619,6 +1647,7 @@ struct AttnArgs {
   int seg_stride, n_tokens;
   unsigned grid;
   size_t lds;              // dynamic LDS for the staged row list
+  int slice_div = 1;       // lists per KV-head slice (per-head selection: the group size)
 };
 
 template <class T, int G, bool kIdx>
@@ -1627,7 +1656,7 @@ void launch_attn_partial(const AttnArgs& a, hipStream_t s) {
       static_cast<const T*>(a.q), a.n_kv_heads, a.scale, static_cast<const T*>(a.k_src), static_cast<const T*>(a.v_src),
       a.n_sel, a.buf_rows, a.rows, a.src_rows, static_cast<const T*>(a.k_local), static_cast<const T*>(a.v_local),
       a.window, a.local_start, a.n_local, a.n_chunks, a.part, a.out, a.out_bf16, a.lse_out, a.seg_state,
-      a.seg_stride, a.n_tokens);
+      a.seg_stride, a.n_tokens, a.slice_div);
 }
 
 template <int G, bool kIdx>
@@ -1636,7 +1665,8 @@ void launch_attn_mfma(const AttnArgs& a, hipStream_t s) {
       static_cast<const uint16_t*>(a.q), a.n_kv_heads, a.scale, static_cast<const uint16_t*>(a.k_src),
       static_cast<const uint16_t*>(a.v_src), a.n_sel, a.buf_rows, a.rows, a.src_rows,
       static_cast<const uint16_t*>(a.k_local), static_cast<const uint16_t*>(a.v_local), a.window, a.local_start,
-      a.n_local, a.n_chunks, a.part, a.out, a.out_bf16, a.lse_out, a.seg_state, a.seg_stride, a.n_tokens);
+      a.n_local, a.n_chunks, a.part, a.out, a.out_bf16, a.lse_out, a.seg_state, a.seg_stride, a.n_tokens,
+      a.slice_div);
 }
 
 template <bool kIdx>
@@ -1665,7 +1695,7 @@ int sparse_decode_attn(const void* q, int32_t dtype, int64_t n_slices, int32_t n
                        int32_t buf_rows, const int32_t* rows, int64_t src_rows, const void* k_local,
                        const void* v_local, int32_t window, int32_t local_start, int32_t n_local, void* out,
                        int32_t out_dtype, float* lse_out, void* workspace, size_t workspace_bytes, void* stream,
-                       const int32_t* seg_state = nullptr, int32_t n_tokens = 0) {
+                       const int32_t* seg_state = nullptr, int32_t n_tokens = 0, int32_t slice_div = 1) {
   const bool indexed = rows != nullptr;
   if (!q || !out || !n_sel) return fail(LOUISKV_ERR_NULL, "q, out and n_sel are required");
   if (buf_rows > 0 && (!k_src || !v_src))
@@ -1700,6 +1730,7 @@ int sparse_decode_attn(const void* q, int32_t dtype, int64_t n_slices, int32_t n
   a.part = static_cast<float*>(workspace);
   a.out = out; a.out_bf16 = out_dtype == LOUISKV_BF16; a.lse_out = lse_out;
   a.seg_state = seg_state; a.seg_stride = kSegRing + window; a.n_tokens = n_tokens;
+  a.slice_div = slice_div;
   a.grid = (unsigned)(n_slices * n_chunks);
   // a chunk spans at most ceil(total / n_chunks) <= ceil((buf_rows + window) / n_chunks) rows
   a.lds = indexed ? (size_t)(((int64_t)buf_rows + window + n_chunks - 1) / n_chunks + 1) * sizeof(int) : 0;
@@ -1747,6 +1778,50 @@ extern "C" int louiskv_sparse_decode_attn_rows(const void* q, int32_t dtype, int
   return sparse_decode_attn(q, dtype, n_slices, n_kv_heads, group_size, d, scale, k_pool, v_pool, n_sel, budget,
                             sel_rows, pool_rows, k_local, v_local, window, local_start, n_local, out, out_dtype,
                             lse_out, workspace, workspace_bytes, stream);
+}
+
+extern "C" int louiskv_retrieve_rows_per_head(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads,
+                                              int32_t group_size, int32_t d, double scale, const float* reps,
+                                              const int32_t* unit_start, const int32_t* unit_size, int32_t units_cap,
+                                              int32_t n_units, int32_t budget, const uint8_t* fire,
+                                              int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel,
+                                              int32_t* sel_rows, double* scores_out, void* workspace,
+                                              size_t workspace_bytes, void* stream) {
+  int st = check_retrieve_common(q, dtype, n_slices, n_kv_heads, group_size, d, reps, unit_start, unit_size, units_cap,
+                                 n_units, budget, sel_units, n_sel_units, n_sel);
+  if (st) return st;
+  if (budget > 0 && !sel_rows) return fail(LOUISKV_ERR_NULL, "sel_rows is required when budget > 0");
+  // one list per query head: the scorer runs with groups of one over
+  // n_slices * group_size lists, each reading its KV head's units
+  const int64_t lists = n_slices * group_size;
+  if (lists > INT32_MAX) return fail(LOUISKV_ERR_SHAPE, "problem too large for one launch");
+  const size_t need = align_up((size_t)lists * units_cap * kMaxGroupSize * sizeof(double), 256);
+  if (!workspace || workspace_bytes < need)
+    return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  return score_and_select(q, dtype, lists, n_kv_heads * group_size, 1, d, scale, reps, unit_start, unit_size,
+                          units_cap, n_units, budget, fire, sel_units, n_sel_units, n_sel, sel_rows, scores_out,
+                          static_cast<double*>(workspace), nullptr, 0, as_stream(stream), group_size);
+}
+
+extern "C" int louiskv_sparse_decode_attn_rows_per_head(const void* q, int32_t dtype, int64_t n_slices,
+                                                        int32_t n_kv_heads, int32_t group_size, int32_t d,
+                                                        float scale, const void* k_pool, const void* v_pool,
+                                                        int64_t pool_rows, const int32_t* sel_rows,
+                                                        const int32_t* n_sel, int32_t budget, const void* k_local,
+                                                        const void* v_local, int32_t window, int32_t local_start,
+                                                        int32_t n_local, void* out, int32_t out_dtype,
+                                                        float* lse_out, void* workspace, size_t workspace_bytes,
+                                                        void* stream) {
+  if (!sel_rows) return fail(LOUISKV_ERR_NULL, "sel_rows is required");
+  if (group_size < 1 || group_size > kMaxGroupSize)
+    return fail(LOUISKV_ERR_UNSUPPORTED, "group_size=%d must be in [1, %d]", group_size, kMaxGroupSize);
+  if (n_kv_heads < 1 || n_slices < 1 || n_slices % n_kv_heads != 0 || n_slices * group_size > INT32_MAX)
+    return fail(LOUISKV_ERR_SHAPE, "n_slices=%lld must be a positive multiple of n_kv_heads=%d", (long long)n_slices,
+                n_kv_heads);
+  // one list per query head over its KV head's pool and window
+  return sparse_decode_attn(q, dtype, n_slices * group_size, n_kv_heads * group_size, 1, d, scale, k_pool, v_pool,
+                            n_sel, budget, sel_rows, pool_rows, k_local, v_local, window, local_start, n_local, out,
+                            out_dtype, lse_out, workspace, workspace_bytes, stream, nullptr, 0, group_size);
 }
 
 extern "C" int louiskv_sparse_decode_attn_seg(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads,

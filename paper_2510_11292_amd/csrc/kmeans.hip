@@ -829,6 +829,46 @@ __global__ void pack_pool_kernel(const T* __restrict__ src, const int32_t* __res
   }
 }
 
+// Page-level index: one wave per (slice, page).  Lane l sums dims 2l, 2l+1 of
+// the page's keys in float64 (row order) and writes their mean rounded once
+// to float32; the page's K/V rows are copied to the pool in token order.
+template <class T>
+__global__ __launch_bounds__(256)
+void page_units_kernel(const T* __restrict__ keys, const T* __restrict__ values, int n_tokens, int page_len,
+                       int n_pages, int64_t n_items, float* __restrict__ reps, int units_cap,
+                       int32_t* __restrict__ unit_start, int32_t* __restrict__ unit_size, T* __restrict__ k_pool,
+                       T* __restrict__ v_pool, int64_t pool_rows) {
+  const int64_t item = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (item >= n_items) return;
+  const int lane = threadIdx.x & 63;
+  const int64_t s = item / n_pages;
+  const int p = (int)(item - s * n_pages);
+  const int a = p * page_len;
+  const int len = min(page_len, n_tokens - a);
+  double x0 = 0.0, x1 = 0.0;
+  for (int r = 0; r < len; ++r) {
+    const size_t o = ((size_t)s * n_tokens + a + r) * kHeadDim + 2 * lane;
+    x0 += (double)load_as_f32(keys, o);
+    x1 += (double)load_as_f32(keys, o + 1);
+    if (k_pool) {
+      const size_t po = ((size_t)s * pool_rows + a + r) * kHeadDim + 2 * lane;
+      k_pool[po] = keys[o];
+      k_pool[po + 1] = keys[o + 1];
+      if (v_pool) {
+        v_pool[po] = values[o];
+        v_pool[po + 1] = values[o + 1];
+      }
+    }
+  }
+  float* rep = reps + ((size_t)s * units_cap + p) * kHeadDim;
+  rep[2 * lane] = (float)(x0 / (double)len);
+  rep[2 * lane + 1] = (float)(x1 / (double)len);
+  if (lane == 0) {
+    unit_start[s * units_cap + p] = a;
+    unit_size[s * units_cap + p] = len;
+  }
+}
+
 // ------------------------------------------------------------------ host side
 
 struct Ws {
@@ -1156,6 +1196,44 @@ extern "C" int louiskv_cluster_prefill_pipelined(
   }
   LKV_CHECK_HIP(hipEventRecord(reinterpret_cast<hipEvent_t>(chunk_events[n_chunks]), cp));
   LKV_CHECK_HIP(hipStreamWaitEvent(s, reinterpret_cast<hipEvent_t>(chunk_events[n_chunks]), 0));
+  return LOUISKV_OK;
+}
+
+extern "C" int louiskv_page_prefill(const void* keys, const void* values, int32_t dtype, int64_t n_slices,
+                                    int32_t n_tokens, int32_t d, int32_t page_len, float* reps, int32_t units_cap,
+                                    int32_t* unit_start, int32_t* unit_size, void* k_pool, void* v_pool,
+                                    int64_t pool_rows, int32_t pool_on_host, void* stream) {
+  if (!keys || !reps || !unit_start || !unit_size)
+    return fail(LOUISKV_ERR_NULL, "keys, reps, unit_start and unit_size are required");
+  if (v_pool && !values) return fail(LOUISKV_ERR_NULL, "v_pool given without values");
+  if (v_pool && !k_pool) return fail(LOUISKV_ERR_NULL, "v_pool given without k_pool");
+  if (dtype != LOUISKV_F32 && dtype != LOUISKV_BF16) return fail(LOUISKV_ERR_DTYPE, "unknown dtype %d", dtype);
+  if (d != kHeadDim) return fail(LOUISKV_ERR_UNSUPPORTED, "head dim %d not supported (only 128)", d);
+  if (n_slices < 1 || n_tokens < 1 || page_len < 1)
+    return fail(LOUISKV_ERR_SHAPE, "n_slices=%lld n_tokens=%d page_len=%d", (long long)n_slices, n_tokens, page_len);
+  const int n_pages = ceil_div(n_tokens, page_len);
+  if (units_cap < n_pages) return fail(LOUISKV_ERR_SHAPE, "units_cap=%d < %d pages", units_cap, n_pages);
+  if (k_pool && pool_rows < n_tokens)
+    return fail(LOUISKV_ERR_SHAPE, "pool_rows=%lld < n_tokens=%d", (long long)pool_rows, n_tokens);
+  const int64_t items = n_slices * n_pages;
+  if ((items + 3) / 4 > INT32_MAX) return fail(LOUISKV_ERR_SHAPE, "problem too large for one launch");
+  int st;
+  if (pool_on_host && ((st = device_view_of_host_pool(k_pool, &k_pool)) || (st = device_view_of_host_pool(v_pool, &v_pool))))
+    return st;
+  hipStream_t s = as_stream(stream);
+  const unsigned grid = (unsigned)((items + 3) / 4);
+  if (dtype == LOUISKV_BF16)
+    page_units_kernel<uint16_t><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(keys),
+                                                      static_cast<const uint16_t*>(values), n_tokens, page_len,
+                                                      n_pages, items, reps, units_cap, unit_start, unit_size,
+                                                      static_cast<uint16_t*>(k_pool), static_cast<uint16_t*>(v_pool),
+                                                      pool_rows);
+  else
+    page_units_kernel<float><<<grid, 256, 0, s>>>(static_cast<const float*>(keys), static_cast<const float*>(values),
+                                                   n_tokens, page_len, n_pages, items, reps, units_cap, unit_start,
+                                                   unit_size, static_cast<float*>(k_pool), static_cast<float*>(v_pool),
+                                                   pool_rows);
+  LKV_CHECK_LAUNCH();
   return LOUISKV_OK;
 }
 

@@ -27,6 +27,12 @@ dense KV_critical buffers that louiskv_retrieve gathers; for a host pool the
 default keeps them as a cache of pool rows (louiskv_retrieve_delta), so a
 retrieval moves only the rows the previous selection did not hold.
 
+EngineConfig also selects the ablation baselines of Appendix D.3 and
+Appendix B: trigger="stride" (louiskv_fire_every in place of the boundary
+test), index="pages" (louiskv_page_prefill in place of the clustering) and
+selection="per_head" (louiskv_retrieve_rows_per_head and
+louiskv_sparse_decode_attn_rows_per_head).
+
 Python only allocates tensors and passes pointers; every step of the path
 runs in the library's kernels.
 """
@@ -59,6 +65,12 @@ class EngineConfig:
     mode: int = L.REF_ANCHOR
     head_dim: int = 128
     segments: str = "fixed"    # "fixed" seg_len-token runs, or "boundary" (seg_len is then the cap)
+    # ablation baselines (Appendix D.3, Appendix B); the defaults are the method
+    trigger: str = "boundary"  # "boundary" (the query-similarity test) or "stride" (every `stride` steps)
+    stride: int = 16
+    index: str = "clusters"    # "clusters" (k-means) or "pages" (n_clusters is then the page count)
+    page_len: int = 16
+    selection: str = "group"   # "group" (group-consistent) or "per_head"
 
     @property
     def n_groups(self) -> int:
@@ -85,6 +97,9 @@ def config_from_workload(wl, n_groups: Optional[int] = None, mode: int = L.REF_A
                 seg_len=wl.seg_len, budget=wl.budget, window=wl.window, tau=wl.tau, mode=mode,
                 head_dim=wl.head_dim)
     base.update(kw)
+    if base.get("index", "clusters") == "pages":
+        # the prompt's units are its pages
+        base["n_clusters"] = -(-base["prompt_len"] // base.get("page_len", 16))
     return EngineConfig(**base)
 
 
@@ -105,7 +120,18 @@ class LouisKVEngine:
         # KV_critical as a cache of pool rows: the default for a host-resident pool
         self.delta = (not self.zero_copy and pool_on_host) if delta is None else bool(delta)
         self.delta = self.delta and cfg.budget >= 1
+        if cfg.trigger not in ("boundary", "stride") or cfg.stride < 1:
+            raise ValueError((cfg.trigger, cfg.stride))
+        if cfg.index not in ("clusters", "pages") or cfg.page_len < 1:
+            raise ValueError((cfg.index, cfg.page_len))
+        if cfg.selection not in ("group", "per_head"):
+            raise ValueError(cfg.selection)
+        self.per_head = cfg.selection == "per_head"
+        if self.per_head and not (self.zero_copy and cfg.segments == "fixed"):
+            raise ValueError("per-head selection is built for zero-copy retrieval with fixed segments")
         S, d, cap, G = cfg.n_slices, cfg.head_dim, cfg.units_cap, cfg.n_groups
+        # selection lists: one per KV-head slice, or one per query head
+        nl = S * (cfg.n_q_heads // cfg.n_kv_heads if self.per_head else 1)
         dev = self.device
         i32 = dict(dtype=torch.int32, device=dev)
         self.reps = torch.zeros(S, cap, d, dtype=torch.float32, device=dev)
@@ -122,7 +148,7 @@ class LouisKVEngine:
         self.k_local = torch.zeros(S, cfg.window, d, dtype=dtype, device=dev)
         self.v_local = torch.zeros(S, cfg.window, d, dtype=dtype, device=dev)
         if self.zero_copy:
-            self.sel_rows = torch.zeros(S, max(cfg.budget, 1), **i32)
+            self.sel_rows = torch.zeros(nl, max(cfg.budget, 1), **i32)
             self.k_buf = self.v_buf = None
         else:
             self.sel_rows = None
@@ -132,15 +158,15 @@ class LouisKVEngine:
             self.buf_row = torch.full((S, max(cfg.budget, 1)), -1, **i32)
             self.slot_list = torch.zeros(S, max(cfg.budget, 1), **i32)
             self.n_fetched = torch.zeros(S, **i32)
-        self.sel_units = torch.zeros(S, cap, **i32)
-        self.n_sel_units = torch.zeros(S, **i32)
-        self.n_sel = torch.zeros(S, **i32)
+        self.sel_units = torch.zeros(nl, cap, **i32)
+        self.n_sel_units = torch.zeros(nl, **i32)
+        self.n_sel = torch.zeros(nl, **i32)
         self.q_ref = torch.zeros(G, cfg.n_q_heads, d, dtype=dtype, device=dev)
         self.fire = torch.zeros(G, dtype=torch.uint8, device=dev)
         self.r = torch.zeros(G, dtype=torch.float64, device=dev)
         self.out = torch.zeros(G, cfg.n_q_heads, d, dtype=out_dtype or dtype, device=dev)
         self.lse = torch.zeros(G, cfg.n_q_heads, dtype=torch.float32, device=dev)
-        self.scores = torch.zeros(S, cap, dtype=torch.float64, device=dev) if keep_scores else None
+        self.scores = torch.zeros(nl, cap, dtype=torch.float64, device=dev) if keep_scores else None
         if cfg.segments not in ("fixed", "boundary"):
             raise ValueError(cfg.segments)
         self.seg_state = (torch.zeros(S, L.segment_state_ints(cfg.window), **i32)
@@ -151,7 +177,10 @@ class LouisKVEngine:
         # chunk's pool rows on a second stream beside the next chunk's clustering
         self.prefill_chunk = None if prefill_chunk is None else max(1, min(int(prefill_chunk), S))
         self.copy_engine = bool(copy_engine)
-        if self.prefill_chunk is None:
+        if cfg.index == "pages":
+            self.ws_prefill = None
+            self.prefill_chunk = None
+        elif self.prefill_chunk is None:
             self.ws_prefill = torch.empty(L.cluster_prefill_workspace_size(S, cfg.prompt_len, cfg.n_clusters, dc),
                                           **u8)
         else:
@@ -164,7 +193,11 @@ class LouisKVEngine:
             self.copy_stream = torch.cuda.Stream(device=dev)
         g = cfg.n_q_heads // cfg.n_kv_heads
         rows = max(cfg.budget, 1)
-        if self.zero_copy:
+        if self.per_head:
+            self.ws_retrieve = torch.empty(L.retrieve_rows_workspace_size(nl, cap), **u8)
+            self.ws_attn = torch.empty(max(L.sparse_decode_attn_rows_workspace_size(nl, 1, rows, cfg.window), 1),
+                                       **u8)
+        elif self.zero_copy:
             self.ws_retrieve = torch.empty(L.retrieve_rows_workspace_size(S, cap), **u8)
             self.ws_attn = torch.empty(max(L.sparse_decode_attn_rows_workspace_size(S, g, rows, cfg.window), 1), **u8)
         elif self.delta:
@@ -182,7 +215,12 @@ class LouisKVEngine:
         write (louiskv_pack_pool).  pack_event, if given, is recorded between
         the two on the current stream."""
         c = self.cfg
-        if self.prefill_chunk is not None:
+        if c.index == "pages":
+            L.page_prefill(prompt_keys, c.page_len, self.reps, self.unit_start, self.unit_size, prompt_values,
+                           self.k_pool, self.v_pool, pool_on_host=self.pool_on_host)
+            if pack_event is not None:
+                pack_event.record()
+        elif self.prefill_chunk is not None:
             if iter_events is not None or pack_event is not None:
                 raise ValueError("the pipelined prefill takes no iteration or pack events")
             L.cluster_prefill_pipelined(prompt_keys, c.n_clusters, c.n_iters, init_idx, self.reps, self.unit_start,
@@ -218,6 +256,8 @@ class LouisKVEngine:
         c = self.cfg
         if not 0 <= g < c.n_groups:
             raise IndexError(g)
+        if self.per_head:
+            raise ValueError("group views are built for group-consistent selection")
         h = c.n_kv_heads
         v = copy.copy(self)
         v.cfg = dataclasses.replace(c, n_slices=h)
@@ -264,11 +304,19 @@ class LouisKVEngine:
         """One decode step: q_t [G][Hq][d], k_t and v_t [S][d]."""
         c = self.cfg
         t = self.t
-        L.boundary_check(q_t, self.q_ref, c.tau, c.mode, t == 0, self.fire, self.r)
+        if c.trigger == "stride":
+            L.fire_every(self.fire, t, c.stride)
+        else:
+            L.boundary_check(q_t, self.q_ref, c.tau, c.mode, t == 0, self.fire, self.r)
         if self.seg_state is not None:
             self._step_boundary_segments(q_t, k_t, v_t)
             return
-        if self.zero_copy:
+        if self.per_head:
+            L.retrieve_rows_per_head(q_t, c.n_kv_heads, self.reps, self.unit_start, self.unit_size,
+                                     self.n_units_before(t), c.budget, self.sel_units, self.n_sel_units, self.n_sel,
+                                     self.sel_rows, fire=self.fire, scores_out=self.scores,
+                                     workspace=self.ws_retrieve)
+        elif self.zero_copy:
             L.retrieve_rows(q_t, c.n_kv_heads, self.reps, self.unit_start, self.unit_size, self.n_units_before(t),
                             c.budget, self.sel_units, self.n_sel_units, self.n_sel, self.sel_rows, fire=self.fire,
                             scores_out=self.scores, workspace=self.ws_retrieve)
@@ -283,7 +331,11 @@ class LouisKVEngine:
                          self.unit_size, c.n_clusters, self.k_pool, self.v_pool, c.prompt_len,
                          pool_on_host=self.pool_on_host)
         _, _, n_local, local_start = L.window_info(t, c.window, c.seg_len)
-        if self.zero_copy:
+        if self.per_head:
+            L.sparse_decode_attn_rows_per_head(q_t, c.n_kv_heads, self.k_pool, self.v_pool, self.sel_rows,
+                                               self.n_sel, self.k_local, self.v_local, local_start, n_local,
+                                               self.out, self.lse, workspace=self.ws_attn)
+        elif self.zero_copy:
             L.sparse_decode_attn_rows(q_t, c.n_kv_heads, self.k_pool, self.v_pool, self.sel_rows, self.n_sel,
                                       self.k_local, self.v_local, local_start, n_local, self.out, self.lse,
                                       workspace=self.ws_attn)

@@ -64,6 +64,17 @@ _SIGS = {
         _P, _I32, _I64, _I32, _I32, _I32, _F,
         _P, _P, _I64, _P, _P, _I32, _P, _P, _I32, _I32, _I32,
         _P, _I32, _P, _P, _SZ, _P]),
+    "louiskv_fire_every": (ctypes.c_int, [_P, _I64, _I32, _I32, _P]),
+    "louiskv_page_prefill": (ctypes.c_int, [
+        _P, _P, _I32, _I64, _I32, _I32, _I32, _P, _I32, _P, _P, _P, _P, _I64, _I32, _P]),
+    "louiskv_retrieve_rows_per_head": (ctypes.c_int, [
+        _P, _I32, _I64, _I32, _I32, _I32, _D,
+        _P, _P, _P, _I32, _I32, _I32, _P,
+        _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "louiskv_sparse_decode_attn_rows_per_head": (ctypes.c_int, [
+        _P, _I32, _I64, _I32, _I32, _I32, _F,
+        _P, _P, _I64, _P, _P, _I32, _P, _P, _I32, _I32, _I32,
+        _P, _I32, _P, _P, _SZ, _P]),
     "louiskv_sparse_decode_attn_workspace_size": (_SZ, [_I64, _I32, _I32, _I32, _I32]),
     "louiskv_sparse_decode_attn": (ctypes.c_int, [
         _P, _I32, _I64, _I32, _I32, _I32, _F,
@@ -331,6 +342,59 @@ def sparse_decode_attn_rows(q, n_kv_heads: int, k_pool, v_pool, sel_rows, n_sel,
     ws, wsb = _ws(sparse_decode_attn_rows_workspace_size(s, gs, budget, window, d), q.device, workspace)
     sc = (1.0 / d ** 0.5) if scale is None else scale
     _check(load_library().louiskv_sparse_decode_attn_rows(
+        _ptr(q), _dtype_code(q), s, n_kv_heads, gs, d, float(sc), _ptr(k_pool), _ptr(v_pool), k_pool.shape[1],
+        _ptr(sel_rows), _ptr(n_sel), budget, _ptr(k_local), _ptr(v_local), window, local_start, n_local,
+        _ptr(out), _dtype_code(out), _ptr(lse_out), _ptr(ws), wsb, _stream(stream)))
+
+
+# ------------------------------------------------------ ablation baselines
+
+def fire_every(fire, step: int, stride: int, stream=None):
+    """Fixed-stride trigger: fire[g] = (step % stride == 0) for every group."""
+    _check(load_library().louiskv_fire_every(_ptr(fire), fire.shape[0], step, stride, _stream(stream)))
+
+
+def page_prefill(keys, page_len: int, reps, unit_start, unit_size, values=None, k_pool=None, v_pool=None,
+                 pool_on_host: bool = False, stream=None):
+    """Page-level index of the prompt (mean key per page), pool in token order."""
+    s, n, d = keys.shape
+    pool_rows = k_pool.shape[1] if k_pool is not None else 0
+    _check(load_library().louiskv_page_prefill(
+        _ptr(keys), _ptr(values), _dtype_code(keys), s, n, d, page_len, _ptr(reps), reps.shape[1],
+        _ptr(unit_start), _ptr(unit_size), _ptr(k_pool), _ptr(v_pool), pool_rows, int(pool_on_host),
+        _stream(stream)))
+
+
+def retrieve_rows_per_head(q, n_kv_heads: int, reps, unit_start, unit_size, n_units: int, budget: int, sel_units,
+                           n_sel_units, n_sel, sel_rows, fire=None, scale: Optional[float] = None, scores_out=None,
+                           workspace=None, stream=None):
+    """One selection per query head; outputs have n_slices * group_size lists."""
+    g, hq, d = q.shape
+    s = reps.shape[0]
+    cap = reps.shape[1]
+    gs = hq // n_kv_heads
+    ws, wsb = _ws(retrieve_rows_workspace_size(s * gs, cap), q.device, workspace)
+    sc = (1.0 / d ** 0.5) if scale is None else scale
+    _check(load_library().louiskv_retrieve_rows_per_head(
+        _ptr(q), _dtype_code(q), s, n_kv_heads, gs, d, float(sc),
+        _ptr(reps), _ptr(unit_start), _ptr(unit_size), cap, n_units, budget, _ptr(fire),
+        _ptr(sel_units), _ptr(n_sel_units), _ptr(n_sel), _ptr(sel_rows), _ptr(scores_out),
+        _ptr(ws), wsb, _stream(stream)))
+
+
+def sparse_decode_attn_rows_per_head(q, n_kv_heads: int, k_pool, v_pool, sel_rows, n_sel, k_local, v_local,
+                                     local_start: int, n_local: int, out, lse_out=None, scale: Optional[float] = None,
+                                     workspace=None, stream=None):
+    """Attention of every query head over its own listed pool rows and its KV
+    head's local window."""
+    g, hq, d = q.shape
+    s = k_pool.shape[0]
+    gs = hq // n_kv_heads
+    budget = sel_rows.shape[1]
+    window = k_local.shape[1] if k_local is not None else 0
+    ws, wsb = _ws(sparse_decode_attn_rows_workspace_size(s * gs, 1, budget, window, d), q.device, workspace)
+    sc = (1.0 / d ** 0.5) if scale is None else scale
+    _check(load_library().louiskv_sparse_decode_attn_rows_per_head(
         _ptr(q), _dtype_code(q), s, n_kv_heads, gs, d, float(sc), _ptr(k_pool), _ptr(v_pool), k_pool.shape[1],
         _ptr(sel_rows), _ptr(n_sel), budget, _ptr(k_local), _ptr(v_local), window, local_start, n_local,
         _ptr(out), _dtype_code(out), _ptr(lse_out), _ptr(ws), wsb, _stream(stream)))

@@ -166,6 +166,33 @@ def test_pipelined_prefill_validates_on_the_host(lib):
     assert lib.louiskv_cluster_prefill_pipelined_workspace_size(0, 32768, 128, 1024, 1, 1, 1) == 0
 
 
+def test_ablation_calls_validate_on_the_host(lib):
+    """The ablation baselines' calls refuse bad arguments before any launch."""
+    P = ctypes.c_void_p
+    dummy = P(16)
+    assert lib.louiskv_fire_every(None, 8, 0, 4, None) == 1
+    assert lib.louiskv_fire_every(dummy, 8, 0, 0, None) == 2
+    assert lib.louiskv_fire_every(dummy, 8, -1, 4, None) == 2
+    # 1000 tokens in pages of 16 are 63 units: a table of 62 is too small
+    assert lib.louiskv_page_prefill(dummy, None, 1, 2, 1000, 128, 16, dummy, 62, dummy, dummy, None, None, 0, 0,
+                                    None) == 2
+    assert lib.louiskv_page_prefill(dummy, None, 1, 2, 1000, 128, 0, dummy, 63, dummy, dummy, None, None, 0, 0,
+                                    None) == 2
+    assert lib.louiskv_page_prefill(dummy, None, 1, 2, 1000, 128, 16, dummy, 63, dummy, dummy, dummy, None, 999, 0,
+                                    None) == 2
+    assert lib.louiskv_page_prefill(dummy, None, 1, 2, 1000, 128, 16, dummy, 63, dummy, dummy, dummy, dummy, 1000, 0,
+                                    None) == 1   # v_pool without values
+    # per-head calls: a group of 9 query heads is past the limit
+    assert lib.louiskv_retrieve_rows_per_head(dummy, 1, 8, 8, 9, 128, 0.1, dummy, dummy, dummy, 64, 64, 16, None,
+                                              dummy, dummy, dummy, dummy, None, dummy, 1 << 30, None) == 4
+    assert lib.louiskv_sparse_decode_attn_rows_per_head(dummy, 1, 8, 8, 9, 128, 0.1, dummy, dummy, 100, dummy,
+                                                        dummy, 16, dummy, dummy, 8, 0, 1, dummy, 1, None, dummy,
+                                                        1 << 30, None) == 4
+    assert lib.louiskv_sparse_decode_attn_rows_per_head(dummy, 1, 8, 8, 4, 128, 0.1, dummy, dummy, 100, None,
+                                                        dummy, 16, dummy, dummy, 8, 0, 1, dummy, 1, None, dummy,
+                                                        1 << 30, None) == 1
+
+
 def test_workspace_sizes_are_positive(lib):
     assert lib.louiskv_cluster_prefill_workspace_size(256, 32768, 128, 1024, 1) > 256 * 32768 * 4
     assert lib.louiskv_retrieve_workspace_size(256, 1024, 2048) > 0

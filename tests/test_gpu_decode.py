@@ -359,31 +359,35 @@ def _check_delta_buffers(eng, gi, H):
 
 
 def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, segments="fixed", delta=None,
-              layer_by_layer=False):
+              layer_by_layer=False, **ablation):
     """Prefill on the GPU, then `steps` decode steps on the GPU and in the
     oracle (started from the GPU's prefill state), step-locked.  With
     layer_by_layer each step runs group by group (one launch sequence per
     layer) through views of the engine's tensors."""
     from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
     data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(n_groups)], gen_len=steps)
-    cfg = config_from_workload(wl, n_groups=n_groups, mode=mode, gen_len=steps, segments=segments)
+    cfg = config_from_workload(wl, n_groups=n_groups, mode=mode, gen_len=steps, segments=segments, **ablation)
     odt = torch.float32
     eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, pool_on_host=pool_on_host, keep_scores=True,
                         out_dtype=odt, zero_copy=zero_copy, delta=delta)
     eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
     torch.cuda.synchronize()
     H, g = wl.n_kv_heads, wl.group_size
+    C = cfg.n_clusters     # prompt units: clusters, or pages with index="pages"
+    per_head = cfg.selection == "per_head"
+    NL = H * g if per_head else H      # selection lists per group
     decs = []
     for gi in range(n_groups):
         sl = slice(gi * H, (gi + 1) * H)
         st = oracle.PrefillState(
-            reps=list(to64(eng.reps[sl, :wl.n_clusters])),
-            unit_start=list(to_np(eng.unit_start[sl, :wl.n_clusters]).astype(np.int64)),
-            unit_size=list(to_np(eng.unit_size[sl, :wl.n_clusters]).astype(np.int64)),
+            reps=list(to64(eng.reps[sl, :C])),
+            unit_start=list(to_np(eng.unit_start[sl, :C]).astype(np.int64)),
+            unit_size=list(to_np(eng.unit_size[sl, :C]).astype(np.int64)),
             k_pool=list(to64(eng.k_pool[sl, :wl.prompt_len])),
             v_pool=list(to64(eng.v_pool[sl, :wl.prompt_len])))
         decs.append(oracle.GroupDecoder(st, wl.n_q_heads, wl.budget, wl.window, wl.seg_len, wl.tau,
-                                        "prev" if mode == 0 else "anchor", segments=segments))
+                                        "prev" if mode == 0 else "anchor", segments=segments,
+                                        trigger=cfg.trigger, stride=cfg.stride, selection=cfg.selection))
     stats = dict(fires=0, excused=0, evictions=0, sizes=set(), fetched=0, selected=0)
     if layer_by_layer and pool_on_host:
         _require_interior_host_mapping(eng.k_pool, wl.n_kv_heads)
@@ -396,7 +400,11 @@ def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, seg
         fire, r = to_np(eng.fire), to_np(eng.r)
         for gi, dec in enumerate(decs):
             q64 = to64(data.queries[t, gi])
-            want_fire = t == 0 or oracle.boundary_fires(oracle.query_similarity(q64, dec.q_ref), wl.tau, False)
+            if cfg.trigger == "stride":
+                want_fire = oracle.stride_fires(t + 1, cfg.stride)
+                assert bool(fire[gi]) == want_fire, (t, gi)
+            else:
+                want_fire = t == 0 or oracle.boundary_fires(oracle.query_similarity(q64, dec.q_ref), wl.tau, False)
             if bool(fire[gi]) != want_fire:
                 rr = oracle.query_similarity(q64, dec.q_ref)
                 assert abs(rr - wl.tau) <= REL * max(abs(rr), wl.tau), (t, gi, rr)
@@ -405,17 +413,19 @@ def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, seg
             if fire[gi]:
                 stats["fires"] += 1
                 override = []
-                for h in range(H):
-                    s = gi * H + h
+                for li in range(NL):
+                    s = gi * NL + li
+                    h = li // g if per_head else li
                     got = to_np(eng.sel_units[s, :int(eng.n_sel_units[s])]).tolist()
-                    a = oracle.group_scores(q64[h * g:(h + 1) * g], np.asarray(dec.reps[h]), 1 / np.sqrt(128))
+                    heads = slice(li, li + 1) if per_head else slice(h * g, (h + 1) * g)
+                    a = oracle.group_scores(q64[heads], np.asarray(dec.reps[h]), 1 / np.sqrt(128))
                     np.testing.assert_allclose(to_np(eng.scores[s, :len(a)]), a, rtol=1e-12, atol=1e-300)
                     stats["excused"] += selection_matches(a, dec.unit_size[h], wl.budget, got)
                     override.append(got)
             rec = dec.step(q64, to64(data.gen_keys[t, gi * H:(gi + 1) * H]),
                            to64(data.gen_values[t, gi * H:(gi + 1) * H]), fire_override=bool(fire[gi]),
                            select_override=override)
-            assert to_np(eng.n_sel[gi * H:(gi + 1) * H]).tolist() == rec.n_sel
+            assert to_np(eng.n_sel[gi * NL:(gi + 1) * NL]).tolist() == rec.n_sel
             if eng.delta and fire[gi]:
                 _check_delta_buffers(eng, gi, H)
                 stats["fetched"] += int(eng.n_fetched[gi * H:(gi + 1) * H].sum())
@@ -592,6 +602,82 @@ def test_layer_by_layer_equals_batched_at_full_layer_count():
         assert err <= 1e-5 * max(1.0, a.out.abs().max().item()), (t, err)
         assert (a.lse - b.lse).abs().max().item() <= 1e-5, t
     assert fires > G * steps // 8
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("host", [False, True])
+def test_page_prefill_matches_oracle(dtype, host):
+    """louiskv_page_prefill: page means bit-exact against the oracle's page
+    index (ragged last page), unit tables exact, pool rows in token order and
+    rows past the prompt untouched."""
+    L = _L()
+    S, N, P, extra = 3, 1000, 16, 9
+    g = torch.Generator(device=DEV).manual_seed(51)
+    keys = (torch.randn(S, N, 128, generator=g, device=DEV) * 2).to(dtype)
+    values = torch.randn(S, N, 128, generator=g, device=DEV).to(dtype)
+    n_pages = -(-N // P)
+    cap = n_pages + 4
+    reps = torch.full((S, cap, 128), 7.0, device=DEV)
+    us = torch.full((S, cap), -5, dtype=torch.int32, device=DEV)
+    uz = torch.full((S, cap), -5, dtype=torch.int32, device=DEV)
+    if host:
+        kp = torch.full((S, N + extra, 128), 3, dtype=dtype).pin_memory()
+        vp = torch.full((S, N + extra, 128), 4, dtype=dtype).pin_memory()
+    else:
+        kp = torch.full((S, N + extra, 128), 3, dtype=dtype, device=DEV)
+        vp = torch.full((S, N + extra, 128), 4, dtype=dtype, device=DEV)
+    L.page_prefill(keys, P, reps, us, uz, values=values, k_pool=kp, v_pool=vp, pool_on_host=host)
+    torch.cuda.synchronize()
+    for sl in range(S):
+        r, a, z = oracle.page_units(to64(keys[sl]), P)
+        assert np.array_equal(to64(reps[sl, :n_pages]), r)
+        assert to_np(us[sl, :n_pages]).tolist() == a.tolist() and to_np(uz[sl, :n_pages]).tolist() == z.tolist()
+    assert torch.all(reps[:, n_pages:] == 7.0) and torch.all(us[:, n_pages:] == -5)
+    assert torch.equal(kp[:, :N].cpu(), keys.cpu()) and torch.equal(vp[:, :N].cpu(), values.cpu())
+    assert torch.all(kp[:, N:].cpu() == 3) and torch.all(vp[:, N:].cpu() == 4)
+
+
+def test_fire_every():
+    """louiskv_fire_every sets every group's flag on multiples of the stride."""
+    L = _L()
+    fire = torch.full((37,), 9, dtype=torch.uint8, device=DEV)
+    for step in range(12):
+        L.fire_every(fire, step, 5)
+        torch.cuda.synchronize()
+        assert torch.all(fire == (1 if step % 5 == 0 else 0)), step
+
+
+def _ablation_wl():
+    return synth.get_workload("si-lo-16k").replace(prompt_len=2048, n_clusters=64, budget=512, name="si-lo-16k")
+
+
+def test_decode_loop_stride_trigger():
+    """Fixed-stride trigger (a retrieval every 5 steps) through the decode
+    loop, step-locked with the oracle (bf16 reduction with evictions)."""
+    st = _run_loop(_ablation_wl(), 2, 200, mode=1, trigger="stride", stride=5)
+    assert st["fires"] == 2 * 40 and st["evictions"] > 0
+
+
+def test_decode_loop_page_index():
+    """Page-level index (16-token pages of the prompt in place of clusters)
+    through the decode loop with the gathered KV_critical."""
+    st = _run_loop(_ablation_wl(), 2, 200, mode=1, zero_copy=False, index="pages", page_len=16)
+    assert st["fires"] > 30
+
+
+def test_decode_loop_per_head_selection():
+    """Per-head selection (each of the four query heads of a KV head ranks
+    and selects alone) step-locked with the oracle, bf16 (matrix-core
+    attention over one head per list)."""
+    st = _run_loop(_ablation_wl(), 2, 200, mode=1, selection="per_head")
+    assert st["fires"] > 30 and st["evictions"] > 0
+
+
+def test_decode_loop_per_head_selection_fp32():
+    """Per-head selection on the tiny fp32 workload (vector attention path)."""
+    wl = synth.get_workload("tiny-4k")
+    st = _run_loop(wl, 1, 160, mode=1, selection="per_head")
+    assert st["fires"] > 10
 
 
 def test_host_pool_flag_rejects_device_memory():
