@@ -283,30 +283,146 @@ __device__ __forceinline__ uint64_t unit_key(double a, int id) {
 }
 __device__ __forceinline__ int key_unit(uint64_t k) { return kMaxUnits - 1 - (int)(k & (kMaxUnits - 1)); }
 
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
-  const int lo = __shfl_xor((int)(uint32_t)v, m, kWave);
-  const int hi = __shfl_xor((int)(uint32_t)(v >> 32), m, kWave);
-  return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
-}
-
-// Bitonic merge steps jj = jj0, jj0/2, .., 1 of stage k on one key per lane,
-// element index i = 64*chunk + lane; partners are in the same wave.
-__device__ __forceinline__ uint64_t bitonic_in_wave(uint64_t v, int i, int k, int jj0) {
-  for (int jj = jj0; jj > 0; jj >>= 1) {
-    const uint64_t o = shfl_xor_u64(v, jj);
-    const bool desc = (i & k) == 0;
-    const bool lower = (i & jj) == 0;
-    v = (desc == lower) ? (v > o ? v : o) : (v < o ? v : o);
+// The key of lane (lane ^ JJ), JJ < 64.  Distances 1 and 2 are quad
+// permutations and 4 and 8 row shifts (DPP, no LDS crossbar); 16 and 32 go
+// through ds_bpermute.
+template <int JJ>
+__device__ __forceinline__ uint64_t xor_partner_u64(uint64_t v, int lane) {
+  const int lo = (int)(uint32_t)v, hi = (int)(uint32_t)(v >> 32);
+  int plo, phi;
+  if constexpr (JJ == 1 || JJ == 2) {
+    constexpr int ctl = JJ == 1 ? 0xB1 : 0x4E;   // quad_perm [1,0,3,2] and [2,3,0,1]
+    plo = __builtin_amdgcn_update_dpp(lo, lo, ctl, 0xF, 0xF, false);
+    phi = __builtin_amdgcn_update_dpp(hi, hi, ctl, 0xF, 0xF, false);
+  } else if constexpr (JJ == 4 || JJ == 8) {
+    // inside a 16-lane row: lanes with bit JJ clear read lane + JJ (row_shl),
+    // the others lane - JJ (row_shr)
+    const int alo = __builtin_amdgcn_update_dpp(lo, lo, 0x100 + JJ, 0xF, 0xF, false);
+    const int ahi = __builtin_amdgcn_update_dpp(hi, hi, 0x100 + JJ, 0xF, 0xF, false);
+    const int blo = __builtin_amdgcn_update_dpp(lo, lo, 0x110 + JJ, 0xF, 0xF, false);
+    const int bhi = __builtin_amdgcn_update_dpp(hi, hi, 0x110 + JJ, 0xF, 0xF, false);
+    const bool up = (lane & JJ) != 0;
+    plo = up ? blo : alo;
+    phi = up ? bhi : ahi;
+  } else {
+    plo = __shfl_xor(lo, JJ, kWave);
+    phi = __shfl_xor(hi, JJ, kWave);
   }
-  return v;
+  return ((uint64_t)(uint32_t)phi << 32) | (uint32_t)plo;
 }
 
-// One block per fired slice: float64 group-consistent scores (Appendix B),
+// One compare-exchange step at distance JJ of bitonic stage k (element index i).
+template <int JJ>
+__device__ __forceinline__ uint64_t bitonic_step(uint64_t v, int i, int k) {
+  const uint64_t o = xor_partner_u64<JJ>(v, i & 63);
+  // the lane keeps the larger key iff its block sorts descending and it is
+  // the lower element of the pair, or ascending and the upper one; keys are
+  // distinct except padding zeros, so one compare decides
+  const bool keep_larger = ((i & k) == 0) == ((i & JJ) == 0);
+  return ((v > o) == keep_larger) ? v : o;
+}
+
+// Bitonic merge steps jj = jj0, jj0/2, .., 1 of stage k on two independent
+// keys per lane (element indices i0, i1 = 64*chunk + lane; partners are in
+// the same wave); two chains give the scheduler independent work to overlap.
+__device__ __forceinline__ void bitonic_in_wave2(uint64_t& v0, uint64_t& v1, int i0, int i1, int k, int jj0) {
+  if (jj0 >= 32) { v0 = bitonic_step<32>(v0, i0, k); v1 = bitonic_step<32>(v1, i1, k); }
+  if (jj0 >= 16) { v0 = bitonic_step<16>(v0, i0, k); v1 = bitonic_step<16>(v1, i1, k); }
+  if (jj0 >= 8) { v0 = bitonic_step<8>(v0, i0, k); v1 = bitonic_step<8>(v1, i1, k); }
+  if (jj0 >= 4) { v0 = bitonic_step<4>(v0, i0, k); v1 = bitonic_step<4>(v1, i1, k); }
+  if (jj0 >= 2) { v0 = bitonic_step<2>(v0, i0, k); v1 = bitonic_step<2>(v1, i1, k); }
+  v0 = bitonic_step<1>(v0, i0, k);
+  v1 = bitonic_step<1>(v1, i1, k);
+}
+
+constexpr int kLogitThreads = 256;
+constexpr int kLogitWaves = kLogitThreads / 64;
+constexpr int kMaxLogitParts = 16;
+
+// Logit workspace per call: the logits [S][units_cap][kMaxGroupSize].
+size_t logit_ws_doubles(int64_t S, int units_cap) { return (size_t)S * units_cap * kMaxGroupSize; }
+
+// Unit count of slice ps: the argument, or its own count with
+// boundary-delimited segments (the argument then bounds it).
+__device__ __forceinline__ int slice_units(const int32_t* seg_state, int seg_stride, int64_t ps, int n_units_arg) {
+  return seg_state ? min(max(seg_state[ps * seg_stride + kSegNUnits], 1), n_units_arg) : n_units_arg;
+}
+
+// Logits l_ju = q_j . rep_u * scale of the group-consistent score (Appendix
+// B), float64, for one part of one fired slice's units (n_parts blocks per
+// slice, so that few slices still spread over many CUs): 16 lanes per unit,
+// lane sub holding dims 8*sub..+7 of the G queries in float64 registers,
+// kSelBatch quads of units in flight per wave.
+template <class T, int G>
+__global__ __launch_bounds__(kLogitThreads)
+void unit_logits_kernel(const T* __restrict__ q, int n_kv_heads, double scale, const float* __restrict__ reps,
+                        int units_cap, int n_units_arg, const uint8_t* __restrict__ fire,
+                        double* __restrict__ logit_ws, const int32_t* __restrict__ seg_state, int seg_stride,
+                        int slice_div, int n_parts) {
+  const int64_t s = blockIdx.x / n_parts;
+  const int part = (int)(blockIdx.x - s * n_parts);
+  const int64_t grp = s / n_kv_heads;
+  if (fire && !fire[grp]) return;
+  const int64_t ps = s / slice_div;     // per-head lists read their KV head's units
+  const int n_units = slice_units(seg_state, seg_stride, ps, n_units_arg);
+  const int per = (n_units + n_parts - 1) / n_parts;
+  const int u_begin = part * per, u_end = min(n_units, u_begin + per);
+  if (u_begin >= u_end) return;
+  const int kvh = (int)(s - grp * n_kv_heads);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int sub = lane & 15, quad = lane >> 4;
+  const int n_q_heads = n_kv_heads * G;
+  double qd[G][8];
+#pragma unroll
+  for (int j = 0; j < G; ++j)
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      qd[j][e] = (double)load_as_f32(q, ((size_t)grp * n_q_heads + (size_t)kvh * G + j) * kHeadDim + 8 * sub + e);
+  double* lg = logit_ws + (size_t)s * units_cap * G;
+  const float* rs = reps + (size_t)ps * units_cap * kHeadDim;
+  for (int u0 = u_begin + w * 4 * kSelBatch; u0 < u_end; u0 += kLogitWaves * 4 * kSelBatch) {
+    float4 x[kSelBatch][2];
+#pragma unroll
+    for (int i = 0; i < kSelBatch; ++i) {
+      const int u = min(u0 + 4 * i + quad, u_end - 1);   // past the end: re-read the last unit, unused
+      const float4* r4 = reinterpret_cast<const float4*>(rs + (size_t)u * kHeadDim + 8 * sub);
+      x[i][0] = r4[0];
+      x[i][1] = r4[1];
+    }
+#pragma unroll
+    for (int i = 0; i < kSelBatch; ++i) {
+      const int u = u0 + 4 * i + quad;
+      const double xd[8] = {x[i][0].x, x[i][0].y, x[i][0].z, x[i][0].w, x[i][1].x, x[i][1].y, x[i][1].z, x[i][1].w};
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        double a = 0.0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) a = fma(qd[j][e], xd[e], a);
+        a = row16_sum_f64(a) * scale;
+        if (u < u_end && sub == j) lg[(size_t)u * G + j] = a;
+      }
+    }
+  }
+}
+
+// Number of logit blocks per slice: 1 (the selection kernel computes them
+// itself) once there are enough slices for the chip, else enough blocks
+// for it, at least 64 units per block.
+int logit_parts(int64_t n_slices, int n_units) {
+  if (n_slices >= 128) return 1;
+  int parts = (int)std::min<int64_t>(kMaxLogitParts, std::max<int64_t>(1, (1024 + n_slices - 1) / n_slices));
+  while (parts > 1 && (n_units + parts - 1) / parts < 64) --parts;
+  return parts;
+}
+
+// One block per fired slice: the float64 group-consistent scores (Appendix B),
 // a descending bitonic sort of the unit keys, prefix-stop under the budget,
 // the selected unit list and the pool-row list that the gather kernel copies.
-//  pass 1  logits l_ju = q_j . rep_u * scale and their maxima M_j, 16 lanes
-//          per unit (lane sub holds dims 8*sub..+7 of the G queries in float64
-//          registers), kSelBatch quads of units in flight per wave; the unit
+//  pass 1  the logits and their maxima M_j: with own_logits the block computes
+//          them as unit_logits_kernel does (one block per slice fills the
+//          chip when many slices fire); otherwise unit_logits_kernel has
+//          written them, spread over several blocks per slice.  The unit
 //          sizes go to LDS.
 //  pass 2  e_ju = exp(l_ju - M_j) and Z_j = sum_u e_ju.
 //  pass 3  A_u = (1/g) sum_j e_ju / Z_j and the sort keys.
@@ -320,7 +436,7 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
                          int32_t* __restrict__ sel_units, int32_t* __restrict__ n_sel_units,
                          int32_t* __restrict__ n_sel, double* __restrict__ scores_out,
                          double* __restrict__ logit_ws, int32_t* __restrict__ row_ws, int n_pad_arg,
-                         const int32_t* __restrict__ seg_state, int seg_stride, int slice_div) {
+                         const int32_t* __restrict__ seg_state, int seg_stride, int slice_div, int own_logits) {
   extern __shared__ __align__(16) char smem[];
   uint64_t* s_key = reinterpret_cast<uint64_t*>(smem);            // [n_pad_arg]
   int* s_size = reinterpret_cast<int*>(s_key + n_pad_arg);        // [n_pad_arg] unit sizes by unit id
@@ -338,57 +454,66 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
   const int64_t ps = s / slice_div;
   // with boundary-delimited segments each slice has its own unit count (the
   // argument is then an upper bound that sized the LDS)
-  int n_units = n_units_arg, n_pad = n_pad_arg;
+  const int n_units = slice_units(seg_state, seg_stride, ps, n_units_arg);
+  int n_pad = n_pad_arg;
   if (seg_state) {
-    n_units = min(max(seg_state[ps * seg_stride + kSegNUnits], 1), n_units_arg);
     n_pad = 64;
     while (n_pad < n_units) n_pad <<= 1;
   }
-  const int kvh = (int)(s - grp * n_kv_heads);
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int sub = lane & 15, quad = lane >> 4;
-  const int n_q_heads = n_kv_heads * G;
   const int32_t* us = unit_size + (size_t)ps * units_cap;
   for (int u = tid; u < n_units; u += kSelThreads) s_size[u] = max(us[u], 0);
 
-  double qd[G][8];
-#pragma unroll
-  for (int j = 0; j < G; ++j)
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      qd[j][e] = (double)load_as_f32(q, ((size_t)grp * n_q_heads + (size_t)kvh * G + j) * kHeadDim + 8 * sub + e);
-
-  // pass 1
+  // pass 1: maxima of the logits, computed here (own_logits: many slices,
+  // one block each) or read back from unit_logits_kernel (few slices)
   double mx[G];
 #pragma unroll
   for (int j = 0; j < G; ++j) mx[j] = -__builtin_inf();
   double* lg = logit_ws + (size_t)s * units_cap * G;
-  const float* rs = reps + (size_t)ps * units_cap * kHeadDim;
-  for (int u0 = w * 4 * kSelBatch; u0 < n_units; u0 += kSelWaves * 4 * kSelBatch) {
-    float4 x[kSelBatch][2];
+  if (own_logits) {
+    const int64_t grp_q = grp;
+    const int kvh = (int)(s - grp * n_kv_heads);
+    const int sub = lane & 15, quad = lane >> 4;
+    const int n_q_heads = n_kv_heads * G;
+    double qd[G][8];
 #pragma unroll
-    for (int i = 0; i < kSelBatch; ++i) {
-      const int u = min(u0 + 4 * i + quad, n_units - 1);   // past the end: re-read the last unit, unused
-      const float4* r4 = reinterpret_cast<const float4*>(rs + (size_t)u * kHeadDim + 8 * sub);
-      x[i][0] = r4[0];
-      x[i][1] = r4[1];
-    }
+    for (int j = 0; j < G; ++j)
 #pragma unroll
-    for (int i = 0; i < kSelBatch; ++i) {
-      const int u = u0 + 4 * i + quad;
-      const double xd[8] = {x[i][0].x, x[i][0].y, x[i][0].z, x[i][0].w, x[i][1].x, x[i][1].y, x[i][1].z, x[i][1].w};
+      for (int e = 0; e < 8; ++e)
+        qd[j][e] = (double)load_as_f32(q, ((size_t)grp_q * n_q_heads + (size_t)kvh * G + j) * kHeadDim + 8 * sub + e);
+    const float* rs = reps + (size_t)ps * units_cap * kHeadDim;
+    for (int u0 = w * 4 * kSelBatch; u0 < n_units; u0 += kSelWaves * 4 * kSelBatch) {
+      float4 x[kSelBatch][2];
 #pragma unroll
-      for (int j = 0; j < G; ++j) {
-        double a = 0.0;
+      for (int i = 0; i < kSelBatch; ++i) {
+        const int u = min(u0 + 4 * i + quad, n_units - 1);   // past the end: re-read the last unit, unused
+        const float4* r4 = reinterpret_cast<const float4*>(rs + (size_t)u * kHeadDim + 8 * sub);
+        x[i][0] = r4[0];
+        x[i][1] = r4[1];
+      }
 #pragma unroll
-        for (int e = 0; e < 8; ++e) a = fma(qd[j][e], xd[e], a);
-        a = row16_sum_f64(a) * scale;
-        if (u < n_units) {
-          mx[j] = fmax(mx[j], a);
-          if (sub == j) lg[(size_t)u * G + j] = a;
+      for (int i = 0; i < kSelBatch; ++i) {
+        const int u = u0 + 4 * i + quad;
+        const double xd[8] = {x[i][0].x, x[i][0].y, x[i][0].z, x[i][0].w,
+                              x[i][1].x, x[i][1].y, x[i][1].z, x[i][1].w};
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+          double a = 0.0;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) a = fma(qd[j][e], xd[e], a);
+          a = row16_sum_f64(a) * scale;
+          if (u < n_units) {
+            mx[j] = fmax(mx[j], a);
+            if (sub == j) lg[(size_t)u * G + j] = a;
+          }
         }
       }
+    }
+  } else {
+    for (int u = tid; u < n_units; u += kSelThreads) {
+#pragma unroll
+      for (int j = 0; j < G; ++j) mx[j] = fmax(mx[j], lg[(size_t)u * G + j]);
     }
   }
 #pragma unroll
@@ -445,32 +570,41 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
   __syncthreads();
 
   // bitonic sort, descending keys (n_pad >= 64)
+  // (chunks c and c + kSelWaves of a wave go together; a missing second
+  // chunk is a copy of the first, sorted and dropped)
   const int n_chunk = n_pad / 64;
-  for (int c = w; c < n_chunk; c += kSelWaves) {
-    const int i = 64 * c + lane;
-    uint64_t v = s_key[i];
-    for (int k = 2; k <= 64; k <<= 1) v = bitonic_in_wave(v, i, k, k >> 1);
-    s_key[i] = v;
+  for (int c = w; c < n_chunk; c += 2 * kSelWaves) {
+    const int c1 = c + kSelWaves < n_chunk ? c + kSelWaves : c;
+    const int i0 = 64 * c + lane, i1 = 64 * c1 + lane;
+    uint64_t v0 = s_key[i0], v1 = s_key[i1];
+#pragma unroll
+    for (int k = 2; k <= 64; k <<= 1) bitonic_in_wave2(v0, v1, i0, i1, k, k >> 1);
+    s_key[i0] = v0;
+    if (c1 != c) s_key[i1] = v1;
   }
   __syncthreads();
   for (int k = 128; k <= n_pad; k <<= 1) {
     for (int jj = k >> 1; jj >= 64; jj >>= 1) {
-      for (int i = tid; i < n_pad; i += kSelThreads) {
-        const int p = i ^ jj;
-        if (p > i) {
-          const uint64_t a = s_key[i], b = s_key[p];
-          const bool desc = (i & k) == 0;
-          if (desc ? a < b : a > b) {
-            s_key[i] = b;
-            s_key[p] = a;
-          }
+      // pair t: i has a zero at bit jj, its partner p = i + jj
+      for (int t = tid; t < n_pad / 2; t += kSelThreads) {
+        const int i = ((t & ~(jj - 1)) << 1) | (t & (jj - 1));
+        const int p = i | jj;
+        const uint64_t a = s_key[i], b = s_key[p];
+        const bool desc = (i & k) == 0;
+        if (desc ? a < b : a > b) {
+          s_key[i] = b;
+          s_key[p] = a;
         }
       }
       __syncthreads();
     }
-    for (int c = w; c < n_chunk; c += kSelWaves) {
-      const int i = 64 * c + lane;
-      s_key[i] = bitonic_in_wave(s_key[i], i, k, 32);
+    for (int c = w; c < n_chunk; c += 2 * kSelWaves) {
+      const int c1 = c + kSelWaves < n_chunk ? c + kSelWaves : c;
+      const int i0 = 64 * c + lane, i1 = 64 * c1 + lane;
+      uint64_t v0 = s_key[i0], v1 = s_key[i1];
+      bitonic_in_wave2(v0, v1, i0, i1, k, 32);
+      s_key[i0] = v0;
+      if (c1 != c) s_key[i1] = v1;
     }
     __syncthreads();
   }
@@ -1243,7 +1377,8 @@ int check_dtype(int dtype) {
 
 size_t retrieve_ws_bytes(int64_t S, int units_cap, int budget, int G) {
   Carver cv(nullptr);
-  cv.take<double>((size_t)S * units_cap * G);
+  (void)G;
+  cv.take<double>(logit_ws_doubles(S, units_cap));
   cv.take<int32_t>((size_t)S * std::max(budget, 1));
   return align_up(cv.used, 256);
 }
@@ -1431,10 +1566,17 @@ int score_and_select(const void* q, int32_t dtype, int64_t n_slices, int32_t n_k
   while (n_pad < n_units) n_pad <<= 1;
   const size_t lds = (size_t)n_pad * (sizeof(uint64_t) + 2 * sizeof(int));
   (void)d;
+  const int parts = logit_parts(n_slices, n_units);
+  if ((int64_t)n_slices * parts > INT32_MAX) return fail(LOUISKV_ERR_SHAPE, "problem too large for one launch");
 #define LKV_SEL(T, G)                                                                                                  \
+  if (parts > 1)                                                                                                       \
+    unit_logits_kernel<T, G><<<(unsigned)(n_slices * parts), kLogitThreads, 0, s>>>(                                   \
+        static_cast<const T*>(q), n_kv_heads, scale, reps, units_cap, n_units, fire, logit_ws, seg_state,            \
+        seg_stride, slice_div, parts);                                                                                \
   score_select_kernel<T, G><<<(unsigned)n_slices, kSelThreads, lds, s>>>(                                              \
       static_cast<const T*>(q), n_kv_heads, scale, reps, unit_start, unit_size, units_cap, n_units, budget, fire,    \
-      sel_units, n_sel_units, n_sel, scores_out, logit_ws, rows, n_pad, seg_state, seg_stride, slice_div)
+      sel_units, n_sel_units, n_sel, scores_out, logit_ws, rows, n_pad, seg_state, seg_stride, slice_div,            \
+      parts == 1 ? 1 : 0)
 #define LKV_SEL_G(T)                  \
   switch (group_size) {               \
     case 1: LKV_SEL(T, 1); break;     \
@@ -1501,7 +1643,7 @@ int retrieve_gather(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv
   if (!workspace || workspace_bytes < need)
     return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
   Carver cv(workspace);
-  double* logit_ws = cv.take<double>((size_t)n_slices * units_cap * kMaxGroupSize);
+  double* logit_ws = cv.take<double>(logit_ws_doubles(n_slices, units_cap));
   int32_t* row_ws = cv.take<int32_t>((size_t)n_slices * std::max(budget, 1));
   hipStream_t s = as_stream(stream);
   if ((st = score_and_select(q, dtype, n_slices, n_kv_heads, group_size, d, scale, reps, unit_start, unit_size,
@@ -1535,7 +1677,7 @@ int retrieve_rows(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_h
                                  n_units, budget, sel_units, n_sel_units, n_sel);
   if (st) return st;
   if (budget > 0 && !sel_rows) return fail(LOUISKV_ERR_NULL, "sel_rows is required when budget > 0");
-  const size_t need = align_up((size_t)n_slices * units_cap * kMaxGroupSize * sizeof(double), 256);
+  const size_t need = align_up(logit_ws_doubles(n_slices, units_cap) * sizeof(double), 256);
   if (!workspace || workspace_bytes < need)
     return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
   return score_and_select(q, dtype, n_slices, n_kv_heads, group_size, d, scale, reps, unit_start, unit_size, units_cap,
@@ -1581,7 +1723,7 @@ extern "C" int louiskv_retrieve_seg(const void* q, int32_t dtype, int64_t n_slic
 
 extern "C" size_t louiskv_retrieve_rows_workspace_size(int64_t n_slices, int32_t units_cap) {
   if (n_slices < 1 || units_cap < 1) return 0;
-  return align_up((size_t)n_slices * units_cap * kMaxGroupSize * sizeof(double), 256);
+  return align_up(logit_ws_doubles(n_slices, units_cap) * sizeof(double), 256);
 }
 
 extern "C" int louiskv_retrieve_rows(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads,
@@ -1795,7 +1937,7 @@ extern "C" int louiskv_retrieve_rows_per_head(const void* q, int32_t dtype, int6
   // n_slices * group_size lists, each reading its KV head's units
   const int64_t lists = n_slices * group_size;
   if (lists > INT32_MAX) return fail(LOUISKV_ERR_SHAPE, "problem too large for one launch");
-  const size_t need = align_up((size_t)lists * units_cap * kMaxGroupSize * sizeof(double), 256);
+  const size_t need = align_up(logit_ws_doubles(lists, units_cap) * sizeof(double), 256);
   if (!workspace || workspace_bytes < need)
     return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
   return score_and_select(q, dtype, lists, n_kv_heads * group_size, 1, d, scale, reps, unit_start, unit_size,
@@ -1859,7 +2001,7 @@ extern "C" int louiskv_sparse_decode_attn_rows_seg(const void* q, int32_t dtype,
 extern "C" size_t louiskv_retrieve_delta_workspace_size(int64_t n_slices, int32_t units_cap, int32_t budget) {
   if (n_slices < 1 || units_cap < 1 || budget < 1) return 0;
   Carver cv(nullptr);
-  cv.take<double>((size_t)n_slices * units_cap * kMaxGroupSize);
+  cv.take<double>(logit_ws_doubles(n_slices, units_cap));
   cv.take<int32_t>((size_t)n_slices * budget);   // selected pool rows
   cv.take<int32_t>((size_t)n_slices * budget);   // fetch slots
   cv.take<int32_t>((size_t)n_slices * budget);   // fetch rows
@@ -1894,7 +2036,7 @@ extern "C" int louiskv_retrieve_delta(const void* q, int32_t dtype, int64_t n_sl
   if (!workspace || workspace_bytes < need)
     return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
   Carver cv(workspace);
-  double* logit_ws = cv.take<double>((size_t)n_slices * units_cap * kMaxGroupSize);
+  double* logit_ws = cv.take<double>(logit_ws_doubles(n_slices, units_cap));
   int32_t* row_ws = cv.take<int32_t>((size_t)n_slices * budget);
   int32_t* fslot = cv.take<int32_t>((size_t)n_slices * budget);
   int32_t* frow = cv.take<int32_t>((size_t)n_slices * budget);

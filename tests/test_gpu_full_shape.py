@@ -122,6 +122,8 @@ def _check_step(eng, data, wl, t, gi, q_ref_before, stats):
         vp = eng.v_pool[s].index_select(0, rows.to(eng.v_pool.device))
         if eng.zero_copy:
             assert to_np(eng.sel_rows[s, :nsel]).tolist() == idx
+        elif eng.delta:
+            _check_delta_slots(eng, s, nsel, idx)
         else:
             assert torch.equal(eng.k_buf[s, :nsel].cpu(), kp.cpu()) and torch.equal(eng.v_buf[s, :nsel].cpu(), vp.cpu())
         # local window after the append: tokens nev*seg .. t in their ring slots
@@ -146,16 +148,28 @@ def _check_step(eng, data, wl, t, gi, q_ref_before, stats):
     stats["checked"] += 1
 
 
+def _check_delta_slots(eng, s, nsel, idx):
+    """KV_critical as a cache of pool rows: the listed slots hold copies of
+    exactly the selected pool rows (in slot order, not rank order)."""
+    bslots = to_np(eng.slot_list[s, :nsel]).astype(np.int64)
+    held = to_np(eng.buf_row[s])[bslots].astype(np.int64)
+    assert len(set(bslots.tolist())) == nsel and sorted(held.tolist()) == sorted(idx)
+    hi = torch.as_tensor(held, dtype=torch.long)
+    bi = torch.as_tensor(bslots, dtype=torch.long)
+    assert torch.equal(eng.k_buf[s].cpu()[bi], eng.k_pool[s].cpu()[hi])
+    assert torch.equal(eng.v_buf[s].cpu()[bi], eng.v_pool[s].cpu()[hi])
+
+
 def _sample_steps(wl):
     T, W, seg = wl.gen_len, wl.window, wl.seg_len
     base = {0, 1, 2, 3, W - 1, W, W + 1, W + seg, W + seg + 1, T // 2, T - 2, T - 1}
     return {t for t in base if 0 <= t < T}
 
 
-# The engine's default retrieval (zero-copy rows for device pools, the dense
-# KV_critical gather for the host pool), plus the dense gather on the
-# benchmark workload.
-DECODE_CASES = [(n, None) for n in LARGE] + [("li-so-32k", "dense")]
+# The engine's default retrieval (zero-copy rows for device pools, delta
+# transfers into KV_critical for the host pool), plus the dense gather on the
+# benchmark workload and on the host pool.
+DECODE_CASES = [(n, None) for n in LARGE] + [("li-so-32k", "dense"), ("host-131k", "dense")]
 
 
 @pytest.mark.parametrize("name,retrieval", DECODE_CASES)
@@ -166,7 +180,8 @@ def test_decode_full_shape_sampled(name, retrieval):
     data = synth.make_slices(wl, DEV)
     cfg = config_from_workload(wl, mode=L.REF_ANCHOR)
     eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, pool_on_host=wl.pool_on_host, keep_scores=True,
-                        out_dtype=torch.float32, zero_copy=False if retrieval == "dense" else None)
+                        out_dtype=torch.float32, zero_copy=False if retrieval == "dense" else None,
+                        delta=False if retrieval == "dense" else None)
     eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
     torch.cuda.synchronize()
     groups = (0, wl.n_groups - 1)
@@ -240,6 +255,8 @@ def _check_step_boundary(eng, data, wl, t, gi, q_ref_before, before, fires, stat
         vp = eng.v_pool[s].index_select(0, rows.to(eng.v_pool.device))
         if eng.zero_copy:
             assert to_np(eng.sel_rows[s, :nsel]).tolist() == idx
+        elif eng.delta:
+            _check_delta_slots(eng, s, nsel, idx)
         else:
             assert torch.equal(eng.k_buf[s, :nsel].cpu(), kp.cpu()) and torch.equal(eng.v_buf[s, :nsel].cpu(), vp.cpu())
         n_after, win1 = int(after[h, 0]), int(after[h, 1])
