@@ -115,6 +115,10 @@ def time_attention(eng, wl, reps=20):
             L.sparse_decode_attn_rows(q, c.n_kv_heads, eng.k_pool, eng.v_pool, eng.sel_rows, eng.n_sel,
                                       eng.k_local, eng.v_local, local_start, n_local, eng.out, eng.lse,
                                       workspace=eng.ws_attn, stream=st)
+        elif eng.delta:
+            L.sparse_decode_attn_rows(q, c.n_kv_heads, eng.k_buf, eng.v_buf, eng.slot_list, eng.n_sel,
+                                      eng.k_local, eng.v_local, local_start, n_local, eng.out, eng.lse,
+                                      workspace=eng.ws_attn, stream=st)
         else:
             L.sparse_decode_attn(q, c.n_kv_heads, eng.k_buf, eng.v_buf, eng.n_sel, eng.k_local, eng.v_local,
                                  local_start, n_local, eng.out, eng.lse, workspace=eng.ws_attn, stream=st)
@@ -278,6 +282,55 @@ def cpu_baseline(wl, data, budget_s: float):
                    f"of 1 of {wl.n_groups} layer groups in {t_dec * n:.1f}s, scaled by the group count"),
         "host_cpus": len(os.sched_getaffinity(0)), "cpu": platform.processor() or platform.machine(),
     }
+
+
+def host_link_rates(eng, data, mib: int = 256, reps: int = 4) -> dict:
+    """Achievable host-link rates next to the path's own: pinned-memory DMA
+    copies of `mib` MiB each way (hipMemcpyAsync through torch), and the
+    zero-copy gather of louiskv_retrieve reading the selected rows of every
+    slice from the host pool (all groups fired), in GB/s."""
+    import torch
+    from paper_2510_11292_amd import louiskv as L
+    n = mib * (1 << 20)
+    if hasattr(torch._C, "_host_emptyCache"):
+        torch._C._host_emptyCache()   # pinned blocks of engines already freed
+    host = torch.empty(n, dtype=torch.uint8).pin_memory()
+    dev = torch.empty(n, dtype=torch.uint8, device=eng.device)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def rate(fn, nbytes):
+        fn()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return nbytes * reps / (e0.elapsed_time(e1) / 1e3) / 1e9
+
+    out = {"h2d_dma_GBps": rate(lambda: dev.copy_(host, non_blocking=True), n),
+           "d2h_dma_GBps": rate(lambda: host.copy_(dev, non_blocking=True), n)}
+    del host, dev
+    c = eng.cfg
+    kb = torch.empty(c.n_slices, c.budget, c.head_dim, dtype=eng.dtype, device=eng.device)
+    vb = torch.empty_like(kb)
+    su = torch.empty(c.n_slices, c.units_cap, dtype=torch.int32, device=eng.device)
+    nsu = torch.empty(c.n_slices, dtype=torch.int32, device=eng.device)
+    ns = torch.empty_like(nsu)
+    ws = torch.empty(L.retrieve_workspace_size(c.n_slices, c.units_cap, c.budget), dtype=torch.uint8,
+                     device=eng.device)
+    q = data.queries[0]
+
+    def gather():
+        L.retrieve(q, c.n_kv_heads, eng.reps, eng.unit_start, eng.unit_size, c.n_clusters, eng.k_pool, eng.v_pool,
+                   c.budget, su, nsu, ns, kb, vb, pool_on_host=True, workspace=ws)
+    gather()
+    torch.cuda.synchronize()
+    moved = int(ns.sum()) * 2 * c.head_dim * kb.element_size()
+    out["zero_copy_gather_GBps"] = rate(gather, moved)
+    out["gather_bytes"] = moved
+    del kb, vb, ws
+    return out
 
 
 def time_pipelined_prefill(eng, data, chunk: int, copy_engine: bool, reps: int = 3) -> float:
@@ -444,6 +497,11 @@ def main() -> int:
         else:
             layer_ms = layer_by_layer_decode_ms(eng, data, wl)
             log(f"decode layer by layer: {layer_ms:.2f} ms ({wl.gen_len / (layer_ms / 1e3):.0f} steps/s)")
+    link = None
+    if eng.pool_on_host:
+        link = host_link_rates(eng, data)
+        log(f"host link: DMA {link['h2d_dma_GBps']:.1f} GB/s in, {link['d2h_dma_GBps']:.1f} GB/s out; "
+            f"zero-copy gather of selected rows {link['zero_copy_gather_GBps']:.1f} GB/s")
     pipelined = None
     if args.prefill_chunk >= 0:
         chunk = args.prefill_chunk or wl.n_kv_heads
@@ -490,6 +548,7 @@ def main() -> int:
         "pool_pack_ms": t_pack * 1e3,
         "decode_ms": t_dec * 1e3,
         "prefill_pipelined": pipelined,
+        "host_link": link,
         "roofline": {
             "kernel": "kmeans_assign (bf16 MFMA, fused argmin)",
             "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
@@ -497,7 +556,7 @@ def main() -> int:
             "avg_launch_ms": t_assign * 1e3, "flops_per_launch": flops_per_launch,
         },
         "attention_roofline": {
-            "kernel": ("sparse_decode_attn_rows" if eng.zero_copy else "sparse_decode_attn")
+            "kernel": ("sparse_decode_attn_rows" if (eng.zero_copy or eng.delta) else "sparse_decode_attn")
             + " (bf16 MFMA scores, all slices)", "bound": "hbm",
             "achieved": attn_bytes / t_attn / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": attn_bytes / t_attn / 1e9 / PEAK_HBM_GBS, "avg_launch_us": t_attn * 1e6,
