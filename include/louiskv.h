@@ -425,6 +425,26 @@ int louiskv_sparse_decode_attn_rows(const void* q, int32_t dtype, int64_t n_slic
                                     void* out, int32_t out_dtype, float* lse_out,
                                     void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * louiskv_boundary_check and louiskv_segment_output (fixed segments) of one
+ * decode step in a single launch, for callers that run them back to back:
+ * the boundary blocks and the store blocks are independent, because the store
+ * writes only the unit it creates (index n_clusters + evicted segment) and
+ * pool rows past every existing unit, which the step's retrieval does not
+ * read; so the retrieval may follow this call directly.  Arguments as the two
+ * calls (q .. fire_out as louiskv_boundary_check, k_new .. pool_on_host as
+ * louiskv_segment_output); outputs are theirs, bit for bit.
+ */
+int louiskv_decode_prologue(const void* q, void* q_ref, int32_t dtype, int64_t n_groups,
+                            int32_t n_q_heads, int32_t d, double tau, int32_t mode,
+                            int32_t first_step, double* r_out, uint8_t* fire_out,
+                            const void* k_new, const void* v_new, int64_t n_slices,
+                            void* k_local, void* v_local, int32_t window, int32_t step,
+                            int32_t seg_len, float* reps, int32_t* unit_start,
+                            int32_t* unit_size, int32_t units_cap, int32_t n_clusters,
+                            void* k_pool, void* v_pool, int64_t pool_rows, int32_t prompt_len,
+                            int32_t pool_on_host, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Decode stage with boundary-delimited segments                             */
 /* ------------------------------------------------------------------------ */

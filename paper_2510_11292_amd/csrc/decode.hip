@@ -54,12 +54,11 @@ constexpr int kBndHeadsPerPass = 32;   // 16 lane groups x 2 heads, all loads is
 // 8*sub..+7), each 16-lane group takes two heads per pass; the float64 dot
 // product and norms of a head are DPP row sums.  Cosines in float64.
 template <class T>
-__global__ __launch_bounds__(256)
-void boundary_kernel(const T* __restrict__ q, T* __restrict__ q_ref, int n_heads, double tau, int mode,
-                     int first, double* __restrict__ r_out, uint8_t* __restrict__ fire_out) {
+__device__ __forceinline__ void boundary_group(const T* __restrict__ q, T* __restrict__ q_ref, int n_heads,
+                                               double tau, int mode, int first, double* __restrict__ r_out,
+                                               uint8_t* __restrict__ fire_out, int g) {
   __shared__ double s_part[16];
   __shared__ int s_fire;
-  const int g = blockIdx.x;
   const int tid = threadIdx.x, sub = tid & 15, hg = tid >> 4;
   const size_t base = (size_t)g * n_heads * kHeadDim;
   double acc = 0.0;
@@ -113,19 +112,29 @@ void boundary_kernel(const T* __restrict__ q, T* __restrict__ q_ref, int n_heads
   }
 }
 
+template <class T>
+__global__ __launch_bounds__(256)
+void boundary_kernel(const T* __restrict__ q, T* __restrict__ q_ref, int n_heads, double tau, int mode,
+                     int first, double* __restrict__ r_out, uint8_t* __restrict__ fire_out) {
+  boundary_group(q, q_ref, n_heads, tau, mode, first, r_out, fire_out, (int)blockIdx.x);
+}
+
 // ------------------------------------------------------------------ decode store
 
 // One wave per slice: optional eviction of the oldest segment (mean key as a new
 // unit, rows copied to the pool), then the new token enters its ring slot.
+// (Lane l moves dims 2l, 2l+1 of every row, so the eviction's reads of the
+// oldest slots and the new token's write into one of them are one lane's
+// accesses, in its program order; the wave waits for its loads before the
+// write.)
 template <class T>
-__global__ __launch_bounds__(64)
-void store_decode_kernel(const T* __restrict__ k_new, const T* __restrict__ v_new, T* __restrict__ k_local,
-                         T* __restrict__ v_local, int window, int step, int seg_len, int evict_seg,
-                         float* __restrict__ reps, int32_t* __restrict__ unit_start, int32_t* __restrict__ unit_size,
-                         int units_cap, int n_clusters, T* __restrict__ k_pool, T* __restrict__ v_pool,
-                         int64_t pool_rows, int prompt_len) {
-  const int64_t s = blockIdx.x;
-  const int lane = threadIdx.x;
+__device__ __forceinline__ void store_slice(const T* __restrict__ k_new, const T* __restrict__ v_new,
+                                            T* __restrict__ k_local, T* __restrict__ v_local, int window, int step,
+                                            int seg_len, int evict_seg, float* __restrict__ reps,
+                                            int32_t* __restrict__ unit_start, int32_t* __restrict__ unit_size,
+                                            int units_cap, int n_clusters, T* __restrict__ k_pool,
+                                            T* __restrict__ v_pool, int64_t pool_rows, int prompt_len, int64_t s,
+                                            int lane) {
   const size_t lbase = (size_t)s * window * kHeadDim;
   if (evict_seg >= 0) {
     const int slot0 = (int)(((int64_t)evict_seg * seg_len) % window);
@@ -154,7 +163,7 @@ void store_decode_kernel(const T* __restrict__ k_new, const T* __restrict__ v_ne
       unit_start[s * units_cap + unit] = (int32_t)prow;
       unit_size[s * units_cap + unit] = seg_len;
     }
-    __syncthreads();
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the evicted rows are in before the slot is rewritten
   }
   const int slot = step % window;
   const size_t o = lbase + (size_t)slot * kHeadDim + 2 * lane;
@@ -163,6 +172,41 @@ void store_decode_kernel(const T* __restrict__ k_new, const T* __restrict__ v_ne
   k_local[o + 1] = k_new[n + 1];
   v_local[o] = v_new[n];
   v_local[o + 1] = v_new[n + 1];
+}
+
+template <class T>
+__global__ __launch_bounds__(64)
+void store_decode_kernel(const T* __restrict__ k_new, const T* __restrict__ v_new, T* __restrict__ k_local,
+                         T* __restrict__ v_local, int window, int step, int seg_len, int evict_seg,
+                         float* __restrict__ reps, int32_t* __restrict__ unit_start, int32_t* __restrict__ unit_size,
+                         int units_cap, int n_clusters, T* __restrict__ k_pool, T* __restrict__ v_pool,
+                         int64_t pool_rows, int prompt_len) {
+  store_slice(k_new, v_new, k_local, v_local, window, step, seg_len, evict_seg, reps, unit_start, unit_size,
+              units_cap, n_clusters, k_pool, v_pool, pool_rows, prompt_len, (int64_t)blockIdx.x, (int)threadIdx.x);
+}
+
+// The boundary test and the fixed-segment store of one decode step in one
+// launch: blocks 0..n_groups-1 test their group, the others store four slices
+// each (one wave per slice).  The two are independent: the store writes only
+// the unit it creates and rows past every existing unit, which this step's
+// retrieval does not read.
+template <class T>
+__global__ __launch_bounds__(256)
+void decode_prologue_kernel(const T* __restrict__ q, T* __restrict__ q_ref, int n_heads, double tau, int mode,
+                            int first, double* __restrict__ r_out, uint8_t* __restrict__ fire_out, int n_groups,
+                            const T* __restrict__ k_new, const T* __restrict__ v_new, T* __restrict__ k_local,
+                            T* __restrict__ v_local, int64_t n_slices, int window, int step, int seg_len,
+                            int evict_seg, float* __restrict__ reps, int32_t* __restrict__ unit_start,
+                            int32_t* __restrict__ unit_size, int units_cap, int n_clusters, T* __restrict__ k_pool,
+                            T* __restrict__ v_pool, int64_t pool_rows, int prompt_len) {
+  if ((int)blockIdx.x < n_groups) {
+    boundary_group(q, q_ref, n_heads, tau, mode, first, r_out, fire_out, (int)blockIdx.x);
+    return;
+  }
+  const int64_t s = (int64_t)(blockIdx.x - n_groups) * 4 + (threadIdx.x >> 6);
+  if (s >= n_slices) return;
+  store_slice(k_new, v_new, k_local, v_local, window, step, seg_len, evict_seg, reps, unit_start, unit_size,
+              units_cap, n_clusters, k_pool, v_pool, pool_rows, prompt_len, s, (int)(threadIdx.x & 63));
 }
 
 // store_cache(decode) with boundary-delimited segments, one wave per slice.
@@ -1482,6 +1526,54 @@ extern "C" int louiskv_segment_output(const void* k_new, const void* v_new, int3
         static_cast<const float*>(k_new), static_cast<const float*>(v_new), static_cast<float*>(k_local),
         static_cast<float*>(v_local), window, step, seg_len, ev, reps, unit_start, unit_size, units_cap, n_clusters,
         static_cast<float*>(k_pool), static_cast<float*>(v_pool), pool_rows, prompt_len);
+  LKV_CHECK_LAUNCH();
+  return LOUISKV_OK;
+}
+
+extern "C" int louiskv_decode_prologue(const void* q, void* q_ref, int32_t dtype, int64_t n_groups,
+                                       int32_t n_q_heads, int32_t d, double tau, int32_t mode, int32_t first_step,
+                                       double* r_out, uint8_t* fire_out, const void* k_new, const void* v_new,
+                                       int64_t n_slices, void* k_local, void* v_local, int32_t window, int32_t step,
+                                       int32_t seg_len, float* reps, int32_t* unit_start, int32_t* unit_size,
+                                       int32_t units_cap, int32_t n_clusters, void* k_pool, void* v_pool,
+                                       int64_t pool_rows, int32_t prompt_len, int32_t pool_on_host, void* stream) {
+  if (!q || !q_ref || !fire_out) return fail(LOUISKV_ERR_NULL, "q, q_ref and fire_out are required");
+  if (!k_new || !v_new || !k_local || !v_local) return fail(LOUISKV_ERR_NULL, "k_new, v_new, k_local, v_local required");
+  int st = check_dtype(dtype);
+  if (st) return st;
+  if (d != kHeadDim) return fail(LOUISKV_ERR_UNSUPPORTED, "head dim %d not supported (only 128)", d);
+  if (n_groups < 1 || n_q_heads < 1 || n_slices < 1 || (n_slices + 3) / 4 + n_groups > INT32_MAX)
+    return fail(LOUISKV_ERR_SHAPE, "n_groups=%lld n_q_heads=%d n_slices=%lld", (long long)n_groups, n_q_heads,
+                (long long)n_slices);
+  if (mode != LOUISKV_REF_PREV && mode != LOUISKV_REF_ANCHOR) return fail(LOUISKV_ERR_SHAPE, "unknown mode %d", mode);
+  if (pool_on_host && ((st = device_view_of_host_pool(k_pool, &k_pool)) || (st = device_view_of_host_pool(v_pool, &v_pool))))
+    return st;
+  int32_t ev = -1, n_ev = 0;
+  if ((st = louiskv_window_info(step, window, seg_len, &ev, &n_ev, nullptr, nullptr))) return st;
+  if (ev >= 0) {
+    if (!reps || !unit_start || !unit_size) return fail(LOUISKV_ERR_NULL, "unit tables required for an eviction");
+    if (n_clusters < 0 || (int64_t)n_clusters + ev >= units_cap)
+      return fail(LOUISKV_ERR_SHAPE, "unit %d exceeds units_cap=%d", n_clusters + ev, units_cap);
+    if ((k_pool || v_pool) && (int64_t)prompt_len + (int64_t)(ev + 1) * seg_len > pool_rows)
+      return fail(LOUISKV_ERR_SHAPE, "segment rows exceed pool_rows=%lld", (long long)pool_rows);
+    if (v_pool && !k_pool) return fail(LOUISKV_ERR_NULL, "v_pool given without k_pool");
+  }
+  hipStream_t s = as_stream(stream);
+  const unsigned grid = (unsigned)(n_groups + (n_slices + 3) / 4);
+  if (dtype == LOUISKV_BF16)
+    decode_prologue_kernel<uint16_t><<<grid, 256, 0, s>>>(
+        static_cast<const uint16_t*>(q), static_cast<uint16_t*>(q_ref), n_q_heads, tau, mode, first_step ? 1 : 0,
+        r_out, fire_out, (int)n_groups, static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new),
+        static_cast<uint16_t*>(k_local), static_cast<uint16_t*>(v_local), n_slices, window, step, seg_len, ev, reps,
+        unit_start, unit_size, units_cap, n_clusters, static_cast<uint16_t*>(k_pool), static_cast<uint16_t*>(v_pool),
+        pool_rows, prompt_len);
+  else
+    decode_prologue_kernel<float><<<grid, 256, 0, s>>>(
+        static_cast<const float*>(q), static_cast<float*>(q_ref), n_q_heads, tau, mode, first_step ? 1 : 0, r_out,
+        fire_out, (int)n_groups, static_cast<const float*>(k_new), static_cast<const float*>(v_new),
+        static_cast<float*>(k_local), static_cast<float*>(v_local), n_slices, window, step, seg_len, ev, reps,
+        unit_start, unit_size, units_cap, n_clusters, static_cast<float*>(k_pool), static_cast<float*>(v_pool),
+        pool_rows, prompt_len);
   LKV_CHECK_LAUNCH();
   return LOUISKV_OK;
 }

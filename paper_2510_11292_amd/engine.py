@@ -14,7 +14,9 @@ paper's Algorithm 1:
              louiskv_retrieve for the groups that fired (scores see the units
              evicted before this step), louiskv_segment_output (window append,
              oldest-segment eviction), louiskv_sparse_decode_attn over
-             [KV_critical : KV_local].  With segments="boundary" the output
+             [KV_critical : KV_local].  With fixed segments the boundary test
+             and the store run as one launch (louiskv_decode_prologue) before
+             the retrieval, which does not read what the store writes.  With segments="boundary" the output
              segments are delimited by the fired boundaries (the *_seg and
              louiskv_segment_output_boundary calls, per-slice window state
              on the device).
@@ -107,7 +109,7 @@ class LouisKVEngine:
     def __init__(self, cfg: EngineConfig, dtype: torch.dtype, device="cuda", pool_on_host: bool = False,
                  keep_scores: bool = False, out_dtype: Optional[torch.dtype] = None,
                  zero_copy: Optional[bool] = None, delta: Optional[bool] = None,
-                 prefill_chunk: Optional[int] = None, copy_engine: bool = True):
+                 prefill_chunk: Optional[int] = None, copy_engine: bool = True, fuse_prologue: bool = True):
         self.cfg = cfg
         self.dtype = dtype
         self.device = torch.device(device)
@@ -127,6 +129,9 @@ class LouisKVEngine:
         if cfg.selection not in ("group", "per_head"):
             raise ValueError(cfg.selection)
         self.per_head = cfg.selection == "per_head"
+        # boundary test and fixed-segment store of a step in one launch
+        # (louiskv_decode_prologue); with fuse_prologue=False as two calls
+        self.fuse_prologue = bool(fuse_prologue)
         if self.per_head and not (self.zero_copy and cfg.segments == "fixed"):
             raise ValueError("per-head selection is built for zero-copy retrieval with fixed segments")
         S, d, cap, G = cfg.n_slices, cfg.head_dim, cfg.units_cap, cfg.n_groups
@@ -304,8 +309,15 @@ class LouisKVEngine:
         """One decode step: q_t [G][Hq][d], k_t and v_t [S][d]."""
         c = self.cfg
         t = self.t
+        fused = self.fuse_prologue and c.trigger == "boundary" and self.seg_state is None
         if c.trigger == "stride":
             L.fire_every(self.fire, t, c.stride)
+        elif fused:
+            # the store writes only this step's new unit and pool rows, which
+            # the retrieval below does not read, so it may come first
+            L.decode_prologue(q_t, self.q_ref, c.tau, c.mode, t == 0, self.fire, self.r, k_t, v_t, self.k_local,
+                              self.v_local, t, c.seg_len, self.reps, self.unit_start, self.unit_size, c.n_clusters,
+                              self.k_pool, self.v_pool, c.prompt_len, pool_on_host=self.pool_on_host)
         else:
             L.boundary_check(q_t, self.q_ref, c.tau, c.mode, t == 0, self.fire, self.r)
         if self.seg_state is not None:
@@ -327,9 +339,10 @@ class LouisKVEngine:
                        self.k_pool, self.v_pool, c.budget, self.sel_units, self.n_sel_units, self.n_sel,
                        self.k_buf, self.v_buf, fire=self.fire, pool_on_host=self.pool_on_host,
                        scores_out=self.scores, workspace=self.ws_retrieve)
-        L.segment_output(k_t, v_t, self.k_local, self.v_local, t, c.seg_len, self.reps, self.unit_start,
-                         self.unit_size, c.n_clusters, self.k_pool, self.v_pool, c.prompt_len,
-                         pool_on_host=self.pool_on_host)
+        if not fused:
+            L.segment_output(k_t, v_t, self.k_local, self.v_local, t, c.seg_len, self.reps, self.unit_start,
+                             self.unit_size, c.n_clusters, self.k_pool, self.v_pool, c.prompt_len,
+                             pool_on_host=self.pool_on_host)
         _, _, n_local, local_start = L.window_info(t, c.window, c.seg_len)
         if self.per_head:
             L.sparse_decode_attn_rows_per_head(q_t, c.n_kv_heads, self.k_pool, self.v_pool, self.sel_rows,

@@ -65,6 +65,9 @@ _SIGS = {
         _P, _P, _I64, _P, _P, _I32, _P, _P, _I32, _I32, _I32,
         _P, _I32, _P, _P, _SZ, _P]),
     "louiskv_fire_every": (ctypes.c_int, [_P, _I64, _I32, _I32, _P]),
+    "louiskv_decode_prologue": (ctypes.c_int, [
+        _P, _P, _I32, _I64, _I32, _I32, _D, _I32, _I32, _P, _P,
+        _P, _P, _I64, _P, _P, _I32, _I32, _I32, _P, _P, _P, _I32, _I32, _P, _P, _I64, _I32, _I32, _P]),
     "louiskv_page_prefill": (ctypes.c_int, [
         _P, _P, _I32, _I64, _I32, _I32, _I32, _P, _I32, _P, _P, _P, _P, _I64, _I32, _P]),
     "louiskv_retrieve_rows_per_head": (ctypes.c_int, [
@@ -345,6 +348,21 @@ def sparse_decode_attn_rows(q, n_kv_heads: int, k_pool, v_pool, sel_rows, n_sel,
         _ptr(q), _dtype_code(q), s, n_kv_heads, gs, d, float(sc), _ptr(k_pool), _ptr(v_pool), k_pool.shape[1],
         _ptr(sel_rows), _ptr(n_sel), budget, _ptr(k_local), _ptr(v_local), window, local_start, n_local,
         _ptr(out), _dtype_code(out), _ptr(lse_out), _ptr(ws), wsb, _stream(stream)))
+
+
+def decode_prologue(q, q_ref, tau: float, mode: int, first_step: bool, fire, r_out, k_new, v_new, k_local, v_local,
+                    step: int, seg_len: int, reps, unit_start, unit_size, n_clusters: int, k_pool=None, v_pool=None,
+                    prompt_len: int = 0, pool_on_host: bool = False, stream=None):
+    """boundary_check and segment_output (fixed segments) in one launch."""
+    g, hq, d = q.shape
+    s = k_new.shape[0]
+    window = k_local.shape[1]
+    pool_rows = k_pool.shape[1] if k_pool is not None else 0
+    _check(load_library().louiskv_decode_prologue(
+        _ptr(q), _ptr(q_ref), _dtype_code(q), g, hq, d, float(tau), mode, int(first_step), _ptr(r_out), _ptr(fire),
+        _ptr(k_new), _ptr(v_new), s, _ptr(k_local), _ptr(v_local), window, step, seg_len, _ptr(reps),
+        _ptr(unit_start), _ptr(unit_size), reps.shape[1], n_clusters, _ptr(k_pool), _ptr(v_pool), pool_rows,
+        prompt_len, int(pool_on_host), _stream(stream)))
 
 
 # ------------------------------------------------------ ablation baselines

@@ -193,6 +193,23 @@ def test_ablation_calls_validate_on_the_host(lib):
                                                         1 << 30, None) == 1
 
 
+def test_decode_prologue_validates_on_the_host(lib):
+    """The fused boundary test and store refuse missing buffers, a bad mode
+    and an eviction with no unit room before any launch."""
+    P = ctypes.c_void_p
+    d = P(16)
+
+    def call(q=d, k_new=d, mode=1, step=0, units_cap=100, n_clusters=8):
+        return lib.louiskv_decode_prologue(q, d, 1, 2, 32, 128, 0.9, mode, 1, None, d, k_new, d, 16, d, d, 64, step,
+                                           16, d, d, d, units_cap, n_clusters, None, None, 0, 0, 0, None)
+    assert call(q=None) == 1
+    assert call(k_new=None) == 1
+    assert call(mode=5) == 2
+    # step 64 with a 64-token window and 16-token segments evicts segment 0
+    # into unit n_clusters, which needs units_cap > n_clusters
+    assert call(step=64, units_cap=8, n_clusters=8) == 2
+
+
 def test_workspace_sizes_are_positive(lib):
     assert lib.louiskv_cluster_prefill_workspace_size(256, 32768, 128, 1024, 1) > 256 * 32768 * 4
     assert lib.louiskv_retrieve_workspace_size(256, 1024, 2048) > 0

@@ -680,6 +680,55 @@ def test_decode_loop_per_head_selection_fp32():
     assert st["fires"] > 10
 
 
+@pytest.mark.parametrize("case", ["bf16-zero-copy", "fp32-gather", "bf16-host-delta"])
+def test_fused_prologue_equals_separate_calls(case):
+    """louiskv_decode_prologue (boundary test and store in one launch, before
+    the retrieval) leaves every output and every piece of state exactly as
+    louiskv_boundary_check and louiskv_segment_output called around it do,
+    through evictions."""
+    from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
+    if case == "fp32-gather":
+        wl = synth.get_workload("tiny-4k").replace(window=64, seg_len=16)
+        kw = dict(zero_copy=False)
+        host = False
+    elif case == "bf16-host-delta":
+        wl = synth.get_workload("host-131k").replace(prompt_len=2048, n_clusters=64, budget=512, name="host-131k")
+        kw = {}
+        host = True
+    else:
+        wl = _ablation_wl()
+        kw = {}
+        host = False
+    steps = 200
+    G = 2 if wl.n_layers > 1 else 1
+    data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(G)], gen_len=steps)
+    cfg = config_from_workload(wl, n_groups=G, gen_len=steps)
+    dt = data.prompt_keys.dtype
+    a = LouisKVEngine(cfg, dt, DEV, pool_on_host=host, out_dtype=torch.float32, fuse_prologue=True, **kw)
+    b = LouisKVEngine(cfg, dt, DEV, pool_on_host=host, out_dtype=torch.float32, fuse_prologue=False, **kw)
+    for e in (a, b):
+        e.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    names = ["fire", "r", "q_ref", "k_local", "v_local", "reps", "unit_start", "unit_size", "n_sel", "out", "lse"]
+    names += ["sel_rows"] if a.zero_copy else ["k_buf", "v_buf"]
+    fires = 0
+    for t in range(steps):
+        for e in (a, b):
+            e.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        torch.cuda.synchronize()
+        fires += int(a.fire.sum())
+        for n in names:
+            x, y = getattr(a, n), getattr(b, n)
+            assert torch.equal(x, y) or (n == "r" and t == 0), (t, n)
+    # pool rows written so far: the prompt and the evicted segments (the rest
+    # of both pools is uninitialised memory)
+    L = _L()
+    rows = cfg.prompt_len + L.window_info(steps - 1, cfg.window, cfg.seg_len)[1] * cfg.seg_len
+    assert rows > cfg.prompt_len
+    assert torch.equal(a.k_pool[:, :rows].cpu(), b.k_pool[:, :rows].cpu())
+    assert torch.equal(a.v_pool[:, :rows].cpu(), b.v_pool[:, :rows].cpu())
+    assert fires > 10
+
+
 def test_host_pool_flag_rejects_device_memory():
     """pool_on_host=1 with device tensors is refused on the host, before any launch."""
     L = _L()
