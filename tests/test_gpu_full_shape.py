@@ -322,3 +322,46 @@ def test_decode_full_shape_boundary_segments(name):
     assert (st[:, 4] == 0).all()
     assert stats["fires"] > 0 and stats["evictions"] > 0
     assert stats["checked"] >= 2 * len(steps)
+
+
+@pytest.mark.parametrize("name", ["li-so-32k", "host-131k"])
+def test_pipelined_prefill_full_shape(name):
+    """The pipelined prefill (one layer's slices per chunk, pool writes on a
+    second stream; copy engines for the host pool) at full size against the
+    one-pass prefill: unit tables, centroids and permutations of every slice
+    identical, and the pool rows of sampled slices identical."""
+    from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
+    L = _L()
+    wl = synth.get_workload(name)
+    data = synth.make_slices(wl, DEV)
+    cfg = config_from_workload(wl)
+    dt = data.prompt_keys.dtype
+    eng = LouisKVEngine(cfg, dt, DEV, pool_on_host=wl.pool_on_host)
+    eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    torch.cuda.synchronize()
+    names = ("reps", "unit_start", "unit_size", "assign", "perm")
+    ref = {n: getattr(eng, n).clone() for n in names}
+    sample = (0, wl.n_slices // 2 + 3, wl.n_slices - 1)
+    ref_pool = [(eng.k_pool[s, :wl.prompt_len].clone(), eng.v_pool[s, :wl.prompt_len].clone()) for s in sample]
+    for n in names:
+        getattr(eng, n).zero_()
+    for s in sample:
+        eng.k_pool[s].zero_()
+        eng.v_pool[s].zero_()
+    chunk = wl.n_kv_heads
+    events = [torch.cuda.Event() for _ in range(-(-wl.n_slices // chunk) + 1)]
+    for e in events:
+        e.record()
+    ws = torch.empty(L.cluster_prefill_pipelined_workspace_size(chunk, wl.prompt_len, wl.n_clusters, L.BF16,
+                                                                wl.pool_on_host, True), dtype=torch.uint8, device=DEV)
+    print(f"pipelined prefill {name}: {wl.n_slices} slices in chunks of {chunk}", flush=True)
+    L.cluster_prefill_pipelined(data.prompt_keys, wl.n_clusters, wl.n_iters, data.init_idx, eng.reps,
+                                eng.unit_start, eng.unit_size, eng.assign, eng.perm, data.prompt_values, eng.k_pool,
+                                eng.v_pool, chunk, events, torch.cuda.Stream(), pool_on_host=wl.pool_on_host,
+                                copy_engine=True, workspace=ws)
+    torch.cuda.synchronize()
+    for n in names:
+        assert torch.equal(getattr(eng, n), ref[n]), n
+    for (kr, vr), s in zip(ref_pool, sample):
+        assert torch.equal(eng.k_pool[s, :wl.prompt_len].cpu(), kr.cpu())
+        assert torch.equal(eng.v_pool[s, :wl.prompt_len].cpu(), vr.cpu())
