@@ -365,3 +365,80 @@ def test_pipelined_prefill_full_shape(name):
     for (kr, vr), s in zip(ref_pool, sample):
         assert torch.equal(eng.k_pool[s, :wl.prompt_len].cpu(), kr.cpu())
         assert torch.equal(eng.v_pool[s, :wl.prompt_len].cpu(), vr.cpu())
+
+
+ABLATIONS = {
+    "stride-5": dict(trigger="stride", stride=5),
+    "pages-16": dict(index="pages", page_len=16),
+    "per-head": dict(selection="per_head"),
+}
+
+
+@pytest.mark.parametrize("variant", sorted(ABLATIONS))
+def test_ablation_baselines_full_shape_sampled(variant):
+    """The ablation baselines on li-so-32k at full size (all 256 slices per
+    launch; 2048 page units per slice for the page index, 1024 per-head lists
+    for per-head selection): at sampled steps of two groups, the trigger, the
+    scores and selection of every list against the oracle, the row lists and
+    the attention output recomputed from the GPU's state."""
+    from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
+    L = _L()
+    wl = synth.get_workload("li-so-32k")
+    data = synth.make_slices(wl, DEV)
+    kw = ABLATIONS[variant]
+    cfg = config_from_workload(wl, **kw)
+    eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, keep_scores=True, out_dtype=torch.float32)
+    eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    torch.cuda.synchronize()
+    H, g, P, C = wl.n_kv_heads, wl.group_size, wl.prompt_len, cfg.n_clusters
+    per_head = cfg.selection == "per_head"
+    NL = H * g if per_head else H
+    scale = 1 / np.sqrt(128)
+    if cfg.index == "pages":
+        assert C == P // 16
+        for s in (0, wl.n_slices - 1):
+            r, a, z = oracle.page_units(to64(data.prompt_keys[s]), 16)
+            assert np.array_equal(to64(eng.reps[s, :C]), r)
+            assert to_np(eng.unit_start[s, :C]).tolist() == a.tolist()
+            assert torch.equal(eng.k_pool[s, :P], data.prompt_keys[s])
+    groups = (0, wl.n_groups - 1)
+    steps = {0, 1, 2, 5, 10, 37, 64, 100, wl.gen_len - 1}
+    checked = fired = 0
+    for t in range(wl.gen_len):
+        eng.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        fire = to_np(eng.fire)
+        if cfg.trigger == "stride":
+            assert (fire == (1 if t % cfg.stride == 0 else 0)).all(), t
+        if t not in steps:
+            continue
+        torch.cuda.synchronize()
+        _, _, n_local, local_start = L.window_info(t, wl.window, wl.seg_len)
+        slots = [(local_start + i) % wl.window for i in range(n_local)]
+        n_units = eng.n_units_before(t)
+        for gi in groups:
+            q64 = to64(data.queries[t, gi])
+            for li in range(NL):
+                s_list = gi * NL + li
+                h = li // g if per_head else li
+                s = gi * H + h
+                heads = slice(li, li + 1) if per_head else slice(h * g, (h + 1) * g)
+                sizes = to_np(eng.unit_size[s, :n_units]).astype(np.int64)
+                starts = to_np(eng.unit_start[s, :n_units]).astype(np.int64)
+                got = to_np(eng.sel_units[s_list, :int(eng.n_sel_units[s_list])]).tolist()
+                if fire[gi]:
+                    fired += 1
+                    a = oracle.group_scores(q64[heads], to64(eng.reps[s, :n_units]), scale)
+                    np.testing.assert_allclose(to_np(eng.scores[s_list, :n_units]), a, rtol=1e-12, atol=1e-300)
+                    selection_matches(a, sizes, wl.budget, got)
+                idx = [rr for u in got for rr in range(int(starts[u]), int(starts[u] + sizes[u]))]
+                nsel = int(eng.n_sel[s_list])
+                assert nsel == len(idx) <= wl.budget
+                assert to_np(eng.sel_rows[s_list, :nsel]).tolist() == idx
+                rows = torch.as_tensor(idx, dtype=torch.long, device=DEV)
+                kk = np.concatenate([to64(eng.k_pool[s].index_select(0, rows)), to64(eng.k_local[s, slots])])
+                vv = np.concatenate([to64(eng.v_pool[s].index_select(0, rows)), to64(eng.v_local[s, slots])])
+                o, _ = oracle.attention(q64[heads], kk, vv, scale)
+                err = np.abs(to64(eng.out[gi, heads]) - o).max()
+                assert err <= 2e-3, (variant, t, s_list, err)
+                checked += 1
+    assert checked >= len(steps) * 2 * NL and fired > 0
