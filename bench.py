@@ -179,11 +179,11 @@ def dense_decode_ms(wl, data, cfg, dtype, reps=2):
     return ms / reps
 
 
-def layer_by_layer_decode_ms(eng, data, wl, reps=2):
-    """The decode loop with every step run group by group (one launch
-    sequence per layer of the sequence, the order in which a model produces
-    its queries), one HIP graph per decode step (as a serving loop captures
-    its steps), replayed after a fresh prefill; mean ms of the loop."""
+def layer_by_layer_decode_ms(eng, data, wl, n_steps, reps=2):
+    """The first n_steps decode steps with every step run group by group (one
+    launch sequence per layer of the sequence, the order in which a model
+    produces its queries), one HIP graph per decode step (as a serving loop
+    captures its steps), replayed after a fresh prefill; mean ms of the loop."""
     import torch
 
     def one_step(t):
@@ -192,13 +192,13 @@ def layer_by_layer_decode_ms(eng, data, wl, reps=2):
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
-        for t in range(wl.gen_len):
+        for t in range(n_steps):
             one_step(t)
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
     graphs = []
     eng.t = 0
-    for t in range(wl.gen_len):
+    for t in range(n_steps):
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             one_step(t)
@@ -487,7 +487,7 @@ def main() -> int:
     dense_ms = None
     if (eng.zero_copy or eng.delta) and not args.eager:
         dense_ms = dense_decode_ms(wl, data, cfg, dtype)
-    layer_ms = None
+    layer_ms = layer_steps = None
     if not args.eager and not args.no_layer_by_layer:
         if eng.pool_on_host:
             # not timed: capturing this path group by group (the whole loop
@@ -495,8 +495,10 @@ def main() -> int:
             # is not established
             log("decode layer by layer: not timed for a host-resident pool")
         else:
-            layer_ms = layer_by_layer_decode_ms(eng, data, wl)
-            log(f"decode layer by layer: {layer_ms:.2f} ms ({wl.gen_len / (layer_ms / 1e3):.0f} steps/s)")
+            layer_steps = min(wl.gen_len, 512)
+            layer_ms = layer_by_layer_decode_ms(eng, data, wl, layer_steps)
+            log(f"decode layer by layer: {layer_steps} steps in {layer_ms:.2f} ms "
+                f"({layer_steps / (layer_ms / 1e3):.0f} steps/s)")
     link = None
     if eng.pool_on_host:
         link = host_link_rates(eng, data)
@@ -541,7 +543,7 @@ def main() -> int:
         },
         "decode_steps_per_s": wl.gen_len / t_dec,
         "decode_steps_per_s_gathered_kv_critical": (wl.gen_len / (dense_ms / 1e3)) if dense_ms else None,
-        "decode_steps_per_s_layer_by_layer": (wl.gen_len / (layer_ms / 1e3)) if layer_ms else None,
+        "decode_steps_per_s_layer_by_layer": (layer_steps / (layer_ms / 1e3)) if layer_ms else None,
         "delta_rows_moved_per_selected": (float(moved[0]) / max(float(moved[1]), 1.0)) if eng.delta else None,
         "prefill_ms": t_pre * 1e3,
         "cluster_ms": t_cluster * 1e3,
