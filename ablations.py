@@ -32,7 +32,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-# name -> EngineConfig overrides (tau, trigger, stride, index, page_len, selection, mode)
+# name -> EngineConfig overrides (tau, trigger, stride, index, page_len, seg_len, selection, mode); the
+# page-level baseline uses 16-token pages on both sides (prompt pages and output segments)
 VARIANTS = {
     "louiskv": {},
     "tau=0.5": {"tau": 0.5},
@@ -43,9 +44,9 @@ VARIANTS = {
     "fixed stride 5": {"trigger": "stride", "stride": 5},
     "fixed stride 16": {"trigger": "stride", "stride": 16},
     "per-head selection": {"selection": "per_head"},
-    "pages 16": {"index": "pages", "page_len": 16},
-    "every step, clusters": {"trigger": "stride", "stride": 1},
-    "every step, pages 16": {"trigger": "stride", "stride": 1, "index": "pages", "page_len": 16},
+    "pages 16": {"index": "pages", "page_len": 16, "seg_len": 16},
+    "every-step clusters": {"trigger": "stride", "stride": 1},
+    "every-step pages 16": {"trigger": "stride", "stride": 1, "index": "pages", "page_len": 16, "seg_len": 16},
 }
 
 
