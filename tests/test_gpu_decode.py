@@ -121,6 +121,7 @@ RETRIEVE_CASES = [
     (torch.bfloat16, 2, 8, 4, 4348, 4096, 40),    # 131K-prompt unit count: 8192-entry sort
     (torch.float32, 2, 2, 3, 200, 300, 15),       # group size that is not a power of two
     (torch.bfloat16, 1, 8, 4, 1, 64, 40),         # a single unit
+    (torch.bfloat16, 16, 8, 4, 300, 512, 20),     # 128 slices: the selection block computes its own logits
 ]
 
 
