@@ -360,7 +360,7 @@ void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restri
                         const float* __restrict__ cnorm, int32_t* __restrict__ assign,
                         int32_t* __restrict__ counts, int n_tokens, int n_clusters, int n_ctiles,
                         int blocks_per_slice, int hist_in_lds, int use_bound, uint4* __restrict__ kswz,
-                        int kswz_mode) {
+                        int kswz_mode, int32_t* __restrict__ dirty) {
   __shared__ __align__(16) char s_ring0[kBf16StageBytes];
   __shared__ __align__(16) char s_ring1[kBf16StageBytes];
   __shared__ __align__(16) char s_ring2[kBf16StageBytes];
@@ -488,6 +488,11 @@ void assign_bf16_kernel(const uint16_t* __restrict__ keys, const uint4* __restri
     zi[kt] = bidx[kt];
     zv[kt] = (h == 0) && key < n_tokens;
     if (zv[kt]) assign[(size_t)slice * n_tokens + key] = bidx[kt];
+    // a key that changed cluster marks both clusters for the update
+    if (dirty && zv[kt] && bidx[kt] != zp[kt]) {
+      dirty[(size_t)slice * n_clusters + bidx[kt]] = 1;
+      if (zp[kt] >= 0 && zp[kt] < n_clusters) dirty[(size_t)slice * n_clusters + zp[kt]] = 1;
+    }
   }
   if (counts) {
     __syncthreads();
@@ -686,7 +691,8 @@ __global__ void centroid_update_kernel(const T* __restrict__ keys, const int32_t
                                        const int32_t* __restrict__ offsets, int32_t* __restrict__ counts,
                                        const float* centroids_in, float* centroids_out, int stride, int n_tokens,
                                        int n_clusters, int64_t n_rows, uint4* __restrict__ frag,
-                                       float* __restrict__ cnorm, int n_ctiles, int zero_counts) {
+                                       float* __restrict__ cnorm, int n_ctiles, int zero_counts,
+                                       int32_t* __restrict__ dirty, int skip_clean) {
   constexpr int kDims = 16 / sizeof(T);          // dims per 16-byte piece (8 bf16, 4 fp32)
   constexpr int kLpr = kHeadDim / kDims;         // lanes per row
   constexpr int kRpl = kWave / kLpr;             // rows per wave load
@@ -698,6 +704,17 @@ __global__ void centroid_update_kernel(const T* __restrict__ keys, const int32_t
   const int c = (int)(row - s * n_clusters);
   const int n = counts[s * n_clusters + c];
   float* dst = centroids_out + ((size_t)s * stride + c) * kHeadDim;
+  if (dirty) {
+    // a cluster that no key entered or left keeps its members, hence its
+    // mean and the operand prepared from it; the flag is cleared for the
+    // next assignment either way
+    const int was_dirty = dirty[row];
+    if (lane == 0) dirty[row] = 0;
+    if (skip_clean && !was_dirty) {
+      if (zero_counts && lane == 0) counts[s * n_clusters + c] = 0;
+      return;
+    }
+  }
   if (n == 0) {
     // empty: the centroid (and its operand from the previous preparation) stay
     if (centroids_in != centroids_out) {
@@ -878,6 +895,7 @@ struct Ws {
   int32_t* offsets;
   int32_t* cursor;
   int32_t* members;
+  int32_t* dirty;   // per cluster: a key entered or left it in the last assignment
   uint4* kswz;   // bf16 key operands in B-operand order (kswz_mode of the assignment)
   size_t bytes;
 };
@@ -900,6 +918,7 @@ Ws carve(void* base, int64_t n_slices, int n_tokens, int n_clusters, int dtype) 
   w.offsets = cv.take<int32_t>((size_t)n_slices * (n_clusters + 1));
   w.cursor = cv.take<int32_t>((size_t)n_slices * n_clusters);
   w.members = cv.take<int32_t>((size_t)n_slices * n_tokens);
+  w.dirty = cv.take<int32_t>((size_t)n_slices * n_clusters);
   w.kswz = dtype == LOUISKV_BF16
                ? cv.take<uint4>((size_t)n_slices * ceil_div(n_tokens, kBf16KeysPerBlock) * kBf16KeysPerBlock * 16)
                : nullptr;
@@ -926,15 +945,18 @@ int launch_prep(const float* reps, int stride, int64_t S, int C, int dtype, cons
 
 // use_bound: assign holds a valid previous assignment; kswz_mode: 0 keys only,
 // 1 keys and store the operand copy, 2 read the copy (bf16 path only).
+// mark_dirty: flag the clusters a key enters or leaves (bf16 path; needs the
+// previous assignment, i.e. use_bound).
 int launch_assign(const void* keys, int dtype, int64_t S, int N, int C, const Ws& w, int32_t* assign,
-                  bool with_counts, bool use_bound, int kswz_mode, hipStream_t st) {
+                  bool with_counts, bool use_bound, int kswz_mode, hipStream_t st, bool mark_dirty = false) {
   const int n_ctiles = n_ctiles_for(C, dtype);
   if (dtype == LOUISKV_BF16) {
     const int bps = ceil_div(N, kBf16KeysPerBlock);
     const bool hist_lds = (size_t)C * 4 <= (size_t)kBf16StageBytes;
     assign_bf16_kernel<<<(unsigned)(S * bps), kBf16Threads, 0, st>>>(
         static_cast<const uint16_t*>(keys), w.frag, w.cnorm, assign, with_counts ? w.counts : nullptr, N, C,
-        n_ctiles, bps, hist_lds ? 1 : 0, use_bound ? 1 : 0, w.kswz, kswz_mode);
+        n_ctiles, bps, hist_lds ? 1 : 0, use_bound ? 1 : 0, w.kswz, kswz_mode,
+        mark_dirty && use_bound ? w.dirty : nullptr);
   } else {
     const int bps = ceil_div(N, kF32KeysPerBlock);
     size_t lds = (size_t)kF32StageTiles * (kF32TileU4 * 16 + kTileC * 4);
@@ -961,20 +983,25 @@ int launch_scan_scatter(const int32_t* assign, int64_t S, int N, int C, const Ws
 
 // Centroid update; with prep_next, also the next iteration's operand and
 // cleared counts (the work of launch_prep for the iterations after the first).
+// dirty_mode: 0 no flags (every cluster), 1 every cluster and clear the
+// flags, 2 only the flagged clusters (the others keep centroid and operand)
+// and clear the flags.
 int launch_sum(const void* keys, int dtype, int64_t S, int N, int C, const Ws& w, const float* cin, float* cout,
-               int stride, bool prep_next, hipStream_t st) {
+               int stride, bool prep_next, hipStream_t st, int dirty_mode = 0) {
   const int64_t rows = S * C;
   const int grid = (int)((rows + 3) / 4);
   const int n_ctiles = n_ctiles_for(C, dtype);
   uint4* frag = prep_next ? w.frag : nullptr;
+  int32_t* dirty = dirty_mode ? w.dirty : nullptr;
+  const int skip = dirty_mode == 2 ? 1 : 0;
   if (dtype == LOUISKV_BF16)
     centroid_update_kernel<uint16_t><<<grid, 256, 0, st>>>(static_cast<const uint16_t*>(keys), w.members,
                                                             w.offsets, w.counts, cin, cout, stride, N, C, rows, frag,
-                                                            w.cnorm, n_ctiles, prep_next ? 1 : 0);
+                                                            w.cnorm, n_ctiles, prep_next ? 1 : 0, dirty, skip);
   else
     centroid_update_kernel<float><<<grid, 256, 0, st>>>(static_cast<const float*>(keys), w.members, w.offsets,
                                                          w.counts, cin, cout, stride, N, C, rows, frag, w.cnorm,
-                                                         n_ctiles, prep_next ? 1 : 0);
+                                                         n_ctiles, prep_next ? 1 : 0, dirty, skip);
   LKV_CHECK_LAUNCH();
   return LOUISKV_OK;
 }
@@ -1023,11 +1050,15 @@ int run_cluster(const void* keys, int dtype, int64_t S, int N, int C, int n_iter
   if ((st = launch_prep(reps, units_cap, S, C, dtype, w, true, s))) return st;
   for (int it = 0; it < n_iters; ++it) {
     if (iter_events) LKV_CHECK_HIP(hipEventRecord(reinterpret_cast<hipEvent_t>(iter_events[2 * it]), s));
-    if ((st = launch_assign(keys, dtype, S, N, C, w, assign, true, it > 0, it == 0 ? 1 : 2, s)))
+    // from the second iteration on (bf16), the assignment flags the clusters
+    // that keys entered or left and the update recomputes only those
+    const bool track = dtype == LOUISKV_BF16;
+    if ((st = launch_assign(keys, dtype, S, N, C, w, assign, true, it > 0, it == 0 ? 1 : 2, s, track)))
       return st;
     if (iter_events) LKV_CHECK_HIP(hipEventRecord(reinterpret_cast<hipEvent_t>(iter_events[2 * it + 1]), s));
     if ((st = launch_scan_scatter(assign, S, N, C, w, s))) return st;
-    if ((st = launch_sum(keys, dtype, S, N, C, w, reps, reps, units_cap, it + 1 < n_iters, s)))
+    if ((st = launch_sum(keys, dtype, S, N, C, w, reps, reps, units_cap, it + 1 < n_iters, s,
+                         track ? (it == 0 ? 1 : 2) : 0)))
       return st;
   }
   {
