@@ -846,6 +846,11 @@ __global__ void pack_pool_kernel(const T* __restrict__ src, const int32_t* __res
   }
 }
 
+__global__ void fill_i32_kernel(int32_t* __restrict__ p, int32_t v, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
 // Page-level index: one wave per (slice, page).  Lane l sums dims 2l, 2l+1 of
 // the page's keys in float64 (row order) and writes their mean rounded once
 // to float32; the page's K/V rows are copied to the pool in token order.
@@ -1313,7 +1318,12 @@ extern "C" int louiskv_kmeans_update(const void* keys, int32_t dtype, int64_t n_
     return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need.bytes, workspace_bytes);
   const Ws w = carve(workspace, n_slices, n_tokens, n_clusters, dtype);
   hipStream_t s = as_stream(stream);
-  LKV_CHECK_HIP(hipMemsetAsync(w.counts, 0, sizeof(int32_t) * n_slices * n_clusters, s));
+  {
+    // a fill kernel rather than a memset node, so the call stays safe to capture
+    const int64_t n = n_slices * n_clusters;
+    fill_i32_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(w.counts, 0, n);
+    LKV_CHECK_LAUNCH();
+  }
   const int bps = ceil_div(n_tokens, kCountKeys);
   const bool lds_ok = (size_t)n_clusters * 4 <= kMaxHistLds;
   count_kernel<<<(unsigned)(n_slices * bps), 256, lds_ok ? (size_t)n_clusters * 4 : 0, s>>>(

@@ -730,6 +730,55 @@ def test_fused_prologue_equals_separate_calls(case):
     assert fires > 10
 
 
+@pytest.mark.parametrize("case", ["zero-copy", "boundary-segments", "host-delta"])
+def test_decode_graph_replays_match_eager(case):
+    """The decode loop captured once as a HIP graph (as the benchmark runs it)
+    and replayed three times, each after a fresh eager prefill and with eager
+    work and synchronisations between the replays, gives at every step the
+    outputs and selection sizes of the eager loop."""
+    from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
+    host = case == "host-delta"
+    if host:
+        wl = synth.get_workload("host-131k").replace(prompt_len=2048, n_clusters=64, budget=512, name="host-131k")
+    else:
+        wl = _ablation_wl()
+    seg = dict(segments="boundary", window=64, seg_len=16) if case == "boundary-segments" else {}
+    steps, G = 160, 2
+    data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(G)], gen_len=steps)
+    cfg = config_from_workload(wl, n_groups=G, gen_len=steps, **seg)
+    eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, pool_on_host=host, out_dtype=torch.float32)
+    hist = torch.zeros(steps, *eng.out.shape, device=DEV)
+    hist_n = torch.zeros(steps, *eng.n_sel.shape, dtype=torch.int32, device=DEV)
+
+    def loop():
+        for t in range(steps):
+            eng.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+            hist[t].copy_(eng.out)
+            hist_n[t].copy_(eng.n_sel)
+    eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    loop()
+    torch.cuda.synchronize()
+    ref, ref_n = hist.clone(), hist_n.clone()
+    assert int((ref_n > 0).sum()) > 0
+    eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    eng.t = 0
+    with torch.cuda.graph(graph):
+        loop()
+    for rep in range(3):
+        hist.zero_()
+        hist_n.zero_()
+        eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+        torch.cuda.synchronize()
+        print(f"graph replay {rep} ({case})", flush=True)
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(hist, ref), (case, rep)
+        assert torch.equal(hist_n, ref_n), (case, rep)
+    del graph
+
+
 def test_host_pool_flag_rejects_device_memory():
     """pool_on_host=1 with device tensors is refused on the host, before any launch."""
     L = _L()
