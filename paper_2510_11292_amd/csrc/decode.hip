@@ -1419,9 +1419,8 @@ int check_dtype(int dtype) {
   return LOUISKV_OK;
 }
 
-size_t retrieve_ws_bytes(int64_t S, int units_cap, int budget, int G) {
+size_t retrieve_ws_bytes(int64_t S, int units_cap, int budget) {
   Carver cv(nullptr);
-  (void)G;
   cv.take<double>(logit_ws_doubles(S, units_cap));
   cv.take<int32_t>((size_t)S * std::max(budget, 1));
   return align_up(cv.used, 256);
@@ -1639,7 +1638,7 @@ extern "C" int louiskv_segment_output_boundary(const void* k_new, const void* v_
 
 extern "C" size_t louiskv_retrieve_workspace_size(int64_t n_slices, int32_t units_cap, int32_t budget) {
   if (n_slices < 1 || units_cap < 1 || budget < 0) return 0;
-  return retrieve_ws_bytes(n_slices, units_cap, budget, kMaxGroupSize);
+  return retrieve_ws_bytes(n_slices, units_cap, budget);
 }
 
 namespace louiskv {
@@ -1731,7 +1730,7 @@ int retrieve_gather(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv
   void* vpd = const_cast<void*>(v_pool);
   if (pool_on_host && ((st = device_view_of_host_pool(k_pool, &kpd)) || (st = device_view_of_host_pool(v_pool, &vpd))))
     return st;
-  const size_t need = retrieve_ws_bytes(n_slices, units_cap, budget, kMaxGroupSize);
+  const size_t need = retrieve_ws_bytes(n_slices, units_cap, budget);
   if (!workspace || workspace_bytes < need)
     return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
   Carver cv(workspace);
