@@ -264,6 +264,19 @@ def cpu_baseline(wl, data, budget_s: float):
     results += [oracle.kmeans(f64(data.prompt_keys[h]), data.init_idx[h].cpu().numpy(), 1, bf16)
                 for h in range(km_slices, H)]
 
+    # the same k-means on one core: two iterations of one slice, scaled to the
+    # workload's iteration count (every iteration costs the same)
+    keys_per_s_1 = None
+    try:
+        from threadpoolctl import threadpool_limits
+        it1 = min(2, wl.n_iters)
+        with threadpool_limits(limits=1):
+            t0 = time.time()
+            oracle.kmeans(f64(data.prompt_keys[0]), data.init_idx[0].cpu().numpy(), it1, bf16)
+            t1 = time.time() - t0
+        keys_per_s_1 = wl.prompt_len / (t1 * wl.n_iters / it1)
+    except Exception:  # pragma: no cover
+        pass
     st = oracle.prefill_state_from_kmeans([f64(data.prompt_keys[h]) for h in range(H)],
                                           [f64(data.prompt_values[h]) for h in range(H)], results)
     dec = oracle.GroupDecoder(st, wl.n_q_heads, wl.budget, wl.window, wl.seg_len, wl.tau, "anchor")
@@ -276,10 +289,11 @@ def cpu_baseline(wl, data, budget_s: float):
     steps_per_s = 1.0 / (t_dec * wl.n_groups)
     return {
         "value": keys_per_s, "unit": "keys/s", "cores": int(blas_threads), "kind": "oracle",
-        "decode_steps_per_s": steps_per_s,
+        "decode_steps_per_s": steps_per_s, "value_1_core": keys_per_s_1,
         "sample": (f"k-means of {km_slices} of {wl.n_slices} slices ({wl.prompt_len} keys, C={wl.n_clusters}, "
                    f"{wl.n_iters} iterations) in {t_km:.1f}s, scaled linearly; decode: {n} of {wl.gen_len} steps "
-                   f"of 1 of {wl.n_groups} layer groups in {t_dec * n:.1f}s, scaled by the group count"),
+                   f"of 1 of {wl.n_groups} layer groups in {t_dec * n:.1f}s, scaled by the group count; "
+                   f"value_1_core: 2 iterations of one slice on one thread, scaled to {wl.n_iters}"),
         "host_cpus": len(os.sched_getaffinity(0)), "cpu": platform.processor() or platform.machine(),
     }
 
