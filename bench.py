@@ -45,6 +45,8 @@ PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "kmeans_assign_traffic_li-so-32k.md")
 ASSIGN_SOURCES = [os.path.join(ROOT, "paper_2510_11292_amd", "csrc", f) for f in ("kmeans.hip", "common.h")]
+ATTN_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_traffic_li-so-32k.md")
+ATTN_SOURCES = [os.path.join(ROOT, "paper_2510_11292_amd", "csrc", f) for f in ("decode.hip", "common.h")]
 
 
 def log(msg: str) -> None:
@@ -70,21 +72,21 @@ def sources_sha256(paths) -> str:
     return h.hexdigest()
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per assignment launch from the committed counter summary
+def measured_traffic(workload: str, path: str = TRAFFIC_FILE, sources=ASSIGN_SOURCES):
+    """HBM bytes per launch of a kernel from its committed counter summary
     (FETCH_SIZE + WRITE_SIZE, calibrated on a plain copy), or None when the
     summary is missing, covers another workload, or the kernel's sources have
     changed since the counters were taken."""
-    if not os.path.exists(TRAFFIC_FILE):
+    if not os.path.exists(path):
         return None
     fields = {}
-    with open(TRAFFIC_FILE) as f:
+    with open(path) as f:
         for line in f:
             if line.startswith("- ") and ": " in line:
                 k, v = line[2:].split(": ", 1)
                 fields[k.strip()] = v.strip().strip("`")
     try:
-        if fields.get("workload") != workload or fields.get("kernel_sources_sha256") != sources_sha256(ASSIGN_SOURCES):
+        if fields.get("workload") != workload or fields.get("kernel_sources_sha256") != sources_sha256(sources):
             return None
         return float(fields["fetch_bytes_per_launch"]) + float(fields["write_bytes_per_launch"])
     except (KeyError, ValueError):
@@ -577,6 +579,8 @@ def main() -> int:
             "achieved": attn_bytes / t_attn / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": attn_bytes / t_attn / 1e9 / PEAK_HBM_GBS, "avg_launch_us": t_attn * 1e6,
             "bytes_per_launch": attn_bytes,
+            "traffic": (measured_traffic(wl.name, ATTN_TRAFFIC_FILE, ATTN_SOURCES)
+                        if eng.zero_copy and args.segments == "fixed" else None),
         },
     }
     log(f"clustering {t_cluster * 1e3:.2f} ms + pool pack {t_pack * 1e3:.2f} ms; decode {t_dec * 1e3:.2f} ms ({wl.gen_len / t_dec:.0f} steps/s), "
