@@ -5,6 +5,7 @@ import ctypes
 import os
 import re
 import subprocess
+import sys
 
 import numpy as np
 import pytest
@@ -217,3 +218,11 @@ def test_workspace_sizes_are_positive(lib):
     assert lib.louiskv_sparse_decode_attn_workspace_size(256, 4, 128, 2048, 128) == 0
     assert lib.louiskv_sparse_decode_attn_workspace_size(8, 4, 128, 2048, 128) > 0
     assert lib.louiskv_cluster_prefill_workspace_size(0, 1, 128, 1, 1) == 0
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU; asked for more it exits with a message."""
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2 and "one GPU" in r.stderr and r.stdout == ""
