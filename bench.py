@@ -53,11 +53,19 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def make_inputs(wl, device):
+def make_inputs(wl, device, layer_major: bool = False):
+    """Seeded inputs of every (sequence, layer) group, sequence by sequence;
+    with layer_major the groups are ordered layer by layer (all sequences of
+    layer 0, then layer 1, ...) so that one layer of the batch is a contiguous
+    run of slices."""
     import torch
     import synth
     t0 = time.time()
-    data = synth.make_slices(wl, device)
+    if layer_major:
+        groups = [(seq, layer) for layer in range(wl.n_layers) for seq in range(wl.batch)]
+    else:
+        groups = [(seq, layer) for seq in range(wl.batch) for layer in range(wl.n_layers)]
+    data = synth.make_slices(wl, device, groups=groups)
     torch.cuda.synchronize()
     log(f"generated inputs for {data.n_slices} slices in {time.time() - t0:.1f}s")
     return data
@@ -189,7 +197,8 @@ def layer_by_layer_decode_ms(eng, data, wl, n_steps, reps=2):
     import torch
 
     def one_step(t):
-        eng.step_layer_by_layer(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        # one launch sequence per layer: the batch's groups of a layer are contiguous
+        eng.step_layer_by_layer(data.queries[t], data.gen_keys[t], data.gen_values[t], groups_per_launch=wl.batch)
     eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
@@ -512,6 +521,13 @@ def main() -> int:
             log("decode layer by layer: not timed for a host-resident pool")
         else:
             layer_steps = min(wl.gen_len, 512)
+            if wl.batch > 1:
+                # one launch sequence per layer needs the batch's groups of a
+                # layer next to each other (the batched loop above runs faster
+                # with the sequence-major order)
+                del data
+                torch.cuda.empty_cache()
+                data = make_inputs(wl, dev, layer_major=True)
             layer_ms = layer_by_layer_decode_ms(eng, data, wl, layer_steps)
             log(f"decode layer by layer: {layer_steps} steps in {layer_ms:.2f} ms "
                 f"({layer_steps / (layer_ms / 1e3):.0f} steps/s)")

@@ -253,49 +253,60 @@ class LouisKVEngine:
                   "n_sel", "scores", "seg_state")
     _PER_GROUP = ("q_ref", "fire", "r", "out", "lse")
 
-    def group_view(self, g: int) -> "LouisKVEngine":
-        """An engine over group g alone (one layer of one sequence) that shares
-        this engine's storage: its calls read and write the same tensors, so a
-        decode step can run group by group, as a model runs its layers."""
+    def group_view(self, g: int, n: int = 1) -> "LouisKVEngine":
+        """An engine over groups g .. g+n-1 alone (one layer of n sequences when
+        the groups are ordered layer by layer) that shares this engine's
+        storage: its calls read and write the same tensors, so a decode step
+        can run layer by layer, as a model runs its layers."""
         import copy
         c = self.cfg
-        if not 0 <= g < c.n_groups:
-            raise IndexError(g)
+        if n < 1 or not 0 <= g or g + n > c.n_groups:
+            raise IndexError((g, n))
         if self.per_head:
             raise ValueError("group views are built for group-consistent selection")
         h = c.n_kv_heads
         v = copy.copy(self)
-        v.cfg = dataclasses.replace(c, n_slices=h)
+        v.cfg = dataclasses.replace(c, n_slices=h * n)
         for name in self._PER_SLICE:
             t = getattr(self, name, None)
             if t is not None:
-                setattr(v, name, t[g * h:(g + 1) * h])
+                setattr(v, name, t[g * h:(g + n) * h])
         for name in self._PER_GROUP:
-            setattr(v, name, getattr(self, name)[g:g + 1])
+            setattr(v, name, getattr(self, name)[g:g + n])
         # fewer slices per launch can take a larger workspace (split-KV
         # attention partials); the views run one after another and share it
         if not hasattr(self, "_view_ws_attn"):
+            self._view_ws_attn = {}
+        if n not in self._view_ws_attn:
             gs = c.n_q_heads // h
             rows = max(c.budget, 1)
             if self.zero_copy or self.delta:
-                need = L.sparse_decode_attn_rows_workspace_size(h, gs, rows, c.window)
+                need = L.sparse_decode_attn_rows_workspace_size(h * n, gs, rows, c.window)
             else:
-                need = L.sparse_decode_attn_workspace_size(h, gs, rows, c.window)
-            self._view_ws_attn = (self.ws_attn if need <= self.ws_attn.numel() else
-                                  torch.empty(need, dtype=torch.uint8, device=self.device))
-        v.ws_attn = self._view_ws_attn
+                need = L.sparse_decode_attn_workspace_size(h * n, gs, rows, c.window)
+            self._view_ws_attn[n] = (self.ws_attn if need <= self.ws_attn.numel() else
+                                     torch.empty(need, dtype=torch.uint8, device=self.device))
+        v.ws_attn = self._view_ws_attn[n]
         return v
 
-    def step_layer_by_layer(self, q_t: torch.Tensor, k_t: torch.Tensor, v_t: torch.Tensor) -> None:
-        """One decode step run group by group (one launch sequence per layer,
-        the order in which a model produces its queries); results equal step()."""
+    def step_layer_by_layer(self, q_t: torch.Tensor, k_t: torch.Tensor, v_t: torch.Tensor,
+                            groups_per_launch: int = 1) -> None:
+        """One decode step run in launches of groups_per_launch consecutive
+        groups (one layer at a time, the order in which a model produces its
+        queries: with the groups ordered layer by layer, groups_per_launch =
+        batch size gives one launch sequence per layer); results equal step()."""
         c = self.cfg
         h = c.n_kv_heads
-        if not hasattr(self, "_views"):
-            self._views = [self.group_view(g) for g in range(c.n_groups)]
-        for g, v in enumerate(self._views):
+        n = groups_per_launch
+        if c.n_groups % n:
+            raise ValueError(f"{c.n_groups} groups do not split into launches of {n}")
+        if getattr(self, "_views_n", None) != n:
+            self._views = [self.group_view(g, n) for g in range(0, c.n_groups, n)]
+            self._views_n = n
+        for i, v in enumerate(self._views):
+            g = i * n
             v.t = self.t
-            v.step(q_t[g:g + 1], k_t[g * h:(g + 1) * h], v_t[g * h:(g + 1) * h])
+            v.step(q_t[g:g + n], k_t[g * h:(g + n) * h], v_t[g * h:(g + n) * h])
         self.t += 1
 
     # ---------------------------------------------------------------- decode

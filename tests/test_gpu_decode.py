@@ -583,25 +583,28 @@ def test_layer_by_layer_equals_batched_at_full_layer_count():
     G, steps = 32, 170
     data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(G)], gen_len=steps)
     cfg = config_from_workload(wl, n_groups=G, gen_len=steps)
-    engs = [LouisKVEngine(cfg, torch.bfloat16, DEV, out_dtype=torch.float32) for _ in range(2)]
+    # batched; one group per launch; four groups per launch (a layer of a batch of four)
+    engs = [LouisKVEngine(cfg, torch.bfloat16, DEV, out_dtype=torch.float32) for _ in range(3)]
     for e in engs:
         e.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
     fires = 0
     for t in range(steps):
         engs[0].step(data.queries[t], data.gen_keys[t], data.gen_values[t])
         engs[1].step_layer_by_layer(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        engs[2].step_layer_by_layer(data.queries[t], data.gen_keys[t], data.gen_values[t], groups_per_launch=4)
         torch.cuda.synchronize()
-        a, b = engs
-        assert torch.equal(a.fire, b.fire), t
+        a = engs[0]
         fires += int(a.fire.sum())
-        for name in ("n_sel", "n_sel_units", "sel_units", "unit_start", "unit_size", "reps"):
-            assert torch.equal(getattr(a, name), getattr(b, name)), (t, name)
-        for i in range(a.n_sel.shape[0]):
-            n = int(a.n_sel[i])
-            assert torch.equal(a.sel_rows[i, :n], b.sel_rows[i, :n]), (t, i)
-        err = (a.out - b.out).abs().max().item()
-        assert err <= 1e-5 * max(1.0, a.out.abs().max().item()), (t, err)
-        assert (a.lse - b.lse).abs().max().item() <= 1e-5, t
+        for b in engs[1:]:
+            assert torch.equal(a.fire, b.fire), t
+            for name in ("n_sel", "n_sel_units", "sel_units", "unit_start", "unit_size", "reps"):
+                assert torch.equal(getattr(a, name), getattr(b, name)), (t, name)
+            for i in range(a.n_sel.shape[0]):
+                n = int(a.n_sel[i])
+                assert torch.equal(a.sel_rows[i, :n], b.sel_rows[i, :n]), (t, i)
+            err = (a.out - b.out).abs().max().item()
+            assert err <= 1e-5 * max(1.0, a.out.abs().max().item()), (t, err)
+            assert (a.lse - b.lse).abs().max().item() <= 1e-5, t
     assert fires > G * steps // 8
 
 
