@@ -314,6 +314,65 @@ def test_sparse_decode_attn_rows(dtype, odt, G, H, g, B, PR, W, nl, ls):
         np.testing.assert_allclose(to64(lse[grp, h * g:(h + 1) * g]), l, rtol=1e-5, atol=1e-5)
 
 
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_split_kv_merge_repeats_on_one_workspace(dtype):
+    """Split-KV attention keeps the chunk partials in the workspace between its
+    two launches: repeated eager calls and graph replays on one workspace all
+    write the output of a call with a fresh workspace (the output is poisoned
+    with NaN before each call)."""
+    L = _L()
+    G, H, g, B, PR, W, nl, ls = 2, 8, 4, 700, 3000, 64, 40, 60
+    S = G * H
+    gen = _gen(4242)
+    q = torch.randn(G, H * g, 128, generator=gen, device=DEV).to(dtype)
+    kp = torch.randn(S, PR, 128, generator=gen, device=DEV).mul(2).to(dtype)
+    vp = torch.randn(S, PR, 128, generator=gen, device=DEV).to(dtype)
+    kl = torch.randn(S, W, 128, generator=gen, device=DEV).to(dtype)
+    vl = torch.randn(S, W, 128, generator=gen, device=DEV).to(dtype)
+    rows = torch.randint(0, PR, (S, B), generator=gen, device=DEV, dtype=torch.int32)
+    nsel = torch.randint(0, B + 1, (S,), generator=gen, device=DEV, dtype=torch.int32)
+    nsel[3] = 0
+    wsb = L.sparse_decode_attn_rows_workspace_size(S, g, B, W)
+    assert wsb > 0, "the case must split the rows over several blocks"
+    ws = torch.empty(wsb, dtype=torch.uint8, device=DEV)
+    out = torch.empty(G, H * g, 128, dtype=torch.float32, device=DEV)
+    lse = torch.empty(G, H * g, dtype=torch.float32, device=DEV)
+
+    def call():
+        L.sparse_decode_attn_rows(q, H, kp, vp, rows, nsel, kl, vl, ls, nl, out, lse, workspace=ws)
+
+    results = []
+    for _ in range(3):
+        out.fill_(float("nan"))
+        lse.fill_(float("nan"))
+        call()
+        torch.cuda.synchronize()
+        results.append((out.clone(), lse.clone()))
+    # a fresh workspace gives the same result as the reused one
+    ref_out = torch.empty_like(out)
+    ref_lse = torch.empty_like(lse)
+    L.sparse_decode_attn_rows(q, H, kp, vp, rows, nsel, kl, vl, ls, nl, ref_out, ref_lse)
+    torch.cuda.synchronize()
+    assert not torch.isnan(ref_out).any()
+    for o, l in results:
+        assert torch.equal(o, ref_out) and torch.equal(l, ref_lse)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(graph, stream=side):
+            call()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        out.fill_(float("nan"))
+        lse.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref_out) and torch.equal(lse, ref_lse)
+
+
 def test_sparse_decode_attn_rows_clamps_list_entries():
     """Entries outside [0, pool_rows) are clamped into the pool by the kernel."""
     L = _L()
