@@ -13,6 +13,7 @@ from .louiskv_oracle import (
     kmeans_assign,
     kmeans_update,
     kmeans,
+    kmeans_finish,
     KMeansResult,
     clustering_cost,
     segment_mean,
@@ -29,7 +30,7 @@ from .decode_driver import PrefillState, GroupDecoder, prefill_state_from_kmeans
 
 __all__ = [
     "round_to_bf16", "round_to_f32", "squared_distances", "kmeans_assign",
-    "kmeans_update", "kmeans", "KMeansResult", "clustering_cost",
+    "kmeans_update", "kmeans", "kmeans_finish", "KMeansResult", "clustering_cost",
     "segment_mean", "page_units", "query_similarity", "boundary_fires", "stride_fires",
     "group_scores", "select_budget", "gather_units", "attention",
     "PrefillState", "GroupDecoder", "prefill_state_from_kmeans", "prefill_state_from_pages",

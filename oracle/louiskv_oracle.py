@@ -139,12 +139,21 @@ def kmeans(keys, init_idx, n_iters: int, bf16_operand: bool,
         if keep_history:
             hist.append(c.copy())
             costs.append(clustering_cost(k, z, c))
+    return kmeans_finish(z, c, hist, costs)
+
+
+def kmeans_finish(z, centroids, history=None, costs=None) -> KMeansResult:
+    """The cluster layout of a final assignment: member counts, CSR offsets of
+    each cluster and the token ids grouped by cluster (ascending inside a
+    cluster), the order in which the pool stores the prompt rows."""
+    z = np.asarray(z, dtype=np.int64)
+    c = np.asarray(centroids, dtype=F64)
     counts = np.bincount(z, minlength=c.shape[0])
     offsets = np.zeros(c.shape[0] + 1, dtype=np.int64)
     offsets[1:] = np.cumsum(counts)
     perm = np.argsort(z, kind="stable")
     return KMeansResult(z=z, centroids=c, counts=counts, offsets=offsets,
-                        perm=perm, history=hist, costs=costs)
+                        perm=perm, history=list(history or []), costs=list(costs or []))
 
 
 # ---------------------------------------------------------------------------

@@ -563,6 +563,55 @@ def pin_decode_per_head(orc):
         assert np.allclose(ra.out, rb.out, rtol=1e-10, atol=1e-12)
 
 
-DECODE_PINS = [pin_decode_dense_special_case, pin_decode_frozen_and_schedule, pin_decode_boundary_modes,
+def pin_prefill_pool_packing(orc):
+    """The unified pool after prefill (Section 4.2, Fig. 4, Algorithm 1's
+    prompt offload): each cluster is one contiguous run of pool rows holding
+    exactly the prompt tokens the final assignment gives it, in ascending
+    token order, for keys and values alike; the runs follow cluster order and
+    tile the prompt; a run's index vector is the mean of its rows.  A decode
+    step whose budget takes a strict subset of the clusters attends to
+    exactly the member tokens of the chosen clusters plus the window, checked
+    with torch SDPA over those tokens taken from the unpermuted prompt."""
+    rng = RNG(47)
+    h_kv, p, d, c, g = 2, 120, 8, 6, 2
+    pk = rng.standard_normal((h_kv, p, d)) * 2
+    pv = rng.standard_normal((h_kv, p, d))
+    res = [orc.kmeans(pk[h], rng.permutation(p)[:c], n_iters=4, bf16_operand=False) for h in range(h_kv)]
+    st = orc.prefill_state_from_kmeans(pk, pv, res)
+    for h in range(h_kv):
+        z = np.asarray(res[h].z)
+        start = 0
+        for cl in range(c):
+            members = np.flatnonzero(z == cl)
+            n = members.size
+            assert int(st.unit_start[h][cl]) == start and int(st.unit_size[h][cl]) == n, (h, cl)
+            assert np.array_equal(np.asarray(st.k_pool[h])[start:start + n], pk[h][members])
+            assert np.array_equal(np.asarray(st.v_pool[h])[start:start + n], pv[h][members])
+            if n:
+                assert np.allclose(st.reps[h][cl], pk[h][members].mean(0), rtol=1e-6, atol=1e-6)
+            start += n
+        assert start == p
+    # a partial selection attends to the member tokens of the chosen clusters
+    gk = rng.standard_normal((3, h_kv, d)) * 2
+    gv = rng.standard_normal((3, h_kv, d))
+    q = rng.standard_normal((3, h_kv * g, d))
+    dec = orc.GroupDecoder(st, h_kv * g, budget=p // 2, window=16, seg_len=4, tau=1.5, mode="prev")
+    s = 1 / np.sqrt(d)
+    for t in range(3):
+        rec = dec.step(q[t], gk[t], gv[t])
+        assert all(0 < n < p for n in rec.n_sel)
+        for h in range(h_kv):
+            toks = np.flatnonzero(np.isin(np.asarray(res[h].z), rec.sel_units[h]))
+            assert toks.size == rec.n_sel[h]
+            kk = torch.from_numpy(np.concatenate([pk[h][toks], gk[:t + 1, h]]))
+            vv = torch.from_numpy(np.concatenate([pv[h][toks], gv[:t + 1, h]]))
+            qq = torch.from_numpy(q[t, h * g:(h + 1) * g])
+            ref = torch.nn.functional.scaled_dot_product_attention(
+                qq[None, :, None, :], kk[None, None].expand(1, g, -1, -1),
+                vv[None, None].expand(1, g, -1, -1), scale=s)[0, :, 0].numpy()
+            assert np.allclose(rec.out[h * g:(h + 1) * g], ref, rtol=1e-10, atol=1e-12)
+
+
+DECODE_PINS = [pin_prefill_pool_packing, pin_decode_dense_special_case, pin_decode_frozen_and_schedule, pin_decode_boundary_modes,
                pin_decode_boundary_segments, pin_page_units, pin_decode_stride_trigger, pin_decode_per_head]
 ALL_PINS = ALL_PINS + DECODE_PINS

@@ -14,7 +14,7 @@ import torch
 sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
 import oracle  # noqa: E402
 import synth  # noqa: E402
-from parity_utils import to64  # noqa: E402
+from parity_utils import check_kmeans_trajectory, gpu_kmeans_states, report, to64  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -58,6 +58,15 @@ def test_c_caller_matches_python_binding(tmp_path):
     assert np.array_equal(c_assign, eng.assign.cpu().numpy())
     assert np.array_equal(c_reps, eng.reps.cpu().numpy())
     assert np.array_equal(c_out, torch.stack(outs).cpu().numpy())
-    # and the clustering is the oracle's (up to excused near-ties)
-    res = oracle.kmeans(to64(data.prompt_keys[0]), data.init_idx[0].cpu().numpy(), wl.n_iters, True)
-    assert int((c_assign[0] != res.z).sum()) <= 2
+    # and the clustering is the oracle's: equal, or a run whose every
+    # iteration is an exact argmin and exact means up to excused near-ties
+    from paper_2510_11292_amd import louiskv
+    states = gpu_kmeans_states(louiskv, data.prompt_keys, data.init_idx, C)
+    excused = 0
+    for s in range(S):
+        k64, init = to64(data.prompt_keys[s]), data.init_idx[s].cpu().numpy()
+        res = oracle.kmeans(k64, init, wl.n_iters, True)
+        if not np.array_equal(c_assign[s], res.z):
+            excused += check_kmeans_trajectory(k64, init, wl.n_iters, True, lambda it: tuple(x[s] for x in states(it)))
+    report("C caller k-means", dict(excused=excused), bound=max(2, S * N * wl.n_iters // 10000),
+           of="assignment near-ties")

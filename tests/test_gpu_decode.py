@@ -9,7 +9,8 @@ import torch
 sys.path.insert(0, os.path.dirname(__file__))
 import oracle  # noqa: E402
 import synth  # noqa: E402
-from parity_utils import REL, check_rows_rel, selection_matches, to64, to_np  # noqa: E402
+from parity_utils import (REL, check_prefill_against_state, check_rows_rel, gpu_kmeans_states,  # noqa: E402
+                          oracle_prefill_state, report, selection_matches, to64, to_np)
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -436,18 +437,29 @@ def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, seg
     C = cfg.n_clusters     # prompt units: clusters, or pages with index="pages"
     per_head = cfg.selection == "per_head"
     NL = H * g if per_head else H      # selection lists per group
+    # the oracle's own prefill (k-means, then the pool packed cluster by
+    # cluster, or the page index); the GPU's unit table and pool must equal it
     decs = []
+    k_excused = adopted = 0
+    bf16 = data.prompt_keys.dtype == torch.bfloat16
+    states = gpu_kmeans_states(_L(), data.prompt_keys, data.init_idx, C) if cfg.index == "clusters" else None
     for gi in range(n_groups):
         sl = slice(gi * H, (gi + 1) * H)
-        st = oracle.PrefillState(
-            reps=list(to64(eng.reps[sl, :C])),
-            unit_start=list(to_np(eng.unit_start[sl, :C]).astype(np.int64)),
-            unit_size=list(to_np(eng.unit_size[sl, :C]).astype(np.int64)),
-            k_pool=list(to64(eng.k_pool[sl, :wl.prompt_len])),
-            v_pool=list(to64(eng.v_pool[sl, :wl.prompt_len])))
+        k64, v64 = to64(data.prompt_keys[sl]), to64(data.prompt_values[sl])
+        if cfg.index == "pages":
+            st = oracle.prefill_state_from_pages(k64, v64, cfg.page_len)
+        else:
+            st, ex, ad = oracle_prefill_state(k64, v64, to_np(data.init_idx[sl]), wl.n_iters, bf16,
+                                              to_np(eng.assign[sl]), to64(eng.reps[sl, :C]), states,
+                                              list(range(sl.start, sl.stop)))
+            k_excused += ex
+            adopted += ad
+        check_prefill_against_state(eng.reps[sl], eng.unit_start[sl], eng.unit_size[sl], eng.k_pool[sl],
+                                    eng.v_pool[sl], st, wl.prompt_len)
         decs.append(oracle.GroupDecoder(st, wl.n_q_heads, wl.budget, wl.window, wl.seg_len, wl.tau,
                                         "prev" if mode == 0 else "anchor", segments=segments,
                                         trigger=cfg.trigger, stride=cfg.stride, selection=cfg.selection))
+    assert k_excused <= max(2, n_groups * H * wl.prompt_len * wl.n_iters // 10000), k_excused
     stats = dict(fires=0, excused=0, evictions=0, sizes=set(), fetched=0, selected=0)
     if layer_by_layer and pool_on_host:
         _require_interior_host_mapping(eng.k_pool, wl.n_kv_heads)
@@ -508,6 +520,10 @@ def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, seg
                 assert (stt[:, 0] == dec.n_units()).all(), (t, stt[:, 0], dec.n_units())
                 assert (stt[:, 1] == dec.local[0][0][0]).all(), (t, stt[:, 1], dec.local[0][0][0])
                 assert (stt[:, 4] == 0).all()
+    stats["kmeans_excused"] = k_excused
+    stats["kmeans_adopted"] = adopted
+    report(f"decode loop {wl.name} groups={n_groups} steps={steps}", stats,
+           bound=max(3, stats["fires"] // 100), of="boundary and selection near-ties")
     return stats
 
 

@@ -27,7 +27,7 @@ sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
 
 import oracle  # noqa: E402
 import synth  # noqa: E402
-from parity_utils import REL, check_assignment, selection_matches, to64, to_np  # noqa: E402
+from parity_utils import REL, check_assignment, report, selection_matches, to64, to_np  # noqa: E402
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -215,6 +215,8 @@ def test_decode_full_shape_sampled(name, retrieval):
                 last_fire[gi] = t
     assert stats["fires"] > 0
     assert stats["checked"] >= 2 * len(steps)
+    report(f"full-shape decode {name}", stats, bound=max(3, stats["fires"] // 100),
+           of="boundary and selection near-ties")
 
 
 def _check_step_boundary(eng, data, wl, t, gi, q_ref_before, before, fires, stats):
@@ -322,6 +324,8 @@ def test_decode_full_shape_boundary_segments(name):
     assert (st[:, 4] == 0).all()
     assert stats["fires"] > 0 and stats["evictions"] > 0
     assert stats["checked"] >= 2 * len(steps)
+    report(f"full-shape boundary-segment decode {name}", stats, bound=max(3, stats["fires"] // 100),
+           of="boundary and selection near-ties")
 
 
 @pytest.mark.parametrize("name", ["li-so-32k", "host-131k"])

@@ -15,6 +15,7 @@ from oracle_pins import ALL_PINS  # noqa: E402
 
 F64 = np.float64
 ORIG = {n: getattr(L, n) for n in ("kmeans_update", "group_scores", "attention")}
+ORIG_PREFILL = DD.prefill_state_from_kmeans
 
 
 def _sqdist_plus(keys, centroids):
@@ -139,6 +140,13 @@ def _head_scores_group(q_t, head, reps, scale):
     return L.group_scores(np.asarray(q_t, F64)[base:base + 2], reps, scale)
 
 
+def _prefill_token_order(prompt_keys, prompt_values, results):
+    st = ORIG_PREFILL(prompt_keys, prompt_values, results)
+    st.k_pool = [np.asarray(k, F64) for k in prompt_keys]
+    st.v_pool = [np.asarray(v, F64) for v in prompt_values]
+    return st
+
+
 MUTATIONS = {
     "distance_cross_term_sign": ("squared_distances", _sqdist_plus),
     "distance_dropped_centroid_norm": ("squared_distances", _sqdist_no_cnorm),
@@ -162,6 +170,7 @@ MUTATIONS = {
     "pages_drop_ragged_tail": ("page_units", _pages_drop_tail),
     "per_head_uses_first_head": ("head_scores", _head_scores_first_head),
     "per_head_uses_group_average": ("head_scores", _head_scores_group),
+    "pool_left_in_token_order": ("prefill_state_from_kmeans", _prefill_token_order),
 }
 
 
