@@ -31,7 +31,9 @@
  * --------------------------------
  * Ownership   The caller owns every buffer, including workspaces; the library
  *             never allocates or frees memory and keeps no state except a
- *             thread-local last-error string.
+ *             thread-local last-error string, and the static device array of
+ *             the one allocation-free call
+ *             (louiskv_sparse_decode_attn_rows_noalloc).
  * Pointers    Device pointers, except KV pools that the caller declares host
  *             resident (pool_on_host = 1): those must be pinned, device-mapped
  *             host memory (hipHostMalloc), which kernels read and write
@@ -424,6 +426,39 @@ int louiskv_sparse_decode_attn_rows(const void* q, int32_t dtype, int64_t n_slic
                                     int32_t window, int32_t local_start, int32_t n_local,
                                     void* out, int32_t out_dtype, float* lse_out,
                                     void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * louiskv_sparse_decode_attn_rows for callers that cannot allocate: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Arguments, arithmetic and outputs are those of
+ * louiskv_sparse_decode_attn_rows (bit for bit), without the workspace: the
+ * split-KV partials go to a static device array of
+ * LOUISKV_NOALLOC_SCRATCH_BYTES that every GPU the library runs on holds
+ * until the process ends.  The call allocates nothing; its first call on a
+ * device looks up that device's copy of the array (hipGetSymbolAddress).
+ *
+ * Size limit  The launch's partials, louiskv_sparse_decode_attn_rows_workspace_size()
+ *             of the same arguments, must fit LOUISKV_NOALLOC_SCRATCH_BYTES;
+ *             larger launches return LOUISKV_ERR_WORKSPACE before anything is
+ *             launched.  (A launch that fills the chip with one block per
+ *             slice needs no partials at all.)
+ * Sharing     Every call on one GPU uses the same array, which keeps the last
+ *             call's contents (the kernels write every partial they read, so
+ *             nothing needs clearing).  Calls that overlap on one GPU (two
+ *             streams, two threads, two captured graphs replayed together)
+ *             race on it: serialise them.
+ */
+#define LOUISKV_NOALLOC_SCRATCH_BYTES (8u << 20)
+
+int louiskv_sparse_decode_attn_rows_noalloc(const void* q, int32_t dtype, int64_t n_slices,
+                                            int32_t n_kv_heads, int32_t group_size, int32_t d,
+                                            float scale, const void* k_pool, const void* v_pool,
+                                            int64_t pool_rows, const int32_t* sel_rows,
+                                            const int32_t* n_sel, int32_t budget,
+                                            const void* k_local, const void* v_local,
+                                            int32_t window, int32_t local_start, int32_t n_local,
+                                            void* out, int32_t out_dtype, float* lse_out,
+                                            void* stream);
 
 /*
  * louiskv_boundary_check and louiskv_segment_output (fixed segments) of one

@@ -3,6 +3,8 @@
 // (Appendix B; Algorithm 1 Retrieve) and sparse decode attention (Section 3.1).
 #include <algorithm>
 
+#include <mutex>
+
 #include "common.h"
 
 namespace louiskv {
@@ -2011,6 +2013,67 @@ extern "C" int louiskv_sparse_decode_attn_rows(const void* q, int32_t dtype, int
   return sparse_decode_attn(q, dtype, n_slices, n_kv_heads, group_size, d, scale, k_pool, v_pool, n_sel, budget,
                             sel_rows, pool_rows, k_local, v_local, window, local_start, n_local, out, out_dtype,
                             lse_out, workspace, workspace_bytes, stream);
+}
+
+// ---------------------------------------------------------------------------
+// Allocation-free attention over listed pool rows.  The split-KV partials live
+// in a static device array instead of a caller workspace.  The array's name
+// is only a host-side stand-in: host code uses the device address that
+// hipGetSymbolAddress returns, looked up once per device.
+
+static __device__ __align__(256) float scratch[LOUISKV_NOALLOC_SCRATCH_BYTES / sizeof(float)];
+
+namespace louiskv {
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices] = {};
+
+// The current device's copy of `scratch`.
+int scratch_on_current_device(void** addr) {
+  int dev = -1;
+  LKV_CHECK_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(LOUISKV_ERR_UNSUPPORTED, "device %d: the allocation-free calls serve devices 0..%d", dev,
+                kMaxDevices - 1);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* p = nullptr;
+    LKV_CHECK_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(LOUISKV_ERR_HIP, "hipGetSymbolAddress gave no address for the scratch array");
+    g_scratch_addr[dev] = p;
+  }
+  *addr = g_scratch_addr[dev];
+  return LOUISKV_OK;
+}
+
+}  // namespace
+}  // namespace louiskv
+
+extern "C" int louiskv_sparse_decode_attn_rows_noalloc(const void* q, int32_t dtype, int64_t n_slices,
+                                                       int32_t n_kv_heads, int32_t group_size, int32_t d,
+                                                       float scale, const void* k_pool, const void* v_pool,
+                                                       int64_t pool_rows, const int32_t* sel_rows,
+                                                       const int32_t* n_sel, int32_t budget, const void* k_local,
+                                                       const void* v_local, int32_t window, int32_t local_start,
+                                                       int32_t n_local, void* out, int32_t out_dtype,
+                                                       float* lse_out, void* stream) {
+  if (!sel_rows) return fail(LOUISKV_ERR_NULL, "sel_rows is required");
+  if (n_slices >= 1 && group_size >= 1 && budget >= 0 && window >= 0) {
+    const size_t need = attn_ws_bytes(n_slices, group_size, budget, window, true);
+    if (need > LOUISKV_NOALLOC_SCRATCH_BYTES)
+      return fail(LOUISKV_ERR_WORKSPACE,
+                  "the allocation-free call holds at most %zu bytes of partials and this launch needs %zu; "
+                  "use louiskv_sparse_decode_attn_rows with a workspace",
+                  (size_t)LOUISKV_NOALLOC_SCRATCH_BYTES, need);
+  }
+  void* ws = nullptr;
+  const int st = scratch_on_current_device(&ws);
+  if (st) return st;
+  return sparse_decode_attn(q, dtype, n_slices, n_kv_heads, group_size, d, scale, k_pool, v_pool, n_sel, budget,
+                            sel_rows, pool_rows, k_local, v_local, window, local_start, n_local, out, out_dtype,
+                            lse_out, ws, LOUISKV_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 extern "C" int louiskv_retrieve_rows_per_head(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads,

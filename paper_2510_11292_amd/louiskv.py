@@ -64,6 +64,10 @@ _SIGS = {
         _P, _I32, _I64, _I32, _I32, _I32, _F,
         _P, _P, _I64, _P, _P, _I32, _P, _P, _I32, _I32, _I32,
         _P, _I32, _P, _P, _SZ, _P]),
+    "louiskv_sparse_decode_attn_rows_noalloc": (ctypes.c_int, [
+        _P, _I32, _I64, _I32, _I32, _I32, _F,
+        _P, _P, _I64, _P, _P, _I32, _P, _P, _I32, _I32, _I32,
+        _P, _I32, _P, _P]),
     "louiskv_fire_every": (ctypes.c_int, [_P, _I64, _I32, _I32, _P]),
     "louiskv_decode_prologue": (ctypes.c_int, [
         _P, _P, _I32, _I64, _I32, _I32, _D, _I32, _I32, _P, _P,
@@ -348,6 +352,26 @@ def sparse_decode_attn_rows(q, n_kv_heads: int, k_pool, v_pool, sel_rows, n_sel,
         _ptr(q), _dtype_code(q), s, n_kv_heads, gs, d, float(sc), _ptr(k_pool), _ptr(v_pool), k_pool.shape[1],
         _ptr(sel_rows), _ptr(n_sel), budget, _ptr(k_local), _ptr(v_local), window, local_start, n_local,
         _ptr(out), _dtype_code(out), _ptr(lse_out), _ptr(ws), wsb, _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 8 << 20   # LOUISKV_NOALLOC_SCRATCH_BYTES
+
+
+def sparse_decode_attn_rows_noalloc(q, n_kv_heads: int, k_pool, v_pool, sel_rows, n_sel, k_local, v_local,
+                                    local_start: int, n_local: int, out, lse_out=None,
+                                    scale: Optional[float] = None, stream=None):
+    """sparse_decode_attn_rows without a workspace: the split-KV partials use
+    the library's static device array (at most NOALLOC_SCRATCH_BYTES)."""
+    g, hq, d = q.shape
+    s = n_sel.shape[0]
+    gs = hq // n_kv_heads
+    budget = sel_rows.shape[1]
+    window = k_local.shape[1] if k_local is not None else 0
+    sc = (1.0 / d ** 0.5) if scale is None else scale
+    _check(load_library().louiskv_sparse_decode_attn_rows_noalloc(
+        _ptr(q), _dtype_code(q), s, n_kv_heads, gs, d, float(sc), _ptr(k_pool), _ptr(v_pool), k_pool.shape[1],
+        _ptr(sel_rows), _ptr(n_sel), budget, _ptr(k_local), _ptr(v_local), window, local_start, n_local,
+        _ptr(out), _dtype_code(out), _ptr(lse_out), _stream(stream)))
 
 
 def decode_prologue(q, q_ref, tau: float, mode: int, first_step: bool, fire, r_out, k_new, v_new, k_local, v_local,
