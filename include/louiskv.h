@@ -428,6 +428,57 @@ int louiskv_sparse_decode_attn_rows(const void* q, int32_t dtype, int64_t n_slic
                                     void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * One decode step of Algorithm 1 for n_groups (sequence, layer) groups, with
+ * fixed output segments and the KV pool in device memory, in two launches:
+ * the boundary test (Section 4.1 equation for r_t), the decode-stage
+ * store_cache (Section 4.2: window append, oldest-segment eviction), the
+ * group-consistent retrieval of the groups that fired (Appendix B scores,
+ * Section 3.1 budget, Algorithm 1 Retrieve; KV_critical kept as the list of
+ * selected pool rows) and the attention over [KV_critical : KV_local]
+ * (Section 3.1), current token included.  Meant for few groups per call (one
+ * layer of a model at a time): every kernel spreads a slice over many
+ * blocks, and the blocks of a slice hand over through the workspace (the
+ * last one to finish a phase completes it) instead of through extra
+ * launches.
+ *
+ * Results equal, bit for bit, louiskv_decode_prologue + louiskv_retrieve_rows
+ * + louiskv_sparse_decode_attn_rows (the selected units, rows, scores, r,
+ * decisions, reference queries, window, unit table and pool), except the
+ * attention output and lse, which split each slice's rows differently
+ * (float32 summation order; same tolerance as those calls).
+ *
+ * Arguments are those of the three calls: q, q_ref, tau, mode, r_out,
+ * fire_out as louiskv_boundary_check (the first step is step == 0); k_new,
+ * v_new, k_local, v_local, window, seg_len, reps, unit_start, unit_size,
+ * units_cap, n_clusters, k_pool, v_pool, pool_rows, prompt_len as
+ * louiskv_segment_output (device pools only); budget, sel_units,
+ * n_sel_units, n_sel, sel_rows [n_slices][max(budget, 1)], scores_out
+ * (nullable) as louiskv_retrieve_rows; out, out_dtype, lse_out (nullable) as
+ * louiskv_sparse_decode_attn_rows.  n_slices = n_groups * n_kv_heads and the
+ * group size n_q_heads / n_kv_heads is 1, 2, 4 or 8.  The units scored at
+ * step t are the clusters and the segments evicted before step t.
+ *
+ * workspace  louiskv_decode_step_workspace_size() bytes.  It must be zero
+ *            before its first use (for example allocated zeroed); every call
+ *            leaves its arrival counters at zero again, so it is reused
+ *            without clearing.  Calls that share it must not overlap.
+ */
+size_t louiskv_decode_step_workspace_size(int64_t n_slices, int32_t dtype, int32_t group_size,
+                                          int32_t units_cap, int32_t budget, int32_t window);
+
+int louiskv_decode_step(const void* q, void* q_ref, int32_t dtype, int64_t n_groups,
+                        int32_t n_q_heads, int32_t n_kv_heads, int32_t d, double tau,
+                        int32_t mode, int32_t step, double* r_out, uint8_t* fire_out,
+                        const void* k_new, const void* v_new, void* k_local, void* v_local,
+                        int32_t window, int32_t seg_len, float* reps, int32_t* unit_start,
+                        int32_t* unit_size, int32_t units_cap, int32_t n_clusters,
+                        void* k_pool, void* v_pool, int64_t pool_rows, int32_t prompt_len,
+                        int32_t budget, int32_t* sel_units, int32_t* n_sel_units,
+                        int32_t* n_sel, int32_t* sel_rows, double* scores_out, void* out,
+                        int32_t out_dtype, float* lse_out, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+/*
  * louiskv_sparse_decode_attn_rows for callers that cannot allocate: code under
  * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
  * Arguments, arithmetic and outputs are those of

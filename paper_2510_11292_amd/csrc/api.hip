@@ -1,6 +1,9 @@
 // Status strings, the thread-local last-error text, and the local-window rule.
 #include <stdarg.h>
 
+#include <mutex>
+#include <unordered_map>
+
 #include "common.h"
 
 namespace louiskv {
@@ -37,6 +40,42 @@ int device_view_of_host_pool(const void* p, void** dev) {
                 "pool_on_host=1 needs pinned, device-mapped host memory (hipHostMalloc); %p is not", p);
   }
   *dev = attr.devicePointer;
+  return LOUISKV_OK;
+}
+
+namespace {
+std::mutex g_lds_mu;
+std::unordered_map<const void*, size_t> g_static_lds;   // per kernel
+int g_max_lds[64] = {};                                  // per device
+}  // namespace
+
+int check_lds(const void* kernel, size_t dynamic_lds) {
+  int dev = 0;
+  LKV_CHECK_HIP(hipGetDevice(&dev));
+  size_t stat = 0;
+  int limit = 0;
+  {
+    std::lock_guard<std::mutex> lock(g_lds_mu);
+    auto it = g_static_lds.find(kernel);
+    if (it == g_static_lds.end()) {
+      hipFuncAttributes attr;
+      LKV_CHECK_HIP(hipFuncGetAttributes(&attr, kernel));
+      it = g_static_lds.emplace(kernel, attr.sharedSizeBytes).first;
+    }
+    stat = it->second;
+    if (dev >= 0 && dev < 64) {
+      if (!g_max_lds[dev]) {
+        int a = 0, b = 0;
+        LKV_CHECK_HIP(hipDeviceGetAttribute(&a, hipDeviceAttributeMaxSharedMemoryPerBlock, dev));
+        LKV_CHECK_HIP(hipDeviceGetAttribute(&b, hipDeviceAttributeSharedMemPerBlockOptin, dev));
+        g_max_lds[dev] = std::max(a, b);
+      }
+      limit = g_max_lds[dev];
+    }
+  }
+  if (limit <= 0 || stat + dynamic_lds > (size_t)limit)
+    return fail(LOUISKV_ERR_UNSUPPORTED, "launch needs %zu bytes of LDS (%zu static + %zu dynamic), the device has %d",
+                stat + dynamic_lds, stat, dynamic_lds, limit);
   return LOUISKV_OK;
 }
 

@@ -33,6 +33,11 @@ int device_view_of_host_pool(const void* p, void** dev);
 
 #define LKV_CHECK_LAUNCH() LKV_CHECK_HIP(hipGetLastError())
 
+// LOUISKV_OK when a launch of `kernel` with `dynamic_lds` bytes of dynamic
+// LDS fits the current device's LDS per workgroup (its static LDS counted),
+// else LOUISKV_ERR_UNSUPPORTED: such a launch is refused, never attempted.
+int check_lds(const void* kernel, size_t dynamic_lds);
+
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // Carves aligned sub-buffers out of a caller-owned workspace.

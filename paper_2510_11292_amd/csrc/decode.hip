@@ -52,19 +52,20 @@ __device__ __forceinline__ void load_row8(const float* p, float* x) {
 
 constexpr int kBndHeadsPerPass = 32;   // 16 lane groups x 2 heads, all loads issued together
 
-// One block of 4 waves per group.  16 lanes per head (lane sub holds dims
-// 8*sub..+7), each 16-lane group takes two heads per pass; the float64 dot
-// product and norms of a head are DPP row sums.  Cosines in float64.
+// r of group g (Section 4.1): the mean over the group's n_heads query heads
+// of cos(q_ref, q), in float64; NaN at the first step.  Threads 0..255 load:
+// 16 lanes per head (lane sub holds dims 8*sub..+7), each 16-lane group takes
+// two heads per pass, the dot product and norms of a head are DPP row sums.
+// Every thread of the block must call it (one barrier); every thread gets r,
+// summed in the same order, so blocks that test the same group agree bit
+// for bit.
 template <class T>
-__device__ __forceinline__ void boundary_group(const T* __restrict__ q, T* __restrict__ q_ref, int n_heads,
-                                               double tau, int mode, int first, double* __restrict__ r_out,
-                                               uint8_t* __restrict__ fire_out, int g) {
-  __shared__ double s_part[16];
-  __shared__ int s_fire;
+__device__ __forceinline__ double boundary_r(const T* __restrict__ q, const T* __restrict__ q_ref, int n_heads,
+                                             int first, int64_t g, double* s_part /* [16] in LDS */) {
   const int tid = threadIdx.x, sub = tid & 15, hg = tid >> 4;
   const size_t base = (size_t)g * n_heads * kHeadDim;
   double acc = 0.0;
-  if (!first) {
+  if (!first && tid < 256) {
     for (int p = 0; p < n_heads; p += kBndHeadsPerPass) {
       float a[2][8], b[2][8];
       bool ok[2];
@@ -92,23 +93,32 @@ __device__ __forceinline__ void boundary_group(const T* __restrict__ q, T* __res
       }
     }
   }
-  if (sub == 0) s_part[hg] = acc;
+  if (tid < 256 && sub == 0) s_part[hg] = acc;
   __syncthreads();
+  if (first) return __builtin_nan("");
+  double r = 0.0;
+  for (int i = 0; i < 16; ++i) r += s_part[i];
+  return r / (double)n_heads;
+}
+
+// One block of 4 waves per group: r, the decision (first step, or r < tau),
+// and the reference query's update (every step in PREV mode, at a fire in
+// ANCHOR mode).
+template <class T>
+__device__ __forceinline__ void boundary_group(const T* __restrict__ q, T* __restrict__ q_ref, int n_heads,
+                                               double tau, int mode, int first, double* __restrict__ r_out,
+                                               uint8_t* __restrict__ fire_out, int g) {
+  __shared__ double s_part[16];
+  const int tid = threadIdx.x;
+  const size_t base = (size_t)g * n_heads * kHeadDim;
+  const double r = boundary_r(q, q_ref, n_heads, first, g, s_part);
+  const int fire = first ? 1 : (r < tau ? 1 : 0);
   if (tid == 0) {
-    double r = __builtin_nan("");
-    int fire = 1;
-    if (!first) {
-      r = 0.0;
-      for (int i = 0; i < 16; ++i) r += s_part[i];
-      r /= (double)n_heads;
-      fire = r < tau ? 1 : 0;
-    }
     if (r_out) r_out[g] = r;
     fire_out[g] = (uint8_t)fire;
-    s_fire = fire;
   }
-  __syncthreads();
-  if (mode == LOUISKV_REF_PREV || s_fire) {
+  __syncthreads();   // every thread has read q_ref before it is rewritten
+  if (mode == LOUISKV_REF_PREV || fire) {
     const int n = n_heads * kHeadDim;
     for (int i = tid; i < n; i += 256) q_ref[base + i] = q[base + i];
   }
@@ -462,6 +472,368 @@ int logit_parts(int64_t n_slices, int n_units) {
   return parts;
 }
 
+// A logit of the selection workspace.  kShared: written by other blocks of
+// the same launch, so read coherently at device scope (the per-XCD L2 may
+// hold an older copy of the line).
+template <bool kShared>
+__device__ __forceinline__ double load_logit(const double* p) {
+  if constexpr (kShared)
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else
+    return *p;
+}
+
+// The selection of one fired slice once its logits l_ju (lg, [unit][G]) and
+// their per-head maxima M_j (s_m) are known, with the unit sizes in s_size:
+//  pass 2  e_ju = exp(l_ju - M_j) and Z_j = sum_u e_ju (kSelThreads threads);
+//  pass 3  A_u = (1/g) sum_j e_ju / Z_j and the sort keys;
+//  sort    64-key chunks in registers for merge distances below 64 (no
+//          barrier), LDS steps with a barrier for the longer ones;
+//  then the prefix stop under the budget, the selected unit list and the
+//  pool-row list.  kShared: the logits come from other blocks of the launch;
+//  they are read coherently and the exponentials are recomputed in pass 3
+//  instead of written back (the results are the same, bit for bit).
+template <int G, bool kShared>
+__device__ __forceinline__ void select_after_max(double* __restrict__ lg, const double* s_m, int n_units, int n_pad,
+                                                 int64_t s, int64_t ps, int units_cap, int budget,
+                                                 const int32_t* __restrict__ unit_start,
+                                                 int32_t* __restrict__ sel_units, int32_t* __restrict__ n_sel_units,
+                                                 int32_t* __restrict__ n_sel, int32_t* __restrict__ row_ws,
+                                                 double* __restrict__ scores_out, uint64_t* s_key, int* s_size,
+                                                 int* s_incl) {
+  __shared__ double s_rz[G][kSelWaves];
+  __shared__ double s_z[G];
+  __shared__ int s_ntake;
+  __shared__ int s_wsum[kSelWaves];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  // pass 2: exponentials and their sums per head.  Up to kRegUnits units per
+  // thread the logits are loaded in one batch and their exponentials stay in
+  // registers for pass 3; beyond that they are kept in the logit workspace
+  // (recomputed in pass 3 when other blocks wrote them).  Either way each
+  // thread sums its units in increasing order.
+  constexpr int kRegUnits = 4;
+  const bool in_regs = n_units <= kRegUnits * kSelThreads;
+  double ev[kRegUnits][G];
+  double zs[G];
+#pragma unroll
+  for (int j = 0; j < G; ++j) zs[j] = 0.0;
+  if (in_regs) {
+#pragma unroll
+    for (int i = 0; i < kRegUnits; ++i) {
+      const int u = tid + i * kSelThreads;
+#pragma unroll
+      for (int j = 0; j < G; ++j) ev[i][j] = u < n_units ? load_logit<kShared>(lg + (size_t)u * G + j) : 0.0;
+    }
+#pragma unroll
+    for (int i = 0; i < kRegUnits; ++i) {
+      if (tid + i * kSelThreads < n_units) {
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+          ev[i][j] = exp(ev[i][j] - s_m[j]);
+          zs[j] += ev[i][j];
+        }
+      }
+    }
+  } else {
+    for (int u = tid; u < n_units; u += kSelThreads) {
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        const double e = exp(load_logit<kShared>(lg + (size_t)u * G + j) - s_m[j]);
+        if (!kShared) lg[(size_t)u * G + j] = e;
+        zs[j] += e;
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    const double z = wave_sum(zs[j]);
+    if (lane == 0) s_rz[j][w] = z;
+  }
+  __syncthreads();
+  if (tid < G) {
+    double z = 0.0;
+    for (int q2 = 0; q2 < kSelWaves; ++q2) z += s_rz[tid][q2];
+    s_z[tid] = z;
+  }
+  __syncthreads();
+
+  // pass 3: averaged probabilities and sort keys (padding keys 0 rank last)
+  if (in_regs) {
+#pragma unroll
+    for (int i = 0; i < kRegUnits; ++i) {
+      const int u = tid + i * kSelThreads;
+      if (u < n_pad) {
+        uint64_t key = 0;
+        if (u < n_units) {
+          double a = 0.0;
+#pragma unroll
+          for (int j = 0; j < G; ++j) a += ev[i][j] / s_z[j];
+          a /= (double)G;
+          key = unit_key(a, u);
+          if (scores_out) scores_out[(size_t)s * units_cap + u] = a;
+        }
+        s_key[u] = key;
+      }
+    }
+  } else {
+    for (int u = tid; u < n_pad; u += kSelThreads) {
+      uint64_t key = 0;
+      if (u < n_units) {
+        double a = 0.0;
+#pragma unroll
+        for (int j = 0; j < G; ++j)
+          a += (kShared ? exp(load_logit<kShared>(lg + (size_t)u * G + j) - s_m[j]) : lg[(size_t)u * G + j]) / s_z[j];
+        a /= (double)G;
+        key = unit_key(a, u);
+        if (scores_out) scores_out[(size_t)s * units_cap + u] = a;
+      }
+      s_key[u] = key;
+    }
+  }
+  __syncthreads();
+
+  // The prefix stop (Section 3.1 budget; units taken in rank order until the
+  // next one does not fit) by radix selection: the boundary unit is the first
+  // one in rank order whose size exceeds what the units ranked above it leave
+  // of the budget.  Keys are distinct, so 8-bit digits from the top narrow
+  // the candidates to the bucket in which the token count of the higher keys
+  // crosses the remaining budget, until that bucket holds one unit; every
+  // unit with a higher key is taken.  Then only the taken units are sorted.
+  // Histograms per pair of waves: a unit adds (size << 16) + 1 to its digit's
+  // entry, so one 64-bit word counts tokens (bits 16..) and units (bits
+  // 0..15; at most kMaxUnits per slice), and LDS atomics conflict only inside
+  // a pair.  Two sets alternate between passes, so a pass clears the other
+  // set while its own is scanned (2 x 4 x 256 words: 16 KiB of LDS).  Leading bytes that every key shares (the sign and
+  // high exponent bits of the scores) are skipped: the search starts at the
+  // first byte where the keys' OR and AND differ.
+  constexpr int kHists = kSelWaves / 2;
+  __shared__ uint64_t s_hist[2][kHists][256];
+  __shared__ uint64_t s_or[kSelWaves], s_and[kSelWaves];
+  __shared__ uint64_t s_prefix, s_thresh;
+  __shared__ int64_t s_rem;
+  __shared__ int s_pbits, s_state, s_nsel_units;   // state: 0 searching, 1 boundary found, 2 every unit fits
+  {
+    uint64_t ko = 0, ka = ~0ull;
+    for (int u = tid; u < n_units; u += kSelThreads) {
+      ko |= s_key[u];
+      ka &= s_key[u];
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      ko |= __shfl_xor(ko, o, kWave);
+      ka &= __shfl_xor(ka, o, kWave);
+    }
+    if (lane == 0) {
+      s_or[w] = ko;
+      s_and[w] = ka;
+    }
+  }
+  for (int i = tid; i < 2 * kHists * 256; i += kSelThreads) (&s_hist[0][0][0])[i] = 0;
+  __syncthreads();
+  if (tid == 0) {
+    uint64_t ko = 0, ka = ~0ull;
+    for (int q2 = 0; q2 < kSelWaves; ++q2) {
+      ko |= s_or[q2];
+      ka &= s_and[q2];
+    }
+    const uint64_t diff = ko ^ ka;          // bits where the keys differ
+    const int lead = diff ? __builtin_clzll(diff) / 8 * 8 : 56;   // whole shared bytes
+    s_pbits = lead;
+    s_prefix = lead ? (ko >> (64 - lead)) : 0;
+    s_rem = budget;
+    s_state = 0;
+    s_nsel_units = 0;
+  }
+  __syncthreads();
+  int set = 0;
+  while (s_state == 0) {
+    const int pbits = s_pbits;
+    const uint64_t prefix = s_prefix;
+    const int shift = 56 - pbits;
+    for (int u = tid; u < n_units; u += kSelThreads) {
+      const uint64_t k = s_key[u];
+      if (pbits == 0 || (k >> (64 - pbits)) == prefix) {
+        const int dg = (int)((k >> shift) & 255u);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&s_hist[set][w % kHists][dg]),
+                  ((unsigned long long)(uint32_t)s_size[key_unit(k)] << 16) + 1ull);
+      }
+    }
+    __syncthreads();
+    if (w == 0) {
+      // lane l holds digits 255 - 4l .. 252 - 4l, highest first
+      int64_t v[4];
+      int cnt[4];
+      int64_t tot = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        uint64_t h = 0;
+#pragma unroll
+        for (int q2 = 0; q2 < kHists; ++q2) h += s_hist[set][q2][255 - 4 * lane - i];
+        v[i] = (int64_t)(h >> 16);
+        cnt[i] = (int)(h & 0xffffu);
+        tot += v[i];
+      }
+      int64_t incl = tot;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int64_t y = __shfl_up(incl, o, kWave);
+        if (lane >= o) incl += y;
+      }
+      int64_t cum = incl - tot;   // tokens of the digits above this lane's
+      const int64_t rem = s_rem;
+      int hit = -1, hit_cnt = 0;
+      int64_t before = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (hit < 0 && cum + v[i] > rem) {
+          hit = 255 - 4 * lane - i;
+          hit_cnt = cnt[i];
+          before = cum;
+        }
+        cum += v[i];
+      }
+      const uint64_t found = __builtin_amdgcn_ballot_w64(hit >= 0);
+      if (found == 0) {
+        if (lane == 0) s_state = 2;    // the candidates are every unit (first pass) and all fit
+      } else if (lane == (int)__builtin_ctzll(found)) {
+        s_prefix = (prefix << 8) | (uint64_t)hit;
+        s_rem = rem - before;
+        s_pbits = pbits + 8;
+        if (hit_cnt == 1 || pbits + 8 == 64) s_state = 1;
+      }
+    } else {
+      for (int i = tid - 64; i < kHists * 256; i += kSelThreads - 64) (&s_hist[set ^ 1][0][0])[i] = 0;
+    }
+    set ^= 1;
+    __syncthreads();
+  }
+  if (s_state == 1) {
+    // the boundary unit is the one key under the final prefix
+    const int pb = s_pbits;
+    const uint64_t pf = s_prefix;
+    for (int u = tid; u < n_units; u += kSelThreads) {
+      const uint64_t k = s_key[u];
+      if ((pb == 64 ? k : (k >> (64 - pb))) == pf) s_thresh = k;
+    }
+  }
+  __syncthreads();
+  // the taken keys, compacted to the front of s_key and sorted there
+  const bool take_all = s_state == 2;
+  const uint64_t thresh = take_all ? 0 : s_thresh;
+  constexpr int kPerThread = kMaxUnits / kSelThreads;
+  uint64_t mine[kPerThread];
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i) {
+    const int u = tid + i * kSelThreads;
+    mine[i] = u < n_units ? s_key[u] : 0;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i) {
+    const int u = tid + i * kSelThreads;
+    if (u < n_units && (take_all || mine[i] > thresh)) s_key[atomicAdd(&s_nsel_units, 1)] = mine[i];
+  }
+  __syncthreads();
+  const int n_taken = s_nsel_units;
+  n_pad = 64;
+  while (n_pad < n_taken) n_pad <<= 1;
+  for (int i = n_taken + tid; i < n_pad; i += kSelThreads) s_key[i] = 0;   // padding ranks last
+  __syncthreads();
+
+  // bitonic sort, descending keys (n_pad >= 64)
+  // (chunks c and c + kSelWaves of a wave go together; a missing second
+  // chunk is a copy of the first, sorted and dropped)
+  const int n_chunk = n_pad / 64;
+  for (int c = w; c < n_chunk; c += 2 * kSelWaves) {
+    const int c1 = c + kSelWaves < n_chunk ? c + kSelWaves : c;
+    const int i0 = 64 * c + lane, i1 = 64 * c1 + lane;
+    uint64_t v0 = s_key[i0], v1 = s_key[i1];
+#pragma unroll
+    for (int k = 2; k <= 64; k <<= 1) bitonic_in_wave2(v0, v1, i0, i1, k, k >> 1);
+    s_key[i0] = v0;
+    if (c1 != c) s_key[i1] = v1;
+  }
+  __syncthreads();
+  for (int k = 128; k <= n_pad; k <<= 1) {
+    for (int jj = k >> 1; jj >= 64; jj >>= 1) {
+      // pair t: i has a zero at bit jj, its partner p = i + jj
+      for (int t = tid; t < n_pad / 2; t += kSelThreads) {
+        const int i = ((t & ~(jj - 1)) << 1) | (t & (jj - 1));
+        const int p = i | jj;
+        const uint64_t a = s_key[i], b = s_key[p];
+        const bool desc = (i & k) == 0;
+        if (desc ? a < b : a > b) {
+          s_key[i] = b;
+          s_key[p] = a;
+        }
+      }
+      __syncthreads();
+    }
+    for (int c = w; c < n_chunk; c += 2 * kSelWaves) {
+      const int c1 = c + kSelWaves < n_chunk ? c + kSelWaves : c;
+      const int i0 = 64 * c + lane, i1 = 64 * c1 + lane;
+      uint64_t v0 = s_key[i0], v1 = s_key[i1];
+      bitonic_in_wave2(v0, v1, i0, i1, k, 32);
+      s_key[i0] = v0;
+      if (c1 != c) s_key[i1] = v1;
+    }
+    __syncthreads();
+  }
+
+  // inclusive size sums in rank order (all within the budget by construction)
+  if (tid == 0) s_ntake = 0;
+  int carry = 0;
+  for (int base = 0; base < n_taken; base += kSelThreads) {
+    const int p = base + tid;
+    const int v = p < n_taken ? s_size[key_unit(s_key[p])] : 0;
+    int x = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o, kWave);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) s_wsum[w] = x;
+    __syncthreads();
+    int wp = 0;
+    for (int q2 = 0; q2 < w; ++q2) wp += s_wsum[q2];
+    const long long inc = (long long)carry + wp + x;
+    if (p < n_taken) {
+      s_incl[p] = inc > 0x3fffffff ? 0x3fffffff : (int)inc;   // sums past the budget are never read
+      if (inc <= budget) atomicAdd(&s_ntake, 1);
+    }
+    int tot = 0;
+    for (int q2 = 0; q2 < kSelWaves; ++q2) tot += s_wsum[q2];
+    carry = (int)std::min<long long>((long long)carry + tot, 0x3fffffff);
+    __syncthreads();
+  }
+  const int ntake = s_ntake;
+  const int nsel = ntake > 0 ? s_incl[ntake - 1] : 0;
+  const int32_t* ustart = unit_start + (size_t)ps * units_cap;
+  int32_t* rows = row_ws + (size_t)s * budget;
+  // the unit list in rank order; each rank's key slot then holds its unit's
+  // first pool row and size (the starts loaded together, one per thread)
+  for (int p = tid; p < ntake; p += kSelThreads) {
+    const int u = key_unit(s_key[p]);
+    sel_units[(size_t)s * units_cap + p] = u;
+    s_key[p] = ((uint64_t)(uint32_t)ustart[u] << 32) | (uint32_t)s_size[u];
+  }
+  __syncthreads();
+  // one wave per selected unit: its rows in order
+  for (int p = w; p < ntake; p += kSelWaves) {
+    const uint64_t e = s_key[p];
+    const int sz = (int)(uint32_t)e;
+    const int st0 = (int)(uint32_t)(e >> 32);
+    const int ex = s_incl[p] - sz;
+    for (int i = lane; i < sz; i += kWave) rows[ex + i] = st0 + i;
+  }
+  if (tid == 0) {
+    n_sel_units[s] = ntake;
+    n_sel[s] = nsel;
+  }
+}
+
 // One block per fired slice: the float64 group-consistent scores (Appendix B),
 // a descending bitonic sort of the unit keys, prefix-stop under the budget,
 // the selected unit list and the pool-row list that the gather kernel copies.
@@ -487,10 +859,8 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
   uint64_t* s_key = reinterpret_cast<uint64_t*>(smem);            // [n_pad_arg]
   int* s_size = reinterpret_cast<int*>(s_key + n_pad_arg);        // [n_pad_arg] unit sizes by unit id
   int* s_incl = s_size + n_pad_arg;                                // [n_pad_arg] inclusive size sums by rank
-  __shared__ double s_rm[G][kSelWaves], s_rz[G][kSelWaves];
-  __shared__ double s_m[G], s_z[G];
-  __shared__ int s_ntake;
-  __shared__ int s_wsum[kSelWaves];
+  __shared__ double s_rm[G][kSelWaves];
+  __shared__ double s_m[G];
 
   const int64_t s = blockIdx.x;
   const int64_t grp = s / n_kv_heads;
@@ -575,129 +945,147 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
   }
   __syncthreads();
 
-  // pass 2: exponentials (kept in the logit workspace) and their sums per head
-  double zs[G];
+  select_after_max<G, false>(lg, s_m, n_units, n_pad, s, ps, units_cap, budget, unit_start, sel_units, n_sel_units,
+                             n_sel, row_ws, scores_out, s_key, s_size, s_incl);
+}
+
+// The first launch of a fused decode step (fixed segments, device pool), one
+// block of kSelThreads per (slice, part of its units):
+//  - every block computes its group's r and decision (boundary_r: the same
+//    value in every block); one block per group writes them;
+//  - block 0 of each slice runs the fixed-segment store (window append and
+//    oldest-segment eviction, store_slice on its first wave): it writes only
+//    the unit it creates and rows past every existing unit, which the
+//    retrieval below does not read;
+//  - blocks of a group that did not fire stop there; the others compute the
+//    float64 logits of their part of the units (the arithmetic of
+//    unit_logits_kernel) and their per-head maxima, write them with
+//    device-scope stores and count themselves in; the last block of the
+//    slice to arrive resets the counter and makes the selection from all the
+//    parts (select_after_max), as score_select_kernel does.
+// The reference query is left for the attention launch to update.
+template <class T, int G>
+__global__ __launch_bounds__(kSelThreads)
+void step_select_kernel(const T* __restrict__ q, const T* __restrict__ q_ref, int n_kv_heads, double tau, int first,
+                        double* __restrict__ r_out, uint8_t* __restrict__ fire_out, const T* __restrict__ k_new,
+                        const T* __restrict__ v_new, T* __restrict__ k_local, T* __restrict__ v_local, int window,
+                        int step, int seg_len, int evict_seg, float* __restrict__ reps,
+                        int32_t* __restrict__ unit_start, int32_t* __restrict__ unit_size, int units_cap,
+                        int n_clusters, T* __restrict__ k_pool, T* __restrict__ v_pool, int64_t pool_rows,
+                        int prompt_len, double scale, int n_units, int budget, int32_t* __restrict__ sel_units,
+                        int32_t* __restrict__ n_sel_units, int32_t* __restrict__ n_sel,
+                        int32_t* __restrict__ sel_rows, double* __restrict__ scores_out,
+                        double* __restrict__ logit_ws, double* __restrict__ part_max, int32_t* __restrict__ counter,
+                        int n_parts, int n_pad) {
+  extern __shared__ __align__(16) char smem[];
+  uint64_t* s_key = reinterpret_cast<uint64_t*>(smem);            // [n_pad]
+  int* s_size = reinterpret_cast<int*>(s_key + n_pad);            // [n_pad] unit sizes by unit id
+  int* s_incl = s_size + n_pad;                                    // [n_pad] inclusive size sums by rank
+  __shared__ double s_bpart[16];
+  __shared__ double s_rm[G][kSelWaves];
+  __shared__ double s_m[G];
+  __shared__ int s_last;
+  const int64_t s = blockIdx.x / n_parts;
+  const int part = (int)(blockIdx.x - s * n_parts);
+  const int64_t grp = s / n_kv_heads;
+  const int kvh = (int)(s - grp * n_kv_heads);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n_q_heads = n_kv_heads * G;
+
+  const double r = boundary_r(q, q_ref, n_q_heads, first, grp, s_bpart);
+  const bool fire = first || r < tau;
+  if (part == 0 && kvh == 0 && tid == 0) {
+    if (r_out) r_out[grp] = r;
+    fire_out[grp] = (uint8_t)(fire ? 1 : 0);
+  }
+  if (part == 0 && w == 0)
+    store_slice(k_new, v_new, k_local, v_local, window, step, seg_len, evict_seg, reps, unit_start, unit_size,
+                units_cap, n_clusters, k_pool, v_pool, pool_rows, prompt_len, s, lane);
+  if (!fire) return;
+
+  // logits of this part's units and their maxima
+  const int per = (n_units + n_parts - 1) / n_parts;
+  const int u_begin = part * per, u_end = min(n_units, u_begin + per);
+  const int sub = lane & 15, quad = lane >> 4;
+  double mx[G];
 #pragma unroll
-  for (int j = 0; j < G; ++j) zs[j] = 0.0;
-  for (int u = tid; u < n_units; u += kSelThreads) {
+  for (int j = 0; j < G; ++j) mx[j] = -__builtin_inf();
+  double* lg = logit_ws + (size_t)s * units_cap * G;
+  if (u_begin < u_end) {
+    double qd[G][8];
 #pragma unroll
-    for (int j = 0; j < G; ++j) {
-      const double e = exp(lg[(size_t)u * G + j] - s_m[j]);
-      lg[(size_t)u * G + j] = e;
-      zs[j] += e;
+    for (int j = 0; j < G; ++j)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        qd[j][e] = (double)load_as_f32(q, ((size_t)grp * n_q_heads + (size_t)kvh * G + j) * kHeadDim + 8 * sub + e);
+    const float* rs = reps + (size_t)s * units_cap * kHeadDim;
+    for (int u0 = u_begin + w * 4 * kSelBatch; u0 < u_end; u0 += kSelWaves * 4 * kSelBatch) {
+      float4 x[kSelBatch][2];
+#pragma unroll
+      for (int i = 0; i < kSelBatch; ++i) {
+        const int u = min(u0 + 4 * i + quad, u_end - 1);   // past the end: re-read the last unit, unused
+        const float4* r4 = reinterpret_cast<const float4*>(rs + (size_t)u * kHeadDim + 8 * sub);
+        x[i][0] = r4[0];
+        x[i][1] = r4[1];
+      }
+#pragma unroll
+      for (int i = 0; i < kSelBatch; ++i) {
+        const int u = u0 + 4 * i + quad;
+        const double xd[8] = {x[i][0].x, x[i][0].y, x[i][0].z, x[i][0].w,
+                              x[i][1].x, x[i][1].y, x[i][1].z, x[i][1].w};
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+          double a = 0.0;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) a = fma(qd[j][e], xd[e], a);
+          a = row16_sum_f64(a) * scale;
+          if (u < u_end) {
+            mx[j] = fmax(mx[j], a);
+            if (sub == j) __hip_atomic_store(lg + (size_t)u * G + j, a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          }
+        }
+      }
     }
   }
 #pragma unroll
   for (int j = 0; j < G; ++j) {
-    const double z = wave_sum(zs[j]);
-    if (lane == 0) s_rz[j][w] = z;
+    const double m = wave_max(mx[j]);
+    if (lane == 0) s_rm[j][w] = m;
   }
   __syncthreads();
   if (tid < G) {
-    double z = 0.0;
-    for (int q2 = 0; q2 < kSelWaves; ++q2) z += s_rz[tid][q2];
-    s_z[tid] = z;
+    double m = s_rm[tid][0];
+    for (int q2 = 1; q2 < kSelWaves; ++q2) m = fmax(m, s_rm[tid][q2]);
+    __hip_atomic_store(part_max + ((size_t)s * n_parts + part) * G + tid, m, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
   }
+  // count this part in once its stores are done; the last one selects
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-
-  // pass 3: averaged probabilities and sort keys (padding keys 0 rank last)
-  for (int u = tid; u < n_pad; u += kSelThreads) {
-    uint64_t key = 0;
-    if (u < n_units) {
-      double a = 0.0;
-#pragma unroll
-      for (int j = 0; j < G; ++j) a += lg[(size_t)u * G + j] / s_z[j];
-      a /= (double)G;
-      key = unit_key(a, u);
-      if (scores_out) scores_out[(size_t)s * units_cap + u] = a;
-    }
-    s_key[u] = key;
-  }
-  __syncthreads();
-
-  // bitonic sort, descending keys (n_pad >= 64)
-  // (chunks c and c + kSelWaves of a wave go together; a missing second
-  // chunk is a copy of the first, sorted and dropped)
-  const int n_chunk = n_pad / 64;
-  for (int c = w; c < n_chunk; c += 2 * kSelWaves) {
-    const int c1 = c + kSelWaves < n_chunk ? c + kSelWaves : c;
-    const int i0 = 64 * c + lane, i1 = 64 * c1 + lane;
-    uint64_t v0 = s_key[i0], v1 = s_key[i1];
-#pragma unroll
-    for (int k = 2; k <= 64; k <<= 1) bitonic_in_wave2(v0, v1, i0, i1, k, k >> 1);
-    s_key[i0] = v0;
-    if (c1 != c) s_key[i1] = v1;
-  }
-  __syncthreads();
-  for (int k = 128; k <= n_pad; k <<= 1) {
-    for (int jj = k >> 1; jj >= 64; jj >>= 1) {
-      // pair t: i has a zero at bit jj, its partner p = i + jj
-      for (int t = tid; t < n_pad / 2; t += kSelThreads) {
-        const int i = ((t & ~(jj - 1)) << 1) | (t & (jj - 1));
-        const int p = i | jj;
-        const uint64_t a = s_key[i], b = s_key[p];
-        const bool desc = (i & k) == 0;
-        if (desc ? a < b : a > b) {
-          s_key[i] = b;
-          s_key[p] = a;
-        }
-      }
-      __syncthreads();
-    }
-    for (int c = w; c < n_chunk; c += 2 * kSelWaves) {
-      const int c1 = c + kSelWaves < n_chunk ? c + kSelWaves : c;
-      const int i0 = 64 * c + lane, i1 = 64 * c1 + lane;
-      uint64_t v0 = s_key[i0], v1 = s_key[i1];
-      bitonic_in_wave2(v0, v1, i0, i1, k, 32);
-      s_key[i0] = v0;
-      if (c1 != c) s_key[i1] = v1;
-    }
-    __syncthreads();
-  }
-
-  // prefix stop: count ranks whose inclusive size sum stays within the budget
-  if (tid == 0) s_ntake = 0;
-  int carry = 0;
-  for (int base = 0; base < n_units; base += kSelThreads) {
-    const int p = base + tid;
-    const int v = p < n_units ? s_size[key_unit(s_key[p])] : 0;
-    int x = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(x, o, kWave);
-      if (lane >= o) x += y;
-    }
-    if (lane == 63) s_wsum[w] = x;
-    __syncthreads();
-    int wp = 0;
-    for (int q2 = 0; q2 < w; ++q2) wp += s_wsum[q2];
-    const long long inc = (long long)carry + wp + x;
-    if (p < n_units) {
-      s_incl[p] = inc > 0x3fffffff ? 0x3fffffff : (int)inc;   // sums past the budget are never read
-      if (inc <= budget) atomicAdd(&s_ntake, 1);
-    }
-    int tot = 0;
-    for (int q2 = 0; q2 < kSelWaves; ++q2) tot += s_wsum[q2];
-    carry = (int)std::min<long long>((long long)carry + tot, 0x3fffffff);
-    __syncthreads();
-  }
-  const int ntake = s_ntake;
-  const int nsel = ntake > 0 ? s_incl[ntake - 1] : 0;
-  const int32_t* ustart = unit_start + (size_t)ps * units_cap;
-  int32_t* rows = row_ws + (size_t)s * budget;
-  // one wave per selected unit: its rank in the list, then its rows in order
-  for (int p = w; p < ntake; p += kSelWaves) {
-    const int u = key_unit(s_key[p]);
-    const int sz = s_size[u];
-    const int ex = s_incl[p] - sz;
-    const int st0 = ustart[u];
-    if (lane == 0) sel_units[(size_t)s * units_cap + p] = u;
-    for (int i = lane; i < sz; i += kWave) rows[ex + i] = st0 + i;
-  }
   if (tid == 0) {
-    n_sel_units[s] = ntake;
-    n_sel[s] = nsel;
+    const int old = __hip_atomic_fetch_add(counter + s, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = old == n_parts - 1;
+    if (s_last) __hip_atomic_store(counter + s, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
+  __syncthreads();
+  if (!s_last) return;
+  // the parts' maxima (one coherent load per thread, all in flight) and the unit sizes
+  __shared__ double s_pmax[kMaxLogitParts * kMaxGroupSize];
+  if (tid < n_parts * G)
+    s_pmax[tid] = __hip_atomic_load(part_max + (size_t)s * n_parts * G + tid, __ATOMIC_RELAXED,
+                                    __HIP_MEMORY_SCOPE_AGENT);
+  const int32_t* us = unit_size + (size_t)s * units_cap;
+  for (int u = tid; u < n_units; u += kSelThreads) s_size[u] = max(us[u], 0);
+  __syncthreads();
+  if (tid < G) {
+    double m = -__builtin_inf();
+    for (int p2 = 0; p2 < n_parts; ++p2) m = fmax(m, s_pmax[p2 * G + tid]);
+    s_m[tid] = m;
+  }
+  __syncthreads();
+  select_after_max<G, true>(lg, s_m, n_units, n_pad, s, s, units_cap, budget, unit_start, sel_units, n_sel_units,
+                            n_sel, sel_rows, scores_out, s_key, s_size, s_incl);
 }
 
 // Copy selected pool rows into KV_critical: 16 lanes per row, 16 rows per pass.
@@ -912,6 +1300,13 @@ __device__ __forceinline__ void stage_row_list(const int32_t* __restrict__ list,
 // merges the chunk partials.
 constexpr int kAttnTargetBlocks = 256;
 constexpr int kAttnMinRows = 256;
+// A fused decode step over few slices spreads each slice's rows over many
+// small blocks: kStepAttnRows rows per block of kStepAttnWaves waves.
+#ifndef LKV_STEP_ATTN_ROWS
+#define LKV_STEP_ATTN_ROWS 128
+#endif
+constexpr int kStepAttnWaves = 4;
+constexpr int kStepAttnRows = LKV_STEP_ATTN_ROWS;
 
 // Sum over the 16 lanes of a DPP row, result in every lane of the row:
 // butterflies over lane^1, lane^2 (quad permutes), then the mirrored halves
@@ -973,6 +1368,103 @@ constexpr int attn_waves() {
   return sizeof(T) == 2 && G <= 4 ? 16 : 8;
 }
 
+// What the attention blocks of a fused decode step do beyond the attention:
+// with `counter` (per-slice arrival counters, zero between calls) a slice's
+// chunk partials are merged by its last block to finish instead of by
+// attn_combine_kernel, and with `q_ref` one block per group stores the
+// step's query as the new reference (every step in PREV mode, at a fire in
+// ANCHOR mode) once the boundary test has read the old one.
+struct StepSync {
+  int32_t* counter;
+  void* q_ref;
+  const uint8_t* fire;
+  int mode;
+};
+
+template <class T>
+__device__ __forceinline__ void update_q_ref(const StepSync& sync, const T* __restrict__ q, int64_t grp, int n_elems,
+                                             int tid, int n_threads) {
+  if (!(sync.mode == LOUISKV_REF_PREV || sync.fire[grp])) return;
+  T* dst = static_cast<T*>(sync.q_ref) + (size_t)grp * n_elems;
+  const T* src = q + (size_t)grp * n_elems;
+  for (int i = tid; i < n_elems; i += n_threads) dst[i] = src[i];
+}
+
+// The last of a slice's n_chunks blocks to arrive merges their partials,
+// (m, l, acc[128]) per head in base 2, in chunk order with the arithmetic of
+// attn_combine_kernel, so the outputs equal the two-kernel path's bit for bit.
+// Partials are written and read with device-scope atomic stores and loads
+// (coherent across the per-XCD L2 caches); a block waits for its stores
+// before it counts itself in, and the last one resets the counter.  The
+// merging block first stages every chunk's (m, l) in LDS (s_ml, n_chunks * G
+// pairs), then each thread takes one head and two dims and reads their
+// accumulators kMergeBatch chunks at a time, all loads of a batch in flight.
+constexpr int kMergeBatch = 16;
+
+template <int G>
+__device__ __forceinline__ void attn_last_block_merge(const float* __restrict__ part, int32_t* __restrict__ counter,
+                                                      int64_t s, int n_chunks, void* __restrict__ out, int out_bf16,
+                                                      float* __restrict__ lse_out, int tid, int n_threads,
+                                                      float2* s_ml) {
+  __shared__ int s_last;
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (tid == 0) {
+    const int old = __hip_atomic_fetch_add(counter + s, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = old == n_chunks - 1;
+    if (s_last) __hip_atomic_store(counter + s, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  if (!s_last) return;
+  constexpr size_t pstride = 2 + kHeadDim;
+  const float* ps = part + (size_t)s * n_chunks * G * pstride;
+  for (int i = tid; i < n_chunks * G; i += n_threads) {
+    const uint64_t v = __hip_atomic_load(reinterpret_cast<const uint64_t*>(ps + (size_t)i * pstride),
+                                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_ml[i] = make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
+  }
+  __syncthreads();
+  for (int i = tid; i < G * (kHeadDim / 2); i += n_threads) {
+    const int j = i / (kHeadDim / 2), lane = i % (kHeadDim / 2);
+    float mm = -__builtin_inff();
+    for (int c = 0; c < n_chunks; ++c) mm = fmaxf(mm, s_ml[c * G + j].x);
+    float ll = 0.f, a0 = 0.f, a1 = 0.f;
+    if (mm != -__builtin_inff()) {
+      const uint64_t* pa = reinterpret_cast<const uint64_t*>(ps + (size_t)j * pstride + 2) + lane;
+      for (int c0 = 0; c0 < n_chunks; c0 += kMergeBatch) {
+        uint64_t v[kMergeBatch];
+#pragma unroll
+        for (int b = 0; b < kMergeBatch; ++b)
+          v[b] = c0 + b < n_chunks ? __hip_atomic_load(pa + (size_t)(c0 + b) * G * (pstride / 2), __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT)
+                                   : 0;
+#pragma unroll
+        for (int b = 0; b < kMergeBatch; ++b) {
+          if (c0 + b < n_chunks) {
+            const float2 ml = s_ml[(c0 + b) * G + j];
+            const float w = __builtin_amdgcn_exp2f(ml.x - mm);
+            ll += ml.y * w;
+            a0 += __uint_as_float((uint32_t)v[b]) * w;
+            a1 += __uint_as_float((uint32_t)(v[b] >> 32)) * w;
+          }
+        }
+      }
+    }
+    const float inv = ll > 0.f ? 1.f / ll : 0.f;
+    const size_t row = (size_t)s * G + j;
+    if (out_bf16) {
+      uint16_t* o = static_cast<uint16_t*>(out) + row * kHeadDim;
+      store_from_f32(o, 2 * lane, a0 * inv);
+      store_from_f32(o, 2 * lane + 1, a1 * inv);
+    } else {
+      float* o = static_cast<float*>(out) + row * kHeadDim;
+      store_from_f32(o, 2 * lane, a0 * inv);
+      store_from_f32(o, 2 * lane + 1, a1 * inv);
+    }
+    if (lse_out && lane == 0) lse_out[row] = ll > 0.f ? 0.6931471805599453f * (mm + log2f(ll)) : -__builtin_inff();
+  }
+}
+
 // Merge NW wave states (base-2 maximum m and sum l per head, acc per head and
 // dim, all in LDS) into the block's result: the normalised output and lse when
 // the block covers the whole slice (n_chunks == 1), else the chunk partial
@@ -981,7 +1473,8 @@ template <int G, int NW>
 __device__ __forceinline__ void attn_block_merge(const float (*s_m)[G], const float (*s_l)[G],
                                                  const float (*s_acc)[G][kHeadDim], int tid, int64_t s, int chunk,
                                                  int n_chunks, float* __restrict__ part, void* __restrict__ out,
-                                                 int out_bf16, float* __restrict__ lse_out) {
+                                                 int out_bf16, float* __restrict__ lse_out,
+                                                 int32_t* __restrict__ counter, float2* s_ml) {
   for (int i = tid; i < G * kHeadDim; i += NW * 64) {
     const int j = i / kHeadDim, k = i % kHeadDim;
     float mm = -__builtin_inff();
@@ -1006,13 +1499,23 @@ __device__ __forceinline__ void attn_block_merge(const float (*s_m)[G], const fl
     } else {
       const size_t pstride = 2 + kHeadDim;
       float* pout = part + ((size_t)s * n_chunks + chunk) * G * pstride;
-      pout[j * pstride + 2 + k] = aa;
-      if (k == 0) {
-        pout[j * pstride + 0] = mm;
-        pout[j * pstride + 1] = ll;
+      if (counter) {   // read back by another block of this launch
+        __hip_atomic_store(pout + j * pstride + 2 + k, aa, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (k == 0) {
+          __hip_atomic_store(pout + j * pstride + 0, mm, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(pout + j * pstride + 1, ll, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      } else {
+        pout[j * pstride + 2 + k] = aa;
+        if (k == 0) {
+          pout[j * pstride + 0] = mm;
+          pout[j * pstride + 1] = ll;
+        }
       }
     }
   }
+  if (counter && n_chunks > 1)
+    attn_last_block_merge<G>(part, counter, s, n_chunks, out, out_bf16, lse_out, tid, NW * 64, s_ml);
 }
 
 // With boundary-delimited segments the window of slice s holds the tokens
@@ -1041,8 +1544,8 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
                          const T* __restrict__ k_local, const T* __restrict__ v_local, int window, int local_start_arg,
                          int n_local_arg, int n_chunks, float* __restrict__ part, void* __restrict__ out, int out_bf16,
                          float* __restrict__ lse_out, const int32_t* __restrict__ seg_state, int seg_stride,
-                         int n_tokens, int slice_div) {
-  extern __shared__ int s_rows[];     // kIdx: the chunk's entries of the row list
+                         int n_tokens, int slice_div, StepSync sync) {
+  extern __shared__ __align__(16) int s_rows[];   // kIdx: the chunk's entries of the row list
   constexpr int R = attn_rows_in_flight<T, G>();
   constexpr int kAttnWaves = attn_waves<T, G>();
   constexpr int kAttnThreads = kAttnWaves * 64;
@@ -1054,6 +1557,7 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
   const int64_t grp = s / n_kv_heads;
   const int kvh = (int)(s - grp * n_kv_heads);
   const int tid = threadIdx.x, sub = tid & 15, rg = tid >> 4;   // 64 row groups of 16 lanes
+  if (sync.q_ref && chunk == 0 && kvh == 0) update_q_ref(sync, q, grp, n_kv_heads * G * kHeadDim, tid, kAttnThreads);
   int local_start = local_start_arg, n_local = n_local_arg;
   // slice_div > 1: per-head lists, s is a query head and ps its KV head's slice
   const int64_t ps = s / slice_div;
@@ -1182,7 +1686,8 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
     }
   }
   __syncthreads();
-  attn_block_merge<G, kAttnWaves>(s_m, s_l, s_acc, tid, s, chunk, n_chunks, part, out, out_bf16, lse_out);
+  attn_block_merge<G, kAttnWaves>(s_m, s_l, s_acc, tid, s, chunk, n_chunks, part, out, out_bf16, lse_out,
+                                  sync.counter, reinterpret_cast<float2*>(s_rows));
 }
 
 // ---- bf16: scores on the matrix cores
@@ -1213,17 +1718,17 @@ constexpr int attn_mfma_waves() {
 // row (lane owns dims 8(l%16)..+7, rows 4k + l/16 of the tile for k = 0..3),
 // where P V accumulates in float32 on the vector ALUs.  Output and partials as
 // attn_partial_kernel.
-template <int G, bool kIdx>
-__global__ __launch_bounds__((attn_mfma_waves<G>() * 64))
+template <int G, bool kIdx, int NW = attn_mfma_waves<G>()>
+__global__ __launch_bounds__((NW * 64))
 void attn_mfma_kernel(const uint16_t* __restrict__ q, int n_kv_heads, float scale, const uint16_t* __restrict__ k_buf,
                       const uint16_t* __restrict__ v_buf, const int32_t* __restrict__ n_sel, int buf_rows,
                       const int32_t* __restrict__ rows, int64_t src_rows,
                       const uint16_t* __restrict__ k_local, const uint16_t* __restrict__ v_local, int window,
                       int local_start_arg, int n_local_arg, int n_chunks, float* __restrict__ part,
                       void* __restrict__ out, int out_bf16, float* __restrict__ lse_out,
-                      const int32_t* __restrict__ seg_state, int seg_stride, int n_tokens, int slice_div) {
-  extern __shared__ int s_rows[];     // kIdx: the chunk's entries of the row list
-  constexpr int NW = attn_mfma_waves<G>();
+                      const int32_t* __restrict__ seg_state, int seg_stride, int n_tokens, int slice_div,
+                      StepSync sync) {
+  extern __shared__ __align__(16) int s_rows[];   // kIdx: the chunk's entries of the row list
   constexpr int NM = G == 8 ? 2 : 1;        // matrix ops per k-chunk, 4 heads each
   constexpr int GA = G < 4 ? G : 4;         // distinct heads in one op's output
   __shared__ float4 s_p[NW][NM][64];
@@ -1235,6 +1740,7 @@ void attn_mfma_kernel(const uint16_t* __restrict__ q, int n_kv_heads, float scal
   const int kvh = (int)(s - grp * n_kv_heads);
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, p16 = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);    // wave-uniform, kept in a scalar register
+  if (sync.q_ref && chunk == 0 && kvh == 0) update_q_ref(sync, q, grp, n_kv_heads * G * kHeadDim, tid, NW * 64);
   int local_start = local_start_arg, n_local = n_local_arg;
   // slice_div > 1: per-head lists, s is a query head and ps its KV head's slice
   const int64_t ps = s / slice_div;
@@ -1381,7 +1887,8 @@ void attn_mfma_kernel(const uint16_t* __restrict__ q, int n_kv_heads, float scal
     }
   }
   __syncthreads();
-  attn_block_merge<G, NW>(s_m, s_l, s_acc, tid, s, chunk, n_chunks, part, out, out_bf16, lse_out);
+  attn_block_merge<G, NW>(s_m, s_l, s_acc, tid, s, chunk, n_chunks, part, out, out_bf16, lse_out, sync.counter,
+                          reinterpret_cast<float2*>(s_rows));
 }
 
 // One wave per (slice, head): merge the chunk partials.
@@ -1441,6 +1948,18 @@ int attn_chunks(int64_t S, int buf_rows, int window, bool indexed) {
 
 size_t attn_ws_bytes(int64_t S, int G, int buf_rows, int window, bool indexed) {
   const int nc = attn_chunks(S, buf_rows, window, indexed);
+  return nc == 1 ? 0 : align_up((size_t)S * nc * G * (2 + kHeadDim) * sizeof(float), 256);
+}
+
+// Chunks per slice of the fused decode step's bf16 attention: kStepAttnRows
+// rows each, whatever the slice count (the step serves few slices at a time).
+int step_attn_chunks(int buf_rows, int window) {
+  return std::max(1, (int)(((int64_t)buf_rows + window + kStepAttnRows - 1) / kStepAttnRows));
+}
+
+// Partials of the fused step's attention (merged in-kernel), by dtype.
+size_t step_attn_part_bytes(int64_t S, int G, int buf_rows, int window, int dtype) {
+  const int nc = dtype == LOUISKV_BF16 ? step_attn_chunks(buf_rows, window) : attn_chunks(S, buf_rows, window, true);
   return nc == 1 ? 0 : align_up((size_t)S * nc * G * (2 + kHeadDim) * sizeof(float), 256);
 }
 
@@ -1661,7 +2180,9 @@ int score_and_select(const void* q, int32_t dtype, int64_t n_slices, int32_t n_k
   (void)d;
   const int parts = logit_parts(n_slices, n_units);
   if ((int64_t)n_slices * parts > INT32_MAX) return fail(LOUISKV_ERR_SHAPE, "problem too large for one launch");
+  int st = LOUISKV_OK;
 #define LKV_SEL(T, G)                                                                                                  \
+  if ((st = check_lds(reinterpret_cast<const void*>(&score_select_kernel<T, G>), lds))) return st;                     \
   if (parts > 1)                                                                                                       \
     unit_logits_kernel<T, G><<<(unsigned)(n_slices * parts), kLogitThreads, 0, s>>>(                                   \
         static_cast<const T*>(q), n_kv_heads, scale, reps, units_cap, n_units, fire, logit_ws, seg_state,            \
@@ -1883,6 +2404,8 @@ struct AttnArgs {
   unsigned grid;
   size_t lds;              // dynamic LDS for the staged row list
   int slice_div = 1;       // lists per KV-head slice (per-head selection: the group size)
+  StepSync sync = {nullptr, nullptr, nullptr, 0};   // fused decode step: in-kernel merge, q_ref update
+  int step_waves = 0;      // fused decode step, bf16: waves per block (0: the default block)
 };
 
 template <class T, int G, bool kIdx>
@@ -1891,17 +2414,25 @@ void launch_attn_partial(const AttnArgs& a, hipStream_t s) {
       static_cast<const T*>(a.q), a.n_kv_heads, a.scale, static_cast<const T*>(a.k_src), static_cast<const T*>(a.v_src),
       a.n_sel, a.buf_rows, a.rows, a.src_rows, static_cast<const T*>(a.k_local), static_cast<const T*>(a.v_local),
       a.window, a.local_start, a.n_local, a.n_chunks, a.part, a.out, a.out_bf16, a.lse_out, a.seg_state,
-      a.seg_stride, a.n_tokens, a.slice_div);
+      a.seg_stride, a.n_tokens, a.slice_div, a.sync);
 }
 
-template <int G, bool kIdx>
-void launch_attn_mfma(const AttnArgs& a, hipStream_t s) {
-  attn_mfma_kernel<G, kIdx><<<a.grid, attn_mfma_waves<G>() * 64, a.lds, s>>>(
+template <int G, bool kIdx, int NW>
+void launch_attn_mfma_nw(const AttnArgs& a, hipStream_t s) {
+  attn_mfma_kernel<G, kIdx, NW><<<a.grid, NW * 64, a.lds, s>>>(
       static_cast<const uint16_t*>(a.q), a.n_kv_heads, a.scale, static_cast<const uint16_t*>(a.k_src),
       static_cast<const uint16_t*>(a.v_src), a.n_sel, a.buf_rows, a.rows, a.src_rows,
       static_cast<const uint16_t*>(a.k_local), static_cast<const uint16_t*>(a.v_local), a.window, a.local_start,
       a.n_local, a.n_chunks, a.part, a.out, a.out_bf16, a.lse_out, a.seg_state, a.seg_stride, a.n_tokens,
-      a.slice_div);
+      a.slice_div, a.sync);
+}
+
+template <int G, bool kIdx>
+void launch_attn_mfma(const AttnArgs& a, hipStream_t s) {
+  if (kIdx && a.step_waves == kStepAttnWaves)
+    launch_attn_mfma_nw<G, kIdx, kStepAttnWaves>(a, s);
+  else
+    launch_attn_mfma_nw<G, kIdx, attn_mfma_waves<G>()>(a, s);
 }
 
 template <bool kIdx>
@@ -1930,7 +2461,8 @@ int sparse_decode_attn(const void* q, int32_t dtype, int64_t n_slices, int32_t n
                        int32_t buf_rows, const int32_t* rows, int64_t src_rows, const void* k_local,
                        const void* v_local, int32_t window, int32_t local_start, int32_t n_local, void* out,
                        int32_t out_dtype, float* lse_out, void* workspace, size_t workspace_bytes, void* stream,
-                       const int32_t* seg_state = nullptr, int32_t n_tokens = 0, int32_t slice_div = 1) {
+                       const int32_t* seg_state = nullptr, int32_t n_tokens = 0, int32_t slice_div = 1,
+                       const StepSync* step_sync = nullptr) {
   const bool indexed = rows != nullptr;
   if (!q || !out || !n_sel) return fail(LOUISKV_ERR_NULL, "q, out and n_sel are required");
   if (buf_rows > 0 && (!k_src || !v_src))
@@ -1950,9 +2482,11 @@ int sparse_decode_attn(const void* q, int32_t dtype, int64_t n_slices, int32_t n
     return fail(LOUISKV_ERR_SHAPE, "buf_rows=%d window=%d local_start=%d n_local=%d", buf_rows, window, local_start,
                 n_local);
   if (indexed && buf_rows > 0 && src_rows < 1) return fail(LOUISKV_ERR_SHAPE, "pool_rows=%lld", (long long)src_rows);
-  const int n_chunks = attn_chunks(n_slices, buf_rows, window, indexed);
+  const bool step_bf16 = step_sync && indexed && dtype == LOUISKV_BF16;
+  const int n_chunks = step_bf16 ? step_attn_chunks(buf_rows, window) : attn_chunks(n_slices, buf_rows, window, indexed);
   if ((int64_t)n_slices * n_chunks > INT32_MAX) return fail(LOUISKV_ERR_SHAPE, "problem too large for one launch");
-  const size_t need = attn_ws_bytes(n_slices, group_size, buf_rows, window, indexed);
+  const size_t need = step_sync ? step_attn_part_bytes(n_slices, group_size, buf_rows, window, dtype)
+                                : attn_ws_bytes(n_slices, group_size, buf_rows, window, indexed);
   if (need > 0 && (!workspace || workspace_bytes < need))
     return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
   AttnArgs a;
@@ -1966,16 +2500,22 @@ int sparse_decode_attn(const void* q, int32_t dtype, int64_t n_slices, int32_t n
   a.out = out; a.out_bf16 = out_dtype == LOUISKV_BF16; a.lse_out = lse_out;
   a.seg_state = seg_state; a.seg_stride = kSegRing + window; a.n_tokens = n_tokens;
   a.slice_div = slice_div;
+  if (step_sync) {
+    a.sync = *step_sync;
+    a.step_waves = step_bf16 ? kStepAttnWaves : 0;
+  }
   a.grid = (unsigned)(n_slices * n_chunks);
   // a chunk spans at most ceil(total / n_chunks) <= ceil((buf_rows + window) / n_chunks) rows
   a.lds = indexed ? (size_t)(((int64_t)buf_rows + window + n_chunks - 1) / n_chunks + 1) * sizeof(int) : 0;
+  if (step_sync && n_chunks > 1)   // the merging block stages every chunk's (m, l) per head there
+    a.lds = std::max(a.lds, (size_t)n_chunks * group_size * sizeof(float2));
   hipStream_t s = as_stream(stream);
   if (indexed)
     launch_attn<true>(dtype, group_size, a, s);
   else
     launch_attn<false>(dtype, group_size, a, s);
   LKV_CHECK_LAUNCH();
-  if (n_chunks == 1) return LOUISKV_OK;     // the blocks wrote the output themselves
+  if (n_chunks == 1 || step_sync) return LOUISKV_OK;     // the blocks wrote the output themselves
   const int64_t n_rows = n_slices * group_size;
   const int cgrid = (int)((n_rows + 3) / 4);
   if (out_dtype == LOUISKV_BF16)
@@ -2013,6 +2553,130 @@ extern "C" int louiskv_sparse_decode_attn_rows(const void* q, int32_t dtype, int
   return sparse_decode_attn(q, dtype, n_slices, n_kv_heads, group_size, d, scale, k_pool, v_pool, n_sel, budget,
                             sel_rows, pool_rows, k_local, v_local, window, local_start, n_local, out, out_dtype,
                             lse_out, workspace, workspace_bytes, stream);
+}
+
+// ---------------------------------------------------------------------------
+// One decode step of Algorithm 1 in two launches (fixed segments, pool in
+// device memory, KV_critical as a row list).
+
+namespace louiskv {
+namespace {
+
+// Workspace of louiskv_decode_step: two arrival counters per slice (which
+// must be zero before the first call and are zero after every call), the
+// logits and per-part maxima of the selection, the attention partials.
+struct StepLayout {
+  size_t counters, logits, pmax, part, total;
+};
+
+StepLayout step_layout(int64_t S, int dtype, int G, int units_cap, int budget, int window) {
+  StepLayout L{};
+  Carver cv(nullptr);
+  cv.take<int32_t>((size_t)2 * S);
+  L.logits = align_up(cv.used, 256);
+  cv.take<double>((size_t)S * units_cap * G);
+  L.pmax = align_up(cv.used, 256);
+  cv.take<double>((size_t)S * kMaxLogitParts * G);
+  L.part = align_up(cv.used, 256);
+  cv.take<char>(step_attn_part_bytes(S, G, budget, window, dtype));
+  L.counters = 0;
+  L.total = align_up(cv.used, 256);
+  return L;
+}
+
+}  // namespace
+}  // namespace louiskv
+
+extern "C" size_t louiskv_decode_step_workspace_size(int64_t n_slices, int32_t dtype, int32_t group_size,
+                                                     int32_t units_cap, int32_t budget, int32_t window) {
+  if (n_slices < 1 || group_size < 1 || group_size > kMaxGroupSize || units_cap < 1 || budget < 0 || window < 0 ||
+      (dtype != LOUISKV_F32 && dtype != LOUISKV_BF16))
+    return 0;
+  return step_layout(n_slices, dtype, group_size, units_cap, budget, window).total;
+}
+
+extern "C" int louiskv_decode_step(const void* q, void* q_ref, int32_t dtype, int64_t n_groups, int32_t n_q_heads,
+                                   int32_t n_kv_heads, int32_t d, double tau, int32_t mode, int32_t step,
+                                   double* r_out, uint8_t* fire_out, const void* k_new, const void* v_new,
+                                   void* k_local, void* v_local, int32_t window, int32_t seg_len, float* reps,
+                                   int32_t* unit_start, int32_t* unit_size, int32_t units_cap, int32_t n_clusters,
+                                   void* k_pool, void* v_pool, int64_t pool_rows, int32_t prompt_len, int32_t budget,
+                                   int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel, int32_t* sel_rows,
+                                   double* scores_out, void* out, int32_t out_dtype, float* lse_out,
+                                   void* workspace, size_t workspace_bytes, void* stream) {
+  if (!q || !q_ref || !fire_out || !k_new || !v_new || !k_local || !v_local || !out)
+    return fail(LOUISKV_ERR_NULL, "q, q_ref, fire_out, k_new, v_new, k_local, v_local and out are required");
+  if (!reps || !unit_start || !unit_size || !k_pool || !v_pool || !sel_units || !n_sel_units || !n_sel || !sel_rows)
+    return fail(LOUISKV_ERR_NULL, "unit tables, pools and selection outputs are required");
+  int st = check_dtype(dtype);
+  if (st) return st;
+  if ((st = check_dtype(out_dtype))) return st;
+  if (d != kHeadDim) return fail(LOUISKV_ERR_UNSUPPORTED, "head dim %d not supported (only 128)", d);
+  if (n_kv_heads < 1 || n_groups < 1 || n_q_heads < 1 || n_q_heads % n_kv_heads != 0 ||
+      n_groups * n_kv_heads > INT32_MAX)
+    return fail(LOUISKV_ERR_SHAPE, "n_groups=%lld n_q_heads=%d n_kv_heads=%d", (long long)n_groups, n_q_heads,
+                n_kv_heads);
+  const int group_size = n_q_heads / n_kv_heads;
+  if (group_size != 1 && group_size != 2 && group_size != 4 && group_size != 8)
+    return fail(LOUISKV_ERR_UNSUPPORTED, "group_size=%d must be 1, 2, 4 or 8", group_size);
+  if (mode != LOUISKV_REF_PREV && mode != LOUISKV_REF_ANCHOR) return fail(LOUISKV_ERR_SHAPE, "unknown mode %d", mode);
+  if (budget < 0 || prompt_len < 0 || n_clusters < 1) 
+    return fail(LOUISKV_ERR_SHAPE, "budget=%d prompt_len=%d n_clusters=%d", budget, prompt_len, n_clusters);
+  int32_t ev = -1, n_ev = 0, n_local = 0, local_start = 0;
+  if ((st = louiskv_window_info(step, window, seg_len, &ev, &n_ev, &n_local, &local_start))) return st;
+  // units scorable at this step: the clusters and the segments evicted before it
+  int32_t n_ev_before = 0;
+  if (step > 0 && (st = louiskv_window_info(step - 1, window, seg_len, nullptr, &n_ev_before, nullptr, nullptr)))
+    return st;
+  const int64_t n_units = (int64_t)n_clusters + n_ev_before;
+  if (n_units > units_cap || n_units > kMaxUnits || (ev >= 0 && (int64_t)n_clusters + ev >= units_cap))
+    return fail(LOUISKV_ERR_SHAPE, "units %lld (and an evicted one) exceed units_cap=%d (at most %d)",
+                (long long)n_units, units_cap, kMaxUnits);
+  if ((int64_t)prompt_len + (int64_t)(ev + 1) * seg_len > pool_rows || pool_rows < 1)
+    return fail(LOUISKV_ERR_SHAPE, "segment rows exceed pool_rows=%lld", (long long)pool_rows);
+  const int64_t n_slices = n_groups * n_kv_heads;
+  const StepLayout lay = step_layout(n_slices, dtype, group_size, units_cap, budget, window);
+  if (!workspace || workspace_bytes < lay.total)
+    return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", lay.total, workspace_bytes);
+  char* ws = static_cast<char*>(workspace);
+  int32_t* sel_counter = reinterpret_cast<int32_t*>(ws + lay.counters);
+  int32_t* attn_counter = sel_counter + n_slices;
+  double* logit_ws = reinterpret_cast<double*>(ws + lay.logits);
+  double* part_max = reinterpret_cast<double*>(ws + lay.pmax);
+  const int n_parts = logit_parts(n_slices, (int)n_units);
+  int n_pad = 64;
+  while (n_pad < n_units) n_pad <<= 1;
+  const size_t lds = (size_t)n_pad * (sizeof(uint64_t) + 2 * sizeof(int));
+  const double scale = 1.0 / sqrt((double)kHeadDim);
+  hipStream_t s = as_stream(stream);
+  const unsigned grid = (unsigned)(n_slices * n_parts);
+#define LKV_STEP_SEL(T, G)                                                                                           \
+  if ((st = check_lds(reinterpret_cast<const void*>(&step_select_kernel<T, G>), lds))) return st;                    \
+  step_select_kernel<T, G><<<grid, kSelThreads, lds, s>>>(                                                           \
+      static_cast<const T*>(q), static_cast<const T*>(q_ref), n_kv_heads, tau, step == 0 ? 1 : 0, r_out, fire_out,  \
+      static_cast<const T*>(k_new), static_cast<const T*>(v_new), static_cast<T*>(k_local), static_cast<T*>(v_local), \
+      window, step, seg_len, ev, reps, unit_start, unit_size, units_cap, n_clusters, static_cast<T*>(k_pool),        \
+      static_cast<T*>(v_pool), pool_rows, prompt_len, scale, (int)n_units, budget, sel_units, n_sel_units, n_sel,     \
+      sel_rows, scores_out, logit_ws, part_max, sel_counter, n_parts, n_pad)
+#define LKV_STEP_SEL_G(T)                   \
+  switch (group_size) {                     \
+    case 1: LKV_STEP_SEL(T, 1); break;      \
+    case 2: LKV_STEP_SEL(T, 2); break;      \
+    case 4: LKV_STEP_SEL(T, 4); break;      \
+    default: LKV_STEP_SEL(T, 8); break;     \
+  }
+  if (dtype == LOUISKV_BF16) {
+    LKV_STEP_SEL_G(uint16_t)
+  } else {
+    LKV_STEP_SEL_G(float)
+  }
+#undef LKV_STEP_SEL_G
+#undef LKV_STEP_SEL
+  LKV_CHECK_LAUNCH();
+  const StepSync sync = {attn_counter, q_ref, fire_out, mode};
+  return sparse_decode_attn(q, dtype, n_slices, n_kv_heads, group_size, d, (float)scale, k_pool, v_pool, n_sel,
+                            budget, sel_rows, pool_rows, k_local, v_local, window, local_start, n_local, out,
+                            out_dtype, lse_out, ws + lay.part, lay.total - lay.part, stream, nullptr, 0, 1, &sync);
 }
 
 // ---------------------------------------------------------------------------
@@ -2201,6 +2865,7 @@ extern "C" int louiskv_retrieve_delta(const void* q, int32_t dtype, int64_t n_sl
                              logit_ws, seg_state, seg_state ? kSegRing + window : 0, s)))
     return st;
   const size_t lds = (size_t)((pool_rows + 31) / 32) * sizeof(uint32_t);
+  if ((st = check_lds(reinterpret_cast<const void*>(&delta_plan_kernel), lds))) return st;
   delta_plan_kernel<<<(unsigned)n_slices, kPlanThreads, lds, s>>>(row_ws, n_sel, fire, n_kv_heads, budget, pool_rows,
                                                                   buf_row, slot_list, fslot, frow, nfetch, n_fetched);
   LKV_CHECK_LAUNCH();

@@ -21,6 +21,10 @@ paper's Algorithm 1:
              louiskv_segment_output_boundary calls, per-slice window state
              on the device).
 
+A call over few slices (a layer at a time, the group views below) runs the
+whole step as louiskv_decode_step: the same stages in two launches that
+spread each slice over many blocks.
+
 With the pool in device memory the engine runs zero-copy by default:
 louiskv_retrieve_rows keeps KV_critical as a list of pool rows and
 louiskv_sparse_decode_attn_rows reads them from the pool, so a fired step
@@ -49,6 +53,10 @@ import torch
 from . import louiskv as L
 
 MAX_UNITS = 8192   # units one slice's retrieval scores (the library's limit)
+# a call over at most this many slices runs the decode step as louiskv_decode_step
+# (two launches, each slice spread over many blocks); larger ones use the
+# per-stage calls, whose kernels fill the chip with one block per slice
+FUSED_STEP_MAX_SLICES = 64
 
 
 @dataclass(frozen=True)
@@ -109,7 +117,8 @@ class LouisKVEngine:
     def __init__(self, cfg: EngineConfig, dtype: torch.dtype, device="cuda", pool_on_host: bool = False,
                  keep_scores: bool = False, out_dtype: Optional[torch.dtype] = None,
                  zero_copy: Optional[bool] = None, delta: Optional[bool] = None,
-                 prefill_chunk: Optional[int] = None, copy_engine: bool = True, fuse_prologue: bool = True):
+                 prefill_chunk: Optional[int] = None, copy_engine: bool = True, fuse_prologue: bool = True,
+                 fused_step: Optional[bool] = None):
         self.cfg = cfg
         self.dtype = dtype
         self.device = torch.device(device)
@@ -211,7 +220,26 @@ class LouisKVEngine:
         else:
             self.ws_retrieve = torch.empty(L.retrieve_workspace_size(S, cap, cfg.budget), **u8)
             self.ws_attn = torch.empty(max(L.sparse_decode_attn_workspace_size(S, g, rows, cfg.window), 1), **u8)
+        # the whole decode step in two launches (louiskv_decode_step): built for
+        # fixed segments over a device pool with the row-list KV_critical and
+        # group-consistent selection; fused_step=None uses it for calls over
+        # few slices (a layer at a time), True for every call, False never
+        self._fused_ok = (self.zero_copy and not pool_on_host and cfg.segments == "fixed"
+                          and cfg.trigger == "boundary" and not self.per_head
+                          and cfg.n_q_heads // cfg.n_kv_heads in (1, 2, 4, 8))
+        if fused_step and not self._fused_ok:
+            raise ValueError("the fused decode step needs fixed segments, a device pool, zero-copy retrieval "
+                             "and group-consistent selection")
+        self.fused_step = fused_step
+        self.ws_step = None
+        if self._fused_ok and fused_step is not False:
+            self.ws_step = torch.zeros(L.decode_step_workspace_size(S, dc, g, cap, cfg.budget, cfg.window), **u8)
         self.t = 0
+
+    def _use_fused_step(self) -> bool:
+        if not self._fused_ok or self.fused_step is False:
+            return False
+        return bool(self.fused_step) or self.cfg.n_slices <= FUSED_STEP_MAX_SLICES
 
     # ---------------------------------------------------------------- prefill
     def prefill(self, prompt_keys: torch.Tensor, prompt_values: torch.Tensor, init_idx: torch.Tensor,
@@ -320,6 +348,14 @@ class LouisKVEngine:
         """One decode step: q_t [G][Hq][d], k_t and v_t [S][d]."""
         c = self.cfg
         t = self.t
+        if self._use_fused_step():
+            L.decode_step(q_t, self.q_ref, c.tau, c.mode, t, self.fire, self.r, k_t, v_t, self.k_local,
+                          self.v_local, c.seg_len, self.reps, self.unit_start, self.unit_size, c.n_clusters,
+                          self.k_pool, self.v_pool, c.prompt_len, c.budget, self.sel_units, self.n_sel_units,
+                          self.n_sel, self.sel_rows, self.out, self.lse, scores_out=self.scores,
+                          workspace=self.ws_step)
+            self.t += 1
+            return
         fused = self.fuse_prologue and c.trigger == "boundary" and self.seg_state is None
         if c.trigger == "stride":
             L.fire_every(self.fire, t, c.stride)

@@ -876,3 +876,59 @@ def test_host_pool_flag_rejects_device_memory():
     assert ei.value.status == 4
     torch.cuda.synchronize()
     assert torch.all(nsel == -5) and torch.all(kb == 7)
+
+
+@pytest.mark.parametrize("case", ["bf16-anchor", "bf16-prev", "fp32-anchor"])
+def test_decode_step_equals_stage_calls(case):
+    """louiskv_decode_step (boundary, store, retrieval and attention of a step
+    in two launches, blocks of a slice handing over through the workspace)
+    against the stage calls it replaces, every step of a run with evictions:
+    decisions, r, reference queries, scores, selections, row lists, unit
+    tables, window and pool equal bit for bit; the attention output and lse
+    too in fp32 (same chunks, same merge arithmetic), within 1e-5 in bf16
+    (the step splits each slice's rows into smaller chunks).  The arrival
+    counters in the workspace are zero after every step."""
+    from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
+    dname, mname = case.split("-")
+    mode = _L().REF_PREV if mname == "prev" else _L().REF_ANCHOR
+    if dname == "bf16":
+        wl = synth.get_workload("si-lo-16k").replace(prompt_len=2048, n_clusters=64, budget=512, name="si-lo-16k")
+        n_groups, steps = 2, 300
+    else:
+        wl = synth.get_workload("tiny-4k")
+        n_groups, steps = 1, 256
+    data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(n_groups)], gen_len=steps)
+    cfg = config_from_workload(wl, n_groups=n_groups, mode=mode, gen_len=steps)
+    dt = data.prompt_keys.dtype
+    a = LouisKVEngine(cfg, dt, DEV, out_dtype=torch.float32, keep_scores=True, fused_step=False)
+    b = LouisKVEngine(cfg, dt, DEV, out_dtype=torch.float32, keep_scores=True, fused_step=True)
+    for e in (a, b):
+        e.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    S = cfg.n_slices
+    fires = evictions = 0
+    for t in range(steps):
+        a.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        b.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        torch.cuda.synchronize()
+        assert torch.equal(a.fire, b.fire), t
+        assert torch.equal(a.r.view(torch.int64), b.r.view(torch.int64)), t
+        for name in ("q_ref", "n_sel", "n_sel_units", "scores", "reps", "unit_start", "unit_size", "k_local",
+                     "v_local"):
+            assert torch.equal(getattr(a, name), getattr(b, name)), (t, name)
+        written = wl.prompt_len + _L().window_info(t, wl.window, wl.seg_len)[1] * wl.seg_len   # pool rows so far
+        assert torch.equal(a.k_pool[:, :written], b.k_pool[:, :written]), t
+        assert torch.equal(a.v_pool[:, :written], b.v_pool[:, :written]), t
+        for i in range(S):
+            assert torch.equal(a.sel_units[i, :int(a.n_sel_units[i])], b.sel_units[i, :int(b.n_sel_units[i])]), (t, i)
+            assert torch.equal(a.sel_rows[i, :int(a.n_sel[i])], b.sel_rows[i, :int(b.n_sel[i])]), (t, i)
+        if dname == "fp32":
+            assert torch.equal(a.out, b.out) and torch.equal(a.lse, b.lse), t
+        else:
+            err = (a.out - b.out).abs().max().item()
+            assert err <= 1e-5 * max(1.0, a.out.abs().max().item()), (t, err)
+            assert (a.lse - b.lse).abs().max().item() <= 1e-5, t
+        assert int(b.ws_step[:8 * S].view(torch.int32).abs().sum()) == 0, t
+        fires += int(a.fire.sum())
+        evictions += int(_L().window_info(t, wl.window, wl.seg_len)[0] >= 0)
+    print(f"[decode step] {case}: {steps} steps, {fires} group fires, {evictions} evictions", flush=True)
+    assert fires >= (2 if mname == "prev" else 20) and evictions > 2
