@@ -42,6 +42,7 @@ if ROOT not in sys.path:
 
 METRIC = "prompt keys clustered/s; retrieval+sparse-attn decode steps/s at 32K ctx"
 PEAK_BF16_TFLOPS = 2500.0
+PEAK_FP32_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "kmeans_assign_traffic_li-so-32k.md")
 ASSIGN_SOURCES = [os.path.join(ROOT, "paper_2510_11292_amd", "csrc", f) for f in ("kmeans.hip", "common.h")]
@@ -189,27 +190,39 @@ def dense_decode_ms(wl, data, cfg, dtype, reps=2):
     return ms / reps
 
 
-def layer_by_layer_decode_ms(eng, data, wl, n_steps, reps=2):
-    """The first n_steps decode steps with every step run group by group (one
-    launch sequence per layer of the sequence, the order in which a model
+def layer_by_layer_decode_ms(eng, data, wl, n_steps, reps=2, t0=0):
+    """Decode steps t0 .. t0 + n_steps - 1 with every step run group by group
+    (one launch sequence per layer of the batch, the order in which a model
     produces its queries), one HIP graph per decode step (as a serving loop
-    captures its steps), replayed after a fresh prefill; mean ms of the loop."""
+    captures its steps), replayed after a fresh prefill and the first t0 steps
+    (one batched graph, untimed); mean ms of the timed steps."""
     import torch
 
     def one_step(t):
         # one launch sequence per layer: the batch's groups of a layer are contiguous
         eng.step_layer_by_layer(data.queries[t], data.gen_keys[t], data.gen_values[t], groups_per_launch=wl.batch)
+
+    def advance():
+        for t in range(t0):
+            eng.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
     eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
-        for t in range(n_steps):
+        advance()
+        for t in range(t0, t0 + n_steps):
             one_step(t)
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
+    pre = None
+    if t0 > 0:
+        pre = torch.cuda.CUDAGraph()
+        eng.t = 0
+        with torch.cuda.graph(pre):
+            advance()
     graphs = []
-    eng.t = 0
-    for t in range(n_steps):
+    eng.t = t0
+    for t in range(t0, t0 + n_steps):
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             one_step(t)
@@ -217,6 +230,8 @@ def layer_by_layer_decode_ms(eng, data, wl, n_steps, reps=2):
     ms = 0.0
     for _ in range(reps):
         eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+        if pre is not None:
+            pre.replay()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         for g in graphs:
@@ -224,8 +239,47 @@ def layer_by_layer_decode_ms(eng, data, wl, n_steps, reps=2):
         e1.record()
         torch.cuda.synchronize()
         ms += e0.elapsed_time(e1)
-    del graphs
+    del graphs, pre
     return ms / reps
+
+
+def layer_roofline(attn_bytes: float, sec_per_step: float) -> dict:
+    """HBM fraction of the layer-by-layer decode: the K/V rows one step
+    attends to over all layers (the attention kernel's algorithmic bytes on
+    the final state, the dominant traffic of a step) per measured step time."""
+    achieved = attn_bytes / sec_per_step / 1e9
+    return {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS, "bytes_per_step": attn_bytes, "us_per_step": sec_per_step * 1e6}
+
+
+def layer_window(wl, n: int = 512):
+    """The decode steps timed group by group: the last n of the generation,
+    where the most evicted segments are units."""
+    n = min(n, wl.gen_len)
+    return wl.gen_len - n, n
+
+
+def delta_fetch_rate(eng, data, wl) -> dict:
+    """Host-link rate of the delta transfers: one louiskv_retrieve_delta with
+    every group fired on the engine's final state, with an early query, so
+    that many selected rows are new; bytes moved over the host link / time."""
+    import torch
+    from paper_2510_11292_amd import louiskv as L
+    c = eng.cfg
+    fire = torch.ones_like(eng.fire)
+    fired = eng.fire
+    eng.fire = fire
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    n_units = eng.n_units_before(c.gen_len - 1)
+    e0.record()
+    eng._retrieve_delta(data.queries[0], n_units, eng.seg_state)
+    e1.record()
+    torch.cuda.synchronize()
+    moved = int(eng.n_fetched.sum()) * 2 * c.head_dim * eng.k_buf.element_size()
+    sec = e0.elapsed_time(e1) / 1e3
+    eng.fire = fired
+    return {"delta_fetch_GBps": moved / sec / 1e9, "delta_fetch_bytes": moved, "delta_call_ms": sec * 1e3,
+            "what": "one louiskv_retrieve_delta (scores, selection, plan, fetch) with every group fired"}
 
 
 def copy_calibration(mib: int):
@@ -391,6 +445,95 @@ def time_pipelined_prefill(eng, data, chunk: int, copy_engine: bool, reps: int =
     return total / reps
 
 
+def workload_pass(name: str, dev: str, layer_steps: int = 512) -> dict:
+    """One stated timed pass of a workload other than the headline one, after
+    one untimed pass: the clustering (keys/s and the assignment kernel's MFMA
+    fraction, from HIP events on its stream), the decode loop as one HIP graph
+    (steps/s), the attention kernel on the final state (GB/s and HBM
+    fraction), the last `layer_steps` decode steps group by group (steps/s)
+    and, for a host-resident pool, the host-link rates of the same run."""
+    import torch
+    import synth
+    from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
+    from paper_2510_11292_amd import louiskv as L
+    wl = synth.get_workload(name)
+    t_start = time.time()
+    # layer-major group order: a layer of the batch is one contiguous view
+    data = make_inputs(wl, dev, layer_major=wl.batch > 1)
+    cfg = config_from_workload(wl, mode=L.REF_ANCHOR)
+    dtype = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    eng = LouisKVEngine(cfg, dtype, dev, pool_on_host=wl.pool_on_host)
+    iters = wl.n_iters
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * iters)] for _ in range(2)]
+    for evs in ev:
+        for e in evs:
+            e.record()
+    ph = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(2)]
+
+    def decode_all():
+        for t in range(wl.gen_len):
+            eng.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+    eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        decode_all()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    eng.t = 0
+    with torch.cuda.graph(graph):
+        decode_all()
+    for i in range(2):
+        ph[i][0].record()
+        eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx, iter_events=ev[i], pack_event=ph[i][3])
+        ph[i][1].record()
+        graph.replay()
+        ph[i][2].record()
+    torch.cuda.synchronize()
+    t_cluster = ph[1][0].elapsed_time(ph[1][3]) / 1e3
+    t_pre = ph[1][0].elapsed_time(ph[1][1]) / 1e3
+    t_dec = ph[1][1].elapsed_time(ph[1][2]) / 1e3
+    t_assign = sum(ev[1][2 * k].elapsed_time(ev[1][2 * k + 1]) for k in range(iters)) / iters / 1e3
+    flops = 2.0 * wl.prompt_len * wl.n_clusters * wl.head_dim * wl.n_slices
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
+    t_attn, attn_bytes = time_attention(eng, wl)
+    out = {
+        "config": {"batch": wl.batch, "layers": wl.n_layers, "kv_heads": wl.n_kv_heads, "prompt_tokens":
+                   wl.prompt_len, "clusters": wl.n_clusters, "decode_steps": wl.gen_len, "budget": wl.budget,
+                   "dtype": wl.dtype, "pool": "pinned host" if wl.pool_on_host else "hbm"},
+        "timed": "one pass (prefill + every decode step) after one untimed pass",
+        "keys_per_s": wl.n_slices * wl.prompt_len / t_cluster,
+        "cluster_ms": t_cluster * 1e3, "pool_pack_ms": (t_pre - t_cluster) * 1e3,
+        "assign_roofline": {"achieved": flops / t_assign / 1e12, "peak": peak, "unit": "TFLOP/s",
+                            "frac": flops / t_assign / 1e12 / peak, "avg_launch_ms": t_assign * 1e3,
+                            "bound": "mfma", "dtype": wl.dtype},
+        "decode_steps_per_s": wl.gen_len / t_dec,
+        "attention_roofline": {"achieved": attn_bytes / t_attn / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                               "frac": attn_bytes / t_attn / 1e9 / PEAK_HBM_GBS, "avg_launch_us": t_attn * 1e6,
+                               "bytes_per_launch": attn_bytes, "bound": "hbm",
+                               "reads": "the pool rows of the selection (row list)" if eng.zero_copy else
+                                        "the HBM KV_critical buffers (slot list)"},
+    }
+    del graph
+    t0, n = layer_window(wl, layer_steps)
+    lms = layer_by_layer_decode_ms(eng, data, wl, n, reps=1, t0=t0)
+    out["decode_steps_per_s_layer_by_layer"] = n / (lms / 1e3)
+    out["layer_by_layer_steps"] = f"steps {t0}..{t0 + n - 1} of {wl.gen_len}, one HIP graph per step"
+    out["layer_by_layer_roofline"] = layer_roofline(attn_bytes, lms / 1e3 / n)
+    if eng.pool_on_host:
+        out["host_link"] = host_link_rates(eng, data)
+        out["host_link"].update(delta_fetch_rate(eng, data, wl))
+    log(f"{name}: {out['keys_per_s']:.3g} keys/s (assign {out['assign_roofline']['frac']:.3f} of peak), decode "
+        f"{out['decode_steps_per_s']:.0f} steps/s, layer by layer {out['decode_steps_per_s_layer_by_layer']:.0f}, "
+        f"attention {out['attention_roofline']['achieved']:.0f} GB/s; {time.time() - t_start:.0f}s")
+    del eng, data
+    torch.cuda.empty_cache()
+    if hasattr(torch._C, "_host_emptyCache"):
+        torch._C._host_emptyCache()
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -409,6 +552,8 @@ def main() -> int:
                          "(default: one layer's KV heads; -1 skips it)")
     ap.add_argument("--no-layer-by-layer", action="store_true",
                     help="skip the decode timing with one launch sequence per layer")
+    ap.add_argument("--workloads", default="tiny-4k,si-lo-16k,li-lo-32k-b4,host-131k",
+                    help="other workloads timed after the headline one, one pass each ('none' skips them)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after the run, copy this many MiB three times (counter calibration for profiles)")
     args = ap.parse_args()
@@ -512,25 +657,19 @@ def main() -> int:
     dense_ms = None
     if (eng.zero_copy or eng.delta) and not args.eager:
         dense_ms = dense_decode_ms(wl, data, cfg, dtype)
-    layer_ms = layer_steps = None
+    layer_ms = layer_steps = layer_t0 = None
     if not args.eager and not args.no_layer_by_layer:
-        if eng.pool_on_host:
-            # not timed: capturing this path group by group (the whole loop
-            # as one graph) ended in a host segmentation fault whose cause
-            # is not established
-            log("decode layer by layer: not timed for a host-resident pool")
-        else:
-            layer_steps = min(wl.gen_len, 512)
-            if wl.batch > 1:
-                # one launch sequence per layer needs the batch's groups of a
-                # layer next to each other (the batched loop above runs faster
-                # with the sequence-major order)
-                del data
-                torch.cuda.empty_cache()
-                data = make_inputs(wl, dev, layer_major=True)
-            layer_ms = layer_by_layer_decode_ms(eng, data, wl, layer_steps)
-            log(f"decode layer by layer: {layer_steps} steps in {layer_ms:.2f} ms "
-                f"({layer_steps / (layer_ms / 1e3):.0f} steps/s)")
+        layer_t0, layer_steps = layer_window(wl)
+        if wl.batch > 1:
+            # one launch sequence per layer needs the batch's groups of a
+            # layer next to each other (the batched loop above runs faster
+            # with the sequence-major order)
+            del data
+            torch.cuda.empty_cache()
+            data = make_inputs(wl, dev, layer_major=True)
+        layer_ms = layer_by_layer_decode_ms(eng, data, wl, layer_steps, t0=layer_t0)
+        log(f"decode layer by layer: steps {layer_t0}..{layer_t0 + layer_steps - 1} in {layer_ms:.2f} ms "
+            f"({layer_steps / (layer_ms / 1e3):.0f} steps/s)")
     link = None
     if eng.pool_on_host:
         link = host_link_rates(eng, data)
@@ -576,6 +715,10 @@ def main() -> int:
         "decode_steps_per_s": wl.gen_len / t_dec,
         "decode_steps_per_s_gathered_kv_critical": (wl.gen_len / (dense_ms / 1e3)) if dense_ms else None,
         "decode_steps_per_s_layer_by_layer": (layer_steps / (layer_ms / 1e3)) if layer_ms else None,
+        "layer_by_layer_steps": (f"steps {layer_t0}..{layer_t0 + layer_steps - 1} of {wl.gen_len}, one HIP graph "
+                                 f"per step, {wl.n_layers} launch sequences per step") if layer_ms else None,
+        "layer_by_layer_roofline": (layer_roofline(attn_bytes, layer_ms / 1e3 / layer_steps)
+                                    if layer_ms else None),
         "delta_rows_moved_per_selected": (float(moved[0]) / max(float(moved[1]), 1.0)) if eng.delta else None,
         "prefill_ms": t_pre * 1e3,
         "cluster_ms": t_cluster * 1e3,
@@ -609,6 +752,11 @@ def main() -> int:
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(wl, data, args.cpu_budget_s)
+    others = [w for w in args.workloads.split(",") if w and w != "none" and w != wl.name]
+    if others:
+        del eng, data
+        torch.cuda.empty_cache()
+        out["workloads"] = {w: workload_pass(w, dev) for w in others}
     print(json.dumps(out), flush=True)
     return 0
 

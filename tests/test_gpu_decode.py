@@ -932,3 +932,60 @@ def test_decode_step_equals_stage_calls(case):
         evictions += int(_L().window_info(t, wl.window, wl.seg_len)[0] >= 0)
     print(f"[decode step] {case}: {steps} steps, {fires} group fires, {evictions} evictions", flush=True)
     assert fires >= (2 if mname == "prev" else 20) and evictions > 2
+
+
+@pytest.mark.parametrize("case", ["host-delta", "fused-device"])
+def test_layer_by_layer_step_graphs_match_eager(case):
+    """The group-by-group decode captured as one HIP graph per step (as the
+    benchmark times it) and replayed twice after fresh prefills equals the
+    eager group-by-group loop: over a pinned host pool with delta transfers
+    (interior pointers of the pool resolved per group view at capture time),
+    and over a device pool, where each view runs the two-launch decode step
+    whose workspace counters must return to zero on every replay."""
+    from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
+    host = case == "host-delta"
+    if host:
+        wl = synth.get_workload("host-131k").replace(prompt_len=2048, n_clusters=64, budget=512, name="host-131k")
+    else:
+        wl = synth.get_workload("si-lo-16k").replace(prompt_len=2048, n_clusters=64, budget=512, name="si-lo-16k")
+    steps, G = 96, 2
+    data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(G)], gen_len=steps)
+    cfg = config_from_workload(wl, n_groups=G, gen_len=steps)
+    eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, pool_on_host=host, out_dtype=torch.float32)
+    if not host:
+        assert eng.group_view(0)._use_fused_step()
+    hist = torch.zeros(steps, *eng.out.shape, device=DEV)
+    hist_n = torch.zeros(steps, *eng.n_sel.shape, dtype=torch.int32, device=DEV)
+
+    def one_step(t):
+        eng.step_layer_by_layer(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        hist[t].copy_(eng.out)
+        hist_n[t].copy_(eng.n_sel)
+    eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    for t in range(steps):
+        one_step(t)
+    torch.cuda.synchronize()
+    ref, ref_n = hist.clone(), hist_n.clone()
+    assert int((ref_n > 0).sum()) > 0
+    graphs = []
+    eng.t = 0
+    for t in range(steps):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            one_step(t)
+        graphs.append(g)
+    print(f"captured {len(graphs)} step graphs ({case})", flush=True)
+    for rep in range(2):
+        hist.zero_()
+        hist_n.zero_()
+        eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+        torch.cuda.synchronize()
+        for g in graphs:
+            g.replay()
+        torch.cuda.synchronize()
+        print(f"step-graph replay {rep} ({case})", flush=True)
+        assert torch.equal(hist, ref), (case, rep)
+        assert torch.equal(hist_n, ref_n), (case, rep)
+        if not host:
+            assert int(eng.ws_step[:8 * cfg.n_slices].view(torch.int32).abs().sum()) == 0
+    del graphs
