@@ -577,7 +577,8 @@ def main() -> int:
     wl = synth.get_workload(args.workload)
     mode = L.REF_ANCHOR if args.mode == "anchor" else L.REF_PREV
     data = make_inputs(wl, dev)
-    cfg = config_from_workload(wl, mode=mode, segments=args.segments)
+    cfg = config_from_workload(wl, mode=mode, segments=args.segments,
+                               allow_unit_overflow=args.segments == "boundary")
     dtype = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
     eng = LouisKVEngine(cfg, dtype, dev, pool_on_host=wl.pool_on_host)
 
@@ -720,6 +721,7 @@ def main() -> int:
         "layer_by_layer_roofline": (layer_roofline(attn_bytes, layer_ms / 1e3 / layer_steps)
                                     if layer_ms else None),
         "delta_rows_moved_per_selected": (float(moved[0]) / max(float(moved[1]), 1.0)) if eng.delta else None,
+        "segment_overflow": eng.segment_overflow() if args.segments == "boundary" else None,
         "prefill_ms": t_pre * 1e3,
         "cluster_ms": t_cluster * 1e3,
         "pool_pack_ms": t_pack * 1e3,

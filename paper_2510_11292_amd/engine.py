@@ -81,17 +81,28 @@ class EngineConfig:
     index: str = "clusters"    # "clusters" (k-means) or "pages" (n_clusters is then the page count)
     page_len: int = 16
     selection: str = "group"   # "group" (group-consistent) or "per_head"
+    # boundary segments: a generation can evict up to one segment per step,
+    # more units than a slice's retrieval can score (MAX_UNITS).  Such a
+    # configuration is refused unless the caller accepts that segments past
+    # the limit are dropped; segment_overflow() then reports whether any was.
+    allow_unit_overflow: bool = False
 
     @property
     def n_groups(self) -> int:
         return self.n_slices // self.n_kv_heads
 
     @property
+    def units_needed(self) -> int:
+        """Units a slice can reach: clusters plus the segments the window can evict."""
+        if self.segments == "boundary":
+            return self.n_clusters + max(0, self.gen_len - self.window)   # one segment per step at most
+        ev = 0 if self.gen_len <= self.window else (self.gen_len - self.window + self.seg_len - 1) // self.seg_len
+        return self.n_clusters + ev
+
+    @property
     def units_cap(self) -> int:
         if self.segments == "boundary":
-            # at most one segment leaves per step once the window is full; the
-            # scorer handles at most MAX_UNITS units per slice
-            return min(self.n_clusters + max(0, self.gen_len - self.window), MAX_UNITS)
+            return min(self.units_needed, MAX_UNITS)
         ev = 0 if self.gen_len <= self.window else (self.gen_len - self.window + self.seg_len - 1) // self.seg_len
         return self.n_clusters + ev
 
@@ -183,6 +194,11 @@ class LouisKVEngine:
         self.scores = torch.zeros(nl, cap, dtype=torch.float64, device=dev) if keep_scores else None
         if cfg.segments not in ("fixed", "boundary"):
             raise ValueError(cfg.segments)
+        if cfg.units_needed > MAX_UNITS and not cfg.allow_unit_overflow:
+            raise ValueError(f"up to {cfg.units_needed} units per slice ({cfg.n_clusters} clusters and the segments "
+                             f"of {cfg.gen_len} steps) exceed the {MAX_UNITS} a retrieval scores; segments past "
+                             f"the limit would not be attended. Pass allow_unit_overflow=True to accept that and "
+                             f"check segment_overflow().")
         self.seg_state = (torch.zeros(S, L.segment_state_ints(cfg.window), **i32)
                           if cfg.segments == "boundary" else None)
         dc = L.BF16 if dtype == torch.bfloat16 else L.F32
@@ -235,6 +251,14 @@ class LouisKVEngine:
         if self._fused_ok and fused_step is not False:
             self.ws_step = torch.zeros(L.decode_step_workspace_size(S, dc, g, cap, cfg.budget, cfg.window), **u8)
         self.t = 0
+
+    def segment_overflow(self) -> bool:
+        """True if some evicted segment could not become a unit (the unit table
+        was full), so its tokens are no longer attended (boundary segments;
+        reads the state's overflow flag, a device-to-host copy)."""
+        if self.seg_state is None:
+            return False
+        return bool((self.seg_state[:, 4] != 0).any())
 
     def _use_fused_step(self) -> bool:
         if not self._fused_ok or self.fused_step is False:

@@ -989,3 +989,38 @@ def test_layer_by_layer_step_graphs_match_eager(case):
         if not host:
             assert int(eng.ws_step[:8 * cfg.n_slices].view(torch.int32).abs().sum()) == 0
     del graphs
+
+
+def test_boundary_segment_overflow_is_reported():
+    """Boundary-delimited segments with every step firing (tau > 1): each
+    token is a segment of its own, so after W + (8192 - C) steps the unit
+    table (8192 units, the most a retrieval scores) is full.  The engine
+    refuses the configuration unless told to accept dropped segments; with
+    that, segments keep becoming units while there is room (the flag stays
+    clear and the unit count grows by one per step) and the first one that
+    does not fit raises the overflow flag, which segment_overflow() reports."""
+    from paper_2510_11292_amd.engine import LouisKVEngine, MAX_UNITS, config_from_workload
+    wl = synth.get_workload("si-lo-16k").replace(prompt_len=256, n_clusters=32, budget=64, window=64, seg_len=16,
+                                                 tau=1.5, name="si-lo-16k")
+    full_at = wl.window + (MAX_UNITS - wl.n_clusters)      # first step whose segment finds no room
+    steps = full_at + 24
+    data = synth.make_slices(wl, DEV, groups=[(0, 0)], gen_len=steps)
+    cfg = config_from_workload(wl, n_groups=1, gen_len=steps, segments="boundary")
+    with pytest.raises(ValueError, match="allow_unit_overflow"):
+        LouisKVEngine(cfg, torch.bfloat16, DEV)
+    cfg = config_from_workload(wl, n_groups=1, gen_len=steps, segments="boundary", allow_unit_overflow=True)
+    assert cfg.units_cap == MAX_UNITS
+    eng = LouisKVEngine(cfg, torch.bfloat16, DEV, out_dtype=torch.float32)
+    eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    for t in range(steps):
+        eng.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        if t in (full_at - 1, full_at):
+            torch.cuda.synchronize()
+            n_units = to_np(eng.seg_state[:, 0])
+            if t == full_at - 1:
+                assert (n_units == MAX_UNITS).all() and not eng.segment_overflow(), (t, n_units)
+            else:
+                assert eng.segment_overflow(), t
+    torch.cuda.synchronize()
+    assert bool(eng.fire.all()) and eng.segment_overflow()
+    print(f"[overflow] unit table full at step {full_at - 1}; overflow reported from step {full_at}", flush=True)

@@ -295,7 +295,9 @@ def test_decode_full_shape_boundary_segments(name):
     L = _L()
     wl = synth.get_workload(name)
     data = synth.make_slices(wl, DEV)
-    cfg = config_from_workload(wl, mode=L.REF_ANCHOR, segments="boundary")
+    # 16K steps could evict more segments than a slice can score; the run
+    # accepts that and then checks that no segment was dropped
+    cfg = config_from_workload(wl, mode=L.REF_ANCHOR, segments="boundary", allow_unit_overflow=True)
     eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, pool_on_host=wl.pool_on_host, keep_scores=True,
                         out_dtype=torch.float32)
     eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
@@ -321,7 +323,7 @@ def test_decode_full_shape_boundary_segments(name):
             if fire[gi]:
                 last_fire[gi] = t
     st = to_np(eng.seg_state)
-    assert (st[:, 4] == 0).all()
+    assert (st[:, 4] == 0).all() and not eng.segment_overflow()
     assert stats["fires"] > 0 and stats["evictions"] > 0
     assert stats["checked"] >= 2 * len(steps)
     report(f"full-shape boundary-segment decode {name}", stats, bound=max(3, stats["fires"] // 100),

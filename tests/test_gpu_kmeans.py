@@ -296,3 +296,61 @@ def test_cluster_prefill_pipelined_equals_one_pass(dtype, S, N, C, chunk, host, 
     idx = ref["perm"][S - 1].long()
     assert torch.equal(k_seen[S - 1, :N], keys[S - 1, idx])
     assert torch.equal(v_seen[S - 1, :N], values[S - 1, idx])
+
+
+@pytest.mark.parametrize("host", [True, False])
+def test_cluster_prefill_pipelined_matches_oracle(host):
+    """The pipelined prefill (chunks of one layer's slices, each chunk's pool
+    write on a copy stream beside the next chunk's clustering) against the
+    oracle directly: for every slice of two groups of a reduced host-131k
+    workload, the oracle's k-means and cluster-by-cluster packing
+    (prefill_state_from_kmeans) equal the GPU's centroids, unit table and pool,
+    with any divergent run step-locked iteration by iteration through the
+    pipelined call itself."""
+    from parity_utils import check_prefill_against_state, oracle_prefill_state
+    L = _L()
+    wl = synth.get_workload("host-131k").replace(prompt_len=2048, n_clusters=64, name="host-131k")
+    data = synth.make_slices(wl, DEV, groups=[(0, 0), (0, 1)], gen_len=1)
+    S, N, C, H = data.n_slices, wl.prompt_len, wl.n_clusters, wl.n_kv_heads
+    dt = data.prompt_keys.dtype
+
+    def run(iters):
+        reps = torch.zeros(S, C, 128, device=DEV)
+        ustart = torch.zeros(S, C, dtype=torch.int32, device=DEV)
+        usize = torch.zeros_like(ustart)
+        assign = torch.zeros(S, N, dtype=torch.int32, device=DEV)
+        perm = torch.zeros_like(assign)
+        if host:
+            kp = torch.zeros(S, N, 128, dtype=dt).pin_memory()
+            vp = torch.zeros(S, N, 128, dtype=dt).pin_memory()
+        else:
+            kp = torch.zeros(S, N, 128, dtype=dt, device=DEV)
+            vp = torch.zeros(S, N, 128, dtype=dt, device=DEV)
+        events = [torch.cuda.Event() for _ in range(-(-S // H) + 1)]
+        for e in events:
+            e.record()
+        L.cluster_prefill_pipelined(data.prompt_keys, C, iters, data.init_idx, reps, ustart, usize, assign, perm,
+                                    data.prompt_values, kp, vp, H, events, torch.cuda.Stream(), pool_on_host=host,
+                                    copy_engine=True)
+        torch.cuda.synchronize()
+        return reps, ustart, usize, assign, kp, vp
+
+    reps, ustart, usize, assign, kp, vp = run(wl.n_iters)
+    cache = {}
+
+    def states(it):
+        if it not in cache:
+            r = run(it)
+            cache[it] = (to_np(r[3]).astype(np.int64), to64(r[0]))
+        return cache[it]
+    k_excused = adopted = 0
+    for gi in range(2):
+        sl = slice(gi * H, (gi + 1) * H)
+        st, ex, ad = oracle_prefill_state(to64(data.prompt_keys[sl]), to64(data.prompt_values[sl]),
+                                          to_np(data.init_idx[sl]), wl.n_iters, True, to_np(assign[sl]),
+                                          to64(reps[sl]), states, list(range(sl.start, sl.stop)))
+        check_prefill_against_state(reps[sl], ustart[sl], usize[sl], kp[sl], vp[sl], st, N)
+        k_excused += ex
+        adopted += ad
+    report(f"pipelined prefill vs oracle host={host}", dict(excused=k_excused, adopted=adopted),
+           bound=max(2, S * N * wl.n_iters // 10000), of="assignment near-ties")
