@@ -279,7 +279,8 @@ def delta_fetch_rate(eng, data, wl) -> dict:
     sec = e0.elapsed_time(e1) / 1e3
     eng.fire = fired
     return {"delta_fetch_GBps": moved / sec / 1e9, "delta_fetch_bytes": moved, "delta_call_ms": sec * 1e3,
-            "what": "one louiskv_retrieve_delta (scores, selection, plan, fetch) with every group fired"}
+            "what": f"one {'louiskv_retrieve_cached' if eng.cached else 'louiskv_retrieve_delta'} (scores, "
+                    f"selection, plan, fetch) with every group fired"}
 
 
 def copy_calibration(mib: int):
@@ -473,11 +474,22 @@ def workload_pass(name: str, dev: str, layer_steps: int = 512) -> dict:
     def decode_all():
         for t in range(wl.gen_len):
             eng.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+    # rows copied into KV_critical against rows selected over the fired slices
+    # of the untimed pass (counted on the device)
+    moved = torch.zeros(2, dtype=torch.int64, device=dev)
+
+    def decode_all_counting():
+        for t in range(wl.gen_len):
+            eng.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+            if eng.delta:
+                fired = eng.fire.repeat_interleave(wl.n_kv_heads).bool()
+                moved[0] += eng.n_fetched.sum()
+                moved[1] += torch.where(fired, eng.n_sel, 0).sum()
     eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
-        decode_all()
+        decode_all_counting()
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
     graph = torch.cuda.CUDAGraph()
@@ -524,6 +536,10 @@ def workload_pass(name: str, dev: str, layer_steps: int = 512) -> dict:
     if eng.pool_on_host:
         out["host_link"] = host_link_rates(eng, data)
         out["host_link"].update(delta_fetch_rate(eng, data, wl))
+        mv = moved.tolist()
+        out["host_link"].update({"kv_critical_rows": eng.cache_rows, "budget": wl.budget,
+                                 "fetched_rows": mv[0], "selected_rows": mv[1],
+                                 "fetched_fraction": mv[0] / max(mv[1], 1)})
     log(f"{name}: {out['keys_per_s']:.3g} keys/s (assign {out['assign_roofline']['frac']:.3f} of peak), decode "
         f"{out['decode_steps_per_s']:.0f} steps/s, layer by layer {out['decode_steps_per_s_layer_by_layer']:.0f}, "
         f"attention {out['attention_roofline']['achieved']:.0f} GB/s; {time.time() - t_start:.0f}s")

@@ -691,6 +691,44 @@ int louiskv_retrieve_delta(const void* q, int32_t dtype, int64_t n_slices,
                            int32_t* n_fetched, double* scores_out,
                            void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * louiskv_retrieve_delta with a larger buffer kept as a least-recently-used
+ * cache of pool rows: cache_rows >= budget slots per slice, so that rows
+ * selected at earlier boundaries and selected again stay in HBM (Appendix A
+ * names the transfer as the remaining bottleneck; rows tend to return because
+ * adjacent selections overlap, Section 4.1 Observation 1).  For every fired
+ * slice at decode step `step`: the same scores, ranking and prefix-stop
+ * selection; a slot whose row is selected again keeps it; the k newly
+ * selected rows (rank order) go to the k slots, among those not selected at
+ * this step, with the smallest (slot_step, slot index), i.e. empty slots
+ * first, then the rows selected longest ago, paired in slot order, and are
+ * copied from the pool; slot_list lists the n_sel slots holding the
+ * selection, in slot order.  Attend with louiskv_sparse_decode_attn_rows over
+ * k_buf/v_buf as the pool (cache_rows rows) and slot_list as the row list.
+ * buf_row    in/out [n_slices][cache_rows] int32: pool row of each slot, -1
+ *            when empty; all -1 before the first retrieval.
+ * slot_step  in/out [n_slices][cache_rows] int32: decode step at which the
+ *            slot's row was last selected, -1 when empty; reset together
+ *            with buf_row.  Steps must grow from call to call (0 <= step <
+ *            2^24 - 1); a stale state (not reset) can leave rows without a
+ *            slot, never write outside the buffers.
+ * k_buf, v_buf  [n_slices][cache_rows][d] dtype.  slot_list [n_slices][budget].
+ * Workspace louiskv_retrieve_delta_workspace_size().  Other arguments as
+ * louiskv_retrieve_delta.
+ */
+int louiskv_retrieve_cached(const void* q, int32_t dtype, int64_t n_slices,
+                            int32_t n_kv_heads, int32_t group_size, int32_t d, double scale,
+                            const float* reps, const int32_t* unit_start,
+                            const int32_t* unit_size, int32_t units_cap, int32_t n_units,
+                            const int32_t* seg_state, int32_t window,
+                            const void* k_pool, const void* v_pool, int64_t pool_rows,
+                            int32_t pool_on_host, int32_t budget, int32_t cache_rows,
+                            int32_t step, const uint8_t* fire, int32_t* sel_units,
+                            int32_t* n_sel_units, int32_t* n_sel, void* k_buf, void* v_buf,
+                            int32_t* buf_row, int32_t* slot_step, int32_t* slot_list,
+                            int32_t* n_fetched, double* scores_out,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Ablation baselines                                                        */
 /* ------------------------------------------------------------------------ */

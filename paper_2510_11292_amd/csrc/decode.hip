@@ -663,22 +663,23 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
     __syncthreads();
     if (w == 0) {
       // lane l holds digits 255 - 4l .. 252 - 4l, highest first
-      int64_t v[4];
+      // (a slice's tokens, hence every sum below, stay under 2^31)
+      int v[4];
       int cnt[4];
-      int64_t tot = 0;
+      int tot = 0;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         uint64_t h = 0;
 #pragma unroll
         for (int q2 = 0; q2 < kHists; ++q2) h += s_hist[set][q2][255 - 4 * lane - i];
-        v[i] = (int64_t)(h >> 16);
+        v[i] = (int)(h >> 16);
         cnt[i] = (int)(h & 0xffffu);
         tot += v[i];
       }
-      int64_t incl = tot;
+      int incl = tot;
 #pragma unroll
       for (int o = 1; o < 64; o <<= 1) {
-        const int64_t y = __shfl_up(incl, o, kWave);
+        const int y = __shfl_up(incl, o, kWave);
         if (lane >= o) incl += y;
       }
       int64_t cum = incl - tot;   // tokens of the digits above this lane's
@@ -1241,7 +1242,204 @@ void delta_plan_kernel(const int32_t* __restrict__ row_ws, const int32_t* __rest
     const bool v = i < budget && brow[i] >= 0;
     int ex;
     const int tot = block_scan_flag(v, s_w, ex);
-    if (v) slot_list[(size_t)s * budget + s_base[2] + ex] = i;
+    if (v && s_base[2] + ex < budget) slot_list[(size_t)s * budget + s_base[2] + ex] = i;
+    __syncthreads();
+    if (tid == 0) s_base[2] += tot;
+    __syncthreads();
+  }
+}
+
+// KV_critical as an LRU cache of pool rows: cache_rows >= budget slots per
+// slice, slot_step[s][i] the decode step at which slot i's row was last
+// selected (-1: empty).  For a fired slice at decode step `step`:
+//  - every slot whose row is selected again keeps it (slot_step = step);
+//  - the k newly selected rows (selection order) go to the k other slots with
+//    the smallest (slot_step, slot), paired in slot order: empty slots first,
+//    then the rows selected longest ago;
+//  - slot_list lists the n_sel slots holding the selection, in slot order.
+// The k-th smallest slot_step + 1 among the candidates comes from a radix
+// select over 24 bits (8 per pass, per-wave histograms), the ties at the
+// threshold in slot order from a block scan.
+constexpr int kCacheMaxStep = (1 << 24) - 2;
+
+__global__ __launch_bounds__(kPlanThreads)
+void cache_plan_kernel(const int32_t* __restrict__ row_ws, const int32_t* __restrict__ n_sel,
+                       const uint8_t* __restrict__ fire, int n_kv_heads, int budget, int cache_rows,
+                       int64_t pool_rows, int step, int32_t* __restrict__ buf_row, int32_t* __restrict__ slot_step,
+                       int32_t* __restrict__ slot_list, int32_t* __restrict__ fetch_slot,
+                       int32_t* __restrict__ fetch_row, int32_t* __restrict__ n_fetch,
+                       int32_t* __restrict__ n_fetch_out) {
+  extern __shared__ uint32_t s_bits[];   // one bit per pool row
+  __shared__ int s_w[kPlanWaves];
+  __shared__ int s_hist[kPlanWaves][256];
+  __shared__ int s_base[3];
+  __shared__ int s_k, s_below, s_thr, s_take_eq, s_victims;
+  const int64_t s = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  if (fire && !fire[s / n_kv_heads]) {
+    if (tid == 0) {
+      n_fetch[s] = 0;
+      if (n_fetch_out) n_fetch_out[s] = 0;
+    }
+    return;
+  }
+  const int n = min(max(n_sel[s], 0), budget);
+  const int words = (int)((pool_rows + 31) / 32);
+  const int32_t* rows = row_ws + (size_t)s * budget;
+  int32_t* brow = buf_row + (size_t)s * cache_rows;
+  int32_t* bstep = slot_step + (size_t)s * cache_rows;
+  for (int i = tid; i < words; i += kPlanThreads) s_bits[i] = 0u;
+  if (tid == 0) s_k = 0;
+  __syncthreads();
+  for (int p = tid; p < n; p += kPlanThreads) {
+    const int r = rows[p];
+    if (r >= 0 && r < pool_rows) atomicOr(&s_bits[r >> 5], 1u << (r & 31));
+  }
+  __syncthreads();
+  // hits: slots whose row is selected again (test and clear its bit)
+  for (int i = tid; i < cache_rows; i += kPlanThreads) {
+    const int r = brow[i];
+    if (r >= 0 && r < pool_rows) {
+      const uint32_t bit = 1u << (r & 31);
+      if (atomicAnd(&s_bits[r >> 5], ~bit) & bit) bstep[i] = step;
+    }
+  }
+  __syncthreads();
+  // the new rows: still marked
+  int kk = 0;
+  for (int p = tid; p < n; p += kPlanThreads) {
+    const int r = rows[p];
+    kk += (r >= 0 && r < pool_rows && (s_bits[r >> 5] >> (r & 31) & 1u)) ? 1 : 0;
+  }
+  kk = wave_sum_int(kk);
+  if (lane == 0) atomicAdd(&s_k, kk);
+  __syncthreads();
+  const int k = s_k;
+  // the k-th smallest key v = slot_step + 1 (0 = empty) among the slots not
+  // selected now (v <= step), by 8-bit digits from bit 23
+  int below = 0;   // candidates with a key below the prefix's range, taken whole
+  int prefix = 0;
+  for (int shift = 16; shift >= 0 && k > 0; shift -= 8) {
+    for (int i = tid; i < kPlanWaves * 256; i += kPlanThreads) (&s_hist[0][0])[i] = 0;
+    __syncthreads();
+    for (int i = tid; i < cache_rows; i += kPlanThreads) {
+      const int v = bstep[i] + 1;
+      if (v <= step && (shift == 16 || (v >> (shift + 8)) == prefix)) atomicAdd(&s_hist[wv][(v >> shift) & 255], 1);
+    }
+    __syncthreads();
+    if (wv == 0) {
+      // lane l holds digits 4l .. 4l + 3, lowest first
+      int c[4], tot = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        int h = 0;
+        for (int q2 = 0; q2 < kPlanWaves; ++q2) h += s_hist[q2][4 * lane + i];
+        c[i] = h;
+        tot += h;
+      }
+      int incl = tot;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o, kWave);
+        if (lane >= o) incl += y;
+      }
+      int cum = below + incl - tot;
+      int hit = -1, before = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (hit < 0 && cum + c[i] >= k) {
+          hit = 4 * lane + i;
+          before = cum;
+        }
+        cum += c[i];
+      }
+      const uint64_t found = __builtin_amdgcn_ballot_w64(hit >= 0);
+      const int all = __shfl(incl, 63, kWave);
+      if (found && lane == (int)__builtin_ctzll(found)) {
+        s_below = before;
+        s_thr = (prefix << 8) | hit;
+      } else if (!found && lane == 0) {
+        // fewer than k candidates (only a stale slot_step leaves that): every
+        // candidate is a victim, the threshold above them all
+        s_below = below + all;
+        s_thr = (prefix << 8) + 256;
+      }
+    }
+    __syncthreads();
+    below = s_below;
+    prefix = s_thr;
+  }
+  // victims: keys below the threshold, then the first (k - below) slots with
+  // the threshold key, in slot order; the k-th new row goes to the k-th victim
+  if (tid == 0) {
+    s_base[0] = 0;
+    s_base[1] = 0;
+    s_take_eq = k - below;
+  }
+  __syncthreads();
+  const int thr = prefix;
+  const int rounds = (cache_rows + kPlanThreads - 1) / kPlanThreads;
+  for (int rd = 0; rd < rounds && k > 0; ++rd) {
+    const int i = rd * kPlanThreads + tid;
+    const int v = i < cache_rows ? bstep[i] + 1 : step + 1;
+    const bool eq = v <= step && v == thr;
+    int ex_eq;
+    const int tot_eq = block_scan_flag(eq, s_w, ex_eq);
+    const bool victim = v <= step && (v < thr || (eq && s_base[1] + ex_eq < s_take_eq));
+    int ex;
+    const int tot = block_scan_flag(victim, s_w, ex);
+    if (victim) fetch_slot[(size_t)s * budget + s_base[0] + ex] = i;
+    __syncthreads();
+    if (tid == 0) {
+      s_base[0] += tot;
+      s_base[1] += tot_eq;
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    s_victims = s_base[0];
+    s_base[0] = 0;
+  }
+  __syncthreads();
+  const int prounds = (n + kPlanThreads - 1) / kPlanThreads;
+  for (int rd = 0; rd < prounds; ++rd) {
+    const int p = rd * kPlanThreads + tid;
+    int r = -1;
+    bool nw = false;
+    if (p < n) {
+      r = rows[p];
+      nw = r >= 0 && r < pool_rows && (s_bits[r >> 5] >> (r & 31) & 1u);
+    }
+    int ex;
+    const int tot = block_scan_flag(nw, s_w, ex);
+    if (nw) {
+      // kq < k <= the victims found when slot_step was reset with buf_row; a
+      // stale state can leave fewer, and such rows then get no slot
+      const int kq = s_base[0] + ex;
+      const int slot = kq < s_victims ? fetch_slot[(size_t)s * budget + kq] : -1;
+      fetch_row[(size_t)s * budget + kq] = slot >= 0 ? r : -1;
+      if (slot >= 0 && slot < cache_rows) {
+        brow[slot] = r;
+        bstep[slot] = step;
+      }
+    }
+    __syncthreads();
+    if (tid == 0) s_base[0] += tot;
+    __syncthreads();
+  }
+  if (tid == 0) {
+    n_fetch[s] = k;
+    if (n_fetch_out) n_fetch_out[s] = k;
+    s_base[2] = 0;
+  }
+  __syncthreads();
+  // the slots that hold the selection, in slot order
+  for (int rd = 0; rd < rounds; ++rd) {
+    const int i = rd * kPlanThreads + tid;
+    const bool v = i < cache_rows && bstep[i] == step;
+    int ex;
+    const int tot = block_scan_flag(v, s_w, ex);
+    if (v && s_base[2] + ex < budget) slot_list[(size_t)s * budget + s_base[2] + ex] = i;
     __syncthreads();
     if (tid == 0) s_base[2] += tot;
     __syncthreads();
@@ -1254,7 +1452,7 @@ __global__ __launch_bounds__(256)
 void delta_fetch_kernel(const T* __restrict__ k_pool, const T* __restrict__ v_pool, int64_t pool_rows,
                         const int32_t* __restrict__ fetch_slot, const int32_t* __restrict__ fetch_row,
                         const int32_t* __restrict__ n_fetch, int budget, int blocks_per_slice, int rows_per_block,
-                        T* __restrict__ k_buf, T* __restrict__ v_buf) {
+                        T* __restrict__ k_buf, T* __restrict__ v_buf, int buf_rows) {
   const int64_t s = blockIdx.x / blocks_per_slice;
   const int b = (int)(blockIdx.x - s * blocks_per_slice);
   const int n = n_fetch[s];
@@ -1266,11 +1464,11 @@ void delta_fetch_kernel(const T* __restrict__ k_pool, const T* __restrict__ v_po
   for (int k = r0 + (threadIdx.x >> 4); k < r1; k += 16) {
     const int64_t pr = fetch_row[(size_t)s * budget + k];
     const int slot = fetch_slot[(size_t)s * budget + k];
-    if (pr < 0 || pr >= pool_rows || slot < 0 || slot >= budget) continue;
+    if (pr < 0 || pr >= pool_rows || slot < 0 || slot >= buf_rows) continue;
     const uint4* ks = reinterpret_cast<const uint4*>(k_pool + ((size_t)s * pool_rows + pr) * kHeadDim);
     const uint4* vs = reinterpret_cast<const uint4*>(v_pool + ((size_t)s * pool_rows + pr) * kHeadDim);
-    uint4* kd = reinterpret_cast<uint4*>(k_buf + ((size_t)s * budget + slot) * kHeadDim);
-    uint4* vd = reinterpret_cast<uint4*>(v_buf + ((size_t)s * budget + slot) * kHeadDim);
+    uint4* kd = reinterpret_cast<uint4*>(k_buf + ((size_t)s * buf_rows + slot) * kHeadDim);
+    uint4* vd = reinterpret_cast<uint4*>(v_buf + ((size_t)s * buf_rows + slot) * kHeadDim);
 #pragma unroll
     for (int q = sub; q < kU4; q += 16) {
       const uint4 a = ks[q], c = vs[q];
@@ -2827,21 +3025,28 @@ extern "C" size_t louiskv_retrieve_delta_workspace_size(int64_t n_slices, int32_
   return align_up(cv.used, 256);
 }
 
-extern "C" int louiskv_retrieve_delta(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads,
-                                      int32_t group_size, int32_t d, double scale, const float* reps,
-                                      const int32_t* unit_start, const int32_t* unit_size, int32_t units_cap,
-                                      int32_t n_units, const int32_t* seg_state, int32_t window,
-                                      const void* k_pool, const void* v_pool, int64_t pool_rows,
-                                      int32_t pool_on_host, int32_t budget, const uint8_t* fire,
-                                      int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel, void* k_buf,
-                                      void* v_buf, int32_t* buf_row, int32_t* slot_list, int32_t* n_fetched,
-                                      double* scores_out, void* workspace, size_t workspace_bytes, void* stream) {
+namespace louiskv {
+namespace {
+// Scores and selection, then the transfer plan (delta: the buffer holds the
+// last selection only; cached: an LRU cache of cache_rows pool rows) and the
+// fetch of the planned rows.
+int retrieve_into_buffer(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads, int32_t group_size,
+                         int32_t d, double scale, const float* reps, const int32_t* unit_start,
+                         const int32_t* unit_size, int32_t units_cap, int32_t n_units, const int32_t* seg_state,
+                         int32_t window, const void* k_pool, const void* v_pool, int64_t pool_rows,
+                         int32_t pool_on_host, int32_t budget, int32_t cache_rows, int32_t step,
+                         const uint8_t* fire, int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel, void* k_buf,
+                         void* v_buf, int32_t* buf_row, int32_t* slot_step, int32_t* slot_list, int32_t* n_fetched,
+                         double* scores_out, void* workspace, size_t workspace_bytes, void* stream) {
   int st = check_retrieve_common(q, dtype, n_slices, n_kv_heads, group_size, d, reps, unit_start, unit_size, units_cap,
                                  n_units, budget, sel_units, n_sel_units, n_sel);
   if (st) return st;
   if (!k_pool || !v_pool || !k_buf || !v_buf || !buf_row || !slot_list)
     return fail(LOUISKV_ERR_NULL, "k_pool, v_pool, k_buf, v_buf, buf_row and slot_list are required");
   if (budget < 1) return fail(LOUISKV_ERR_SHAPE, "budget=%d must be >= 1", budget);
+  if (cache_rows < budget) return fail(LOUISKV_ERR_SHAPE, "cache_rows=%d < budget=%d", cache_rows, budget);
+  if (slot_step && (step < 0 || step > kCacheMaxStep))
+    return fail(LOUISKV_ERR_SHAPE, "step=%d must be in [0, %d]", step, kCacheMaxStep);
   if (pool_rows < 1 || pool_rows > kDeltaMaxPoolRows)
     return fail(LOUISKV_ERR_UNSUPPORTED, "pool_rows=%lld must be in [1, %lld]", (long long)pool_rows,
                 (long long)kDeltaMaxPoolRows);
@@ -2865,9 +3070,17 @@ extern "C" int louiskv_retrieve_delta(const void* q, int32_t dtype, int64_t n_sl
                              logit_ws, seg_state, seg_state ? kSegRing + window : 0, s)))
     return st;
   const size_t lds = (size_t)((pool_rows + 31) / 32) * sizeof(uint32_t);
-  if ((st = check_lds(reinterpret_cast<const void*>(&delta_plan_kernel), lds))) return st;
-  delta_plan_kernel<<<(unsigned)n_slices, kPlanThreads, lds, s>>>(row_ws, n_sel, fire, n_kv_heads, budget, pool_rows,
-                                                                  buf_row, slot_list, fslot, frow, nfetch, n_fetched);
+  if (slot_step) {
+    if ((st = check_lds(reinterpret_cast<const void*>(&cache_plan_kernel), lds))) return st;
+    cache_plan_kernel<<<(unsigned)n_slices, kPlanThreads, lds, s>>>(row_ws, n_sel, fire, n_kv_heads, budget,
+                                                                    cache_rows, pool_rows, step, buf_row, slot_step,
+                                                                    slot_list, fslot, frow, nfetch, n_fetched);
+  } else {
+    if ((st = check_lds(reinterpret_cast<const void*>(&delta_plan_kernel), lds))) return st;
+    delta_plan_kernel<<<(unsigned)n_slices, kPlanThreads, lds, s>>>(row_ws, n_sel, fire, n_kv_heads, budget,
+                                                                    pool_rows, buf_row, slot_list, fslot, frow, nfetch,
+                                                                    n_fetched);
+  }
   LKV_CHECK_LAUNCH();
   const int rpb = 128;
   const int bps = (budget + rpb - 1) / rpb;
@@ -2876,11 +3089,45 @@ extern "C" int louiskv_retrieve_delta(const void* q, int32_t dtype, int64_t n_sl
     delta_fetch_kernel<uint16_t><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(kpd),
                                                       static_cast<const uint16_t*>(vpd), pool_rows, fslot, frow, nfetch,
                                                       budget, bps, rpb, static_cast<uint16_t*>(k_buf),
-                                                      static_cast<uint16_t*>(v_buf));
+                                                      static_cast<uint16_t*>(v_buf), cache_rows);
   else
     delta_fetch_kernel<float><<<grid, 256, 0, s>>>(static_cast<const float*>(kpd), static_cast<const float*>(vpd),
                                                    pool_rows, fslot, frow, nfetch, budget, bps, rpb,
-                                                   static_cast<float*>(k_buf), static_cast<float*>(v_buf));
+                                                   static_cast<float*>(k_buf), static_cast<float*>(v_buf), cache_rows);
   LKV_CHECK_LAUNCH();
   return LOUISKV_OK;
+}
+}  // namespace
+}  // namespace louiskv
+
+extern "C" int louiskv_retrieve_delta(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads,
+                                      int32_t group_size, int32_t d, double scale, const float* reps,
+                                      const int32_t* unit_start, const int32_t* unit_size, int32_t units_cap,
+                                      int32_t n_units, const int32_t* seg_state, int32_t window,
+                                      const void* k_pool, const void* v_pool, int64_t pool_rows,
+                                      int32_t pool_on_host, int32_t budget, const uint8_t* fire,
+                                      int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel, void* k_buf,
+                                      void* v_buf, int32_t* buf_row, int32_t* slot_list, int32_t* n_fetched,
+                                      double* scores_out, void* workspace, size_t workspace_bytes, void* stream) {
+  return retrieve_into_buffer(q, dtype, n_slices, n_kv_heads, group_size, d, scale, reps, unit_start, unit_size,
+                              units_cap, n_units, seg_state, window, k_pool, v_pool, pool_rows, pool_on_host, budget,
+                              budget, 0, fire, sel_units, n_sel_units, n_sel, k_buf, v_buf, buf_row, nullptr,
+                              slot_list, n_fetched, scores_out, workspace, workspace_bytes, stream);
+}
+
+extern "C" int louiskv_retrieve_cached(const void* q, int32_t dtype, int64_t n_slices, int32_t n_kv_heads,
+                                       int32_t group_size, int32_t d, double scale, const float* reps,
+                                       const int32_t* unit_start, const int32_t* unit_size, int32_t units_cap,
+                                       int32_t n_units, const int32_t* seg_state, int32_t window,
+                                       const void* k_pool, const void* v_pool, int64_t pool_rows,
+                                       int32_t pool_on_host, int32_t budget, int32_t cache_rows, int32_t step,
+                                       const uint8_t* fire, int32_t* sel_units, int32_t* n_sel_units,
+                                       int32_t* n_sel, void* k_buf, void* v_buf, int32_t* buf_row,
+                                       int32_t* slot_step, int32_t* slot_list, int32_t* n_fetched,
+                                       double* scores_out, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!slot_step) return fail(LOUISKV_ERR_NULL, "slot_step is required");
+  return retrieve_into_buffer(q, dtype, n_slices, n_kv_heads, group_size, d, scale, reps, unit_start, unit_size,
+                              units_cap, n_units, seg_state, window, k_pool, v_pool, pool_rows, pool_on_host, budget,
+                              cache_rows, step, fire, sel_units, n_sel_units, n_sel, k_buf, v_buf, buf_row, slot_step,
+                              slot_list, n_fetched, scores_out, workspace, workspace_bytes, stream);
 }

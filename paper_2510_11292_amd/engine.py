@@ -57,6 +57,9 @@ MAX_UNITS = 8192   # units one slice's retrieval scores (the library's limit)
 # (two launches, each slice spread over many blocks); larger ones use the
 # per-stage calls, whose kernels fill the chip with one block per slice
 FUSED_STEP_MAX_SLICES = 64
+# KV_critical over a host-resident pool: an LRU cache of this many budgets of
+# pool rows per slice in HBM (the default; cache_rows overrides it)
+HOST_CACHE_BUDGETS = 8
 
 
 @dataclass(frozen=True)
@@ -129,7 +132,7 @@ class LouisKVEngine:
                  keep_scores: bool = False, out_dtype: Optional[torch.dtype] = None,
                  zero_copy: Optional[bool] = None, delta: Optional[bool] = None,
                  prefill_chunk: Optional[int] = None, copy_engine: bool = True, fuse_prologue: bool = True,
-                 fused_step: Optional[bool] = None):
+                 fused_step: Optional[bool] = None, cache_rows: Optional[int] = None):
         self.cfg = cfg
         self.dtype = dtype
         self.device = torch.device(device)
@@ -142,6 +145,15 @@ class LouisKVEngine:
         # KV_critical as a cache of pool rows: the default for a host-resident pool
         self.delta = (not self.zero_copy and pool_on_host) if delta is None else bool(delta)
         self.delta = self.delta and cfg.budget >= 1
+        # cache_rows > budget keeps KV_critical as an LRU cache of that many
+        # pool rows per slice (louiskv_retrieve_cached): rows selected again
+        # after a few steps away are still resident and need no transfer
+        if cache_rows is None and self.delta and pool_on_host:
+            cache_rows = min(HOST_CACHE_BUDGETS * max(cfg.budget, 1), cfg.pool_rows)
+        self.cached = cache_rows is not None and int(cache_rows) > max(cfg.budget, 1)
+        if self.cached and not self.delta:
+            raise ValueError("an LRU cache of pool rows needs delta transfers (zero_copy=False)")
+        self.cache_rows = int(cache_rows) if self.cached else max(cfg.budget, 1)
         if cfg.trigger not in ("boundary", "stride") or cfg.stride < 1:
             raise ValueError((cfg.trigger, cfg.stride))
         if cfg.index not in ("clusters", "pages") or cfg.page_len < 1:
@@ -177,10 +189,11 @@ class LouisKVEngine:
             self.k_buf = self.v_buf = None
         else:
             self.sel_rows = None
-            self.k_buf = torch.zeros(S, max(cfg.budget, 1), d, dtype=dtype, device=dev)
-            self.v_buf = torch.zeros(S, max(cfg.budget, 1), d, dtype=dtype, device=dev)
+            self.k_buf = torch.zeros(S, self.cache_rows, d, dtype=dtype, device=dev)
+            self.v_buf = torch.zeros(S, self.cache_rows, d, dtype=dtype, device=dev)
+        self.slot_step = torch.full((S, self.cache_rows), -1, **i32) if self.cached else None
         if self.delta:
-            self.buf_row = torch.full((S, max(cfg.budget, 1)), -1, **i32)
+            self.buf_row = torch.full((S, self.cache_rows), -1, **i32)
             self.slot_list = torch.zeros(S, max(cfg.budget, 1), **i32)
             self.n_fetched = torch.zeros(S, **i32)
         self.sel_units = torch.zeros(nl, cap, **i32)
@@ -297,12 +310,14 @@ class LouisKVEngine:
             L.segment_state_init(self.seg_state, c.window, c.n_clusters)
         if self.delta:
             self.buf_row.fill_(-1)
+        if self.cached:
+            self.slot_step.fill_(-1)
         self.t = 0
 
     # ------------------------------------------------------- layer by layer
     _PER_SLICE = ("reps", "unit_start", "unit_size", "assign", "perm", "k_pool", "v_pool", "k_local", "v_local",
-                  "sel_rows", "k_buf", "v_buf", "buf_row", "slot_list", "n_fetched", "sel_units", "n_sel_units",
-                  "n_sel", "scores", "seg_state")
+                  "sel_rows", "k_buf", "v_buf", "buf_row", "slot_step", "slot_list", "n_fetched", "sel_units",
+                  "n_sel_units", "n_sel", "scores", "seg_state")
     _PER_GROUP = ("q_ref", "fire", "r", "out", "lse")
 
     def group_view(self, g: int, n: int = 1) -> "LouisKVEngine":
@@ -468,9 +483,17 @@ class LouisKVEngine:
         self.t += 1
 
     def _retrieve_delta(self, q_t, n_units: int, seg_state) -> None:
-        """Retrieval into KV_critical kept as a cache of pool rows (only the
-        rows the slice's previous selection lacks are copied)."""
+        """Retrieval into KV_critical kept as a cache of pool rows: only the
+        selected rows the buffer lacks are copied (the buffer holds the last
+        selection, or with cache_rows an LRU set of recently selected rows)."""
         c = self.cfg
+        if self.cached:
+            L.retrieve_cached(q_t, c.n_kv_heads, self.reps, self.unit_start, self.unit_size, n_units, self.k_pool,
+                              self.v_pool, max(c.budget, 1), self.t, self.sel_units, self.n_sel_units, self.n_sel,
+                              self.k_buf, self.v_buf, self.buf_row, self.slot_step, self.slot_list, fire=self.fire,
+                              seg_state=seg_state, window=c.window, n_fetched=self.n_fetched,
+                              pool_on_host=self.pool_on_host, scores_out=self.scores, workspace=self.ws_retrieve)
+            return
         L.retrieve_delta(q_t, c.n_kv_heads, self.reps, self.unit_start, self.unit_size, n_units, self.k_pool,
                          self.v_pool, max(c.budget, 1), self.sel_units, self.n_sel_units, self.n_sel, self.k_buf,
                          self.v_buf, self.buf_row, self.slot_list, fire=self.fire, seg_state=seg_state,

@@ -120,6 +120,11 @@ _SIGS = {
         _P, _P, _P, _I32, _I32, _P, _I32,
         _P, _P, _I64, _I32, _I32, _P,
         _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "louiskv_retrieve_cached": (ctypes.c_int, [
+        _P, _I32, _I64, _I32, _I32, _I32, _D,
+        _P, _P, _P, _I32, _I32, _P, _I32,
+        _P, _P, _I64, _I32, _I32, _I32, _I32, _P,
+        _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
 }
 
 EXPORTED = sorted(_SIGS)
@@ -582,6 +587,24 @@ def retrieve_delta(q, n_kv_heads: int, reps, unit_start, unit_size, n_units: int
         _ptr(reps), _ptr(unit_start), _ptr(unit_size), cap, n_units, _ptr(seg_state), window,
         _ptr(k_pool), _ptr(v_pool), k_pool.shape[1], int(pool_on_host), budget, _ptr(fire),
         _ptr(sel_units), _ptr(n_sel_units), _ptr(n_sel), _ptr(k_buf), _ptr(v_buf), _ptr(buf_row),
+        _ptr(slot_list), _ptr(n_fetched), _ptr(scores_out), _ptr(ws), wsb, _stream(stream)))
+
+
+def retrieve_cached(q, n_kv_heads: int, reps, unit_start, unit_size, n_units: int, k_pool, v_pool, budget: int,
+                    step: int, sel_units, n_sel_units, n_sel, k_buf, v_buf, buf_row, slot_step, slot_list, fire=None,
+                    seg_state=None, window: int = 0, n_fetched=None, scale: Optional[float] = None,
+                    pool_on_host: bool = False, scores_out=None, workspace=None, stream=None):
+    """Retrieval into KV_critical kept as an LRU cache of k_buf.shape[1] pool rows."""
+    g, hq, d = q.shape
+    s = reps.shape[0]
+    cap = reps.shape[1]
+    ws, wsb = _ws(retrieve_delta_workspace_size(s, cap, budget), q.device, workspace)
+    sc = (1.0 / d ** 0.5) if scale is None else scale
+    _check(load_library().louiskv_retrieve_cached(
+        _ptr(q), _dtype_code(q), s, n_kv_heads, hq // n_kv_heads, d, float(sc),
+        _ptr(reps), _ptr(unit_start), _ptr(unit_size), cap, n_units, _ptr(seg_state), window,
+        _ptr(k_pool), _ptr(v_pool), k_pool.shape[1], int(pool_on_host), budget, k_buf.shape[1], step, _ptr(fire),
+        _ptr(sel_units), _ptr(n_sel_units), _ptr(n_sel), _ptr(k_buf), _ptr(v_buf), _ptr(buf_row), _ptr(slot_step),
         _ptr(slot_list), _ptr(n_fetched), _ptr(scores_out), _ptr(ws), wsb, _stream(stream)))
 
 

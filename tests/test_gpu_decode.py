@@ -400,9 +400,29 @@ def test_sparse_decode_attn_rows_clamps_list_entries():
 
 # ------------------------------------------------------------------ whole decode loop
 
-def _check_delta_buffers(eng, gi, H):
+def _lru_model(buf_row, slot_step, rows, step):
+    """The LRU policy of the cached KV_critical, written out: slots whose row
+    is selected again keep it; the new rows, in selection order, go to the
+    other slots with the smallest (last step, slot), taken in slot order."""
+    buf_row, slot_step = buf_row.copy(), slot_step.copy()
+    pos = {int(r): i for i, r in enumerate(buf_row) if r >= 0}
+    new = []
+    for r in rows:
+        if r in pos:
+            slot_step[pos[r]] = step
+        else:
+            new.append(r)
+    cand = sorted((i for i in range(len(buf_row)) if slot_step[i] < step), key=lambda i: (slot_step[i], i))
+    for r, i in zip(new, sorted(cand[:len(new)])):
+        buf_row[i], slot_step[i] = r, step
+    return buf_row, slot_step, [i for i in range(len(buf_row)) if slot_step[i] == step], len(new)
+
+
+def _check_delta_buffers(eng, gi, H, before=None, t=None):
     """KV_critical kept as a cache of pool rows: the listed slots hold exactly
-    the selected rows (as copies of their pool rows), every slot at most once."""
+    the selected rows (as copies of their pool rows), every slot at most once;
+    with an LRU cache, slots, steps and the fetch count follow the policy
+    from the state before the step."""
     for h in range(H):
         s = gi * H + h
         n = int(eng.n_sel[s])
@@ -413,14 +433,22 @@ def _check_delta_buffers(eng, gi, H):
         want = sorted(r for u in units for r in range(int(eng.unit_start[s, u]),
                                                        int(eng.unit_start[s, u]) + int(eng.unit_size[s, u])))
         assert sorted(held.tolist()) == want
-        assert (to_np(eng.buf_row[s]) >= 0).sum() == n
+        if eng.cached:
+            rows = [r for u in units for r in range(int(eng.unit_start[s, u]),
+                                                    int(eng.unit_start[s, u]) + int(eng.unit_size[s, u]))]
+            b_row, b_step, lst, k = _lru_model(before[0][s], before[1][s], rows, t)
+            assert np.array_equal(to_np(eng.buf_row[s]), b_row), (t, s)
+            assert np.array_equal(to_np(eng.slot_step[s]), b_step), (t, s)
+            assert slots.tolist() == lst and int(eng.n_fetched[s]) == k, (t, s)
+        else:
+            assert (to_np(eng.buf_row[s]) >= 0).sum() == n
         idx = torch.as_tensor(held, dtype=torch.long)
         assert torch.equal(eng.k_buf[s, torch.as_tensor(slots)].cpu(), eng.k_pool[s].cpu()[idx])
         assert torch.equal(eng.v_buf[s, torch.as_tensor(slots)].cpu(), eng.v_pool[s].cpu()[idx])
 
 
 def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, segments="fixed", delta=None,
-              layer_by_layer=False, **ablation):
+              layer_by_layer=False, cache_rows=None, **ablation):
     """Prefill on the GPU, then `steps` decode steps on the GPU and in the
     oracle (started from the GPU's prefill state), step-locked.  With
     layer_by_layer each step runs group by group (one launch sequence per
@@ -430,7 +458,7 @@ def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, seg
     cfg = config_from_workload(wl, n_groups=n_groups, mode=mode, gen_len=steps, segments=segments, **ablation)
     odt = torch.float32
     eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, pool_on_host=pool_on_host, keep_scores=True,
-                        out_dtype=odt, zero_copy=zero_copy, delta=delta)
+                        out_dtype=odt, zero_copy=zero_copy, delta=delta, cache_rows=cache_rows)
     eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
     torch.cuda.synchronize()
     H, g = wl.n_kv_heads, wl.group_size
@@ -464,6 +492,7 @@ def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, seg
     if layer_by_layer and pool_on_host:
         _require_interior_host_mapping(eng.k_pool, wl.n_kv_heads)
     for t in range(steps):
+        before = (to_np(eng.buf_row), to_np(eng.slot_step)) if eng.cached else None
         if layer_by_layer:
             eng.step_layer_by_layer(data.queries[t], data.gen_keys[t], data.gen_values[t])
         else:
@@ -499,7 +528,7 @@ def _run_loop(wl, n_groups, steps, mode, pool_on_host=False, zero_copy=None, seg
                            select_override=override)
             assert to_np(eng.n_sel[gi * NL:(gi + 1) * NL]).tolist() == rec.n_sel
             if eng.delta and fire[gi]:
-                _check_delta_buffers(eng, gi, H)
+                _check_delta_buffers(eng, gi, H, before, t)
                 stats["fetched"] += int(eng.n_fetched[gi * H:(gi + 1) * H].sum())
                 stats["selected"] += int(eng.n_sel[gi * H:(gi + 1) * H].sum())
             got = to64(eng.out[gi])
@@ -558,10 +587,25 @@ def test_decode_loop_host_pool(delta):
     host link, either every selected row (gather) or only the rows the
     previous selection did not hold (delta, the engine's default there)."""
     wl = synth.get_workload("host-131k").replace(prompt_len=2048, n_clusters=64, budget=512, name="host-131k")
-    st = _run_loop(wl, 1, 200, mode=1, pool_on_host=True, delta=delta)
+    st = _run_loop(wl, 1, 200, mode=1, pool_on_host=True, delta=delta, cache_rows=wl.budget if delta else None)
     assert st["fires"] > 20
     if delta:
         assert 0 < st["fetched"] < st["selected"]
+
+
+@pytest.mark.parametrize("segments", ["fixed", "boundary"])
+def test_decode_loop_host_pool_lru_cache(segments):
+    """KV_critical as an LRU cache of four budgets of pool rows over a pinned
+    host pool: oracle parity of every step, and slots, steps and fetch counts
+    equal to the LRU policy written out in Python; the cache fetches fewer
+    rows than the one-budget buffer on the same inputs."""
+    wl = synth.get_workload("host-131k").replace(prompt_len=2048, n_clusters=64, budget=512, window=64, seg_len=16,
+                                                 name="host-131k")
+    st = _run_loop(wl, 1, 200, mode=1, pool_on_host=True, segments=segments, cache_rows=4 * 512)
+    assert st["fires"] > 20 and 0 < st["fetched"] < st["selected"]
+    base = _run_loop(wl, 1, 200, mode=1, pool_on_host=True, segments=segments, cache_rows=wl.budget)
+    print(f"fetched rows: LRU cache {st['fetched']}, one budget {base['fetched']}", flush=True)
+    assert st["fetched"] < base["fetched"]
 
 
 def test_decode_loop_delta_device_pool():
@@ -808,14 +852,14 @@ def test_fused_prologue_equals_separate_calls(case):
     assert fires > 10
 
 
-@pytest.mark.parametrize("case", ["zero-copy", "boundary-segments", "host-delta"])
+@pytest.mark.parametrize("case", ["zero-copy", "boundary-segments", "host-delta", "host-lru-cache"])
 def test_decode_graph_replays_match_eager(case):
     """The decode loop captured once as a HIP graph (as the benchmark runs it)
     and replayed three times, each after a fresh eager prefill and with eager
     work and synchronisations between the replays, gives at every step the
     outputs and selection sizes of the eager loop."""
     from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
-    host = case == "host-delta"
+    host = case.startswith("host")
     if host:
         wl = synth.get_workload("host-131k").replace(prompt_len=2048, n_clusters=64, budget=512, name="host-131k")
     else:
@@ -824,7 +868,8 @@ def test_decode_graph_replays_match_eager(case):
     steps, G = 160, 2
     data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(G)], gen_len=steps)
     cfg = config_from_workload(wl, n_groups=G, gen_len=steps, **seg)
-    eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, pool_on_host=host, out_dtype=torch.float32)
+    eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, pool_on_host=host, out_dtype=torch.float32,
+                        cache_rows=3 * wl.budget if case == "host-lru-cache" else wl.budget)
     hist = torch.zeros(steps, *eng.out.shape, device=DEV)
     hist_n = torch.zeros(steps, *eng.n_sel.shape, dtype=torch.int32, device=DEV)
 
@@ -938,12 +983,13 @@ def test_decode_step_equals_stage_calls(case):
 def test_layer_by_layer_step_graphs_match_eager(case):
     """The group-by-group decode captured as one HIP graph per step (as the
     benchmark times it) and replayed twice after fresh prefills equals the
-    eager group-by-group loop: over a pinned host pool with delta transfers
-    (interior pointers of the pool resolved per group view at capture time),
+    eager group-by-group loop: over a pinned host pool with the default LRU
+    cache of pool rows (interior pointers of the pool resolved per group view
+    at capture time, the decode step baked into each graph),
     and over a device pool, where each view runs the two-launch decode step
     whose workspace counters must return to zero on every replay."""
     from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
-    host = case == "host-delta"
+    host = case.startswith("host")
     if host:
         wl = synth.get_workload("host-131k").replace(prompt_len=2048, n_clusters=64, budget=512, name="host-131k")
     else:
