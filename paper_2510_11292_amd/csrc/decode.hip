@@ -1154,6 +1154,28 @@ __device__ __forceinline__ int block_scan_flag(int flag, int* s_w, int& excl) {
   return total;
 }
 
+// Exclusive block-wide prefix sum of one count per thread; returns the total.
+__device__ __forceinline__ int block_scan_count(int c, int* s_w, int& excl) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  int incl = c;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += y;
+  }
+  if (lane == 63) s_w[w] = incl;
+  __syncthreads();
+  int before = 0, total = 0;
+  for (int q = 0; q < kPlanWaves; ++q) {
+    const int x = s_w[q];
+    before += q < w ? x : 0;
+    total += x;
+  }
+  __syncthreads();
+  excl = before + incl - c;
+  return total;
+}
+
 __global__ __launch_bounds__(kPlanThreads)
 void delta_plan_kernel(const int32_t* __restrict__ row_ws, const int32_t* __restrict__ n_sel,
                        const uint8_t* __restrict__ fire, int n_kv_heads, int budget, int64_t pool_rows,
@@ -1257,11 +1279,36 @@ void delta_plan_kernel(const int32_t* __restrict__ row_ws, const int32_t* __rest
 //    the smallest (slot_step, slot), paired in slot order: empty slots first,
 //    then the rows selected longest ago;
 //  - slot_list lists the n_sel slots holding the selection, in slot order.
-// The k-th smallest slot_step + 1 among the candidates comes from a radix
-// select over 24 bits (8 per pass, per-wave histograms), the ties at the
-// threshold in slot order from a block scan.
+// Thread t holds slots [R t, R t + R) in registers for the whole plan.  The
+// k-th smallest key slot_step + 1 among the candidates (slots not selected
+// now) comes from a radix select by 8-bit digits (per-wave histograms), the
+// ties at the threshold in slot order from block scans.
 constexpr int kCacheMaxStep = (1 << 24) - 2;
+constexpr int kCacheMaxSlotsPerThread = 32;   // (64 would spill registers)
+constexpr int kCacheMaxRows = kPlanThreads * kCacheMaxSlotsPerThread;
 
+// x[j] = a[i0 + j] for j < R (fill past n), in 16-byte loads where the run
+// is aligned and whole (a thread's run is consecutive, so a wave's plain
+// loads would each touch 64 lines)
+template <int R>
+__device__ __forceinline__ void load_run(const int32_t* a, int i0, int n, int fill, int (&x)[R]) {
+  const bool vec = ((reinterpret_cast<uintptr_t>(a + i0) & 15u) == 0) && i0 + R <= n;
+  if (vec) {
+#pragma unroll
+    for (int j = 0; j < R; j += 4) {
+      const int4 v = *reinterpret_cast<const int4*>(a + i0 + j);
+      x[j] = v.x;
+      x[j + 1] = v.y;
+      x[j + 2] = v.z;
+      x[j + 3] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < R; ++j) x[j] = i0 + j < n ? a[i0 + j] : fill;
+  }
+}
+
+template <int R>
 __global__ __launch_bounds__(kPlanThreads)
 void cache_plan_kernel(const int32_t* __restrict__ row_ws, const int32_t* __restrict__ n_sel,
                        const uint8_t* __restrict__ fire, int n_kv_heads, int budget, int cache_rows,
@@ -1272,8 +1319,7 @@ void cache_plan_kernel(const int32_t* __restrict__ row_ws, const int32_t* __rest
   extern __shared__ uint32_t s_bits[];   // one bit per pool row
   __shared__ int s_w[kPlanWaves];
   __shared__ int s_hist[kPlanWaves][256];
-  __shared__ int s_base[3];
-  __shared__ int s_k, s_below, s_thr, s_take_eq, s_victims;
+  __shared__ int s_k, s_below, s_thr;
   const int64_t s = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   if (fire && !fire[s / n_kv_heads]) {
@@ -1288,6 +1334,13 @@ void cache_plan_kernel(const int32_t* __restrict__ row_ws, const int32_t* __rest
   const int32_t* rows = row_ws + (size_t)s * budget;
   int32_t* brow = buf_row + (size_t)s * cache_rows;
   int32_t* bstep = slot_step + (size_t)s * cache_rows;
+  const int i0 = tid * R;
+  // key[j] = slot_step + 1 of slot i0 + j (0: empty); slots past the end
+  // take step + 1, which is never a candidate
+  int key[R];
+  load_run<R>(bstep, i0, cache_rows, step, key);
+#pragma unroll
+  for (int j = 0; j < R; ++j) key[j] += 1;
   for (int i = tid; i < words; i += kPlanThreads) s_bits[i] = 0u;
   if (tid == 0) s_k = 0;
   __syncthreads();
@@ -1297,13 +1350,23 @@ void cache_plan_kernel(const int32_t* __restrict__ row_ws, const int32_t* __rest
   }
   __syncthreads();
   // hits: slots whose row is selected again (test and clear its bit)
-  for (int i = tid; i < cache_rows; i += kPlanThreads) {
-    const int r = brow[i];
+  uint64_t hit = 0;
+  int row[R];
+  load_run<R>(brow, i0, cache_rows, -1, row);
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    const int r = row[j];
     if (r >= 0 && r < pool_rows) {
       const uint32_t bit = 1u << (r & 31);
-      if (atomicAnd(&s_bits[r >> 5], ~bit) & bit) bstep[i] = step;
+      if (atomicAnd(&s_bits[r >> 5], ~bit) & bit) hit |= 1ull << j;
     }
   }
+#pragma unroll
+  for (int j = 0; j < R; ++j)
+    if (hit >> j & 1ull) {
+      key[j] = step + 1;
+      bstep[i0 + j] = step;
+    }
   __syncthreads();
   // the new rows: still marked
   int kk = 0;
@@ -1315,16 +1378,40 @@ void cache_plan_kernel(const int32_t* __restrict__ row_ws, const int32_t* __rest
   if (lane == 0) atomicAdd(&s_k, kk);
   __syncthreads();
   const int k = s_k;
-  // the k-th smallest key v = slot_step + 1 (0 = empty) among the slots not
-  // selected now (v <= step), by 8-bit digits from bit 23
+  // radix select of the k-th smallest candidate key, from the highest digit
+  // that step + 1 uses
   int below = 0;   // candidates with a key below the prefix's range, taken whole
   int prefix = 0;
-  for (int shift = 16; shift >= 0 && k > 0; shift -= 8) {
+  const int top = step < 255 ? 0 : step < 65535 ? 8 : 16;
+  for (int shift = top; shift >= 0 && k > 0; shift -= 8) {
     for (int i = tid; i < kPlanWaves * 256; i += kPlanThreads) (&s_hist[0][0])[i] = 0;
     __syncthreads();
-    for (int i = tid; i < cache_rows; i += kPlanThreads) {
-      const int v = bstep[i] + 1;
-      if (v <= step && (shift == 16 || (v >> (shift + 8)) == prefix)) atomicAdd(&s_hist[wv][(v >> shift) & 255], 1);
+    // runs of one digit are counted in a register and added once; a thread's
+    // last run is added once per wave when the wave's agree
+    int cur = -1, cnt = 0;
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      const int x = key[j];
+      if (x <= step && (x >> (shift + 8)) == prefix) {
+        const int dg = (x >> shift) & 255;
+        if (dg != cur) {
+          if (cnt) atomicAdd(&s_hist[wv][cur], cnt);
+          cur = dg;
+          cnt = 0;
+        }
+        ++cnt;
+      }
+    }
+    const uint64_t m = __builtin_amdgcn_ballot_w64(cnt > 0);
+    if (m) {
+      const int lead = (int)__builtin_ctzll(m);
+      const int d0 = __shfl(cur, lead, kWave);
+      if (__builtin_amdgcn_ballot_w64(cnt > 0 && cur != d0) == 0) {
+        const int tot = wave_sum_int(cnt);
+        if (lane == lead) atomicAdd(&s_hist[wv][d0], tot);
+      } else if (cnt > 0) {
+        atomicAdd(&s_hist[wv][cur], cnt);
+      }
     }
     __syncthreads();
     if (wv == 0) {
@@ -1344,20 +1431,20 @@ void cache_plan_kernel(const int32_t* __restrict__ row_ws, const int32_t* __rest
         if (lane >= o) incl += y;
       }
       int cum = below + incl - tot;
-      int hit = -1, before = 0;
+      int hit_d = -1, before = 0;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        if (hit < 0 && cum + c[i] >= k) {
-          hit = 4 * lane + i;
+        if (hit_d < 0 && cum + c[i] >= k) {
+          hit_d = 4 * lane + i;
           before = cum;
         }
         cum += c[i];
       }
-      const uint64_t found = __builtin_amdgcn_ballot_w64(hit >= 0);
+      const uint64_t found = __builtin_amdgcn_ballot_w64(hit_d >= 0);
       const int all = __shfl(incl, 63, kWave);
       if (found && lane == (int)__builtin_ctzll(found)) {
         s_below = before;
-        s_thr = (prefix << 8) | hit;
+        s_thr = (prefix << 8) | hit_d;
       } else if (!found && lane == 0) {
         // fewer than k candidates (only a stale slot_step leaves that): every
         // candidate is a victim, the threshold above them all
@@ -1370,37 +1457,42 @@ void cache_plan_kernel(const int32_t* __restrict__ row_ws, const int32_t* __rest
     prefix = s_thr;
   }
   // victims: keys below the threshold, then the first (k - below) slots with
-  // the threshold key, in slot order; the k-th new row goes to the k-th victim
-  if (tid == 0) {
-    s_base[0] = 0;
-    s_base[1] = 0;
-    s_take_eq = k - below;
-  }
-  __syncthreads();
+  // the threshold key, in slot order; the q-th new row (selection order) goes
+  // to the q-th victim (slot order)
   const int thr = prefix;
-  const int rounds = (cache_rows + kPlanThreads - 1) / kPlanThreads;
-  for (int rd = 0; rd < rounds && k > 0; ++rd) {
-    const int i = rd * kPlanThreads + tid;
-    const int v = i < cache_rows ? bstep[i] + 1 : step + 1;
-    const bool eq = v <= step && v == thr;
-    int ex_eq;
-    const int tot_eq = block_scan_flag(eq, s_w, ex_eq);
-    const bool victim = v <= step && (v < thr || (eq && s_base[1] + ex_eq < s_take_eq));
-    int ex;
-    const int tot = block_scan_flag(victim, s_w, ex);
-    if (victim) fetch_slot[(size_t)s * budget + s_base[0] + ex] = i;
-    __syncthreads();
-    if (tid == 0) {
-      s_base[0] += tot;
-      s_base[1] += tot_eq;
+  const int take_eq = k - below;
+  uint64_t victim = 0;
+  int n_victims = 0, v_first = 0;
+  if (k > 0) {
+    int n_lt = 0, n_eq = 0;
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      n_lt += key[j] <= step && key[j] < thr;
+      n_eq += key[j] <= step && key[j] == thr;
     }
-    __syncthreads();
+    int eq_before;
+    block_scan_count(n_eq, s_w, eq_before);
+    int e = eq_before;
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      const int x = key[j];
+      if (x > step) continue;
+      if (x < thr || (x == thr && e < take_eq)) victim |= 1ull << j;
+      e += x == thr;
+    }
+    n_victims = block_scan_count(__popcll(victim), s_w, v_first);
+#pragma unroll
+    for (int j = 0, o = v_first; j < R; ++j)
+      if (victim >> j & 1ull) {
+        if (o < budget) fetch_slot[(size_t)s * budget + o] = i0 + j;
+        ++o;
+      }
   }
-  if (tid == 0) {
-    s_victims = s_base[0];
-    s_base[0] = 0;
-  }
+  n_victims = min(n_victims, budget);
   __syncthreads();
+  // the new rows in selection order: the q-th takes victim q's slot (rows
+  // beyond the victims, only possible with a stale slot_step, get none)
+  int base = 0;
   const int prounds = (n + kPlanThreads - 1) / kPlanThreads;
   for (int rd = 0; rd < prounds; ++rd) {
     const int p = rd * kPlanThreads + tid;
@@ -1413,37 +1505,40 @@ void cache_plan_kernel(const int32_t* __restrict__ row_ws, const int32_t* __rest
     int ex;
     const int tot = block_scan_flag(nw, s_w, ex);
     if (nw) {
-      // kq < k <= the victims found when slot_step was reset with buf_row; a
-      // stale state can leave fewer, and such rows then get no slot
-      const int kq = s_base[0] + ex;
-      const int slot = kq < s_victims ? fetch_slot[(size_t)s * budget + kq] : -1;
-      fetch_row[(size_t)s * budget + kq] = slot >= 0 ? r : -1;
+      const int q = base + ex;
+      const int slot = q < n_victims ? fetch_slot[(size_t)s * budget + q] : -1;
+      fetch_row[(size_t)s * budget + q] = slot >= 0 ? r : -1;
       if (slot >= 0 && slot < cache_rows) {
         brow[slot] = r;
         bstep[slot] = step;
       }
     }
-    __syncthreads();
-    if (tid == 0) s_base[0] += tot;
-    __syncthreads();
+    base += tot;
   }
   if (tid == 0) {
     n_fetch[s] = k;
     if (n_fetch_out) n_fetch_out[s] = k;
-    s_base[2] = 0;
   }
-  __syncthreads();
-  // the slots that hold the selection, in slot order
-  for (int rd = 0; rd < rounds; ++rd) {
-    const int i = rd * kPlanThreads + tid;
-    const bool v = i < cache_rows && bstep[i] == step;
-    int ex;
-    const int tot = block_scan_flag(v, s_w, ex);
-    if (v && s_base[2] + ex < budget) slot_list[(size_t)s * budget + s_base[2] + ex] = i;
-    __syncthreads();
-    if (tid == 0) s_base[2] += tot;
-    __syncthreads();
+  // the slots that hold the selection, in slot order: hits and the victims
+  // that took a new row
+  uint64_t held = hit;
+  {
+    int o = v_first;
+#pragma unroll
+    for (int j = 0; j < R; ++j)
+      if (victim >> j & 1ull) {
+        if (o < min(k, n_victims)) held |= 1ull << j;
+        ++o;
+      }
   }
+  int before;
+  block_scan_count(__popcll(held), s_w, before);
+#pragma unroll
+  for (int j = 0, o = before; j < R; ++j)
+    if (held >> j & 1ull) {
+      if (o < budget) slot_list[(size_t)s * budget + o] = i0 + j;
+      ++o;
+    }
 }
 
 // Copy the planned rows pool -> buffer slot: 16 lanes per row, 16 rows per pass.
@@ -3045,6 +3140,8 @@ int retrieve_into_buffer(const void* q, int32_t dtype, int64_t n_slices, int32_t
     return fail(LOUISKV_ERR_NULL, "k_pool, v_pool, k_buf, v_buf, buf_row and slot_list are required");
   if (budget < 1) return fail(LOUISKV_ERR_SHAPE, "budget=%d must be >= 1", budget);
   if (cache_rows < budget) return fail(LOUISKV_ERR_SHAPE, "cache_rows=%d < budget=%d", cache_rows, budget);
+  if (slot_step && cache_rows > kCacheMaxRows)
+    return fail(LOUISKV_ERR_UNSUPPORTED, "cache_rows=%d exceeds %d", cache_rows, kCacheMaxRows);
   if (slot_step && (step < 0 || step > kCacheMaxStep))
     return fail(LOUISKV_ERR_SHAPE, "step=%d must be in [0, %d]", step, kCacheMaxStep);
   if (pool_rows < 1 || pool_rows > kDeltaMaxPoolRows)
@@ -3071,10 +3168,13 @@ int retrieve_into_buffer(const void* q, int32_t dtype, int64_t n_slices, int32_t
     return st;
   const size_t lds = (size_t)((pool_rows + 31) / 32) * sizeof(uint32_t);
   if (slot_step) {
-    if ((st = check_lds(reinterpret_cast<const void*>(&cache_plan_kernel), lds))) return st;
-    cache_plan_kernel<<<(unsigned)n_slices, kPlanThreads, lds, s>>>(row_ws, n_sel, fire, n_kv_heads, budget,
-                                                                    cache_rows, pool_rows, step, buf_row, slot_step,
-                                                                    slot_list, fslot, frow, nfetch, n_fetched);
+    // the smallest per-thread slot run that covers cache_rows
+    const int per = (cache_rows + kPlanThreads - 1) / kPlanThreads;
+    auto plan = per <= 8 ? &cache_plan_kernel<8> : per <= 16 ? &cache_plan_kernel<16> : &cache_plan_kernel<32>;
+    if ((st = check_lds(reinterpret_cast<const void*>(plan), lds))) return st;
+    plan<<<(unsigned)n_slices, kPlanThreads, lds, s>>>(row_ws, n_sel, fire, n_kv_heads, budget, cache_rows, pool_rows,
+                                                       step, buf_row, slot_step, slot_list, fslot, frow, nfetch,
+                                                       n_fetched);
   } else {
     if ((st = check_lds(reinterpret_cast<const void*>(&delta_plan_kernel), lds))) return st;
     delta_plan_kernel<<<(unsigned)n_slices, kPlanThreads, lds, s>>>(row_ws, n_sel, fire, n_kv_heads, budget,

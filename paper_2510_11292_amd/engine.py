@@ -149,7 +149,7 @@ class LouisKVEngine:
         # pool rows per slice (louiskv_retrieve_cached): rows selected again
         # after a few steps away are still resident and need no transfer
         if cache_rows is None and self.delta and pool_on_host:
-            cache_rows = min(HOST_CACHE_BUDGETS * max(cfg.budget, 1), cfg.pool_rows)
+            cache_rows = min(HOST_CACHE_BUDGETS * max(cfg.budget, 1), cfg.pool_rows, L.CACHE_MAX_ROWS)
         self.cached = cache_rows is not None and int(cache_rows) > max(cfg.budget, 1)
         if self.cached and not self.delta:
             raise ValueError("an LRU cache of pool rows needs delta transfers (zero_copy=False)")

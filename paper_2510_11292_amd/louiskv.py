@@ -590,6 +590,9 @@ def retrieve_delta(q, n_kv_heads: int, reps, unit_start, unit_size, n_units: int
         _ptr(slot_list), _ptr(n_fetched), _ptr(scores_out), _ptr(ws), wsb, _stream(stream)))
 
 
+CACHE_MAX_ROWS = 32768   # louiskv_retrieve_cached: slots per slice at most
+
+
 def retrieve_cached(q, n_kv_heads: int, reps, unit_start, unit_size, n_units: int, k_pool, v_pool, budget: int,
                     step: int, sel_units, n_sel_units, n_sel, k_buf, v_buf, buf_row, slot_step, slot_list, fire=None,
                     seg_state=None, window: int = 0, n_fetched=None, scale: Optional[float] = None,
