@@ -727,7 +727,8 @@ def main() -> int:
             "ref_mode": args.mode, "segments": args.segments,
             "decode_launch": "eager" if graph is None else "hip_graph",
             "kv_critical": ("pool row list (zero-copy)" if eng.zero_copy else
-                            "cache of pool rows (delta transfers)" if eng.delta else "gathered copy"),
+                            f"LRU cache of {eng.cache_rows} pool rows per slice" if eng.cached else
+                            "last selection's pool rows (delta transfers)" if eng.delta else "gathered copy"),
         },
         "decode_steps_per_s": wl.gen_len / t_dec,
         "decode_steps_per_s_gathered_kv_critical": (wl.gen_len / (dense_ms / 1e3)) if dense_ms else None,

@@ -713,7 +713,7 @@ int louiskv_retrieve_delta(const void* q, int32_t dtype, int64_t n_slices,
  *            2^24 - 1); a stale state (not reset) can leave rows without a
  *            slot, never write outside the buffers.
  * k_buf, v_buf  [n_slices][cache_rows][d] dtype.  slot_list [n_slices][budget].
- * budget <= cache_rows <= 32768 (LOUISKV_ERR_UNSUPPORTED above: the plan
+ * budget <= cache_rows <= 65536 (LOUISKV_ERR_UNSUPPORTED above: the plan
  * keeps every slot's step in registers).
  * Workspace louiskv_retrieve_delta_workspace_size().  Other arguments as
  * louiskv_retrieve_delta.

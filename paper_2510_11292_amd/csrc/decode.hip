@@ -1284,7 +1284,7 @@ void delta_plan_kernel(const int32_t* __restrict__ row_ws, const int32_t* __rest
 // now) comes from a radix select by 8-bit digits (per-wave histograms), the
 // ties at the threshold in slot order from block scans.
 constexpr int kCacheMaxStep = (1 << 24) - 2;
-constexpr int kCacheMaxSlotsPerThread = 32;   // (64 would spill registers)
+constexpr int kCacheMaxSlotsPerThread = 64;
 constexpr int kCacheMaxRows = kPlanThreads * kCacheMaxSlotsPerThread;
 
 // x[j] = a[i0 + j] for j < R (fill past n), in 16-byte loads where the run
@@ -1351,14 +1351,17 @@ void cache_plan_kernel(const int32_t* __restrict__ row_ws, const int32_t* __rest
   __syncthreads();
   // hits: slots whose row is selected again (test and clear its bit)
   uint64_t hit = 0;
-  int row[R];
-  load_run<R>(brow, i0, cache_rows, -1, row);
 #pragma unroll
-  for (int j = 0; j < R; ++j) {
-    const int r = row[j];
-    if (r >= 0 && r < pool_rows) {
-      const uint32_t bit = 1u << (r & 31);
-      if (atomicAnd(&s_bits[r >> 5], ~bit) & bit) hit |= 1ull << j;
+  for (int j0 = 0; j0 < R; j0 += 16) {
+    int row[16];
+    load_run<16>(brow, i0 + j0, cache_rows, -1, row);
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int r = row[j];
+      if (r >= 0 && r < pool_rows) {
+        const uint32_t bit = 1u << (r & 31);
+        if (atomicAnd(&s_bits[r >> 5], ~bit) & bit) hit |= 1ull << (j0 + j);
+      }
     }
   }
 #pragma unroll
@@ -3170,7 +3173,8 @@ int retrieve_into_buffer(const void* q, int32_t dtype, int64_t n_slices, int32_t
   if (slot_step) {
     // the smallest per-thread slot run that covers cache_rows
     const int per = (cache_rows + kPlanThreads - 1) / kPlanThreads;
-    auto plan = per <= 8 ? &cache_plan_kernel<8> : per <= 16 ? &cache_plan_kernel<16> : &cache_plan_kernel<32>;
+    auto plan = per <= 8 ? &cache_plan_kernel<8> : per <= 16 ? &cache_plan_kernel<16>
+              : per <= 32 ? &cache_plan_kernel<32> : &cache_plan_kernel<64>;
     if ((st = check_lds(reinterpret_cast<const void*>(plan), lds))) return st;
     plan<<<(unsigned)n_slices, kPlanThreads, lds, s>>>(row_ws, n_sel, fire, n_kv_heads, budget, cache_rows, pool_rows,
                                                        step, buf_row, slot_step, slot_list, fslot, frow, nfetch,

@@ -59,7 +59,7 @@ MAX_UNITS = 8192   # units one slice's retrieval scores (the library's limit)
 FUSED_STEP_MAX_SLICES = 64
 # KV_critical over a host-resident pool: an LRU cache of this many budgets of
 # pool rows per slice in HBM (the default; cache_rows overrides it)
-HOST_CACHE_BUDGETS = 8
+HOST_CACHE_BUDGETS = 16
 
 
 @dataclass(frozen=True)

@@ -590,7 +590,7 @@ def retrieve_delta(q, n_kv_heads: int, reps, unit_start, unit_size, n_units: int
         _ptr(slot_list), _ptr(n_fetched), _ptr(scores_out), _ptr(ws), wsb, _stream(stream)))
 
 
-CACHE_MAX_ROWS = 32768   # louiskv_retrieve_cached: slots per slice at most
+CACHE_MAX_ROWS = 65536   # louiskv_retrieve_cached: slots per slice at most
 
 
 def retrieve_cached(q, n_kv_heads: int, reps, unit_start, unit_size, n_units: int, k_pool, v_pool, budget: int,

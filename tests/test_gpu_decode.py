@@ -593,15 +593,18 @@ def test_decode_loop_host_pool(delta):
         assert 0 < st["fetched"] < st["selected"]
 
 
-@pytest.mark.parametrize("segments", ["fixed", "boundary"])
-def test_decode_loop_host_pool_lru_cache(segments):
-    """KV_critical as an LRU cache of four budgets of pool rows over a pinned
-    host pool: oracle parity of every step, and slots, steps and fetch counts
-    equal to the LRU policy written out in Python; the cache fetches fewer
-    rows than the one-budget buffer on the same inputs."""
-    wl = synth.get_workload("host-131k").replace(prompt_len=2048, n_clusters=64, budget=512, window=64, seg_len=16,
-                                                 name="host-131k")
-    st = _run_loop(wl, 1, 200, mode=1, pool_on_host=True, segments=segments, cache_rows=4 * 512)
+@pytest.mark.parametrize("segments,prompt,budget,cache", [("fixed", 2048, 512, 4 * 512),
+                                                           ("boundary", 2048, 512, 4 * 512),
+                                                           ("fixed", 4096, 1024, 36 * 1024)])
+def test_decode_loop_host_pool_lru_cache(segments, prompt, budget, cache):
+    """KV_critical as an LRU cache of pool rows over a pinned host pool (four
+    budgets; and 36 K slots, more than the pool's rows, which takes the plan's
+    longest register runs): oracle parity of every step, and slots, steps and
+    fetch counts equal to the LRU policy written out in Python; the cache
+    fetches fewer rows than the one-budget buffer on the same inputs."""
+    wl = synth.get_workload("host-131k").replace(prompt_len=prompt, n_clusters=64, budget=budget, window=64,
+                                                 seg_len=16, name="host-131k")
+    st = _run_loop(wl, 1, 200, mode=1, pool_on_host=True, segments=segments, cache_rows=cache)
     assert st["fires"] > 20 and 0 < st["fetched"] < st["selected"]
     base = _run_loop(wl, 1, 200, mode=1, pool_on_host=True, segments=segments, cache_rows=wl.budget)
     print(f"fetched rows: LRU cache {st['fetched']}, one budget {base['fetched']}", flush=True)
