@@ -321,12 +321,8 @@ __global__ void seg_state_init_kernel(int32_t* __restrict__ state, int64_t n_sli
 #ifndef LKV_SEL_THREADS
 #define LKV_SEL_THREADS 512
 #endif
-#ifndef LKV_SEL_BATCH
-#define LKV_SEL_BATCH 4
-#endif
 constexpr int kSelThreads = LKV_SEL_THREADS;
 constexpr int kSelWaves = kSelThreads / 64;
-constexpr int kSelBatch = LKV_SEL_BATCH;   // unit quads per wave with loads in flight
 constexpr int kUnitIdBits = 13;       // kMaxUnits = 2^13
 
 // Sort key of a unit: larger is ranked first.  The score (a non-negative
@@ -405,10 +401,96 @@ __device__ __forceinline__ int slice_units(const int32_t* seg_state, int seg_str
 }
 
 // Logits l_ju = q_j . rep_u * scale of the group-consistent score (Appendix
-// B), float64, for one part of one fired slice's units (n_parts blocks per
-// slice, so that few slices still spread over many CUs): 16 lanes per unit,
-// lane sub holding dims 8*sub..+7 of the G queries in float64 registers,
-// kSelBatch quads of units in flight per wave.
+// B) in float64.  A unit's 128 dimensions are split over kLPU lanes (8 for
+// up to 4 heads per group, else 16): lane `sub` holds the 4-dim pieces
+// 4*sub + 4*kLPU*c (c = 0 .. kDims/4 - 1) of the G queries in float64
+// registers, so that each 16-byte load of a lane group reads whole 128-byte
+// lines of the unit's row; the lanes' partial dot products are summed over
+// the lane group by DPP.  A wave takes 32 units per iteration,
+// all their loads in flight (16 KiB a wave).  The per-stage and the fused selection kernels
+// share this code, so their scores are equal bit for bit.
+template <int G>
+struct LogitLayout {
+  static constexpr int kLPU = G <= 4 ? 8 : 16;        // lanes per unit
+  static constexpr int kDims = kHeadDim / kLPU;       // dims per lane
+  static constexpr int kGroups = 64 / kLPU;           // units per wave instruction
+  static constexpr int kPerLane = 32 / kGroups;       // units per lane per iteration
+};
+constexpr int kLogitUnitsPerIter = 32;
+
+template <int G, class T>
+__device__ __forceinline__ void load_q_f64(const T* __restrict__ q, size_t row0, int lane,
+                                           double (&qd)[G][LogitLayout<G>::kDims]) {
+  using LL = LogitLayout<G>;
+  const int sub = lane % LL::kLPU;
+#pragma unroll
+  for (int j = 0; j < G; ++j)
+#pragma unroll
+    for (int e = 0; e < LL::kDims; ++e)
+      qd[j][e] = (double)load_as_f32(q, (row0 + j) * kHeadDim + (e / 4) * (4 * LL::kLPU) + 4 * sub + e % 4);
+}
+
+// Sum of a float64 over the kLPU lanes of a unit's lane group.
+template <int kLPU>
+__device__ __forceinline__ double lane_group_sum_f64(double x) {
+#define LKV_DPP64(ctrl)                                                                                   \
+  {                                                                                                       \
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)__double2loint(x), ctrl, 0xF, 0xF, false);        \
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)__double2hiint(x), ctrl, 0xF, 0xF, false);        \
+    x += __hiloint2double(hi, lo);                                                                        \
+  }
+  LKV_DPP64(0xB1) LKV_DPP64(0x4E) LKV_DPP64(0x141)
+  if constexpr (kLPU == 16) LKV_DPP64(0x140)
+#undef LKV_DPP64
+  return x;
+}
+
+// The logits of units u0 .. u0 + 31 (those below u_end): maxima per head into
+// mx, each logit stored once (kShared: with device-scope stores, for another
+// block of the same launch to read).
+template <int G, bool kShared>
+__device__ __forceinline__ void wave_unit_logits(const double (&qd)[G][LogitLayout<G>::kDims],
+                                                 const float* __restrict__ rs, int u0, int u_end, double scale,
+                                                 double* __restrict__ lg, double (&mx)[G], int lane) {
+  using LL = LogitLayout<G>;
+  const int sub = lane % LL::kLPU, gid = lane / LL::kLPU;
+  float4 x[LL::kPerLane][LL::kDims / 4];
+#pragma unroll
+  for (int i = 0; i < LL::kPerLane; ++i) {
+    const int u = min(u0 + i * LL::kGroups + gid, u_end - 1);   // past the end: re-read the last unit, unused
+    const float* r = rs + (size_t)u * kHeadDim + 4 * sub;
+#pragma unroll
+    for (int c = 0; c < LL::kDims / 4; ++c) x[i][c] = *reinterpret_cast<const float4*>(r + 4 * LL::kLPU * c);
+  }
+#pragma unroll
+  for (int i = 0; i < LL::kPerLane; ++i) {
+    const int u = u0 + i * LL::kGroups + gid;
+    double xd[LL::kDims];
+#pragma unroll
+    for (int c = 0; c < LL::kDims / 4; ++c) {
+      xd[4 * c] = x[i][c].x; xd[4 * c + 1] = x[i][c].y; xd[4 * c + 2] = x[i][c].z; xd[4 * c + 3] = x[i][c].w;
+    }
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      double a = 0.0;
+#pragma unroll
+      for (int e = 0; e < LL::kDims; ++e) a = fma(qd[j][e], xd[e], a);
+      a = lane_group_sum_f64<LL::kLPU>(a) * scale;
+      if (u < u_end) {
+        mx[j] = fmax(mx[j], a);
+        if (sub == j) {
+          if constexpr (kShared)
+            __hip_atomic_store(lg + (size_t)u * G + j, a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          else
+            lg[(size_t)u * G + j] = a;
+        }
+      }
+    }
+  }
+}
+
+// The logits of one part of one fired slice's units (n_parts blocks per
+// slice, so that few slices still spread over many CUs).
 template <class T, int G>
 __global__ __launch_bounds__(kLogitThreads)
 void unit_logits_kernel(const T* __restrict__ q, int n_kv_heads, double scale, const float* __restrict__ reps,
@@ -427,39 +509,16 @@ void unit_logits_kernel(const T* __restrict__ q, int n_kv_heads, double scale, c
   const int kvh = (int)(s - grp * n_kv_heads);
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int sub = lane & 15, quad = lane >> 4;
   const int n_q_heads = n_kv_heads * G;
-  double qd[G][8];
-#pragma unroll
-  for (int j = 0; j < G; ++j)
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      qd[j][e] = (double)load_as_f32(q, ((size_t)grp * n_q_heads + (size_t)kvh * G + j) * kHeadDim + 8 * sub + e);
+  double qd[G][LogitLayout<G>::kDims];
+  load_q_f64<G>(q, (size_t)grp * n_q_heads + (size_t)kvh * G, lane, qd);
   double* lg = logit_ws + (size_t)s * units_cap * G;
   const float* rs = reps + (size_t)ps * units_cap * kHeadDim;
-  for (int u0 = u_begin + w * 4 * kSelBatch; u0 < u_end; u0 += kLogitWaves * 4 * kSelBatch) {
-    float4 x[kSelBatch][2];
+  double mx[G];   // unused here: the selection kernel takes the maxima of the stored logits
 #pragma unroll
-    for (int i = 0; i < kSelBatch; ++i) {
-      const int u = min(u0 + 4 * i + quad, u_end - 1);   // past the end: re-read the last unit, unused
-      const float4* r4 = reinterpret_cast<const float4*>(rs + (size_t)u * kHeadDim + 8 * sub);
-      x[i][0] = r4[0];
-      x[i][1] = r4[1];
-    }
-#pragma unroll
-    for (int i = 0; i < kSelBatch; ++i) {
-      const int u = u0 + 4 * i + quad;
-      const double xd[8] = {x[i][0].x, x[i][0].y, x[i][0].z, x[i][0].w, x[i][1].x, x[i][1].y, x[i][1].z, x[i][1].w};
-#pragma unroll
-      for (int j = 0; j < G; ++j) {
-        double a = 0.0;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) a = fma(qd[j][e], xd[e], a);
-        a = row16_sum_f64(a) * scale;
-        if (u < u_end && sub == j) lg[(size_t)u * G + j] = a;
-      }
-    }
-  }
+  for (int j = 0; j < G; ++j) mx[j] = -__builtin_inf();
+  for (int u0 = u_begin + w * kLogitUnitsPerIter; u0 < u_end; u0 += kLogitWaves * kLogitUnitsPerIter)
+    wave_unit_logits<G, false>(qd, rs, u0, u_end, scale, lg, mx, lane);
 }
 
 // Number of logit blocks per slice: 1 (the selection kernel computes them
@@ -889,44 +948,13 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
   for (int j = 0; j < G; ++j) mx[j] = -__builtin_inf();
   double* lg = logit_ws + (size_t)s * units_cap * G;
   if (own_logits) {
-    const int64_t grp_q = grp;
     const int kvh = (int)(s - grp * n_kv_heads);
-    const int sub = lane & 15, quad = lane >> 4;
     const int n_q_heads = n_kv_heads * G;
-    double qd[G][8];
-#pragma unroll
-    for (int j = 0; j < G; ++j)
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        qd[j][e] = (double)load_as_f32(q, ((size_t)grp_q * n_q_heads + (size_t)kvh * G + j) * kHeadDim + 8 * sub + e);
+    double qd[G][LogitLayout<G>::kDims];
+    load_q_f64<G>(q, (size_t)grp * n_q_heads + (size_t)kvh * G, lane, qd);
     const float* rs = reps + (size_t)ps * units_cap * kHeadDim;
-    for (int u0 = w * 4 * kSelBatch; u0 < n_units; u0 += kSelWaves * 4 * kSelBatch) {
-      float4 x[kSelBatch][2];
-#pragma unroll
-      for (int i = 0; i < kSelBatch; ++i) {
-        const int u = min(u0 + 4 * i + quad, n_units - 1);   // past the end: re-read the last unit, unused
-        const float4* r4 = reinterpret_cast<const float4*>(rs + (size_t)u * kHeadDim + 8 * sub);
-        x[i][0] = r4[0];
-        x[i][1] = r4[1];
-      }
-#pragma unroll
-      for (int i = 0; i < kSelBatch; ++i) {
-        const int u = u0 + 4 * i + quad;
-        const double xd[8] = {x[i][0].x, x[i][0].y, x[i][0].z, x[i][0].w,
-                              x[i][1].x, x[i][1].y, x[i][1].z, x[i][1].w};
-#pragma unroll
-        for (int j = 0; j < G; ++j) {
-          double a = 0.0;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) a = fma(qd[j][e], xd[e], a);
-          a = row16_sum_f64(a) * scale;
-          if (u < n_units) {
-            mx[j] = fmax(mx[j], a);
-            if (sub == j) lg[(size_t)u * G + j] = a;
-          }
-        }
-      }
-    }
+    for (int u0 = w * kLogitUnitsPerIter; u0 < n_units; u0 += kSelWaves * kLogitUnitsPerIter)
+      wave_unit_logits<G, false>(qd, rs, u0, n_units, scale, lg, mx, lane);
   } else {
     for (int u = tid; u < n_units; u += kSelThreads) {
 #pragma unroll
@@ -1008,46 +1036,16 @@ void step_select_kernel(const T* __restrict__ q, const T* __restrict__ q_ref, in
   // logits of this part's units and their maxima
   const int per = (n_units + n_parts - 1) / n_parts;
   const int u_begin = part * per, u_end = min(n_units, u_begin + per);
-  const int sub = lane & 15, quad = lane >> 4;
   double mx[G];
 #pragma unroll
   for (int j = 0; j < G; ++j) mx[j] = -__builtin_inf();
   double* lg = logit_ws + (size_t)s * units_cap * G;
   if (u_begin < u_end) {
-    double qd[G][8];
-#pragma unroll
-    for (int j = 0; j < G; ++j)
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        qd[j][e] = (double)load_as_f32(q, ((size_t)grp * n_q_heads + (size_t)kvh * G + j) * kHeadDim + 8 * sub + e);
+    double qd[G][LogitLayout<G>::kDims];
+    load_q_f64<G>(q, (size_t)grp * n_q_heads + (size_t)kvh * G, lane, qd);
     const float* rs = reps + (size_t)s * units_cap * kHeadDim;
-    for (int u0 = u_begin + w * 4 * kSelBatch; u0 < u_end; u0 += kSelWaves * 4 * kSelBatch) {
-      float4 x[kSelBatch][2];
-#pragma unroll
-      for (int i = 0; i < kSelBatch; ++i) {
-        const int u = min(u0 + 4 * i + quad, u_end - 1);   // past the end: re-read the last unit, unused
-        const float4* r4 = reinterpret_cast<const float4*>(rs + (size_t)u * kHeadDim + 8 * sub);
-        x[i][0] = r4[0];
-        x[i][1] = r4[1];
-      }
-#pragma unroll
-      for (int i = 0; i < kSelBatch; ++i) {
-        const int u = u0 + 4 * i + quad;
-        const double xd[8] = {x[i][0].x, x[i][0].y, x[i][0].z, x[i][0].w,
-                              x[i][1].x, x[i][1].y, x[i][1].z, x[i][1].w};
-#pragma unroll
-        for (int j = 0; j < G; ++j) {
-          double a = 0.0;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) a = fma(qd[j][e], xd[e], a);
-          a = row16_sum_f64(a) * scale;
-          if (u < u_end) {
-            mx[j] = fmax(mx[j], a);
-            if (sub == j) __hip_atomic_store(lg + (size_t)u * G + j, a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          }
-        }
-      }
-    }
+    for (int u0 = u_begin + w * kLogitUnitsPerIter; u0 < u_end; u0 += kSelWaves * kLogitUnitsPerIter)
+      wave_unit_logits<G, true>(qd, rs, u0, u_end, scale, lg, mx, lane);
   }
 #pragma unroll
   for (int j = 0; j < G; ++j) {
