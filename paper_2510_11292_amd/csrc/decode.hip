@@ -1599,7 +1599,7 @@ constexpr int kAttnMinRows = 256;
 #ifndef LKV_STEP_ATTN_ROWS
 #define LKV_STEP_ATTN_ROWS 128
 #endif
-constexpr int kStepAttnWaves = 4;
+constexpr int kStepAttnWaves = 8;
 constexpr int kStepAttnRows = LKV_STEP_ATTN_ROWS;
 
 // Sum over the 16 lanes of a DPP row, result in every lane of the row:
