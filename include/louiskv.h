@@ -479,6 +479,49 @@ int louiskv_decode_step(const void* q, void* q_ref, int32_t dtype, int64_t n_gro
                         size_t workspace_bytes, void* stream);
 
 /*
+ * louiskv_decode_step with KV_critical kept as an LRU cache of pool rows in
+ * device memory (louiskv_retrieve_cached), for a pool in device or pinned host
+ * memory (Algorithm 1 offloads the KV cache; Appendix A names the transfer
+ * as the bottleneck): the boundary test, store and selection launch as in
+ * louiskv_decode_step (the store writes the pool through pool_on_host's
+ * device mapping), then the transfer plan of the fired slices and the copy
+ * of the rows the cache lacks, then the attention over the cached rows
+ * through slot_list.  Four launches.
+ *
+ * Results equal louiskv_decode_prologue + louiskv_retrieve_cached +
+ * louiskv_sparse_decode_attn_rows over (k_buf, v_buf, slot_list) bit for
+ * bit (selection, scores, r, decisions, reference queries, window, unit
+ * table, pool, buffer rows, slot steps, slot list, fetch counts and cached
+ * rows), except the attention output and lse (float32 summation order).
+ *
+ * Arguments as louiskv_decode_step, plus: pool_on_host as
+ * louiskv_retrieve_cached (k_pool, v_pool in pinned host memory); budget >= 1;
+ * cache_rows, k_buf, v_buf, buf_row, slot_step, slot_list, n_fetched
+ * (nullable) as louiskv_retrieve_cached (budget <= cache_rows <= 65536,
+ * pool_rows <= 524288, step <= 2^24 - 2).  sel_rows [n_slices][budget]
+ * receives the selected pool rows (the plan's input).
+ *
+ * workspace  louiskv_decode_step_cached_workspace_size() bytes, zero before
+ *            its first use, as louiskv_decode_step's.
+ */
+size_t louiskv_decode_step_cached_workspace_size(int64_t n_slices, int32_t dtype, int32_t group_size,
+                                                 int32_t units_cap, int32_t budget, int32_t window);
+
+int louiskv_decode_step_cached(const void* q, void* q_ref, int32_t dtype, int64_t n_groups,
+                               int32_t n_q_heads, int32_t n_kv_heads, int32_t d, double tau,
+                               int32_t mode, int32_t step, double* r_out, uint8_t* fire_out,
+                               const void* k_new, const void* v_new, void* k_local, void* v_local,
+                               int32_t window, int32_t seg_len, float* reps, int32_t* unit_start,
+                               int32_t* unit_size, int32_t units_cap, int32_t n_clusters,
+                               void* k_pool, void* v_pool, int64_t pool_rows, int32_t pool_on_host,
+                               int32_t prompt_len, int32_t budget, int32_t cache_rows, void* k_buf,
+                               void* v_buf, int32_t* buf_row, int32_t* slot_step, int32_t* slot_list,
+                               int32_t* n_fetched, int32_t* sel_units, int32_t* n_sel_units,
+                               int32_t* n_sel, int32_t* sel_rows, double* scores_out, void* out,
+                               int32_t out_dtype, float* lse_out, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/*
  * louiskv_sparse_decode_attn_rows for callers that cannot allocate: code under
  * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
  * Arguments, arithmetic and outputs are those of

@@ -2860,10 +2860,13 @@ namespace {
 // must be zero before the first call and are zero after every call), the
 // logits and per-part maxima of the selection, the attention partials.
 struct StepLayout {
-  size_t counters, logits, pmax, part, total;
+  size_t counters, logits, pmax, fetch, part, total;
 };
 
-StepLayout step_layout(int64_t S, int dtype, int G, int units_cap, int budget, int window) {
+// Workspace of a decode step: the arrival counters (zero between calls),
+// logits and part maxima, with a cached KV_critical the transfer plan's
+// scratch (fetch slots, rows, counts), and the attention partials.
+StepLayout step_layout(int64_t S, int dtype, int G, int units_cap, int budget, int window, bool cached = false) {
   StepLayout L{};
   Carver cv(nullptr);
   cv.take<int32_t>((size_t)2 * S);
@@ -2871,12 +2874,27 @@ StepLayout step_layout(int64_t S, int dtype, int G, int units_cap, int budget, i
   cv.take<double>((size_t)S * units_cap * G);
   L.pmax = align_up(cv.used, 256);
   cv.take<double>((size_t)S * kMaxLogitParts * G);
+  L.fetch = align_up(cv.used, 256);
+  if (cached) cv.take<int32_t>((size_t)S * (2 * (size_t)std::max(budget, 1) + 1));
   L.part = align_up(cv.used, 256);
   cv.take<char>(step_attn_part_bytes(S, G, budget, window, dtype));
   L.counters = 0;
   L.total = align_up(cv.used, 256);
   return L;
 }
+
+int plan_and_fetch(const int32_t* row_ws, const int32_t* n_sel, const uint8_t* fire, int64_t n_slices,
+                   int32_t n_kv_heads, int32_t budget, int32_t cache_rows, int64_t pool_rows, int32_t step,
+                   int32_t* buf_row, int32_t* slot_step, int32_t* slot_list, int32_t* fslot, int32_t* frow,
+                   int32_t* nfetch, int32_t* n_fetched, int32_t dtype, const void* kpd, const void* vpd, void* k_buf,
+                   void* v_buf, hipStream_t s);
+
+// KV_critical kept as an LRU cache of pool rows (louiskv_decode_step_cached).
+struct StepCache {
+  int32_t pool_on_host, cache_rows;
+  void *k_buf, *v_buf;
+  int32_t *buf_row, *slot_step, *slot_list, *n_fetched;
+};
 
 }  // namespace
 }  // namespace louiskv
@@ -2889,15 +2907,16 @@ extern "C" size_t louiskv_decode_step_workspace_size(int64_t n_slices, int32_t d
   return step_layout(n_slices, dtype, group_size, units_cap, budget, window).total;
 }
 
-extern "C" int louiskv_decode_step(const void* q, void* q_ref, int32_t dtype, int64_t n_groups, int32_t n_q_heads,
-                                   int32_t n_kv_heads, int32_t d, double tau, int32_t mode, int32_t step,
-                                   double* r_out, uint8_t* fire_out, const void* k_new, const void* v_new,
-                                   void* k_local, void* v_local, int32_t window, int32_t seg_len, float* reps,
-                                   int32_t* unit_start, int32_t* unit_size, int32_t units_cap, int32_t n_clusters,
-                                   void* k_pool, void* v_pool, int64_t pool_rows, int32_t prompt_len, int32_t budget,
-                                   int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel, int32_t* sel_rows,
-                                   double* scores_out, void* out, int32_t out_dtype, float* lse_out,
-                                   void* workspace, size_t workspace_bytes, void* stream) {
+namespace louiskv {
+namespace {
+int decode_step_impl(const void* q, void* q_ref, int32_t dtype, int64_t n_groups, int32_t n_q_heads,
+                     int32_t n_kv_heads, int32_t d, double tau, int32_t mode, int32_t step, double* r_out,
+                     uint8_t* fire_out, const void* k_new, const void* v_new, void* k_local, void* v_local,
+                     int32_t window, int32_t seg_len, float* reps, int32_t* unit_start, int32_t* unit_size,
+                     int32_t units_cap, int32_t n_clusters, void* k_pool, void* v_pool, int64_t pool_rows,
+                     int32_t prompt_len, int32_t budget, int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel,
+                     int32_t* sel_rows, double* scores_out, void* out, int32_t out_dtype, float* lse_out,
+                     void* workspace, size_t workspace_bytes, void* stream, const StepCache* cache) {
   if (!q || !q_ref || !fire_out || !k_new || !v_new || !k_local || !v_local || !out)
     return fail(LOUISKV_ERR_NULL, "q, q_ref, fire_out, k_new, v_new, k_local, v_local and out are required");
   if (!reps || !unit_start || !unit_size || !k_pool || !v_pool || !sel_units || !n_sel_units || !n_sel || !sel_rows)
@@ -2929,7 +2948,23 @@ extern "C" int louiskv_decode_step(const void* q, void* q_ref, int32_t dtype, in
   if ((int64_t)prompt_len + (int64_t)(ev + 1) * seg_len > pool_rows || pool_rows < 1)
     return fail(LOUISKV_ERR_SHAPE, "segment rows exceed pool_rows=%lld", (long long)pool_rows);
   const int64_t n_slices = n_groups * n_kv_heads;
-  const StepLayout lay = step_layout(n_slices, dtype, group_size, units_cap, budget, window);
+  void* kpd = k_pool;
+  void* vpd = v_pool;
+  if (cache) {
+    if (!cache->k_buf || !cache->v_buf || !cache->buf_row || !cache->slot_step || !cache->slot_list)
+      return fail(LOUISKV_ERR_NULL, "k_buf, v_buf, buf_row, slot_step and slot_list are required");
+    if (budget < 1 || cache->cache_rows < budget || cache->cache_rows > kCacheMaxRows)
+      return fail(LOUISKV_ERR_SHAPE, "cache_rows=%d must be in [budget=%d, %d]", cache->cache_rows, budget,
+                  kCacheMaxRows);
+    if (step > kCacheMaxStep) return fail(LOUISKV_ERR_SHAPE, "step=%d must be at most %d", step, kCacheMaxStep);
+    if (pool_rows > kDeltaMaxPoolRows)
+      return fail(LOUISKV_ERR_UNSUPPORTED, "pool_rows=%lld must be at most %lld", (long long)pool_rows,
+                  (long long)kDeltaMaxPoolRows);
+    if (cache->pool_on_host &&
+        ((st = device_view_of_host_pool(k_pool, &kpd)) || (st = device_view_of_host_pool(v_pool, &vpd))))
+      return st;
+  }
+  const StepLayout lay = step_layout(n_slices, dtype, group_size, units_cap, budget, window, cache != nullptr);
   if (!workspace || workspace_bytes < lay.total)
     return fail(LOUISKV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", lay.total, workspace_bytes);
   char* ws = static_cast<char*>(workspace);
@@ -2949,8 +2984,8 @@ extern "C" int louiskv_decode_step(const void* q, void* q_ref, int32_t dtype, in
   step_select_kernel<T, G><<<grid, kSelThreads, lds, s>>>(                                                           \
       static_cast<const T*>(q), static_cast<const T*>(q_ref), n_kv_heads, tau, step == 0 ? 1 : 0, r_out, fire_out,  \
       static_cast<const T*>(k_new), static_cast<const T*>(v_new), static_cast<T*>(k_local), static_cast<T*>(v_local), \
-      window, step, seg_len, ev, reps, unit_start, unit_size, units_cap, n_clusters, static_cast<T*>(k_pool),        \
-      static_cast<T*>(v_pool), pool_rows, prompt_len, scale, (int)n_units, budget, sel_units, n_sel_units, n_sel,     \
+      window, step, seg_len, ev, reps, unit_start, unit_size, units_cap, n_clusters, static_cast<T*>(kpd),           \
+      static_cast<T*>(vpd), pool_rows, prompt_len, scale, (int)n_units, budget, sel_units, n_sel_units, n_sel,         \
       sel_rows, scores_out, logit_ws, part_max, sel_counter, n_parts, n_pad)
 #define LKV_STEP_SEL_G(T)                   \
   switch (group_size) {                     \
@@ -2968,10 +3003,66 @@ extern "C" int louiskv_decode_step(const void* q, void* q_ref, int32_t dtype, in
 #undef LKV_STEP_SEL
   LKV_CHECK_LAUNCH();
   const StepSync sync = {attn_counter, q_ref, fire_out, mode};
-  return sparse_decode_attn(q, dtype, n_slices, n_kv_heads, group_size, d, (float)scale, k_pool, v_pool, n_sel,
-                            budget, sel_rows, pool_rows, k_local, v_local, window, local_start, n_local, out,
-                            out_dtype, lse_out, ws + lay.part, lay.total - lay.part, stream, nullptr, 0, 1, &sync);
+  if (!cache)
+    return sparse_decode_attn(q, dtype, n_slices, n_kv_heads, group_size, d, (float)scale, k_pool, v_pool, n_sel,
+                              budget, sel_rows, pool_rows, k_local, v_local, window, local_start, n_local, out,
+                              out_dtype, lse_out, ws + lay.part, lay.total - lay.part, stream, nullptr, 0, 1, &sync);
+  // the fired slices' selections (sel_rows) into the cache, then the
+  // attention over the cached rows through the slot list
+  int32_t* fslot = reinterpret_cast<int32_t*>(ws + lay.fetch);
+  int32_t* frow = fslot + (size_t)n_slices * budget;
+  int32_t* nfetch = frow + (size_t)n_slices * budget;
+  if ((st = plan_and_fetch(sel_rows, n_sel, fire_out, n_slices, n_kv_heads, budget, cache->cache_rows, pool_rows,
+                           step, cache->buf_row, cache->slot_step, cache->slot_list, fslot, frow, nfetch,
+                           cache->n_fetched, dtype, kpd, vpd, cache->k_buf, cache->v_buf, s)))
+    return st;
+  return sparse_decode_attn(q, dtype, n_slices, n_kv_heads, group_size, d, (float)scale, cache->k_buf, cache->v_buf,
+                            n_sel, budget, cache->slot_list, cache->cache_rows, k_local, v_local, window, local_start,
+                            n_local, out, out_dtype, lse_out, ws + lay.part, lay.total - lay.part, stream, nullptr, 0, 1,
+                            &sync);
 }
+}  // namespace
+}  // namespace louiskv
+
+extern "C" int louiskv_decode_step(const void* q, void* q_ref, int32_t dtype, int64_t n_groups, int32_t n_q_heads,
+                                   int32_t n_kv_heads, int32_t d, double tau, int32_t mode, int32_t step,
+                                   double* r_out, uint8_t* fire_out, const void* k_new, const void* v_new,
+                                   void* k_local, void* v_local, int32_t window, int32_t seg_len, float* reps,
+                                   int32_t* unit_start, int32_t* unit_size, int32_t units_cap, int32_t n_clusters,
+                                   void* k_pool, void* v_pool, int64_t pool_rows, int32_t prompt_len, int32_t budget,
+                                   int32_t* sel_units, int32_t* n_sel_units, int32_t* n_sel, int32_t* sel_rows,
+                                   double* scores_out, void* out, int32_t out_dtype, float* lse_out,
+                                   void* workspace, size_t workspace_bytes, void* stream) {
+  return decode_step_impl(q, q_ref, dtype, n_groups, n_q_heads, n_kv_heads, d, tau, mode, step, r_out, fire_out, k_new,
+                          v_new, k_local, v_local, window, seg_len, reps, unit_start, unit_size, units_cap, n_clusters,
+                          k_pool, v_pool, pool_rows, prompt_len, budget, sel_units, n_sel_units, n_sel, sel_rows,
+                          scores_out, out, out_dtype, lse_out, workspace, workspace_bytes, stream, nullptr);
+}
+
+extern "C" size_t louiskv_decode_step_cached_workspace_size(int64_t n_slices, int32_t dtype, int32_t group_size,
+                                                            int32_t units_cap, int32_t budget, int32_t window) {
+  if (n_slices < 1 || group_size < 1 || group_size > kMaxGroupSize || units_cap < 1 || budget < 1 || window < 0 ||
+      (dtype != LOUISKV_F32 && dtype != LOUISKV_BF16))
+    return 0;
+  return step_layout(n_slices, dtype, group_size, units_cap, budget, window, true).total;
+}
+
+extern "C" int louiskv_decode_step_cached(
+    const void* q, void* q_ref, int32_t dtype, int64_t n_groups, int32_t n_q_heads, int32_t n_kv_heads, int32_t d,
+    double tau, int32_t mode, int32_t step, double* r_out, uint8_t* fire_out, const void* k_new, const void* v_new,
+    void* k_local, void* v_local, int32_t window, int32_t seg_len, float* reps, int32_t* unit_start,
+    int32_t* unit_size, int32_t units_cap, int32_t n_clusters, void* k_pool, void* v_pool, int64_t pool_rows,
+    int32_t pool_on_host, int32_t prompt_len, int32_t budget, int32_t cache_rows, void* k_buf, void* v_buf,
+    int32_t* buf_row, int32_t* slot_step, int32_t* slot_list, int32_t* n_fetched, int32_t* sel_units,
+    int32_t* n_sel_units, int32_t* n_sel, int32_t* sel_rows, double* scores_out, void* out, int32_t out_dtype,
+    float* lse_out, void* workspace, size_t workspace_bytes, void* stream) {
+  const StepCache cache{pool_on_host, cache_rows, k_buf, v_buf, buf_row, slot_step, slot_list, n_fetched};
+  return decode_step_impl(q, q_ref, dtype, n_groups, n_q_heads, n_kv_heads, d, tau, mode, step, r_out, fire_out, k_new,
+                          v_new, k_local, v_local, window, seg_len, reps, unit_start, unit_size, units_cap, n_clusters,
+                          k_pool, v_pool, pool_rows, prompt_len, budget, sel_units, n_sel_units, n_sel, sel_rows,
+                          scores_out, out, out_dtype, lse_out, workspace, workspace_bytes, stream, &cache);
+}
+
 
 // ---------------------------------------------------------------------------
 // Allocation-free attention over listed pool rows.  The split-KV partials live
@@ -3123,6 +3214,50 @@ extern "C" size_t louiskv_retrieve_delta_workspace_size(int64_t n_slices, int32_
 
 namespace louiskv {
 namespace {
+// The transfer plan of the fired slices' selections (row_ws: [S][budget]
+// pool rows, n_sel each) into the KV_critical buffers (slot_step: the LRU
+// cache of cache_rows slots; null: the buffer holds the last selection) and
+// the copy of the planned rows; fslot, frow [S][budget] and nfetch [S] are
+// scratch.
+int plan_and_fetch(const int32_t* row_ws, const int32_t* n_sel, const uint8_t* fire, int64_t n_slices,
+                   int32_t n_kv_heads, int32_t budget, int32_t cache_rows, int64_t pool_rows, int32_t step,
+                   int32_t* buf_row, int32_t* slot_step, int32_t* slot_list, int32_t* fslot, int32_t* frow,
+                   int32_t* nfetch, int32_t* n_fetched, int32_t dtype, const void* kpd, const void* vpd, void* k_buf,
+                   void* v_buf, hipStream_t s) {
+  int st;
+  const size_t lds = (size_t)((pool_rows + 31) / 32) * sizeof(uint32_t);
+  if (slot_step) {
+    // the smallest per-thread slot run that covers cache_rows
+    const int per = (cache_rows + kPlanThreads - 1) / kPlanThreads;
+    auto plan = per <= 8 ? &cache_plan_kernel<8> : per <= 16 ? &cache_plan_kernel<16>
+              : per <= 32 ? &cache_plan_kernel<32> : &cache_plan_kernel<64>;
+    if ((st = check_lds(reinterpret_cast<const void*>(plan), lds))) return st;
+    plan<<<(unsigned)n_slices, kPlanThreads, lds, s>>>(row_ws, n_sel, fire, n_kv_heads, budget, cache_rows, pool_rows,
+                                                       step, buf_row, slot_step, slot_list, fslot, frow, nfetch,
+                                                       n_fetched);
+  } else {
+    if ((st = check_lds(reinterpret_cast<const void*>(&delta_plan_kernel), lds))) return st;
+    delta_plan_kernel<<<(unsigned)n_slices, kPlanThreads, lds, s>>>(row_ws, n_sel, fire, n_kv_heads, budget,
+                                                                    pool_rows, buf_row, slot_list, fslot, frow, nfetch,
+                                                                    n_fetched);
+  }
+  LKV_CHECK_LAUNCH();
+  const int rpb = 128;
+  const int bps = (budget + rpb - 1) / rpb;
+  const unsigned grid = (unsigned)(n_slices * bps);
+  if (dtype == LOUISKV_BF16)
+    delta_fetch_kernel<uint16_t><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(kpd),
+                                                      static_cast<const uint16_t*>(vpd), pool_rows, fslot, frow, nfetch,
+                                                      budget, bps, rpb, static_cast<uint16_t*>(k_buf),
+                                                      static_cast<uint16_t*>(v_buf), cache_rows);
+  else
+    delta_fetch_kernel<float><<<grid, 256, 0, s>>>(static_cast<const float*>(kpd), static_cast<const float*>(vpd),
+                                                   pool_rows, fslot, frow, nfetch, budget, bps, rpb,
+                                                   static_cast<float*>(k_buf), static_cast<float*>(v_buf), cache_rows);
+  LKV_CHECK_LAUNCH();
+  return LOUISKV_OK;
+}
+
 // Scores and selection, then the transfer plan (delta: the buffer holds the
 // last selection only; cached: an LRU cache of cache_rows pool rows) and the
 // fetch of the planned rows.
@@ -3167,37 +3302,8 @@ int retrieve_into_buffer(const void* q, int32_t dtype, int64_t n_slices, int32_t
                              units_cap, n_units, budget, fire, sel_units, n_sel_units, n_sel, row_ws, scores_out,
                              logit_ws, seg_state, seg_state ? kSegRing + window : 0, s)))
     return st;
-  const size_t lds = (size_t)((pool_rows + 31) / 32) * sizeof(uint32_t);
-  if (slot_step) {
-    // the smallest per-thread slot run that covers cache_rows
-    const int per = (cache_rows + kPlanThreads - 1) / kPlanThreads;
-    auto plan = per <= 8 ? &cache_plan_kernel<8> : per <= 16 ? &cache_plan_kernel<16>
-              : per <= 32 ? &cache_plan_kernel<32> : &cache_plan_kernel<64>;
-    if ((st = check_lds(reinterpret_cast<const void*>(plan), lds))) return st;
-    plan<<<(unsigned)n_slices, kPlanThreads, lds, s>>>(row_ws, n_sel, fire, n_kv_heads, budget, cache_rows, pool_rows,
-                                                       step, buf_row, slot_step, slot_list, fslot, frow, nfetch,
-                                                       n_fetched);
-  } else {
-    if ((st = check_lds(reinterpret_cast<const void*>(&delta_plan_kernel), lds))) return st;
-    delta_plan_kernel<<<(unsigned)n_slices, kPlanThreads, lds, s>>>(row_ws, n_sel, fire, n_kv_heads, budget,
-                                                                    pool_rows, buf_row, slot_list, fslot, frow, nfetch,
-                                                                    n_fetched);
-  }
-  LKV_CHECK_LAUNCH();
-  const int rpb = 128;
-  const int bps = (budget + rpb - 1) / rpb;
-  const unsigned grid = (unsigned)(n_slices * bps);
-  if (dtype == LOUISKV_BF16)
-    delta_fetch_kernel<uint16_t><<<grid, 256, 0, s>>>(static_cast<const uint16_t*>(kpd),
-                                                      static_cast<const uint16_t*>(vpd), pool_rows, fslot, frow, nfetch,
-                                                      budget, bps, rpb, static_cast<uint16_t*>(k_buf),
-                                                      static_cast<uint16_t*>(v_buf), cache_rows);
-  else
-    delta_fetch_kernel<float><<<grid, 256, 0, s>>>(static_cast<const float*>(kpd), static_cast<const float*>(vpd),
-                                                   pool_rows, fslot, frow, nfetch, budget, bps, rpb,
-                                                   static_cast<float*>(k_buf), static_cast<float*>(v_buf), cache_rows);
-  LKV_CHECK_LAUNCH();
-  return LOUISKV_OK;
+  return plan_and_fetch(row_ws, n_sel, fire, n_slices, n_kv_heads, budget, cache_rows, pool_rows, step, buf_row,
+                        slot_step, slot_list, fslot, frow, nfetch, n_fetched, dtype, kpd, vpd, k_buf, v_buf, s);
 }
 }  // namespace
 }  // namespace louiskv

@@ -253,16 +253,23 @@ class LouisKVEngine:
         # fixed segments over a device pool with the row-list KV_critical and
         # group-consistent selection; fused_step=None uses it for calls over
         # few slices (a layer at a time), True for every call, False never
-        self._fused_ok = (self.zero_copy and not pool_on_host and cfg.segments == "fixed"
-                          and cfg.trigger == "boundary" and not self.per_head
-                          and cfg.n_q_heads // cfg.n_kv_heads in (1, 2, 4, 8))
+        # (louiskv_decode_step_cached: the same with the LRU cache of pool
+        # rows, in four launches, for device or host pools)
+        step_shape_ok = (cfg.segments == "fixed" and cfg.trigger == "boundary" and not self.per_head
+                         and cfg.n_q_heads // cfg.n_kv_heads in (1, 2, 4, 8))
+        self._fused_cached = step_shape_ok and self.cached
+        self._fused_ok = step_shape_ok and ((self.zero_copy and not pool_on_host) or self._fused_cached)
         if fused_step and not self._fused_ok:
-            raise ValueError("the fused decode step needs fixed segments, a device pool, zero-copy retrieval "
-                             "and group-consistent selection")
+            raise ValueError("the fused decode step needs fixed segments, group-consistent selection and either "
+                             "zero-copy retrieval over a device pool or an LRU cache of pool rows")
         self.fused_step = fused_step
         self.ws_step = None
         if self._fused_ok and fused_step is not False:
-            self.ws_step = torch.zeros(L.decode_step_workspace_size(S, dc, g, cap, cfg.budget, cfg.window), **u8)
+            size = (L.decode_step_cached_workspace_size if self._fused_cached else L.decode_step_workspace_size)
+            self.ws_step = torch.zeros(size(S, dc, g, cap, cfg.budget, cfg.window), **u8)
+            if self._fused_cached:
+                # the selected pool rows, the plan's input
+                self.sel_rows_step = torch.zeros(S, cfg.budget, **i32)
         self.t = 0
 
     def segment_overflow(self) -> bool:
@@ -316,8 +323,8 @@ class LouisKVEngine:
 
     # ------------------------------------------------------- layer by layer
     _PER_SLICE = ("reps", "unit_start", "unit_size", "assign", "perm", "k_pool", "v_pool", "k_local", "v_local",
-                  "sel_rows", "k_buf", "v_buf", "buf_row", "slot_step", "slot_list", "n_fetched", "sel_units",
-                  "n_sel_units", "n_sel", "scores", "seg_state")
+                  "sel_rows", "sel_rows_step", "k_buf", "v_buf", "buf_row", "slot_step", "slot_list",
+                  "n_fetched", "sel_units", "n_sel_units", "n_sel", "scores", "seg_state")
     _PER_GROUP = ("q_ref", "fire", "r", "out", "lse")
 
     def group_view(self, g: int, n: int = 1) -> "LouisKVEngine":
@@ -388,11 +395,20 @@ class LouisKVEngine:
         c = self.cfg
         t = self.t
         if self._use_fused_step():
-            L.decode_step(q_t, self.q_ref, c.tau, c.mode, t, self.fire, self.r, k_t, v_t, self.k_local,
-                          self.v_local, c.seg_len, self.reps, self.unit_start, self.unit_size, c.n_clusters,
-                          self.k_pool, self.v_pool, c.prompt_len, c.budget, self.sel_units, self.n_sel_units,
-                          self.n_sel, self.sel_rows, self.out, self.lse, scores_out=self.scores,
-                          workspace=self.ws_step)
+            if self._fused_cached:
+                L.decode_step_cached(q_t, self.q_ref, c.tau, c.mode, t, self.fire, self.r, k_t, v_t, self.k_local,
+                                     self.v_local, c.seg_len, self.reps, self.unit_start, self.unit_size,
+                                     c.n_clusters, self.k_pool, self.v_pool, c.prompt_len, c.budget, self.k_buf,
+                                     self.v_buf, self.buf_row, self.slot_step, self.slot_list, self.sel_units,
+                                     self.n_sel_units, self.n_sel, self.sel_rows_step, self.out, self.lse,
+                                     n_fetched=self.n_fetched, scores_out=self.scores,
+                                     pool_on_host=self.pool_on_host, workspace=self.ws_step)
+            else:
+                L.decode_step(q_t, self.q_ref, c.tau, c.mode, t, self.fire, self.r, k_t, v_t, self.k_local,
+                              self.v_local, c.seg_len, self.reps, self.unit_start, self.unit_size, c.n_clusters,
+                              self.k_pool, self.v_pool, c.prompt_len, c.budget, self.sel_units, self.n_sel_units,
+                              self.n_sel, self.sel_rows, self.out, self.lse, scores_out=self.scores,
+                              workspace=self.ws_step)
             self.t += 1
             return
         fused = self.fuse_prologue and c.trigger == "boundary" and self.seg_state is None

@@ -65,10 +65,16 @@ _SIGS = {
         _P, _P, _I64, _P, _P, _I32, _P, _P, _I32, _I32, _I32,
         _P, _I32, _P, _P, _SZ, _P]),
     "louiskv_decode_step_workspace_size": (_SZ, [_I64, _I32, _I32, _I32, _I32, _I32]),
+    "louiskv_decode_step_cached_workspace_size": (_SZ, [_I64, _I32, _I32, _I32, _I32, _I32]),
     "louiskv_decode_step": (ctypes.c_int, [
         _P, _P, _I32, _I64, _I32, _I32, _I32, _D, _I32, _I32, _P, _P,
         _P, _P, _P, _P, _I32, _I32, _P, _P, _P, _I32, _I32,
         _P, _P, _I64, _I32, _I32, _P, _P, _P, _P, _P, _P, _I32, _P, _P, _SZ, _P]),
+    "louiskv_decode_step_cached": (ctypes.c_int, [
+        _P, _P, _I32, _I64, _I32, _I32, _I32, _D, _I32, _I32, _P, _P,
+        _P, _P, _P, _P, _I32, _I32, _P, _P, _P, _I32, _I32,
+        _P, _P, _I64, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P,
+        _P, _P, _P, _P, _P, _P, _I32, _P, _P, _SZ, _P]),
     "louiskv_sparse_decode_attn_rows_noalloc": (ctypes.c_int, [
         _P, _I32, _I64, _I32, _I32, _I32, _F,
         _P, _P, _I64, _P, _P, _I32, _P, _P, _I32, _I32, _I32,
@@ -390,6 +396,37 @@ def decode_step(q, q_ref, tau: float, mode: int, step: int, fire, r_out, k_new, 
         _ptr(unit_size), reps.shape[1], n_clusters, _ptr(k_pool), _ptr(v_pool), k_pool.shape[1], prompt_len,
         budget, _ptr(sel_units), _ptr(n_sel_units), _ptr(n_sel), _ptr(sel_rows), _ptr(scores_out), _ptr(out),
         _dtype_code(out), _ptr(lse_out), _ptr(workspace), workspace.numel(), _stream(stream)))
+
+
+def decode_step_cached_workspace_size(n_slices: int, dtype_code: int, group_size: int, units_cap: int, budget: int,
+                                      window: int) -> int:
+    return int(load_library().louiskv_decode_step_cached_workspace_size(n_slices, dtype_code, group_size, units_cap,
+                                                                        budget, window))
+
+
+def decode_step_cached(q, q_ref, tau: float, mode: int, step: int, fire, r_out, k_new, v_new, k_local, v_local,
+                       seg_len: int, reps, unit_start, unit_size, n_clusters: int, k_pool, v_pool, prompt_len: int,
+                       budget: int, k_buf, v_buf, buf_row, slot_step, slot_list, sel_units, n_sel_units, n_sel,
+                       sel_rows, out, lse_out=None, n_fetched=None, scores_out=None, pool_on_host: bool = False,
+                       workspace=None, stream=None):
+    """One decode step with KV_critical kept as an LRU cache of k_buf.shape[1]
+    pool rows, in four launches.  workspace: zero-filled before its first use."""
+    g, hq, d = q.shape
+    s = k_new.shape[0]
+    h = s // g
+    window = k_local.shape[1]
+    dt = _dtype_code(q)
+    if workspace is None:
+        workspace = torch.zeros(decode_step_cached_workspace_size(s, dt, hq // h, reps.shape[1], budget, window),
+                                dtype=torch.uint8, device=q.device)
+    _check(load_library().louiskv_decode_step_cached(
+        _ptr(q), _ptr(q_ref), dt, g, hq, h, d, float(tau), mode, step, _ptr(r_out), _ptr(fire),
+        _ptr(k_new), _ptr(v_new), _ptr(k_local), _ptr(v_local), window, seg_len, _ptr(reps), _ptr(unit_start),
+        _ptr(unit_size), reps.shape[1], n_clusters, _ptr(k_pool), _ptr(v_pool), k_pool.shape[1], int(pool_on_host),
+        prompt_len, budget, k_buf.shape[1], _ptr(k_buf), _ptr(v_buf), _ptr(buf_row), _ptr(slot_step),
+        _ptr(slot_list), _ptr(n_fetched), _ptr(sel_units), _ptr(n_sel_units), _ptr(n_sel), _ptr(sel_rows),
+        _ptr(scores_out), _ptr(out), _dtype_code(out), _ptr(lse_out), _ptr(workspace), workspace.numel(),
+        _stream(stream)))
 
 
 NOALLOC_SCRATCH_BYTES = 8 << 20   # LOUISKV_NOALLOC_SCRATCH_BYTES

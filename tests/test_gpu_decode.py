@@ -926,7 +926,8 @@ def test_host_pool_flag_rejects_device_memory():
     assert torch.all(nsel == -5) and torch.all(kb == 7)
 
 
-@pytest.mark.parametrize("case", ["bf16-anchor", "bf16-prev", "fp32-anchor"])
+@pytest.mark.parametrize("case", ["bf16-anchor", "bf16-prev", "fp32-anchor", "bf16-anchor-hostcache",
+                                  "fp32-prev-hostcache"])
 def test_decode_step_equals_stage_calls(case):
     """louiskv_decode_step (boundary, store, retrieval and attention of a step
     in two launches, blocks of a slice handing over through the workspace)
@@ -935,9 +936,13 @@ def test_decode_step_equals_stage_calls(case):
     tables, window and pool equal bit for bit; the attention output and lse
     too in fp32 (same chunks, same merge arithmetic), within 1e-5 in bf16
     (the step splits each slice's rows into smaller chunks).  The arrival
-    counters in the workspace are zero after every step."""
+    counters in the workspace are zero after every step.  hostcache:
+    louiskv_decode_step_cached over a pinned host pool with an LRU cache of
+    four budgets against the stage calls with the same cache (buffer rows,
+    slot steps, slot lists, fetch counts and cached rows equal too)."""
     from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
-    dname, mname = case.split("-")
+    dname, mname = case.split("-")[:2]
+    cached = case.endswith("hostcache")
     mode = _L().REF_PREV if mname == "prev" else _L().REF_ANCHOR
     if dname == "bf16":
         wl = synth.get_workload("si-lo-16k").replace(prompt_len=2048, n_clusters=64, budget=512, name="si-lo-16k")
@@ -948,8 +953,10 @@ def test_decode_step_equals_stage_calls(case):
     data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(n_groups)], gen_len=steps)
     cfg = config_from_workload(wl, n_groups=n_groups, mode=mode, gen_len=steps)
     dt = data.prompt_keys.dtype
-    a = LouisKVEngine(cfg, dt, DEV, out_dtype=torch.float32, keep_scores=True, fused_step=False)
-    b = LouisKVEngine(cfg, dt, DEV, out_dtype=torch.float32, keep_scores=True, fused_step=True)
+    kw = dict(pool_on_host=True, cache_rows=4 * wl.budget) if cached else {}
+    a = LouisKVEngine(cfg, dt, DEV, out_dtype=torch.float32, keep_scores=True, fused_step=False, **kw)
+    b = LouisKVEngine(cfg, dt, DEV, out_dtype=torch.float32, keep_scores=True, fused_step=True, **kw)
+    assert b._use_fused_step() and (b._fused_cached == cached)
     for e in (a, b):
         e.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
     S = cfg.n_slices
@@ -968,7 +975,18 @@ def test_decode_step_equals_stage_calls(case):
         assert torch.equal(a.v_pool[:, :written], b.v_pool[:, :written]), t
         for i in range(S):
             assert torch.equal(a.sel_units[i, :int(a.n_sel_units[i])], b.sel_units[i, :int(b.n_sel_units[i])]), (t, i)
-            assert torch.equal(a.sel_rows[i, :int(a.n_sel[i])], b.sel_rows[i, :int(b.n_sel[i])]), (t, i)
+            if cached:
+                n = int(b.n_sel[i])
+                assert torch.equal(a.slot_list[i, :n], b.slot_list[i, :n]), (t, i)
+                sl = b.slot_list[i, :n].long()
+                assert torch.equal(a.k_buf[i, sl], b.k_buf[i, sl]) and torch.equal(a.v_buf[i, sl], b.v_buf[i, sl])
+            else:
+                assert torch.equal(a.sel_rows[i, :int(a.n_sel[i])], b.sel_rows[i, :int(b.n_sel[i])]), (t, i)
+        if cached:
+            for name in ("buf_row", "slot_step"):
+                assert torch.equal(getattr(a, name), getattr(b, name)), (t, name)
+            fired = a.fire.repeat_interleave(cfg.n_kv_heads).bool()
+            assert torch.equal(torch.where(fired, a.n_fetched, 0), torch.where(fired, b.n_fetched, 0)), t
         if dname == "fp32":
             assert torch.equal(a.out, b.out) and torch.equal(a.lse, b.lse), t
         else:
@@ -1001,8 +1019,9 @@ def test_layer_by_layer_step_graphs_match_eager(case):
     data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(G)], gen_len=steps)
     cfg = config_from_workload(wl, n_groups=G, gen_len=steps)
     eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, pool_on_host=host, out_dtype=torch.float32)
-    if not host:
-        assert eng.group_view(0)._use_fused_step()
+    # each view runs the fused step: two launches over a device pool, four
+    # with the LRU cache over the host pool
+    assert eng.group_view(0)._use_fused_step() and eng.group_view(0)._fused_cached == host
     hist = torch.zeros(steps, *eng.out.shape, device=DEV)
     hist_n = torch.zeros(steps, *eng.n_sel.shape, dtype=torch.int32, device=DEV)
 
@@ -1035,8 +1054,7 @@ def test_layer_by_layer_step_graphs_match_eager(case):
         print(f"step-graph replay {rep} ({case})", flush=True)
         assert torch.equal(hist, ref), (case, rep)
         assert torch.equal(hist_n, ref_n), (case, rep)
-        if not host:
-            assert int(eng.ws_step[:8 * cfg.n_slices].view(torch.int32).abs().sum()) == 0
+        assert int(eng.ws_step[:8 * cfg.n_slices].view(torch.int32).abs().sum()) == 0
     del graphs
 
 
