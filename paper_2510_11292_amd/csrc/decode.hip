@@ -1693,7 +1693,7 @@ __device__ __forceinline__ void update_q_ref(const StepSync& sync, const T* __re
 // merging block first stages every chunk's (m, l) in LDS (s_ml, n_chunks * G
 // pairs), then each thread takes one head and two dims and reads their
 // accumulators kMergeBatch chunks at a time, all loads of a batch in flight.
-constexpr int kMergeBatch = 16;
+constexpr int kMergeBatch = 32;
 
 template <int G>
 __device__ __forceinline__ void attn_last_block_merge(const float* __restrict__ part, int32_t* __restrict__ counter,
