@@ -127,6 +127,18 @@ int main(void) {
          louiskv_retrieve_delta(p, LOUISKV_BF16, 8, 8, 4, 128, 0.088, fp, ip, ip, 64, 64, NULL, 128, p, p, 4096, 0,
                                 256, up, ip, ip, ip, NULL, NULL, ip, ip, ip, dp, p, sizeof(buf), NULL),
          LOUISKV_ERR_NULL);
+  expect("retrieve_cached NULL slot_step",
+         louiskv_retrieve_cached(p, LOUISKV_BF16, 8, 8, 4, 128, 0.088, fp, ip, ip, 64, 64, NULL, 128, p, p, 4096, 0,
+                                 256, 1024, 5, up, ip, ip, ip, p, p, ip, NULL, ip, ip, dp, p, sizeof(buf), NULL),
+         LOUISKV_ERR_NULL);
+  expect("retrieve_cached cache below the budget",
+         louiskv_retrieve_cached(p, LOUISKV_BF16, 8, 8, 4, 128, 0.088, fp, ip, ip, 64, 64, NULL, 128, p, p, 4096, 0,
+                                 256, 128, 5, up, ip, ip, ip, p, p, ip, ip, ip, ip, dp, p, sizeof(buf), NULL),
+         LOUISKV_ERR_SHAPE);
+  expect("retrieve_cached cache beyond the plan's register runs",
+         louiskv_retrieve_cached(p, LOUISKV_BF16, 8, 8, 4, 128, 0.088, fp, ip, ip, 64, 64, NULL, 128, p, p, 4096, 0,
+                                 256, 70000, 5, up, ip, ip, ip, p, p, ip, ip, ip, ip, dp, p, sizeof(buf), NULL),
+         LOUISKV_ERR_UNSUPPORTED);
 
   /* attention */
   expect("attn_rows group size",
@@ -164,6 +176,28 @@ int main(void) {
          louiskv_decode_step(p, p, LOUISKV_BF16, 1, 32, 8, 128, 0.9, LOUISKV_REF_ANCHOR, 5, dp, up, p, p, p, p, 128,
                              32, fp, ip, ip, 1024, 1024, p, p, 34000, 32768, 2048, ip, ip, ip, ip, dp, p,
                              LOUISKV_F32, fp, p, 64, NULL), LOUISKV_ERR_WORKSPACE);
+
+  /* the decode step with the LRU cache of pool rows */
+  if (louiskv_decode_step_cached_workspace_size(8, LOUISKV_BF16, 4, 1024, 0, 128) != 0 ||
+      louiskv_decode_step_cached_workspace_size(8, LOUISKV_BF16, 4, 1024, 2048, 128) == 0) {
+    printf("FAIL decode_step_cached_workspace_size\n");
+    ++failures;
+  }
+  expect("decode_step_cached NULL k_buf",
+         louiskv_decode_step_cached(p, p, LOUISKV_BF16, 1, 32, 8, 128, 0.9, LOUISKV_REF_ANCHOR, 5, dp, up, p, p, p,
+                                    p, 128, 32, fp, ip, ip, 1024, 1024, p, p, 34000, 0, 32768, 2048, 4096, NULL, p,
+                                    ip, ip, ip, ip, ip, ip, ip, ip, dp, p, LOUISKV_F32, fp, p, sizeof(buf), NULL),
+         LOUISKV_ERR_NULL);
+  expect("decode_step_cached cache below the budget",
+         louiskv_decode_step_cached(p, p, LOUISKV_BF16, 1, 32, 8, 128, 0.9, LOUISKV_REF_ANCHOR, 5, dp, up, p, p, p,
+                                    p, 128, 32, fp, ip, ip, 1024, 1024, p, p, 34000, 0, 32768, 2048, 1024, p, p,
+                                    ip, ip, ip, ip, ip, ip, ip, ip, dp, p, LOUISKV_F32, fp, p, sizeof(buf), NULL),
+         LOUISKV_ERR_SHAPE);
+  expect("decode_step_cached pool beyond the plan's bitmap",
+         louiskv_decode_step_cached(p, p, LOUISKV_BF16, 1, 32, 8, 128, 0.9, LOUISKV_REF_ANCHOR, 5, dp, up, p, p, p,
+                                    p, 128, 32, fp, ip, ip, 1024, 1024, p, p, 600000, 0, 32768, 2048, 4096, p, p,
+                                    ip, ip, ip, ip, ip, ip, ip, ip, dp, p, LOUISKV_F32, fp, p, sizeof(buf), NULL),
+         LOUISKV_ERR_UNSUPPORTED);
 
   printf("%d failed checks\n", failures);
   return failures;
