@@ -1347,14 +1347,17 @@ void cache_plan_kernel(const int32_t* __restrict__ row_ws, const int32_t* __rest
     if (r >= 0 && r < pool_rows) atomicOr(&s_bits[r >> 5], 1u << (r & 31));
   }
   __syncthreads();
-  // hits: slots whose row is selected again (test and clear its bit)
+  // hits: slots whose row is selected again (test and clear its bit); the
+  // thread's own run only, read in pieces of up to 16 slots
+  constexpr int kPiece = R < 16 ? R : 16;
+  static_assert(R % kPiece == 0, "a run splits into whole pieces");
   uint64_t hit = 0;
 #pragma unroll
-  for (int j0 = 0; j0 < R; j0 += 16) {
-    int row[16];
-    load_run<16>(brow, i0 + j0, cache_rows, -1, row);
+  for (int j0 = 0; j0 < R; j0 += kPiece) {
+    int row[kPiece];
+    load_run<kPiece>(brow, i0 + j0, cache_rows, -1, row);
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
+    for (int j = 0; j < kPiece; ++j) {
       const int r = row[j];
       if (r >= 0 && r < pool_rows) {
         const uint32_t bit = 1u << (r & 31);

@@ -686,6 +686,15 @@ def test_decode_loop_layer_by_layer_boundary_delta():
     assert st["fires"] > 30 and st["evictions"] > 10 and 0 < st["fetched"] < st["selected"]
 
 
+def test_decode_loop_layer_by_layer_device_lru_cache():
+    """Group-by-group steps over a device pool with KV_critical as an LRU
+    cache of three budgets (each view runs the four-launch cached decode
+    step): oracle parity and the LRU policy at every step."""
+    wl = synth.get_workload("si-lo-16k").replace(prompt_len=2048, n_clusters=64, budget=512, name="si-lo-16k")
+    st = _run_loop(wl, 2, 200, mode=1, zero_copy=False, delta=True, layer_by_layer=True, cache_rows=3 * 512)
+    assert st["fires"] > 30 and 0 < st["fetched"] < st["selected"]
+
+
 def test_decode_loop_layer_by_layer_host_pool():
     """Group-by-group steps with the pool in pinned host memory (delta
     transfers): each group's calls take pointers into the middle of the pool."""
@@ -927,7 +936,7 @@ def test_host_pool_flag_rejects_device_memory():
 
 
 @pytest.mark.parametrize("case", ["bf16-anchor", "bf16-prev", "fp32-anchor", "bf16-anchor-hostcache",
-                                  "fp32-prev-hostcache"])
+                                  "fp32-prev-hostcache", "bf16-anchor-g8", "bf16-prev-g1-hostcache"])
 def test_decode_step_equals_stage_calls(case):
     """louiskv_decode_step (boundary, store, retrieval and attention of a step
     in two launches, blocks of a slice handing over through the workspace)
@@ -943,6 +952,7 @@ def test_decode_step_equals_stage_calls(case):
     from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
     dname, mname = case.split("-")[:2]
     cached = case.endswith("hostcache")
+    gsize = next((int(p[1:]) for p in case.split("-") if p[0] == "g" and p[1:].isdigit()), None)
     mode = _L().REF_PREV if mname == "prev" else _L().REF_ANCHOR
     if dname == "bf16":
         wl = synth.get_workload("si-lo-16k").replace(prompt_len=2048, n_clusters=64, budget=512, name="si-lo-16k")
@@ -950,6 +960,8 @@ def test_decode_step_equals_stage_calls(case):
     else:
         wl = synth.get_workload("tiny-4k")
         n_groups, steps = 1, 256
+    if gsize is not None:   # other query-group sizes: 8 KV heads, g query heads each
+        wl = wl.replace(n_q_heads=wl.n_kv_heads * gsize)
     data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(n_groups)], gen_len=steps)
     cfg = config_from_workload(wl, n_groups=n_groups, mode=mode, gen_len=steps)
     dt = data.prompt_keys.dtype
