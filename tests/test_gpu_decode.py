@@ -611,6 +611,17 @@ def test_decode_loop_host_pool_lru_cache(segments, prompt, budget, cache):
     assert st["fetched"] < base["fetched"]
 
 
+@pytest.mark.parametrize("cache", [10240, 16896])
+def test_decode_loop_host_pool_lru_cache_evicting(cache):
+    """The LRU cache smaller than the pool, at the sizes that take the plan's
+    16- and 32-slot register runs (20 K-token prompt indexed by 16-token
+    pages, 2048-token budget): slots, steps and fetch counts follow the
+    policy at every step while rows are evicted, with oracle parity."""
+    wl = synth.get_workload("host-131k").replace(prompt_len=20480, n_clusters=1280, budget=2048, name="host-131k")
+    st = _run_loop(wl, 1, 120, mode=1, pool_on_host=True, cache_rows=cache, index="pages", page_len=16)
+    assert st["fires"] > 15 and 0 < st["fetched"] < st["selected"]
+
+
 def test_decode_loop_delta_device_pool():
     """Delta transfers over a pool in device memory (bf16 reduction with
     evictions, two groups)."""
