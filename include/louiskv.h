@@ -429,8 +429,8 @@ int louiskv_sparse_decode_attn_rows(const void* q, int32_t dtype, int64_t n_slic
 
 /*
  * One decode step of Algorithm 1 for n_groups (sequence, layer) groups, with
- * fixed output segments and the KV pool in device memory, in two launches:
- * the boundary test (Section 4.1 equation for r_t), the decode-stage
+ * fixed output segments and the KV pool in device memory, in one launch for
+ * bf16 and two for float32: the boundary test (Section 4.1 equation for r_t), the decode-stage
  * store_cache (Section 4.2: window append, oldest-segment eviction), the
  * group-consistent retrieval of the groups that fired (Appendix B scores,
  * Section 3.1 budget, Algorithm 1 Retrieve; KV_critical kept as the list of
@@ -439,7 +439,10 @@ int louiskv_sparse_decode_attn_rows(const void* q, int32_t dtype, int64_t n_slic
  * layer of a model at a time): every kernel spreads a slice over many
  * blocks, and the blocks of a slice hand over through the workspace (the
  * last one to finish a phase completes it) instead of through extra
- * launches.
+ * launches.  In the one-launch form each block of a slice scores a part of
+ * the units and attends a chunk of the rows; when the group fires, blocks
+ * wait (bounded) for the slice's last scoring block to publish the
+ * selection.
  *
  * Results equal, bit for bit, louiskv_decode_prologue + louiskv_retrieve_rows
  * + louiskv_sparse_decode_attn_rows (the selected units, rows, scores, r,
@@ -460,8 +463,13 @@ int louiskv_sparse_decode_attn_rows(const void* q, int32_t dtype, int64_t n_slic
  *
  * workspace  louiskv_decode_step_workspace_size() bytes.  It must be zero
  *            before its first use (for example allocated zeroed); every call
- *            leaves its arrival counters at zero again, so it is reused
- *            without clearing.  Calls that share it must not overlap.
+ *            leaves its arrival counters and flags at zero again, so it is
+ *            reused without clearing.  Calls that share it must not overlap.
+ *            Its first (4 * n_slices + 1) * 64 int32 words are those
+ *            counters and flags; the last of them is a status word that a
+ *            block sets to 1 if its wait for a selection ever gave up (after
+ *            about a million polls, which a correct launch never reaches),
+ *            and that the library never clears.
  */
 size_t louiskv_decode_step_workspace_size(int64_t n_slices, int32_t dtype, int32_t group_size,
                                           int32_t units_cap, int32_t budget, int32_t window);

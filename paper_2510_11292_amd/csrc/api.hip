@@ -47,7 +47,20 @@ namespace {
 std::mutex g_lds_mu;
 std::unordered_map<const void*, size_t> g_static_lds;   // per kernel
 int g_max_lds[64] = {};                                  // per device
+int g_cus[64] = {};                                      // per device
 }  // namespace
+
+int device_cu_count() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  std::lock_guard<std::mutex> lock(g_lds_mu);
+  if (!g_cus[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    g_cus[dev] = n;
+  }
+  return g_cus[dev];
+}
 
 int check_lds(const void* kernel, size_t dynamic_lds) {
   int dev = 0;

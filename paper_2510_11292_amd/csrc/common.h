@@ -38,6 +38,10 @@ int device_view_of_host_pool(const void* p, void** dev);
 // else LOUISKV_ERR_UNSUPPORTED: such a launch is refused, never attempted.
 int check_lds(const void* kernel, size_t dynamic_lds);
 
+// Compute units of the current device (looked up once per device), or 0 if
+// the runtime cannot tell.
+int device_cu_count();
+
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // Carves aligned sub-buffers out of a caller-owned workspace.

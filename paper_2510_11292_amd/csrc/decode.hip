@@ -390,6 +390,8 @@ __device__ __forceinline__ void bitonic_in_wave2(uint64_t& v0, uint64_t& v1, int
 constexpr int kLogitThreads = 256;
 constexpr int kLogitWaves = kLogitThreads / 64;
 constexpr int kMaxLogitParts = 16;
+// Parts of a fused decode step's selection: up to one per block of a slice.
+constexpr int kMaxSelectParts = 32;
 
 // Logit workspace per call: the logits [S][units_cap][kMaxGroupSize].
 size_t logit_ws_doubles(int64_t S, int units_cap) { return (size_t)S * units_cap * kMaxGroupSize; }
@@ -552,7 +554,9 @@ __device__ __forceinline__ double load_logit(const double* p) {
 //  pool-row list.  kShared: the logits come from other blocks of the launch;
 //  they are read coherently and the exponentials are recomputed in pass 3
 //  instead of written back (the results are the same, bit for bit).
-template <int G, bool kShared>
+//  kPublish: the row list and its length are read by other blocks of the
+//  launch, so they are written with device-scope stores.
+template <int G, bool kShared, bool kPublish = false>
 __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const double* s_m, int n_units, int n_pad,
                                                  int64_t s, int64_t ps, int units_cap, int budget,
                                                  const int32_t* __restrict__ unit_start,
@@ -886,11 +890,19 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
     const int sz = (int)(uint32_t)e;
     const int st0 = (int)(uint32_t)(e >> 32);
     const int ex = s_incl[p] - sz;
-    for (int i = lane; i < sz; i += kWave) rows[ex + i] = st0 + i;
+    for (int i = lane; i < sz; i += kWave) {
+      if constexpr (kPublish)
+        __hip_atomic_store(rows + ex + i, st0 + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      else
+        rows[ex + i] = st0 + i;
+    }
   }
   if (tid == 0) {
     n_sel_units[s] = ntake;
-    n_sel[s] = nsel;
+    if constexpr (kPublish)
+      __hip_atomic_store(n_sel + s, nsel, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else
+      n_sel[s] = nsel;
   }
 }
 
@@ -993,45 +1005,33 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
 //    slice to arrive resets the counter and makes the selection from all the
 //    parts (select_after_max), as score_select_kernel does.
 // The reference query is left for the attention launch to update.
-template <class T, int G>
-__global__ __launch_bounds__(kSelThreads)
-void step_select_kernel(const T* __restrict__ q, const T* __restrict__ q_ref, int n_kv_heads, double tau, int first,
-                        double* __restrict__ r_out, uint8_t* __restrict__ fire_out, const T* __restrict__ k_new,
-                        const T* __restrict__ v_new, T* __restrict__ k_local, T* __restrict__ v_local, int window,
-                        int step, int seg_len, int evict_seg, float* __restrict__ reps,
-                        int32_t* __restrict__ unit_start, int32_t* __restrict__ unit_size, int units_cap,
-                        int n_clusters, T* __restrict__ k_pool, T* __restrict__ v_pool, int64_t pool_rows,
-                        int prompt_len, double scale, int n_units, int budget, int32_t* __restrict__ sel_units,
-                        int32_t* __restrict__ n_sel_units, int32_t* __restrict__ n_sel,
-                        int32_t* __restrict__ sel_rows, double* __restrict__ scores_out,
-                        double* __restrict__ logit_ws, double* __restrict__ part_max, int32_t* __restrict__ counter,
-                        int n_parts, int n_pad) {
-  extern __shared__ __align__(16) char smem[];
+// A fired slice's part `part` of the selection work in a decode step: the
+// logits of the part's units and their per-head maxima, written with
+// device-scope stores; the part then counts itself in at the slice's
+// counter (`counter`), and the last part to arrive resets it, loads every part's maxima
+// and the unit sizes and makes the selection (select_after_max, the same
+// code as the per-stage kernel, so scores and selections are equal bit for
+// bit).  Returns true in the block that made the selection.
+template <class T, int G, bool kPublish>
+__device__ __forceinline__ bool select_part(const T* __restrict__ q, int n_kv_heads, int64_t s, int part, int n_parts,
+                                            double scale, const float* __restrict__ reps, int units_cap, int n_units,
+                                            int n_pad, int budget, const int32_t* __restrict__ unit_start,
+                                            const int32_t* __restrict__ unit_size, int32_t* __restrict__ sel_units,
+                                            int32_t* __restrict__ n_sel_units, int32_t* __restrict__ n_sel,
+                                            int32_t* __restrict__ sel_rows, double* __restrict__ scores_out,
+                                            double* __restrict__ logit_ws, double* __restrict__ part_max,
+                                            int32_t* __restrict__ counter, char* smem) {
   uint64_t* s_key = reinterpret_cast<uint64_t*>(smem);            // [n_pad]
   int* s_size = reinterpret_cast<int*>(s_key + n_pad);            // [n_pad] unit sizes by unit id
   int* s_incl = s_size + n_pad;                                    // [n_pad] inclusive size sums by rank
-  __shared__ double s_bpart[16];
   __shared__ double s_rm[G][kSelWaves];
   __shared__ double s_m[G];
   __shared__ int s_last;
-  const int64_t s = blockIdx.x / n_parts;
-  const int part = (int)(blockIdx.x - s * n_parts);
   const int64_t grp = s / n_kv_heads;
   const int kvh = (int)(s - grp * n_kv_heads);
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n_q_heads = n_kv_heads * G;
-
-  const double r = boundary_r(q, q_ref, n_q_heads, first, grp, s_bpart);
-  const bool fire = first || r < tau;
-  if (part == 0 && kvh == 0 && tid == 0) {
-    if (r_out) r_out[grp] = r;
-    fire_out[grp] = (uint8_t)(fire ? 1 : 0);
-  }
-  if (part == 0 && w == 0)
-    store_slice(k_new, v_new, k_local, v_local, window, step, seg_len, evict_seg, reps, unit_start, unit_size,
-                units_cap, n_clusters, k_pool, v_pool, pool_rows, prompt_len, s, lane);
-  if (!fire) return;
 
   // logits of this part's units and their maxima
   const int per = (n_units + n_parts - 1) / n_parts;
@@ -1063,14 +1063,14 @@ void step_select_kernel(const T* __restrict__ q, const T* __restrict__ q_ref, in
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (tid == 0) {
-    const int old = __hip_atomic_fetch_add(counter + s, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int old = __hip_atomic_fetch_add(counter, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     s_last = old == n_parts - 1;
-    if (s_last) __hip_atomic_store(counter + s, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (s_last) __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   __syncthreads();
-  if (!s_last) return;
+  if (!s_last) return false;
   // the parts' maxima (one coherent load per thread, all in flight) and the unit sizes
-  __shared__ double s_pmax[kMaxLogitParts * kMaxGroupSize];
+  __shared__ double s_pmax[kMaxSelectParts * kMaxGroupSize];
   if (tid < n_parts * G)
     s_pmax[tid] = __hip_atomic_load(part_max + (size_t)s * n_parts * G + tid, __ATOMIC_RELAXED,
                                     __HIP_MEMORY_SCOPE_AGENT);
@@ -1083,8 +1083,51 @@ void step_select_kernel(const T* __restrict__ q, const T* __restrict__ q_ref, in
     s_m[tid] = m;
   }
   __syncthreads();
-  select_after_max<G, true>(lg, s_m, n_units, n_pad, s, s, units_cap, budget, unit_start, sel_units, n_sel_units,
-                            n_sel, sel_rows, scores_out, s_key, s_size, s_incl);
+  select_after_max<G, true, kPublish>(lg, s_m, n_units, n_pad, s, s, units_cap, budget, unit_start, sel_units,
+                                      n_sel_units, n_sel, sel_rows, scores_out, s_key, s_size, s_incl);
+  return true;
+}
+
+// The first launch of a two-launch decode step: one 512-thread block per
+// (slice, part of its units).  Every block computes its group's r (the same
+// float64 value in every block), block 0 of a slice runs the fixed-segment
+// store, and if the group fired each block does its part of the selection
+// (select_part).
+template <class T, int G>
+__global__ __launch_bounds__(kSelThreads)
+void step_select_kernel(const T* __restrict__ q, const T* __restrict__ q_ref, int n_kv_heads, double tau, int first,
+                        double* __restrict__ r_out, uint8_t* __restrict__ fire_out, const T* __restrict__ k_new,
+                        const T* __restrict__ v_new, T* __restrict__ k_local, T* __restrict__ v_local, int window,
+                        int step, int seg_len, int evict_seg, float* __restrict__ reps,
+                        int32_t* __restrict__ unit_start, int32_t* __restrict__ unit_size, int units_cap,
+                        int n_clusters, T* __restrict__ k_pool, T* __restrict__ v_pool, int64_t pool_rows,
+                        int prompt_len, double scale, int n_units, int budget, int32_t* __restrict__ sel_units,
+                        int32_t* __restrict__ n_sel_units, int32_t* __restrict__ n_sel,
+                        int32_t* __restrict__ sel_rows, double* __restrict__ scores_out,
+                        double* __restrict__ logit_ws, double* __restrict__ part_max, int32_t* __restrict__ counter,
+                        int n_parts, int n_pad) {
+  extern __shared__ __align__(16) char smem[];
+  __shared__ double s_bpart[16];
+  const int64_t s = blockIdx.x / n_parts;
+  const int part = (int)(blockIdx.x - s * n_parts);
+  const int64_t grp = s / n_kv_heads;
+  const int kvh = (int)(s - grp * n_kv_heads);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  const double r = boundary_r(q, q_ref, n_kv_heads * G, first, grp, s_bpart);
+  const bool fire = first || r < tau;
+  if (part == 0 && kvh == 0 && tid == 0) {
+    if (r_out) r_out[grp] = r;
+    fire_out[grp] = (uint8_t)(fire ? 1 : 0);
+  }
+  if (part == 0 && w == 0)
+    store_slice(k_new, v_new, k_local, v_local, window, step, seg_len, evict_seg, reps, unit_start, unit_size,
+                units_cap, n_clusters, k_pool, v_pool, pool_rows, prompt_len, s, lane);
+  if (!fire) return;
+  select_part<T, G, false>(q, n_kv_heads, s, part, n_parts, scale, reps, units_cap, n_units, n_pad, budget,
+                           unit_start, unit_size, sel_units, n_sel_units, n_sel, sel_rows, scores_out, logit_ws,
+                           part_max, counter + s, smem);
 }
 
 // Copy selected pool rows into KV_critical: 16 lanes per row, 16 rows per pass.
@@ -1698,8 +1741,8 @@ __device__ __forceinline__ void update_q_ref(const StepSync& sync, const T* __re
 // accumulators kMergeBatch chunks at a time, all loads of a batch in flight.
 constexpr int kMergeBatch = 32;
 
-template <int G>
-__device__ __forceinline__ void attn_last_block_merge(const float* __restrict__ part, int32_t* __restrict__ counter,
+template <int G, bool kOneTrip = false>
+__device__ __forceinline__ bool attn_last_block_merge(const float* __restrict__ part, int32_t* __restrict__ counter,
                                                       int64_t s, int n_chunks, void* __restrict__ out, int out_bf16,
                                                       float* __restrict__ lse_out, int tid, int n_threads,
                                                       float2* s_ml) {
@@ -1707,14 +1750,62 @@ __device__ __forceinline__ void attn_last_block_merge(const float* __restrict__ 
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (tid == 0) {
-    const int old = __hip_atomic_fetch_add(counter + s, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int old = __hip_atomic_fetch_add(counter, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     s_last = old == n_chunks - 1;
-    if (s_last) __hip_atomic_store(counter + s, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (s_last) __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   __syncthreads();
-  if (!s_last) return;
+  if (!s_last) return false;
   constexpr size_t pstride = 2 + kHeadDim;
   const float* ps = part + (size_t)s * n_chunks * G * pstride;
+  if (kOneTrip && n_chunks <= kMergeBatch) {
+    // every chunk's (m, l) and accumulators of a thread's head and two dims
+    // loaded at once: one round trip, the same arithmetic as below
+    for (int i = tid; i < G * (kHeadDim / 2); i += n_threads) {
+      const int j = i / (kHeadDim / 2), lane = i % (kHeadDim / 2);
+      const uint64_t* pm = reinterpret_cast<const uint64_t*>(ps + (size_t)j * pstride);
+      const uint64_t* pa = reinterpret_cast<const uint64_t*>(ps + (size_t)j * pstride + 2) + lane;
+      uint64_t mlv[kMergeBatch], v[kMergeBatch];
+#pragma unroll
+      for (int c = 0; c < kMergeBatch; ++c) {
+        mlv[c] = c < n_chunks ? __hip_atomic_load(pm + (size_t)c * G * (pstride / 2), __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT)
+                              : 0;
+        v[c] = c < n_chunks ? __hip_atomic_load(pa + (size_t)c * G * (pstride / 2), __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT)
+                            : 0;
+      }
+      float mm = -__builtin_inff();
+#pragma unroll
+      for (int c = 0; c < kMergeBatch; ++c)
+        if (c < n_chunks) mm = fmaxf(mm, __uint_as_float((uint32_t)mlv[c]));
+      float ll = 0.f, a0 = 0.f, a1 = 0.f;
+      if (mm != -__builtin_inff()) {
+#pragma unroll
+        for (int c = 0; c < kMergeBatch; ++c) {
+          if (c < n_chunks) {
+            const float w = __builtin_amdgcn_exp2f(__uint_as_float((uint32_t)mlv[c]) - mm);
+            ll += __uint_as_float((uint32_t)(mlv[c] >> 32)) * w;
+            a0 += __uint_as_float((uint32_t)v[c]) * w;
+            a1 += __uint_as_float((uint32_t)(v[c] >> 32)) * w;
+          }
+        }
+      }
+      const float inv = ll > 0.f ? 1.f / ll : 0.f;
+      const size_t row = (size_t)s * G + j;
+      if (out_bf16) {
+        uint16_t* o = static_cast<uint16_t*>(out) + row * kHeadDim;
+        store_from_f32(o, 2 * lane, a0 * inv);
+        store_from_f32(o, 2 * lane + 1, a1 * inv);
+      } else {
+        float* o = static_cast<float*>(out) + row * kHeadDim;
+        store_from_f32(o, 2 * lane, a0 * inv);
+        store_from_f32(o, 2 * lane + 1, a1 * inv);
+      }
+      if (lse_out && lane == 0) lse_out[row] = ll > 0.f ? 0.6931471805599453f * (mm + log2f(ll)) : -__builtin_inff();
+    }
+    return true;
+  }
   for (int i = tid; i < n_chunks * G; i += n_threads) {
     const uint64_t v = __hip_atomic_load(reinterpret_cast<const uint64_t*>(ps + (size_t)i * pstride),
                                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1760,14 +1851,17 @@ __device__ __forceinline__ void attn_last_block_merge(const float* __restrict__ 
     }
     if (lse_out && lane == 0) lse_out[row] = ll > 0.f ? 0.6931471805599453f * (mm + log2f(ll)) : -__builtin_inff();
   }
+  return true;
 }
 
 // Merge NW wave states (base-2 maximum m and sum l per head, acc per head and
 // dim, all in LDS) into the block's result: the normalised output and lse when
 // the block covers the whole slice (n_chunks == 1), else the chunk partial
-// (m, l, acc[128]) per head for attn_combine_kernel.
-template <int G, int NW>
-__device__ __forceinline__ void attn_block_merge(const float (*s_m)[G], const float (*s_l)[G],
+// (m, l, acc[128]) per head for attn_combine_kernel, or, with `counter` (the
+// slice's arrival counter), for the in-kernel merge.  True when this block
+// wrote the slice's output (one chunk, or the last block of an in-kernel merge).
+template <int G, int NW, bool kOneTrip = false>
+__device__ __forceinline__ bool attn_block_merge(const float (*s_m)[G], const float (*s_l)[G],
                                                  const float (*s_acc)[G][kHeadDim], int tid, int64_t s, int chunk,
                                                  int n_chunks, float* __restrict__ part, void* __restrict__ out,
                                                  int out_bf16, float* __restrict__ lse_out,
@@ -1811,8 +1905,10 @@ __device__ __forceinline__ void attn_block_merge(const float (*s_m)[G], const fl
       }
     }
   }
-  if (counter && n_chunks > 1)
-    attn_last_block_merge<G>(part, counter, s, n_chunks, out, out_bf16, lse_out, tid, NW * 64, s_ml);
+  if (n_chunks == 1) return true;
+  if (counter)
+    return attn_last_block_merge<G, kOneTrip>(part, counter, s, n_chunks, out, out_bf16, lse_out, tid, NW * 64, s_ml);
+  return false;
 }
 
 // With boundary-delimited segments the window of slice s holds the tokens
@@ -1984,7 +2080,7 @@ void attn_partial_kernel(const T* __restrict__ q, int n_kv_heads, float scale, c
   }
   __syncthreads();
   attn_block_merge<G, kAttnWaves>(s_m, s_l, s_acc, tid, s, chunk, n_chunks, part, out, out_bf16, lse_out,
-                                  sync.counter, reinterpret_cast<float2*>(s_rows));
+                                  sync.counter ? sync.counter + s : nullptr, reinterpret_cast<float2*>(s_rows));
 }
 
 // ---- bf16: scores on the matrix cores
@@ -2003,6 +2099,121 @@ __device__ __forceinline__ float row16_max(float x) {
 template <int G>
 constexpr int attn_mfma_waves() {
   return G == 8 ? 8 : 16;
+}
+
+// The A operand of the score MFMAs from the slice's G query rows (qs): row
+// m = l%16 of op mi holds head 4*mi + m % min(G, 4); k-chunk c covers dims
+// 32c..32c+31.
+template <int G, int NM = (G == 8 ? 2 : 1)>
+__device__ __forceinline__ void load_attn_q(const uint16_t* __restrict__ qs, int lane, attn_bf16x8 (&qa)[NM][4]) {
+  constexpr int GA = G < 4 ? G : 4;
+  const int g = lane >> 4, p16 = lane & 15;
+#pragma unroll
+  for (int mi = 0; mi < NM; ++mi)
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      qa[mi][c] = __builtin_bit_cast(
+          attn_bf16x8, *reinterpret_cast<const uint4*>(qs + (size_t)(4 * mi + p16 % GA) * kHeadDim + 32 * c + 8 * g));
+}
+
+// One 16-row tile of a wave: the scores of the tile's K rows (kx: lane l
+// holds row l%16) from v_mfma_f32_16x16x32_bf16, the base-2 online softmax
+// update of (m, l, acc) and P V with the tile's V rows (vx: rows 4k + l/16,
+// dims 8(l%16)..+7).  s_pw is the wave's LDS slot for the probabilities.
+template <int G, int NM = (G == 8 ? 2 : 1)>
+__device__ __forceinline__ void attn_mfma_tile(const attn_bf16x8 (&qa)[NM][4], const uint4 (&kx)[4],
+                                               const uint4 (&vx)[4], bool kvalid, float qscale, float (&m)[G],
+                                               float (&l)[G], float (&acc)[G][8], float4 (*s_pw)[64], int lane) {
+  const int g = lane >> 4;
+  __builtin_amdgcn_sched_barrier(0);   // keep the tile's loads ahead of their first use
+  attn_floatx4 sacc[NM];
+#pragma unroll
+  for (int mi = 0; mi < NM; ++mi) {
+    sacc[mi] = attn_floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      sacc[mi] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[mi][c], __builtin_bit_cast(attn_bf16x8, kx[c]), sacc[mi],
+                                                        0, 0, 0);
+  }
+  float sc[G];
+  bool grow = false;
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    const float x = sacc[j / 4][j % 4] * qscale;    // head j of row kr (regs i >= GA repeat heads)
+    sc[j] = kvalid ? x : -__builtin_inff();
+    grow |= sc[j] > m[j];
+  }
+  // rescale only when some row's score exceeds its head's running maximum
+  if (__builtin_amdgcn_ballot_w64(grow)) {
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      const float mn = fmaxf(m[j], row16_max(sc[j]));
+      const float corr = mn == -__builtin_inff() ? 1.f : __builtin_amdgcn_exp2f(m[j] - mn);
+      l[j] *= corr;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[j][e] *= corr;
+      m[j] = mn;
+    }
+  }
+  float pr[NM * 4];
+#pragma unroll
+  for (int j = 0; j < NM * 4; ++j) pr[j] = 0.f;
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    pr[j] = kvalid ? __builtin_amdgcn_exp2f(sc[j] - m[j]) : 0.f;
+    l[j] += pr[j];
+  }
+  // probabilities of row p16 to the lanes that hold its V row
+#pragma unroll
+  for (int mi = 0; mi < NM; ++mi)
+    s_pw[mi][lane] = make_float4(pr[4 * mi], pr[4 * mi + 1], pr[4 * mi + 2], pr[4 * mi + 3]);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    float pk[NM * 4];
+#pragma unroll
+    for (int mi = 0; mi < NM; ++mi) {
+      const float4 f = s_pw[mi][4 * k + g + 16 * g];
+      pk[4 * mi] = f.x; pk[4 * mi + 1] = f.y; pk[4 * mi + 2] = f.z; pk[4 * mi + 3] = f.w;
+    }
+    float vf[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t wv = (&vx[k].x)[i];
+      vf[2 * i] = __uint_as_float(wv << 16);
+      vf[2 * i + 1] = __uint_as_float(wv & 0xffff0000u);
+    }
+#pragma unroll
+    for (int j = 0; j < G; ++j)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[j][e] = fmaf(pk[j], vf[e], acc[j][e]);
+  }
+}
+
+// A wave's totals into its LDS slot: l over the 16 row positions, acc over
+// the 4 lane groups (m is wave-uniform).
+template <int G>
+__device__ __forceinline__ void attn_wave_to_lds(const float (&m)[G], float (&l)[G], float (&acc)[G][8], float* s_mw,
+                                                 float* s_lw, float (*s_accw)[kHeadDim], int lane) {
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    l[j] = row16_sum(l[j]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      acc[j][e] += __shfl_xor(acc[j][e], 16, kWave);
+      acc[j][e] += __shfl_xor(acc[j][e], 32, kWave);
+    }
+  }
+  if (lane < 16) {
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      if (lane == 0) {
+        s_mw[j] = m[j];
+        s_lw[j] = l[j];
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s_accw[j][8 * lane + e] = acc[j][e];
+    }
+  }
 }
 
 // Block (chunk, slice) for bf16 K/V.  A wave takes 16-row tiles t = w, w+NW, ...
@@ -2027,7 +2238,6 @@ void attn_mfma_kernel(const uint16_t* __restrict__ q, int n_kv_heads, float scal
                       StepSync sync) {
   extern __shared__ __align__(16) int s_rows[];   // kIdx: the chunk's entries of the row list
   constexpr int NM = G == 8 ? 2 : 1;        // matrix ops per k-chunk, 4 heads each
-  constexpr int GA = G < 4 ? G : 4;         // distinct heads in one op's output
   __shared__ float4 s_p[NW][NM][64];
   __shared__ float s_m[NW][G], s_l[NW][G];
   __shared__ float s_acc[NW][G][kHeadDim];
@@ -2048,15 +2258,8 @@ void attn_mfma_kernel(const uint16_t* __restrict__ q, int n_kv_heads, float scal
   const int r1 = (int)((int64_t)total * (chunk + 1) / n_chunks);
   const int n_tiles = (r1 - r0 + 15) / 16;   // block-uniform
 
-  // A operand: row m = l%16 holds head 4*mi + m % GA; k-chunk c covers dims 32c..32c+31
   attn_bf16x8 qa[NM][4];
-  const uint16_t* qs0 = q + ((size_t)grp * n_kv_heads + kvh) * G * kHeadDim;
-#pragma unroll
-  for (int mi = 0; mi < NM; ++mi)
-#pragma unroll
-    for (int c = 0; c < 4; ++c)
-      qa[mi][c] = __builtin_bit_cast(
-          attn_bf16x8, *reinterpret_cast<const uint4*>(qs0 + (size_t)(4 * mi + p16 % GA) * kHeadDim + 32 * c + 8 * g));
+  load_attn_q<G>(q + ((size_t)grp * n_kv_heads + kvh) * G * kHeadDim, lane, qa);
   const float qscale = scale * kLog2e;
   float m[G], l[G], acc[G][8];
 #pragma unroll
@@ -2099,93 +2302,264 @@ void attn_mfma_kernel(const uint16_t* __restrict__ q, int n_kv_heads, float scal
       const size_t voff = row_off(vr < r1 ? vr : r0, vloc);
       vx[k] = *reinterpret_cast<const uint4*>((vloc ? vl : vb) + voff + 8 * p16);
     }
-    __builtin_amdgcn_sched_barrier(0);   // keep the tile's loads ahead of their first use
-    attn_floatx4 sacc[NM];
-#pragma unroll
-    for (int mi = 0; mi < NM; ++mi) {
-      sacc[mi] = attn_floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int c = 0; c < 4; ++c)
-        sacc[mi] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[mi][c], __builtin_bit_cast(attn_bf16x8, kx[c]), sacc[mi],
-                                                          0, 0, 0);
-    }
-    float sc[G];
-    bool grow = false;
-#pragma unroll
-    for (int j = 0; j < G; ++j) {
-      const float x = sacc[j / 4][j % 4] * qscale;    // head j of row kr (regs i >= GA repeat heads)
-      sc[j] = kvalid ? x : -__builtin_inff();
-      grow |= sc[j] > m[j];
-    }
-    // rescale only when some row's score exceeds its head's running maximum
-    if (__builtin_amdgcn_ballot_w64(grow)) {
-#pragma unroll
-      for (int j = 0; j < G; ++j) {
-        const float mn = fmaxf(m[j], row16_max(sc[j]));
-        const float corr = mn == -__builtin_inff() ? 1.f : __builtin_amdgcn_exp2f(m[j] - mn);
-        l[j] *= corr;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[j][e] *= corr;
-        m[j] = mn;
-      }
-    }
-    float pr[NM * 4];
-#pragma unroll
-    for (int j = 0; j < NM * 4; ++j) pr[j] = 0.f;
-#pragma unroll
-    for (int j = 0; j < G; ++j) {
-      pr[j] = kvalid ? __builtin_amdgcn_exp2f(sc[j] - m[j]) : 0.f;
-      l[j] += pr[j];
-    }
-    // probabilities of row p16 to the lanes that hold its V row
-#pragma unroll
-    for (int mi = 0; mi < NM; ++mi)
-      s_p[w][mi][lane] = make_float4(pr[4 * mi], pr[4 * mi + 1], pr[4 * mi + 2], pr[4 * mi + 3]);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      float pk[NM * 4];
-#pragma unroll
-      for (int mi = 0; mi < NM; ++mi) {
-        const float4 f = s_p[w][mi][4 * k + g + 16 * g];
-        pk[4 * mi] = f.x; pk[4 * mi + 1] = f.y; pk[4 * mi + 2] = f.z; pk[4 * mi + 3] = f.w;
-      }
-      float vf[8];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint32_t wv = (&vx[k].x)[i];
-        vf[2 * i] = __uint_as_float(wv << 16);
-        vf[2 * i + 1] = __uint_as_float(wv & 0xffff0000u);
-      }
-#pragma unroll
-      for (int j = 0; j < G; ++j)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[j][e] = fmaf(pk[j], vf[e], acc[j][e]);
-    }
+    attn_mfma_tile<G>(qa, kx, vx, kvalid, qscale, m, l, acc, s_p[w], lane);
   }
-  // wave totals: l over the 16 row positions, acc over the 4 lane groups (m is wave-uniform)
+  attn_wave_to_lds<G>(m, l, acc, s_m[w], s_l[w], s_acc[w], lane);
+  __syncthreads();
+  attn_block_merge<G, NW>(s_m, s_l, s_acc, tid, s, chunk, n_chunks, part, out, out_bf16, lse_out,
+                          sync.counter ? sync.counter + s : nullptr, reinterpret_cast<float2*>(s_rows));
+}
+
+// ---------------------------------------------------------------------------
+// A bf16 decode step over few slices in one launch: n_blk blocks per slice,
+// every one of which does a part of the retrieval and a chunk of the
+// attention, so that a layer's few slices spread over the whole chip.
+//
+// Block c of slice s computes r (the same float64 value in every block of
+// the group) while it loads its chunk's entries of the row list of the last
+// fire, the list length and its Q operand; block 0 runs the fixed-segment
+// store.  If the group fired, the block computes the logits of its part of
+// the units and counts itself in (select_part): the last block to arrive
+// makes the selection, writes the row list with device-scope stores and
+// raises the slice's ready flag; the others wait for the flag and read the
+// new list entries coherently.  Only blocks that have arrived wait, and they
+// wait for the last arrival, which is running and waits for nothing, so the
+// wait ends whatever the scheduling (it is bounded all the same: past
+// kStepSpinLimit polls a block records a time-out in the status word and goes
+// on).  Then the block attends its chunk of the slice's row sequence (the
+// selected rows, padded to the budget, then the window rows), two 16-row
+// tiles per wave in flight; the newest window row is read from k_new/v_new,
+// since the store of the same launch may not have reached the ring yet.  The
+// last block of a slice to finish merges the chunk partials, and lowers the
+// ready flag after a fire.
+//
+// Every block counts itself in at its group's counter once it has read q_ref;
+// the last to arrive stores the new reference query (every step in PREV mode,
+// at a fire in ANCHOR mode) and resets the counter, so that counters and flags
+// are zero between calls.
+constexpr int kStepSpinLimit = 1 << 20;
+// Counters and flags of the fused step sit kStepSyncStride ints apart, each
+// in a 256-byte block of its own: atomics on one line serialise.
+constexpr int kStepSyncStride = 64;
+// Blocks per slice: at most the one-trip merge's chunk count.
+constexpr int kStepMaxBlocks = kMergeBatch;
+static_assert(kStepMaxBlocks <= kMaxSelectParts, "a selection part per block");
+// List entries a thread loads before it knows whether the group fired.
+constexpr int kStepListEarly = 2;
+
+struct FusedStep {
+  const uint16_t* q;
+  uint16_t* q_ref;
+  int64_t n_slices;
+  int n_kv_heads, first, mode;
+  double tau;
+  double* r_out;
+  uint8_t* fire_out;
+  const uint16_t *k_new, *v_new;
+  uint16_t *k_local, *v_local;
+  int window, step, seg_len, evict_seg;
+  float* reps;
+  int32_t *unit_start, *unit_size;
+  int units_cap, n_clusters;
+  uint16_t *k_pool, *v_pool;
+  int64_t pool_rows;
+  int prompt_len;
+  double scale;
+  int n_units, budget;
+  int32_t *sel_units, *n_sel_units, *n_sel, *sel_rows;
+  double* scores_out;
+  double *logit_ws, *part_max;
+  int32_t *sel_counter, *attn_counter, *ready, *grp_counter, *status;
+  int n_blk, chunk_rows, n_pad;
+  int local_start, n_local;
+  float* part;
+  void* out;
+  int out_bf16;
+  float* lse_out;
+};
+
+// LDS of the attention part of the fused step: wave probability slots,
+// per-wave (m, l, acc), the merge's (m, l) pairs and the chunk's list entries.
+template <int G>
+constexpr size_t fused_attn_lds(int n_blk, int chunk_rows) {
+  constexpr int NM = G == 8 ? 2 : 1;
+  return (size_t)kSelWaves * NM * 64 * sizeof(float4) + (size_t)2 * kSelWaves * G * sizeof(float) +
+         (size_t)kSelWaves * G * kHeadDim * sizeof(float) + (size_t)n_blk * G * sizeof(float2) +
+         (size_t)chunk_rows * sizeof(int);
+}
+
+template <int G>
+__global__ __launch_bounds__(kSelThreads)
+void step_fused_kernel(const FusedStep a) {
+  constexpr int NW = kSelWaves;
+  constexpr int NM = G == 8 ? 2 : 1;
+  extern __shared__ __align__(16) char smem[];
+  __shared__ double s_bpart[16];
+  __shared__ int s_grp_last;
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, p16 = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int nb = a.n_blk;
+  const int64_t s = blockIdx.x / nb;
+  const int c = (int)(blockIdx.x - s * nb);
+  const int64_t grp = s / a.n_kv_heads;
+  const int kvh = (int)(s - grp * a.n_kv_heads);
+  const int n_q_heads = a.n_kv_heads * G;
+  // the chunk: positions [p0, p1) of the slice's row sequence, the selected
+  // ones [p0, sel_hi)
+  const int p0 = c * a.chunk_rows;
+  const int p1 = max(p0, min(p0 + a.chunk_rows, a.budget + a.n_local));
+  const int sel_hi = max(p0, min(p1, a.budget));
+  const int32_t* rl = a.sel_rows + (size_t)s * a.budget;
+
+  // the list of the last fire, its length and the Q operand, loaded with the
+  // boundary test's inputs (every access to the list and its length is a
+  // device-scope load: selecting blocks of this launch write them on a fire)
+  int early[kStepListEarly];
 #pragma unroll
-  for (int j = 0; j < G; ++j) {
-    l[j] = row16_sum(l[j]);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      acc[j][e] += __shfl_xor(acc[j][e], 16, kWave);
-      acc[j][e] += __shfl_xor(acc[j][e], 32, kWave);
-    }
+  for (int e = 0; e < kStepListEarly; ++e) {
+    const int i = tid + e * kSelThreads;
+    early[e] = p0 + i < sel_hi ? __hip_atomic_load(rl + p0 + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
   }
-  if (lane < 16) {
-#pragma unroll
-    for (int j = 0; j < G; ++j) {
-      if (lane == 0) {
-        s_m[w][j] = m[j];
-        s_l[w][j] = l[j];
+  int nsel = __hip_atomic_load(a.n_sel + s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  attn_bf16x8 qa[NM][4];
+  load_attn_q<G>(a.q + (size_t)s * G * kHeadDim, lane, qa);
+  const double r = boundary_r(a.q, a.q_ref, n_q_heads, a.first, grp, s_bpart);
+  const bool fire = a.first || r < a.tau;
+  if (c == 0 && kvh == 0 && tid == 0) {
+    if (a.r_out) a.r_out[grp] = r;
+    a.fire_out[grp] = (uint8_t)(fire ? 1 : 0);
+  }
+  if (c == 0 && w == 0)
+    store_slice(a.k_new, a.v_new, a.k_local, a.v_local, a.window, a.step, a.seg_len, a.evict_seg, a.reps,
+                a.unit_start, a.unit_size, a.units_cap, a.n_clusters, a.k_pool, a.v_pool, a.pool_rows, a.prompt_len,
+                s, lane);
+
+  // attention LDS (after the selection's, which it may reuse)
+  float4 (*s_p)[NM][64] = reinterpret_cast<float4 (*)[NM][64]>(smem);
+  float (*s_m)[G] = reinterpret_cast<float (*)[G]>(s_p + NW);
+  float (*s_l)[G] = s_m + NW;
+  float (*s_acc)[G][kHeadDim] = reinterpret_cast<float (*)[G][kHeadDim]>(s_l + NW);
+  float2* s_ml = reinterpret_cast<float2*>(s_acc + NW);
+  int* s_rows = reinterpret_cast<int*>(s_ml + nb * G);
+  auto clamp_row = [&](int row) { return (int)min<int64_t>(max(row, 0), a.pool_rows - 1); };
+  if (fire) {
+    const bool selected = select_part<uint16_t, G, true>(
+        a.q, a.n_kv_heads, s, c, nb, a.scale, a.reps, a.units_cap, a.n_units, a.n_pad, a.budget, a.unit_start,
+        a.unit_size, a.sel_units, a.n_sel_units, a.n_sel, a.sel_rows, a.scores_out, a.logit_ws, a.part_max,
+        a.sel_counter + s * kStepSyncStride, smem);
+    if (selected) {
+      // the list is out before the flag goes up
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+      if (tid == 0) __hip_atomic_store(a.ready + s * kStepSyncStride, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+      if (tid == 0) {
+        int polls = 0;
+        while (__hip_atomic_load(a.ready + s * kStepSyncStride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
+          if (++polls >= kStepSpinLimit) {
+            __hip_atomic_store(a.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            break;
+          }
+          __builtin_amdgcn_s_sleep(8);
+        }
       }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) s_acc[w][j][8 * p16 + e] = acc[j][e];
+      __syncthreads();
     }
+    nsel = __hip_atomic_load(a.n_sel + s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (int i = tid; p0 + i < sel_hi; i += kSelThreads)
+      s_rows[i] = clamp_row(__hip_atomic_load(rl + p0 + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+    load_attn_q<G>(a.q + (size_t)s * G * kHeadDim, lane, qa);   // not kept in registers across the selection
+  } else {
+#pragma unroll
+    for (int e = 0; e < kStepListEarly; ++e) {
+      const int i = tid + e * kSelThreads;
+      if (p0 + i < sel_hi) s_rows[i] = clamp_row(early[e]);
+    }
+    for (int i = tid + kStepListEarly * kSelThreads; p0 + i < sel_hi; i += kSelThreads)
+      s_rows[i] = clamp_row(__hip_atomic_load(rl + p0 + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
   }
   __syncthreads();
-  attn_block_merge<G, NW>(s_m, s_l, s_acc, tid, s, chunk, n_chunks, part, out, out_bf16, lse_out, sync.counter,
-                          reinterpret_cast<float2*>(s_rows));
+  nsel = max(0, min(nsel, a.budget));
+
+  // the chunk's rows: 16-row tiles t = w, w + NW, ...
+  const uint16_t* kb = a.k_pool + (size_t)s * a.pool_rows * kHeadDim;
+  const uint16_t* vb = a.v_pool + (size_t)s * a.pool_rows * kHeadDim;
+  const uint16_t* kl = a.k_local + (size_t)s * a.window * kHeadDim;
+  const uint16_t* vl = a.v_local + (size_t)s * a.window * kHeadDim;
+  const uint16_t* kn = a.k_new + (size_t)s * kHeadDim;
+  const uint16_t* vn = a.v_new + (size_t)s * kHeadDim;
+  const int newest = a.step % a.window;
+  // the row at position pos of the chunk, or NULL if there is none
+  auto row_ptr = [&](int pos, const uint16_t* pool, const uint16_t* ring, const uint16_t* cur) -> const uint16_t* {
+    if (pos >= p1) return nullptr;
+    if (pos < a.budget) return pos < nsel ? pool + (size_t)s_rows[pos - p0] * kHeadDim : nullptr;
+    int slot = a.local_start + (pos - a.budget);   // local_start < window and pos - budget < n_local <= window
+    slot -= slot >= a.window ? a.window : 0;
+    return slot == newest ? cur : ring + (size_t)slot * kHeadDim;
+  };
+  auto load_tile = [&](int t, uint4 (&kx)[4], uint4 (&vx)[4]) -> bool {
+    const int tb = p0 + 16 * t;
+    const uint16_t* kp = row_ptr(tb + p16, kb, kl, kn);
+#pragma unroll
+    for (int cc = 0; cc < 4; ++cc) kx[cc] = kp ? *reinterpret_cast<const uint4*>(kp + 32 * cc + 8 * g) : uint4{};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint16_t* vp = row_ptr(tb + 4 * k + g, vb, vl, vn);
+      vx[k] = vp ? *reinterpret_cast<const uint4*>(vp + 8 * p16) : uint4{};
+    }
+    return kp != nullptr;
+  };
+  // the block has read q_ref: count it in at the group's counter, after its
+  // main loads (a wave's loads complete in order, and this atomic, on one
+  // address for the whole group, returns late)
+  int grp_old = 0;
+  bool arrived = false;
+  auto arrive_group = [&]() {
+    if (arrived) return;
+    arrived = true;
+    __builtin_amdgcn_sched_barrier(0);
+    if (tid == 0)
+      grp_old = __hip_atomic_fetch_add(a.grp_counter + grp * kStepSyncStride, 1, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+  };
+  float m[G], l[G], acc[G][8];
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    m[j] = -__builtin_inff();
+    l[j] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[j][e] = 0.f;
+  }
+  const float qscale = (float)a.scale * kLog2e;
+  const int n_tiles = (p1 - p0 + 15) / 16;
+  constexpr int kInFlight = G == 8 ? 1 : 2;   // tiles per wave in flight (G = 8: registers for one)
+  for (int t = w; t < n_tiles; t += kInFlight * NW) {
+    uint4 kx0[4], vx0[4], kx1[4], vx1[4];
+    const bool two = kInFlight == 2 && t + NW < n_tiles;
+    const bool kv0 = load_tile(t, kx0, vx0);
+    const bool kv1 = two ? load_tile(t + NW, kx1, vx1) : false;
+    arrive_group();
+    attn_mfma_tile<G>(qa, kx0, vx0, kv0, qscale, m, l, acc, s_p[w], lane);
+    if (two) attn_mfma_tile<G>(qa, kx1, vx1, kv1, qscale, m, l, acc, s_p[w], lane);
+  }
+  arrive_group();
+  attn_wave_to_lds<G>(m, l, acc, s_m[w], s_l[w], s_acc[w], lane);
+  __syncthreads();
+  const bool done = attn_block_merge<G, NW, true>(s_m, s_l, s_acc, tid, s, c, nb, a.part, a.out, a.out_bf16,
+                                                  a.lse_out, a.attn_counter + s * kStepSyncStride, s_ml);
+  if (done && fire && tid == 0)
+    __hip_atomic_store(a.ready + s * kStepSyncStride, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+  // the group's last block to arrive moves its reference query
+  if (tid == 0) s_grp_last = grp_old == a.n_kv_heads * nb - 1;
+  __syncthreads();
+  if (!s_grp_last) return;
+  if (tid == 0) __hip_atomic_store(a.grp_counter + grp * kStepSyncStride, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (a.mode == LOUISKV_REF_PREV || fire) {
+    const size_t base = (size_t)grp * n_q_heads * kHeadDim;
+    for (int i = tid; i < n_q_heads * kHeadDim / 8; i += kSelThreads)
+      reinterpret_cast<uint4*>(a.q_ref + base)[i] = reinterpret_cast<const uint4*>(a.q + base)[i];
+  }
 }
 
 // One wave per (slice, head): merge the chunk partials.
@@ -2254,9 +2628,11 @@ int step_attn_chunks(int buf_rows, int window) {
   return std::max(1, (int)(((int64_t)buf_rows + window + kStepAttnRows - 1) / kStepAttnRows));
 }
 
-// Partials of the fused step's attention (merged in-kernel), by dtype.
+// Partials of the fused step's attention (merged in-kernel), by dtype (bf16:
+// the two-launch step's chunks or the one-launch step's blocks per slice).
 size_t step_attn_part_bytes(int64_t S, int G, int buf_rows, int window, int dtype) {
-  const int nc = dtype == LOUISKV_BF16 ? step_attn_chunks(buf_rows, window) : attn_chunks(S, buf_rows, window, true);
+  const int nc = dtype == LOUISKV_BF16 ? std::max(step_attn_chunks(buf_rows, window), kStepMaxBlocks)
+                                       : attn_chunks(S, buf_rows, window, true);
   return nc == 1 ? 0 : align_up((size_t)S * nc * G * (2 + kHeadDim) * sizeof(float), 256);
 }
 
@@ -2853,30 +3229,31 @@ extern "C" int louiskv_sparse_decode_attn_rows(const void* q, int32_t dtype, int
 }
 
 // ---------------------------------------------------------------------------
-// One decode step of Algorithm 1 in two launches (fixed segments, pool in
-// device memory, KV_critical as a row list).
+// One decode step of Algorithm 1 in one launch (bf16: step_fused_kernel) or
+// two (float32, and with the LRU cache: step_select_kernel, then the
+// attention) (fixed segments, KV_critical as a row list).
 
 namespace louiskv {
 namespace {
 
-// Workspace of louiskv_decode_step: two arrival counters per slice (which
-// must be zero before the first call and are zero after every call), the
-// logits and per-part maxima of the selection, the attention partials.
 struct StepLayout {
   size_t counters, logits, pmax, fetch, part, total;
 };
 
-// Workspace of a decode step: the arrival counters (zero between calls),
-// logits and part maxima, with a cached KV_critical the transfer plan's
-// scratch (fetch slots, rows, counts), and the attention partials.
+// Workspace of a decode step: the arrival counters and flags (zero between
+// calls; the one-launch step keeps selection and attention counters and
+// ready flags per slice, group counters and a status word kStepSyncStride
+// ints apart, the two-launch step its two counters per slice packed at the
+// start), logits and part maxima, with a cached KV_critical the transfer
+// plan's scratch (fetch slots, rows, counts), and the attention partials.
 StepLayout step_layout(int64_t S, int dtype, int G, int units_cap, int budget, int window, bool cached = false) {
   StepLayout L{};
   Carver cv(nullptr);
-  cv.take<int32_t>((size_t)2 * S);
+  cv.take<int32_t>(((size_t)4 * S + 1) * kStepSyncStride);
   L.logits = align_up(cv.used, 256);
   cv.take<double>((size_t)S * units_cap * G);
   L.pmax = align_up(cv.used, 256);
-  cv.take<double>((size_t)S * kMaxLogitParts * G);
+  cv.take<double>((size_t)S * std::max(kMaxLogitParts, kMaxSelectParts) * G);
   L.fetch = align_up(cv.used, 256);
   if (cached) cv.take<int32_t>((size_t)S * (2 * (size_t)std::max(budget, 1) + 1));
   L.part = align_up(cv.used, 256);
@@ -2981,6 +3358,85 @@ int decode_step_impl(const void* q, void* q_ref, int32_t dtype, int64_t n_groups
   const size_t lds = (size_t)n_pad * (sizeof(uint64_t) + 2 * sizeof(int));
   const double scale = 1.0 / sqrt((double)kHeadDim);
   hipStream_t s = as_stream(stream);
+  if (!cache && dtype == LOUISKV_BF16) {   // the whole step in one launch
+    // blocks per slice: one per kStepAttnRows rows (a 16-row tile per wave),
+    // at most kStepMaxBlocks and at most one per compute unit over the launch
+    // (a block of the selection's register footprint fills one)
+    const int cus = device_cu_count();
+    const int nb = (int)std::max<int64_t>(
+        1, std::min<int64_t>({(int64_t)kStepMaxBlocks, (int64_t)step_attn_chunks(budget, window),
+                              (cus > 0 ? cus : 256) / n_slices}));
+    const int64_t total_rows = (int64_t)budget + window;
+    const int chunk_rows = (int)(((total_rows + nb - 1) / nb + 15) / 16 * 16);
+    if (n_slices * nb > INT32_MAX) return fail(LOUISKV_ERR_SHAPE, "problem too large for one launch");
+    FusedStep fa{};
+    fa.q = static_cast<const uint16_t*>(q);
+    fa.q_ref = static_cast<uint16_t*>(q_ref);
+    fa.n_slices = n_slices;
+    fa.n_kv_heads = n_kv_heads;
+    fa.first = step == 0 ? 1 : 0;
+    fa.mode = mode;
+    fa.tau = tau;
+    fa.r_out = r_out;
+    fa.fire_out = fire_out;
+    fa.k_new = static_cast<const uint16_t*>(k_new);
+    fa.v_new = static_cast<const uint16_t*>(v_new);
+    fa.k_local = static_cast<uint16_t*>(k_local);
+    fa.v_local = static_cast<uint16_t*>(v_local);
+    fa.window = window;
+    fa.step = step;
+    fa.seg_len = seg_len;
+    fa.evict_seg = ev;
+    fa.reps = reps;
+    fa.unit_start = unit_start;
+    fa.unit_size = unit_size;
+    fa.units_cap = units_cap;
+    fa.n_clusters = n_clusters;
+    fa.k_pool = static_cast<uint16_t*>(k_pool);
+    fa.v_pool = static_cast<uint16_t*>(v_pool);
+    fa.pool_rows = pool_rows;
+    fa.prompt_len = prompt_len;
+    fa.scale = scale;
+    fa.n_units = (int)n_units;
+    fa.budget = budget;
+    fa.sel_units = sel_units;
+    fa.n_sel_units = n_sel_units;
+    fa.n_sel = n_sel;
+    fa.sel_rows = sel_rows;
+    fa.scores_out = scores_out;
+    fa.logit_ws = logit_ws;
+    fa.part_max = part_max;
+    fa.sel_counter = sel_counter;
+    fa.attn_counter = sel_counter + n_slices * kStepSyncStride;
+    fa.ready = sel_counter + 2 * n_slices * kStepSyncStride;
+    fa.grp_counter = sel_counter + 3 * n_slices * kStepSyncStride;
+    fa.status = sel_counter + 4 * n_slices * kStepSyncStride;
+    fa.n_blk = nb;
+    fa.chunk_rows = chunk_rows;
+    fa.n_pad = n_pad;
+    fa.local_start = local_start;
+    fa.n_local = n_local;
+    fa.part = reinterpret_cast<float*>(ws + lay.part);
+    fa.out = out;
+    fa.out_bf16 = out_dtype == LOUISKV_BF16;
+    fa.lse_out = lse_out;
+    const unsigned fgrid = (unsigned)(n_slices * nb);
+#define LKV_STEP_FUSED(G)                                                                                   \
+  {                                                                                                         \
+    const size_t flds = std::max(lds, fused_attn_lds<G>(nb, chunk_rows));                                   \
+    if ((st = check_lds(reinterpret_cast<const void*>(&step_fused_kernel<G>), flds))) return st;            \
+    step_fused_kernel<G><<<fgrid, kSelThreads, flds, s>>>(fa);                                              \
+  }
+    switch (group_size) {
+      case 1: LKV_STEP_FUSED(1); break;
+      case 2: LKV_STEP_FUSED(2); break;
+      case 4: LKV_STEP_FUSED(4); break;
+      default: LKV_STEP_FUSED(8); break;
+    }
+#undef LKV_STEP_FUSED
+    LKV_CHECK_LAUNCH();
+    return LOUISKV_OK;
+  }
   const unsigned grid = (unsigned)(n_slices * n_parts);
 #define LKV_STEP_SEL(T, G)                                                                                           \
   if ((st = check_lds(reinterpret_cast<const void*>(&step_select_kernel<T, G>), lds))) return st;                    \

@@ -22,8 +22,8 @@ paper's Algorithm 1:
              on the device).
 
 A call over few slices (a layer at a time, the group views below) runs the
-whole step as louiskv_decode_step: the same stages in two launches that
-spread each slice over many blocks.
+whole step as louiskv_decode_step: the same stages in one launch (bf16; two
+in float32) that spreads each slice over many blocks.
 
 With the pool in device memory the engine runs zero-copy by default:
 louiskv_retrieve_rows keeps KV_critical as a list of pool rows and
@@ -54,7 +54,7 @@ from . import louiskv as L
 
 MAX_UNITS = 8192   # units one slice's retrieval scores (the library's limit)
 # a call over at most this many slices runs the decode step as louiskv_decode_step
-# (two launches, each slice spread over many blocks); larger ones use the
+# (one launch in bf16, each slice spread over many blocks); larger ones use the
 # per-stage calls, whose kernels fill the chip with one block per slice
 FUSED_STEP_MAX_SLICES = 64
 # KV_critical over a host-resident pool: an LRU cache of this many budgets of
@@ -249,7 +249,7 @@ class LouisKVEngine:
         else:
             self.ws_retrieve = torch.empty(L.retrieve_workspace_size(S, cap, cfg.budget), **u8)
             self.ws_attn = torch.empty(max(L.sparse_decode_attn_workspace_size(S, g, rows, cfg.window), 1), **u8)
-        # the whole decode step in two launches (louiskv_decode_step): built for
+        # the whole decode step in one launch (louiskv_decode_step): built for
         # fixed segments over a device pool with the row-list KV_critical and
         # group-consistent selection; fused_step=None uses it for calls over
         # few slices (a layer at a time), True for every call, False never
@@ -361,6 +361,17 @@ class LouisKVEngine:
             self._view_ws_attn[n] = (self.ws_attn if need <= self.ws_attn.numel() else
                                      torch.empty(need, dtype=torch.uint8, device=self.device))
         v.ws_attn = self._view_ws_attn[n]
+        # the fused step's workspace (counters zero between calls) sized for
+        # the view, shared by the views of n groups, which run one at a time
+        if self.ws_step is not None:
+            if not hasattr(self, "_view_ws_step"):
+                self._view_ws_step = {}
+            if n not in self._view_ws_step:
+                size = (L.decode_step_cached_workspace_size if self._fused_cached else L.decode_step_workspace_size)
+                dc = L.BF16 if self.dtype == torch.bfloat16 else L.F32
+                self._view_ws_step[n] = torch.zeros(size(h * n, dc, c.n_q_heads // h, c.units_cap, c.budget,
+                                                         c.window), dtype=torch.uint8, device=self.device)
+            v.ws_step = self._view_ws_step[n]
         return v
 
     def step_layer_by_layer(self, q_t: torch.Tensor, k_t: torch.Tensor, v_t: torch.Tensor,

@@ -381,7 +381,8 @@ def decode_step(q, q_ref, tau: float, mode: int, step: int, fire, r_out, k_new, 
                 budget: int, sel_units, n_sel_units, n_sel, sel_rows, out, lse_out=None, scores_out=None,
                 workspace=None, stream=None):
     """One decode step (boundary, store, retrieval of the fired groups, attention)
-    in two launches.  workspace: zero-filled before its first use."""
+    in one launch (bf16; two in float32).  workspace: zero-filled before its
+    first use."""
     g, hq, d = q.shape
     s = k_new.shape[0]
     h = s // g

@@ -218,6 +218,12 @@ def test_workspace_sizes_are_positive(lib):
     assert lib.louiskv_sparse_decode_attn_workspace_size(256, 4, 128, 2048, 128) == 0
     assert lib.louiskv_sparse_decode_attn_workspace_size(8, 4, 128, 2048, 128) > 0
     assert lib.louiskv_cluster_prefill_workspace_size(0, 1, 128, 1, 1) == 0
+    # the decode step's counters and flags (256 bytes apart, zero between
+    # calls), then the selection's logits, part maxima and attention partials
+    S, G, cap, budget, window = 8, 4, 1100, 2048, 128
+    step = lib.louiskv_decode_step_workspace_size(S, 1, G, cap, budget, window)
+    assert step >= 256 * (4 * S + 1) + S * cap * G * 8 + S * 32 * G * 8 + S * 32 * G * 130 * 4
+    assert lib.louiskv_decode_step_workspace_size(S, 1, 9, cap, budget, window) == 0
 
 
 def test_bench_refuses_more_than_one_gpu():

@@ -45,7 +45,7 @@ def test_c_caller_matches_python_binding(tmp_path):
     assert r.returncode == 0, r.stderr
     cfg = config_from_workload(wl, n_groups=1)
     # the C caller runs the per-stage calls, so the engine does too (not the
-    # two-launch step it takes by default for a single group)
+    # one-launch step it takes by default for a single group)
     eng = LouisKVEngine(cfg, torch.bfloat16, DEV, out_dtype=torch.float32, fuse_prologue=False, fused_step=False)
     eng.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
     outs = []

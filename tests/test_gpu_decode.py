@@ -947,16 +947,20 @@ def test_host_pool_flag_rejects_device_memory():
 
 
 @pytest.mark.parametrize("case", ["bf16-anchor", "bf16-prev", "fp32-anchor", "bf16-anchor-hostcache",
-                                  "fp32-prev-hostcache", "bf16-anchor-g8", "bf16-prev-g1-hostcache"])
+                                  "fp32-prev-hostcache", "bf16-anchor-g8", "bf16-prev-g1-hostcache", "bf16-prev-g2",
+                                  "bf16-anchor-g1-b100"])
 def test_decode_step_equals_stage_calls(case):
     """louiskv_decode_step (boundary, store, retrieval and attention of a step
-    in two launches, blocks of a slice handing over through the workspace)
-    against the stage calls it replaces, every step of a run with evictions:
-    decisions, r, reference queries, scores, selections, row lists, unit
-    tables, window and pool equal bit for bit; the attention output and lse
-    too in fp32 (same chunks, same merge arithmetic), within 1e-5 in bf16
-    (the step splits each slice's rows into smaller chunks).  The arrival
-    counters in the workspace are zero after every step.  hostcache:
+    in one launch in bf16, whose attention blocks wait for a fired slice's
+    selection blocks, and in two launches in fp32; blocks of a slice hand over
+    through the workspace) against the stage calls it replaces, every step of
+    a run with evictions: decisions, r, reference queries, scores, selections,
+    row lists, unit tables, window and pool equal bit for bit; the attention
+    output and lse too in fp32 (same chunks, same merge arithmetic), within
+    1e-5 in bf16 (the step splits each slice's rows into smaller chunks).
+    Group sizes 1, 2, 4 and 8; b100: a 100-row budget, so that the selected
+    rows and the window share an attention chunk.  The arrival counters, ready
+    flags and status word in the workspace are zero after every step.  hostcache:
     louiskv_decode_step_cached over a pinned host pool with an LRU cache of
     four budgets against the stage calls with the same cache (buffer rows,
     slot steps, slot lists, fetch counts and cached rows equal too)."""
@@ -964,6 +968,7 @@ def test_decode_step_equals_stage_calls(case):
     dname, mname = case.split("-")[:2]
     cached = case.endswith("hostcache")
     gsize = next((int(p[1:]) for p in case.split("-") if p[0] == "g" and p[1:].isdigit()), None)
+    bsize = next((int(p[1:]) for p in case.split("-") if p[0] == "b" and p[1:].isdigit()), None)
     mode = _L().REF_PREV if mname == "prev" else _L().REF_ANCHOR
     if dname == "bf16":
         wl = synth.get_workload("si-lo-16k").replace(prompt_len=2048, n_clusters=64, budget=512, name="si-lo-16k")
@@ -973,6 +978,8 @@ def test_decode_step_equals_stage_calls(case):
         n_groups, steps = 1, 256
     if gsize is not None:   # other query-group sizes: 8 KV heads, g query heads each
         wl = wl.replace(n_q_heads=wl.n_kv_heads * gsize)
+    if bsize is not None:   # a budget whose rows and the window's split into ragged attention chunks
+        wl = wl.replace(budget=bsize)
     data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(n_groups)], gen_len=steps)
     cfg = config_from_workload(wl, n_groups=n_groups, mode=mode, gen_len=steps)
     dt = data.prompt_keys.dtype
@@ -1016,7 +1023,7 @@ def test_decode_step_equals_stage_calls(case):
             err = (a.out - b.out).abs().max().item()
             assert err <= 1e-5 * max(1.0, a.out.abs().max().item()), (t, err)
             assert (a.lse - b.lse).abs().max().item() <= 1e-5, t
-        assert int(b.ws_step[:8 * S].view(torch.int32).abs().sum()) == 0, t
+        assert int(b.ws_step[:256 * (4 * S + 1)].view(torch.int32).abs().sum()) == 0, t
         fires += int(a.fire.sum())
         evictions += int(_L().window_info(t, wl.window, wl.seg_len)[0] >= 0)
     print(f"[decode step] {case}: {steps} steps, {fires} group fires, {evictions} evictions", flush=True)
@@ -1030,8 +1037,8 @@ def test_layer_by_layer_step_graphs_match_eager(case):
     eager group-by-group loop: over a pinned host pool with the default LRU
     cache of pool rows (interior pointers of the pool resolved per group view
     at capture time, the decode step baked into each graph),
-    and over a device pool, where each view runs the two-launch decode step
-    whose workspace counters must return to zero on every replay."""
+    and over a device pool, where each view runs the one-launch decode step
+    whose workspace counters and flags must return to zero on every replay."""
     from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
     host = case.startswith("host")
     if host:
@@ -1042,7 +1049,7 @@ def test_layer_by_layer_step_graphs_match_eager(case):
     data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(G)], gen_len=steps)
     cfg = config_from_workload(wl, n_groups=G, gen_len=steps)
     eng = LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, pool_on_host=host, out_dtype=torch.float32)
-    # each view runs the fused step: two launches over a device pool, four
+    # each view runs the fused step: one launch over a device pool, four
     # with the LRU cache over the host pool
     assert eng.group_view(0)._use_fused_step() and eng.group_view(0)._fused_cached == host
     hist = torch.zeros(steps, *eng.out.shape, device=DEV)
@@ -1077,7 +1084,8 @@ def test_layer_by_layer_step_graphs_match_eager(case):
         print(f"step-graph replay {rep} ({case})", flush=True)
         assert torch.equal(hist, ref), (case, rep)
         assert torch.equal(hist_n, ref_n), (case, rep)
-        assert int(eng.ws_step[:8 * cfg.n_slices].view(torch.int32).abs().sum()) == 0
+        assert all(int(w[:256 * (4 * cfg.n_kv_heads + 1)].view(torch.int32).abs().sum()) == 0
+                   for w in eng._view_ws_step.values())
     del graphs
 
 
