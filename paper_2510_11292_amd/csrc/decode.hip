@@ -990,21 +990,6 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
                              n_sel, row_ws, scores_out, s_key, s_size, s_incl);
 }
 
-// The first launch of a fused decode step (fixed segments, device pool), one
-// block of kSelThreads per (slice, part of its units):
-//  - every block computes its group's r and decision (boundary_r: the same
-//    value in every block); one block per group writes them;
-//  - block 0 of each slice runs the fixed-segment store (window append and
-//    oldest-segment eviction, store_slice on its first wave): it writes only
-//    the unit it creates and rows past every existing unit, which the
-//    retrieval below does not read;
-//  - blocks of a group that did not fire stop there; the others compute the
-//    float64 logits of their part of the units (the arithmetic of
-//    unit_logits_kernel) and their per-head maxima, write them with
-//    device-scope stores and count themselves in; the last block of the
-//    slice to arrive resets the counter and makes the selection from all the
-//    parts (select_after_max), as score_select_kernel does.
-// The reference query is left for the attention launch to update.
 // A fired slice's part `part` of the selection work in a decode step: the
 // logits of the part's units and their per-head maxima, written with
 // device-scope stores; the part then counts itself in at the slice's
@@ -1088,11 +1073,15 @@ __device__ __forceinline__ bool select_part(const T* __restrict__ q, int n_kv_he
   return true;
 }
 
-// The first launch of a two-launch decode step: one 512-thread block per
-// (slice, part of its units).  Every block computes its group's r (the same
-// float64 value in every block), block 0 of a slice runs the fixed-segment
-// store, and if the group fired each block does its part of the selection
-// (select_part).
+// The first launch of a two-launch decode step (fixed segments): one
+// 512-thread block per (slice, part of its units).  Every block computes its
+// group's r (the same float64 value in every block; one block per group
+// writes it and the decision), block 0 of a slice runs the fixed-segment
+// store (window append and oldest-segment eviction on its first wave: it
+// writes only the unit it creates and rows past every existing unit, which
+// the retrieval does not read), and if the group fired each block does its
+// part of the selection (select_part).  The reference query is left for the
+// attention launch to update.
 template <class T, int G>
 __global__ __launch_bounds__(kSelThreads)
 void step_select_kernel(const T* __restrict__ q, const T* __restrict__ q_ref, int n_kv_heads, double tau, int first,

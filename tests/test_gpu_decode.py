@@ -948,7 +948,7 @@ def test_host_pool_flag_rejects_device_memory():
 
 @pytest.mark.parametrize("case", ["bf16-anchor", "bf16-prev", "fp32-anchor", "bf16-anchor-hostcache",
                                   "fp32-prev-hostcache", "bf16-anchor-g8", "bf16-prev-g1-hostcache", "bf16-prev-g2",
-                                  "bf16-anchor-g1-b100"])
+                                  "bf16-anchor-g1-b100", "bf16-anchor-n8", "bf16-prev-g8-n8"])
 def test_decode_step_equals_stage_calls(case):
     """louiskv_decode_step (boundary, store, retrieval and attention of a step
     in one launch in bf16, whose attention blocks wait for a fired slice's
@@ -959,7 +959,8 @@ def test_decode_step_equals_stage_calls(case):
     output and lse too in fp32 (same chunks, same merge arithmetic), within
     1e-5 in bf16 (the step splits each slice's rows into smaller chunks).
     Group sizes 1, 2, 4 and 8; b100: a 100-row budget, so that the selected
-    rows and the window share an attention chunk.  The arrival counters, ready
+    rows and the window share an attention chunk; n8: 8 groups (64 slices),
+    so that a slice gets 4 blocks of 160 rows and a wave several tiles.  The arrival counters, ready
     flags and status word in the workspace are zero after every step.  hostcache:
     louiskv_decode_step_cached over a pinned host pool with an LRU cache of
     four budgets against the stage calls with the same cache (buffer rows,
@@ -969,10 +970,11 @@ def test_decode_step_equals_stage_calls(case):
     cached = case.endswith("hostcache")
     gsize = next((int(p[1:]) for p in case.split("-") if p[0] == "g" and p[1:].isdigit()), None)
     bsize = next((int(p[1:]) for p in case.split("-") if p[0] == "b" and p[1:].isdigit()), None)
+    ngroups = next((int(p[1:]) for p in case.split("-") if p[0] == "n" and p[1:].isdigit()), None)
     mode = _L().REF_PREV if mname == "prev" else _L().REF_ANCHOR
     if dname == "bf16":
         wl = synth.get_workload("si-lo-16k").replace(prompt_len=2048, n_clusters=64, budget=512, name="si-lo-16k")
-        n_groups, steps = 2, 300
+        n_groups, steps = ngroups or 2, 300
     else:
         wl = synth.get_workload("tiny-4k")
         n_groups, steps = 1, 256
