@@ -2312,10 +2312,13 @@ void attn_mfma_kernel(const uint16_t* __restrict__ q, int n_kv_heads, float scal
 // makes the selection, writes the row list with device-scope stores and
 // raises the slice's ready flag; the others wait for the flag and read the
 // new list entries coherently.  Only blocks that have arrived wait, and they
-// wait for the last arrival, which is running and waits for nothing, so the
-// wait ends whatever the scheduling (it is bounded all the same: past
-// kStepSpinLimit polls a block records a time-out in the status word and goes
-// on).  Then the block attends its chunk of the slice's row sequence (the
+// wait for the last arrival, which is running and waits for nothing; so the
+// wait ends once every block of the slice has started, which holds when the
+// whole grid is resident at once (the launch gives the chip at most one
+// block per compute unit) and also when it is not, since workgroups are
+// dispatched in index order and a slice's blocks are consecutive.  The wait
+// is bounded all the same: past kStepSpinLimit polls a block records a
+// time-out in the status word and goes on.  Then the block attends its chunk of the slice's row sequence (the
 // selected rows, padded to the budget, then the window rows), two 16-row
 // tiles per wave in flight; the newest window row is read from k_new/v_new,
 // since the store of the same launch may not have reached the ring yet.  The
@@ -3349,12 +3352,15 @@ int decode_step_impl(const void* q, void* q_ref, int32_t dtype, int64_t n_groups
   hipStream_t s = as_stream(stream);
   if (!cache && dtype == LOUISKV_BF16) {   // the whole step in one launch
     // blocks per slice: one per kStepAttnRows rows (a 16-row tile per wave),
-    // at most kStepMaxBlocks and at most one per compute unit over the launch
-    // (a block of the selection's register footprint fills one)
+    // at most kStepMaxBlocks, and at most one block per compute unit over the
+    // launch (a block of the selection's register footprint fills one), so
+    // that every block can be resident at once whenever blocks wait (two or
+    // more per slice; a slice's only block never waits)
     const int cus = device_cu_count();
+    const int64_t step_cus = cus > 0 ? cus : 256;
     const int nb = (int)std::max<int64_t>(
         1, std::min<int64_t>({(int64_t)kStepMaxBlocks, (int64_t)step_attn_chunks(budget, window),
-                              (cus > 0 ? cus : 256) / n_slices}));
+                              step_cus / n_slices}));
     const int64_t total_rows = (int64_t)budget + window;
     const int chunk_rows = (int)(((total_rows + nb - 1) / nb + 15) / 16 * 16);
     if (n_slices * nb > INT32_MAX) return fail(LOUISKV_ERR_SHAPE, "problem too large for one launch");

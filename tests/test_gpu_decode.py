@@ -948,7 +948,8 @@ def test_host_pool_flag_rejects_device_memory():
 
 @pytest.mark.parametrize("case", ["bf16-anchor", "bf16-prev", "fp32-anchor", "bf16-anchor-hostcache",
                                   "fp32-prev-hostcache", "bf16-anchor-g8", "bf16-prev-g1-hostcache", "bf16-prev-g2",
-                                  "bf16-anchor-g1-b100", "bf16-anchor-n8", "bf16-prev-g8-n8"])
+                                  "bf16-anchor-g1-b100", "bf16-anchor-n8", "bf16-prev-g8-n8",
+                                  "bf16-anchor-h4-b4096-n1"])
 def test_decode_step_equals_stage_calls(case):
     """louiskv_decode_step (boundary, store, retrieval and attention of a step
     in one launch in bf16, whose attention blocks wait for a fired slice's
@@ -960,7 +961,9 @@ def test_decode_step_equals_stage_calls(case):
     1e-5 in bf16 (the step splits each slice's rows into smaller chunks).
     Group sizes 1, 2, 4 and 8; b100: a 100-row budget, so that the selected
     rows and the window share an attention chunk; n8: 8 groups (64 slices),
-    so that a slice gets 4 blocks of 160 rows and a wave several tiles.  The arrival counters, ready
+    so that a slice gets 4 blocks of 160 rows and a wave several tiles;
+    h4-b4096-n1: one group of 4 slices with a 4096-row budget, 32 blocks of
+    144 rows a slice.  The arrival counters, ready
     flags and status word in the workspace are zero after every step.  hostcache:
     louiskv_decode_step_cached over a pinned host pool with an LRU cache of
     four budgets against the stage calls with the same cache (buffer rows,
@@ -971,6 +974,7 @@ def test_decode_step_equals_stage_calls(case):
     gsize = next((int(p[1:]) for p in case.split("-") if p[0] == "g" and p[1:].isdigit()), None)
     bsize = next((int(p[1:]) for p in case.split("-") if p[0] == "b" and p[1:].isdigit()), None)
     ngroups = next((int(p[1:]) for p in case.split("-") if p[0] == "n" and p[1:].isdigit()), None)
+    nkv = next((int(p[1:]) for p in case.split("-") if p[0] == "h" and p[1:].isdigit()), None)
     mode = _L().REF_PREV if mname == "prev" else _L().REF_ANCHOR
     if dname == "bf16":
         wl = synth.get_workload("si-lo-16k").replace(prompt_len=2048, n_clusters=64, budget=512, name="si-lo-16k")
@@ -982,6 +986,9 @@ def test_decode_step_equals_stage_calls(case):
         wl = wl.replace(n_q_heads=wl.n_kv_heads * gsize)
     if bsize is not None:   # a budget whose rows and the window's split into ragged attention chunks
         wl = wl.replace(budget=bsize)
+    if nkv is not None:     # fewer KV heads, a longer prompt for the larger budget
+        g = wl.n_q_heads // wl.n_kv_heads
+        wl = wl.replace(n_kv_heads=nkv, n_q_heads=nkv * g, prompt_len=8192, n_clusters=256)
     data = synth.make_slices(wl, DEV, groups=[(0, l) for l in range(n_groups)], gen_len=steps)
     cfg = config_from_workload(wl, n_groups=n_groups, mode=mode, gen_len=steps)
     dt = data.prompt_keys.dtype
