@@ -468,8 +468,11 @@ int louiskv_sparse_decode_attn_rows(const void* q, int32_t dtype, int64_t n_slic
  *            Its first (4 * n_slices + 1) * 64 int32 words are those
  *            counters and flags; the last of them is a status word that a
  *            block sets to 1 if its wait for a selection ever gave up (after
- *            about a million polls, which a correct launch never reaches),
- *            and that the library never clears.
+ *            about a million polls, which a correct launch never reaches;
+ *            the environment variable LOUISKV_STEP_SPIN_LIMIT lowers that
+ *            bound, for tests of this path), and that the library never
+ *            clears.  The outputs of a step that set it are undefined and
+ *            the workspace must be zeroed before its next use.
  */
 size_t louiskv_decode_step_workspace_size(int64_t n_slices, int32_t dtype, int32_t group_size,
                                           int32_t units_cap, int32_t budget, int32_t window);

@@ -2,6 +2,7 @@
 // segment eviction (Section 4.2 decode stage), group-consistent retrieval
 // (Appendix B; Algorithm 1 Retrieve) and sparse decode attention (Section 3.1).
 #include <algorithm>
+#include <cstdlib>
 
 #include <mutex>
 
@@ -2317,8 +2318,10 @@ void attn_mfma_kernel(const uint16_t* __restrict__ q, int n_kv_heads, float scal
 // whole grid is resident at once (the launch gives the chip at most one
 // block per compute unit) and also when it is not, since workgroups are
 // dispatched in index order and a slice's blocks are consecutive.  The wait
-// is bounded all the same: past kStepSpinLimit polls a block records a
-// time-out in the status word and goes on.  Then the block attends its chunk of the slice's row sequence (the
+// is bounded all the same: past spin_limit polls (kStepSpinLimit, or fewer
+// from LOUISKV_STEP_SPIN_LIMIT, for tests of this path) a block records a
+// time-out in the status word and goes on; its row-list entries are clamped
+// into the pool, so that such a step reads no memory out of bounds.  Then the block attends its chunk of the slice's row sequence (the
 // selected rows, padded to the budget, then the window rows), two 16-row
 // tiles per wave in flight; the newest window row is read from k_new/v_new,
 // since the store of the same launch may not have reached the ring yet.  The
@@ -2362,7 +2365,7 @@ struct FusedStep {
   double* scores_out;
   double *logit_ws, *part_max;
   int32_t *sel_counter, *attn_counter, *ready, *grp_counter, *status;
-  int n_blk, chunk_rows, n_pad;
+  int n_blk, chunk_rows, n_pad, spin_limit;
   int local_start, n_local;
   float* part;
   void* out;
@@ -2448,7 +2451,7 @@ void step_fused_kernel(const FusedStep a) {
       if (tid == 0) {
         int polls = 0;
         while (__hip_atomic_load(a.ready + s * kStepSyncStride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
-          if (++polls >= kStepSpinLimit) {
+          if (++polls >= a.spin_limit) {
             __hip_atomic_store(a.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             break;
           }
@@ -3232,6 +3235,17 @@ struct StepLayout {
   size_t counters, logits, pmax, fetch, part, total;
 };
 
+// Polls of the one-launch step's bounded wait: kStepSpinLimit, or fewer from
+// LOUISKV_STEP_SPIN_LIMIT (tests of the time-out path).
+int step_spin_limit() {
+  const char* e = getenv("LOUISKV_STEP_SPIN_LIMIT");
+  if (e && *e) {
+    const long v = strtol(e, nullptr, 10);
+    if (v >= 1 && v <= kStepSpinLimit) return (int)v;
+  }
+  return kStepSpinLimit;
+}
+
 // Workspace of a decode step: the arrival counters and flags (zero between
 // calls; the one-launch step keeps selection and attention counters and
 // ready flags per slice, group counters and a status word kStepSyncStride
@@ -3409,6 +3423,7 @@ int decode_step_impl(const void* q, void* q_ref, int32_t dtype, int64_t n_groups
     fa.n_blk = nb;
     fa.chunk_rows = chunk_rows;
     fa.n_pad = n_pad;
+    fa.spin_limit = step_spin_limit();
     fa.local_start = local_start;
     fa.n_local = n_local;
     fa.part = reinterpret_cast<float*>(ws + lay.part);

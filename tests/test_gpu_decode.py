@@ -1039,6 +1039,46 @@ def test_decode_step_equals_stage_calls(case):
     assert fires >= (2 if mname == "prev" else 20) and evictions > 2
 
 
+def test_decode_step_wait_is_bounded(monkeypatch):
+    """The one-launch step's wait for a fired slice's selection is bounded:
+    with the bound forced down to one poll (LOUISKV_STEP_SPIN_LIMIT=1) the
+    blocks of the first step, which always fires, give up at once (the
+    selection of 1024 units takes far longer than a poll), the launch
+    completes, and the workspace's status word reports the time-out.  That
+    step's outputs are undefined; with the workspace zeroed and the default
+    bound the next steps equal the stage calls again and leave the status
+    word at zero."""
+    from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
+    wl = synth.get_workload("si-lo-16k").replace(prompt_len=8192, n_clusters=1024, budget=2048, name="si-lo-16k")
+    steps = 6
+    data = synth.make_slices(wl, DEV, groups=[(0, 0)], gen_len=steps)
+    cfg = config_from_workload(wl, n_groups=1, gen_len=steps)
+    S = cfg.n_slices
+    status_at = 256 * 4 * S   # byte offset of the status word (after 4 S counters/flags 256 bytes apart)
+    a = LouisKVEngine(cfg, torch.bfloat16, DEV, out_dtype=torch.float32, fused_step=False)
+    b = LouisKVEngine(cfg, torch.bfloat16, DEV, out_dtype=torch.float32, fused_step=True)
+    for e in (a, b):
+        e.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    monkeypatch.setenv("LOUISKV_STEP_SPIN_LIMIT", "1")
+    print("[bounded wait] step 0 with a one-poll bound", flush=True)
+    b.step(data.queries[0], data.gen_keys[0], data.gen_values[0])
+    torch.cuda.synchronize()
+    assert int(b.ws_step[status_at:status_at + 4].view(torch.int32)) == 1
+    monkeypatch.delenv("LOUISKV_STEP_SPIN_LIMIT")
+    # start both engines again from the same state, b with a cleared workspace
+    for e in (a, b):
+        e.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    b.ws_step.zero_()
+    for t in range(steps):
+        a.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        b.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        torch.cuda.synchronize()
+        assert torch.equal(a.n_sel, b.n_sel) and torch.equal(a.sel_units, b.sel_units), t
+        err = (a.out - b.out).abs().max().item()
+        assert err <= 1e-5 * max(1.0, a.out.abs().max().item()), (t, err)
+        assert int(b.ws_step[:status_at + 4].view(torch.int32).abs().sum()) == 0, t
+
+
 @pytest.mark.parametrize("case", ["host-delta", "fused-device"])
 def test_layer_by_layer_step_graphs_match_eager(case):
     """The group-by-group decode captured as one HIP graph per step (as the
