@@ -148,6 +148,49 @@ int main(int argc, char** argv) {
   }
   CHECK_HIP(hipDeviceSynchronize());
 
+  /* the same decode through louiskv_decode_step (boundary, store, retrieval
+     and attention of a step in one call), from a fresh prefill */
+  float* reps2 = zeros((size_t)S * cap * D * 4);
+  int32_t* ustart2 = zeros((size_t)S * cap * 4);
+  int32_t* usize2 = zeros((size_t)S * cap * 4);
+  int32_t* assign2 = zeros((size_t)S * N * 4);
+  int32_t* perm2 = zeros((size_t)S * N * 4);
+  void* kpool2 = zeros((size_t)S * pool_rows * row);
+  void* vpool2 = zeros((size_t)S * pool_rows * row);
+  void* ws2 = zeros(wsb);
+  CHECK_LKV(louiskv_cluster_prefill(keys, LOUISKV_BF16, S, N, D, C, iters, init, reps2, cap, ustart2, usize2,
+                                    assign2, perm2, values, kpool2, vpool2, pool_rows, 0, NULL, ws2, wsb, NULL));
+  void* qref2 = zeros((size_t)G * HQ * row);
+  uint8_t* fire2 = zeros(G);
+  double* r2 = zeros((size_t)G * 8);
+  void* kloc2 = zeros((size_t)S * W * row);
+  void* vloc2 = zeros((size_t)S * W * row);
+  int32_t* sel_units2 = zeros((size_t)S * cap * 4);
+  int32_t* n_sel_units2 = zeros((size_t)S * 4);
+  int32_t* n_sel2 = zeros((size_t)S * 4);
+  int32_t* sel_rows2 = zeros((size_t)S * B * 4);
+  size_t swsb = louiskv_decode_step_workspace_size(S, LOUISKV_BF16, g, cap, B, W);
+  if (swsb == 0) {
+    fprintf(stderr, "louiskv_decode_step_workspace_size returned 0\n");
+    return 1;
+  }
+  void* sws = zeros(swsb);   /* zero before the first call; every call leaves its counters at zero */
+  float* out2 = zeros((size_t)G * HQ * D * 4);
+  float* lse2 = zeros((size_t)G * HQ * 4);
+  float* hout2 = malloc((size_t)T * G * HQ * D * 4);
+  for (int t = 0; t < T; ++t) {
+    CHECK_HIP(hipMemcpy(q, hq + (size_t)t * G * HQ * D, (size_t)G * HQ * row, hipMemcpyHostToDevice));
+    CHECK_HIP(hipMemcpy(knew, hgk + (size_t)t * S * D, (size_t)S * row, hipMemcpyHostToDevice));
+    CHECK_HIP(hipMemcpy(vnew, hgv + (size_t)t * S * D, (size_t)S * row, hipMemcpyHostToDevice));
+    CHECK_LKV(louiskv_decode_step(q, qref2, LOUISKV_BF16, G, HQ, HKV, D, tau, LOUISKV_REF_ANCHOR, t, r2, fire2,
+                                  knew, vnew, kloc2, vloc2, W, seg, reps2, ustart2, usize2, cap, C, kpool2, vpool2,
+                                  pool_rows, N, B, sel_units2, n_sel_units2, n_sel2, sel_rows2, NULL, out2,
+                                  LOUISKV_F32, lse2, sws, swsb, NULL));
+    CHECK_HIP(hipMemcpy(hout2 + (size_t)t * G * HQ * D, out2, (size_t)G * HQ * D * 4, hipMemcpyDeviceToHost));
+  }
+  CHECK_HIP(hipDeviceSynchronize());
+  write_file(dir, "out_attn_step.bin", hout2, (size_t)T * G * HQ * D * 4);
+
   int32_t* hassign = malloc((size_t)S * N * 4);
   float* hreps = malloc((size_t)S * cap * D * 4);
   CHECK_HIP(hipMemcpy(hassign, assign, (size_t)S * N * 4, hipMemcpyDeviceToHost));
@@ -155,6 +198,7 @@ int main(int argc, char** argv) {
   write_file(dir, "out_assign.bin", hassign, (size_t)S * N * 4);
   write_file(dir, "out_reps.bin", hreps, (size_t)S * cap * D * 4);
   write_file(dir, "out_attn.bin", hout, (size_t)T * G * HQ * D * 4);
-  printf("abi_example: %d slices, %d tokens, %d clusters, %d decode steps done\n", S, N, C, T);
+  printf("abi_example: %d slices, %d tokens, %d clusters, %d decode steps done (per-stage calls and "
+         "louiskv_decode_step)\n", S, N, C, T);
   return 0;
 }

@@ -2,7 +2,8 @@
 __graft_entry__.build()): a k-means prefill and a decode loop through
 include/louiskv.h alone give the same assignments, centroids and attention
 outputs, bit for bit, as the same calls through the Python binding, and the
-assignments agree with the oracle."""
+assignments agree with the oracle; a second C loop over
+louiskv_decode_step equals the binding's one-launch step bit for bit."""
 import os
 import subprocess
 import sys
@@ -60,6 +61,18 @@ def test_c_caller_matches_python_binding(tmp_path):
     assert np.array_equal(c_assign, eng.assign.cpu().numpy())
     assert np.array_equal(c_reps, eng.reps.cpu().numpy())
     assert np.array_equal(c_out, torch.stack(outs).cpu().numpy())
+    # the C loop over louiskv_decode_step: the binding's one-launch step bit
+    # for bit, the per-stage calls up to the summation order of the attention
+    c_step = np.frombuffer((tmp_path / "out_attn_step.bin").read_bytes(), dtype=np.float32).reshape(T, G, HQ, 128)
+    eng2 = LouisKVEngine(cfg, torch.bfloat16, DEV, out_dtype=torch.float32, fused_step=True)
+    eng2.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    outs2 = []
+    for t in range(T):
+        eng2.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        outs2.append(eng2.out.clone())
+    torch.cuda.synchronize()
+    assert np.array_equal(c_step, torch.stack(outs2).cpu().numpy())
+    assert np.abs(c_step - c_out).max() <= 1e-5 * max(1.0, float(np.abs(c_out).max()))
     # and the clustering is the oracle's: equal, or a run whose every
     # iteration is an exact argmin and exact means up to excused near-ties
     from paper_2510_11292_amd import louiskv
