@@ -77,7 +77,7 @@ typedef enum louiskv_status {
   LOUISKV_ERR_NULL = 1,           /* a required pointer is NULL */
   LOUISKV_ERR_SHAPE = 2,          /* sizes are inconsistent or out of range */
   LOUISKV_ERR_DTYPE = 3,          /* unknown dtype code */
-  LOUISKV_ERR_UNSUPPORTED = 4,    /* valid request this build does not serve (d != 128 ...) */
+  LOUISKV_ERR_UNSUPPORTED = 4,    /* valid request the library does not serve (d != 128 ...) */
   LOUISKV_ERR_WORKSPACE = 5,      /* workspace NULL or smaller than *_workspace_size() */
   LOUISKV_ERR_HIP = 6             /* HIP runtime or launch failure */
 } louiskv_status;
