@@ -388,6 +388,40 @@ __device__ __forceinline__ void bitonic_in_wave2(uint64_t& v0, uint64_t& v1, int
   v1 = bitonic_step<1>(v1, i1, k);
 }
 
+// A wave's 128 keys (two a lane: element indices lane and 64 + lane) sorted
+// in descending order, in registers.
+__device__ __forceinline__ void sort128_desc(uint64_t& v0, uint64_t& v1, int lane) {
+  const int i0 = lane, i1 = kWave + lane;
+#pragma unroll
+  for (int k = 2; k <= kWave; k <<= 1) bitonic_in_wave2(v0, v1, i0, i1, k, k >> 1);
+  // stage 128, distance 64: the partners are a lane's two keys
+  if (v0 < v1) {
+    const uint64_t t = v0;
+    v0 = v1;
+    v1 = t;
+  }
+  bitonic_in_wave2(v0, v1, i0, i1, 2 * kWave, kWave / 2);
+}
+
+// The 128 largest of two descending 128-key lists (t, v; same layout), in
+// descending order into t: the elementwise maxima of t and v reversed are
+// those keys as a bitonic sequence, which the last stage of the network sorts.
+__device__ __forceinline__ void merge_top128(uint64_t& t0, uint64_t& t1, uint64_t v0, uint64_t v1, int lane) {
+  const int src = kWave - 1 - lane;   // element 127 - i of v sits in lane 63 - i%64, the other register
+  const uint64_t r1 = ((uint64_t)(uint32_t)__shfl((int)(uint32_t)(v1 >> 32), src, kWave) << 32) |
+                      (uint32_t)__shfl((int)(uint32_t)v1, src, kWave);
+  const uint64_t r0 = ((uint64_t)(uint32_t)__shfl((int)(uint32_t)(v0 >> 32), src, kWave) << 32) |
+                      (uint32_t)__shfl((int)(uint32_t)v0, src, kWave);
+  t0 = t0 > r1 ? t0 : r1;
+  t1 = t1 > r0 ? t1 : r0;
+  if (t0 < t1) {
+    const uint64_t t = t0;
+    t0 = t1;
+    t1 = t;
+  }
+  bitonic_in_wave2(t0, t1, lane, kWave + lane, 2 * kWave, kWave / 2);
+}
+
 constexpr int kLogitThreads = 256;
 constexpr int kLogitWaves = kLogitThreads / 64;
 constexpr int kMaxLogitParts = 16;
@@ -567,6 +601,8 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
                                                  int* s_incl) {
   __shared__ double s_rz[G][kSelWaves];
   __shared__ double s_z[G];
+  __shared__ int s_rtok[kSelWaves];
+  __shared__ long long s_tok;
   __shared__ int s_ntake;
   __shared__ int s_wsum[kSelWaves];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -576,11 +612,13 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
   // thread the logits are loaded in one batch and their exponentials stay in
   // registers for pass 3; beyond that they are kept in the logit workspace
   // (recomputed in pass 3 when other blocks wrote them).  Either way each
-  // thread sums its units in increasing order.
+  // thread sums its units in increasing order.  The units' token count is
+  // summed on the way (it decides below which search runs first).
   constexpr int kRegUnits = 4;
   const bool in_regs = n_units <= kRegUnits * kSelThreads;
   double ev[kRegUnits][G];
   double zs[G];
+  int tok = 0;
 #pragma unroll
   for (int j = 0; j < G; ++j) zs[j] = 0.0;
   if (in_regs) {
@@ -593,6 +631,7 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
 #pragma unroll
     for (int i = 0; i < kRegUnits; ++i) {
       if (tid + i * kSelThreads < n_units) {
+        tok += s_size[tid + i * kSelThreads];
 #pragma unroll
         for (int j = 0; j < G; ++j) {
           ev[i][j] = exp(ev[i][j] - s_m[j]);
@@ -602,6 +641,7 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
     }
   } else {
     for (int u = tid; u < n_units; u += kSelThreads) {
+      tok += s_size[u];
 #pragma unroll
       for (int j = 0; j < G; ++j) {
         const double e = exp(load_logit<kShared>(lg + (size_t)u * G + j) - s_m[j]);
@@ -615,11 +655,19 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
     const double z = wave_sum(zs[j]);
     if (lane == 0) s_rz[j][w] = z;
   }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) tok += __shfl_xor(tok, o, kWave);
+  if (lane == 0) s_rtok[w] = tok;
   __syncthreads();
   if (tid < G) {
     double z = 0.0;
     for (int q2 = 0; q2 < kSelWaves; ++q2) z += s_rz[tid][q2];
     s_z[tid] = z;
+  }
+  if (tid == kWave) {
+    long long t = 0;
+    for (int q2 = 0; q2 < kSelWaves; ++q2) t += s_rtok[q2];
+    s_tok = t;
   }
   __syncthreads();
 
@@ -659,232 +707,317 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
   __syncthreads();
 
   // The prefix stop (Section 3.1 budget; units taken in rank order until the
-  // next one does not fit) by radix selection: the boundary unit is the first
-  // one in rank order whose size exceeds what the units ranked above it leave
-  // of the budget.  Keys are distinct, so 8-bit digits from the top narrow
-  // the candidates to the bucket in which the token count of the higher keys
-  // crosses the remaining budget, until that bucket holds one unit; every
-  // unit with a higher key is taken.  Then only the taken units are sorted.
-  // Histograms per pair of waves: a unit adds (size << 16) + 1 to its digit's
-  // entry, so one 64-bit word counts tokens (bits 16..) and units (bits
-  // 0..15; at most kMaxUnits per slice), and LDS atomics conflict only inside
-  // a pair.  Two sets alternate between passes, so a pass clears the other
-  // set while its own is scanned (2 x 4 x 256 words: 16 KiB of LDS).  Leading bytes that every key shares (the sign and
-  // high exponent bits of the scores) are skipped: the search starts at the
-  // first byte where the keys' OR and AND differ.
-  constexpr int kHists = kSelWaves / 2;
-  __shared__ uint64_t s_hist[2][kHists][256];
-  __shared__ uint64_t s_or[kSelWaves], s_and[kSelWaves];
-  __shared__ uint64_t s_prefix, s_thresh;
-  __shared__ int64_t s_rem;
-  __shared__ int s_pbits, s_state, s_nsel_units;   // state: 0 searching, 1 boundary found, 2 every unit fits
-  {
-    uint64_t ko = 0, ka = ~0ull;
-    for (int u = tid; u < n_units; u += kSelThreads) {
-      ko |= s_key[u];
-      ka &= s_key[u];
-    }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      ko |= __shfl_xor(ko, o, kWave);
-      ka &= __shfl_xor(ka, o, kWave);
-    }
-    if (lane == 0) {
-      s_or[w] = ko;
-      s_and[w] = ka;
-    }
-  }
-  for (int i = tid; i < 2 * kHists * 256; i += kSelThreads) (&s_hist[0][0][0])[i] = 0;
-  __syncthreads();
-  if (tid == 0) {
-    uint64_t ko = 0, ka = ~0ull;
-    for (int q2 = 0; q2 < kSelWaves; ++q2) {
-      ko |= s_or[q2];
-      ka &= s_and[q2];
-    }
-    const uint64_t diff = ko ^ ka;          // bits where the keys differ
-    const int lead = diff ? __builtin_clzll(diff) / 8 * 8 : 56;   // whole shared bytes
-    s_pbits = lead;
-    s_prefix = lead ? (ko >> (64 - lead)) : 0;
-    s_rem = budget;
-    s_state = 0;
-    s_nsel_units = 0;
-  }
-  __syncthreads();
-  int set = 0;
-  while (s_state == 0) {
-    const int pbits = s_pbits;
-    const uint64_t prefix = s_prefix;
-    const int shift = 56 - pbits;
-    for (int u = tid; u < n_units; u += kSelThreads) {
-      const uint64_t k = s_key[u];
-      if (pbits == 0 || (k >> (64 - pbits)) == prefix) {
-        const int dg = (int)((k >> shift) & 255u);
-        atomicAdd(reinterpret_cast<unsigned long long*>(&s_hist[set][w % kHists][dg]),
-                  ((unsigned long long)(uint32_t)s_size[key_unit(k)] << 16) + 1ull);
+  // next one does not fit), first over the 128 highest keys: each wave sorts
+  // its 128-key chunks of s_key in registers and keeps the 128 largest keys
+  // it has seen (merge_top128), wave 0 merges the waves' lists, takes their
+  // inclusive size sums and finds where the budget stops the prefix.  If it
+  // stops inside those 128, or every unit fits, that is the selection (the
+  // same units in the same order as the full search below); otherwise the
+  // search below runs.  Tried when the budget holds fewer than kTopTry units
+  // of the mean size, so that it rarely needs the full search after it.
+  constexpr int kTopTry = 96;
+  const int32_t* ustart = unit_start + (size_t)ps * units_cap;
+  int32_t* rows = row_ws + (size_t)s * budget;
+  __shared__ uint64_t s_top[kSelWaves][2 * kWave];
+  __shared__ int s_fast;
+  if (tid == 0) s_fast = 0;
+  if ((long long)budget * n_units < (long long)kTopTry * s_tok) {
+    {
+      uint64_t t0 = 0, t1 = 0;
+      bool have = false;
+      for (int ch = w; ch * 2 * kWave < n_pad; ch += kSelWaves) {
+        const int b = ch * 2 * kWave;
+        uint64_t v0 = b + lane < n_pad ? s_key[b + lane] : 0;
+        uint64_t v1 = b + kWave + lane < n_pad ? s_key[b + kWave + lane] : 0;
+        sort128_desc(v0, v1, lane);
+        if (have) {
+          merge_top128(t0, t1, v0, v1, lane);
+        } else {
+          t0 = v0;
+          t1 = v1;
+          have = true;
+        }
       }
+      s_top[w][lane] = t0;
+      s_top[w][kWave + lane] = t1;
     }
     __syncthreads();
     if (w == 0) {
-      // lane l holds digits 255 - 4l .. 252 - 4l, highest first
-      // (a slice's tokens, hence every sum below, stay under 2^31)
-      int v[4];
-      int cnt[4];
-      int tot = 0;
+      uint64_t t0 = s_top[0][lane], t1 = s_top[0][kWave + lane];
+      for (int q2 = 1; q2 < kSelWaves; ++q2) merge_top128(t0, t1, s_top[q2][lane], s_top[q2][kWave + lane], lane);
+      const int n_real = min(2 * kWave, n_units);   // the list's real keys (the rest are padding zeros)
+      const int i0 = lane, i1 = kWave + lane;
+      const int z0 = i0 < n_real ? s_size[key_unit(t0)] : 0;
+      const int z1 = i1 < n_real ? s_size[key_unit(t1)] : 0;
+      int x0 = z0, x1 = z1;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        uint64_t h = 0;
-#pragma unroll
-        for (int q2 = 0; q2 < kHists; ++q2) h += s_hist[set][q2][255 - 4 * lane - i];
-        v[i] = (int)(h >> 16);
-        cnt[i] = (int)(h & 0xffffu);
-        tot += v[i];
-      }
-      int incl = tot;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(incl, o, kWave);
-        if (lane >= o) incl += y;
-      }
-      int64_t cum = incl - tot;   // tokens of the digits above this lane's
-      const int64_t rem = s_rem;
-      int hit = -1, hit_cnt = 0;
-      int64_t before = 0;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (hit < 0 && cum + v[i] > rem) {
-          hit = 255 - 4 * lane - i;
-          hit_cnt = cnt[i];
-          before = cum;
+      for (int o = 1; o < kWave; o <<= 1) {
+        const int y0 = __shfl_up(x0, o, kWave), y1 = __shfl_up(x1, o, kWave);
+        if (lane >= o) {
+          x0 += y0;
+          x1 += y1;
         }
-        cum += v[i];
       }
-      const uint64_t found = __builtin_amdgcn_ballot_w64(hit >= 0);
-      if (found == 0) {
-        if (lane == 0) s_state = 2;    // the candidates are every unit (first pass) and all fit
-      } else if (lane == (int)__builtin_ctzll(found)) {
-        s_prefix = (prefix << 8) | (uint64_t)hit;
-        s_rem = rem - before;
-        s_pbits = pbits + 8;
-        if (hit_cnt == 1 || pbits + 8 == 64) s_state = 1;
+      const long long inc0 = x0, inc1 = (long long)__shfl(x0, kWave - 1, kWave) + x1;
+      const int ntake = __popcll(__builtin_amdgcn_ballot_w64(i0 < n_real && inc0 <= budget)) +
+                        __popcll(__builtin_amdgcn_ballot_w64(i1 < n_real && inc1 <= budget));
+      // the first unit left out must be a real key (nonzero), or every unit taken
+      const int nb = ntake < kWave ? ntake : ntake - kWave;
+      const uint64_t k0 = ((uint64_t)(uint32_t)__shfl((int)(uint32_t)(t0 >> 32), nb & (kWave - 1), kWave) << 32) |
+                          (uint32_t)__shfl((int)(uint32_t)t0, nb & (kWave - 1), kWave);
+      const uint64_t k1 = ((uint64_t)(uint32_t)__shfl((int)(uint32_t)(t1 >> 32), nb & (kWave - 1), kWave) << 32) |
+                          (uint32_t)__shfl((int)(uint32_t)t1, nb & (kWave - 1), kWave);
+      const uint64_t kb = ntake < kWave ? k0 : k1;
+      const bool fast = ntake < n_real ? kb != 0 : n_real == n_units;
+      if (fast) {
+        if (i0 < ntake) {
+          const int u = key_unit(t0);
+          sel_units[(size_t)s * units_cap + i0] = u;
+          s_key[i0] = ((uint64_t)(uint32_t)ustart[u] << 32) | (uint32_t)z0;
+          s_incl[i0] = inc0 > 0x3fffffff ? 0x3fffffff : (int)inc0;
+        }
+        if (i1 < ntake) {
+          const int u = key_unit(t1);
+          sel_units[(size_t)s * units_cap + i1] = u;
+          s_key[i1] = ((uint64_t)(uint32_t)ustart[u] << 32) | (uint32_t)z1;
+          s_incl[i1] = inc1 > 0x3fffffff ? 0x3fffffff : (int)inc1;
+        }
       }
-    } else {
-      for (int i = tid - 64; i < kHists * 256; i += kSelThreads - 64) (&s_hist[set ^ 1][0][0])[i] = 0;
+      if (lane == 0) {
+        s_fast = fast ? 1 : 0;
+        if (fast) s_ntake = ntake;
+      }
     }
-    set ^= 1;
+  }
+  __syncthreads();
+  if (!s_fast) {
+    // The full search: radix selection.  The boundary unit is the first
+    // one in rank order whose size exceeds what the units ranked above it leave
+    // of the budget.  Keys are distinct, so 8-bit digits from the top narrow
+    // the candidates to the bucket in which the token count of the higher keys
+    // crosses the remaining budget, until that bucket holds one unit; every
+    // unit with a higher key is taken.  Then only the taken units are sorted.
+    // Histograms per pair of waves: a unit adds (size << 16) + 1 to its digit's
+    // entry, so one 64-bit word counts tokens (bits 16..) and units (bits
+    // 0..15; at most kMaxUnits per slice), and LDS atomics conflict only inside
+    // a pair.  Two sets alternate between passes, so a pass clears the other
+    // set while its own is scanned (2 x 4 x 256 words: 16 KiB of LDS).
+    // Leading bytes that every key shares (the sign and high exponent bits of
+    // the scores) are skipped: the search starts at the first byte where the
+    // keys' OR and AND differ.
+    constexpr int kHists = kSelWaves / 2;
+    __shared__ uint64_t s_hist[2][kHists][256];
+    __shared__ uint64_t s_or[kSelWaves], s_and[kSelWaves];
+    __shared__ uint64_t s_prefix, s_thresh;
+    __shared__ int64_t s_rem;
+    __shared__ int s_pbits, s_state, s_nsel_units;   // state: 0 searching, 1 boundary found, 2 every unit fits
+    {
+      uint64_t ko = 0, ka = ~0ull;
+      for (int u = tid; u < n_units; u += kSelThreads) {
+        ko |= s_key[u];
+        ka &= s_key[u];
+      }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        ko |= __shfl_xor(ko, o, kWave);
+        ka &= __shfl_xor(ka, o, kWave);
+      }
+      if (lane == 0) {
+        s_or[w] = ko;
+        s_and[w] = ka;
+      }
+    }
+    for (int i = tid; i < 2 * kHists * 256; i += kSelThreads) (&s_hist[0][0][0])[i] = 0;
     __syncthreads();
-  }
-  if (s_state == 1) {
-    // the boundary unit is the one key under the final prefix
-    const int pb = s_pbits;
-    const uint64_t pf = s_prefix;
-    for (int u = tid; u < n_units; u += kSelThreads) {
-      const uint64_t k = s_key[u];
-      if ((pb == 64 ? k : (k >> (64 - pb))) == pf) s_thresh = k;
+    if (tid == 0) {
+      uint64_t ko = 0, ka = ~0ull;
+      for (int q2 = 0; q2 < kSelWaves; ++q2) {
+        ko |= s_or[q2];
+        ka &= s_and[q2];
+      }
+      const uint64_t diff = ko ^ ka;          // bits where the keys differ
+      const int lead = diff ? __builtin_clzll(diff) / 8 * 8 : 56;   // whole shared bytes
+      s_pbits = lead;
+      s_prefix = lead ? (ko >> (64 - lead)) : 0;
+      s_rem = budget;
+      s_state = 0;
+      s_nsel_units = 0;
     }
-  }
-  __syncthreads();
-  // the taken keys, compacted to the front of s_key and sorted there
-  const bool take_all = s_state == 2;
-  const uint64_t thresh = take_all ? 0 : s_thresh;
-  constexpr int kPerThread = kMaxUnits / kSelThreads;
-  uint64_t mine[kPerThread];
-#pragma unroll
-  for (int i = 0; i < kPerThread; ++i) {
-    const int u = tid + i * kSelThreads;
-    mine[i] = u < n_units ? s_key[u] : 0;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < kPerThread; ++i) {
-    const int u = tid + i * kSelThreads;
-    if (u < n_units && (take_all || mine[i] > thresh)) s_key[atomicAdd(&s_nsel_units, 1)] = mine[i];
-  }
-  __syncthreads();
-  const int n_taken = s_nsel_units;
-  n_pad = 64;
-  while (n_pad < n_taken) n_pad <<= 1;
-  for (int i = n_taken + tid; i < n_pad; i += kSelThreads) s_key[i] = 0;   // padding ranks last
-  __syncthreads();
-
-  // bitonic sort, descending keys (n_pad >= 64)
-  // (chunks c and c + kSelWaves of a wave go together; a missing second
-  // chunk is a copy of the first, sorted and dropped)
-  const int n_chunk = n_pad / 64;
-  for (int c = w; c < n_chunk; c += 2 * kSelWaves) {
-    const int c1 = c + kSelWaves < n_chunk ? c + kSelWaves : c;
-    const int i0 = 64 * c + lane, i1 = 64 * c1 + lane;
-    uint64_t v0 = s_key[i0], v1 = s_key[i1];
-#pragma unroll
-    for (int k = 2; k <= 64; k <<= 1) bitonic_in_wave2(v0, v1, i0, i1, k, k >> 1);
-    s_key[i0] = v0;
-    if (c1 != c) s_key[i1] = v1;
-  }
-  __syncthreads();
-  for (int k = 128; k <= n_pad; k <<= 1) {
-    for (int jj = k >> 1; jj >= 64; jj >>= 1) {
-      // pair t: i has a zero at bit jj, its partner p = i + jj
-      for (int t = tid; t < n_pad / 2; t += kSelThreads) {
-        const int i = ((t & ~(jj - 1)) << 1) | (t & (jj - 1));
-        const int p = i | jj;
-        const uint64_t a = s_key[i], b = s_key[p];
-        const bool desc = (i & k) == 0;
-        if (desc ? a < b : a > b) {
-          s_key[i] = b;
-          s_key[p] = a;
+    __syncthreads();
+    int set = 0;
+    while (s_state == 0) {
+      const int pbits = s_pbits;
+      const uint64_t prefix = s_prefix;
+      const int shift = 56 - pbits;
+      for (int u = tid; u < n_units; u += kSelThreads) {
+        const uint64_t k = s_key[u];
+        if (pbits == 0 || (k >> (64 - pbits)) == prefix) {
+          const int dg = (int)((k >> shift) & 255u);
+          atomicAdd(reinterpret_cast<unsigned long long*>(&s_hist[set][w % kHists][dg]),
+                    ((unsigned long long)(uint32_t)s_size[key_unit(k)] << 16) + 1ull);
         }
       }
       __syncthreads();
+      if (w == 0) {
+        // lane l holds digits 255 - 4l .. 252 - 4l, highest first
+        // (a slice's tokens, hence every sum below, stay under 2^31)
+        int v[4];
+        int cnt[4];
+        int tot = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          uint64_t h = 0;
+#pragma unroll
+          for (int q2 = 0; q2 < kHists; ++q2) h += s_hist[set][q2][255 - 4 * lane - i];
+          v[i] = (int)(h >> 16);
+          cnt[i] = (int)(h & 0xffffu);
+          tot += v[i];
+        }
+        int incl = tot;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(incl, o, kWave);
+          if (lane >= o) incl += y;
+        }
+        int64_t cum = incl - tot;   // tokens of the digits above this lane's
+        const int64_t rem = s_rem;
+        int hit = -1, hit_cnt = 0;
+        int64_t before = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (hit < 0 && cum + v[i] > rem) {
+            hit = 255 - 4 * lane - i;
+            hit_cnt = cnt[i];
+            before = cum;
+          }
+          cum += v[i];
+        }
+        const uint64_t found = __builtin_amdgcn_ballot_w64(hit >= 0);
+        if (found == 0) {
+          if (lane == 0) s_state = 2;    // the candidates are every unit (first pass) and all fit
+        } else if (lane == (int)__builtin_ctzll(found)) {
+          s_prefix = (prefix << 8) | (uint64_t)hit;
+          s_rem = rem - before;
+          s_pbits = pbits + 8;
+          if (hit_cnt == 1 || pbits + 8 == 64) s_state = 1;
+        }
+      } else {
+        for (int i = tid - 64; i < kHists * 256; i += kSelThreads - 64) (&s_hist[set ^ 1][0][0])[i] = 0;
+      }
+      set ^= 1;
+      __syncthreads();
     }
+    if (s_state == 1) {
+      // the boundary unit is the one key under the final prefix
+      const int pb = s_pbits;
+      const uint64_t pf = s_prefix;
+      for (int u = tid; u < n_units; u += kSelThreads) {
+        const uint64_t k = s_key[u];
+        if ((pb == 64 ? k : (k >> (64 - pb))) == pf) s_thresh = k;
+      }
+    }
+    __syncthreads();
+    // the taken keys, compacted to the front of s_key and sorted there
+    const bool take_all = s_state == 2;
+    const uint64_t thresh = take_all ? 0 : s_thresh;
+    constexpr int kPerThread = kMaxUnits / kSelThreads;
+    uint64_t mine[kPerThread];
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) {
+      const int u = tid + i * kSelThreads;
+      mine[i] = u < n_units ? s_key[u] : 0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) {
+      const int u = tid + i * kSelThreads;
+      if (u < n_units && (take_all || mine[i] > thresh)) s_key[atomicAdd(&s_nsel_units, 1)] = mine[i];
+    }
+    __syncthreads();
+    const int n_taken = s_nsel_units;
+    n_pad = 64;
+    while (n_pad < n_taken) n_pad <<= 1;
+    for (int i = n_taken + tid; i < n_pad; i += kSelThreads) s_key[i] = 0;   // padding ranks last
+    __syncthreads();
+
+    // bitonic sort, descending keys (n_pad >= 64)
+    // (chunks c and c + kSelWaves of a wave go together; a missing second
+    // chunk is a copy of the first, sorted and dropped)
+    const int n_chunk = n_pad / 64;
     for (int c = w; c < n_chunk; c += 2 * kSelWaves) {
       const int c1 = c + kSelWaves < n_chunk ? c + kSelWaves : c;
       const int i0 = 64 * c + lane, i1 = 64 * c1 + lane;
       uint64_t v0 = s_key[i0], v1 = s_key[i1];
-      bitonic_in_wave2(v0, v1, i0, i1, k, 32);
+#pragma unroll
+      for (int k = 2; k <= 64; k <<= 1) bitonic_in_wave2(v0, v1, i0, i1, k, k >> 1);
       s_key[i0] = v0;
       if (c1 != c) s_key[i1] = v1;
     }
     __syncthreads();
-  }
+    for (int k = 128; k <= n_pad; k <<= 1) {
+      for (int jj = k >> 1; jj >= 64; jj >>= 1) {
+        // pair t: i has a zero at bit jj, its partner p = i + jj
+        for (int t = tid; t < n_pad / 2; t += kSelThreads) {
+          const int i = ((t & ~(jj - 1)) << 1) | (t & (jj - 1));
+          const int p = i | jj;
+          const uint64_t a = s_key[i], b = s_key[p];
+          const bool desc = (i & k) == 0;
+          if (desc ? a < b : a > b) {
+            s_key[i] = b;
+            s_key[p] = a;
+          }
+        }
+        __syncthreads();
+      }
+      for (int c = w; c < n_chunk; c += 2 * kSelWaves) {
+        const int c1 = c + kSelWaves < n_chunk ? c + kSelWaves : c;
+        const int i0 = 64 * c + lane, i1 = 64 * c1 + lane;
+        uint64_t v0 = s_key[i0], v1 = s_key[i1];
+        bitonic_in_wave2(v0, v1, i0, i1, k, 32);
+        s_key[i0] = v0;
+        if (c1 != c) s_key[i1] = v1;
+      }
+      __syncthreads();
+    }
 
-  // inclusive size sums in rank order (all within the budget by construction)
-  if (tid == 0) s_ntake = 0;
-  int carry = 0;
-  for (int base = 0; base < n_taken; base += kSelThreads) {
-    const int p = base + tid;
-    const int v = p < n_taken ? s_size[key_unit(s_key[p])] : 0;
-    int x = v;
+    // inclusive size sums in rank order (all within the budget by construction)
+    if (tid == 0) s_ntake = 0;
+    int carry = 0;
+    for (int base = 0; base < n_taken; base += kSelThreads) {
+      const int p = base + tid;
+      const int v = p < n_taken ? s_size[key_unit(s_key[p])] : 0;
+      int x = v;
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(x, o, kWave);
-      if (lane >= o) x += y;
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o, kWave);
+        if (lane >= o) x += y;
+      }
+      if (lane == 63) s_wsum[w] = x;
+      __syncthreads();
+      int wp = 0;
+      for (int q2 = 0; q2 < w; ++q2) wp += s_wsum[q2];
+      const long long inc = (long long)carry + wp + x;
+      if (p < n_taken) {
+        s_incl[p] = inc > 0x3fffffff ? 0x3fffffff : (int)inc;   // sums past the budget are never read
+        if (inc <= budget) atomicAdd(&s_ntake, 1);
+      }
+      int tot = 0;
+      for (int q2 = 0; q2 < kSelWaves; ++q2) tot += s_wsum[q2];
+      carry = (int)std::min<long long>((long long)carry + tot, 0x3fffffff);
+      __syncthreads();
     }
-    if (lane == 63) s_wsum[w] = x;
-    __syncthreads();
-    int wp = 0;
-    for (int q2 = 0; q2 < w; ++q2) wp += s_wsum[q2];
-    const long long inc = (long long)carry + wp + x;
-    if (p < n_taken) {
-      s_incl[p] = inc > 0x3fffffff ? 0x3fffffff : (int)inc;   // sums past the budget are never read
-      if (inc <= budget) atomicAdd(&s_ntake, 1);
+    // the unit list in rank order; each rank's key slot then holds its unit's
+    // first pool row and size (the starts loaded together, one per thread)
+    const int ntake_full = s_ntake;
+    for (int p = tid; p < ntake_full; p += kSelThreads) {
+      const int u = key_unit(s_key[p]);
+      sel_units[(size_t)s * units_cap + p] = u;
+      s_key[p] = ((uint64_t)(uint32_t)ustart[u] << 32) | (uint32_t)s_size[u];
     }
-    int tot = 0;
-    for (int q2 = 0; q2 < kSelWaves; ++q2) tot += s_wsum[q2];
-    carry = (int)std::min<long long>((long long)carry + tot, 0x3fffffff);
-    __syncthreads();
-  }
-  const int ntake = s_ntake;
-  const int nsel = ntake > 0 ? s_incl[ntake - 1] : 0;
-  const int32_t* ustart = unit_start + (size_t)ps * units_cap;
-  int32_t* rows = row_ws + (size_t)s * budget;
-  // the unit list in rank order; each rank's key slot then holds its unit's
-  // first pool row and size (the starts loaded together, one per thread)
-  for (int p = tid; p < ntake; p += kSelThreads) {
-    const int u = key_unit(s_key[p]);
-    sel_units[(size_t)s * units_cap + p] = u;
-    s_key[p] = ((uint64_t)(uint32_t)ustart[u] << 32) | (uint32_t)s_size[u];
   }
   __syncthreads();
+  const int ntake = s_ntake;
+  const int nsel = ntake > 0 ? s_incl[ntake - 1] : 0;
   // one wave per selected unit: its rows in order
   for (int p = w; p < ntake; p += kSelWaves) {
     const uint64_t e = s_key[p];
