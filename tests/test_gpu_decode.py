@@ -261,6 +261,48 @@ def test_retrieve_rows(dtype, G, H, g, U, B, maxsz):
         assert to_np(sel_rows[s, :len(idx)]).tolist() == idx
 
 
+@pytest.mark.parametrize("n_small", [200, 100])
+def test_retrieve_rows_after_the_top_keys(n_small):
+    """The selection's first search takes the 128 highest keys: with the
+    best-scored n_small units one token each and the rest 100 (the budget
+    holds about 25 units of the mean size, so that search runs) the 128 best
+    all fit, so the full search decides (n_small = 200: 200 small units and
+    18 large ones), or the prefix stops past them (n_small = 100: the budget
+    stop falls inside the 128 at the 119th unit); either way the selection is
+    the oracle's."""
+    L = _L()
+    G, H, g, U, B = 1, 8, 4, 1024, 2000
+    S = G * H
+    gen = _gen(U + B + n_small)
+    q = torch.randn(G, H * g, 128, generator=gen, device=DEV).mul(2).to(torch.bfloat16)
+    reps = torch.randn(S, U, 128, generator=gen, device=DEV)
+    q64, r64 = to64(q), to64(reps)
+    sizes = torch.full((S, U), 100, dtype=torch.int32)
+    scores = []
+    for s in range(S):
+        a = oracle.group_scores(q64[0, s * g:(s + 1) * g], r64[s], 1 / np.sqrt(128))
+        scores.append(a)
+        sizes[s, torch.from_numpy(np.argsort(-a, kind="stable")[:n_small].copy())] = 1
+    sizes = sizes.to(DEV)
+    starts = torch.zeros_like(sizes)
+    starts[:, 1:] = torch.cumsum(sizes, 1)[:, :-1].to(torch.int32)
+    sel_rows = torch.full((S, B), -7, dtype=torch.int32, device=DEV)
+    sel = torch.full((S, U), -1, dtype=torch.int32, device=DEV)
+    nsu = torch.full((S,), -1, dtype=torch.int32, device=DEV)
+    nsel = torch.full((S,), -1, dtype=torch.int32, device=DEV)
+    fire = torch.ones(G, dtype=torch.uint8, device=DEV)
+    L.retrieve_rows(q, H, reps, starts, sizes, U, B, sel, nsu, nsel, sel_rows, fire=fire)
+    torch.cuda.synchronize()
+    sz, st = to_np(sizes), to_np(starts)
+    for s in range(S):
+        got = to_np(sel[s, :int(nsu[s])]).tolist()
+        selection_matches(scores[s], sz[s], B, got)
+        assert len(got) == (218 if n_small == 200 else 119), (s, len(got))
+        idx = [r for u in got for r in range(int(st[s, u]), int(st[s, u] + sz[s, u]))]
+        assert int(nsel[s]) == len(idx) <= B
+        assert to_np(sel_rows[s, :len(idx)]).tolist() == idx
+
+
 ROWS_ATTN_CASES = [
     # (dtype, out dtype, n_groups, n_kv, g, budget, pool rows, window, n_local, local_start)
     (torch.bfloat16, torch.float32, 32, 8, 4, 2048, 6000, 128, 128, 17),   # one block per slice
