@@ -324,6 +324,11 @@ __global__ void seg_state_init_kernel(int32_t* __restrict__ state, int64_t n_sli
 #endif
 constexpr int kSelThreads = LKV_SEL_THREADS;
 constexpr int kSelWaves = kSelThreads / 64;
+// The selection's score sums are taken as kSumThreads threads would take
+// them, for every block size that divides it (see select_after_max).
+constexpr int kSumThreads = 512;
+constexpr int kSmallSelThreads = 256;   // retrieval blocks when slices outnumber compute units
+static_assert(kSumThreads % kSelThreads == 0, "the block size must divide the summation width");
 constexpr int kUnitIdBits = 13;       // kMaxUnits = 2^13
 
 // Sort key of a unit: larger is ranked first.  The score (a non-negative
@@ -581,7 +586,7 @@ __device__ __forceinline__ double load_logit(const double* p) {
 
 // The selection of one fired slice once its logits l_ju (lg, [unit][G]) and
 // their per-head maxima M_j (s_m) are known, with the unit sizes in s_size:
-//  pass 2  e_ju = exp(l_ju - M_j) and Z_j = sum_u e_ju (kSelThreads threads);
+//  pass 2  e_ju = exp(l_ju - M_j) and Z_j = sum_u e_ju (the block's threads);
 //  pass 3  A_u = (1/g) sum_j e_ju / Z_j and the sort keys;
 //  sort    64-key chunks in registers for merge distances below 64 (no
 //          barrier), LDS steps with a barrier for the longer ones;
@@ -591,7 +596,7 @@ __device__ __forceinline__ double load_logit(const double* p) {
 //  instead of written back (the results are the same, bit for bit).
 //  kPublish: the row list and its length are read by other blocks of the
 //  launch, so they are written with device-scope stores.
-template <int G, bool kShared, bool kPublish = false>
+template <int G, bool kShared, bool kPublish = false, int NT = kSelThreads>
 __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const double* s_m, int n_units, int n_pad,
                                                  int64_t s, int64_t ps, int units_cap, int budget,
                                                  const int32_t* __restrict__ unit_start,
@@ -599,74 +604,92 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
                                                  int32_t* __restrict__ n_sel, int32_t* __restrict__ row_ws,
                                                  double* __restrict__ scores_out, uint64_t* s_key, int* s_size,
                                                  int* s_incl) {
-  __shared__ double s_rz[G][kSelWaves];
+  constexpr int NW = NT / 64;
+  static_assert(kSumThreads % NT == 0 && NT >= 128, "block size");
+  __shared__ double s_rz[G][kSumThreads / 64];
   __shared__ double s_z[G];
-  __shared__ int s_rtok[kSelWaves];
+  __shared__ int s_rtok[NW];
   __shared__ long long s_tok;
   __shared__ int s_ntake;
-  __shared__ int s_wsum[kSelWaves];
+  __shared__ int s_wsum[NW];
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  // pass 2: exponentials and their sums per head.  Up to kRegUnits units per
-  // thread the logits are loaded in one batch and their exponentials stay in
-  // registers for pass 3; beyond that they are kept in the logit workspace
-  // (recomputed in pass 3 when other blocks wrote them).  Either way each
-  // thread sums its units in increasing order.  The units' token count is
-  // summed on the way (it decides below which search runs first).
+  // pass 2: exponentials and their sums per head.  The sums are taken as
+  // kSumThreads threads would take them, whatever the block size: virtual
+  // thread v sums the units v, v + kSumThreads, .. in increasing order, then
+  // each virtual wave is summed over its lanes and the virtual waves in
+  // order; a thread runs the virtual threads tid + k * NT (k < NV), so the
+  // scores are the same bit for bit for every block size.  Up to kRegUnits
+  // units per thread the logits are loaded in one batch and their
+  // exponentials stay in registers for pass 3; beyond that they are kept in
+  // the logit workspace (recomputed in pass 3 when other blocks wrote them).
+  // The units' token count is summed on the way (it decides below which
+  // search runs first).
   constexpr int kRegUnits = 4;
-  const bool in_regs = n_units <= kRegUnits * kSelThreads;
+  constexpr int NV = kSumThreads / NT;   // virtual threads per thread
+  constexpr int RV = kRegUnits / NV;     // register units per virtual thread
+  static_assert(RV * NV == kRegUnits, "register units");
+  const bool in_regs = n_units <= RV * kSumThreads;
   double ev[kRegUnits][G];
-  double zs[G];
+  double zs[NV][G];
   int tok = 0;
 #pragma unroll
-  for (int j = 0; j < G; ++j) zs[j] = 0.0;
+  for (int k = 0; k < NV; ++k)
+#pragma unroll
+    for (int j = 0; j < G; ++j) zs[k][j] = 0.0;
   if (in_regs) {
 #pragma unroll
-    for (int i = 0; i < kRegUnits; ++i) {
-      const int u = tid + i * kSelThreads;
+    for (int r = 0; r < kRegUnits; ++r) {
+      const int u = tid + (r / RV) * NT + (r % RV) * kSumThreads;
 #pragma unroll
-      for (int j = 0; j < G; ++j) ev[i][j] = u < n_units ? load_logit<kShared>(lg + (size_t)u * G + j) : 0.0;
+      for (int j = 0; j < G; ++j) ev[r][j] = u < n_units ? load_logit<kShared>(lg + (size_t)u * G + j) : 0.0;
     }
 #pragma unroll
-    for (int i = 0; i < kRegUnits; ++i) {
-      if (tid + i * kSelThreads < n_units) {
-        tok += s_size[tid + i * kSelThreads];
+    for (int r = 0; r < kRegUnits; ++r) {
+      const int u = tid + (r / RV) * NT + (r % RV) * kSumThreads;
+      if (u < n_units) {
+        tok += s_size[u];
 #pragma unroll
         for (int j = 0; j < G; ++j) {
-          ev[i][j] = exp(ev[i][j] - s_m[j]);
-          zs[j] += ev[i][j];
+          ev[r][j] = exp(ev[r][j] - s_m[j]);
+          zs[r / RV][j] += ev[r][j];
         }
       }
     }
   } else {
-    for (int u = tid; u < n_units; u += kSelThreads) {
-      tok += s_size[u];
 #pragma unroll
-      for (int j = 0; j < G; ++j) {
-        const double e = exp(load_logit<kShared>(lg + (size_t)u * G + j) - s_m[j]);
-        if (!kShared) lg[(size_t)u * G + j] = e;
-        zs[j] += e;
+    for (int k = 0; k < NV; ++k) {
+      for (int u = tid + k * NT; u < n_units; u += kSumThreads) {
+        tok += s_size[u];
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+          const double e = exp(load_logit<kShared>(lg + (size_t)u * G + j) - s_m[j]);
+          if (!kShared) lg[(size_t)u * G + j] = e;
+          zs[k][j] += e;
+        }
       }
     }
   }
 #pragma unroll
-  for (int j = 0; j < G; ++j) {
-    const double z = wave_sum(zs[j]);
-    if (lane == 0) s_rz[j][w] = z;
-  }
+  for (int k = 0; k < NV; ++k)
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      const double z = wave_sum(zs[k][j]);
+      if (lane == 0) s_rz[j][w + k * NW] = z;
+    }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) tok += __shfl_xor(tok, o, kWave);
   if (lane == 0) s_rtok[w] = tok;
   __syncthreads();
   if (tid < G) {
     double z = 0.0;
-    for (int q2 = 0; q2 < kSelWaves; ++q2) z += s_rz[tid][q2];
+    for (int q2 = 0; q2 < kSumThreads / 64; ++q2) z += s_rz[tid][q2];
     s_z[tid] = z;
   }
   if (tid == kWave) {
     long long t = 0;
-    for (int q2 = 0; q2 < kSelWaves; ++q2) t += s_rtok[q2];
+    for (int q2 = 0; q2 < NW; ++q2) t += s_rtok[q2];
     s_tok = t;
   }
   __syncthreads();
@@ -674,14 +697,14 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
   // pass 3: averaged probabilities and sort keys (padding keys 0 rank last)
   if (in_regs) {
 #pragma unroll
-    for (int i = 0; i < kRegUnits; ++i) {
-      const int u = tid + i * kSelThreads;
+    for (int r = 0; r < kRegUnits; ++r) {
+      const int u = tid + (r / RV) * NT + (r % RV) * kSumThreads;
       if (u < n_pad) {
         uint64_t key = 0;
         if (u < n_units) {
           double a = 0.0;
 #pragma unroll
-          for (int j = 0; j < G; ++j) a += ev[i][j] / s_z[j];
+          for (int j = 0; j < G; ++j) a += ev[r][j] / s_z[j];
           a /= (double)G;
           key = unit_key(a, u);
           if (scores_out) scores_out[(size_t)s * units_cap + u] = a;
@@ -690,7 +713,7 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
       }
     }
   } else {
-    for (int u = tid; u < n_pad; u += kSelThreads) {
+    for (int u = tid; u < n_pad; u += NT) {
       uint64_t key = 0;
       if (u < n_units) {
         double a = 0.0;
@@ -718,14 +741,14 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
   constexpr int kTopTry = 96;
   const int32_t* ustart = unit_start + (size_t)ps * units_cap;
   int32_t* rows = row_ws + (size_t)s * budget;
-  __shared__ uint64_t s_top[kSelWaves][2 * kWave];
+  __shared__ uint64_t s_top[NW][2 * kWave];
   __shared__ int s_fast;
   if (tid == 0) s_fast = 0;
   if ((long long)budget * n_units < (long long)kTopTry * s_tok) {
     {
       uint64_t t0 = 0, t1 = 0;
       bool have = false;
-      for (int ch = w; ch * 2 * kWave < n_pad; ch += kSelWaves) {
+      for (int ch = w; ch * 2 * kWave < n_pad; ch += NW) {
         const int b = ch * 2 * kWave;
         uint64_t v0 = b + lane < n_pad ? s_key[b + lane] : 0;
         uint64_t v1 = b + kWave + lane < n_pad ? s_key[b + kWave + lane] : 0;
@@ -744,7 +767,7 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
     __syncthreads();
     if (w == 0) {
       uint64_t t0 = s_top[0][lane], t1 = s_top[0][kWave + lane];
-      for (int q2 = 1; q2 < kSelWaves; ++q2) merge_top128(t0, t1, s_top[q2][lane], s_top[q2][kWave + lane], lane);
+      for (int q2 = 1; q2 < NW; ++q2) merge_top128(t0, t1, s_top[q2][lane], s_top[q2][kWave + lane], lane);
       const int n_real = min(2 * kWave, n_units);   // the list's real keys (the rest are padding zeros)
       const int i0 = lane, i1 = kWave + lane;
       const int z0 = i0 < n_real ? s_size[key_unit(t0)] : 0;
@@ -805,15 +828,15 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
     // Leading bytes that every key shares (the sign and high exponent bits of
     // the scores) are skipped: the search starts at the first byte where the
     // keys' OR and AND differ.
-    constexpr int kHists = kSelWaves / 2;
+    constexpr int kHists = NW / 2;
     __shared__ uint64_t s_hist[2][kHists][256];
-    __shared__ uint64_t s_or[kSelWaves], s_and[kSelWaves];
+    __shared__ uint64_t s_or[NW], s_and[NW];
     __shared__ uint64_t s_prefix, s_thresh;
     __shared__ int64_t s_rem;
     __shared__ int s_pbits, s_state, s_nsel_units;   // state: 0 searching, 1 boundary found, 2 every unit fits
     {
       uint64_t ko = 0, ka = ~0ull;
-      for (int u = tid; u < n_units; u += kSelThreads) {
+      for (int u = tid; u < n_units; u += NT) {
         ko |= s_key[u];
         ka &= s_key[u];
       }
@@ -827,11 +850,11 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
         s_and[w] = ka;
       }
     }
-    for (int i = tid; i < 2 * kHists * 256; i += kSelThreads) (&s_hist[0][0][0])[i] = 0;
+    for (int i = tid; i < 2 * kHists * 256; i += NT) (&s_hist[0][0][0])[i] = 0;
     __syncthreads();
     if (tid == 0) {
       uint64_t ko = 0, ka = ~0ull;
-      for (int q2 = 0; q2 < kSelWaves; ++q2) {
+      for (int q2 = 0; q2 < NW; ++q2) {
         ko |= s_or[q2];
         ka &= s_and[q2];
       }
@@ -849,7 +872,7 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
       const int pbits = s_pbits;
       const uint64_t prefix = s_prefix;
       const int shift = 56 - pbits;
-      for (int u = tid; u < n_units; u += kSelThreads) {
+      for (int u = tid; u < n_units; u += NT) {
         const uint64_t k = s_key[u];
         if (pbits == 0 || (k >> (64 - pbits)) == prefix) {
           const int dg = (int)((k >> shift) & 255u);
@@ -902,7 +925,7 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
           if (hit_cnt == 1 || pbits + 8 == 64) s_state = 1;
         }
       } else {
-        for (int i = tid - 64; i < kHists * 256; i += kSelThreads - 64) (&s_hist[set ^ 1][0][0])[i] = 0;
+        for (int i = tid - 64; i < kHists * 256; i += NT - 64) (&s_hist[set ^ 1][0][0])[i] = 0;
       }
       set ^= 1;
       __syncthreads();
@@ -911,7 +934,7 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
       // the boundary unit is the one key under the final prefix
       const int pb = s_pbits;
       const uint64_t pf = s_prefix;
-      for (int u = tid; u < n_units; u += kSelThreads) {
+      for (int u = tid; u < n_units; u += NT) {
         const uint64_t k = s_key[u];
         if ((pb == 64 ? k : (k >> (64 - pb))) == pf) s_thresh = k;
       }
@@ -920,32 +943,32 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
     // the taken keys, compacted to the front of s_key and sorted there
     const bool take_all = s_state == 2;
     const uint64_t thresh = take_all ? 0 : s_thresh;
-    constexpr int kPerThread = kMaxUnits / kSelThreads;
+    constexpr int kPerThread = kMaxUnits / NT;
     uint64_t mine[kPerThread];
 #pragma unroll
     for (int i = 0; i < kPerThread; ++i) {
-      const int u = tid + i * kSelThreads;
+      const int u = tid + i * NT;
       mine[i] = u < n_units ? s_key[u] : 0;
     }
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < kPerThread; ++i) {
-      const int u = tid + i * kSelThreads;
+      const int u = tid + i * NT;
       if (u < n_units && (take_all || mine[i] > thresh)) s_key[atomicAdd(&s_nsel_units, 1)] = mine[i];
     }
     __syncthreads();
     const int n_taken = s_nsel_units;
     n_pad = 64;
     while (n_pad < n_taken) n_pad <<= 1;
-    for (int i = n_taken + tid; i < n_pad; i += kSelThreads) s_key[i] = 0;   // padding ranks last
+    for (int i = n_taken + tid; i < n_pad; i += NT) s_key[i] = 0;   // padding ranks last
     __syncthreads();
 
     // bitonic sort, descending keys (n_pad >= 64)
-    // (chunks c and c + kSelWaves of a wave go together; a missing second
+    // (chunks c and c + NW of a wave go together; a missing second
     // chunk is a copy of the first, sorted and dropped)
     const int n_chunk = n_pad / 64;
-    for (int c = w; c < n_chunk; c += 2 * kSelWaves) {
-      const int c1 = c + kSelWaves < n_chunk ? c + kSelWaves : c;
+    for (int c = w; c < n_chunk; c += 2 * NW) {
+      const int c1 = c + NW < n_chunk ? c + NW : c;
       const int i0 = 64 * c + lane, i1 = 64 * c1 + lane;
       uint64_t v0 = s_key[i0], v1 = s_key[i1];
 #pragma unroll
@@ -957,7 +980,7 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
     for (int k = 128; k <= n_pad; k <<= 1) {
       for (int jj = k >> 1; jj >= 64; jj >>= 1) {
         // pair t: i has a zero at bit jj, its partner p = i + jj
-        for (int t = tid; t < n_pad / 2; t += kSelThreads) {
+        for (int t = tid; t < n_pad / 2; t += NT) {
           const int i = ((t & ~(jj - 1)) << 1) | (t & (jj - 1));
           const int p = i | jj;
           const uint64_t a = s_key[i], b = s_key[p];
@@ -969,8 +992,8 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
         }
         __syncthreads();
       }
-      for (int c = w; c < n_chunk; c += 2 * kSelWaves) {
-        const int c1 = c + kSelWaves < n_chunk ? c + kSelWaves : c;
+      for (int c = w; c < n_chunk; c += 2 * NW) {
+        const int c1 = c + NW < n_chunk ? c + NW : c;
         const int i0 = 64 * c + lane, i1 = 64 * c1 + lane;
         uint64_t v0 = s_key[i0], v1 = s_key[i1];
         bitonic_in_wave2(v0, v1, i0, i1, k, 32);
@@ -983,7 +1006,7 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
     // inclusive size sums in rank order (all within the budget by construction)
     if (tid == 0) s_ntake = 0;
     int carry = 0;
-    for (int base = 0; base < n_taken; base += kSelThreads) {
+    for (int base = 0; base < n_taken; base += NT) {
       const int p = base + tid;
       const int v = p < n_taken ? s_size[key_unit(s_key[p])] : 0;
       int x = v;
@@ -1002,14 +1025,14 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
         if (inc <= budget) atomicAdd(&s_ntake, 1);
       }
       int tot = 0;
-      for (int q2 = 0; q2 < kSelWaves; ++q2) tot += s_wsum[q2];
+      for (int q2 = 0; q2 < NW; ++q2) tot += s_wsum[q2];
       carry = (int)std::min<long long>((long long)carry + tot, 0x3fffffff);
       __syncthreads();
     }
     // the unit list in rank order; each rank's key slot then holds its unit's
     // first pool row and size (the starts loaded together, one per thread)
     const int ntake_full = s_ntake;
-    for (int p = tid; p < ntake_full; p += kSelThreads) {
+    for (int p = tid; p < ntake_full; p += NT) {
       const int u = key_unit(s_key[p]);
       sel_units[(size_t)s * units_cap + p] = u;
       s_key[p] = ((uint64_t)(uint32_t)ustart[u] << 32) | (uint32_t)s_size[u];
@@ -1019,7 +1042,7 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
   const int ntake = s_ntake;
   const int nsel = ntake > 0 ? s_incl[ntake - 1] : 0;
   // one wave per selected unit: its rows in order
-  for (int p = w; p < ntake; p += kSelWaves) {
+  for (int p = w; p < ntake; p += NW) {
     const uint64_t e = s_key[p];
     const int sz = (int)(uint32_t)e;
     const int st0 = (int)(uint32_t)(e >> 32);
@@ -1052,8 +1075,8 @@ __device__ __forceinline__ void select_after_max(double* __restrict__ lg, const 
 //  pass 3  A_u = (1/g) sum_j e_ju / Z_j and the sort keys.
 //  sort    64-key chunks in registers for merge distances below 64 (no
 //          barrier), LDS steps with a barrier for the longer ones.
-template <class T, int G>
-__global__ __launch_bounds__(kSelThreads)
+template <class T, int G, int NT>
+__global__ __launch_bounds__(NT)
 void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, const float* __restrict__ reps,
                          const int32_t* __restrict__ unit_start, const int32_t* __restrict__ unit_size,
                          int units_cap, int n_units_arg, int budget, const uint8_t* __restrict__ fire,
@@ -1065,7 +1088,8 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
   uint64_t* s_key = reinterpret_cast<uint64_t*>(smem);            // [n_pad_arg]
   int* s_size = reinterpret_cast<int*>(s_key + n_pad_arg);        // [n_pad_arg] unit sizes by unit id
   int* s_incl = s_size + n_pad_arg;                                // [n_pad_arg] inclusive size sums by rank
-  __shared__ double s_rm[G][kSelWaves];
+  constexpr int NW = NT / 64;
+  __shared__ double s_rm[G][NW];
   __shared__ double s_m[G];
 
   const int64_t s = blockIdx.x;
@@ -1085,7 +1109,7 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int32_t* us = unit_size + (size_t)ps * units_cap;
-  for (int u = tid; u < n_units; u += kSelThreads) s_size[u] = max(us[u], 0);
+  for (int u = tid; u < n_units; u += NT) s_size[u] = max(us[u], 0);
 
   // pass 1: maxima of the logits, computed here (own_logits: many slices,
   // one block each) or read back from unit_logits_kernel (few slices)
@@ -1099,10 +1123,10 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
     double qd[G][LogitLayout<G>::kDims];
     load_q_f64<G>(q, (size_t)grp * n_q_heads + (size_t)kvh * G, lane, qd);
     const float* rs = reps + (size_t)ps * units_cap * kHeadDim;
-    for (int u0 = w * kLogitUnitsPerIter; u0 < n_units; u0 += kSelWaves * kLogitUnitsPerIter)
+    for (int u0 = w * kLogitUnitsPerIter; u0 < n_units; u0 += NW * kLogitUnitsPerIter)
       wave_unit_logits<G, false>(qd, rs, u0, n_units, scale, lg, mx, lane);
   } else {
-    for (int u = tid; u < n_units; u += kSelThreads) {
+    for (int u = tid; u < n_units; u += NT) {
 #pragma unroll
       for (int j = 0; j < G; ++j) mx[j] = fmax(mx[j], lg[(size_t)u * G + j]);
     }
@@ -1115,12 +1139,12 @@ void score_select_kernel(const T* __restrict__ q, int n_kv_heads, double scale, 
   __syncthreads();
   if (tid < G) {
     double m = s_rm[tid][0];
-    for (int q2 = 1; q2 < kSelWaves; ++q2) m = fmax(m, s_rm[tid][q2]);
+    for (int q2 = 1; q2 < NW; ++q2) m = fmax(m, s_rm[tid][q2]);
     s_m[tid] = m;
   }
   __syncthreads();
 
-  select_after_max<G, false>(lg, s_m, n_units, n_pad, s, ps, units_cap, budget, unit_start, sel_units, n_sel_units,
+  select_after_max<G, false, false, NT>(lg, s_m, n_units, n_pad, s, ps, units_cap, budget, unit_start, sel_units, n_sel_units,
                              n_sel, row_ws, scores_out, s_key, s_size, s_incl);
 }
 
@@ -2982,16 +3006,26 @@ int score_and_select(const void* q, int32_t dtype, int64_t n_slices, int32_t n_k
   const int parts = logit_parts(n_slices, n_units);
   if ((int64_t)n_slices * parts > INT32_MAX) return fail(LOUISKV_ERR_SHAPE, "problem too large for one launch");
   int st = LOUISKV_OK;
+  // More slices than compute units: 256-thread blocks, two to a compute unit,
+  // so that one block's selection overlaps the other's logit loads (the
+  // scores are the same for both block sizes); else one 512-thread block each.
+  const bool small_blocks = n_slices > device_cu_count();
+#define LKV_SEL_NT(T, G, NT)                                                                                           \
+  if ((st = check_lds(reinterpret_cast<const void*>(&score_select_kernel<T, G, NT>), lds))) return st;                 \
+  score_select_kernel<T, G, NT><<<(unsigned)n_slices, NT, lds, s>>>(                                                   \
+      static_cast<const T*>(q), n_kv_heads, scale, reps, unit_start, unit_size, units_cap, n_units, budget, fire,    \
+      sel_units, n_sel_units, n_sel, scores_out, logit_ws, rows, n_pad, seg_state, seg_stride, slice_div,            \
+      parts == 1 ? 1 : 0)
 #define LKV_SEL(T, G)                                                                                                  \
-  if ((st = check_lds(reinterpret_cast<const void*>(&score_select_kernel<T, G>), lds))) return st;                     \
   if (parts > 1)                                                                                                       \
     unit_logits_kernel<T, G><<<(unsigned)(n_slices * parts), kLogitThreads, 0, s>>>(                                   \
         static_cast<const T*>(q), n_kv_heads, scale, reps, units_cap, n_units, fire, logit_ws, seg_state,            \
         seg_stride, slice_div, parts);                                                                                \
-  score_select_kernel<T, G><<<(unsigned)n_slices, kSelThreads, lds, s>>>(                                              \
-      static_cast<const T*>(q), n_kv_heads, scale, reps, unit_start, unit_size, units_cap, n_units, budget, fire,    \
-      sel_units, n_sel_units, n_sel, scores_out, logit_ws, rows, n_pad, seg_state, seg_stride, slice_div,            \
-      parts == 1 ? 1 : 0)
+  if (small_blocks) {                                                                                                  \
+    LKV_SEL_NT(T, G, kSmallSelThreads);                                                                                \
+  } else {                                                                                                             \
+    LKV_SEL_NT(T, G, kSelThreads);                                                                                     \
+  }
 #define LKV_SEL_G(T)                  \
   switch (group_size) {               \
     case 1: LKV_SEL(T, 1); break;     \
@@ -3010,6 +3044,7 @@ int score_and_select(const void* q, int32_t dtype, int64_t n_slices, int32_t n_k
   }
 #undef LKV_SEL_G
 #undef LKV_SEL
+#undef LKV_SEL_NT
   LKV_CHECK_LAUNCH();
   return LOUISKV_OK;
 }

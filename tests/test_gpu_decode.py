@@ -303,6 +303,57 @@ def test_retrieve_rows_after_the_top_keys(n_small):
         assert to_np(sel_rows[s, :len(idx)]).tolist() == idx
 
 
+@pytest.mark.parametrize("U", [700, 1500])
+def test_retrieve_rows_same_for_every_block_size(U):
+    """With more slices than compute units the retrieval runs 256-thread
+    blocks (two to a compute unit), with fewer 512-thread ones, and the
+    softmax sums keep one summation order: a call over more slices than the
+    device has compute units and the same slices in calls of 32 (logits from
+    their own kernel) give the same scores, selections and row lists bit for
+    bit, and the oracle's selection (700 units: exponentials in registers;
+    1500: in the workspace)."""
+    L = _L()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    H, g, B = 8, 4, 2048
+    G = cus // H + 4
+    S = G * H
+    assert S > cus
+    gen = _gen(U + S)
+    q = torch.randn(G, H * g, 128, generator=gen, device=DEV).mul(2).to(torch.bfloat16)
+    reps = torch.randn(S, U, 128, generator=gen, device=DEV)
+    sizes = torch.randint(1, 60, (S, U), generator=gen, device=DEV, dtype=torch.int32)
+    starts = torch.zeros_like(sizes)
+    starts[:, 1:] = torch.cumsum(sizes, 1)[:, :-1].to(torch.int32)
+    fire = (torch.arange(G, device=DEV) % 5 != 2).to(torch.uint8)
+
+    def run(lo, hi):
+        n = (hi - lo) * H
+        out = (torch.full((n, B), -7, dtype=torch.int32, device=DEV),
+               torch.full((n, U), -1, dtype=torch.int32, device=DEV),
+               torch.full((n,), -1, dtype=torch.int32, device=DEV),
+               torch.full((n,), -1, dtype=torch.int32, device=DEV),
+               torch.full((n, U), -1.0, dtype=torch.float64, device=DEV))
+        sl = slice(lo * H, hi * H)
+        L.retrieve_rows(q[lo:hi], H, reps[sl], starts[sl], sizes[sl], U, B, out[1], out[2], out[3], out[0],
+                        fire=fire[lo:hi], scores_out=out[4])
+        return out
+
+    big = run(0, G)
+    parts = [run(lo, min(G, lo + 4)) for lo in range(0, G, 4)]
+    torch.cuda.synchronize()
+    for k, name in enumerate(("sel_rows", "sel_units", "n_sel_units", "n_sel", "scores")):
+        assert torch.equal(big[k], torch.cat([p[k] for p in parts])), name
+    q64, r64, sz = to64(q), to64(reps), to_np(sizes)
+    for s in range(0, S, 7):
+        grp, h = divmod(s, H)
+        if not fire[grp]:
+            assert int(big[3][s]) == -1
+            continue
+        a = oracle.group_scores(q64[grp, h * g:(h + 1) * g], r64[s], 1 / np.sqrt(128))
+        np.testing.assert_allclose(to_np(big[4][s]), a, rtol=1e-12, atol=1e-300)
+        selection_matches(a, sz[s], B, to_np(big[1][s, :int(big[2][s])]).tolist())
+
+
 ROWS_ATTN_CASES = [
     # (dtype, out dtype, n_groups, n_kv, g, budget, pool rows, window, n_local, local_start)
     (torch.bfloat16, torch.float32, 32, 8, 4, 2048, 6000, 128, 128, 17),   # one block per slice
