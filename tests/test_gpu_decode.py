@@ -303,18 +303,19 @@ def test_retrieve_rows_after_the_top_keys(n_small):
         assert to_np(sel_rows[s, :len(idx)]).tolist() == idx
 
 
-@pytest.mark.parametrize("U", [700, 1500])
-def test_retrieve_rows_same_for_every_block_size(U):
+@pytest.mark.parametrize("U,B", [(700, 2048), (1500, 2048), (8192, 8192)])
+def test_retrieve_rows_same_for_every_block_size(U, B):
     """With more slices than compute units the retrieval runs 256-thread
     blocks (two to a compute unit), with fewer 512-thread ones, and the
     softmax sums keep one summation order: a call over more slices than the
     device has compute units and the same slices in calls of 32 (logits from
     their own kernel) give the same scores, selections and row lists bit for
     bit, and the oracle's selection (700 units: exponentials in registers;
-    1500: in the workspace)."""
+    1500: in the workspace; 8192, the most units a slice may have, with a
+    budget of about 270 of them: the radix search and the block sort)."""
     L = _L()
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    H, g, B = 8, 4, 2048
+    H, g = 8, 4
     G = cus // H + 4
     S = G * H
     assert S > cus
