@@ -184,6 +184,10 @@ ATTN_CASES = [
     (torch.float32, torch.float32, 64, 4, 4, 300, 64, 64, 3),
     (torch.bfloat16, torch.float32, 64, 4, 8, 500, 32, 32, 31),
     (torch.bfloat16, torch.float32, 40, 8, 4, 1000, 128, 0, 0),
+    # one and two query heads a group in bf16 (matrix-core scores), split-KV and one block a slice
+    (torch.bfloat16, torch.float32, 2, 8, 1, 600, 64, 64, 7),
+    (torch.bfloat16, torch.bfloat16, 32, 8, 1, 300, 64, 20, 50),
+    (torch.bfloat16, torch.float32, 32, 8, 2, 1000, 128, 128, 0),
 ]
 
 
@@ -362,6 +366,8 @@ ROWS_ATTN_CASES = [
     (torch.bfloat16, torch.bfloat16, 1, 8, 8, 300, 1000, 32, 32, 5),
     (torch.float32, torch.float32, 1, 8, 4, 512, 2000, 128, 97, 32),
     (torch.float32, torch.float32, 64, 4, 4, 300, 900, 64, 64, 3),
+    (torch.bfloat16, torch.float32, 32, 8, 2, 1024, 3000, 128, 128, 0),
+    (torch.bfloat16, torch.bfloat16, 2, 8, 1, 500, 2000, 64, 30, 10),
 ]
 
 
