@@ -15,6 +15,8 @@ sampled outputs are checked against the oracle one by one.
                the pool rows of the selection,
                the local window and any evicted segment (mean and pool rows),
                and the attention output.
+  layer by     li-so-32k and li-lo-32k-b4: one launch a layer, as the
+  layer        benchmark runs it, step for step against the batched decode.
 """
 import os
 import sys
@@ -448,3 +450,46 @@ def test_ablation_baselines_full_shape_sampled(variant):
                 assert err <= 2e-3, (variant, t, s_list, err)
                 checked += 1
     assert checked >= len(steps) * 2 * NL and fired > 0
+
+
+@pytest.mark.parametrize("name,n_steps", [("li-so-32k", None), ("li-lo-32k-b4", 256)])
+def test_layer_by_layer_full_shape(name, n_steps):
+    """The layer-by-layer decode in the configuration the benchmark times
+    (full-size slices; one launch a layer, the batch's sequences of a layer
+    together) against the batched decode of the same inputs, which
+    test_decode_full_shape_sampled checks against the oracle: the same fires,
+    unit tables, scores, selections and row lists bit for bit at every step,
+    and the same attention outputs up to summation order (li-so-32k: all 128
+    steps; li-lo-32k-b4: the first 256 of 16384, a 1024-slice batched
+    retrieval against 32-slice launches)."""
+    from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
+    _L()
+    wl = synth.get_workload(name)
+    steps = wl.gen_len if n_steps is None else n_steps
+    # layer-major order: a layer's sequences are consecutive groups
+    groups = [(b, l) for l in range(wl.n_layers) for b in range(wl.batch)]
+    data = synth.make_slices(wl, DEV, groups=groups, gen_len=steps)
+    cfg = config_from_workload(wl, gen_len=steps)
+    engs = [LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, keep_scores=True, out_dtype=torch.float32)
+            for _ in range(2)]
+    for e in engs:
+        e.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    a, b = engs
+    fires = 0
+    for t in range(steps):
+        a.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+        b.step_layer_by_layer(data.queries[t], data.gen_keys[t], data.gen_values[t], groups_per_launch=wl.batch)
+        torch.cuda.synchronize()
+        assert torch.equal(a.fire, b.fire), t
+        fires += int(a.fire.sum())
+        for f in ("n_sel", "n_sel_units", "sel_units", "unit_start", "unit_size", "reps"):
+            assert torch.equal(getattr(a, f), getattr(b, f)), (t, f)
+        if bool(a.fire.any()):
+            assert torch.equal(a.scores, b.scores), t
+        n = a.n_sel.long()
+        mask = torch.arange(a.sel_rows.shape[1], device=DEV)[None, :] < n[:, None]
+        assert torch.equal(torch.where(mask, a.sel_rows, 0), torch.where(mask, b.sel_rows, 0)), t
+        err = (a.out - b.out).abs().max().item()
+        assert err <= 1e-5 * max(1.0, a.out.abs().max().item()), (t, err)
+        assert (a.lse - b.lse).abs().max().item() <= 1e-5, t
+    assert fires > 0
