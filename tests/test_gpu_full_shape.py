@@ -15,8 +15,9 @@ sampled outputs are checked against the oracle one by one.
                the pool rows of the selection,
                the local window and any evicted segment (mean and pool rows),
                and the attention output.
-  layer by     li-so-32k and li-lo-32k-b4: one launch a layer, as the
-  layer        benchmark runs it, step for step against the batched decode.
+  layer by     li-so-32k, li-lo-32k-b4 and host-131k: one launch sequence a
+  layer        layer, as the benchmark runs it, step for step against the
+               batched decode.
 """
 import os
 import sys
@@ -452,7 +453,7 @@ def test_ablation_baselines_full_shape_sampled(variant):
     assert checked >= len(steps) * 2 * NL and fired > 0
 
 
-@pytest.mark.parametrize("name,n_steps", [("li-so-32k", None), ("li-lo-32k-b4", 256)])
+@pytest.mark.parametrize("name,n_steps", [("li-so-32k", None), ("li-lo-32k-b4", 256), ("host-131k", 128)])
 def test_layer_by_layer_full_shape(name, n_steps):
     """The layer-by-layer decode in the configuration the benchmark times
     (full-size slices; one launch a layer, the batch's sequences of a layer
@@ -461,7 +462,8 @@ def test_layer_by_layer_full_shape(name, n_steps):
     unit tables, scores, selections and row lists bit for bit at every step,
     and the same attention outputs up to summation order (li-so-32k: all 128
     steps; li-lo-32k-b4: the first 256 of 16384, a 1024-slice batched
-    retrieval against 32-slice launches)."""
+    retrieval against 32-slice launches; host-131k: the first 128 of 8192,
+    the pool in pinned host memory behind the LRU cache of pool rows)."""
     from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
     _L()
     wl = synth.get_workload(name)
@@ -470,8 +472,8 @@ def test_layer_by_layer_full_shape(name, n_steps):
     groups = [(b, l) for l in range(wl.n_layers) for b in range(wl.batch)]
     data = synth.make_slices(wl, DEV, groups=groups, gen_len=steps)
     cfg = config_from_workload(wl, gen_len=steps)
-    engs = [LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, keep_scores=True, out_dtype=torch.float32)
-            for _ in range(2)]
+    engs = [LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, keep_scores=True, out_dtype=torch.float32,
+                          pool_on_host=wl.pool_on_host) for _ in range(2)]
     for e in engs:
         e.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
     a, b = engs
@@ -486,9 +488,15 @@ def test_layer_by_layer_full_shape(name, n_steps):
             assert torch.equal(getattr(a, f), getattr(b, f)), (t, f)
         if bool(a.fire.any()):
             assert torch.equal(a.scores, b.scores), t
+        # the selection as pool rows, or as the cache's slots and their rows
         n = a.n_sel.long()
-        mask = torch.arange(a.sel_rows.shape[1], device=DEV)[None, :] < n[:, None]
-        assert torch.equal(torch.where(mask, a.sel_rows, 0), torch.where(mask, b.sel_rows, 0)), t
+        listed = a.sel_rows if a.sel_rows is not None else a.slot_list
+        other = b.sel_rows if b.sel_rows is not None else b.slot_list
+        mask = torch.arange(listed.shape[1], device=DEV)[None, :] < n[:, None]
+        assert torch.equal(torch.where(mask, listed, 0), torch.where(mask, other, 0)), t
+        if a.sel_rows is None:
+            for f in ("buf_row", "slot_step"):
+                assert torch.equal(getattr(a, f), getattr(b, f)), (t, f)
         err = (a.out - b.out).abs().max().item()
         assert err <= 1e-5 * max(1.0, a.out.abs().max().item()), (t, err)
         assert (a.lse - b.lse).abs().max().item() <= 1e-5, t
