@@ -15,7 +15,7 @@ sampled outputs are checked against the oracle one by one.
                the pool rows of the selection,
                the local window and any evicted segment (mean and pool rows),
                and the attention output.
-  layer by     li-so-32k, li-lo-32k-b4 and host-131k: one launch sequence a
+  layer by     li-so-32k, si-lo-16k, li-lo-32k-b4, host-131k: one launch sequence a
   layer        layer, as the benchmark runs it, step for step against the
                batched decode.
 """
@@ -453,7 +453,8 @@ def test_ablation_baselines_full_shape_sampled(variant):
     assert checked >= len(steps) * 2 * NL and fired > 0
 
 
-@pytest.mark.parametrize("name,n_steps", [("li-so-32k", None), ("li-lo-32k-b4", 256), ("host-131k", 128)])
+@pytest.mark.parametrize("name,n_steps", [("li-so-32k", None), ("si-lo-16k", 512), ("li-lo-32k-b4", 256),
+                                           ("host-131k", 128)])
 def test_layer_by_layer_full_shape(name, n_steps):
     """The layer-by-layer decode in the configuration the benchmark times
     (full-size slices; one launch a layer, the batch's sequences of a layer
@@ -461,7 +462,8 @@ def test_layer_by_layer_full_shape(name, n_steps):
     test_decode_full_shape_sampled checks against the oracle: the same fires,
     unit tables, scores, selections and row lists bit for bit at every step,
     and the same attention outputs up to summation order (li-so-32k: all 128
-    steps; li-lo-32k-b4: the first 256 of 16384, a 1024-slice batched
+    steps; si-lo-16k: the first 512 of 16384, past the first window
+    evictions; li-lo-32k-b4: the first 256 of 16384, a 1024-slice batched
     retrieval against 32-slice launches; host-131k: the first 128 of 8192,
     the pool in pinned host memory behind the LRU cache of pool rows)."""
     from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
