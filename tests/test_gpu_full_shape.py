@@ -18,6 +18,8 @@ sampled outputs are checked against the oracle one by one.
   layer by     li-so-32k, si-lo-16k, li-lo-32k-b4, host-131k: one launch sequence a
   layer        layer, as the benchmark runs it, step for step against the
                batched decode.
+  graph        li-so-32k's 128-step decode loop as one HIP graph, as the
+               benchmark times it, against the eager loop.
 """
 import os
 import sys
@@ -510,3 +512,46 @@ def test_layer_by_layer_full_shape(name, start, n_steps):
         assert err <= 1e-5 * max(1.0, a.out.abs().max().item()), (t, err)
         assert (a.lse - b.lse).abs().max().item() <= 1e-5, t
     assert fires > 0
+
+
+def test_decode_graph_full_shape():
+    """The benchmark's batched decode of li-so-32k: the whole 128-step loop
+    captured as one HIP graph and replayed after a fresh prefill, twice;
+    after each replay the state (unit tables, index vectors, the last step's
+    fires, selection, row list and reference queries) and the last step's
+    attention output equal those of the same loop run eagerly, bit for bit."""
+    from paper_2510_11292_amd.engine import LouisKVEngine, config_from_workload
+    L = _L()
+    wl = synth.get_workload("li-so-32k")
+    data = synth.make_slices(wl, DEV)
+    cfg = config_from_workload(wl, mode=L.REF_ANCHOR)
+    engs = [LouisKVEngine(cfg, data.prompt_keys.dtype, DEV, out_dtype=torch.float32) for _ in range(2)]
+    a, b = engs
+
+    def loop(e):
+        for t in range(wl.gen_len):
+            e.step(data.queries[t], data.gen_keys[t], data.gen_values[t])
+    a.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    loop(a)
+    # b: one eager pass on a side stream (allocations, warm-up), then the capture
+    b.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        loop(b)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    b.t = 0
+    with torch.cuda.graph(graph):
+        loop(b)
+    names = ("reps", "unit_start", "unit_size", "fire", "n_sel", "n_sel_units", "sel_units", "q_ref", "out", "lse")
+    for rep in range(2):
+        b.prefill(data.prompt_keys, data.prompt_values, data.init_idx)
+        graph.replay()
+        torch.cuda.synchronize()
+        for f in names:
+            assert torch.equal(getattr(a, f), getattr(b, f)), (rep, f)
+        n = a.n_sel.long()
+        mask = torch.arange(a.sel_rows.shape[1], device=DEV)[None, :] < n[:, None]
+        assert torch.equal(torch.where(mask, a.sel_rows, 0), torch.where(mask, b.sel_rows, 0)), rep
